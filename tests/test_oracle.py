@@ -1,0 +1,430 @@
+"""Pins of the oracle against what fixes it from outside: library routines,
+closed forms, brute force on tiny inputs and invariants (CPU only).
+
+The paper prints no worked example of the VLA forward, so no golden values
+from it exist; every pin below is independent of the oracle's own code."""
+import math
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import synth
+from oracle import vla_oracle as O
+
+RNG = np.random.default_rng(1234)
+
+
+def rnd(*shape, scale=1.0):
+    return RNG.standard_normal(shape) * scale
+
+
+def t64(x):
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float64))
+
+
+# ---------------------------------------------------------------- primitives
+
+def test_layer_norm_vs_torch_and_properties():
+    x, g, b = rnd(7, 33), rnd(33), rnd(33)
+    ref = F.layer_norm(t64(x), (33,), t64(g), t64(b), eps=1e-6).numpy()
+    assert np.allclose(O.layer_norm(x, g, b), ref, rtol=1e-12, atol=1e-12)
+    y = O.layer_norm(x, np.ones(33), np.zeros(33))
+    assert np.allclose(y.mean(-1), 0, atol=1e-12)
+    assert np.allclose(y.var(-1), 1, atol=1e-5)
+    assert np.allclose(O.layer_norm(3.5 * x, g, b), O.layer_norm(x, g, b), atol=1e-6)
+
+
+def test_rms_norm_vs_torch_and_properties():
+    x, g = rnd(5, 40), rnd(40)
+    ref = F.rms_norm(t64(x), (40,), t64(g), eps=1e-6).numpy()
+    assert np.allclose(O.rms_norm(x, g), ref, rtol=1e-12, atol=1e-12)
+    y = O.rms_norm(x, np.ones(40))
+    assert np.allclose(np.sqrt((y * y).mean(-1)), 1, atol=1e-5)
+    assert np.allclose(O.rms_norm(0.25 * x, g), O.rms_norm(x, g), atol=1e-5)
+
+
+def test_gelu_tanh():
+    x = np.linspace(-6, 6, 1001)
+    ref = F.gelu(t64(x), approximate="tanh").numpy()
+    assert np.allclose(O.gelu_tanh(x), ref, rtol=1e-13, atol=1e-14)
+    assert O.gelu_tanh(np.zeros(1))[0] == 0.0
+    assert np.allclose(O.gelu_tanh(x) - O.gelu_tanh(-x), x, atol=1e-12)  # odd-part identity
+    erf = F.gelu(t64(x)).numpy()
+    assert np.abs(O.gelu_tanh(x) - erf).max() < 1e-3
+
+
+def test_swish():
+    x = np.linspace(-20, 20, 401)
+    assert np.allclose(O.swish(x), F.silu(t64(x)).numpy(), rtol=1e-13, atol=1e-15)
+
+
+def test_softmax_brute_force():
+    s = rnd(3, 6, scale=4.0)
+    for r in range(3):
+        e = [math.exp(v) for v in s[r]]
+        tot = sum(e)
+        assert np.allclose(O.softmax(s)[r], [v / tot for v in e], rtol=1e-13)
+    assert np.allclose(O.softmax(s + 100.0), O.softmax(s), rtol=1e-12)
+
+
+def _attention_brute(q, k, v):
+    sq, nq, hd = q.shape
+    skv, nkv, _ = k.shape
+    out = np.zeros_like(q)
+    for i in range(sq):
+        for h in range(nq):
+            j = h * nkv // nq
+            logits = [sum(q[i, h, d] * k[s, j, d] for d in range(hd)) / math.sqrt(hd) for s in range(skv)]
+            m = max(logits)
+            w = [math.exp(z - m) for z in logits]
+            z = sum(w)
+            for d in range(hd):
+                out[i, h, d] = sum(w[s] * v[s, j, d] for s in range(skv)) / z
+    return out
+
+
+@pytest.mark.parametrize("nq,nkv", [(1, 1), (4, 1), (4, 2), (3, 3)])
+def test_attention_brute_force(nq, nkv):
+    q, k, v = rnd(3, nq, 4), rnd(5, nkv, 4), rnd(5, nkv, 4)
+    assert np.allclose(O.attention(q, k, v), _attention_brute(q, k, v), rtol=1e-12, atol=1e-13)
+
+
+def test_attention_vs_sdpa_gqa_and_invariants():
+    q, k, v = rnd(9, 8, 16), rnd(13, 2, 16), rnd(13, 2, 16)
+    ref = F.scaled_dot_product_attention(t64(q).transpose(0, 1), t64(k).transpose(0, 1),
+                                         t64(v).transpose(0, 1), enable_gqa=True).transpose(0, 1).numpy()
+    assert np.allclose(O.attention(q, k, v), ref, rtol=1e-11, atol=1e-12)
+    # multi-query attention == multi-head attention with the KV head repeated
+    k1, v1 = rnd(13, 1, 16), rnd(13, 1, 16)
+    rep = O.attention(q, np.repeat(k1, 8, axis=1), np.repeat(v1, 8, axis=1))
+    assert np.allclose(O.attention(q, k1, v1), rep, rtol=1e-13)
+    # no mask: permuting the key/value rows changes nothing
+    perm = RNG.permutation(13)
+    assert np.allclose(O.attention(q, k[perm], v[perm]), O.attention(q, k, v), rtol=1e-12)
+    # identical keys -> mean of the values
+    kk = np.repeat(rnd(1, 2, 16), 13, axis=0)
+    mean_v = np.repeat(v.mean(0)[None], 8 // 2, axis=1).reshape(1, 8, 16)
+    got = O.attention(q, kk, v)
+    assert np.allclose(got, np.broadcast_to(np.repeat(v.mean(0), 4, axis=0)[None], got.shape), rtol=1e-12)
+    del mean_v
+    # one dominant logit selects that value row
+    kd = np.zeros((13, 1, 16)); kd[5, 0, :] = 1000.0
+    qd = np.ones((2, 1, 16))
+    assert np.allclose(O.attention(qd, kd, v[:, :1]), np.broadcast_to(v[5, :1], (2, 1, 16)))
+
+
+def test_rope_complex_form_and_properties():
+    x = rnd(6, 3, 8)
+    pos = np.array([0, 1, 2, 7, 40, 300])
+    y = O.rope(x, pos)
+    half = 4
+    z = x[..., :half] + 1j * x[..., half:]
+    theta = 10000.0 ** (-np.arange(half) * 2.0 / 8)
+    zr = z * np.exp(1j * pos[:, None, None] * theta[None, None, :])
+    assert np.allclose(y, np.concatenate([zr.real, zr.imag], -1), rtol=1e-12, atol=1e-12)
+    assert np.allclose(y[0], x[0])  # position 0 is the identity
+    assert np.allclose(np.linalg.norm(y, axis=-1), np.linalg.norm(x, axis=-1))
+    # scores depend on relative position only
+    q, k = rnd(1, 1, 8), rnd(1, 1, 8)
+    s1 = (O.rope(q, [5]) * O.rope(k, [2])).sum()
+    s2 = (O.rope(q, [105]) * O.rope(k, [102])).sum()
+    assert abs(s1 - s2) < 1e-9
+
+
+def test_rope_vs_transformers():
+    from transformers.models.gemma.modeling_gemma import apply_rotary_pos_emb
+    hd = 16
+    x = rnd(5, 2, hd)
+    pos = np.arange(10, 15, dtype=np.float64)
+    inv = 1.0 / (10000.0 ** (np.arange(0, hd, 2) / hd))
+    emb = np.concatenate([pos[:, None] * inv, pos[:, None] * inv], -1)
+    cos, sin = t64(np.cos(emb))[None], t64(np.sin(emb))[None]
+    xt = t64(x).transpose(0, 1)[None]  # [1, heads, seq, hd]
+    ref, _ = apply_rotary_pos_emb(xt, xt, cos, sin)
+    assert np.allclose(O.rope(x, pos), ref[0].transpose(0, 1).numpy(), rtol=1e-12, atol=1e-12)
+
+
+def test_patchify_brute_force():
+    img = rnd(12, 8, 3)
+    p = 4
+    out = O.patchify(img, p)
+    assert out.shape == (6, 48)
+    for i in range(3):
+        for j in range(2):
+            t = i * 2 + j
+            vec = [img[i * p + r, j * p + c, ch] for r in range(p) for c in range(p) for ch in range(3)]
+            assert np.array_equal(out[t], vec)
+
+
+def test_sinusoid_closed_form():
+    d = 16
+    phi0 = O.sinusoid(0.0, d)
+    assert np.array_equal(phi0, np.r_[np.zeros(8), np.ones(8)])
+    t = 0.3
+    phi = O.sinusoid(t, d)
+    assert np.isclose(phi[0], math.sin(2 * math.pi * t / 4e-3))
+    assert np.isclose(phi[7], math.sin(2 * math.pi * t / 4.0))
+    assert np.isclose(phi[8 + 7], math.cos(2 * math.pi * t / 4.0))
+    assert np.allclose(phi[:8] ** 2 + phi[8:] ** 2, 1.0)
+
+
+def test_flow_times():
+    ts, dt = O.flow_times(10)
+    assert np.float32(ts[1]) == np.float32(0.9) and ts[0] == 1.0 and len(ts) == 10
+    assert np.float32(dt) == np.float32(-0.1)
+    ts4, dt4 = O.flow_times(4)
+    assert ts4 == [1.0, 0.75, 0.5, 0.25] and dt4 == -0.25
+
+
+def test_euler_closed_forms():
+    x0 = rnd(4, 3)
+    _, dt = O.flow_times(10)
+    lam = -0.7
+    got = O.euler_integrate(x0, lambda x, t: lam * x, 10)
+    assert np.allclose(got, (1 + lam * dt) ** 10 * x0, rtol=1e-13)
+    b = rnd(4, 3)
+    assert np.allclose(O.euler_integrate(x0, lambda x, t: b, 10), x0 + 10 * dt * b, rtol=1e-13)
+    M = rnd(3, 3, scale=0.3)
+    got = O.euler_integrate(x0, lambda x, t: x @ M.T, 5)
+    _, dt5 = O.flow_times(5)
+    A = np.linalg.matrix_power(np.eye(3) + dt5 * M, 5)
+    assert np.allclose(got, x0 @ A.T, rtol=1e-12)
+    # time dependence: v = t -> x_N = x_0 + dt * sum_k t_k
+    ts, _ = O.flow_times(4)
+    assert np.allclose(O.euler_integrate(x0, lambda x, t: np.full_like(x, t), 4), x0 - 0.25 * sum(ts))
+
+
+def test_bf16_operand_rounding_vs_torch():
+    x = rnd(10000, scale=5.0)
+    ref = t64(x).to(torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(O.bf16(x), ref)
+    assert np.array_equal(O.bf16(synth.normal(2, "q", 1000, 1.0)), synth.bf16_round(synth.normal(2, "q", 1000, 1.0)))
+
+
+# ------------------------------------------------------- layers vs libraries
+
+def _siglip_layer(cfg, P, l):
+    from transformers import SiglipVisionConfig
+    from transformers.models.siglip.modeling_siglip import SiglipEncoderLayer
+    c = SiglipVisionConfig(hidden_size=cfg["vit_dim"], intermediate_size=cfg["vit_mlp"],
+                           num_attention_heads=cfg["vit_heads"], layer_norm_eps=1e-6,
+                           hidden_act="gelu_pytorch_tanh", attention_dropout=0.0)
+    c._attn_implementation = "eager"
+    m = SiglipEncoderLayer(c).double().eval()
+    p = f"vit.{l}."
+    sd = {
+        "layer_norm1.weight": P[p + "ln1.g"], "layer_norm1.bias": P[p + "ln1.b"],
+        "layer_norm2.weight": P[p + "ln2.g"], "layer_norm2.bias": P[p + "ln2.b"],
+        "self_attn.q_proj.weight": P[p + "q.w"], "self_attn.q_proj.bias": P[p + "q.b"],
+        "self_attn.k_proj.weight": P[p + "k.w"], "self_attn.k_proj.bias": P[p + "k.b"],
+        "self_attn.v_proj.weight": P[p + "v.w"], "self_attn.v_proj.bias": P[p + "v.b"],
+        "self_attn.out_proj.weight": P[p + "o.w"], "self_attn.out_proj.bias": P[p + "o.b"],
+        "mlp.fc1.weight": P[p + "fc1.w"], "mlp.fc1.bias": P[p + "fc1.b"],
+        "mlp.fc2.weight": P[p + "fc2.w"], "mlp.fc2.bias": P[p + "fc2.b"],
+    }
+    m.load_state_dict({k: t64(v) for k, v in sd.items()})
+    return m
+
+
+def _gemma_layer(cfg, P, prefix, l, dim, mlp):
+    from transformers import GemmaConfig
+    from transformers.models.gemma.modeling_gemma import GemmaDecoderLayer
+    c = GemmaConfig(hidden_size=dim, intermediate_size=mlp, num_attention_heads=cfg["lm_heads"],
+                    num_key_value_heads=cfg["lm_kv_heads"], head_dim=cfg["head_dim"], rms_norm_eps=1e-6,
+                    hidden_activation="gelu_pytorch_tanh", attention_bias=False, vocab_size=cfg["vocab"])
+    c._attn_implementation = "eager"
+    m = GemmaDecoderLayer(c, layer_idx=l).double().eval()
+    p = f"{prefix}.{l}."
+    sd = {  # Gemma's RMSNorm scales by (1 + weight)
+        "input_layernorm.weight": P[p + "rms1.g"] - 1.0,
+        "post_attention_layernorm.weight": P[p + "rms2.g"] - 1.0,
+        "self_attn.q_proj.weight": P[p + "q.w"], "self_attn.k_proj.weight": P[p + "k.w"],
+        "self_attn.v_proj.weight": P[p + "v.w"], "self_attn.o_proj.weight": P[p + "o.w"],
+        "mlp.gate_proj.weight": P[p + "gate.w"], "mlp.up_proj.weight": P[p + "up.w"],
+        "mlp.down_proj.weight": P[p + "down.w"],
+    }
+    m.load_state_dict({k: t64(np.asarray(v, np.float64)) for k, v in sd.items()})
+    return m
+
+
+def _rope_tables(hd, pos):
+    inv = 1.0 / (10000.0 ** (np.arange(0, hd, 2) / hd))
+    ang = np.asarray(pos, np.float64)[:, None] * inv
+    emb = np.concatenate([ang, ang], -1)
+    return t64(np.cos(emb))[None], t64(np.sin(emb))[None]
+
+
+def _cfg_params(cfg=None):
+    cfg = cfg or synth.micro()
+    return cfg, synth.make_params(cfg, 0)
+
+
+def test_vit_layer_vs_siglip():
+    cfg, P = _cfg_params()
+    x = rnd(16, cfg["vit_dim"])
+    ref = _siglip_layer(cfg, P, 0)(t64(x)[None], None)
+    ref = (ref[0] if isinstance(ref, tuple) else ref)[0].detach().numpy()
+    # transformers computes the softmax in fp32, hence 1e-7
+    assert np.allclose(O.vit_layer(P, cfg, 0, x), ref, rtol=1e-7, atol=1e-7)
+
+
+def test_lm_decoder_layer_vs_gemma():
+    from transformers.cache_utils import DynamicCache
+    cfg = dict(synth.micro(), lm_layers=2)
+    P = synth.make_params(cfg, 0)
+    x = rnd(21, cfg["lm_dim"])
+    pos = np.arange(21)
+    m = _gemma_layer(cfg, P, "lm", 0, cfg["lm_dim"], cfg["lm_mlp"])
+    cache = DynamicCache()
+    with torch.no_grad():
+        ref = m(t64(x)[None], attention_mask=None, position_ids=torch.arange(21)[None],
+                past_key_values=cache, use_cache=True, position_embeddings=_rope_tables(cfg["head_dim"], pos))
+    ref = (ref[0] if isinstance(ref, tuple) else ref)[0].numpy()
+    got, k, v = O.decoder_layer(P, cfg, "lm.0.", x, pos)
+    # Gemma's RMSNorm runs in fp32, hence the tolerance
+    assert np.allclose(got, ref, rtol=2e-5, atol=2e-5)
+    assert np.allclose(k, cache.layers[0].keys[0].transpose(0, 1).numpy(), rtol=2e-5, atol=2e-5)
+    assert np.allclose(v, cache.layers[0].values[0].transpose(0, 1).numpy(), rtol=2e-5, atol=2e-5)
+
+
+def test_expert_velocity_vs_library_assembly():
+    """The whole expert (in-proj, time MLP, decoder layers with the prefix KV in
+    the cache at positions P.., final RMSNorm, out-proj) assembled from torch and
+    transformers modules."""
+    from transformers.cache_utils import DynamicCache
+    cfg = dict(synth.micro(), lm_layers=2, ex_layers=2)
+    P = synth.make_params(cfg, 0)
+    npre, H, A, de = 21, cfg["chunk_len"], cfg["action_dim"], cfg["ex_dim"]
+    nkv, hd = cfg["lm_kv_heads"], cfg["head_dim"]
+    kv = [(rnd(npre, nkv, hd), rnd(npre, nkv, hd)) for _ in range(2)]
+    x, t = rnd(H, A), 0.75
+    got = O.expert_velocity(P, cfg, kv, x, t)
+
+    lin = lambda w, b=None: (lambda z: F.linear(z, t64(P[w]), None if b is None else t64(P[b])))
+    with torch.no_grad():
+        a = lin("ex.in.w", "ex.in.b")(t64(x))
+        phi = t64(O.sinusoid(t, de))[None].expand(H, de)
+        u = lin("ex.time2.w", "ex.time2.b")(F.silu(lin("ex.time1.w", "ex.time1.b")(torch.cat([a, phi], 1))))
+        cache = DynamicCache()
+        for l in range(2):
+            cache.update(t64(kv[l][0]).transpose(0, 1)[None], t64(kv[l][1]).transpose(0, 1)[None], l)
+        pos = np.arange(npre, npre + H)
+        h = u[None]
+        for l in range(2):
+            m = _gemma_layer(cfg, P, "ex", l, de, cfg["ex_mlp"])
+            h = m(h, attention_mask=None, position_ids=torch.from_numpy(pos)[None], past_key_values=cache,
+                  use_cache=True, position_embeddings=_rope_tables(hd, pos))
+            h = h[0] if isinstance(h, tuple) else h
+        ref = lin("ex.out.w", "ex.out.b")(F.rms_norm(h[0], (de,), t64(P["ex.final.g"]), eps=1e-6)).numpy()
+    assert np.allclose(got, ref, rtol=2e-5, atol=2e-5)
+
+
+def test_vlm_prefill_vs_library_assembly():
+    """Phase 1 end to end (ViT from SigLIP layers, post-LN, projector, text
+    embedding x sqrt(d), state row, Gemma layers writing the cache)."""
+    from transformers.cache_utils import DynamicCache
+    cfg = dict(synth.micro(), vit_layers=2, lm_layers=2)
+    P = synth.make_params(cfg, 0)
+    fr = synth.make_frame(cfg, 0, 0)
+    got = O.vlm_prefill(P, cfg, fr)
+    p, dl = cfg["patch"], cfg["lm_dim"]
+    with torch.no_grad():
+        img = t64(fr["pixels"][0])
+        gh, gw = cfg["img_h"] // p, cfg["img_w"] // p
+        # unfold-based patch extraction, reordered to (row, col, channel)
+        patches = img.permute(2, 0, 1).unfold(1, p, p).unfold(2, p, p)  # [3, gh, gw, p, p]
+        patches = patches.permute(1, 2, 3, 4, 0).reshape(gh * gw, p * p * 3)
+        x = F.linear(patches, t64(P["vit.patch.w"]), t64(P["vit.patch.b"])) + t64(P["vit.pos"])
+        for l in range(2):
+            y = _siglip_layer(cfg, P, l)(x[None], None)
+            x = (y[0] if isinstance(y, tuple) else y)[0]
+        x = F.layer_norm(x, (cfg["vit_dim"],), t64(P["vit.post.g"]), t64(P["vit.post.b"]), eps=1e-6)
+        img_tok = F.linear(x, t64(P["proj.w"]), t64(P["proj.b"]))
+        emb = torch.nn.Embedding(cfg["vocab"], dl).double()
+        emb.weight.data = t64(P["lm.embed"])
+        txt = emb(torch.from_numpy(fr["ids"].astype(np.int64))) * math.sqrt(dl)
+        st = F.linear(t64(fr["state"])[None], t64(P["state.w"]), t64(P["state.b"]))
+        h = torch.cat([img_tok, txt, st], 0)[None]
+        n = h.shape[1]
+        cache = DynamicCache()
+        for l in range(2):
+            m = _gemma_layer(cfg, P, "lm", l, dl, cfg["lm_mlp"]) if l == 0 else None
+            if m is None:  # the last layer has no MLP / o-proj weights: only its K, V matter
+                q = F.rms_norm(h[0], (dl,), t64(P[f"lm.{l}.rms1.g"]), eps=1e-6)
+                k = F.linear(q, t64(P[f"lm.{l}.k.w"])).reshape(n, cfg["lm_kv_heads"], -1)
+                v = F.linear(q, t64(P[f"lm.{l}.v.w"])).reshape(n, cfg["lm_kv_heads"], -1)
+                cos, sin = _rope_tables(cfg["head_dim"], np.arange(n))
+                from transformers.models.gemma.modeling_gemma import apply_rotary_pos_emb
+                kt = k.transpose(0, 1)[None]
+                kt, _ = apply_rotary_pos_emb(kt, kt, cos, sin)
+                cache.update(kt, v.transpose(0, 1)[None], l)
+                break
+            h = m(h, attention_mask=None, position_ids=torch.arange(n)[None], past_key_values=cache,
+                  use_cache=True, position_embeddings=_rope_tables(cfg["head_dim"], np.arange(n)))
+            h = h[0] if isinstance(h, tuple) else h
+    for l in range(2):
+        assert np.allclose(got[l][0], cache.layers[l].keys[0].transpose(0, 1).numpy(), rtol=5e-5, atol=5e-5)
+        assert np.allclose(got[l][1], cache.layers[l].values[0].transpose(0, 1).numpy(), rtol=5e-5, atol=5e-5)
+
+
+# ------------------------------------------------------------ model wiring
+
+def test_zero_out_projection_gives_noise_minus_bias():
+    cfg = synth.micro()
+    P = synth.make_params(cfg, 0)
+    P["ex.out.w"] = np.zeros_like(P["ex.out.w"])
+    fr = synth.make_frame(cfg, 0, 0)
+    chunk = O.forward(P, cfg, fr)
+    _, dt = O.flow_times(cfg["n_steps"])
+    b = P["ex.out.b"].astype(np.float64)
+    assert np.allclose(chunk, fr["noise"].astype(np.float64) + cfg["n_steps"] * dt * b, rtol=0, atol=1e-12)
+    assert np.allclose(chunk, fr["noise"] - P["ex.out.b"], atol=1e-6)
+
+
+def test_vit_without_residual_branches_is_patch_embedding():
+    cfg = synth.micro()
+    P = synth.make_params(cfg, 0)
+    for n in ("o.w", "o.b", "fc2.w", "fc2.b"):
+        P["vit.0." + n] = np.zeros_like(P["vit.0." + n])
+    img = synth.make_frame(cfg, 0, 0)["pixels"][0]
+    emb = O.patchify(img.astype(np.float64), cfg["patch"]) @ P["vit.patch.w"].T.astype(np.float64)
+    emb = emb + P["vit.patch.b"] + P["vit.pos"]
+    want = O.layer_norm(emb, P["vit.post.g"], P["vit.post.b"])
+    assert np.allclose(O.vit_view(P, cfg, img), want, rtol=1e-12, atol=1e-12)
+
+
+def test_prefix_rows():
+    cfg = synth.micro()
+    P = synth.make_params(cfg, 0)
+    fr = synth.make_frame(cfg, 0, 0)
+    img = rnd(synth.derived(cfg)["n_img"], cfg["lm_dim"])
+    x0 = O.prefix(P, cfg, fr, img)
+    assert x0.shape == (synth.derived(cfg)["prefix"], cfg["lm_dim"])
+    n = img.shape[0]
+    for i, tok in enumerate(fr["ids"]):
+        assert np.allclose(x0[n + i], P["lm.embed"][tok] * 8.0)  # sqrt(64)
+    st = sum(P["state.w"][:, j].astype(np.float64) * fr["state"][j] for j in range(3)) + P["state.b"]
+    assert np.allclose(x0[-1], st)
+
+
+def test_bf16_config_differs_only_by_operand_rounding():
+    """The bf16 model is the fp32 model with bf16 storage at the documented
+    points; on the same (bf16-valued) weights the two chunks stay close."""
+    c32, c16 = synth.micro(synth.F32), synth.micro(synth.BF16)
+    P = synth.make_params(c16, 0)
+    fr = synth.make_frame(c16, 0, 0)
+    a, b = O.forward(P, c32, fr), O.forward(P, c16, fr)
+    assert 0 < np.abs(a - b).max() < 2e-2
+
+
+def test_multi_view_is_view_major_and_independent():
+    cfg = dict(synth.micro(), n_views=2)
+    P = synth.make_params(cfg, 0)
+    fr = synth.make_frame(cfg, 0, 0)
+    toks = O.image_tokens(P, cfg, fr["pixels"])
+    single = dict(cfg, n_views=1)
+    for v in range(2):
+        want = O.image_tokens(P, single, fr["pixels"][v:v + 1])
+        assert np.allclose(toks[v * 16:(v + 1) * 16], want, rtol=1e-13)
