@@ -1,0 +1,189 @@
+/*
+ * vla.h - C ABI of the MI355X (gfx950) two-phase VLA inference library.
+ *
+ * The library runs the inference pipeline the paper characterises
+ * (Section 2.1, "Vision-Language-Action Models", and its last paragraph on
+ * the execution model): phase 1, a VLM (ViT patch encoder + language-model
+ * prefill), turns a camera frame and an instruction into a per-layer KV
+ * cache; phase 2, a flow-matching action expert, integrates a velocity field
+ * with Euler steps to produce an action chunk, every step attending to that
+ * cache. The VLM prefill of frame N+1 runs concurrently with the action phase
+ * of frame N on a second stream (Section 2.1; Fig. "streamexec" (a)-(c) of
+ * Section 2.4 name the serialized, naive two-stream and ideal schedules).
+ *
+ * Conventions
+ *  - Every function returns 0 (VLA_OK) or a negative status; nothing aborts
+ *    and no C++ exception crosses the ABI. vla_last_error() returns a
+ *    thread-local message for the last failing call on this thread.
+ *  - Pointers documented "device" are HIP device pointers on the model's
+ *    device; "host" pointers are ordinary host memory. They are never mixed.
+ *  - Streams are hipStream_t passed as void*; NULL means the null stream.
+ *  - Objects made by *_create are owned by the library until *_destroy.
+ *    All other buffers are owned by the caller and must stay alive until the
+ *    asynchronous work that reads or writes them has completed.
+ *  - One model may run one prefill and one denoise at a time (they use
+ *    model-owned scratch memory per phase); calls of the same phase on two
+ *    streams at once race.
+ */
+#ifndef VLA_H
+#define VLA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---- */
+#define VLA_OK 0
+#define VLA_EINVAL (-1)       /* invalid argument or configuration            */
+#define VLA_ENOMEM (-2)       /* device or host allocation failed             */
+#define VLA_EHIP (-3)         /* a HIP runtime call failed (message has it)   */
+#define VLA_EUNSUPPORTED (-4) /* valid request this build does not implement  */
+#define VLA_ESTATE (-5)       /* object in the wrong state (e.g. mismatched)  */
+
+/* ---- number types ---- */
+#define VLA_F32 0  /* every tensor and operand fp32                           */
+#define VLA_BF16 1 /* bf16 weights, GEMM operands and KV cache; fp32 elsewhere */
+
+/*
+ * Model shape. The paper fixes no layer shapes (it names the model families,
+ * Section 2.1); the fields below describe a SigLIP-style ViT, a Gemma-style
+ * prefix LM with grouped (multi-query) attention, and a pi0-style action
+ * expert that shares the LM's attention head layout.
+ */
+typedef struct vla_config {
+  int32_t dtype;                                 /* VLA_F32 or VLA_BF16          */
+  int32_t n_views, img_h, img_w, patch;          /* camera views, HWC image, patch */
+  int32_t vit_dim, vit_heads, vit_mlp, vit_layers;
+  int32_t lm_dim, lm_heads, lm_kv_heads, head_dim, lm_mlp, lm_layers;
+  int32_t vocab, n_text, state_dim;              /* state_dim 0 = no state token */
+  int32_t ex_dim, ex_mlp, ex_layers;             /* ex_layers must equal lm_layers */
+  int32_t chunk_len, action_dim, n_steps;        /* action chunk H x A, Euler steps */
+} vla_config;
+
+typedef struct vla_model vla_model;
+typedef struct vla_ctx vla_ctx;
+
+/* One robot frame, all device pointers, read-only for the library. */
+typedef struct vla_frame {
+  const float* pixels;     /* fp32 [n_views, img_h, img_w, 3] (HWC), values as given */
+  const int32_t* text_ids; /* int32 [n_text], each in [0, vocab)                     */
+  const float* state;      /* fp32 [state_dim]; NULL when state_dim == 0             */
+} vla_frame;
+
+/* Pipeline schedules (Fig. "streamexec"): */
+#define VLA_MODE_SERIAL 0     /* both phases of every frame on one stream           */
+#define VLA_MODE_CONCURRENT 1 /* VLM and action streams, hardware dispatcher decides */
+#define VLA_MODE_CU_MASKED 2  /* as CONCURRENT, each stream limited to a CU set      */
+#define VLA_MODE_WG_CAPPED 3  /* as CONCURRENT, VLM grids capped per CU              */
+
+typedef struct vla_sched {
+  int32_t mode;       /* VLA_MODE_*                                                 */
+  int32_t vlm_cus;    /* CU_MASKED: CUs for the VLM stream (multiple of 8)           */
+  int32_t act_cus;    /* CU_MASKED: CUs for the action stream (multiple of 8); the  */
+                      /*   two sets are disjoint and together at most the CU count   */
+  int32_t vlm_wg_cap; /* WG_CAPPED: max VLM workgroups per CU in flight (>= 1)       */
+  int32_t reserved[4];
+} vla_sched;
+
+typedef struct vla_timing {
+  double wall_ms;       /* host wall time of the run, enqueue to final sync   */
+  double frames_per_s;  /* R / wall time                                      */
+  double actions_per_s; /* frames_per_s * chunk_len (chunk rows per second)   */
+  double vlm_ms;        /* GPU time of the VLM phases (events), summed        */
+  double act_ms;        /* GPU time of the action phases (events), summed     */
+} vla_timing;
+
+/* Fill *out with a named preset: "tiny" (fp32, 2+2+2 layers, chunk 8x7,
+ * 4 steps), "pi0" (PaliGemma-3B-shaped VLM + pi0-shaped expert, bf16) or
+ * "pi0_3view" (pi0 with three camera views and 64 text tokens).
+ * VLA_EINVAL for an unknown name or NULL pointers. */
+int vla_preset(const char* name, vla_config* out);
+
+/* Check a configuration without allocating (VLA_EINVAL with a message when
+ * a shape rule fails: n_q % n_kv, ex_layers == lm_layers, patch divides the
+ * image, head_dim a multiple of 32, MLP widths multiples of 16, ...). */
+int vla_validate(const vla_config* cfg);
+
+/* Create a model on the current HIP device: validate cfg, generate every
+ * parameter from `seed` with the counter-based SplitMix64 generator (the
+ * same published generator the test inputs use; bf16 configurations round
+ * the fp32 master value to bf16, nearest-even), upload them and allocate the
+ * per-phase scratch memory. Blocking. The library owns *out. */
+int vla_create(const vla_config* cfg, uint64_t seed, vla_model** out);
+
+/* Free everything the model owns (waits for its streams). NULL is a no-op. */
+int vla_destroy(vla_model* m);
+
+/* Phase-1 -> phase-2 hand-off: the per-layer KV cache [lm_layers][prefix]
+ * [lm_kv_heads * head_dim] of the model's storage type. Caller-owned via
+ * these two calls; destroy NULL is a no-op. */
+int vla_ctx_create(vla_model* m, vla_ctx** out);
+int vla_ctx_destroy(vla_ctx* c);
+
+/* Phase 1 for one frame, enqueued on `stream`, asynchronous: ViT over each
+ * view, projector, prefix [image; text * sqrt(lm_dim); state], LM prefill
+ * writing every layer's K (after RoPE) and V into `ctx`. */
+int vla_vlm_prefill(vla_model* m, const vla_frame* in, vla_ctx* ctx, void* stream);
+
+/* Phase 2 for one frame, enqueued on `stream`, asynchronous: n_steps Euler
+ * steps x <- x + dt * v(x, t) from x_0 = noise at t = 1 to t = 0, each step a
+ * full pass of the expert over [ctx KV; its own KV]. noise and actions are
+ * device fp32 [chunk_len, action_dim] and may alias. Must be ordered after
+ * the prefill that wrote ctx (same stream, or an event wait). */
+int vla_action_denoise(vla_model* m, const vla_ctx* ctx, const float* noise, float* actions,
+                       void* stream);
+
+/* Run R frames through the two-stage pipeline and wait for it. frames:
+ * host array of R vla_frame (device pointers inside); noise: device fp32
+ * [R, chunk_len, action_dim]; actions: device fp32 [R, chunk_len,
+ * action_dim]. The VLM prefill of frame r+1 overlaps the action phase of
+ * frame r (two model-owned contexts, events between the streams) except in
+ * VLA_MODE_SERIAL. Results are bit-identical across modes. t may be NULL. */
+int vla_pipeline_run(vla_model* m, const vla_frame* frames, const float* noise, int32_t R,
+                     const vla_sched* sched, float* actions, vla_timing* t);
+
+/* Parameter inventory (host-side queries). Names follow the logical layout
+ * [out, in] of each matrix, e.g. "lm.3.q.w". */
+int vla_param_count(const vla_model* m, int32_t* count);
+int vla_param_info(const vla_model* m, int32_t i, const char** name, int64_t* numel);
+
+/* Copy one parameter, as the model stores it, to host fp32 in its logical
+ * layout (bf16 values upcast exactly). host_dst: numel floats. Blocking. */
+int vla_export_param(vla_model* m, const char* name, float* host_dst, int64_t numel);
+
+/* Copy layer `layer` of a context's K and V cache to host fp32 buffers of
+ * [prefix, lm_kv_heads * head_dim] each (logical head-dim order). Blocking. */
+int vla_ctx_export_kv(vla_model* m, const vla_ctx* c, int32_t layer, float* host_k, float* host_v);
+
+/* Test entry points for single kernels (same kernels and launch planner as
+ * the phases). dtype VLA_F32 or VLA_BF16 selects the operand type of A and W
+ * (bf16 passed as uint16 bit patterns). All pointers device.
+ *  gemm:      C[M,N] (fp32) = A[M,K] W[N,K]^T + bias[N] (bias may be NULL);
+ *             K a multiple of 8, lda/ldw >= K elements.
+ *  attention: out[Sq, nq*hd] = softmax(q k^T / sqrt(hd)) v per query head,
+ *             query head h reading KV head h / (nq / nkv); keys are
+ *             [k0 (S0 rows); k1 (S1 rows)], values likewise; rows of q have
+ *             nq*hd elements, rows of k/v nkv*hd (operand type); out in the
+ *             operand type. k1/v1 may be NULL when S1 == 0.             */
+int vla_debug_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* A, int32_t lda,
+                   const void* W, int32_t ldw, const float* bias, float* C, void* stream);
+int vla_debug_attention(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int32_t hd,
+                        const void* q, const void* k0, const void* v0, int32_t S0, const void* k1,
+                        const void* v1, int32_t S1, void* out, void* stream);
+
+/* Host-only: values start .. start+n-1 of the library's parameter generator
+ * for (seed, name) with the given mean and std, as fp32 (before any bf16
+ * rounding) into host_dst. Needs no GPU. */
+int vla_debug_generate(uint64_t seed, const char* name, int64_t n, double mean, double stdv,
+                       float* host_dst);
+
+/* Message for the last non-zero status on this thread ("" if none). */
+const char* vla_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VLA_H */

@@ -1,0 +1,221 @@
+"""Python binding of libvla.so, the MI355X two-phase VLA inference library.
+
+Argument marshalling only: every function forwards to the C entry point of
+the same name (see include/vla.h); every step of the computation runs in the
+library's HIP kernels. Device buffers are passed as integer device pointers
+(e.g. ``torch.Tensor.data_ptr()``) and streams as integer ``hipStream_t``
+handles (``torch.cuda.current_stream().cuda_stream``).
+
+Importing this module loads the library and raises if it is not built:
+there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, Iterable, Optional, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libvla.so")
+
+VLA_F32, VLA_BF16 = 0, 1
+MODE_SERIAL, MODE_CONCURRENT, MODE_CU_MASKED, MODE_WG_CAPPED = 0, 1, 2, 3
+MODES = {"serial": MODE_SERIAL, "concurrent": MODE_CONCURRENT, "cu_masked": MODE_CU_MASKED,
+         "wg_capped": MODE_WG_CAPPED}
+
+CONFIG_FIELDS = (
+    "dtype", "n_views", "img_h", "img_w", "patch",
+    "vit_dim", "vit_heads", "vit_mlp", "vit_layers",
+    "lm_dim", "lm_heads", "lm_kv_heads", "head_dim", "lm_mlp", "lm_layers",
+    "vocab", "n_text", "state_dim",
+    "ex_dim", "ex_mlp", "ex_layers", "chunk_len", "action_dim", "n_steps",
+)
+
+
+class vla_config(ctypes.Structure):
+    _fields_ = [(f, ctypes.c_int32) for f in CONFIG_FIELDS]
+
+
+class vla_frame(ctypes.Structure):
+    _fields_ = [("pixels", ctypes.c_void_p), ("text_ids", ctypes.c_void_p), ("state", ctypes.c_void_p)]
+
+
+class vla_sched(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int32), ("vlm_cus", ctypes.c_int32), ("act_cus", ctypes.c_int32),
+                ("vlm_wg_cap", ctypes.c_int32), ("reserved", ctypes.c_int32 * 4)]
+
+
+class vla_timing(ctypes.Structure):
+    _fields_ = [("wall_ms", ctypes.c_double), ("frames_per_s", ctypes.c_double),
+                ("actions_per_s", ctypes.c_double), ("vlm_ms", ctypes.c_double),
+                ("act_ms", ctypes.c_double)]
+
+
+class VlaError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"vla status {code}: {msg}")
+        self.code = code
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python paper_2609_22335_amd/build.py`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64, U64, D = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_double
+    sig = {
+        "vla_preset": [ctypes.c_char_p, ctypes.POINTER(vla_config)],
+        "vla_validate": [ctypes.POINTER(vla_config)],
+        "vla_create": [ctypes.POINTER(vla_config), U64, ctypes.POINTER(P)],
+        "vla_destroy": [P],
+        "vla_ctx_create": [P, ctypes.POINTER(P)],
+        "vla_ctx_destroy": [P],
+        "vla_vlm_prefill": [P, ctypes.POINTER(vla_frame), P, P],
+        "vla_action_denoise": [P, P, P, P, P],
+        "vla_pipeline_run": [P, ctypes.POINTER(vla_frame), P, I32, ctypes.POINTER(vla_sched), P,
+                             ctypes.POINTER(vla_timing)],
+        "vla_param_count": [P, ctypes.POINTER(I32)],
+        "vla_param_info": [P, I32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(I64)],
+        "vla_export_param": [P, ctypes.c_char_p, P, I64],
+        "vla_ctx_export_kv": [P, P, I32, P, P],
+        "vla_debug_gemm": [I32, I32, I32, I32, P, I32, P, I32, P, P, P],
+        "vla_debug_attention": [I32, I32, I32, I32, I32, P, P, P, I32, P, P, I32, P, P],
+        "vla_debug_generate": [U64, ctypes.c_char_p, I64, D, D, P],
+    }
+    for name, args in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = ctypes.c_int
+    lib.vla_last_error.argtypes = []
+    lib.vla_last_error.restype = ctypes.c_char_p
+    return lib
+
+
+_lib = _load()
+
+
+def vla_last_error() -> str:
+    return _lib.vla_last_error().decode()
+
+
+def _check(rc: int) -> None:
+    if rc != 0:
+        raise VlaError(rc, vla_last_error())
+
+
+def _cfg(cfg: Dict[str, int]) -> vla_config:
+    return vla_config(*[int(cfg[f]) for f in CONFIG_FIELDS])
+
+
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if hasattr(x, "data_ptr"):
+        return x.data_ptr()
+    return int(x)
+
+
+def vla_preset(name: str) -> Dict[str, int]:
+    c = vla_config()
+    _check(_lib.vla_preset(name.encode(), ctypes.byref(c)))
+    return {f: int(getattr(c, f)) for f in CONFIG_FIELDS}
+
+
+def vla_validate(cfg: Dict[str, int]) -> None:
+    _check(_lib.vla_validate(ctypes.byref(_cfg(cfg))))
+
+
+def vla_create(cfg: Dict[str, int], seed: int) -> int:
+    out = ctypes.c_void_p()
+    _check(_lib.vla_create(ctypes.byref(_cfg(cfg)), ctypes.c_uint64(seed), ctypes.byref(out)))
+    return out.value
+
+
+def vla_destroy(model: Optional[int]) -> None:
+    _check(_lib.vla_destroy(model))
+
+
+def vla_ctx_create(model: int) -> int:
+    out = ctypes.c_void_p()
+    _check(_lib.vla_ctx_create(model, ctypes.byref(out)))
+    return out.value
+
+
+def vla_ctx_destroy(ctx: Optional[int]) -> None:
+    _check(_lib.vla_ctx_destroy(ctx))
+
+
+def make_frame(pixels, text_ids, state=None) -> vla_frame:
+    """A vla_frame from device buffers (tensors or integer pointers)."""
+    return vla_frame(_ptr(pixels), _ptr(text_ids), _ptr(state))
+
+
+def vla_vlm_prefill(model: int, frame: vla_frame, ctx: int, stream: int = 0) -> None:
+    _check(_lib.vla_vlm_prefill(model, ctypes.byref(frame), ctx, stream or None))
+
+
+def vla_action_denoise(model: int, ctx: int, noise, actions, stream: int = 0) -> None:
+    _check(_lib.vla_action_denoise(model, ctx, _ptr(noise), _ptr(actions), stream or None))
+
+
+def vla_pipeline_run(model: int, frames: Sequence[vla_frame], noise, R: int, mode="serial",
+                     vlm_cus: int = 0, act_cus: int = 0, vlm_wg_cap: int = 0, actions=None) -> Dict[str, float]:
+    arr = (vla_frame * len(frames))(*frames)
+    s = vla_sched(MODES[mode] if isinstance(mode, str) else int(mode), vlm_cus, act_cus, vlm_wg_cap)
+    t = vla_timing()
+    _check(_lib.vla_pipeline_run(model, arr, _ptr(noise), int(R), ctypes.byref(s), _ptr(actions),
+                                 ctypes.byref(t)))
+    return {k: getattr(t, k) for k, _ in vla_timing._fields_}
+
+
+def vla_param_count(model: int) -> int:
+    n = ctypes.c_int32()
+    _check(_lib.vla_param_count(model, ctypes.byref(n)))
+    return n.value
+
+
+def vla_param_info(model: int, i: int) -> Tuple[str, int]:
+    name = ctypes.c_char_p()
+    numel = ctypes.c_int64()
+    _check(_lib.vla_param_info(model, i, ctypes.byref(name), ctypes.byref(numel)))
+    return name.value.decode(), numel.value
+
+
+def vla_export_param(model: int, name: str, numel: int) -> np.ndarray:
+    out = np.empty(numel, dtype=np.float32)
+    _check(_lib.vla_export_param(model, name.encode(), out.ctypes.data, numel))
+    return out
+
+
+def vla_ctx_export_kv(model: int, ctx: int, layer: int, n: int) -> Tuple[np.ndarray, np.ndarray]:
+    k = np.empty(n, dtype=np.float32)
+    v = np.empty(n, dtype=np.float32)
+    _check(_lib.vla_ctx_export_kv(model, ctx, layer, k.ctypes.data, v.ctypes.data))
+    return k, v
+
+
+def vla_debug_gemm(dtype: int, M: int, N: int, K: int, A, lda: int, W, ldw: int, bias, C,
+                   stream: int = 0) -> None:
+    _check(_lib.vla_debug_gemm(dtype, M, N, K, _ptr(A), lda, _ptr(W), ldw, _ptr(bias), _ptr(C),
+                               stream or None))
+
+
+def vla_debug_attention(dtype: int, Sq: int, nq: int, nkv: int, hd: int, q, k0, v0, S0: int,
+                        k1, v1, S1: int, out, stream: int = 0) -> None:
+    _check(_lib.vla_debug_attention(dtype, Sq, nq, nkv, hd, _ptr(q), _ptr(k0), _ptr(v0), S0,
+                                    _ptr(k1), _ptr(v1), S1, _ptr(out), stream or None))
+
+
+def vla_debug_generate(seed: int, name: str, n: int, mean: float, std: float) -> np.ndarray:
+    out = np.empty(n, dtype=np.float32)
+    _check(_lib.vla_debug_generate(ctypes.c_uint64(seed), name.encode(), n, mean, std, out.ctypes.data))
+    return out
+
+
+def exported_symbols() -> Iterable[str]:
+    """Names of the C entry points this binding wraps."""
+    return ["vla_preset", "vla_validate", "vla_create", "vla_destroy", "vla_ctx_create",
+            "vla_ctx_destroy", "vla_vlm_prefill", "vla_action_denoise", "vla_pipeline_run",
+            "vla_param_count", "vla_param_info", "vla_export_param", "vla_ctx_export_kv",
+            "vla_debug_gemm", "vla_debug_attention", "vla_debug_generate", "vla_last_error"]

@@ -1,0 +1,878 @@
+// gfx950 kernels of the two-phase VLA hot path.
+//
+// GEMMs and attention run on the matrix cores (MFMA, 64-wide wavefronts):
+// bf16 operands use v_mfma_f32_16x16x32_bf16, fp32 operands
+// v_mfma_f32_16x16x4_f32; accumulation is always fp32. Norms, softmax,
+// activations, RoPE and the Euler update are fp32 and are fused into the
+// producing kernel where they are elementwise (GEMM epilogues).
+//
+// Every reduction has a fixed order that depends only on the problem shape
+// (tile sizes, split-K and KV-split factors come from the shape), so results
+// do not depend on the grid size, CU mask or on which workgroup ran a tile.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "kernels.h"
+
+namespace vla {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int NUM_CU_PLAN = 256;  // planner constant; never the live CU count
+
+__device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);  // round to nearest, ties to even (finite values)
+  return (uint16_t)(u >> 16);
+}
+
+template <typename T>
+struct TT;
+template <>
+struct TT<float> {
+  static __device__ __forceinline__ float ld(const float* p) { return *p; }
+  static __device__ __forceinline__ void st(float* p, float v) { *p = v; }
+};
+template <>
+struct TT<uint16_t> {
+  static __device__ __forceinline__ float ld(const uint16_t* p) { return bf2f(*p); }
+  static __device__ __forceinline__ void st(uint16_t* p, float v) { *p = f2bf(v); }
+};
+
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float c = 0.7978845608028654f;  // sqrt(2 / pi)
+  return 0.5f * x * (1.f + tanhf(c * (x + 0.044715f * x * x * x)));
+}
+__device__ __forceinline__ float swishf(float x) { return x / (1.f + expf(-x)); }
+
+// One MFMA step over a 16-byte slice of K per lane (8 bf16 or 4 fp32).
+__device__ __forceinline__ f32x4 mfma_step(uint4 a, uint4 b, f32x4 c, uint16_t) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma_step(uint4 a, uint4 b, f32x4 c, float) {
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+  c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+  return c;
+}
+
+// ---------------------------------------------------------------------------
+// GEMM epilogues
+// ---------------------------------------------------------------------------
+
+template <typename T>
+__device__ __forceinline__ void epi_one(const Epi& e, int m, int n, float v) {
+  switch (e.kind) {
+    case EPI_F32: {
+      if (e.bias) v += e.bias[n];
+      if (e.rowadd) v += e.rowadd[(size_t)(m % e.rowadd_period) * e.ldra + n];
+      ((float*)e.out)[(size_t)m * e.ldo + n] = v;
+      break;
+    }
+    case EPI_T: {
+      if (e.bias) v += e.bias[n];
+      TT<T>::st((T*)e.out + (size_t)m * e.ldo + n, v);
+      break;
+    }
+    case EPI_RESID: {
+      if (e.bias) v += e.bias[n];
+      e.resid[(size_t)m * e.ldr + n] += v;
+      break;
+    }
+    case EPI_GELU: {
+      if (e.bias) v += e.bias[n];
+      TT<T>::st((T*)e.out + (size_t)m * e.ldo + n, gelu_tanh(v));
+      break;
+    }
+    case EPI_SWISH: {
+      if (e.bias) v += e.bias[n];
+      TT<T>::st((T*)e.out + (size_t)m * e.ldo + n, swishf(v));
+      break;
+    }
+    case EPI_EULER: {
+      if (e.bias) v += e.bias[n];
+      float* xp = e.x + (size_t)m * e.ldx + n;
+      const float xn = *xp + e.dt * v;
+      *xp = xn;
+      TT<T>::st((T*)e.xop + (size_t)m * e.ldxop + n, xn);
+      break;
+    }
+    default:
+      break;
+  }
+}
+
+// n: a physical column with n % 32 < 16; v1 is the value of column n + 16.
+template <typename T>
+__device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int n, float v0,
+                                         float v1) {
+  if (m >= M) return;
+  if (e.kind == EPI_GEGLU) {
+    if (n + 16 >= N) return;
+    const int g = n >> 5, j = n & 15;
+    TT<T>::st((T*)e.out + (size_t)m * e.ldo + 16 * g + j, gelu_tanh(v0) * v1);
+    return;
+  }
+  if (e.kind == EPI_QKV_ROPE) {
+    if (n + 16 >= N) return;
+    const int hd = e.hd, qcols = e.nq * hd, kcols = e.nkv * hd;
+    if (n < qcols + kcols) {
+      const bool isq = n < qcols;
+      const int rn = isq ? n : n - qcols;
+      const int head = rn / hd, p = rn - head * hd;
+      const int i = 16 * (p >> 5) + (p & 15);  // rotate-half pair (i, i + hd/2)
+      const size_t t = (size_t)(e.pos0 + m) * (hd / 2) + i;
+      const float c = e.rope_cos[t], s = e.rope_sin[t];
+      T* dst = (isq ? (T*)e.q + (size_t)m * e.ldq : (T*)e.k + (size_t)m * e.ldkv) + head * hd;
+      TT<T>::st(dst + i, v0 * c - v1 * s);
+      TT<T>::st(dst + i + hd / 2, v1 * c + v0 * s);
+    } else {
+      const int c0 = n - qcols - kcols;
+      T* dst = (T*)e.v + (size_t)m * e.ldkv;
+      TT<T>::st(dst + c0, v0);
+      TT<T>::st(dst + c0 + 16, v1);
+    }
+    return;
+  }
+  if (n < N) epi_one<T>(e, m, n, v0);
+  if (n + 16 < N) epi_one<T>(e, m, n + 16, v1);
+}
+
+// ---------------------------------------------------------------------------
+// GEMM: C[M, N] = A[M, K] W[N, K]^T, both operands K-contiguous.
+// 256 threads = 4 waves in a 2 x 2 arrangement; each wave owns a
+// (BM/2) x (BN/2) block of 16 x 16 MFMA tiles. A and W tiles are staged
+// through LDS (rows padded by 16 bytes against bank conflicts) with the next
+// K-tile prefetched into registers while the current one is multiplied.
+// Tiles are visited grid-stride so a capped grid computes the same tiles.
+// ---------------------------------------------------------------------------
+
+template <typename T, int BM, int BN, int BK>
+__global__ __launch_bounds__(256) void k_gemm(const T* __restrict__ A, int lda,
+                                              const T* __restrict__ W, int ldw, int M, int N,
+                                              int K, int kchunk, int splits, int tiles_m,
+                                              int tiles_n, Epi e, float* __restrict__ part) {
+  constexpr int VEC = 16 / sizeof(T);
+  constexpr int SW = 4 * VEC;  // K covered by one MFMA step across the 4 lane groups
+  constexpr int LDS = BK + VEC;
+  constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 16, TN = WN / 16;
+  constexpr int KV = BK / VEC;
+  constexpr int AV = BM * KV / 256, BV = BN * KV / 256;
+  static_assert(AV >= 1 && BV >= 1 && (BM * KV) % 256 == 0 && (BN * KV) % 256 == 0, "tile");
+  static_assert(TN % 2 == 0, "paired epilogues need 32-column groups per wave");
+  __shared__ __attribute__((aligned(16))) T sA[BM * LDS];
+  __shared__ __attribute__((aligned(16))) T sB[BN * LDS];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int ntiles = tiles_m * tiles_n * splits;
+  const T dummy = T();
+
+  for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int s = tile % splits;
+    const int t2 = tile / splits;
+    const int tm = t2 % tiles_m, tn = t2 / tiles_m;
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int kbeg = s * kchunk, kend = min(K, kbeg + kchunk);
+
+    f32x4 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    uint4 ra[AV], rb[BV];
+    auto gload = [&](int k0) {
+#pragma unroll
+      for (int i = 0; i < AV; ++i) {
+        const int c = tid + i * 256, r = c / KV, kc = (c % KV) * VEC;
+        const int gm = m0 + r, gk = k0 + kc;
+        ra[i] = (gm < M && gk < kend) ? *(const uint4*)(A + (size_t)gm * lda + gk)
+                                      : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int i = 0; i < BV; ++i) {
+        const int c = tid + i * 256, r = c / KV, kc = (c % KV) * VEC;
+        const int gn = n0 + r, gk = k0 + kc;
+        rb[i] = (gn < N && gk < kend) ? *(const uint4*)(W + (size_t)gn * ldw + gk)
+                                      : make_uint4(0, 0, 0, 0);
+      }
+    };
+
+    if (kbeg < kend) gload(kbeg);
+    for (int k0 = kbeg; k0 < kend; k0 += BK) {
+      __syncthreads();
+#pragma unroll
+      for (int i = 0; i < AV; ++i) {
+        const int c = tid + i * 256, r = c / KV, kc = (c % KV) * VEC;
+        *(uint4*)(sA + r * LDS + kc) = ra[i];
+      }
+#pragma unroll
+      for (int i = 0; i < BV; ++i) {
+        const int c = tid + i * 256, r = c / KV, kc = (c % KV) * VEC;
+        *(uint4*)(sB + r * LDS + kc) = rb[i];
+      }
+      __syncthreads();
+      if (k0 + BK < kend) gload(k0 + BK);
+#pragma unroll
+      for (int ks = 0; ks < BK / SW; ++ks) {
+        uint4 af[TM], bfg[TN];
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+          af[i] = *(const uint4*)(sA + (wm * WM + i * 16 + (lane & 15)) * LDS + ks * SW +
+                                  (lane >> 4) * VEC);
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          bfg[j] = *(const uint4*)(sB + (wn * WN + j * 16 + (lane & 15)) * LDS + ks * SW +
+                                   (lane >> 4) * VEC);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) acc[i][j] = mfma_step(af[i], bfg[j], acc[i][j], dummy);
+      }
+    }
+
+    if (splits > 1) {
+      float* P = part + (size_t)s * M * N;
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + r;
+            const int n = n0 + wn * WN + j * 16 + (lane & 15);
+            if (m < M && n < N) P[(size_t)m * N + n] = acc[i][j][r];
+          }
+    } else {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int jj = 0; jj < TN / 2; ++jj)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + r;
+            const int n = n0 + wn * WN + jj * 32 + (lane & 15);
+            epi_pair<T>(e, M, N, m, n, acc[i][2 * jj][r], acc[i][2 * jj + 1][r]);
+          }
+    }
+  }
+}
+
+// Sum of split-K partials in split order, then the epilogue.
+template <typename T>
+__global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__ part, int splits,
+                                                       int M, int N, Epi e) {
+  const int groups = (N + 31) / 32;
+  const long long total = (long long)M * groups * 16;
+  for (long long idx = blockIdx.x * (long long)blockDim.x + threadIdx.x; idx < total;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const int j = (int)(idx & 15);
+    const long long t = idx >> 4;
+    const int g = (int)(t % groups), m = (int)(t / groups);
+    const int n = g * 32 + j;
+    float v0 = 0.f, v1 = 0.f;
+    for (int s = 0; s < splits; ++s) {
+      const float* P = part + (size_t)s * M * N + (size_t)m * N;
+      if (n < N) v0 += P[n];
+      if (n + 16 < N) v1 += P[n + 16];
+    }
+    epi_pair<T>(e, M, N, m, n, v0, v1);
+  }
+}
+
+struct TileCfg {
+  int bm, bn, bk;
+};
+// bf16 configurations, then fp32 ones.
+static const TileCfg kBf16Cfg[] = {{128, 128, 64}, {64, 128, 64}, {64, 64, 64}, {32, 64, 128}};
+static const TileCfg kF32Cfg[] = {{64, 64, 32}, {32, 64, 64}};
+
+GemmPlan plan_gemm(const GemmDesc& g) {
+  GemmPlan p{};
+  const TileCfg* cfgs = g.dtype == DT_BF16 ? kBf16Cfg : kF32Cfg;
+  int c;
+  if (g.dtype == DT_BF16) {
+    if (g.M >= 256) {
+      const int t128 = ((g.M + 127) / 128) * ((g.N + 127) / 128);
+      c = t128 >= NUM_CU_PLAN ? 0 : 1;
+    } else if (g.M > 32) {
+      c = 2;
+    } else {
+      c = 3;
+    }
+  } else {
+    c = g.M > 32 ? 0 : 1;
+  }
+  const TileCfg t = cfgs[c];
+  const int tiles = ((g.M + t.bm - 1) / t.bm) * ((g.N + t.bn - 1) / t.bn);
+  int splits = 1;
+  const int kblocks = (g.K + t.bk - 1) / t.bk;
+  if (tiles < NUM_CU_PLAN && kblocks >= 4) {
+    splits = std::min((NUM_CU_PLAN + tiles - 1) / tiles, kblocks / 2);
+    splits = std::max(splits, 1);
+  }
+  const int kchunk_blocks = (kblocks + splits - 1) / splits;
+  splits = (kblocks + kchunk_blocks - 1) / kchunk_blocks;
+  p.cfg = c;
+  p.splits = splits;
+  p.tiles = tiles * splits;
+  p.scratch_floats = splits > 1 ? (size_t)splits * g.M * g.N : 0;
+  return p;
+}
+
+template <typename T, int BM, int BN, int BK>
+static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch& s,
+                             const LaunchCaps& caps, hipStream_t st) {
+  const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
+  const int kblocks = (g.K + BK - 1) / BK;
+  const int kchunk = ((kblocks + p.splits - 1) / p.splits) * BK;
+  int grid = p.tiles;
+  if (caps.max_wgs > 0) grid = std::min(grid, caps.max_wgs);
+  k_gemm<T, BM, BN, BK><<<grid, 256, 0, st>>>((const T*)g.A, g.lda, (const T*)g.W, g.ldw, g.M,
+                                               g.N, g.K, kchunk, p.splits, tiles_m, tiles_n,
+                                               g.epi, s.ptr);
+  if (p.splits > 1) {
+    const long long total = (long long)g.M * ((g.N + 31) / 32) * 16;
+    int rgrid = (int)std::min<long long>((total + 255) / 256, 4096);
+    if (caps.max_wgs > 0) rgrid = std::min(rgrid, caps.max_wgs);
+    k_splitk_reduce<T><<<rgrid, 256, 0, st>>>(s.ptr, p.splits, g.M, g.N, g.epi);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm(const GemmDesc& g, const Scratch& s, const LaunchCaps& caps,
+                       hipStream_t st) {
+  const GemmPlan p = plan_gemm(g);
+  if (p.scratch_floats > s.floats) return hipErrorInvalidValue;
+  if (g.dtype == DT_BF16) {
+    switch (p.cfg) {
+      case 0: return run_gemm_t<uint16_t, 128, 128, 64>(g, p, s, caps, st);
+      case 1: return run_gemm_t<uint16_t, 64, 128, 64>(g, p, s, caps, st);
+      case 2: return run_gemm_t<uint16_t, 64, 64, 64>(g, p, s, caps, st);
+      default: return run_gemm_t<uint16_t, 32, 64, 128>(g, p, s, caps, st);
+    }
+  }
+  switch (p.cfg) {
+    case 0: return run_gemm_t<float, 64, 64, 32>(g, p, s, caps, st);
+    default: return run_gemm_t<float, 32, 64, 64>(g, p, s, caps, st);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Attention: unmasked softmax(q k^T / sqrt(hd)) v with grouped KV heads and
+// keys from two segments [k0; k1]. The rows of one KV head's query heads are
+// packed (row r <-> query r / group, head r % group), 64 packed rows per
+// workgroup, 16 per wave. Keys stream in blocks of 32 through LDS (V stored
+// transposed); scores and the online softmax are fp32. P V runs on MFMA: in
+// bf16 with P split into a bf16 high part and a bf16 remainder (two MFMAs,
+// so P keeps ~16 significant bits); in fp32 directly. Long key ranges are
+// split across workgroups and merged in split order by k_attn_combine.
+// ---------------------------------------------------------------------------
+
+constexpr int ATT_BQ = 64, ATT_BKV = 32;
+
+struct AttnArgs {
+  const void* q;
+  const void* k0;
+  const void* v0;
+  const void* k1;
+  const void* v1;
+  void* out;
+  float* po;  // partial outputs [work][splits][64][HDP]
+  float* pm;  // partial row max (log2 domain) [work][splits][64]
+  float* pl;  // partial row sums
+  int ldq, ldkv, ldo, Sq, nq, nkv, hd, S0, S1, segs, splits, qblocks;
+  long long seg_q, seg_kv, seg_o;
+  float scale_log2;
+};
+
+template <typename T, int HDP>
+__global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
+  constexpr int VEC = 16 / sizeof(T);
+  constexpr int SW = 4 * VEC;
+  constexpr int KS = HDP + VEC;          // sK row stride
+  constexpr int VS = ATT_BKV + VEC;      // sVt row stride
+  constexpr int PS = ATT_BKV + 4;        // sP row stride (fp32)
+  constexpr int NQF = HDP / SW;          // Q fragments per lane
+  constexpr int NOT = HDP / 16;          // output tiles per wave
+  __shared__ __attribute__((aligned(16))) T sK[ATT_BKV * KS];
+  __shared__ __attribute__((aligned(16))) T sVt[HDP * VS];
+  __shared__ __attribute__((aligned(16))) float sP[4 * 16 * PS];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int group = a.nq / a.nkv;
+  const int R = a.Sq * group;
+  const int Skv = a.S0 + a.S1;
+  const int nblk = (Skv + ATT_BKV - 1) / ATT_BKV;
+  const int bps = (nblk + a.splits - 1) / a.splits;
+  const int total = a.qblocks * a.nkv * a.segs * a.splits;
+  const T dummy = T();
+
+  for (int w = blockIdx.x; w < total; w += gridDim.x) {
+    const int sp = w % a.splits;
+    const int work = w / a.splits;
+    int t = work;
+    const int qb = t % a.qblocks;
+    t /= a.qblocks;
+    const int j = t % a.nkv;
+    const int seg = t / a.nkv;
+
+    const T* Q = (const T*)a.q + seg * a.seg_q;
+    const T* K0 = (const T*)a.k0 + seg * a.seg_kv + j * a.hd;
+    const T* V0 = (const T*)a.v0 + seg * a.seg_kv + j * a.hd;
+    const T* K1 = a.k1 ? (const T*)a.k1 + seg * a.seg_kv + j * a.hd : nullptr;
+    const T* V1 = a.v1 ? (const T*)a.v1 + seg * a.seg_kv + j * a.hd : nullptr;
+
+    // Q fragments of this lane's packed row (A-operand layout).
+    uint4 qf[NQF];
+    {
+      const int r = qb * ATT_BQ + wave * 16 + (lane & 15);
+      const int sq = r / group, h = j * group + r % group;
+#pragma unroll
+      for (int ks = 0; ks < NQF; ++ks) {
+        const int d = ks * SW + (lane >> 4) * VEC;
+        qf[ks] = (r < R && d < a.hd) ? *(const uint4*)(Q + (size_t)sq * a.ldq + h * a.hd + d)
+                                     : make_uint4(0, 0, 0, 0);
+      }
+    }
+
+    float mrow[4], lrow[4];
+    f32x4 o[NOT];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      mrow[r] = -INFINITY;
+      lrow[r] = 0.f;
+    }
+#pragma unroll
+    for (int d = 0; d < NOT; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    const int b0 = sp * bps, b1 = min(nblk, b0 + bps);
+    for (int b = b0; b < b1; ++b) {
+      __syncthreads();
+      constexpr int NV = ATT_BKV * (HDP / VEC);
+      for (int c = tid; c < NV; c += 256) {
+        const int kk = c / (HDP / VEC), d = (c % (HDP / VEC)) * VEC;
+        const int key = b * ATT_BKV + kk;
+        uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+        if (key < Skv && d < a.hd) {
+          const T* kp = key < a.S0 ? K0 + (size_t)key * a.ldkv : K1 + (size_t)(key - a.S0) * a.ldkv;
+          const T* vp = key < a.S0 ? V0 + (size_t)key * a.ldkv : V1 + (size_t)(key - a.S0) * a.ldkv;
+          kv = *(const uint4*)(kp + d);
+          vv = *(const uint4*)(vp + d);
+        }
+        *(uint4*)(sK + kk * KS + d) = kv;
+        const T* ve = (const T*)&vv;
+#pragma unroll
+        for (int q = 0; q < VEC; ++q) sVt[(d + q) * VS + kk] = ve[q];
+      }
+      __syncthreads();
+
+      // scores for 16 rows x 32 keys
+      f32x4 sacc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+        for (int ks = 0; ks < NQF; ++ks) {
+          const uint4 kf = *(const uint4*)(sK + (nt * 16 + (lane & 15)) * KS + ks * SW +
+                                           (lane >> 4) * VEC);
+          sacc[nt] = mfma_step(qf[ks], kf, sacc[nt], dummy);
+        }
+
+      float p[2][4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          const int key = b * ATT_BKV + nt * 16 + (lane & 15);
+          const float sv = key < Skv ? sacc[nt][r] * a.scale_log2 : -INFINITY;
+          p[nt][r] = sv;
+          mx = fmaxf(mx, sv);
+        }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+        const float mnew = fmaxf(mrow[r], mx);
+        const float alpha = exp2f(mrow[r] - mnew);
+        float sum = 0.f;
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          p[nt][r] = exp2f(p[nt][r] - mnew);
+          sum += p[nt][r];
+        }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off);
+        lrow[r] = lrow[r] * alpha + sum;
+        mrow[r] = mnew;
+#pragma unroll
+        for (int d = 0; d < NOT; ++d) o[d][r] *= alpha;
+      }
+
+      // P to LDS (C layout), back in A-operand layout
+      float* myP = sP + wave * 16 * PS;
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) myP[((lane >> 4) * 4 + r) * PS + nt * 16 + (lane & 15)] = p[nt][r];
+      __builtin_amdgcn_s_waitcnt(0);
+      __builtin_amdgcn_wave_barrier();
+
+#pragma unroll
+      for (int ks = 0; ks < ATT_BKV / SW; ++ks) {
+        const float* pr = myP + (lane & 15) * PS + ks * SW + (lane >> 4) * VEC;
+        if constexpr (sizeof(T) == 2) {
+          uint32_t hi[4], lo[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float x0 = pr[2 * q], x1 = pr[2 * q + 1];
+            const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
+            const uint16_t l0 = f2bf(x0 - bf2f(h0)), l1 = f2bf(x1 - bf2f(h1));
+            hi[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+            lo[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+          }
+          const uint4 phi = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+          const uint4 plo = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+#pragma unroll
+          for (int d = 0; d < NOT; ++d) {
+            const uint4 vf = *(const uint4*)(sVt + (d * 16 + (lane & 15)) * VS + ks * SW + (lane >> 4) * VEC);
+            o[d] = mfma_step(phi, vf, o[d], dummy);
+            o[d] = mfma_step(plo, vf, o[d], dummy);
+          }
+        } else {
+          const uint4 pf = make_uint4(__float_as_uint(pr[0]), __float_as_uint(pr[1]),
+                                      __float_as_uint(pr[2]), __float_as_uint(pr[3]));
+#pragma unroll
+          for (int d = 0; d < NOT; ++d) {
+            const uint4 vf = *(const uint4*)(sVt + (d * 16 + (lane & 15)) * VS + ks * SW + (lane >> 4) * VEC);
+            o[d] = mfma_step(pf, vf, o[d], dummy);
+          }
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+
+    // rows of this lane in the C layout
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int rr = (lane >> 4) * 4 + r;
+      const int prow = qb * ATT_BQ + wave * 16 + rr;
+      if (a.splits == 1) {
+        if (prow >= R) continue;
+        const int sq = prow / group, h = j * group + prow % group;
+        T* op = (T*)a.out + seg * a.seg_o + (size_t)sq * a.ldo + h * a.hd;
+        const float inv = 1.f / lrow[r];
+#pragma unroll
+        for (int d = 0; d < NOT; ++d) {
+          const int col = d * 16 + (lane & 15);
+          if (col < a.hd) TT<T>::st(op + col, o[d][r] * inv);
+        }
+      } else {
+        const size_t base = ((size_t)work * a.splits + sp) * ATT_BQ + wave * 16 + rr;
+#pragma unroll
+        for (int d = 0; d < NOT; ++d) a.po[base * HDP + d * 16 + (lane & 15)] = o[d][r];
+        if ((lane & 15) == 0) {
+          a.pm[base] = mrow[r];
+          a.pl[base] = lrow[r];
+        }
+      }
+    }
+  }
+}
+
+template <typename T, int HDP>
+__global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
+  const int group = a.nq / a.nkv;
+  const int R = a.Sq * group;
+  const int nwork = a.qblocks * a.nkv * a.segs;
+  const long long total = (long long)nwork * ATT_BQ * HDP;
+  for (long long idx = blockIdx.x * (long long)blockDim.x + threadIdx.x; idx < total;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const int d = (int)(idx % HDP);
+    const long long t = idx / HDP;
+    const int row = (int)(t % ATT_BQ);
+    const int work = (int)(t / ATT_BQ);
+    int u = work;
+    const int qb = u % a.qblocks;
+    u /= a.qblocks;
+    const int j = u % a.nkv;
+    const int seg = u / a.nkv;
+    const int prow = qb * ATT_BQ + row;
+    if (prow >= R || d >= a.hd) continue;
+    float mx = -INFINITY;
+    for (int s = 0; s < a.splits; ++s) mx = fmaxf(mx, a.pm[((size_t)work * a.splits + s) * ATT_BQ + row]);
+    float num = 0.f, den = 0.f;
+    for (int s = 0; s < a.splits; ++s) {
+      const size_t base = ((size_t)work * a.splits + s) * ATT_BQ + row;
+      const float m = a.pm[base];
+      if (m == -INFINITY) continue;
+      const float wgt = exp2f(m - mx);
+      num += wgt * a.po[base * HDP + d];
+      den += wgt * a.pl[base];
+    }
+    const int sq = prow / group, h = j * group + prow % group;
+    T* op = (T*)a.out + seg * a.seg_o + (size_t)sq * a.ldo + h * a.hd;
+    TT<T>::st(op + d, num / den);
+  }
+}
+
+static int attn_hdp(int hd, int dtype) {
+  const int sw = dtype == DT_BF16 ? 32 : 16;
+  int h = (hd + sw - 1) / sw * sw;
+  if (h <= 32) return 32;
+  if (h <= 64) return 64;
+  if (h <= 96) return 96;
+  if (h <= 128) return 128;
+  if (h <= 256) return 256;
+  return -1;
+}
+
+static void attn_split(const AttnDesc& d, int* qblocks, int* splits) {
+  const int group = d.nq / d.nkv;
+  *qblocks = (d.Sq * group + ATT_BQ - 1) / ATT_BQ;
+  const int base = *qblocks * d.nkv * d.segs;
+  const int nblk = (d.S0 + d.S1 + ATT_BKV - 1) / ATT_BKV;
+  int s = 1;
+  if (base < 128 && nblk >= 4) s = std::min((128 + base - 1) / base, nblk / 2);
+  s = std::max(s, 1);
+  const int bps = (nblk + s - 1) / s;
+  *splits = (nblk + bps - 1) / bps;
+}
+
+size_t attn_scratch_floats(const AttnDesc& d) {
+  int qb, sp;
+  attn_split(d, &qb, &sp);
+  if (sp == 1) return 0;
+  const int hdp = attn_hdp(d.hd, d.dtype);
+  const size_t rows = (size_t)qb * d.nkv * d.segs * sp * ATT_BQ;
+  return rows * hdp + 2 * rows;
+}
+
+template <typename T, int HDP>
+static hipError_t run_attn_t(const AttnArgs& a, const LaunchCaps& caps, hipStream_t st) {
+  const int total = a.qblocks * a.nkv * a.segs * a.splits;
+  int grid = total;
+  if (caps.max_wgs > 0) grid = std::min(grid, caps.max_wgs);
+  k_attn<T, HDP><<<grid, 256, 0, st>>>(a);
+  if (a.splits > 1) {
+    const long long n = (long long)a.qblocks * a.nkv * a.segs * ATT_BQ * HDP;
+    int cg = (int)std::min<long long>((n + 255) / 256, 4096);
+    if (caps.max_wgs > 0) cg = std::min(cg, caps.max_wgs);
+    k_attn_combine<T, HDP><<<cg, 256, 0, st>>>(a);
+  }
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t run_attn_hd(const AttnArgs& a, int hdp, const LaunchCaps& caps, hipStream_t st) {
+  switch (hdp) {
+    case 32: return run_attn_t<T, 32>(a, caps, st);
+    case 64: return run_attn_t<T, 64>(a, caps, st);
+    case 96: return run_attn_t<T, 96>(a, caps, st);
+    case 128: return run_attn_t<T, 128>(a, caps, st);
+    case 256: return run_attn_t<T, 256>(a, caps, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_attention(const AttnDesc& d, const Scratch& s, const LaunchCaps& caps,
+                            hipStream_t st) {
+  const int hdp = attn_hdp(d.hd, d.dtype);
+  if (hdp < 0 || d.nq % d.nkv != 0 || d.S0 + d.S1 <= 0 || d.Sq <= 0) return hipErrorInvalidValue;
+  AttnArgs a{};
+  a.q = d.q;
+  a.k0 = d.k0;
+  a.v0 = d.v0;
+  a.k1 = d.k1;
+  a.v1 = d.v1;
+  a.out = d.out;
+  a.ldq = d.ldq;
+  a.ldkv = d.ldkv;
+  a.ldo = d.ldo;
+  a.Sq = d.Sq;
+  a.nq = d.nq;
+  a.nkv = d.nkv;
+  a.hd = d.hd;
+  a.S0 = d.S0;
+  a.S1 = d.S1;
+  a.segs = d.segs;
+  a.seg_q = d.seg_q;
+  a.seg_kv = d.seg_kv;
+  a.seg_o = d.seg_o;
+  a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.hd));
+  attn_split(d, &a.qblocks, &a.splits);
+  if (a.splits > 1) {
+    const size_t rows = (size_t)a.qblocks * d.nkv * d.segs * a.splits * ATT_BQ;
+    if (rows * hdp + 2 * rows > s.floats) return hipErrorInvalidValue;
+    a.po = s.ptr;
+    a.pm = s.ptr + rows * hdp;
+    a.pl = a.pm + rows;
+  }
+  if (d.dtype == DT_BF16) return run_attn_hd<uint16_t>(a, hdp, caps, st);
+  return run_attn_hd<float>(a, hdp, caps, st);
+}
+
+// ---------------------------------------------------------------------------
+// Row norms (LayerNorm with biased variance, or RMSNorm), fp32 statistics,
+// one workgroup per row, fixed-order tree reduction.
+// ---------------------------------------------------------------------------
+
+__device__ __forceinline__ float block_sum(float v, float* red) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  return (red[0] + red[1]) + (red[2] + red[3]);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_norm(const float* __restrict__ x, int ldx, int rows,
+                                              int d, const float* __restrict__ g,
+                                              const float* __restrict__ b, int rms, T* out,
+                                              int ldo) {
+  __shared__ float red[4];
+  for (int row = blockIdx.x; row < rows; row += gridDim.x) {
+    const float* xr = x + (size_t)row * ldx;
+    float mean = 0.f;
+    if (!rms) {
+      float s = 0.f;
+      for (int i = threadIdx.x; i < d; i += 256) s += xr[i];
+      mean = block_sum(s, red) / d;
+    }
+    float s2 = 0.f;
+    for (int i = threadIdx.x; i < d; i += 256) {
+      const float c = xr[i] - mean;
+      s2 += c * c;
+    }
+    const float inv = 1.f / sqrtf(block_sum(s2, red) / d + 1e-6f);
+    T* orow = out + (size_t)row * ldo;
+    for (int i = threadIdx.x; i < d; i += 256) {
+      float y = (xr[i] - mean) * inv * g[i];
+      if (b) y += b[i];
+      TT<T>::st(orow + i, y);
+    }
+  }
+}
+
+hipError_t launch_norm(int dtype, const float* x, int ldx, int rows, int d, const float* g,
+                       const float* b, bool rms, void* out, int ldo, hipStream_t st) {
+  const int grid = std::min(rows, 4096);
+  if (dtype == DT_BF16)
+    k_norm<uint16_t><<<grid, 256, 0, st>>>(x, ldx, rows, d, g, b, rms, (uint16_t*)out, ldo);
+  else
+    k_norm<float><<<grid, 256, 0, st>>>(x, ldx, rows, d, g, b, rms, (float*)out, ldo);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Small gathers
+// ---------------------------------------------------------------------------
+
+template <typename T>
+__global__ void k_patchify(const float* __restrict__ pix, int views, int H, int W, int p,
+                           T* __restrict__ out, int ldo) {
+  const int gw = W / p, gh = H / p, T_ = gh * gw, kp = 3 * p * p;
+  const long long total = (long long)views * T_ * ldo;
+  for (long long idx = blockIdx.x * (long long)blockDim.x + threadIdx.x; idx < total;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const int c = (int)(idx % ldo);
+    const long long row = idx / ldo;
+    float v = 0.f;
+    if (c < kp) {
+      const int view = (int)(row / T_), t = (int)(row % T_);
+      const int pi = t / gw, pj = t % gw;
+      const int ch = c % 3, rc = c / 3, pr = rc / p, pc = rc % p;
+      v = pix[(((size_t)view * H + pi * p + pr) * W + pj * p + pc) * 3 + ch];
+    }
+    TT<T>::st(out + idx, v);
+  }
+}
+
+hipError_t launch_patchify(int dtype, const float* pix, int views, int H, int W, int p, void* out,
+                           int ldo, hipStream_t st) {
+  const long long total = (long long)views * (H / p) * (W / p) * ldo;
+  const int grid = (int)std::min<long long>((total + 255) / 256, 4096);
+  if (dtype == DT_BF16)
+    k_patchify<uint16_t><<<grid, 256, 0, st>>>(pix, views, H, W, p, (uint16_t*)out, ldo);
+  else
+    k_patchify<float><<<grid, 256, 0, st>>>(pix, views, H, W, p, (float*)out, ldo);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ void k_embed(const T* __restrict__ E, int d, int vocab, const int32_t* __restrict__ ids,
+                        int n, float scale, float* __restrict__ x, int ldx) {
+  for (int row = blockIdx.x; row < n; row += gridDim.x) {
+    const int id = min(max(ids[row], 0), vocab - 1);  // out-of-range ids are clamped
+    const T* er = E + (size_t)id * d;
+    for (int i = threadIdx.x; i < d; i += blockDim.x) x[(size_t)row * ldx + i] = TT<T>::ld(er + i) * scale;
+  }
+}
+
+hipError_t launch_embed(int dtype, const void* E, int d, int vocab, const int32_t* ids, int n,
+                        float scale, float* x, int ldx, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  const int grid = std::min(n, 1024);
+  if (dtype == DT_BF16)
+    k_embed<uint16_t><<<grid, 256, 0, st>>>((const uint16_t*)E, d, vocab, ids, n, scale, x, ldx);
+  else
+    k_embed<float><<<grid, 256, 0, st>>>((const float*)E, d, vocab, ids, n, scale, x, ldx);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ void k_cvt_pad(const float* __restrict__ src, int rows, int cols, T* __restrict__ dst,
+                          int ld, float* __restrict__ dst32) {
+  const long long total = (long long)rows * ld;
+  for (long long idx = blockIdx.x * (long long)blockDim.x + threadIdx.x; idx < total;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const int c = (int)(idx % ld);
+    const long long r = idx / ld;
+    const float v = c < cols ? src[r * cols + c] : 0.f;
+    TT<T>::st(dst + idx, v);
+    if (dst32 && c < cols) dst32[r * cols + c] = v;
+  }
+}
+
+hipError_t launch_cvt_pad(int dtype, const float* src, int rows, int cols, void* dst, int ld_dst,
+                          float* dst_f32, hipStream_t st) {
+  const long long total = (long long)rows * ld_dst;
+  const int grid = (int)std::min<long long>((total + 255) / 256, 1024);
+  if (dtype == DT_BF16)
+    k_cvt_pad<uint16_t><<<grid, 256, 0, st>>>(src, rows, cols, (uint16_t*)dst, ld_dst, dst_f32);
+  else
+    k_cvt_pad<float><<<grid, 256, 0, st>>>(src, rows, cols, (float*)dst, ld_dst, dst_f32);
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ void k_bcast_row(const T* __restrict__ row, int cols, T* __restrict__ dst, int ld,
+                            int rows) {
+  const long long total = (long long)rows * cols;
+  for (long long idx = blockIdx.x * (long long)blockDim.x + threadIdx.x; idx < total;
+       idx += (long long)gridDim.x * blockDim.x) {
+    const int c = (int)(idx % cols);
+    const long long r = idx / cols;
+    dst[r * ld + c] = row[c];
+  }
+}
+
+hipError_t launch_bcast_row(int dtype, const void* row, int cols, void* dst, int ld_dst, int rows,
+                            hipStream_t st) {
+  const long long total = (long long)rows * cols;
+  const int grid = (int)std::min<long long>((total + 255) / 256, 1024);
+  if (dtype == DT_BF16)
+    k_bcast_row<uint16_t><<<grid, 256, 0, st>>>((const uint16_t*)row, cols, (uint16_t*)dst, ld_dst, rows);
+  else
+    k_bcast_row<float><<<grid, 256, 0, st>>>((const float*)row, cols, (float*)dst, ld_dst, rows);
+  return hipGetLastError();
+}
+
+}  // namespace vla

@@ -1,0 +1,1109 @@
+// Host runtime and C ABI of the two-phase VLA library (see include/vla.h).
+//
+// Phase 1 (VLM prefill) and phase 2 (flow-matching action denoising) are
+// sequences of kernel launches on a caller-given stream. The pipeline runs
+// frame r's action phase on one stream while frame r+1's prefill runs on a
+// second one (the cross-frame pipelining of Section 2.1), with two model-owned
+// contexts so the prefill of frame r+1 never overwrites the cache frame r is
+// still reading.
+#include <hip/hip_ext.h>
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <chrono>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <memory>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/vla.h"
+#include "gen.h"
+#include "kernels.h"
+
+using namespace vla;
+
+// ---------------------------------------------------------------------------
+// Errors
+// ---------------------------------------------------------------------------
+
+static thread_local std::string g_err;
+
+static int fail(int code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+#define HIP_TRY(expr)                                                                   \
+  do {                                                                                  \
+    hipError_t e_ = (expr);                                                             \
+    if (e_ != hipSuccess)                                                               \
+      return fail(VLA_EHIP, std::string(#expr) + ": " + hipGetErrorString(e_));         \
+  } while (0)
+
+#define VLA_TRY(expr)            \
+  do {                           \
+    int r_ = (expr);             \
+    if (r_ != VLA_OK) return r_; \
+  } while (0)
+
+static inline int rnd_up(int x, int m) { return (x + m - 1) / m * m; }
+
+// ---------------------------------------------------------------------------
+// Configuration
+// ---------------------------------------------------------------------------
+
+struct Dims {
+  int gh, gw, tview, nimg, prefix, kp, kp_pad, a_pad, s_pad, rows_v, kvd, qd, qkv_n, vhd;
+};
+
+static Dims derive(const vla_config& c) {
+  Dims d{};
+  d.gh = c.img_h / c.patch;
+  d.gw = c.img_w / c.patch;
+  d.tview = d.gh * d.gw;
+  d.nimg = c.n_views * d.tview;
+  d.prefix = d.nimg + c.n_text + (c.state_dim > 0 ? 1 : 0);
+  d.kp = 3 * c.patch * c.patch;
+  d.kp_pad = rnd_up(d.kp, 8);
+  d.a_pad = rnd_up(c.action_dim, 8);
+  d.s_pad = rnd_up(std::max(c.state_dim, 1), 8);
+  d.rows_v = d.nimg;
+  d.kvd = c.lm_kv_heads * c.head_dim;
+  d.qd = c.lm_heads * c.head_dim;
+  d.qkv_n = d.qd + 2 * d.kvd;
+  d.vhd = c.vit_dim / c.vit_heads;
+  return d;
+}
+
+static int validate(const vla_config* c) {
+  if (!c) return fail(VLA_EINVAL, "config is NULL");
+  auto bad = [](const char* what) { return fail(VLA_EINVAL, std::string("invalid config: ") + what); };
+  if (c->dtype != VLA_F32 && c->dtype != VLA_BF16) return bad("dtype");
+  const int pos[] = {c->n_views, c->img_h, c->img_w, c->patch, c->vit_dim, c->vit_heads, c->vit_mlp,
+                     c->vit_layers, c->lm_dim, c->lm_heads, c->lm_kv_heads, c->head_dim, c->lm_mlp,
+                     c->lm_layers, c->vocab, c->ex_dim, c->ex_mlp, c->ex_layers, c->chunk_len,
+                     c->action_dim, c->n_steps};
+  for (int v : pos)
+    if (v <= 0) return bad("every size except n_text and state_dim must be positive");
+  if (c->n_text < 0 || c->state_dim < 0) return bad("n_text / state_dim negative");
+  if (c->img_h % c->patch || c->img_w % c->patch) return bad("patch must divide the image");
+  if (c->vit_dim % c->vit_heads) return bad("vit_heads must divide vit_dim");
+  const int vhd = c->vit_dim / c->vit_heads;
+  if (vhd % 8 || vhd > 256) return bad("ViT head dim must be a multiple of 8 and <= 256");
+  if (c->lm_heads % c->lm_kv_heads) return bad("lm_heads % lm_kv_heads != 0");
+  if (c->head_dim % 32 || c->head_dim > 256) return bad("head_dim must be a multiple of 32, <= 256");
+  if (c->ex_layers != c->lm_layers) return bad("ex_layers must equal lm_layers (layer-wise KV sharing)");
+  if (c->lm_mlp % 16 || c->ex_mlp % 16) return bad("lm_mlp / ex_mlp must be multiples of 16");
+  if (c->vit_dim % 8 || c->lm_dim % 8 || c->ex_dim % 8 || c->vit_mlp % 8)
+    return bad("model widths must be multiples of 8");
+  if (c->ex_dim % 2) return bad("ex_dim must be even (sinusoid halves)");
+  return VLA_OK;
+}
+
+static bool preset(const char* name, vla_config* o) {
+  if (!name || !o) return false;
+  const std::string n(name);
+  if (n == "tiny") {
+    *o = vla_config{VLA_F32, 1, 128, 128, 16, 256, 4, 1024, 2, 256, 4, 1, 64, 1024, 2,
+                    1024, 16, 0, 128, 512, 2, 8, 7, 4};
+    return true;
+  }
+  if (n == "pi0" || n == "pi0_3view") {
+    *o = vla_config{VLA_BF16, 1, 224, 224, 14, 1152, 16, 4304, 27, 2048, 8, 1, 256, 16384, 18,
+                    1024, 48, 32, 1024, 4096, 18, 50, 32, 10};
+    if (n == "pi0_3view") {
+      o->n_views = 3;
+      o->n_text = 64;
+    }
+    return true;
+  }
+  return false;
+}
+
+// ---------------------------------------------------------------------------
+// Parameters: logical tensors (names and [out, in] shapes of the inventory)
+// placed into device tensors with a row map.
+// ---------------------------------------------------------------------------
+
+enum RowMap { MAP_IDENT = 0, MAP_ROPE, MAP_GATE, MAP_UP };
+
+struct DevTensor {
+  size_t offset = 0;  // into the weight arena
+  int rows = 0, ld = 0, dt = DT_F32;
+  bool vec = false;  // fp32 vector: params sit at column offsets (row_off) of one row
+  size_t bytes() const { return (size_t)rows * ld * (dt == DT_BF16 ? 2 : 4); }
+};
+
+struct ParamRec {
+  std::string name;
+  int rows, cols;
+  double mean, stdv;
+  int tensor;  // index into model tensors
+  int map, row_off, hd;
+};
+
+static int dev_row(const ParamRec& p, int r) {
+  switch (p.map) {
+    case MAP_ROPE: {
+      const int head = r / p.hd, i = r % p.hd, half = p.hd / 2;
+      const int ph = i < half ? 32 * (i / 16) + i % 16 : 32 * ((i - half) / 16) + 16 + (i - half) % 16;
+      return p.row_off + head * p.hd + ph;
+    }
+    case MAP_GATE: return p.row_off + 32 * (r / 16) + r % 16;
+    case MAP_UP: return p.row_off + 32 * (r / 16) + 16 + r % 16;
+    default: return p.row_off + r;
+  }
+}
+
+struct VitLayer {
+  int ln1_g, ln1_b, qkv_w, qkv_b, o_w, o_b, ln2_g, ln2_b, fc1_w, fc1_b, fc2_w, fc2_b;
+};
+struct DecLayer {
+  int rms1, qkv, o, rms2, gu, down;  // tensor ids (-1 when absent)
+};
+
+struct Streams {
+  hipStream_t v = nullptr, a = nullptr;
+};
+
+struct vla_ctx {
+  vla_model* m = nullptr;
+  void* K = nullptr;  // [L][P][kvd]
+  void* V = nullptr;
+};
+
+struct vla_model {
+  vla_config c{};
+  Dims d{};
+  int dt = DT_F32;
+  size_t esz = 4;
+  int device = 0, num_cus = 0;
+  uint64_t seed = 0;
+
+  void* arena = nullptr;
+  size_t arena_bytes = 0;
+  std::vector<DevTensor> T;
+  std::vector<ParamRec> P;
+  std::map<std::string, int> pidx;
+
+  // tensor ids
+  int patch_w, patch_b, pos, post_g, post_b, proj_w, proj_b, embed, state_w = -1, state_b = -1;
+  std::vector<VitLayer> vit;
+  std::vector<DecLayer> lm, ex;
+  int in_w, in_b, t1_w, t1_b, t2_w, t2_b, fin_g, out_w, out_b;
+
+  // constant tables
+  float* rope_cos = nullptr;
+  float* rope_sin = nullptr;
+  void* phi = nullptr;  // [n_steps][ex_dim] operand type
+  float* ck = nullptr;  // [n_steps][ex_dim]: W_2 phi(t_k) + b_2
+
+  // phase scratch
+  struct VlmWs {
+    float *xv, *xl;
+    void *h, *qkv, *att, *mlp, *sbuf;
+    Scratch scr;
+  } vw{};
+  struct ActWs {
+    float* u;
+    void *xop, *a, *hid, *h, *q, *kown, *vown, *att, *mlp;
+    Scratch scr;
+  } aw{};
+  std::vector<void*> allocs;
+
+  // pipeline
+  vla_ctx* pctx[2] = {nullptr, nullptr};
+  std::map<std::pair<int, int>, Streams> mask_streams;
+  Streams plain{};
+  std::vector<hipEvent_t> ev;
+  std::mutex mu;
+
+  char* tptr(int t) const { return (char*)arena + T[t].offset; }
+  float* f32(int t) const { return (float*)tptr(t); }
+};
+
+static size_t dsz(int dt) { return dt == DT_BF16 ? 2 : 4; }
+
+static int add_tensor(vla_model* m, int rows, int ld, int dt, bool vec = false) {
+  DevTensor t;
+  t.rows = rows;
+  t.ld = ld;
+  t.dt = dt;
+  t.vec = vec;
+  m->T.push_back(t);
+  return (int)m->T.size() - 1;
+}
+
+static void add_param(vla_model* m, const std::string& name, int rows, int cols, double mean,
+                      int tensor, int map = MAP_IDENT, int row_off = 0, int hd = 0) {
+  ParamRec p{name, rows, cols, mean, 0.02, tensor, map, row_off, hd};
+  m->pidx[name] = (int)m->P.size();
+  m->P.push_back(p);
+}
+
+// Weight matrix [rows, cols] of the operand type, K padded to 8.
+static int add_mat(vla_model* m, const std::string& name, int rows, int cols) {
+  const int t = add_tensor(m, rows, rnd_up(cols, 8), m->dt);
+  add_param(m, name, rows, cols, 0.0, t);
+  return t;
+}
+// fp32 vector (biases, norm gains: mean 1).
+static int add_vec(vla_model* m, const std::string& name, int n, double mean = 0.0) {
+  const int t = add_tensor(m, 1, n, DT_F32, true);
+  add_param(m, name, 1, n, mean, t);
+  return t;
+}
+
+static void build_inventory(vla_model* m) {
+  const vla_config& c = m->c;
+  const Dims& d = m->d;
+  m->patch_w = add_mat(m, "vit.patch.w", c.vit_dim, d.kp);
+  m->patch_b = add_vec(m, "vit.patch.b", c.vit_dim);
+  m->pos = add_tensor(m, d.tview, c.vit_dim, DT_F32);
+  add_param(m, "vit.pos", d.tview, c.vit_dim, 0.0, m->pos);
+  for (int l = 0; l < c.vit_layers; ++l) {
+    const std::string p = "vit." + std::to_string(l) + ".";
+    VitLayer L{};
+    L.ln1_g = add_vec(m, p + "ln1.g", c.vit_dim, 1.0);
+    L.ln1_b = add_vec(m, p + "ln1.b", c.vit_dim);
+    L.qkv_w = add_tensor(m, 3 * c.vit_dim, c.vit_dim, m->dt);
+    L.qkv_b = add_tensor(m, 1, 3 * c.vit_dim, DT_F32, true);
+    const char* qkv[3] = {"q", "k", "v"};
+    for (int i = 0; i < 3; ++i) {
+      add_param(m, p + qkv[i] + ".w", c.vit_dim, c.vit_dim, 0.0, L.qkv_w, MAP_IDENT, i * c.vit_dim);
+      // biases live in one fp32 row; row_off counts columns for vectors
+      add_param(m, p + qkv[i] + ".b", 1, c.vit_dim, 0.0, L.qkv_b, MAP_IDENT, i * c.vit_dim);
+    }
+    L.o_w = add_mat(m, p + "o.w", c.vit_dim, c.vit_dim);
+    L.o_b = add_vec(m, p + "o.b", c.vit_dim);
+    L.ln2_g = add_vec(m, p + "ln2.g", c.vit_dim, 1.0);
+    L.ln2_b = add_vec(m, p + "ln2.b", c.vit_dim);
+    L.fc1_w = add_mat(m, p + "fc1.w", c.vit_mlp, c.vit_dim);
+    L.fc1_b = add_vec(m, p + "fc1.b", c.vit_mlp);
+    L.fc2_w = add_mat(m, p + "fc2.w", c.vit_dim, c.vit_mlp);
+    L.fc2_b = add_vec(m, p + "fc2.b", c.vit_dim);
+    m->vit.push_back(L);
+  }
+  m->post_g = add_vec(m, "vit.post.g", c.vit_dim, 1.0);
+  m->post_b = add_vec(m, "vit.post.b", c.vit_dim);
+  m->proj_w = add_mat(m, "proj.w", c.lm_dim, c.vit_dim);
+  m->proj_b = add_vec(m, "proj.b", c.lm_dim);
+  m->embed = add_mat(m, "lm.embed", c.vocab, c.lm_dim);
+  if (c.state_dim > 0) {
+    m->state_w = add_mat(m, "state.w", c.lm_dim, c.state_dim);
+    m->state_b = add_vec(m, "state.b", c.lm_dim);
+  }
+  auto dec = [&](const std::string& pre, int layers, int dim, int mlp, bool lm, std::vector<DecLayer>& out) {
+    for (int l = 0; l < layers; ++l) {
+      const std::string p = pre + std::to_string(l) + ".";
+      DecLayer L{-1, -1, -1, -1, -1, -1};
+      L.rms1 = add_vec(m, p + "rms1.g", dim, 1.0);
+      L.qkv = add_tensor(m, d.qkv_n, dim, m->dt);
+      add_param(m, p + "q.w", d.qd, dim, 0.0, L.qkv, MAP_ROPE, 0, c.head_dim);
+      add_param(m, p + "k.w", d.kvd, dim, 0.0, L.qkv, MAP_ROPE, d.qd, c.head_dim);
+      add_param(m, p + "v.w", d.kvd, dim, 0.0, L.qkv, MAP_IDENT, d.qd + d.kvd);
+      if (lm && l == layers - 1) {  // the last LM layer only feeds the cache
+        out.push_back(L);
+        break;
+      }
+      L.o = add_mat(m, p + "o.w", dim, d.qd);
+      L.rms2 = add_vec(m, p + "rms2.g", dim, 1.0);
+      L.gu = add_tensor(m, 2 * mlp, dim, m->dt);
+      add_param(m, p + "gate.w", mlp, dim, 0.0, L.gu, MAP_GATE);
+      add_param(m, p + "up.w", mlp, dim, 0.0, L.gu, MAP_UP);
+      L.down = add_mat(m, p + "down.w", dim, mlp);
+      out.push_back(L);
+    }
+  };
+  dec("lm.", c.lm_layers, c.lm_dim, c.lm_mlp, true, m->lm);
+  m->in_w = add_mat(m, "ex.in.w", c.ex_dim, c.action_dim);
+  m->in_b = add_vec(m, "ex.in.b", c.ex_dim);
+  m->t1_w = add_mat(m, "ex.time1.w", c.ex_dim, 2 * c.ex_dim);
+  m->t1_b = add_vec(m, "ex.time1.b", c.ex_dim);
+  m->t2_w = add_mat(m, "ex.time2.w", c.ex_dim, c.ex_dim);
+  m->t2_b = add_vec(m, "ex.time2.b", c.ex_dim);
+  dec("ex.", c.ex_layers, c.ex_dim, c.ex_mlp, false, m->ex);
+  m->fin_g = add_vec(m, "ex.final.g", c.ex_dim, 1.0);
+  m->out_w = add_mat(m, "ex.out.w", c.action_dim, c.ex_dim);
+  m->out_b = add_vec(m, "ex.out.b", c.action_dim);
+}
+
+// Generate every parameter of one device tensor into a host image and upload.
+static int upload_tensor(vla_model* m, int t, const std::vector<int>& params) {
+  const DevTensor& dt = m->T[t];
+  std::vector<uint8_t> img(dt.bytes(), 0);
+  std::vector<float> vals;
+  for (int pi : params) {
+    const ParamRec& p = m->P[pi];
+    const size_t n = (size_t)p.rows * p.cols;
+    vals.resize(n);
+    gen_normal(m->seed, p.name.c_str(), n, p.mean, p.stdv, vals.data());
+    const bool vec = dt.vec;
+    for (int r = 0; r < p.rows; ++r) {
+      const size_t base = vec ? (size_t)p.row_off : (size_t)dev_row(p, r) * dt.ld;
+      for (int col = 0; col < p.cols; ++col) {
+        float v = vals[(size_t)r * p.cols + col];
+        if (m->dt == DT_BF16) v = bf16_value(bf16_bits(v));  // the model stores bf16 values
+        if (dt.dt == DT_BF16)
+          ((uint16_t*)img.data())[base + col] = bf16_bits(v);
+        else
+          ((float*)img.data())[base + col] = v;
+      }
+    }
+  }
+  HIP_TRY(hipMemcpy(m->tptr(t), img.data(), img.size(), hipMemcpyHostToDevice));
+  return VLA_OK;
+}
+
+static int dmalloc(vla_model* m, void** p, size_t bytes) {
+  bytes = std::max<size_t>(bytes, 256);
+  hipError_t e = hipMalloc(p, bytes);
+  if (e != hipSuccess) return fail(VLA_ENOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
+  m->allocs.push_back(*p);
+  return VLA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Phase bodies
+// ---------------------------------------------------------------------------
+
+struct Run {
+  vla_model* m;
+  hipStream_t st;
+  LaunchCaps caps;
+  const Scratch* scr;
+};
+
+static int gemm(const Run& r, const void* A, int lda, int W, int M, int N, int K, const Epi& e,
+                const void* Wptr = nullptr, int ldw = 0) {
+  vla_model* m = r.m;
+  GemmDesc g{m->dt, A, lda, Wptr ? Wptr : m->tptr(W), Wptr ? ldw : m->T[W].ld, M, N, K, e};
+  hipError_t err = launch_gemm(g, *r.scr, r.caps, r.st);
+  if (err != hipSuccess)
+    return fail(VLA_EHIP, std::string("gemm ") + std::to_string(M) + "x" + std::to_string(N) + "x" +
+                              std::to_string(K) + ": " + hipGetErrorString(err));
+  return VLA_OK;
+}
+
+static int attn(const Run& r, const AttnDesc& a) {
+  hipError_t err = launch_attention(a, *r.scr, r.caps, r.st);
+  if (err != hipSuccess) return fail(VLA_EHIP, std::string("attention: ") + hipGetErrorString(err));
+  return VLA_OK;
+}
+
+static int norm(const Run& r, const float* x, int ldx, int rows, int d, int g, int b, bool rms,
+                void* out, int ldo) {
+  vla_model* m = r.m;
+  hipError_t err = launch_norm(m->dt, x, ldx, rows, d, m->f32(g), b >= 0 ? m->f32(b) : nullptr, rms,
+                               out, ldo, r.st);
+  if (err != hipSuccess) return fail(VLA_EHIP, std::string("norm: ") + hipGetErrorString(err));
+  return VLA_OK;
+}
+
+static Epi epi_kind(int kind, void* out = nullptr, int ldo = 0, const float* bias = nullptr) {
+  Epi e;
+  e.kind = kind;
+  e.out = out;
+  e.ldo = ldo;
+  e.bias = bias;
+  return e;
+}
+static Epi epi_resid(float* x, int ld, const float* bias = nullptr) {
+  Epi e;
+  e.kind = EPI_RESID;
+  e.resid = x;
+  e.ldr = ld;
+  e.bias = bias;
+  return e;
+}
+
+// One Gemma-style decoder layer: RMSNorm -> QKV (+RoPE, K/V stored) ->
+// attention over [past; own] -> O + residual -> RMSNorm -> GeGLU -> down + residual.
+static int decoder_layer(const Run& r, const DecLayer& L, float* x, int rows, int dim, int mlp,
+                         void* h, void* q, void* kout, void* vout, int pos0, const void* kpast,
+                         const void* vpast, int npast, void* att, void* mlpbuf, bool kv_only) {
+  vla_model* m = r.m;
+  const vla_config& c = m->c;
+  const Dims& d = m->d;
+  VLA_TRY(norm(r, x, dim, rows, dim, L.rms1, -1, true, h, dim));
+  Epi e;
+  e.kind = EPI_QKV_ROPE;
+  e.q = q;
+  e.ldq = d.qd;
+  e.k = kout;
+  e.v = vout;
+  e.ldkv = d.kvd;
+  e.nq = c.lm_heads;
+  e.nkv = c.lm_kv_heads;
+  e.hd = c.head_dim;
+  e.pos0 = pos0;
+  e.rope_cos = m->rope_cos;
+  e.rope_sin = m->rope_sin;
+  VLA_TRY(gemm(r, h, dim, L.qkv, rows, d.qkv_n, dim, e));
+  if (kv_only) return VLA_OK;
+  AttnDesc a{};
+  a.dtype = m->dt;
+  a.q = q;
+  a.ldq = d.qd;
+  if (kpast) {
+    a.k0 = kpast;
+    a.v0 = vpast;
+    a.S0 = npast;
+    a.k1 = kout;
+    a.v1 = vout;
+    a.S1 = rows;
+  } else {
+    a.k0 = kout;
+    a.v0 = vout;
+    a.S0 = rows;
+  }
+  a.ldkv = d.kvd;
+  a.out = att;
+  a.ldo = d.qd;
+  a.Sq = rows;
+  a.nq = c.lm_heads;
+  a.nkv = c.lm_kv_heads;
+  a.hd = c.head_dim;
+  a.segs = 1;
+  VLA_TRY(attn(r, a));
+  VLA_TRY(gemm(r, att, d.qd, L.o, rows, dim, d.qd, epi_resid(x, dim)));
+  VLA_TRY(norm(r, x, dim, rows, dim, L.rms2, -1, true, h, dim));
+  VLA_TRY(gemm(r, h, dim, L.gu, rows, 2 * mlp, dim, epi_kind(EPI_GEGLU, mlpbuf, mlp)));
+  VLA_TRY(gemm(r, mlpbuf, mlp, L.down, rows, dim, mlp, epi_resid(x, dim)));
+  return VLA_OK;
+}
+
+static int run_prefill(const Run& r, const vla_frame* f, vla_ctx* ctx) {
+  vla_model* m = r.m;
+  const vla_config& c = m->c;
+  const Dims& d = m->d;
+  auto& w = m->vw;
+  const int dv = c.vit_dim, dl = c.lm_dim, rows = d.rows_v;
+  // ViT: patch embedding + bias + position
+  HIP_TRY(launch_patchify(m->dt, f->pixels, c.n_views, c.img_h, c.img_w, c.patch, w.h, d.kp_pad, r.st));
+  {
+    Epi e = epi_kind(EPI_F32, w.xv, dv, m->f32(m->patch_b));
+    e.rowadd = m->f32(m->pos);
+    e.rowadd_period = d.tview;
+    e.ldra = dv;
+    VLA_TRY(gemm(r, w.h, d.kp_pad, m->patch_w, rows, dv, d.kp_pad, e));
+  }
+  for (int l = 0; l < c.vit_layers; ++l) {
+    const VitLayer& L = m->vit[l];
+    VLA_TRY(norm(r, w.xv, dv, rows, dv, L.ln1_g, L.ln1_b, false, w.h, dv));
+    VLA_TRY(gemm(r, w.h, dv, L.qkv_w, rows, 3 * dv, dv, epi_kind(EPI_T, w.qkv, 3 * dv, m->f32(L.qkv_b))));
+    AttnDesc a{};
+    a.dtype = m->dt;
+    a.q = w.qkv;
+    a.ldq = 3 * dv;
+    a.k0 = (char*)w.qkv + dv * m->esz;
+    a.v0 = (char*)w.qkv + 2 * dv * m->esz;
+    a.S0 = d.tview;
+    a.ldkv = 3 * dv;
+    a.out = w.att;
+    a.ldo = dv;
+    a.Sq = d.tview;
+    a.nq = a.nkv = c.vit_heads;
+    a.hd = d.vhd;
+    a.segs = c.n_views;
+    a.seg_q = a.seg_kv = (long long)d.tview * 3 * dv;
+    a.seg_o = (long long)d.tview * dv;
+    VLA_TRY(attn(r, a));
+    VLA_TRY(gemm(r, w.att, dv, L.o_w, rows, dv, dv, epi_resid(w.xv, dv, m->f32(L.o_b))));
+    VLA_TRY(norm(r, w.xv, dv, rows, dv, L.ln2_g, L.ln2_b, false, w.h, dv));
+    VLA_TRY(gemm(r, w.h, dv, L.fc1_w, rows, c.vit_mlp, dv, epi_kind(EPI_GELU, w.mlp, c.vit_mlp, m->f32(L.fc1_b))));
+    VLA_TRY(gemm(r, w.mlp, c.vit_mlp, L.fc2_w, rows, dv, c.vit_mlp, epi_resid(w.xv, dv, m->f32(L.fc2_b))));
+  }
+  VLA_TRY(norm(r, w.xv, dv, rows, dv, m->post_g, m->post_b, false, w.h, dv));
+  // prefix: [projected image tokens; text * sqrt(d); state projection]
+  VLA_TRY(gemm(r, w.h, dv, m->proj_w, rows, dl, dv, epi_kind(EPI_F32, w.xl, dl, m->f32(m->proj_b))));
+  HIP_TRY(launch_embed(m->dt, m->tptr(m->embed), dl, c.vocab, f->text_ids, c.n_text, std::sqrt((float)dl),
+                       w.xl + (size_t)d.nimg * dl, dl, r.st));
+  if (c.state_dim > 0) {
+    HIP_TRY(launch_cvt_pad(m->dt, f->state, 1, c.state_dim, w.sbuf, d.s_pad, nullptr, r.st));
+    VLA_TRY(gemm(r, w.sbuf, d.s_pad, m->state_w, 1, dl, d.s_pad,
+                 epi_kind(EPI_F32, w.xl + (size_t)(d.prefix - 1) * dl, dl, m->f32(m->state_b))));
+  }
+  // LM prefill writing the cache
+  const size_t layer_kv = (size_t)d.prefix * d.kvd * m->esz;
+  for (int l = 0; l < c.lm_layers; ++l) {
+    void* K = (char*)ctx->K + l * layer_kv;
+    void* V = (char*)ctx->V + l * layer_kv;
+    VLA_TRY(decoder_layer(r, m->lm[l], w.xl, d.prefix, dl, c.lm_mlp, w.h, w.qkv, K, V, 0, nullptr,
+                          nullptr, 0, w.att, w.mlp, l == c.lm_layers - 1));
+  }
+  return VLA_OK;
+}
+
+static int run_denoise(const Run& r, const vla_ctx* ctx, const float* noise, float* x) {
+  vla_model* m = r.m;
+  const vla_config& c = m->c;
+  const Dims& d = m->d;
+  auto& w = m->aw;
+  const int H = c.chunk_len, de = c.ex_dim, A = c.action_dim;
+  const float dt = -1.0f / (float)c.n_steps;
+  HIP_TRY(launch_cvt_pad(m->dt, noise, H, A, w.xop, d.a_pad, x, r.st));
+  const size_t layer_kv = (size_t)d.prefix * d.kvd * m->esz;
+  for (int k = 0; k < c.n_steps; ++k) {
+    // action embedding and time conditioning
+    VLA_TRY(gemm(r, w.xop, d.a_pad, m->in_w, H, de, d.a_pad, epi_kind(EPI_T, w.a, de, m->f32(m->in_b))));
+    VLA_TRY(gemm(r, w.a, de, m->t1_w, H, de, de, epi_kind(EPI_SWISH, w.hid, de, m->ck + (size_t)k * de)));
+    VLA_TRY(gemm(r, w.hid, de, m->t2_w, H, de, de, epi_kind(EPI_F32, w.u, de, m->f32(m->t2_b))));
+    for (int l = 0; l < c.ex_layers; ++l) {
+      const void* K = (const char*)ctx->K + l * layer_kv;
+      const void* V = (const char*)ctx->V + l * layer_kv;
+      VLA_TRY(decoder_layer(r, m->ex[l], w.u, H, de, c.ex_mlp, w.h, w.q, w.kown, w.vown, d.prefix,
+                            K, V, d.prefix, w.att, w.mlp, false));
+    }
+    VLA_TRY(norm(r, w.u, de, H, de, m->fin_g, -1, true, w.h, de));
+    Epi e;
+    e.kind = EPI_EULER;
+    e.bias = m->f32(m->out_b);
+    e.x = x;
+    e.ldx = A;
+    e.xop = w.xop;
+    e.ldxop = d.a_pad;
+    e.dt = dt;
+    VLA_TRY(gemm(r, w.h, de, m->out_w, H, A, de, e));
+  }
+  return VLA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Creation
+// ---------------------------------------------------------------------------
+
+static size_t gemm_scratch(int dt, int M, int N, int K) {
+  GemmDesc g{dt, nullptr, K, nullptr, K, M, N, K, Epi()};
+  return plan_gemm(g).scratch_floats;
+}
+
+static size_t attn_scratch(int dt, int Sq, int nq, int nkv, int hd, int S0, int S1, int segs) {
+  AttnDesc a{};
+  a.dtype = dt;
+  a.Sq = Sq;
+  a.nq = nq;
+  a.nkv = nkv;
+  a.hd = hd;
+  a.S0 = S0;
+  a.S1 = S1;
+  a.segs = segs;
+  return attn_scratch_floats(a);
+}
+
+static int setup_tables(vla_model* m) {
+  const vla_config& c = m->c;
+  const Dims& d = m->d;
+  const int npos = d.prefix + c.chunk_len, half = c.head_dim / 2;
+  std::vector<float> cs((size_t)npos * half), sn((size_t)npos * half);
+  for (int p = 0; p < npos; ++p)
+    for (int i = 0; i < half; ++i) {
+      const double inv = std::pow(10000.0, -2.0 * i / c.head_dim);
+      const double ang = p * inv;
+      cs[(size_t)p * half + i] = (float)std::cos(ang);
+      sn[(size_t)p * half + i] = (float)std::sin(ang);
+    }
+  VLA_TRY(dmalloc(m, (void**)&m->rope_cos, cs.size() * 4));
+  VLA_TRY(dmalloc(m, (void**)&m->rope_sin, sn.size() * 4));
+  HIP_TRY(hipMemcpy(m->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(hipMemcpy(m->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice));
+  // sinusoid phi(t_k): periods log-spaced on [4e-3, 4]; t_k = (N - k) / N in fp32
+  const int de = c.ex_dim, dh = de / 2;
+  std::vector<float> phi((size_t)c.n_steps * de);
+  for (int k = 0; k < c.n_steps; ++k) {
+    const float t = (float)(c.n_steps - k) / (float)c.n_steps;
+    for (int i = 0; i < dh; ++i) {
+      const double frac = dh > 1 ? (double)i / (dh - 1) : 0.0;
+      const double period = 4e-3 * std::pow(4.0 / 4e-3, frac);
+      const double x = 2.0 * M_PI * (double)t / period;
+      phi[(size_t)k * de + i] = (float)std::sin(x);
+      phi[(size_t)k * de + dh + i] = (float)std::cos(x);
+    }
+  }
+  VLA_TRY(dmalloc(m, &m->phi, phi.size() * m->esz));
+  if (m->dt == DT_BF16) {
+    std::vector<uint16_t> hb(phi.size());
+    for (size_t i = 0; i < phi.size(); ++i) hb[i] = bf16_bits(phi[i]);
+    HIP_TRY(hipMemcpy(m->phi, hb.data(), hb.size() * 2, hipMemcpyHostToDevice));
+  } else {
+    HIP_TRY(hipMemcpy(m->phi, phi.data(), phi.size() * 4, hipMemcpyHostToDevice));
+  }
+  VLA_TRY(dmalloc(m, (void**)&m->ck, (size_t)c.n_steps * de * 4));
+  return VLA_OK;
+}
+
+static int setup_workspaces(vla_model* m) {
+  const vla_config& c = m->c;
+  const Dims& d = m->d;
+  const int dt = m->dt;
+  const size_t e = m->esz;
+  const int rv = d.rows_v, P = d.prefix, H = c.chunk_len;
+  const int dv = c.vit_dim, dl = c.lm_dim, de = c.ex_dim;
+  auto& v = m->vw;
+  const int rmax = std::max(rv, P);
+  VLA_TRY(dmalloc(m, (void**)&v.xv, (size_t)rv * dv * 4));
+  VLA_TRY(dmalloc(m, (void**)&v.xl, (size_t)P * dl * 4));
+  VLA_TRY(dmalloc(m, &v.h, (size_t)rmax * std::max({d.kp_pad, dv, dl}) * e));
+  VLA_TRY(dmalloc(m, &v.qkv, (size_t)std::max((size_t)rv * 3 * dv, (size_t)P * d.qd) * e));
+  VLA_TRY(dmalloc(m, &v.att, (size_t)std::max((size_t)rv * dv, (size_t)P * d.qd) * e));
+  VLA_TRY(dmalloc(m, &v.mlp, (size_t)std::max((size_t)rv * c.vit_mlp, (size_t)P * c.lm_mlp) * e));
+  VLA_TRY(dmalloc(m, &v.sbuf, (size_t)d.s_pad * e));
+  size_t sv = 0;
+  auto upd = [](size_t& s, size_t x) { s = std::max(s, x); };
+  upd(sv, gemm_scratch(dt, rv, dv, d.kp_pad));
+  upd(sv, gemm_scratch(dt, rv, 3 * dv, dv));
+  upd(sv, gemm_scratch(dt, rv, dv, dv));
+  upd(sv, gemm_scratch(dt, rv, c.vit_mlp, dv));
+  upd(sv, gemm_scratch(dt, rv, dv, c.vit_mlp));
+  upd(sv, gemm_scratch(dt, rv, dl, dv));
+  upd(sv, gemm_scratch(dt, 1, dl, d.s_pad));
+  upd(sv, gemm_scratch(dt, P, d.qkv_n, dl));
+  upd(sv, gemm_scratch(dt, P, dl, d.qd));
+  upd(sv, gemm_scratch(dt, P, 2 * c.lm_mlp, dl));
+  upd(sv, gemm_scratch(dt, P, dl, c.lm_mlp));
+  upd(sv, attn_scratch(dt, d.tview, c.vit_heads, c.vit_heads, d.vhd, d.tview, 0, c.n_views));
+  upd(sv, attn_scratch(dt, P, c.lm_heads, c.lm_kv_heads, c.head_dim, P, 0, 1));
+  VLA_TRY(dmalloc(m, (void**)&v.scr.ptr, std::max<size_t>(sv, 64) * 4));
+  v.scr.floats = std::max<size_t>(sv, 64);
+
+  auto& a = m->aw;
+  VLA_TRY(dmalloc(m, (void**)&a.u, (size_t)H * de * 4));
+  VLA_TRY(dmalloc(m, &a.xop, (size_t)H * d.a_pad * e));
+  VLA_TRY(dmalloc(m, &a.a, (size_t)H * de * e));
+  VLA_TRY(dmalloc(m, &a.hid, (size_t)H * de * e));
+  VLA_TRY(dmalloc(m, &a.h, (size_t)H * de * e));
+  VLA_TRY(dmalloc(m, &a.q, (size_t)H * d.qd * e));
+  VLA_TRY(dmalloc(m, &a.kown, (size_t)H * d.kvd * e));
+  VLA_TRY(dmalloc(m, &a.vown, (size_t)H * d.kvd * e));
+  VLA_TRY(dmalloc(m, &a.att, (size_t)H * d.qd * e));
+  VLA_TRY(dmalloc(m, &a.mlp, (size_t)H * c.ex_mlp * e));
+  size_t sa = 0;
+  upd(sa, gemm_scratch(dt, H, de, d.a_pad));
+  upd(sa, gemm_scratch(dt, H, de, de));
+  upd(sa, gemm_scratch(dt, c.n_steps, de, de));
+  upd(sa, gemm_scratch(dt, H, d.qkv_n, de));
+  upd(sa, gemm_scratch(dt, H, de, d.qd));
+  upd(sa, gemm_scratch(dt, H, 2 * c.ex_mlp, de));
+  upd(sa, gemm_scratch(dt, H, de, c.ex_mlp));
+  upd(sa, gemm_scratch(dt, H, c.action_dim, de));
+  upd(sa, attn_scratch(dt, H, c.lm_heads, c.lm_kv_heads, c.head_dim, P, H, 1));
+  VLA_TRY(dmalloc(m, (void**)&a.scr.ptr, std::max<size_t>(sa, 64) * 4));
+  a.scr.floats = std::max<size_t>(sa, 64);
+  return VLA_OK;
+}
+
+static int create_impl(const vla_config* cfg, uint64_t seed, vla_model** out) {
+  VLA_TRY(validate(cfg));
+  std::unique_ptr<vla_model> m(new vla_model());
+  m->c = *cfg;
+  m->d = derive(*cfg);
+  m->dt = cfg->dtype == VLA_BF16 ? DT_BF16 : DT_F32;
+  m->esz = dsz(m->dt);
+  m->seed = seed;
+  HIP_TRY(hipGetDevice(&m->device));
+  hipDeviceProp_t prop;
+  HIP_TRY(hipGetDeviceProperties(&prop, m->device));
+  m->num_cus = prop.multiProcessorCount;
+  build_inventory(m.get());
+  size_t off = 0;
+  for (auto& t : m->T) {
+    t.offset = off;
+    off += (t.bytes() + 255) / 256 * 256;
+  }
+  m->arena_bytes = off;
+  hipError_t e = hipMalloc(&m->arena, off);
+  if (e != hipSuccess) return fail(VLA_ENOMEM, std::string("weights: hipMalloc: ") + hipGetErrorString(e));
+  std::vector<std::vector<int>> by_tensor(m->T.size());
+  for (size_t i = 0; i < m->P.size(); ++i) by_tensor[m->P[i].tensor].push_back((int)i);
+  for (size_t t = 0; t < m->T.size(); ++t) {
+    int rc = upload_tensor(m.get(), (int)t, by_tensor[t]);
+    if (rc != VLA_OK) {
+      hipFree(m->arena);
+      return rc;
+    }
+  }
+  int rc = setup_tables(m.get());
+  if (rc == VLA_OK) rc = setup_workspaces(m.get());
+  if (rc == VLA_OK) {
+    // c_k = W_2[:, d_e:] phi(t_k) + b_2 for every step (depends on the step only)
+    Run r{m.get(), nullptr, LaunchCaps{}, &m->aw.scr};
+    const int de = m->c.ex_dim;
+    rc = gemm(r, m->phi, de, -1, m->c.n_steps, de, de, epi_kind(EPI_F32, m->ck, de, m->f32(m->t1_b)),
+              m->tptr(m->t1_w) + (size_t)de * m->esz, m->T[m->t1_w].ld);
+  }
+  if (rc == VLA_OK) {
+    hipError_t se = hipDeviceSynchronize();
+    if (se != hipSuccess) rc = fail(VLA_EHIP, std::string("create: ") + hipGetErrorString(se));
+  }
+  if (rc != VLA_OK) {
+    for (void* p : m->allocs) hipFree(p);
+    hipFree(m->arena);
+    return rc;
+  }
+  *out = m.release();
+  return VLA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Pipeline
+// ---------------------------------------------------------------------------
+
+static int ctx_create_impl(vla_model* m, vla_ctx** out) {
+  std::unique_ptr<vla_ctx> c(new vla_ctx());
+  c->m = m;
+  const size_t bytes = (size_t)m->c.lm_layers * m->d.prefix * m->d.kvd * m->esz;
+  hipError_t e = hipMalloc(&c->K, bytes);
+  if (e != hipSuccess) return fail(VLA_ENOMEM, "ctx K: hipMalloc failed");
+  e = hipMalloc(&c->V, bytes);
+  if (e != hipSuccess) {
+    hipFree(c->K);
+    return fail(VLA_ENOMEM, "ctx V: hipMalloc failed");
+  }
+  *out = c.release();
+  return VLA_OK;
+}
+
+static void cu_mask(int first, int count, int total, std::vector<uint32_t>& mask) {
+  mask.assign((total + 31) / 32, 0u);
+  for (int i = first; i < first + count && i < total; ++i) mask[i / 32] |= 1u << (i % 32);
+}
+
+static int get_streams(vla_model* m, const vla_sched& s, Streams* out) {
+  if (s.mode == VLA_MODE_CU_MASKED) {
+    auto key = std::make_pair(s.vlm_cus, s.act_cus);
+    auto it = m->mask_streams.find(key);
+    if (it == m->mask_streams.end()) {
+      // Bits are spread over the XCDs by the driver (bit i -> XCD i % 8), so
+      // contiguous ranges whose sizes are multiples of 8 give every XCD CUs
+      // of both phases.
+      Streams st;
+      std::vector<uint32_t> mv, ma;
+      cu_mask(0, s.vlm_cus, m->num_cus, mv);
+      cu_mask(s.vlm_cus, s.act_cus, m->num_cus, ma);
+      HIP_TRY(hipExtStreamCreateWithCUMask(&st.v, (uint32_t)mv.size(), mv.data()));
+      HIP_TRY(hipExtStreamCreateWithCUMask(&st.a, (uint32_t)ma.size(), ma.data()));
+      it = m->mask_streams.emplace(key, st).first;
+    }
+    *out = it->second;
+    return VLA_OK;
+  }
+  if (!m->plain.v) {
+    HIP_TRY(hipStreamCreateWithFlags(&m->plain.v, hipStreamNonBlocking));
+    HIP_TRY(hipStreamCreateWithFlags(&m->plain.a, hipStreamNonBlocking));
+  }
+  *out = m->plain;
+  return VLA_OK;
+}
+
+static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noise, int R,
+                         const vla_sched* sched, float* actions, vla_timing* t) {
+  if (!frames || !noise || !actions || !sched) return fail(VLA_EINVAL, "NULL argument");
+  if (R < 1) return fail(VLA_EINVAL, "R must be >= 1");
+  const vla_sched& s = *sched;
+  if (s.mode < VLA_MODE_SERIAL || s.mode > VLA_MODE_WG_CAPPED) return fail(VLA_EINVAL, "unknown mode");
+  if (s.mode == VLA_MODE_CU_MASKED) {
+    if (s.vlm_cus <= 0 || s.act_cus <= 0 || s.vlm_cus % 8 || s.act_cus % 8 ||
+        s.vlm_cus + s.act_cus > m->num_cus)
+      return fail(VLA_EINVAL, "CU split: both counts positive multiples of 8, sum <= CU count (" +
+                                  std::to_string(m->num_cus) + ")");
+  }
+  if (s.mode == VLA_MODE_WG_CAPPED && s.vlm_wg_cap < 1) return fail(VLA_EINVAL, "vlm_wg_cap must be >= 1");
+  std::lock_guard<std::mutex> lock(m->mu);
+  for (int i = 0; i < 2; ++i)
+    if (!m->pctx[i]) VLA_TRY(ctx_create_impl(m, &m->pctx[i]));
+  Streams st;
+  VLA_TRY(get_streams(m, s, &st));
+  if (s.mode == VLA_MODE_SERIAL) st.a = st.v;
+  const size_t need = (size_t)4 * R;
+  while (m->ev.size() < need) {
+    hipEvent_t e;
+    HIP_TRY(hipEventCreate(&e));
+    m->ev.push_back(e);
+  }
+  // events: [4r] VLM start, [4r+1] VLM end, [4r+2] action start, [4r+3] action end
+  LaunchCaps vcaps{}, acaps{};
+  if (s.mode == VLA_MODE_WG_CAPPED) vcaps.max_wgs = s.vlm_wg_cap * m->num_cus;
+  const size_t chunk = (size_t)m->c.chunk_len * m->c.action_dim;
+  HIP_TRY(hipDeviceSynchronize());
+  const auto t0 = std::chrono::steady_clock::now();
+  for (int r = 0; r < R; ++r) {
+    vla_ctx* ctx = m->pctx[r % 2];
+    if (r >= 2 && st.v != st.a) HIP_TRY(hipStreamWaitEvent(st.v, m->ev[4 * (r - 2) + 3], 0));
+    HIP_TRY(hipEventRecord(m->ev[4 * r], st.v));
+    Run rv{m, st.v, vcaps, &m->vw.scr};
+    VLA_TRY(run_prefill(rv, &frames[r], ctx));
+    HIP_TRY(hipEventRecord(m->ev[4 * r + 1], st.v));
+    if (st.v != st.a) HIP_TRY(hipStreamWaitEvent(st.a, m->ev[4 * r + 1], 0));
+    HIP_TRY(hipEventRecord(m->ev[4 * r + 2], st.a));
+    Run ra{m, st.a, acaps, &m->aw.scr};
+    VLA_TRY(run_denoise(ra, ctx, noise + r * chunk, actions + r * chunk));
+    HIP_TRY(hipEventRecord(m->ev[4 * r + 3], st.a));
+  }
+  HIP_TRY(hipStreamSynchronize(st.v));
+  HIP_TRY(hipStreamSynchronize(st.a));
+  const auto t1 = std::chrono::steady_clock::now();
+  if (t) {
+    t->wall_ms = std::chrono::duration<double, std::milli>(t1 - t0).count();
+    t->frames_per_s = R / (t->wall_ms * 1e-3);
+    t->actions_per_s = t->frames_per_s * m->c.chunk_len;
+    t->vlm_ms = t->act_ms = 0;
+    for (int r = 0; r < R; ++r) {
+      float a = 0, b = 0;
+      HIP_TRY(hipEventElapsedTime(&a, m->ev[4 * r], m->ev[4 * r + 1]));
+      HIP_TRY(hipEventElapsedTime(&b, m->ev[4 * r + 2], m->ev[4 * r + 3]));
+      t->vlm_ms += a;
+      t->act_ms += b;
+    }
+  }
+  return VLA_OK;
+}
+
+// ---------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------
+
+#define ABI_GUARD(...)                                            \
+  try {                                                           \
+    g_err.clear();                                                \
+    __VA_ARGS__                                                   \
+  } catch (const std::exception& ex) {                            \
+    return fail(VLA_ENOMEM, std::string("exception: ") + ex.what()); \
+  } catch (...) {                                                 \
+    return fail(VLA_EINVAL, "unknown exception");                 \
+  }
+
+extern "C" {
+
+const char* vla_last_error(void) { return g_err.c_str(); }
+
+int vla_preset(const char* name, vla_config* out) {
+  ABI_GUARD({
+    if (!preset(name, out)) return fail(VLA_EINVAL, std::string("unknown preset ") + (name ? name : "(null)"));
+    return VLA_OK;
+  })
+}
+
+int vla_validate(const vla_config* cfg) { ABI_GUARD({ return validate(cfg); }) }
+
+int vla_create(const vla_config* cfg, uint64_t seed, vla_model** out) {
+  ABI_GUARD({
+    if (!out) return fail(VLA_EINVAL, "out is NULL");
+    *out = nullptr;
+    return create_impl(cfg, seed, out);
+  })
+}
+
+int vla_destroy(vla_model* m) {
+  ABI_GUARD({
+    if (!m) return VLA_OK;
+    hipDeviceSynchronize();
+    for (int i = 0; i < 2; ++i)
+      if (m->pctx[i]) {
+        hipFree(m->pctx[i]->K);
+        hipFree(m->pctx[i]->V);
+        delete m->pctx[i];
+      }
+    for (auto& kv : m->mask_streams) {
+      hipStreamDestroy(kv.second.v);
+      hipStreamDestroy(kv.second.a);
+    }
+    if (m->plain.v) {
+      hipStreamDestroy(m->plain.v);
+      hipStreamDestroy(m->plain.a);
+    }
+    for (auto e : m->ev) hipEventDestroy(e);
+    for (void* p : m->allocs) hipFree(p);
+    hipFree(m->arena);
+    delete m;
+    return VLA_OK;
+  })
+}
+
+int vla_ctx_create(vla_model* m, vla_ctx** out) {
+  ABI_GUARD({
+    if (!m || !out) return fail(VLA_EINVAL, "NULL argument");
+    *out = nullptr;
+    return ctx_create_impl(m, out);
+  })
+}
+
+int vla_ctx_destroy(vla_ctx* c) {
+  ABI_GUARD({
+    if (!c) return VLA_OK;
+    hipFree(c->K);
+    hipFree(c->V);
+    delete c;
+    return VLA_OK;
+  })
+}
+
+int vla_vlm_prefill(vla_model* m, const vla_frame* in, vla_ctx* ctx, void* stream) {
+  ABI_GUARD({
+    if (!m || !in || !ctx || !in->pixels || (!in->text_ids && m->c.n_text > 0))
+      return fail(VLA_EINVAL, "NULL argument");
+    if (m->c.state_dim > 0 && !in->state) return fail(VLA_EINVAL, "state is NULL but state_dim > 0");
+    if (ctx->m != m) return fail(VLA_ESTATE, "context belongs to another model");
+    Run r{m, (hipStream_t)stream, LaunchCaps{}, &m->vw.scr};
+    return run_prefill(r, in, ctx);
+  })
+}
+
+int vla_action_denoise(vla_model* m, const vla_ctx* ctx, const float* noise, float* actions, void* stream) {
+  ABI_GUARD({
+    if (!m || !ctx || !noise || !actions) return fail(VLA_EINVAL, "NULL argument");
+    if (ctx->m != m) return fail(VLA_ESTATE, "context belongs to another model");
+    Run r{m, (hipStream_t)stream, LaunchCaps{}, &m->aw.scr};
+    return run_denoise(r, ctx, noise, actions);
+  })
+}
+
+int vla_pipeline_run(vla_model* m, const vla_frame* frames, const float* noise, int32_t R,
+                     const vla_sched* sched, float* actions, vla_timing* t) {
+  ABI_GUARD({
+    if (!m) return fail(VLA_EINVAL, "model is NULL");
+    return pipeline_impl(m, frames, noise, R, sched, actions, t);
+  })
+}
+
+int vla_param_count(const vla_model* m, int32_t* count) {
+  ABI_GUARD({
+    if (!m || !count) return fail(VLA_EINVAL, "NULL argument");
+    *count = (int32_t)m->P.size();
+    return VLA_OK;
+  })
+}
+
+int vla_param_info(const vla_model* m, int32_t i, const char** name, int64_t* numel) {
+  ABI_GUARD({
+    if (!m || !name || !numel) return fail(VLA_EINVAL, "NULL argument");
+    if (i < 0 || i >= (int32_t)m->P.size()) return fail(VLA_EINVAL, "index out of range");
+    *name = m->P[i].name.c_str();
+    *numel = (int64_t)m->P[i].rows * m->P[i].cols;
+    return VLA_OK;
+  })
+}
+
+int vla_export_param(vla_model* m, const char* name, float* host_dst, int64_t numel) {
+  ABI_GUARD({
+    if (!m || !name || !host_dst) return fail(VLA_EINVAL, "NULL argument");
+    auto it = m->pidx.find(name);
+    if (it == m->pidx.end()) return fail(VLA_EINVAL, std::string("no parameter ") + name);
+    const ParamRec& p = m->P[it->second];
+    if (numel != (int64_t)p.rows * p.cols) return fail(VLA_EINVAL, "numel mismatch");
+    const DevTensor& t = m->T[p.tensor];
+    std::vector<uint8_t> img(t.bytes());
+    HIP_TRY(hipMemcpy(img.data(), m->tptr(p.tensor), img.size(), hipMemcpyDeviceToHost));
+    const bool vec = t.vec;
+    for (int r = 0; r < p.rows; ++r) {
+      const size_t base = vec ? (size_t)p.row_off : (size_t)dev_row(p, r) * t.ld;
+      for (int col = 0; col < p.cols; ++col)
+        host_dst[(size_t)r * p.cols + col] = t.dt == DT_BF16 ? bf16_value(((uint16_t*)img.data())[base + col])
+                                                             : ((float*)img.data())[base + col];
+    }
+    return VLA_OK;
+  })
+}
+
+int vla_ctx_export_kv(vla_model* m, const vla_ctx* c, int32_t layer, float* host_k, float* host_v) {
+  ABI_GUARD({
+    if (!m || !c || !host_k || !host_v) return fail(VLA_EINVAL, "NULL argument");
+    if (layer < 0 || layer >= m->c.lm_layers) return fail(VLA_EINVAL, "layer out of range");
+    if (c->m != m) return fail(VLA_ESTATE, "context belongs to another model");
+    const size_t n = (size_t)m->d.prefix * m->d.kvd;
+    std::vector<uint8_t> img(n * m->esz);
+    for (int w = 0; w < 2; ++w) {
+      const char* src = (const char*)(w ? c->V : c->K) + layer * n * m->esz;
+      HIP_TRY(hipMemcpy(img.data(), src, img.size(), hipMemcpyDeviceToHost));
+      float* dst = w ? host_v : host_k;
+      for (size_t i = 0; i < n; ++i)
+        dst[i] = m->dt == DT_BF16 ? bf16_value(((uint16_t*)img.data())[i]) : ((float*)img.data())[i];
+    }
+    return VLA_OK;
+  })
+}
+
+int vla_debug_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* A, int32_t lda,
+                   const void* W, int32_t ldw, const float* bias, float* C, void* stream) {
+  ABI_GUARD({
+    if (dtype != VLA_F32 && dtype != VLA_BF16) return fail(VLA_EINVAL, "dtype");
+    if (M <= 0 || N <= 0 || K <= 0 || K % 8 || lda < K || ldw < K || lda % 8 || ldw % 8)
+      return fail(VLA_EINVAL, "shape: M, N, K > 0, K, lda, ldw multiples of 8, lda, ldw >= K");
+    if (!A || !W || !C) return fail(VLA_EINVAL, "NULL argument");
+    GemmDesc g{dtype == VLA_BF16 ? DT_BF16 : DT_F32, A, lda, W, ldw, M, N, K, Epi()};
+    g.epi.kind = EPI_F32;
+    g.epi.out = C;
+    g.epi.ldo = N;
+    g.epi.bias = bias;
+    const GemmPlan p = plan_gemm(g);
+    Scratch s;
+    if (p.scratch_floats) {
+      HIP_TRY(hipMalloc(&s.ptr, p.scratch_floats * 4));
+      s.floats = p.scratch_floats;
+    }
+    hipError_t e = launch_gemm(g, s, LaunchCaps{}, (hipStream_t)stream);
+    if (s.ptr) {
+      hipStreamSynchronize((hipStream_t)stream);
+      hipFree(s.ptr);
+    }
+    if (e != hipSuccess) return fail(VLA_EHIP, std::string("gemm: ") + hipGetErrorString(e));
+    return VLA_OK;
+  })
+}
+
+int vla_debug_attention(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int32_t hd, const void* q,
+                        const void* k0, const void* v0, int32_t S0, const void* k1, const void* v1,
+                        int32_t S1, void* out, void* stream) {
+  ABI_GUARD({
+    if (dtype != VLA_F32 && dtype != VLA_BF16) return fail(VLA_EINVAL, "dtype");
+    if (Sq <= 0 || nq <= 0 || nkv <= 0 || nq % nkv || hd <= 0 || hd % 8 || hd > 256 || S0 <= 0 ||
+        S1 < 0)
+      return fail(VLA_EINVAL, "shape");
+    if (!q || !k0 || !v0 || !out || (S1 > 0 && (!k1 || !v1))) return fail(VLA_EINVAL, "NULL argument");
+    AttnDesc a{};
+    a.dtype = dtype == VLA_BF16 ? DT_BF16 : DT_F32;
+    a.q = q;
+    a.ldq = nq * hd;
+    a.k0 = k0;
+    a.v0 = v0;
+    a.S0 = S0;
+    a.k1 = S1 > 0 ? k1 : nullptr;
+    a.v1 = S1 > 0 ? v1 : nullptr;
+    a.S1 = S1;
+    a.ldkv = nkv * hd;
+    a.out = out;
+    a.ldo = nq * hd;
+    a.Sq = Sq;
+    a.nq = nq;
+    a.nkv = nkv;
+    a.hd = hd;
+    a.segs = 1;
+    const size_t need = attn_scratch_floats(a);
+    Scratch s;
+    if (need) {
+      HIP_TRY(hipMalloc(&s.ptr, need * 4));
+      s.floats = need;
+    }
+    hipError_t e = launch_attention(a, s, LaunchCaps{}, (hipStream_t)stream);
+    if (s.ptr) {
+      hipStreamSynchronize((hipStream_t)stream);
+      hipFree(s.ptr);
+    }
+    if (e != hipSuccess) return fail(VLA_EHIP, std::string("attention: ") + hipGetErrorString(e));
+    return VLA_OK;
+  })
+}
+
+int vla_debug_generate(uint64_t seed, const char* name, int64_t n, double mean, double stdv,
+                       float* host_dst) {
+  ABI_GUARD({
+    if (!name || !host_dst || n < 0) return fail(VLA_EINVAL, "bad argument");
+    gen_normal(seed, name, (size_t)n, mean, stdv, host_dst);
+    return VLA_OK;
+  })
+}
+
+}  // extern "C"

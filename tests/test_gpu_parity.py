@@ -1,0 +1,230 @@
+"""GPU parity of the HIP path against the fp64 oracle, through the C ABI.
+
+Tolerances (max abs error of the action chunk, per the build's target):
+  fp32 configurations  <= 1e-4
+  bf16 configurations  <= 2e-2
+Kernel-level cases use bounds derived from the arithmetic (stated per test).
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import vla_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+CHUNK_TOL = {synth.F32: 1e-4, synth.BF16: 2e-2}
+
+
+@pytest.fixture(scope="module")
+def V():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_22335_amd as V
+    return V
+
+
+def G():
+    import gpu_util
+    return gpu_util
+
+
+RNG = np.random.default_rng(7)
+
+GEMM_SHAPES = [
+    (1, 64, 8), (7, 3, 16), (21, 136, 64), (40, 100, 592), (50, 2560, 1024), (50, 1024, 4096),
+    (64, 64, 64), (33, 128, 256), (256, 3456, 1152), (305, 2048, 2048), (512, 8192, 256),
+    (833, 200, 72),
+]
+
+
+@pytest.mark.parametrize("dtype", [0, 1], ids=["f32", "bf16"])
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+def test_gemm_vs_fp64(V, dtype, M, N, K):
+    g = G()
+    g.say(f"gemm dtype={dtype} M={M} N={N} K={K}")
+    A = RNG.standard_normal((M, K))
+    W = RNG.standard_normal((N, K)) * 0.05
+    b = RNG.standard_normal(N).astype(np.float32)
+    Ad, Wd = g.operand_dev(A, dtype), g.operand_dev(W, dtype)
+    C = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    V.vla_debug_gemm(dtype, M, N, K, Ad, K, Wd, K, g.to_dev(b), C)
+    torch.cuda.synchronize()
+    a, w = g.operand_values(A, dtype), g.operand_values(W, dtype)
+    ref = a @ w.T + b
+    # fp32 accumulation of K exact (bf16) or fp32-rounded products:
+    # |err| <= 2 K u sum|a||w| with u = 2^-24
+    bound = 2 * K * 2.0 ** -24 * (np.abs(a) @ np.abs(w).T + np.abs(b)) + 1e-30
+    err = np.abs(C.cpu().numpy() - ref)
+    assert np.all(err <= bound), float((err / bound).max())
+
+
+ATTN_CASES = [  # dtype, Sq, nq, nkv, hd, S0, S1
+    (1, 50, 8, 1, 256, 305, 50),   # expert joint attention (KV split)
+    (1, 305, 8, 1, 256, 305, 0),   # LM prefill, multi-query
+    (1, 256, 16, 16, 72, 256, 0),  # ViT head dim 72 (padded to 96)
+    (1, 5, 2, 1, 32, 21, 5),
+    (0, 8, 4, 1, 64, 80, 8),
+    (0, 80, 4, 1, 64, 80, 0),
+    (0, 64, 4, 4, 64, 64, 0),
+    (0, 3, 2, 2, 32, 1, 0),        # single key
+    (1, 1, 1, 1, 48, 883, 0),      # one query, long keys
+]
+
+
+@pytest.mark.parametrize("case", ATTN_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_attention_vs_oracle(V, case):
+    g = G()
+    dtype, Sq, nq, nkv, hd, S0, S1 = case
+    g.say(f"attention {case}")
+    q = RNG.standard_normal((Sq, nq, hd))
+    k0, v0 = RNG.standard_normal((S0, nkv, hd)), RNG.standard_normal((S0, nkv, hd))
+    k1, v1 = RNG.standard_normal((max(S1, 1), nkv, hd)), RNG.standard_normal((max(S1, 1), nkv, hd))
+    dv = lambda x: g.operand_dev(x.reshape(x.shape[0], -1), dtype)
+    out = torch.empty((Sq, nq * hd), dtype=torch.bfloat16 if dtype else torch.float32, device="cuda")
+    k1d, v1d = dv(k1), dv(v1)
+    V.vla_debug_attention(dtype, Sq, nq, nkv, hd, dv(q), dv(k0), dv(v0), S0,
+                          k1d if S1 else None, v1d if S1 else None, S1, out)
+    torch.cuda.synchronize()
+    val = lambda x: g.operand_values(x, dtype)
+    kk = np.concatenate([val(k0), val(k1)[:S1]], 0)
+    vv = np.concatenate([val(v0), val(v1)[:S1]], 0)
+    ref = O.attention(val(q), kk, vv).reshape(Sq, -1)
+    got = out.float().cpu().numpy()
+    if dtype:
+        # output stored as bf16 (2^-9 relative) + P carried as two bf16 parts (~2^-16)
+        bound = 2.0 ** -8 * np.abs(ref) + 1e-4
+    else:
+        bound = 2e-5 + 1e-5 * np.abs(ref)
+    err = np.abs(got - ref)
+    assert np.all(err <= bound), float((err / bound).max())
+
+
+@pytest.mark.parametrize("cfg", [synth.micro(synth.F32), synth.micro(synth.BF16), synth.TINY],
+                         ids=["micro-f32", "micro-bf16", "tiny"])
+def test_weights_on_device_equal_seeded_generator(V, cfg):
+    g = G()
+    g.say(f"export params {cfg['dtype']}")
+    want = synth.make_params(cfg, 3)
+    with g.model(cfg, 3) as m:
+        n = V.vla_param_count(m)
+        names = [V.vla_param_info(m, i)[0] for i in range(n)]
+        assert sorted(names) == sorted(want)
+        for name in names:
+            got = V.vla_export_param(m, name, want[name].size).reshape(want[name].shape)
+            assert np.array_equal(got, want[name]), name
+
+
+PHASE_CFGS = [
+    ("micro-f32", synth.micro(synth.F32)),
+    ("micro-bf16", synth.micro(synth.BF16)),
+    ("micro-f32-2view", dict(synth.micro(synth.F32), n_views=2, vit_layers=2, lm_layers=2, ex_layers=2)),
+    ("tiny", synth.TINY),
+    ("tiny-bf16", dict(synth.TINY, dtype=synth.BF16)),
+]
+
+
+def _kv_tol(cfg, ref):
+    if cfg["dtype"] == synth.F32:
+        return 1e-4
+    # both sides store K/V in bf16; fp32-vs-fp64 differences before the
+    # rounding flip an element by one bf16 ulp (2^-7 relative at most) and
+    # such flips propagate through later layers at the same order
+    return 2.0 ** -5 * np.abs(ref) + 2e-3
+
+
+@pytest.mark.parametrize("name,cfg", PHASE_CFGS, ids=[p[0] for p in PHASE_CFGS])
+def test_phases_vs_oracle(V, name, cfg):
+    g = G()
+    g.say(f"phases {name}")
+    P = synth.make_params(cfg, 0)
+    fr = synth.make_frame(cfg, 0, 0)
+    cap = {}
+    want = O.forward(P, cfg, fr, cap)
+    with g.model(cfg, 0) as m:
+        got, kv = g.run_frame(m, cfg, fr)
+        got2, _ = g.run_frame(m, cfg, fr)
+    assert np.array_equal(got, got2), "not deterministic"
+    nkvd = cfg["lm_kv_heads"] * cfg["head_dim"]
+    for l, (k, v) in enumerate(kv):
+        rk = cap["kv"][l][0].reshape(-1, nkvd).ravel()
+        rv = cap["kv"][l][1].reshape(-1, nkvd).ravel()
+        assert np.all(np.abs(k - rk) <= _kv_tol(cfg, rk)), (l, float(np.abs(k - rk).max()))
+        assert np.all(np.abs(v - rv) <= _kv_tol(cfg, rv)), (l, float(np.abs(v - rv).max()))
+    err = float(np.abs(got - want).max())
+    print(f"[gpu] {name}: chunk max abs err {err:.3e}", flush=True)
+    assert err <= CHUNK_TOL[cfg["dtype"]]
+
+
+@pytest.mark.timeout(900)
+def test_pi0_full_size_vs_oracle(V):
+    """The PaliGemma-3B-shaped VLM + pi0-shaped expert at its real sizes,
+    frame 0 of seed 0, against the oracle (fp64, bf16 storage points)."""
+    g = G()
+    cfg = synth.PI0
+    g.say("pi0 full size: GPU")
+    fr = synth.make_frame(cfg, 0, 0)
+    with g.model(cfg, 0) as m:
+        got, kv = g.run_frame(m, cfg, fr)
+    g.say("pi0 full size: oracle")
+    P = synth.make_params(cfg, 0)
+    cap = {}
+    want = O.forward(P, cfg, fr, cap)
+    nkvd = cfg["lm_kv_heads"] * cfg["head_dim"]
+    for l in (0, cfg["lm_layers"] - 1):
+        rk = cap["kv"][l][0].reshape(-1, nkvd).ravel()
+        assert np.all(np.abs(kv[l][0] - rk) <= _kv_tol(cfg, rk)), l
+    err = float(np.abs(got - want).max())
+    print(f"[gpu] pi0 chunk max abs err {err:.3e}", flush=True)
+    assert err <= CHUNK_TOL[synth.BF16]
+
+
+@pytest.mark.parametrize("cfg", [synth.micro(synth.BF16), synth.TINY], ids=["micro-bf16", "tiny"])
+def test_pipeline_modes_bit_identical(V, cfg):
+    g = G()
+    R = 5
+    g.say(f"pipeline modes dtype={cfg['dtype']} R={R}")
+    frames = [synth.make_frame(cfg, 11, r) for r in range(R)]
+    dfs = [g.DevFrame(f) for f in frames]
+    noise = torch.stack([d.noise for d in dfs]).contiguous()
+    results = {}
+    with g.model(cfg, 11) as m:
+        ncu = torch.cuda.get_device_properties(0).multi_processor_count
+        modes = [("serial", {}), ("concurrent", {}), ("cu_masked", dict(vlm_cus=(ncu // 2) // 8 * 8, act_cus=16)),
+                 ("wg_capped", dict(vlm_wg_cap=1))]
+        for mode, kw in modes:
+            out = torch.full_like(noise, float("nan"))
+            t = V.vla_pipeline_run(m, [d.c for d in dfs], noise, R, mode=mode, actions=out, **kw)
+            assert t["frames_per_s"] > 0
+            results[mode] = out.cpu().numpy()
+        standalone = [g.run_frame(m, cfg, f)[0] for f in frames]
+    for mode, r in results.items():
+        assert np.array_equal(r, results["serial"]), mode
+    for i in range(R):
+        assert np.array_equal(results["serial"][i].astype(np.float64), standalone[i])
+    # and the pipeline is the oracle's function of each frame
+    P = synth.make_params(cfg, 11)
+    for i in (0, R - 1):
+        want = O.forward(P, cfg, frames[i])
+        assert np.abs(results["serial"][i] - want).max() <= CHUNK_TOL[cfg["dtype"]]
+
+
+def test_abi_errors_on_device(V):
+    g = G()
+    cfg = synth.micro()
+    with g.model(cfg) as m:
+        with pytest.raises(V.VlaError) as e:
+            V.vla_pipeline_run(m, [], torch.zeros(1, device="cuda"), 0, actions=torch.zeros(1, device="cuda"))
+        assert e.value.code == -1
+        with pytest.raises(V.VlaError):
+            V.vla_pipeline_run(m, [V.make_frame(1, 1, 1)], torch.zeros(1, device="cuda"), 1,
+                               mode="cu_masked", vlm_cus=4, act_cus=8, actions=torch.zeros(1, device="cuda"))
+        with pytest.raises(V.VlaError):
+            V.vla_export_param(m, "nope", 3)
+        with g.model(cfg) as m2, g.context(m2) as c2:
+            with pytest.raises(V.VlaError) as e:
+                V.vla_action_denoise(m, c2, torch.zeros(15, device="cuda"), torch.zeros(15, device="cuda"))
+            assert e.value.code == -5
