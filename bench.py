@@ -1,0 +1,205 @@
+#!/usr/bin/env python
+"""Benchmark of the two-phase VLA hot path on one MI355X.
+
+Workload: the PaliGemma-3B-shaped VLM (27-layer ViT, d=1152, 256 patches of
+a 224x224 image; 18-layer LM, d=2048, 8 query heads / 1 KV head of 256,
+GeGLU 16384, prefix 256 image + 48 text + 1 state token) with a pi0-shaped
+flow-matching expert (18 layers, d=1024, GeGLU 4096, chunk 50x32, 10 Euler
+steps), bf16, R=8 independent robot request streams (a new seeded frame per
+stream). One step = vla_pipeline_run over the R frames: the VLM prefill of
+frame r+1 overlaps the action denoising of frame r. Inputs are resident in
+HBM before the timed region.
+
+Prints one JSON line: frames/s of the default schedule as `value`,
+actions/s, every schedule's throughput and its speedup over the serialized
+one, the dominant kernel's roofline fraction (timed live with HIP events on
+its own stream) and the fp64 CPU oracle timed on this host as a baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "VLA frames/sec & actions/sec at R robot streams; MFMA util; speedup vs serialized"
+HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, GB/s
+BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
+
+
+def kernel_work(cfg, tag):
+    """Algorithmic bytes and flops of one launch of a tagged kernel: weights,
+    the A operand and the output (plus the fp32 residual read and write for
+    residual epilogues) each moved once; flops = 2 M N K."""
+    import synth
+    d = synth.derived(cfg)
+    H, P = cfg["chunk_len"], d["prefix"]
+    qd, kvd = cfg["lm_heads"] * cfg["head_dim"], cfg["lm_kv_heads"] * cfg["head_dim"]
+    shapes = {  # tag: (M, N, K, output bytes per element, residual?)
+        "ex.gateup": (H, 2 * cfg["ex_mlp"], cfg["ex_dim"], 2, False),
+        "ex.down": (H, cfg["ex_dim"], cfg["ex_mlp"], 4, True),
+        "ex.qkv": (H, qd + 2 * kvd, cfg["ex_dim"], 2, False),
+        "ex.o": (H, cfg["ex_dim"], qd, 4, True),
+        "lm.gateup": (P, 2 * cfg["lm_mlp"], cfg["lm_dim"], 2, False),
+        "lm.down": (P, cfg["lm_dim"], cfg["lm_mlp"], 4, True),
+        "lm.qkv": (P, qd + 2 * kvd, cfg["lm_dim"], 2, False),
+        "lm.o": (P, cfg["lm_dim"], qd, 4, True),
+        "vit.fc1": (d["n_img"], cfg["vit_mlp"], cfg["vit_dim"], 2, False),
+        "vit.fc2": (d["n_img"], cfg["vit_dim"], cfg["vit_mlp"], 4, True),
+    }
+    M, N, K, ob, resid = shapes[tag]
+    nout = N // 2 if tag.endswith("gateup") else N
+    byts = 2 * N * K + 2 * M * K + (8 if resid else ob) * M * nout
+    return byts, 2.0 * M * N * K
+
+
+def cpu_baseline(cfg, seed):
+    """The fp64 oracle on one frame of the same workload (full VLM prefill
+    and the 10-step denoising of that frame); frames/s = 1 / its time."""
+    import numpy as np
+    import synth
+    from oracle import vla_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    except Exception:  # threadpoolctl missing: report the host CPU count
+        threads = os.cpu_count() or 1
+    print("[bench] cpu baseline: generating oracle parameters", file=sys.stderr, flush=True)
+    P = synth.make_params(cfg, seed)
+    fr = synth.make_frame(cfg, seed, 0)
+    print("[bench] cpu baseline: timing oracle forward of frame 0", file=sys.stderr, flush=True)
+    t0 = time.perf_counter()
+    chunk = O.forward(P, cfg, fr)
+    dt = time.perf_counter() - t0
+    del P
+    return {"value": 1.0 / dt, "unit": "frames/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"frame 0 of the workload: full VLM prefill + {cfg['n_steps']}-step action "
+                      f"denoising, fp64 NumPy, {dt:.1f} s", "seconds": dt}, chunk
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--R", type=int, default=8, help="robot request streams (frames per step)")
+    ap.add_argument("--mode", default="concurrent", help="schedule reported as `value`")
+    ap.add_argument("--modes", default="serial,concurrent,cu_masked,wg_capped")
+    ap.add_argument("--split", default="192,64", help="CU split VLM,action for cu_masked")
+    ap.add_argument("--wg-cap", type=int, default=2, help="VLM workgroups per CU for wg_capped")
+    ap.add_argument("--kernel", default="ex.gateup", help="tag of the kernel timed for the roofline")
+    ap.add_argument("--preset", default="pi0")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; the R robot streams of a "
+                                   "multi-GPU deployment shard across GPUs with no exchange step "
+                                   "(see DESIGN.md); run with --gpus 1"}), flush=True)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2609_22335_amd as V
+    import synth
+
+    torch.cuda.set_device(0)
+    cfg = V.vla_preset(args.preset)
+    seed, R = 0, args.R
+    modes = [m for m in args.modes.split(",") if m]
+    if args.mode not in modes:
+        modes.append(args.mode)
+    vlm_cus, act_cus = (int(x) for x in args.split.split(","))
+
+    print(f"[bench] creating {args.preset} model (seed {seed})", file=sys.stderr, flush=True)
+    m = V.vla_create(cfg, seed)
+    frames_np = [synth.make_frame(cfg, seed, r) for r in range(R)]
+    dev = []
+    for f in frames_np:
+        pix = torch.from_numpy(f["pixels"]).cuda()
+        ids = torch.from_numpy(f["ids"]).cuda()
+        st = torch.from_numpy(f["state"]).cuda() if f["state"].size else None
+        dev.append((pix, ids, st))
+    cframes = [V.make_frame(p, i, s) for p, i, s in dev]
+    noise = torch.from_numpy(np.stack([f["noise"] for f in frames_np])).cuda().contiguous()
+    actions = torch.empty_like(noise)
+    kw = {"serial": {}, "concurrent": {}, "cu_masked": dict(vlm_cus=vlm_cus, act_cus=act_cus),
+          "wg_capped": dict(vlm_wg_cap=args.wg_cap)}
+
+    results, outputs = {}, {}
+    for mode in modes:
+        print(f"[bench] mode {mode}: {args.warmup} warmup + {args.steps} timed steps of R={R}",
+              file=sys.stderr, flush=True)
+        for _ in range(args.warmup):
+            V.vla_pipeline_run(m, cframes, noise, R, mode=mode, actions=actions, **kw[mode])
+        torch.cuda.synchronize()
+        lib_ms = []
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            t = V.vla_pipeline_run(m, cframes, noise, R, mode=mode, actions=actions, **kw[mode])
+            lib_ms.append(t["wall_ms"])
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        fps = args.steps * R / el
+        results[mode] = {"frames_per_s": fps, "actions_per_s": fps * cfg["chunk_len"],
+                         "ms_per_step": 1e3 * el / args.steps,
+                         "median_step_ms": float(np.median(lib_ms)), "min_step_ms": float(np.min(lib_ms)),
+                         "vlm_ms_per_frame": t["vlm_ms"] / R, "action_ms_per_frame": t["act_ms"] / R}
+        outputs[mode] = actions.cpu().numpy().copy()
+    ser = results.get("serial", {}).get("frames_per_s")
+    for mode in results:
+        results[mode]["speedup_vs_serialized"] = (results[mode]["frames_per_s"] / ser) if ser else None
+    identical = all(np.array_equal(outputs[m0], outputs[modes[0]]) for m0 in outputs)
+
+    # dominant kernel, timed live with HIP events on its stream (serial schedule)
+    print(f"[bench] kernel timer on {args.kernel}", file=sys.stderr, flush=True)
+    V.vla_kernel_timer(m, args.kernel)
+    for _ in range(args.steps):
+        V.vla_pipeline_run(m, cframes, noise, R, mode="serial", actions=actions)
+    tot_ms, launches = V.vla_kernel_timer_read(m)
+    V.vla_kernel_timer(m, None)
+    avg_s = tot_ms * 1e-3 / max(launches, 1)
+    byts, flops = kernel_work(cfg, args.kernel)
+    hbm_bound = flops / byts < BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+    if hbm_bound:
+        ach, peak, unit = byts / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
+    else:
+        ach, peak, unit = flops / avg_s / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"
+    roofline = {"bound": "hbm" if hbm_bound else "mfma", "achieved": ach, "peak": peak, "unit": unit,
+                "frac": ach / peak, "traffic": None, "kernel": args.kernel,
+                "avg_us": avg_s * 1e6, "launches": launches,
+                "algorithmic_bytes": byts, "flops": flops}
+    outs = outputs[args.mode]
+    V.vla_destroy(m)
+
+    main_r = results[args.mode]
+    line = {
+        "metric": METRIC, "value": main_r["frames_per_s"], "unit": "frames/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": main_r["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{args.preset}-shaped VLA (PaliGemma-3B-shaped VLM + pi0-shaped "
+                               f"expert), R={R} robot request streams, schedule {args.mode}",
+                   "R": R, "global_batch": R, "chunk": [cfg["chunk_len"], cfg["action_dim"]],
+                   "euler_steps": cfg["n_steps"], "prefix_tokens": synth.derived(cfg)["prefix"],
+                   "parallelism": "1 GPU, 2 streams"},
+        "actions_per_s": main_r["actions_per_s"],
+        "speedup_vs_serialized": main_r["speedup_vs_serialized"],
+        "modes": results, "outputs_identical_across_modes": identical,
+        "roofline": roofline,
+    }
+    if not args.no_cpu_baseline:
+        cb, chunk = cpu_baseline(cfg, seed)
+        cb["max_abs_err_gpu_vs_oracle_frame0"] = float(np.abs(outs[0].astype(np.float64) - chunk).max())
+        line["cpu_baseline"] = cb
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -174,6 +174,17 @@ int vla_debug_attention(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int3
                         const void* q, const void* k0, const void* v0, int32_t S0, const void* k1,
                         const void* v1, int32_t S1, void* out, void* stream);
 
+/* Kernel timer for measurement: while `tag` is set, every launch of the
+ * kernels behind that call site (tags: "vit.patch", "vit.qkv", "vit.attn",
+ * "vit.o", "vit.fc1", "vit.fc2", "proj", "state", "lm.qkv", "lm.attn", "lm.o",
+ * "lm.gateup", "lm.down", "ex.in", "ex.time1", "ex.time2", "ex.qkv",
+ * "ex.attn", "ex.o", "ex.gateup", "ex.down", "ex.out") is bracketed by HIP
+ * events recorded on the stream that launches it. NULL or "" turns it off.
+ * _read waits for the recorded events, returns the summed duration (ms) and
+ * the number of bracketed launches since the last read, and resets both. */
+int vla_kernel_timer(vla_model* m, const char* tag);
+int vla_kernel_timer_read(vla_model* m, double* total_ms, int64_t* launches);
+
 /* Host-only: values start .. start+n-1 of the library's parameter generator
  * for (seed, name) with the given mean and std, as fp32 (before any bf16
  * rounding) into host_dst. Needs no GPU. */

@@ -82,6 +82,8 @@ def _load():
         "vla_debug_gemm": [I32, I32, I32, I32, P, I32, P, I32, P, P, P],
         "vla_debug_attention": [I32, I32, I32, I32, I32, P, P, P, I32, P, P, I32, P, P],
         "vla_debug_generate": [U64, ctypes.c_char_p, I64, D, D, P],
+        "vla_kernel_timer": [P, ctypes.c_char_p],
+        "vla_kernel_timer_read": [P, ctypes.POINTER(D), ctypes.POINTER(I64)],
     }
     for name, args in sig.items():
         fn = getattr(lib, name)
@@ -207,6 +209,17 @@ def vla_debug_attention(dtype: int, Sq: int, nq: int, nkv: int, hd: int, q, k0, 
                                     _ptr(k1), _ptr(v1), S1, _ptr(out), stream or None))
 
 
+def vla_kernel_timer(model: int, tag: Optional[str]) -> None:
+    _check(_lib.vla_kernel_timer(model, tag.encode() if tag else None))
+
+
+def vla_kernel_timer_read(model: int) -> Tuple[float, int]:
+    ms = ctypes.c_double()
+    n = ctypes.c_int64()
+    _check(_lib.vla_kernel_timer_read(model, ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
+
+
 def vla_debug_generate(seed: int, name: str, n: int, mean: float, std: float) -> np.ndarray:
     out = np.empty(n, dtype=np.float32)
     _check(_lib.vla_debug_generate(ctypes.c_uint64(seed), name.encode(), n, mean, std, out.ctypes.data))
@@ -218,4 +231,5 @@ def exported_symbols() -> Iterable[str]:
     return ["vla_preset", "vla_validate", "vla_create", "vla_destroy", "vla_ctx_create",
             "vla_ctx_destroy", "vla_vlm_prefill", "vla_action_denoise", "vla_pipeline_run",
             "vla_param_count", "vla_param_info", "vla_export_param", "vla_ctx_export_kv",
-            "vla_debug_gemm", "vla_debug_attention", "vla_debug_generate", "vla_last_error"]
+            "vla_debug_gemm", "vla_debug_attention", "vla_debug_generate", "vla_kernel_timer",
+            "vla_kernel_timer_read", "vla_last_error"]

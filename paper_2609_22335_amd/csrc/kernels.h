@@ -20,6 +20,8 @@ enum EpiKind {
   EPI_GEGLU,     // gate/up interleaved in 16-row blocks: out_T[m, 16g+j] = T(gelu(gate) * up)
   EPI_QKV_ROPE,  // q/k rotated pairs (rotate-half, permuted rows), v plain; written to q / k / v
   EPI_EULER,     // x[m, n] += dt * (v + bias[n]); xop[m, n] = T(x[m, n])
+  EPI_PART,      // raw fp32 result into out = [splits][M][N] (ldo = its capacity in floats);
+                 // the consumer sums the splits in order
 };
 
 struct Epi {
@@ -59,7 +61,7 @@ struct GemmDesc {
   Epi epi;
 };
 
-// Scratch the kernels may use (split-K partials, attention partials).
+// Scratch the kernels may use (split-K and attention partials).
 struct Scratch {
   float* ptr = nullptr;
   size_t floats = 0;
@@ -102,9 +104,13 @@ struct AttnDesc {
 size_t attn_scratch_floats(const AttnDesc& a);
 hipError_t launch_attention(const AttnDesc& a, const Scratch& s, const LaunchCaps& caps, hipStream_t st);
 
-// Row norms of the fp32 residual stream into an operand buffer.
-hipError_t launch_norm(int dtype, const float* x, int ldx, int rows, int d, const float* g,
-                       const float* b, bool rms, void* out, int ldo, hipStream_t st);
+// Residual add + row norm: x[m] += bias + sum_s part[s][m] in split order
+// (part [splits][rows][d]; nothing is added when splits is 0), then
+// out[m] = LayerNorm (biased variance) or RMSNorm of x[m], times g (+ b),
+// in the operand type. d <= 2048.
+hipError_t launch_norm(int dtype, float* x, int ldx, int rows, int d, const float* part,
+                       int splits, const float* bias, const float* g, const float* b, bool rms,
+                       void* out, int ldo, hipStream_t st);
 
 // Image [views][H][W][3] fp32 -> patches [views * T][ldo] of the operand type,
 // columns beyond 3 p^2 zero.

@@ -147,27 +147,46 @@ __device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int 
 // ---------------------------------------------------------------------------
 // GEMM: C[M, N] = A[M, K] W[N, K]^T, both operands K-contiguous.
 // 256 threads = 4 waves in a 2 x 2 arrangement; each wave owns a
-// (BM/2) x (BN/2) block of 16 x 16 MFMA tiles. A and W tiles are staged
-// through LDS (rows padded by 16 bytes against bank conflicts) with the next
-// K-tile prefetched into registers while the current one is multiplied.
-// Tiles are visited grid-stride so a capped grid computes the same tiles.
+// (BM/2) x (BN/2) block of 16 x 16 MFMA tiles. A and W tiles go through a
+// two-stage LDS ring (rows padded by 16 bytes against bank conflicts) with the
+// next K-tile prefetched into registers, one barrier per K-step. The
+// accumulators are staged through LDS for the epilogue, so epilogue stores are
+// row-contiguous. Split-K partials are summed inside the kernel: the last
+// workgroup to finish a tile (per-tile arrival counter) adds the partials in
+// split order, so the result does not depend on arrival order. Tiles are
+// visited grid-stride so a capped grid computes the same tiles.
 // ---------------------------------------------------------------------------
+
+template <typename T, int BM, int BN, int BK>
+struct GemmSmem {
+  static constexpr int VEC = 16 / sizeof(T);
+  static constexpr int LDS = BK + VEC;
+  static constexpr int CLD = BN + 4;
+  union {
+    struct {
+      T a[2][BM * LDS];
+      T b[2][BN * LDS];
+    } ld;
+    float c[BM * CLD];
+  };
+};
 
 template <typename T, int BM, int BN, int BK>
 __global__ __launch_bounds__(256) void k_gemm(const T* __restrict__ A, int lda,
                                               const T* __restrict__ W, int ldw, int M, int N,
                                               int K, int kchunk, int splits, int tiles_m,
                                               int tiles_n, Epi e, float* __restrict__ part) {
-  constexpr int VEC = 16 / sizeof(T);
+  using SM = GemmSmem<T, BM, BN, BK>;
+  constexpr int VEC = SM::VEC;
   constexpr int SW = 4 * VEC;  // K covered by one MFMA step across the 4 lane groups
-  constexpr int LDS = BK + VEC;
+  constexpr int LDS = SM::LDS;
+  constexpr int CLD = SM::CLD;
   constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 16, TN = WN / 16;
   constexpr int KV = BK / VEC;
   constexpr int AV = BM * KV / 256, BV = BN * KV / 256;
   static_assert(AV >= 1 && BV >= 1 && (BM * KV) % 256 == 0 && (BN * KV) % 256 == 0, "tile");
-  static_assert(TN % 2 == 0, "paired epilogues need 32-column groups per wave");
-  __shared__ __attribute__((aligned(16))) T sA[BM * LDS];
-  __shared__ __attribute__((aligned(16))) T sB[BN * LDS];
+  static_assert(BN % 32 == 0, "paired epilogues need 32-column groups");
+  __shared__ __attribute__((aligned(16))) SM sm;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
@@ -180,6 +199,7 @@ __global__ __launch_bounds__(256) void k_gemm(const T* __restrict__ A, int lda,
     const int tm = t2 % tiles_m, tn = t2 / tiles_m;
     const int m0 = tm * BM, n0 = tn * BN;
     const int kbeg = s * kchunk, kend = min(K, kbeg + kchunk);
+    const int nk = (kend - kbeg + BK - 1) / BK;
 
     f32x4 acc[TM][TN];
 #pragma unroll
@@ -204,32 +224,44 @@ __global__ __launch_bounds__(256) void k_gemm(const T* __restrict__ A, int lda,
                                       : make_uint4(0, 0, 0, 0);
       }
     };
-
-    if (kbeg < kend) gload(kbeg);
-    for (int k0 = kbeg; k0 < kend; k0 += BK) {
-      __syncthreads();
+    auto sstore = [&](int buf) {
 #pragma unroll
       for (int i = 0; i < AV; ++i) {
         const int c = tid + i * 256, r = c / KV, kc = (c % KV) * VEC;
-        *(uint4*)(sA + r * LDS + kc) = ra[i];
+        *(uint4*)(sm.ld.a[buf] + r * LDS + kc) = ra[i];
       }
 #pragma unroll
       for (int i = 0; i < BV; ++i) {
         const int c = tid + i * 256, r = c / KV, kc = (c % KV) * VEC;
-        *(uint4*)(sB + r * LDS + kc) = rb[i];
+        *(uint4*)(sm.ld.b[buf] + r * LDS + kc) = rb[i];
       }
+    };
+
+    __syncthreads();  // the previous tile's epilogue is done with the LDS
+    if (nk > 0) {
+      gload(kbeg);
+      sstore(0);
+      if (nk > 1) gload(kbeg + BK);
+    }
+    for (int it = 0; it < nk; ++it) {
       __syncthreads();
-      if (k0 + BK < kend) gload(k0 + BK);
+      const int buf = it & 1;
+      if (it + 1 < nk) {
+        sstore(buf ^ 1);
+        if (it + 2 < nk) gload(kbeg + (it + 2) * BK);
+      }
+      const T* sa = sm.ld.a[buf];
+      const T* sb = sm.ld.b[buf];
 #pragma unroll
       for (int ks = 0; ks < BK / SW; ++ks) {
         uint4 af[TM], bfg[TN];
 #pragma unroll
         for (int i = 0; i < TM; ++i)
-          af[i] = *(const uint4*)(sA + (wm * WM + i * 16 + (lane & 15)) * LDS + ks * SW +
+          af[i] = *(const uint4*)(sa + (wm * WM + i * 16 + (lane & 15)) * LDS + ks * SW +
                                   (lane >> 4) * VEC);
 #pragma unroll
         for (int j = 0; j < TN; ++j)
-          bfg[j] = *(const uint4*)(sB + (wn * WN + j * 16 + (lane & 15)) * LDS + ks * SW +
+          bfg[j] = *(const uint4*)(sb + (wn * WN + j * 16 + (lane & 15)) * LDS + ks * SW +
                                    (lane >> 4) * VEC);
 #pragma unroll
         for (int i = 0; i < TM; ++i)
@@ -238,29 +270,33 @@ __global__ __launch_bounds__(256) void k_gemm(const T* __restrict__ A, int lda,
       }
     }
 
-    if (splits > 1) {
-      float* P = part + (size_t)s * M * N;
+    // accumulators -> LDS tile [BM][BN]
+    __syncthreads();
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
+      for (int j = 0; j < TN; ++j)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + r;
-            const int n = n0 + wn * WN + j * 16 + (lane & 15);
-            if (m < M && n < N) P[(size_t)m * N + n] = acc[i][j][r];
-          }
+        for (int r = 0; r < 4; ++r)
+          sm.c[(wm * WM + i * 16 + (lane >> 4) * 4 + r) * CLD + wn * WN + j * 16 + (lane & 15)] =
+              acc[i][j][r];
+    __syncthreads();
+
+    constexpr int PAIRS = BM * (BN / 2);  // (row, 32-column group, j < 16)
+    if (splits == 1 && e.kind != EPI_PART) {
+      for (int p = tid; p < PAIRS; p += 256) {
+        const int row = p / (BN / 2), q = p % (BN / 2);
+        const int col = (q >> 4) * 32 + (q & 15);
+        epi_pair<T>(e, M, N, m0 + row, n0 + col, sm.c[row * CLD + col], sm.c[row * CLD + col + 16]);
+      }
     } else {
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int jj = 0; jj < TN / 2; ++jj)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int m = m0 + wm * WM + i * 16 + (lane >> 4) * 4 + r;
-            const int n = n0 + wn * WN + jj * 32 + (lane & 15);
-            epi_pair<T>(e, M, N, m, n, acc[i][2 * jj][r], acc[i][2 * jj + 1][r]);
-          }
+      // raw fp32 partial of split s: [splits][M][N]
+      float* P = (e.kind == EPI_PART ? (float*)e.out : part) + (size_t)s * M * N;
+      for (int p = tid; p < BM * BN; p += 256) {
+        const int row = p / BN, col = p % BN;
+        const int m = m0 + row, n = n0 + col;
+        if (m < M && n < N) P[(size_t)m * N + n] = sm.c[row * CLD + col];
+      }
     }
   }
 }
@@ -291,8 +327,8 @@ struct TileCfg {
   int bm, bn, bk;
 };
 // bf16 configurations, then fp32 ones.
-static const TileCfg kBf16Cfg[] = {{128, 128, 64}, {64, 128, 64}, {64, 64, 64}, {32, 64, 128}};
-static const TileCfg kF32Cfg[] = {{64, 64, 32}, {32, 64, 64}};
+static const TileCfg kBf16Cfg[] = {{128, 128, 64}, {64, 128, 64}, {64, 64, 64}, {32, 64, 64}};
+static const TileCfg kF32Cfg[] = {{64, 64, 32}, {32, 64, 32}};
 
 GemmPlan plan_gemm(const GemmDesc& g) {
   GemmPlan p{};
@@ -311,7 +347,8 @@ GemmPlan plan_gemm(const GemmDesc& g) {
     c = g.M > 32 ? 0 : 1;
   }
   const TileCfg t = cfgs[c];
-  const int tiles = ((g.M + t.bm - 1) / t.bm) * ((g.N + t.bn - 1) / t.bn);
+  const int tm = (g.M + t.bm - 1) / t.bm, tn = (g.N + t.bn - 1) / t.bn;
+  const int tiles = tm * tn;
   int splits = 1;
   const int kblocks = (g.K + t.bk - 1) / t.bk;
   if (tiles < NUM_CU_PLAN && kblocks >= 4) {
@@ -323,7 +360,7 @@ GemmPlan plan_gemm(const GemmDesc& g) {
   p.cfg = c;
   p.splits = splits;
   p.tiles = tiles * splits;
-  p.scratch_floats = splits > 1 ? (size_t)splits * g.M * g.N : 0;
+  p.scratch_floats = (splits > 1 || g.epi.kind == EPI_PART) ? (size_t)splits * g.M * g.N : 0;
   return p;
 }
 
@@ -338,7 +375,7 @@ static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch
   k_gemm<T, BM, BN, BK><<<grid, 256, 0, st>>>((const T*)g.A, g.lda, (const T*)g.W, g.ldw, g.M,
                                                g.N, g.K, kchunk, p.splits, tiles_m, tiles_n,
                                                g.epi, s.ptr);
-  if (p.splits > 1) {
+  if (p.splits > 1 && g.epi.kind != EPI_PART) {
     const long long total = (long long)g.M * ((g.N + 31) / 32) * 16;
     int rgrid = (int)std::min<long long>((total + 255) / 256, 4096);
     if (caps.max_wgs > 0) rgrid = std::min(rgrid, caps.max_wgs);
@@ -350,18 +387,22 @@ static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch
 hipError_t launch_gemm(const GemmDesc& g, const Scratch& s, const LaunchCaps& caps,
                        hipStream_t st) {
   const GemmPlan p = plan_gemm(g);
-  if (p.scratch_floats > s.floats) return hipErrorInvalidValue;
+  if (g.epi.kind == EPI_PART) {
+    if (!g.epi.out || (size_t)p.splits * g.M * g.N > (size_t)g.epi.ldo) return hipErrorInvalidValue;
+  } else if (p.scratch_floats > s.floats) {
+    return hipErrorInvalidValue;
+  }
   if (g.dtype == DT_BF16) {
     switch (p.cfg) {
       case 0: return run_gemm_t<uint16_t, 128, 128, 64>(g, p, s, caps, st);
       case 1: return run_gemm_t<uint16_t, 64, 128, 64>(g, p, s, caps, st);
       case 2: return run_gemm_t<uint16_t, 64, 64, 64>(g, p, s, caps, st);
-      default: return run_gemm_t<uint16_t, 32, 64, 128>(g, p, s, caps, st);
+      default: return run_gemm_t<uint16_t, 32, 64, 64>(g, p, s, caps, st);
     }
   }
   switch (p.cfg) {
     case 0: return run_gemm_t<float, 64, 64, 32>(g, p, s, caps, st);
-    default: return run_gemm_t<float, 32, 64, 64>(g, p, s, caps, st);
+    default: return run_gemm_t<float, 32, 64, 32>(g, p, s, caps, st);
   }
 }
 
@@ -732,42 +773,75 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return (red[0] + red[1]) + (red[2] + red[3]);
 }
 
+// x[m, :] += bias + sum_s part[s, m, :] (split order; skipped when splits is
+// 0), stored back, then out[m, :] = norm(x[m, :]) * g (+ b). Row values stay
+// in registers (d <= 256 * NORM_NPT).
+constexpr int NORM_NPT = 8;
+
 template <typename T>
-__global__ __launch_bounds__(256) void k_norm(const float* __restrict__ x, int ldx, int rows,
-                                              int d, const float* __restrict__ g,
+__global__ __launch_bounds__(256) void k_norm(float* __restrict__ x, int ldx, int rows, int d,
+                                              const float* __restrict__ part, int splits,
+                                              const float* __restrict__ bias,
+                                              const float* __restrict__ g,
                                               const float* __restrict__ b, int rms, T* out,
                                               int ldo) {
   __shared__ float red[4];
+  const size_t pstride = (size_t)rows * d;
   for (int row = blockIdx.x; row < rows; row += gridDim.x) {
-    const float* xr = x + (size_t)row * ldx;
-    float mean = 0.f;
-    if (!rms) {
-      float s = 0.f;
-      for (int i = threadIdx.x; i < d; i += 256) s += xr[i];
-      mean = block_sum(s, red) / d;
+    float* xr = x + (size_t)row * ldx;
+    float v[NORM_NPT];
+    float s1 = 0.f;
+#pragma unroll
+    for (int q = 0; q < NORM_NPT; ++q) {
+      const int i = threadIdx.x + q * 256;
+      v[q] = 0.f;
+      if (i < d) {
+        float t = xr[i];
+        if (splits > 0) {
+          float add = bias ? bias[i] : 0.f;
+          for (int sp = 0; sp < splits; ++sp) add += part[sp * pstride + (size_t)row * d + i];
+          t += add;
+          xr[i] = t;
+        }
+        v[q] = t;
+        s1 += t;
+      }
     }
+    const float mean = rms ? 0.f : block_sum(s1, red) / d;
     float s2 = 0.f;
-    for (int i = threadIdx.x; i < d; i += 256) {
-      const float c = xr[i] - mean;
-      s2 += c * c;
+#pragma unroll
+    for (int q = 0; q < NORM_NPT; ++q) {
+      const int i = threadIdx.x + q * 256;
+      if (i < d) {
+        const float c = v[q] - mean;
+        s2 += c * c;
+      }
     }
     const float inv = 1.f / sqrtf(block_sum(s2, red) / d + 1e-6f);
     T* orow = out + (size_t)row * ldo;
-    for (int i = threadIdx.x; i < d; i += 256) {
-      float y = (xr[i] - mean) * inv * g[i];
-      if (b) y += b[i];
-      TT<T>::st(orow + i, y);
+#pragma unroll
+    for (int q = 0; q < NORM_NPT; ++q) {
+      const int i = threadIdx.x + q * 256;
+      if (i < d) {
+        float y = (v[q] - mean) * inv * g[i];
+        if (b) y += b[i];
+        TT<T>::st(orow + i, y);
+      }
     }
   }
 }
 
-hipError_t launch_norm(int dtype, const float* x, int ldx, int rows, int d, const float* g,
-                       const float* b, bool rms, void* out, int ldo, hipStream_t st) {
+hipError_t launch_norm(int dtype, float* x, int ldx, int rows, int d, const float* part,
+                       int splits, const float* bias, const float* g, const float* b, bool rms,
+                       void* out, int ldo, hipStream_t st) {
+  if (d > 256 * NORM_NPT) return hipErrorInvalidValue;
   const int grid = std::min(rows, 4096);
   if (dtype == DT_BF16)
-    k_norm<uint16_t><<<grid, 256, 0, st>>>(x, ldx, rows, d, g, b, rms, (uint16_t*)out, ldo);
+    k_norm<uint16_t><<<grid, 256, 0, st>>>(x, ldx, rows, d, part, splits, bias, g, b, rms,
+                                           (uint16_t*)out, ldo);
   else
-    k_norm<float><<<grid, 256, 0, st>>>(x, ldx, rows, d, g, b, rms, (float*)out, ldo);
+    k_norm<float><<<grid, 256, 0, st>>>(x, ldx, rows, d, part, splits, bias, g, b, rms,
+                                        (float*)out, ldo);
   return hipGetLastError();
 }
 

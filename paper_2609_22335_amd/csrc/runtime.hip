@@ -222,6 +222,12 @@ struct vla_model {
   std::vector<hipEvent_t> ev;
   std::mutex mu;
 
+  // per-tag kernel timer: every launch whose tag matches is bracketed by
+  // events on its own stream
+  std::string timer_tag;
+  std::vector<hipEvent_t> timer_ev;  // pairs (begin, end)
+  size_t timer_used = 0;
+
   char* tptr(int t) const { return (char*)arena + T[t].offset; }
   float* f32(int t) const { return (float*)tptr(t); }
 };
@@ -378,30 +384,72 @@ struct Run {
   const Scratch* scr;
 };
 
-static int gemm(const Run& r, const void* A, int lda, int W, int M, int N, int K, const Epi& e,
-                const void* Wptr = nullptr, int ldw = 0) {
+static int timer_begin(const Run& r, const char* tag, hipEvent_t* end) {
+  vla_model* m = r.m;
+  *end = nullptr;
+  if (m->timer_tag.empty() || m->timer_tag != tag) return VLA_OK;
+  while (m->timer_ev.size() < m->timer_used + 2) {
+    hipEvent_t e;
+    HIP_TRY(hipEventCreate(&e));
+    m->timer_ev.push_back(e);
+  }
+  HIP_TRY(hipEventRecord(m->timer_ev[m->timer_used], r.st));
+  *end = m->timer_ev[m->timer_used + 1];
+  m->timer_used += 2;
+  return VLA_OK;
+}
+
+static int timer_end(const Run& r, hipEvent_t end) {
+  if (end) HIP_TRY(hipEventRecord(end, r.st));
+  return VLA_OK;
+}
+
+static int gemm(const Run& r, const char* tag, const void* A, int lda, int W, int M, int N, int K,
+                const Epi& e, const void* Wptr = nullptr, int ldw = 0) {
   vla_model* m = r.m;
   GemmDesc g{m->dt, A, lda, Wptr ? Wptr : m->tptr(W), Wptr ? ldw : m->T[W].ld, M, N, K, e};
+  hipEvent_t tend;
+  VLA_TRY(timer_begin(r, tag, &tend));
   hipError_t err = launch_gemm(g, *r.scr, r.caps, r.st);
+  if (err == hipSuccess) VLA_TRY(timer_end(r, tend));
   if (err != hipSuccess)
     return fail(VLA_EHIP, std::string("gemm ") + std::to_string(M) + "x" + std::to_string(N) + "x" +
                               std::to_string(K) + ": " + hipGetErrorString(err));
   return VLA_OK;
 }
 
-static int attn(const Run& r, const AttnDesc& a) {
+static int attn(const Run& r, const char* tag, const AttnDesc& a) {
+  hipEvent_t tend;
+  VLA_TRY(timer_begin(r, tag, &tend));
   hipError_t err = launch_attention(a, *r.scr, r.caps, r.st);
+  if (err == hipSuccess) VLA_TRY(timer_end(r, tend));
   if (err != hipSuccess) return fail(VLA_EHIP, std::string("attention: ") + hipGetErrorString(err));
   return VLA_OK;
 }
 
-static int norm(const Run& r, const float* x, int ldx, int rows, int d, int g, int b, bool rms,
-                void* out, int ldo) {
+// Residual add of `splits` pending partials (from the phase scratch) + bias,
+// then LayerNorm / RMSNorm into `out`.
+static int norm(const Run& r, float* x, int rows, int d, int splits, const float* bias, int g, int b,
+                bool rms, void* out) {
   vla_model* m = r.m;
-  hipError_t err = launch_norm(m->dt, x, ldx, rows, d, m->f32(g), b >= 0 ? m->f32(b) : nullptr, rms,
-                               out, ldo, r.st);
+  hipError_t err = launch_norm(m->dt, x, d, rows, d, r.scr->ptr, splits, bias, m->f32(g),
+                               b >= 0 ? m->f32(b) : nullptr, rms, out, d, r.st);
   if (err != hipSuccess) return fail(VLA_EHIP, std::string("norm: ") + hipGetErrorString(err));
   return VLA_OK;
+}
+
+// GEMM whose result is added to the residual stream by the next norm: the raw
+// result (or its split-K partials) goes to the phase scratch.
+static int gemm_part(const Run& r, const char* tag, const void* A, int lda, int W, int M, int N,
+                     int K, int* splits) {
+  vla_model* m = r.m;
+  Epi e;
+  e.kind = EPI_PART;
+  e.out = r.scr->ptr;
+  e.ldo = (int)std::min<size_t>(r.scr->floats, (size_t)INT32_MAX);
+  GemmDesc g{m->dt, A, lda, m->tptr(W), m->T[W].ld, M, N, K, e};
+  *splits = plan_gemm(g).splits;
+  return gemm(r, tag, A, lda, W, M, N, K, e);
 }
 
 static Epi epi_kind(int kind, void* out = nullptr, int ldo = 0, const float* bias = nullptr) {
@@ -412,24 +460,20 @@ static Epi epi_kind(int kind, void* out = nullptr, int ldo = 0, const float* bia
   e.bias = bias;
   return e;
 }
-static Epi epi_resid(float* x, int ld, const float* bias = nullptr) {
-  Epi e;
-  e.kind = EPI_RESID;
-  e.resid = x;
-  e.ldr = ld;
-  e.bias = bias;
-  return e;
-}
 
-// One Gemma-style decoder layer: RMSNorm -> QKV (+RoPE, K/V stored) ->
-// attention over [past; own] -> O + residual -> RMSNorm -> GeGLU -> down + residual.
-static int decoder_layer(const Run& r, const DecLayer& L, float* x, int rows, int dim, int mlp,
+// One Gemma-style decoder layer: RMSNorm (after adding the pending residual
+// partials) -> QKV (+RoPE, K/V stored) -> attention over [past; own] -> O ->
+// RMSNorm (after adding O) -> GeGLU -> down. The down projection is left
+// pending in the scratch (*pend = its split count) for the next norm.
+static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int rows, int dim, int mlp,
                          void* h, void* q, void* kout, void* vout, int pos0, const void* kpast,
-                         const void* vpast, int npast, void* att, void* mlpbuf, bool kv_only) {
+                         const void* vpast, int npast, void* att, void* mlpbuf, bool kv_only,
+                         int* pend) {
   vla_model* m = r.m;
   const vla_config& c = m->c;
   const Dims& d = m->d;
-  VLA_TRY(norm(r, x, dim, rows, dim, L.rms1, -1, true, h, dim));
+  VLA_TRY(norm(r, x, rows, dim, *pend, nullptr, L.rms1, -1, true, h));
+  *pend = 0;
   Epi e;
   e.kind = EPI_QKV_ROPE;
   e.q = q;
@@ -443,7 +487,7 @@ static int decoder_layer(const Run& r, const DecLayer& L, float* x, int rows, in
   e.pos0 = pos0;
   e.rope_cos = m->rope_cos;
   e.rope_sin = m->rope_sin;
-  VLA_TRY(gemm(r, h, dim, L.qkv, rows, d.qkv_n, dim, e));
+  VLA_TRY(gemm(r, lm ? "lm.qkv" : "ex.qkv", h, dim, L.qkv, rows, d.qkv_n, dim, e));
   if (kv_only) return VLA_OK;
   AttnDesc a{};
   a.dtype = m->dt;
@@ -469,11 +513,13 @@ static int decoder_layer(const Run& r, const DecLayer& L, float* x, int rows, in
   a.nkv = c.lm_kv_heads;
   a.hd = c.head_dim;
   a.segs = 1;
-  VLA_TRY(attn(r, a));
-  VLA_TRY(gemm(r, att, d.qd, L.o, rows, dim, d.qd, epi_resid(x, dim)));
-  VLA_TRY(norm(r, x, dim, rows, dim, L.rms2, -1, true, h, dim));
-  VLA_TRY(gemm(r, h, dim, L.gu, rows, 2 * mlp, dim, epi_kind(EPI_GEGLU, mlpbuf, mlp)));
-  VLA_TRY(gemm(r, mlpbuf, mlp, L.down, rows, dim, mlp, epi_resid(x, dim)));
+  VLA_TRY(attn(r, lm ? "lm.attn" : "ex.attn", a));
+  int so = 0;
+  VLA_TRY(gemm_part(r, lm ? "lm.o" : "ex.o", att, d.qd, L.o, rows, dim, d.qd, &so));
+  VLA_TRY(norm(r, x, rows, dim, so, nullptr, L.rms2, -1, true, h));
+  VLA_TRY(gemm(r, lm ? "lm.gateup" : "ex.gateup", h, dim, L.gu, rows, 2 * mlp, dim,
+               epi_kind(EPI_GEGLU, mlpbuf, mlp)));
+  VLA_TRY(gemm_part(r, lm ? "lm.down" : "ex.down", mlpbuf, mlp, L.down, rows, dim, mlp, pend));
   return VLA_OK;
 }
 
@@ -490,12 +536,14 @@ static int run_prefill(const Run& r, const vla_frame* f, vla_ctx* ctx) {
     e.rowadd = m->f32(m->pos);
     e.rowadd_period = d.tview;
     e.ldra = dv;
-    VLA_TRY(gemm(r, w.h, d.kp_pad, m->patch_w, rows, dv, d.kp_pad, e));
+    VLA_TRY(gemm(r, "vit.patch", w.h, d.kp_pad, m->patch_w, rows, dv, d.kp_pad, e));
   }
+  int pend = 0;
+  const float* pbias = nullptr;
   for (int l = 0; l < c.vit_layers; ++l) {
     const VitLayer& L = m->vit[l];
-    VLA_TRY(norm(r, w.xv, dv, rows, dv, L.ln1_g, L.ln1_b, false, w.h, dv));
-    VLA_TRY(gemm(r, w.h, dv, L.qkv_w, rows, 3 * dv, dv, epi_kind(EPI_T, w.qkv, 3 * dv, m->f32(L.qkv_b))));
+    VLA_TRY(norm(r, w.xv, rows, dv, pend, pbias, L.ln1_g, L.ln1_b, false, w.h));
+    VLA_TRY(gemm(r, "vit.qkv", w.h, dv, L.qkv_w, rows, 3 * dv, dv, epi_kind(EPI_T, w.qkv, 3 * dv, m->f32(L.qkv_b))));
     AttnDesc a{};
     a.dtype = m->dt;
     a.q = w.qkv;
@@ -512,29 +560,32 @@ static int run_prefill(const Run& r, const vla_frame* f, vla_ctx* ctx) {
     a.segs = c.n_views;
     a.seg_q = a.seg_kv = (long long)d.tview * 3 * dv;
     a.seg_o = (long long)d.tview * dv;
-    VLA_TRY(attn(r, a));
-    VLA_TRY(gemm(r, w.att, dv, L.o_w, rows, dv, dv, epi_resid(w.xv, dv, m->f32(L.o_b))));
-    VLA_TRY(norm(r, w.xv, dv, rows, dv, L.ln2_g, L.ln2_b, false, w.h, dv));
-    VLA_TRY(gemm(r, w.h, dv, L.fc1_w, rows, c.vit_mlp, dv, epi_kind(EPI_GELU, w.mlp, c.vit_mlp, m->f32(L.fc1_b))));
-    VLA_TRY(gemm(r, w.mlp, c.vit_mlp, L.fc2_w, rows, dv, c.vit_mlp, epi_resid(w.xv, dv, m->f32(L.fc2_b))));
+    VLA_TRY(attn(r, "vit.attn", a));
+    int so = 0;
+    VLA_TRY(gemm_part(r, "vit.o", w.att, dv, L.o_w, rows, dv, dv, &so));
+    VLA_TRY(norm(r, w.xv, rows, dv, so, m->f32(L.o_b), L.ln2_g, L.ln2_b, false, w.h));
+    VLA_TRY(gemm(r, "vit.fc1", w.h, dv, L.fc1_w, rows, c.vit_mlp, dv, epi_kind(EPI_GELU, w.mlp, c.vit_mlp, m->f32(L.fc1_b))));
+    VLA_TRY(gemm_part(r, "vit.fc2", w.mlp, c.vit_mlp, L.fc2_w, rows, dv, c.vit_mlp, &pend));
+    pbias = m->f32(L.fc2_b);
   }
-  VLA_TRY(norm(r, w.xv, dv, rows, dv, m->post_g, m->post_b, false, w.h, dv));
+  VLA_TRY(norm(r, w.xv, rows, dv, pend, pbias, m->post_g, m->post_b, false, w.h));
   // prefix: [projected image tokens; text * sqrt(d); state projection]
-  VLA_TRY(gemm(r, w.h, dv, m->proj_w, rows, dl, dv, epi_kind(EPI_F32, w.xl, dl, m->f32(m->proj_b))));
+  VLA_TRY(gemm(r, "proj", w.h, dv, m->proj_w, rows, dl, dv, epi_kind(EPI_F32, w.xl, dl, m->f32(m->proj_b))));
   HIP_TRY(launch_embed(m->dt, m->tptr(m->embed), dl, c.vocab, f->text_ids, c.n_text, std::sqrt((float)dl),
                        w.xl + (size_t)d.nimg * dl, dl, r.st));
   if (c.state_dim > 0) {
     HIP_TRY(launch_cvt_pad(m->dt, f->state, 1, c.state_dim, w.sbuf, d.s_pad, nullptr, r.st));
-    VLA_TRY(gemm(r, w.sbuf, d.s_pad, m->state_w, 1, dl, d.s_pad,
+    VLA_TRY(gemm(r, "state", w.sbuf, d.s_pad, m->state_w, 1, dl, d.s_pad,
                  epi_kind(EPI_F32, w.xl + (size_t)(d.prefix - 1) * dl, dl, m->f32(m->state_b))));
   }
   // LM prefill writing the cache
   const size_t layer_kv = (size_t)d.prefix * d.kvd * m->esz;
+  pend = 0;
   for (int l = 0; l < c.lm_layers; ++l) {
     void* K = (char*)ctx->K + l * layer_kv;
     void* V = (char*)ctx->V + l * layer_kv;
-    VLA_TRY(decoder_layer(r, m->lm[l], w.xl, d.prefix, dl, c.lm_mlp, w.h, w.qkv, K, V, 0, nullptr,
-                          nullptr, 0, w.att, w.mlp, l == c.lm_layers - 1));
+    VLA_TRY(decoder_layer(r, true, m->lm[l], w.xl, d.prefix, dl, c.lm_mlp, w.h, w.qkv, K, V, 0, nullptr,
+                          nullptr, 0, w.att, w.mlp, l == c.lm_layers - 1, &pend));
   }
   return VLA_OK;
 }
@@ -550,16 +601,17 @@ static int run_denoise(const Run& r, const vla_ctx* ctx, const float* noise, flo
   const size_t layer_kv = (size_t)d.prefix * d.kvd * m->esz;
   for (int k = 0; k < c.n_steps; ++k) {
     // action embedding and time conditioning
-    VLA_TRY(gemm(r, w.xop, d.a_pad, m->in_w, H, de, d.a_pad, epi_kind(EPI_T, w.a, de, m->f32(m->in_b))));
-    VLA_TRY(gemm(r, w.a, de, m->t1_w, H, de, de, epi_kind(EPI_SWISH, w.hid, de, m->ck + (size_t)k * de)));
-    VLA_TRY(gemm(r, w.hid, de, m->t2_w, H, de, de, epi_kind(EPI_F32, w.u, de, m->f32(m->t2_b))));
+    VLA_TRY(gemm(r, "ex.in", w.xop, d.a_pad, m->in_w, H, de, d.a_pad, epi_kind(EPI_T, w.a, de, m->f32(m->in_b))));
+    VLA_TRY(gemm(r, "ex.time1", w.a, de, m->t1_w, H, de, de, epi_kind(EPI_SWISH, w.hid, de, m->ck + (size_t)k * de)));
+    VLA_TRY(gemm(r, "ex.time2", w.hid, de, m->t2_w, H, de, de, epi_kind(EPI_F32, w.u, de, m->f32(m->t2_b))));
+    int pend = 0;
     for (int l = 0; l < c.ex_layers; ++l) {
       const void* K = (const char*)ctx->K + l * layer_kv;
       const void* V = (const char*)ctx->V + l * layer_kv;
-      VLA_TRY(decoder_layer(r, m->ex[l], w.u, H, de, c.ex_mlp, w.h, w.q, w.kown, w.vown, d.prefix,
-                            K, V, d.prefix, w.att, w.mlp, false));
+      VLA_TRY(decoder_layer(r, false, m->ex[l], w.u, H, de, c.ex_mlp, w.h, w.q, w.kown, w.vown, d.prefix,
+                            K, V, d.prefix, w.att, w.mlp, false, &pend));
     }
-    VLA_TRY(norm(r, w.u, de, H, de, m->fin_g, -1, true, w.h, de));
+    VLA_TRY(norm(r, w.u, H, de, pend, nullptr, m->fin_g, -1, true, w.h));
     Epi e;
     e.kind = EPI_EULER;
     e.bias = m->f32(m->out_b);
@@ -568,7 +620,7 @@ static int run_denoise(const Run& r, const vla_ctx* ctx, const float* noise, flo
     e.xop = w.xop;
     e.ldxop = d.a_pad;
     e.dt = dt;
-    VLA_TRY(gemm(r, w.h, de, m->out_w, H, A, de, e));
+    VLA_TRY(gemm(r, "ex.out", w.h, de, m->out_w, H, A, de, e));
   }
   return VLA_OK;
 }
@@ -577,12 +629,18 @@ static int run_denoise(const Run& r, const vla_ctx* ctx, const float* noise, flo
 // Creation
 // ---------------------------------------------------------------------------
 
-static size_t gemm_scratch(int dt, int M, int N, int K) {
+struct ScratchNeed {
+  size_t floats = 0;
+};
+
+static ScratchNeed gemm_scratch(int dt, int M, int N, int K, bool part = false) {
   GemmDesc g{dt, nullptr, K, nullptr, K, M, N, K, Epi()};
-  return plan_gemm(g).scratch_floats;
+  if (part) g.epi.kind = EPI_PART;
+  const GemmPlan p = plan_gemm(g);
+  return ScratchNeed{p.scratch_floats};
 }
 
-static size_t attn_scratch(int dt, int Sq, int nq, int nkv, int hd, int S0, int S1, int segs) {
+static ScratchNeed attn_scratch(int dt, int Sq, int nq, int nkv, int hd, int S0, int S1, int segs) {
   AttnDesc a{};
   a.dtype = dt;
   a.Sq = Sq;
@@ -592,7 +650,13 @@ static size_t attn_scratch(int dt, int Sq, int nq, int nkv, int hd, int S0, int 
   a.S0 = S0;
   a.S1 = S1;
   a.segs = segs;
-  return attn_scratch_floats(a);
+  return ScratchNeed{attn_scratch_floats(a)};
+}
+
+static int alloc_scratch(vla_model* m, const ScratchNeed& n, Scratch* s) {
+  s->floats = std::max<size_t>(n.floats, 64);
+  VLA_TRY(dmalloc(m, (void**)&s->ptr, s->floats * 4));
+  return VLA_OK;
 }
 
 static int setup_tables(vla_model* m) {
@@ -652,23 +716,22 @@ static int setup_workspaces(vla_model* m) {
   VLA_TRY(dmalloc(m, &v.att, (size_t)std::max((size_t)rv * dv, (size_t)P * d.qd) * e));
   VLA_TRY(dmalloc(m, &v.mlp, (size_t)std::max((size_t)rv * c.vit_mlp, (size_t)P * c.lm_mlp) * e));
   VLA_TRY(dmalloc(m, &v.sbuf, (size_t)d.s_pad * e));
-  size_t sv = 0;
-  auto upd = [](size_t& s, size_t x) { s = std::max(s, x); };
+  ScratchNeed sv;
+  auto upd = [](ScratchNeed& s, ScratchNeed x) { s.floats = std::max(s.floats, x.floats); };
   upd(sv, gemm_scratch(dt, rv, dv, d.kp_pad));
   upd(sv, gemm_scratch(dt, rv, 3 * dv, dv));
-  upd(sv, gemm_scratch(dt, rv, dv, dv));
+  upd(sv, gemm_scratch(dt, rv, dv, dv, true));
   upd(sv, gemm_scratch(dt, rv, c.vit_mlp, dv));
-  upd(sv, gemm_scratch(dt, rv, dv, c.vit_mlp));
+  upd(sv, gemm_scratch(dt, rv, dv, c.vit_mlp, true));
   upd(sv, gemm_scratch(dt, rv, dl, dv));
   upd(sv, gemm_scratch(dt, 1, dl, d.s_pad));
   upd(sv, gemm_scratch(dt, P, d.qkv_n, dl));
-  upd(sv, gemm_scratch(dt, P, dl, d.qd));
+  upd(sv, gemm_scratch(dt, P, dl, d.qd, true));
   upd(sv, gemm_scratch(dt, P, 2 * c.lm_mlp, dl));
-  upd(sv, gemm_scratch(dt, P, dl, c.lm_mlp));
+  upd(sv, gemm_scratch(dt, P, dl, c.lm_mlp, true));
   upd(sv, attn_scratch(dt, d.tview, c.vit_heads, c.vit_heads, d.vhd, d.tview, 0, c.n_views));
   upd(sv, attn_scratch(dt, P, c.lm_heads, c.lm_kv_heads, c.head_dim, P, 0, 1));
-  VLA_TRY(dmalloc(m, (void**)&v.scr.ptr, std::max<size_t>(sv, 64) * 4));
-  v.scr.floats = std::max<size_t>(sv, 64);
+  VLA_TRY(alloc_scratch(m, sv, &v.scr));
 
   auto& a = m->aw;
   VLA_TRY(dmalloc(m, (void**)&a.u, (size_t)H * de * 4));
@@ -681,18 +744,17 @@ static int setup_workspaces(vla_model* m) {
   VLA_TRY(dmalloc(m, &a.vown, (size_t)H * d.kvd * e));
   VLA_TRY(dmalloc(m, &a.att, (size_t)H * d.qd * e));
   VLA_TRY(dmalloc(m, &a.mlp, (size_t)H * c.ex_mlp * e));
-  size_t sa = 0;
+  ScratchNeed sa;
   upd(sa, gemm_scratch(dt, H, de, d.a_pad));
   upd(sa, gemm_scratch(dt, H, de, de));
   upd(sa, gemm_scratch(dt, c.n_steps, de, de));
   upd(sa, gemm_scratch(dt, H, d.qkv_n, de));
-  upd(sa, gemm_scratch(dt, H, de, d.qd));
+  upd(sa, gemm_scratch(dt, H, de, d.qd, true));
   upd(sa, gemm_scratch(dt, H, 2 * c.ex_mlp, de));
-  upd(sa, gemm_scratch(dt, H, de, c.ex_mlp));
+  upd(sa, gemm_scratch(dt, H, de, c.ex_mlp, true));
   upd(sa, gemm_scratch(dt, H, c.action_dim, de));
   upd(sa, attn_scratch(dt, H, c.lm_heads, c.lm_kv_heads, c.head_dim, P, H, 1));
-  VLA_TRY(dmalloc(m, (void**)&a.scr.ptr, std::max<size_t>(sa, 64) * 4));
-  a.scr.floats = std::max<size_t>(sa, 64);
+  VLA_TRY(alloc_scratch(m, sa, &a.scr));
   return VLA_OK;
 }
 
@@ -732,7 +794,7 @@ static int create_impl(const vla_config* cfg, uint64_t seed, vla_model** out) {
     // c_k = W_2[:, d_e:] phi(t_k) + b_2 for every step (depends on the step only)
     Run r{m.get(), nullptr, LaunchCaps{}, &m->aw.scr};
     const int de = m->c.ex_dim;
-    rc = gemm(r, m->phi, de, -1, m->c.n_steps, de, de, epi_kind(EPI_F32, m->ck, de, m->f32(m->t1_b)),
+    rc = gemm(r, "ex.ck", m->phi, de, -1, m->c.n_steps, de, de, epi_kind(EPI_F32, m->ck, de, m->f32(m->t1_b)),
               m->tptr(m->t1_w) + (size_t)de * m->esz, m->T[m->t1_w].ld);
   }
   if (rc == VLA_OK) {
@@ -916,6 +978,7 @@ int vla_destroy(vla_model* m) {
       hipStreamDestroy(m->plain.a);
     }
     for (auto e : m->ev) hipEventDestroy(e);
+    for (auto e : m->timer_ev) hipEventDestroy(e);
     for (void* p : m->allocs) hipFree(p);
     hipFree(m->arena);
     delete m;
@@ -1093,6 +1156,34 @@ int vla_debug_attention(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int3
       hipFree(s.ptr);
     }
     if (e != hipSuccess) return fail(VLA_EHIP, std::string("attention: ") + hipGetErrorString(e));
+    return VLA_OK;
+  })
+}
+
+int vla_kernel_timer(vla_model* m, const char* tag) {
+  ABI_GUARD({
+    if (!m) return fail(VLA_EINVAL, "model is NULL");
+    std::lock_guard<std::mutex> lock(m->mu);
+    m->timer_tag = tag ? tag : "";
+    m->timer_used = 0;
+    return VLA_OK;
+  })
+}
+
+int vla_kernel_timer_read(vla_model* m, double* total_ms, int64_t* launches) {
+  ABI_GUARD({
+    if (!m || !total_ms || !launches) return fail(VLA_EINVAL, "NULL argument");
+    std::lock_guard<std::mutex> lock(m->mu);
+    double tot = 0;
+    for (size_t i = 0; i + 1 < m->timer_used; i += 2) {
+      HIP_TRY(hipEventSynchronize(m->timer_ev[i + 1]));
+      float ms = 0;
+      HIP_TRY(hipEventElapsedTime(&ms, m->timer_ev[i], m->timer_ev[i + 1]));
+      tot += ms;
+    }
+    *total_ms = tot;
+    *launches = (int64_t)(m->timer_used / 2);
+    m->timer_used = 0;
     return VLA_OK;
   })
 }
