@@ -178,8 +178,10 @@ int vla_debug_attention(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int3
  * kernels behind that call site (tags: "vit.patch", "vit.qkv", "vit.attn",
  * "vit.o", "vit.fc1", "vit.fc2", "proj", "state", "lm.qkv", "lm.attn", "lm.o",
  * "lm.gateup", "lm.down", "ex.in", "ex.time1", "ex.time2", "ex.qkv",
- * "ex.attn", "ex.o", "ex.gateup", "ex.down", "ex.out") is bracketed by HIP
- * events recorded on the stream that launches it. NULL or "" turns it off.
+ * "ex.attn", "ex.o", "ex.gateup", "ex.down", "ex.out") records a pair of
+ * HIP events at the start and end of its main kernel (hipExtLaunchKernel
+ * start/stop events, on the launching stream; a separate split-K reduce or
+ * attention-combine kernel is not included). NULL or "" turns it off.
  * _read waits for the recorded events, returns the summed duration (ms) and
  * the number of bracketed launches since the last read, and resets both. */
 int vla_kernel_timer(vla_model* m, const char* tag);

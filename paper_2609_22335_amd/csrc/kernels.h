@@ -59,7 +59,16 @@ struct GemmDesc {
   int ldw;
   int M, N, K;
   Epi epi;
+  // Fragment-ordered weights (skinny kernel, M <= 64): K-slabs per n-block in
+  // the stored tensor and the first slab used; frag_ks == 0 means row-major W.
+  int frag_ks = 0;
+  int frag_ks0 = 0;
 };
+
+// Offset of element (n, k) of a weight stored in MFMA fragment order with KS
+// K-slabs (of frag_slab(dtype) elements) per 16-row n-block.
+size_t frag_index(int n, int k, int KS, int dtype);
+int frag_slab(int dtype);
 
 // Scratch the kernels may use (split-K and attention partials).
 struct Scratch {
@@ -71,6 +80,10 @@ struct Scratch {
 // split or reduction order (results are independent of them).
 struct LaunchCaps {
   int max_wgs = 0;  // 0 = uncapped; otherwise grid-stride over tiles
+  // when set, the main kernel of the launch records these at its own start
+  // and end (measurement only)
+  hipEvent_t ev_start = nullptr;
+  hipEvent_t ev_stop = nullptr;
 };
 
 struct GemmPlan {

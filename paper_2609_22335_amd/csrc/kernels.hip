@@ -9,6 +9,7 @@
 // Every reduction has a fixed order that depends only on the problem shape
 // (tile sizes, split-K and KV-split factors come from the shape), so results
 // do not depend on the grid size, CU mask or on which workgroup ran a tile.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -323,6 +324,147 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__
   }
 }
 
+// ---------------------------------------------------------------------------
+// Skinny GEMM for M <= 64 (the action expert's rows): C[M, N] = A[M, K] W^T
+// with W stored in MFMA fragment order (see frag_index): the 16 x SW fragment
+// of n-block nb and K-slab ks is 1 KB contiguous, lane l holding W[16 nb +
+// l % 16][SW ks + VEC (l / 16) ...]. A workgroup owns 32 columns (two
+// n-blocks, so the paired epilogues stay inside it) and a K-range of
+// 4 * SPW slabs; each wave takes SPW consecutive slabs and issues every load
+// of its range at once (one memory round trip), then the four waves' partial
+// sums are added in wave order through LDS. K-ranges beyond one workgroup
+// are split: EPI_PART leaves the split partials to the consumer, other
+// epilogues go through the split-K reduce kernel.
+// ---------------------------------------------------------------------------
+
+template <typename T, int SPW>
+__global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, int lda,
+                                                const T* __restrict__ Wf, int KS, int ks0, int M,
+                                                int N, int K, int splits, Epi e,
+                                                float* __restrict__ part) {
+  constexpr int VEC = 16 / sizeof(T);
+  constexpr int SW = 4 * VEC;
+  __shared__ float red[4][8][4][64];  // [wave][n-block * 4 + m-tile][r][lane]
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int npairs = (N + 31) / 32;
+  const int nslab = (K + SW - 1) / SW;
+  const int total = npairs * splits;
+  const T dummy = T();
+  for (int w = blockIdx.x; w < total; w += gridDim.x) {
+    const int s = w % splits, np = w / splits;
+    const int sb = (s * 4 + wave) * SPW;
+    uint4 bf[SPW][2], af[SPW][4];
+#pragma unroll
+    for (int q = 0; q < SPW; ++q) {
+      const int ks = sb + q;
+      const bool ok = ks < nslab;
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        bf[q][nb] = ok ? *(const uint4*)(Wf + ((size_t)((2 * np + nb) * KS + ks0 + ks) * 64 + lane) * VEC)
+                       : make_uint4(0, 0, 0, 0);
+      const int k = ks * SW + (lane >> 4) * VEC;
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const int row = mt * 16 + (lane & 15);
+        af[q][mt] = (ok && row < M && k < K) ? *(const uint4*)(A + (size_t)row * lda + k)
+                                             : make_uint4(0, 0, 0, 0);
+      }
+    }
+    f32x4 acc[2][4];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) acc[nb][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < SPW; ++q)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt) acc[nb][mt] = mfma_step(af[q][mt], bf[q][nb], acc[nb][mt], dummy);
+
+    __syncthreads();  // red is free (previous tile's epilogue done)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) red[wave][nb * 4 + mt][r][lane] = acc[nb][mt][r];
+    __syncthreads();
+    // wave w finishes m-tile w: sum the four waves in order, then the epilogue
+    const int mt = wave;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float v[2];
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        v[nb] = ((red[0][nb * 4 + mt][r][lane] + red[1][nb * 4 + mt][r][lane]) +
+                 red[2][nb * 4 + mt][r][lane]) + red[3][nb * 4 + mt][r][lane];
+      const int m = mt * 16 + (lane >> 4) * 4 + r;
+      const int n = np * 32 + (lane & 15);
+      if (m >= M) continue;
+      if (splits == 1 && e.kind != EPI_PART) {
+        epi_pair<T>(e, M, N, m, n, v[0], v[1]);
+      } else {
+        float* P = (e.kind == EPI_PART ? (float*)e.out : part) + (size_t)s * M * N + (size_t)m * N;
+        if (n < N) P[n] = v[0];
+        if (n + 16 < N) P[n + 16] = v[1];
+      }
+    }
+  }
+}
+
+size_t frag_index(int n, int k, int KS, int dtype) {
+  const int vec = dtype == DT_BF16 ? 8 : 4, sw = 4 * vec;
+  const size_t frag = (size_t)(n / 16) * KS + k / sw;
+  const int lane = n % 16 + 16 * ((k % sw) / vec);
+  return (frag * 64 + lane) * vec + k % vec;
+}
+
+int frag_slab(int dtype) { return dtype == DT_BF16 ? 32 : 16; }
+
+static int skinny_spw(const GemmDesc& g) { return g.epi.kind == EPI_PART ? 4 : 8; }
+
+int skinny_splits(const GemmDesc& g) {
+  const int sw = frag_slab(g.dtype);
+  const int per_wg = 4 * skinny_spw(g) * sw;
+  return std::max(1, (g.K + per_wg - 1) / per_wg);
+}
+
+template <typename T, int SPW>
+static hipError_t run_skinny_t(const GemmDesc& g, int splits, const Scratch& s,
+                               const LaunchCaps& caps, hipStream_t st) {
+  int grid = ((g.N + 31) / 32) * splits;
+  if (caps.max_wgs > 0) grid = std::min(grid, caps.max_wgs);
+  hipExtLaunchKernelGGL((k_skinny<T, SPW>), dim3(grid), dim3(256), 0, st, caps.ev_start,
+                        caps.ev_stop, 0, (const T*)g.A, g.lda, (const T*)g.W, g.frag_ks,
+                        g.frag_ks0, g.M, g.N, g.K, splits, g.epi, s.ptr);
+  if (splits > 1 && g.epi.kind != EPI_PART) {
+    const long long total = (long long)g.M * ((g.N + 31) / 32) * 16;
+    int rgrid = (int)std::min<long long>((total + 255) / 256, 4096);
+    if (caps.max_wgs > 0) rgrid = std::min(rgrid, caps.max_wgs);
+    k_splitk_reduce<T><<<rgrid, 256, 0, st>>>(s.ptr, splits, g.M, g.N, g.epi);
+  }
+  return hipGetLastError();
+}
+
+static hipError_t launch_skinny(const GemmDesc& g, const Scratch& s, const LaunchCaps& caps,
+                                hipStream_t st) {
+  if (g.M > 64) return hipErrorInvalidValue;
+  const int splits = skinny_splits(g);
+  const size_t need = (size_t)splits * g.M * g.N;
+  if (g.epi.kind == EPI_PART) {
+    if (!g.epi.out || need > (size_t)g.epi.ldo) return hipErrorInvalidValue;
+  } else if (splits > 1 && need > s.floats) {
+    return hipErrorInvalidValue;
+  }
+  const bool part = g.epi.kind == EPI_PART;
+  if (g.dtype == DT_BF16)
+    return part ? run_skinny_t<uint16_t, 4>(g, splits, s, caps, st)
+                : run_skinny_t<uint16_t, 8>(g, splits, s, caps, st);
+  return part ? run_skinny_t<float, 4>(g, splits, s, caps, st)
+              : run_skinny_t<float, 8>(g, splits, s, caps, st);
+}
+
 struct TileCfg {
   int bm, bn, bk;
 };
@@ -332,6 +474,13 @@ static const TileCfg kF32Cfg[] = {{64, 64, 32}, {32, 64, 32}};
 
 GemmPlan plan_gemm(const GemmDesc& g) {
   GemmPlan p{};
+  if (g.frag_ks > 0) {  // fragment-ordered weights: skinny kernel
+    p.cfg = -1;
+    p.splits = skinny_splits(g);
+    p.tiles = ((g.N + 31) / 32) * p.splits;
+    p.scratch_floats = (p.splits > 1 || g.epi.kind == EPI_PART) ? (size_t)p.splits * g.M * g.N : 0;
+    return p;
+  }
   const TileCfg* cfgs = g.dtype == DT_BF16 ? kBf16Cfg : kF32Cfg;
   int c;
   if (g.dtype == DT_BF16) {
@@ -372,9 +521,9 @@ static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch
   const int kchunk = ((kblocks + p.splits - 1) / p.splits) * BK;
   int grid = p.tiles;
   if (caps.max_wgs > 0) grid = std::min(grid, caps.max_wgs);
-  k_gemm<T, BM, BN, BK><<<grid, 256, 0, st>>>((const T*)g.A, g.lda, (const T*)g.W, g.ldw, g.M,
-                                               g.N, g.K, kchunk, p.splits, tiles_m, tiles_n,
-                                               g.epi, s.ptr);
+  hipExtLaunchKernelGGL((k_gemm<T, BM, BN, BK>), dim3(grid), dim3(256), 0, st, caps.ev_start,
+                        caps.ev_stop, 0, (const T*)g.A, g.lda, (const T*)g.W, g.ldw, g.M, g.N,
+                        g.K, kchunk, p.splits, tiles_m, tiles_n, g.epi, s.ptr);
   if (p.splits > 1 && g.epi.kind != EPI_PART) {
     const long long total = (long long)g.M * ((g.N + 31) / 32) * 16;
     int rgrid = (int)std::min<long long>((total + 255) / 256, 4096);
@@ -386,6 +535,7 @@ static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch
 
 hipError_t launch_gemm(const GemmDesc& g, const Scratch& s, const LaunchCaps& caps,
                        hipStream_t st) {
+  if (g.frag_ks > 0) return launch_skinny(g, s, caps, st);
   const GemmPlan p = plan_gemm(g);
   if (g.epi.kind == EPI_PART) {
     if (!g.epi.out || (size_t)p.splits * g.M * g.N > (size_t)g.epi.ldo) return hipErrorInvalidValue;
@@ -699,7 +849,8 @@ static hipError_t run_attn_t(const AttnArgs& a, const LaunchCaps& caps, hipStrea
   const int total = a.qblocks * a.nkv * a.segs * a.splits;
   int grid = total;
   if (caps.max_wgs > 0) grid = std::min(grid, caps.max_wgs);
-  k_attn<T, HDP><<<grid, 256, 0, st>>>(a);
+  hipExtLaunchKernelGGL((k_attn<T, HDP>), dim3(grid), dim3(256), 0, st, caps.ev_start,
+                        caps.ev_stop, 0, a);
   if (a.splits > 1) {
     const long long n = (long long)a.qblocks * a.nkv * a.segs * ATT_BQ * HDP;
     int cg = (int)std::min<long long>((n + 255) / 256, 4096);
@@ -789,22 +940,44 @@ __global__ __launch_bounds__(256) void k_norm(float* __restrict__ x, int ldx, in
   const size_t pstride = (size_t)rows * d;
   for (int row = blockIdx.x; row < rows; row += gridDim.x) {
     float* xr = x + (size_t)row * ldx;
-    float v[NORM_NPT];
+    float v[NORM_NPT], add[NORM_NPT];
+#pragma unroll
+    for (int q = 0; q < NORM_NPT; ++q) {
+      const int i = threadIdx.x + q * 256;
+      v[q] = i < d ? xr[i] : 0.f;
+      add[q] = (bias && i < d) ? bias[i] : 0.f;
+    }
+    if (splits > 0) {
+      // partials in split order; four splits' loads are issued together
+      const float* pr = part + (size_t)row * d + threadIdx.x;
+      int sp = 0;
+      for (; sp + 4 <= splits; sp += 4) {
+        float t[4][NORM_NPT];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int q = 0; q < NORM_NPT; ++q)
+            t[u][q] = threadIdx.x + q * 256 < d ? pr[(sp + u) * pstride + q * 256] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int q = 0; q < NORM_NPT; ++q) add[q] += t[u][q];
+      }
+      for (; sp < splits; ++sp)
+#pragma unroll
+        for (int q = 0; q < NORM_NPT; ++q)
+          if (threadIdx.x + q * 256 < d) add[q] += pr[sp * pstride + q * 256];
+    }
     float s1 = 0.f;
 #pragma unroll
     for (int q = 0; q < NORM_NPT; ++q) {
       const int i = threadIdx.x + q * 256;
-      v[q] = 0.f;
       if (i < d) {
-        float t = xr[i];
         if (splits > 0) {
-          float add = bias ? bias[i] : 0.f;
-          for (int sp = 0; sp < splits; ++sp) add += part[sp * pstride + (size_t)row * d + i];
-          t += add;
-          xr[i] = t;
+          v[q] += add[q];
+          xr[i] = v[q];
         }
-        v[q] = t;
-        s1 += t;
+        s1 += v[q];
       }
     }
     const float mean = rms ? 0.f : block_sum(s1, red) / d;

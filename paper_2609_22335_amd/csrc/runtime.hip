@@ -100,7 +100,8 @@ static int validate(const vla_config* c) {
   if (c->lm_mlp % 16 || c->ex_mlp % 16) return bad("lm_mlp / ex_mlp must be multiples of 16");
   if (c->vit_dim % 8 || c->lm_dim % 8 || c->ex_dim % 8 || c->vit_mlp % 8)
     return bad("model widths must be multiples of 8");
-  if (c->ex_dim % 2) return bad("ex_dim must be even (sinusoid halves)");
+  if (c->ex_dim % 32) return bad("ex_dim must be a multiple of 32");
+  if (c->chunk_len > 64 || c->n_steps > 64) return bad("chunk_len and n_steps must be <= 64");
   return VLA_OK;
 }
 
@@ -135,7 +136,15 @@ struct DevTensor {
   size_t offset = 0;  // into the weight arena
   int rows = 0, ld = 0, dt = DT_F32;
   bool vec = false;  // fp32 vector: params sit at column offsets (row_off) of one row
-  size_t bytes() const { return (size_t)rows * ld * (dt == DT_BF16 ? 2 : 4); }
+  int fks = 0;       // > 0: MFMA fragment order with fks K-slabs per 16-row block
+  size_t bytes() const {
+    const size_t e = dt == DT_BF16 ? 2 : 4;
+    if (fks > 0) return (size_t)((rows + 31) / 32 * 32) * fks * frag_slab(dt) * e;
+    return (size_t)rows * ld * e;
+  }
+  size_t index(int r, int c) const {
+    return fks > 0 ? frag_index(r, c, fks, dt) : (size_t)r * ld + c;
+  }
 };
 
 struct ParamRec {
@@ -234,12 +243,13 @@ struct vla_model {
 
 static size_t dsz(int dt) { return dt == DT_BF16 ? 2 : 4; }
 
-static int add_tensor(vla_model* m, int rows, int ld, int dt, bool vec = false) {
+static int add_tensor(vla_model* m, int rows, int ld, int dt, bool vec = false, bool frag = false) {
   DevTensor t;
   t.rows = rows;
   t.ld = ld;
   t.dt = dt;
   t.vec = vec;
+  if (frag) t.fks = (ld + frag_slab(dt) - 1) / frag_slab(dt);
   m->T.push_back(t);
   return (int)m->T.size() - 1;
 }
@@ -251,9 +261,10 @@ static void add_param(vla_model* m, const std::string& name, int rows, int cols,
   m->P.push_back(p);
 }
 
-// Weight matrix [rows, cols] of the operand type, K padded to 8.
-static int add_mat(vla_model* m, const std::string& name, int rows, int cols) {
-  const int t = add_tensor(m, rows, rnd_up(cols, 8), m->dt);
+// Weight matrix [rows, cols] of the operand type, K padded to 8; `frag`
+// stores it in MFMA fragment order for the skinny (M <= 64) GEMM.
+static int add_mat(vla_model* m, const std::string& name, int rows, int cols, bool frag = false) {
+  const int t = add_tensor(m, rows, rnd_up(cols, 8), m->dt, false, frag);
   add_param(m, name, rows, cols, 0.0, t);
   return t;
 }
@@ -308,7 +319,7 @@ static void build_inventory(vla_model* m) {
       const std::string p = pre + std::to_string(l) + ".";
       DecLayer L{-1, -1, -1, -1, -1, -1};
       L.rms1 = add_vec(m, p + "rms1.g", dim, 1.0);
-      L.qkv = add_tensor(m, d.qkv_n, dim, m->dt);
+      L.qkv = add_tensor(m, d.qkv_n, dim, m->dt, false, !lm);
       add_param(m, p + "q.w", d.qd, dim, 0.0, L.qkv, MAP_ROPE, 0, c.head_dim);
       add_param(m, p + "k.w", d.kvd, dim, 0.0, L.qkv, MAP_ROPE, d.qd, c.head_dim);
       add_param(m, p + "v.w", d.kvd, dim, 0.0, L.qkv, MAP_IDENT, d.qd + d.kvd);
@@ -316,25 +327,25 @@ static void build_inventory(vla_model* m) {
         out.push_back(L);
         break;
       }
-      L.o = add_mat(m, p + "o.w", dim, d.qd);
+      L.o = add_mat(m, p + "o.w", dim, d.qd, !lm);
       L.rms2 = add_vec(m, p + "rms2.g", dim, 1.0);
-      L.gu = add_tensor(m, 2 * mlp, dim, m->dt);
+      L.gu = add_tensor(m, 2 * mlp, dim, m->dt, false, !lm);
       add_param(m, p + "gate.w", mlp, dim, 0.0, L.gu, MAP_GATE);
       add_param(m, p + "up.w", mlp, dim, 0.0, L.gu, MAP_UP);
-      L.down = add_mat(m, p + "down.w", dim, mlp);
+      L.down = add_mat(m, p + "down.w", dim, mlp, !lm);
       out.push_back(L);
     }
   };
   dec("lm.", c.lm_layers, c.lm_dim, c.lm_mlp, true, m->lm);
-  m->in_w = add_mat(m, "ex.in.w", c.ex_dim, c.action_dim);
+  m->in_w = add_mat(m, "ex.in.w", c.ex_dim, c.action_dim, true);
   m->in_b = add_vec(m, "ex.in.b", c.ex_dim);
-  m->t1_w = add_mat(m, "ex.time1.w", c.ex_dim, 2 * c.ex_dim);
+  m->t1_w = add_mat(m, "ex.time1.w", c.ex_dim, 2 * c.ex_dim, true);
   m->t1_b = add_vec(m, "ex.time1.b", c.ex_dim);
-  m->t2_w = add_mat(m, "ex.time2.w", c.ex_dim, c.ex_dim);
+  m->t2_w = add_mat(m, "ex.time2.w", c.ex_dim, c.ex_dim, true);
   m->t2_b = add_vec(m, "ex.time2.b", c.ex_dim);
   dec("ex.", c.ex_layers, c.ex_dim, c.ex_mlp, false, m->ex);
   m->fin_g = add_vec(m, "ex.final.g", c.ex_dim, 1.0);
-  m->out_w = add_mat(m, "ex.out.w", c.action_dim, c.ex_dim);
+  m->out_w = add_mat(m, "ex.out.w", c.action_dim, c.ex_dim, true);
   m->out_b = add_vec(m, "ex.out.b", c.action_dim);
 }
 
@@ -350,14 +361,15 @@ static int upload_tensor(vla_model* m, int t, const std::vector<int>& params) {
     gen_normal(m->seed, p.name.c_str(), n, p.mean, p.stdv, vals.data());
     const bool vec = dt.vec;
     for (int r = 0; r < p.rows; ++r) {
-      const size_t base = vec ? (size_t)p.row_off : (size_t)dev_row(p, r) * dt.ld;
+      const int pr = vec ? 0 : dev_row(p, r);
       for (int col = 0; col < p.cols; ++col) {
+        const size_t at = vec ? (size_t)p.row_off + col : dt.index(pr, col);
         float v = vals[(size_t)r * p.cols + col];
         if (m->dt == DT_BF16) v = bf16_value(bf16_bits(v));  // the model stores bf16 values
         if (dt.dt == DT_BF16)
-          ((uint16_t*)img.data())[base + col] = bf16_bits(v);
+          ((uint16_t*)img.data())[at] = bf16_bits(v);
         else
-          ((float*)img.data())[base + col] = v;
+          ((float*)img.data())[at] = v;
       }
     }
   }
@@ -384,34 +396,43 @@ struct Run {
   const Scratch* scr;
 };
 
-static int timer_begin(const Run& r, const char* tag, hipEvent_t* end) {
+// Kernel timer: a launch whose tag matches gets a pair of events that its
+// main kernel records at its own start and end.
+static int timer_events(const Run& r, const char* tag, LaunchCaps* caps) {
   vla_model* m = r.m;
-  *end = nullptr;
   if (m->timer_tag.empty() || m->timer_tag != tag) return VLA_OK;
   while (m->timer_ev.size() < m->timer_used + 2) {
     hipEvent_t e;
     HIP_TRY(hipEventCreate(&e));
     m->timer_ev.push_back(e);
   }
-  HIP_TRY(hipEventRecord(m->timer_ev[m->timer_used], r.st));
-  *end = m->timer_ev[m->timer_used + 1];
+  caps->ev_start = m->timer_ev[m->timer_used];
+  caps->ev_stop = m->timer_ev[m->timer_used + 1];
   m->timer_used += 2;
   return VLA_OK;
 }
 
-static int timer_end(const Run& r, hipEvent_t end) {
-  if (end) HIP_TRY(hipEventRecord(end, r.st));
-  return VLA_OK;
+// C = A W[:, koff : koff + K]^T with the epilogue e; W is a weight tensor id.
+static GemmDesc gemm_desc(vla_model* m, const void* A, int lda, int W, int M, int N, int K,
+                          const Epi& e, int koff = 0) {
+  const DevTensor& t = m->T[W];
+  GemmDesc g{m->dt, A, lda, m->tptr(W), t.ld, M, N, K, e};
+  if (t.fks > 0) {
+    g.frag_ks = t.fks;
+    g.frag_ks0 = koff / frag_slab(m->dt);
+  } else {
+    g.W = m->tptr(W) + (size_t)koff * m->esz;
+  }
+  return g;
 }
 
 static int gemm(const Run& r, const char* tag, const void* A, int lda, int W, int M, int N, int K,
-                const Epi& e, const void* Wptr = nullptr, int ldw = 0) {
+                const Epi& e, int koff = 0) {
   vla_model* m = r.m;
-  GemmDesc g{m->dt, A, lda, Wptr ? Wptr : m->tptr(W), Wptr ? ldw : m->T[W].ld, M, N, K, e};
-  hipEvent_t tend;
-  VLA_TRY(timer_begin(r, tag, &tend));
-  hipError_t err = launch_gemm(g, *r.scr, r.caps, r.st);
-  if (err == hipSuccess) VLA_TRY(timer_end(r, tend));
+  const GemmDesc g = gemm_desc(m, A, lda, W, M, N, K, e, koff);
+  LaunchCaps caps = r.caps;
+  VLA_TRY(timer_events(r, tag, &caps));
+  hipError_t err = launch_gemm(g, *r.scr, caps, r.st);
   if (err != hipSuccess)
     return fail(VLA_EHIP, std::string("gemm ") + std::to_string(M) + "x" + std::to_string(N) + "x" +
                               std::to_string(K) + ": " + hipGetErrorString(err));
@@ -419,10 +440,9 @@ static int gemm(const Run& r, const char* tag, const void* A, int lda, int W, in
 }
 
 static int attn(const Run& r, const char* tag, const AttnDesc& a) {
-  hipEvent_t tend;
-  VLA_TRY(timer_begin(r, tag, &tend));
-  hipError_t err = launch_attention(a, *r.scr, r.caps, r.st);
-  if (err == hipSuccess) VLA_TRY(timer_end(r, tend));
+  LaunchCaps caps = r.caps;
+  VLA_TRY(timer_events(r, tag, &caps));
+  hipError_t err = launch_attention(a, *r.scr, caps, r.st);
   if (err != hipSuccess) return fail(VLA_EHIP, std::string("attention: ") + hipGetErrorString(err));
   return VLA_OK;
 }
@@ -447,8 +467,7 @@ static int gemm_part(const Run& r, const char* tag, const void* A, int lda, int 
   e.kind = EPI_PART;
   e.out = r.scr->ptr;
   e.ldo = (int)std::min<size_t>(r.scr->floats, (size_t)INT32_MAX);
-  GemmDesc g{m->dt, A, lda, m->tptr(W), m->T[W].ld, M, N, K, e};
-  *splits = plan_gemm(g).splits;
+  *splits = plan_gemm(gemm_desc(m, A, lda, W, M, N, K, e)).splits;
   return gemm(r, tag, A, lda, W, M, N, K, e);
 }
 
@@ -633,9 +652,10 @@ struct ScratchNeed {
   size_t floats = 0;
 };
 
-static ScratchNeed gemm_scratch(int dt, int M, int N, int K, bool part = false) {
+static ScratchNeed gemm_scratch(int dt, int M, int N, int K, bool part = false, bool frag = false) {
   GemmDesc g{dt, nullptr, K, nullptr, K, M, N, K, Epi()};
   if (part) g.epi.kind = EPI_PART;
+  if (frag) g.frag_ks = (K + frag_slab(dt) - 1) / frag_slab(dt);
   const GemmPlan p = plan_gemm(g);
   return ScratchNeed{p.scratch_floats};
 }
@@ -745,14 +765,14 @@ static int setup_workspaces(vla_model* m) {
   VLA_TRY(dmalloc(m, &a.att, (size_t)H * d.qd * e));
   VLA_TRY(dmalloc(m, &a.mlp, (size_t)H * c.ex_mlp * e));
   ScratchNeed sa;
-  upd(sa, gemm_scratch(dt, H, de, d.a_pad));
-  upd(sa, gemm_scratch(dt, H, de, de));
-  upd(sa, gemm_scratch(dt, c.n_steps, de, de));
-  upd(sa, gemm_scratch(dt, H, d.qkv_n, de));
-  upd(sa, gemm_scratch(dt, H, de, d.qd, true));
-  upd(sa, gemm_scratch(dt, H, 2 * c.ex_mlp, de));
-  upd(sa, gemm_scratch(dt, H, de, c.ex_mlp, true));
-  upd(sa, gemm_scratch(dt, H, c.action_dim, de));
+  upd(sa, gemm_scratch(dt, H, de, d.a_pad, false, true));
+  upd(sa, gemm_scratch(dt, H, de, de, false, true));
+  upd(sa, gemm_scratch(dt, c.n_steps, de, de, false, true));
+  upd(sa, gemm_scratch(dt, H, d.qkv_n, de, false, true));
+  upd(sa, gemm_scratch(dt, H, de, d.qd, true, true));
+  upd(sa, gemm_scratch(dt, H, 2 * c.ex_mlp, de, false, true));
+  upd(sa, gemm_scratch(dt, H, de, c.ex_mlp, true, true));
+  upd(sa, gemm_scratch(dt, H, c.action_dim, de, false, true));
   upd(sa, attn_scratch(dt, H, c.lm_heads, c.lm_kv_heads, c.head_dim, P, H, 1));
   VLA_TRY(alloc_scratch(m, sa, &a.scr));
   return VLA_OK;
@@ -794,8 +814,8 @@ static int create_impl(const vla_config* cfg, uint64_t seed, vla_model** out) {
     // c_k = W_2[:, d_e:] phi(t_k) + b_2 for every step (depends on the step only)
     Run r{m.get(), nullptr, LaunchCaps{}, &m->aw.scr};
     const int de = m->c.ex_dim;
-    rc = gemm(r, "ex.ck", m->phi, de, -1, m->c.n_steps, de, de, epi_kind(EPI_F32, m->ck, de, m->f32(m->t1_b)),
-              m->tptr(m->t1_w) + (size_t)de * m->esz, m->T[m->t1_w].ld);
+    rc = gemm(r, "ex.ck", m->phi, de, m->t1_w, m->c.n_steps, de, de,
+              epi_kind(EPI_F32, m->ck, de, m->f32(m->t1_b)), de);
   }
   if (rc == VLA_OK) {
     hipError_t se = hipDeviceSynchronize();
@@ -1062,10 +1082,12 @@ int vla_export_param(vla_model* m, const char* name, float* host_dst, int64_t nu
     HIP_TRY(hipMemcpy(img.data(), m->tptr(p.tensor), img.size(), hipMemcpyDeviceToHost));
     const bool vec = t.vec;
     for (int r = 0; r < p.rows; ++r) {
-      const size_t base = vec ? (size_t)p.row_off : (size_t)dev_row(p, r) * t.ld;
-      for (int col = 0; col < p.cols; ++col)
-        host_dst[(size_t)r * p.cols + col] = t.dt == DT_BF16 ? bf16_value(((uint16_t*)img.data())[base + col])
-                                                             : ((float*)img.data())[base + col];
+      const int pr = vec ? 0 : dev_row(p, r);
+      for (int col = 0; col < p.cols; ++col) {
+        const size_t at = vec ? (size_t)p.row_off + col : t.index(pr, col);
+        host_dst[(size_t)r * p.cols + col] = t.dt == DT_BF16 ? bf16_value(((uint16_t*)img.data())[at])
+                                                             : ((float*)img.data())[at];
+      }
     }
     return VLA_OK;
   })
