@@ -85,7 +85,12 @@ typedef struct vla_sched {
   int32_t act_cus;    /* CU_MASKED: CUs for the action stream (multiple of 8); the  */
                       /*   two sets are disjoint and together at most the CU count   */
   int32_t vlm_wg_cap; /* WG_CAPPED: max VLM workgroups per CU in flight (>= 1)       */
-  int32_t reserved[4];
+  int32_t act_streams;/* action streams (0 or 1: one; at most 4). With k > 1 the     */
+                      /*   action phases of k consecutive frames (different robots)  */
+                      /*   run concurrently on k streams; not with VLA_MODE_SERIAL   */
+  int32_t graphs;     /* 1: replay each phase as a captured HIP graph (captured on   */
+                      /*   first use and cached per context / action stream)         */
+  int32_t reserved[2];
 } vla_sched;
 
 typedef struct vla_timing {
@@ -117,9 +122,10 @@ int vla_create(const vla_config* cfg, uint64_t seed, vla_model** out);
 /* Free everything the model owns (waits for its streams). NULL is a no-op. */
 int vla_destroy(vla_model* m);
 
-/* Phase-1 -> phase-2 hand-off: the per-layer KV cache [lm_layers][prefix]
- * [lm_kv_heads * head_dim] of the model's storage type. Caller-owned via
- * these two calls; destroy NULL is a no-op. */
+/* Phase-1 -> phase-2 hand-off: the per-layer KV cache of the model's storage
+ * type, K [lm_layers][prefix][lm_kv_heads * head_dim] and V transposed
+ * [lm_layers][lm_kv_heads * head_dim][prefix rounded up to 32]. Caller-owned
+ * via these two calls; destroy NULL is a no-op. */
 int vla_ctx_create(vla_model* m, vla_ctx** out);
 int vla_ctx_destroy(vla_ctx* c);
 
@@ -140,8 +146,10 @@ int vla_action_denoise(vla_model* m, const vla_ctx* ctx, const float* noise, flo
  * host array of R vla_frame (device pointers inside); noise: device fp32
  * [R, chunk_len, action_dim]; actions: device fp32 [R, chunk_len,
  * action_dim]. The VLM prefill of frame r+1 overlaps the action phase of
- * frame r (two model-owned contexts, events between the streams) except in
- * VLA_MODE_SERIAL. Results are bit-identical across modes. t may be NULL. */
+ * frame r (a ring of act_streams + 1 model-owned contexts, events between the
+ * streams) except in VLA_MODE_SERIAL. Results are bit-identical across
+ * modes, action-stream counts and graph replay. t may be NULL. Calls on one
+ * model are serialised. */
 int vla_pipeline_run(vla_model* m, const vla_frame* frames, const float* noise, int32_t R,
                      const vla_sched* sched, float* actions, vla_timing* t);
 
@@ -173,6 +181,15 @@ int vla_debug_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* A
 int vla_debug_attention(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int32_t hd,
                         const void* q, const void* k0, const void* v0, int32_t S0, const void* k1,
                         const void* v1, int32_t S1, void* out, void* stream);
+
+/* Test entry point for the attention kernel of the LM and the expert: as
+ * vla_debug_attention, but V is passed transposed and zero-padded: vt0
+ * [nkv*hd][ldvt0 >= S0 rounded up to 32], vt1 [nkv*hd][ldvt1 >= S1 rounded
+ * up to 32] (padding columns must hold zeros). All pointers device. */
+int vla_debug_attention_vt(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int32_t hd,
+                           const void* q, const void* k0, const void* vt0, int32_t S0, int32_t ldvt0,
+                           const void* k1, const void* vt1, int32_t S1, int32_t ldvt1, void* out,
+                           void* stream);
 
 /* Kernel timer for measurement: while `tag` is set, every launch of the
  * kernels behind that call site (tags: "vit.patch", "vit.qkv", "vit.attn",

@@ -44,7 +44,8 @@ class vla_frame(ctypes.Structure):
 
 class vla_sched(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int32), ("vlm_cus", ctypes.c_int32), ("act_cus", ctypes.c_int32),
-                ("vlm_wg_cap", ctypes.c_int32), ("reserved", ctypes.c_int32 * 4)]
+                ("vlm_wg_cap", ctypes.c_int32), ("act_streams", ctypes.c_int32), ("graphs", ctypes.c_int32),
+                ("reserved", ctypes.c_int32 * 2)]
 
 
 class vla_timing(ctypes.Structure):
@@ -82,6 +83,7 @@ def _load():
         "vla_debug_gemm": [I32, I32, I32, I32, P, I32, P, I32, P, P, P],
         "vla_debug_attention": [I32, I32, I32, I32, I32, P, P, P, I32, P, P, I32, P, P],
         "vla_debug_generate": [U64, ctypes.c_char_p, I64, D, D, P],
+        "vla_debug_attention_vt": [I32, I32, I32, I32, I32, P, P, P, I32, I32, P, P, I32, I32, P, P],
         "vla_kernel_timer": [P, ctypes.c_char_p],
         "vla_kernel_timer_read": [P, ctypes.POINTER(D), ctypes.POINTER(I64)],
     }
@@ -162,9 +164,11 @@ def vla_action_denoise(model: int, ctx: int, noise, actions, stream: int = 0) ->
 
 
 def vla_pipeline_run(model: int, frames: Sequence[vla_frame], noise, R: int, mode="serial",
-                     vlm_cus: int = 0, act_cus: int = 0, vlm_wg_cap: int = 0, actions=None) -> Dict[str, float]:
+                     vlm_cus: int = 0, act_cus: int = 0, vlm_wg_cap: int = 0, actions=None,
+                     act_streams: int = 1, graphs: bool = False) -> Dict[str, float]:
     arr = (vla_frame * len(frames))(*frames)
-    s = vla_sched(MODES[mode] if isinstance(mode, str) else int(mode), vlm_cus, act_cus, vlm_wg_cap)
+    s = vla_sched(MODES[mode] if isinstance(mode, str) else int(mode), vlm_cus, act_cus, vlm_wg_cap,
+                  act_streams, 1 if graphs else 0)
     t = vla_timing()
     _check(_lib.vla_pipeline_run(model, arr, _ptr(noise), int(R), ctypes.byref(s), _ptr(actions),
                                  ctypes.byref(t)))
@@ -209,6 +213,12 @@ def vla_debug_attention(dtype: int, Sq: int, nq: int, nkv: int, hd: int, q, k0, 
                                     _ptr(k1), _ptr(v1), S1, _ptr(out), stream or None))
 
 
+def vla_debug_attention_vt(dtype: int, Sq: int, nq: int, nkv: int, hd: int, q, k0, vt0, S0: int,
+                           ldvt0: int, k1, vt1, S1: int, ldvt1: int, out, stream: int = 0) -> None:
+    _check(_lib.vla_debug_attention_vt(dtype, Sq, nq, nkv, hd, _ptr(q), _ptr(k0), _ptr(vt0), S0, ldvt0,
+                                       _ptr(k1), _ptr(vt1), S1, ldvt1, _ptr(out), stream or None))
+
+
 def vla_kernel_timer(model: int, tag: Optional[str]) -> None:
     _check(_lib.vla_kernel_timer(model, tag.encode() if tag else None))
 
@@ -231,5 +241,6 @@ def exported_symbols() -> Iterable[str]:
     return ["vla_preset", "vla_validate", "vla_create", "vla_destroy", "vla_ctx_create",
             "vla_ctx_destroy", "vla_vlm_prefill", "vla_action_denoise", "vla_pipeline_run",
             "vla_param_count", "vla_param_info", "vla_export_param", "vla_ctx_export_kv",
-            "vla_debug_gemm", "vla_debug_attention", "vla_debug_generate", "vla_kernel_timer",
+            "vla_debug_gemm", "vla_debug_attention", "vla_debug_attention_vt", "vla_debug_generate",
+            "vla_kernel_timer",
             "vla_kernel_timer_read", "vla_last_error"]

@@ -40,6 +40,7 @@ struct Epi {
   void* k = nullptr;
   void* v = nullptr;
   int ldkv = 0;
+  int ldvt = 0;  // > 0: V is stored transposed, element (m, c) at v[c * ldvt + m]
   int nq = 0, nkv = 0, hd = 0, pos0 = 0;
   const float* rope_cos = nullptr;  // [pos][hd/2]
   const float* rope_sin = nullptr;
@@ -115,6 +116,27 @@ struct AttnDesc {
 };
 
 size_t attn_scratch_floats(const AttnDesc& a);
+
+// Attention over keys [k0 (S0 rows); k1 (S1 rows)] with V stored transposed:
+// vt0 [n_kv * hd][ldvt0 >= round32(S0)], vt1 [n_kv * hd][ldvt1 >= round32(S1)],
+// padding columns zero. K rows have ldk elements (head j at column j * hd).
+// q and out as in AttnDesc (one segment). No scratch.
+struct AttnVtDesc {
+  int dtype;
+  const void* q;
+  int ldq;
+  const void* k0;
+  const void* vt0;
+  int S0, ldvt0;
+  const void* k1;
+  const void* vt1;
+  int S1, ldvt1;
+  int ldk;
+  void* out;
+  int ldo;
+  int Sq, nq, nkv, hd;
+};
+hipError_t launch_attention_vt(const AttnVtDesc& d, const LaunchCaps& caps, hipStream_t st);
 hipError_t launch_attention(const AttnDesc& a, const Scratch& s, const LaunchCaps& caps, hipStream_t st);
 
 // Residual add + row norm: x[m] += bias + sum_s part[s][m] in split order

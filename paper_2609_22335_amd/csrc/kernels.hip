@@ -63,6 +63,29 @@ __device__ __forceinline__ f32x4 mfma_step(uint4 a, uint4 b, f32x4 c, float) {
   return c;
 }
 
+// Masked loads go through buffer resources: a byte offset at or past the
+// resource's range returns zero in hardware, so a masked lane just gets an
+// out-of-range offset and no branch is needed. (A predicated pointer load
+// would become a branch, and the compiler drains every outstanding load at
+// such joins, which serialises memory traffic.)
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+constexpr uint32_t OOB = 0x80000000u;
+
+__device__ __forceinline__ Rsrc rsrc(const void* base, size_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0,
+                                           (int)(bytes < 0x7FFFFFFFu ? bytes : 0x7FFFFFFFu), 0x00020000);
+}
+// bytes spanned by `rows` rows of `len` elements at row stride `ld`
+__device__ __forceinline__ size_t span(int rows, size_t ld, int len, size_t esz) {
+  return rows > 0 ? ((size_t)(rows - 1) * ld + len) * esz : 0;
+}
+__device__ __forceinline__ uint4 bld16(Rsrc r, uint32_t off) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+__device__ __forceinline__ float bld1(Rsrc r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
+}
+
 // ---------------------------------------------------------------------------
 // GEMM epilogues
 // ---------------------------------------------------------------------------
@@ -135,9 +158,15 @@ __device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int 
       TT<T>::st(dst + i + hd / 2, v1 * c + v0 * s);
     } else {
       const int c0 = n - qcols - kcols;
-      T* dst = (T*)e.v + (size_t)m * e.ldkv;
-      TT<T>::st(dst + c0, v0);
-      TT<T>::st(dst + c0 + 16, v1);
+      if (e.ldvt > 0) {
+        T* dst = (T*)e.v + m;
+        TT<T>::st(dst + (size_t)c0 * e.ldvt, v0);
+        TT<T>::st(dst + (size_t)(c0 + 16) * e.ldvt, v1);
+      } else {
+        T* dst = (T*)e.v + (size_t)m * e.ldkv;
+        TT<T>::st(dst + c0, v0);
+        TT<T>::st(dst + c0 + 16, v1);
+      }
     }
     return;
   }
@@ -193,6 +222,8 @@ __global__ __launch_bounds__(256) void k_gemm(const T* __restrict__ A, int lda,
   const int wm = wave >> 1, wn = wave & 1;
   const int ntiles = tiles_m * tiles_n * splits;
   const T dummy = T();
+  const Rsrc ra_r = rsrc(A, span(M, lda, K, sizeof(T)));
+  const Rsrc rb_r = rsrc(W, span(N, ldw, K, sizeof(T)));
 
   for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int s = tile % splits;
@@ -214,15 +245,15 @@ __global__ __launch_bounds__(256) void k_gemm(const T* __restrict__ A, int lda,
       for (int i = 0; i < AV; ++i) {
         const int c = tid + i * 256, r = c / KV, kc = (c % KV) * VEC;
         const int gm = m0 + r, gk = k0 + kc;
-        ra[i] = (gm < M && gk < kend) ? *(const uint4*)(A + (size_t)gm * lda + gk)
-                                      : make_uint4(0, 0, 0, 0);
+        const bool ok = gm < M && gk < kend;
+        ra[i] = bld16(ra_r, ok ? (uint32_t)(((size_t)gm * lda + gk) * sizeof(T)) : OOB);
       }
 #pragma unroll
       for (int i = 0; i < BV; ++i) {
         const int c = tid + i * 256, r = c / KV, kc = (c % KV) * VEC;
         const int gn = n0 + r, gk = k0 + kc;
-        rb[i] = (gn < N && gk < kend) ? *(const uint4*)(W + (size_t)gn * ldw + gk)
-                                      : make_uint4(0, 0, 0, 0);
+        const bool ok = gn < N && gk < kend;
+        rb[i] = bld16(rb_r, ok ? (uint32_t)(((size_t)gn * ldw + gk) * sizeof(T)) : OOB);
       }
     };
     auto sstore = [&](int buf) {
@@ -350,6 +381,8 @@ __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, int lda
   const int nslab = (K + SW - 1) / SW;
   const int total = npairs * splits;
   const T dummy = T();
+  const Rsrc rw = rsrc(Wf, (size_t)npairs * 2 * KS * 64 * VEC * sizeof(T));
+  const Rsrc ra = rsrc(A, span(M, lda, K, sizeof(T)));
   for (int w = blockIdx.x; w < total; w += gridDim.x) {
     const int s = w % splits, np = w / splits;
     const int sb = (s * 4 + wave) * SPW;
@@ -360,14 +393,14 @@ __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, int lda
       const bool ok = ks < nslab;
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
-        bf[q][nb] = ok ? *(const uint4*)(Wf + ((size_t)((2 * np + nb) * KS + ks0 + ks) * 64 + lane) * VEC)
-                       : make_uint4(0, 0, 0, 0);
+        bf[q][nb] = bld16(rw, ok ? (uint32_t)((((size_t)(2 * np + nb) * KS + ks0 + ks) * 64 + lane) * VEC * sizeof(T))
+                                 : OOB);
       const int k = ks * SW + (lane >> 4) * VEC;
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt) {
         const int row = mt * 16 + (lane & 15);
-        af[q][mt] = (ok && row < M && k < K) ? *(const uint4*)(A + (size_t)row * lda + k)
-                                             : make_uint4(0, 0, 0, 0);
+        const bool oka = ok && row < M && k < K;
+        af[q][mt] = bld16(ra, oka ? (uint32_t)(((size_t)row * lda + k) * sizeof(T)) : OOB);
       }
     }
     f32x4 acc[2][4];
@@ -616,10 +649,15 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     const int seg = t / a.nkv;
 
     const T* Q = (const T*)a.q + seg * a.seg_q;
-    const T* K0 = (const T*)a.k0 + seg * a.seg_kv + j * a.hd;
-    const T* V0 = (const T*)a.v0 + seg * a.seg_kv + j * a.hd;
-    const T* K1 = a.k1 ? (const T*)a.k1 + seg * a.seg_kv + j * a.hd : nullptr;
-    const T* V1 = a.v1 ? (const T*)a.v1 + seg * a.seg_kv + j * a.hd : nullptr;
+    const T* K0 = (const T*)a.k0 + seg * a.seg_kv;
+    const T* V0 = (const T*)a.v0 + seg * a.seg_kv;
+    const T* K1 = a.k1 ? (const T*)a.k1 + seg * a.seg_kv : K0;
+    const T* V1 = a.v1 ? (const T*)a.v1 + seg * a.seg_kv : V0;
+    const Rsrc rq = rsrc(Q, span(a.Sq, a.ldq, a.nq * a.hd, sizeof(T)));
+    const Rsrc rk0 = rsrc(K0, span(a.S0, a.ldkv, a.nkv * a.hd, sizeof(T)));
+    const Rsrc rv0 = rsrc(V0, span(a.S0, a.ldkv, a.nkv * a.hd, sizeof(T)));
+    const Rsrc rk1 = rsrc(K1, span(a.S1, a.ldkv, a.nkv * a.hd, sizeof(T)));
+    const Rsrc rv1 = rsrc(V1, span(a.S1, a.ldkv, a.nkv * a.hd, sizeof(T)));
 
     // Q fragments of this lane's packed row (A-operand layout).
     uint4 qf[NQF];
@@ -629,8 +667,8 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
 #pragma unroll
       for (int ks = 0; ks < NQF; ++ks) {
         const int d = ks * SW + (lane >> 4) * VEC;
-        qf[ks] = (r < R && d < a.hd) ? *(const uint4*)(Q + (size_t)sq * a.ldq + h * a.hd + d)
-                                     : make_uint4(0, 0, 0, 0);
+        const bool ok = r < R && d < a.hd;
+        qf[ks] = bld16(rq, ok ? (uint32_t)(((size_t)sq * a.ldq + h * a.hd + d) * sizeof(T)) : OOB);
       }
     }
 
@@ -651,13 +689,13 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       for (int c = tid; c < NV; c += 256) {
         const int kk = c / (HDP / VEC), d = (c % (HDP / VEC)) * VEC;
         const int key = b * ATT_BKV + kk;
-        uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-        if (key < Skv && d < a.hd) {
-          const T* kp = key < a.S0 ? K0 + (size_t)key * a.ldkv : K1 + (size_t)(key - a.S0) * a.ldkv;
-          const T* vp = key < a.S0 ? V0 + (size_t)key * a.ldkv : V1 + (size_t)(key - a.S0) * a.ldkv;
-          kv = *(const uint4*)(kp + d);
-          vv = *(const uint4*)(vp + d);
-        }
+        const bool ok = key < Skv && d < a.hd;
+        const bool s0 = key < a.S0;
+        const uint32_t off = ok ? (uint32_t)(((size_t)(s0 ? key : key - a.S0) * a.ldkv + j * a.hd + d) *
+                                             sizeof(T))
+                                : OOB;
+        const uint4 kv = s0 ? bld16(rk0, off) : bld16(rk1, off);
+        const uint4 vv = s0 ? bld16(rv0, off) : bld16(rv1, off);
         *(uint4*)(sK + kk * KS + d) = kv;
         const T* ve = (const T*)&vv;
 #pragma unroll
@@ -910,6 +948,293 @@ hipError_t launch_attention(const AttnDesc& d, const Scratch& s, const LaunchCap
 }
 
 // ---------------------------------------------------------------------------
+// Attention with K and V read straight into MFMA registers (no LDS staging):
+// K row-major [keys][ldk] and V transposed [n_kv * hd][ldvt] (keys
+// contiguous per head-dim column, padded to a multiple of 32 keys with zeros
+// so 16-byte loads stay aligned). The key space is [segment 0 padded to a
+// multiple of 32; segment 1 padded likewise]; keys past a segment's length
+// get a -inf score. A workgroup owns 16 packed query rows (row r <-> query
+// r / group, head r % group of one KV head); its four waves take every
+// fourth 32-key block, with the next block's K and V prefetched into
+// registers, and keep an fp32 online softmax. P V runs on MFMA with P split
+// into bf16 high and remainder parts (bf16) or directly (fp32). The four
+// waves' (max, sum, O) are merged through LDS in wave order.
+// ---------------------------------------------------------------------------
+
+struct Attn2Args {
+  const void* q;
+  const void* k0;
+  const void* vt0;
+  const void* k1;
+  const void* vt1;
+  void* out;
+  int ldq, ldk, ldvt0, ldvt1, ldo;
+  int Sq, nq, nkv, hd, S0, S1;
+  int rtiles;  // 16-row tiles of packed rows per KV head
+  float scale_log2;
+};
+
+template <typename T, int HDP>
+__global__ __launch_bounds__(256) void k_attn2(Attn2Args a) {
+  constexpr int VEC = 16 / sizeof(T);
+  constexpr int SW = 4 * VEC;
+  constexpr int NQF = HDP / SW;   // Q fragments (also K fragments per 16-key tile)
+  constexpr int NOT = HDP / 16;   // output column tiles
+  constexpr int PVS = 32 / SW;    // P V slabs per 32-key block
+  constexpr int PS = 36;          // sP row stride
+  constexpr int OS = HDP + 4;     // sO row stride
+  __shared__ __attribute__((aligned(16))) float sP[4][16 * PS];
+  __shared__ float sO[4][16 * OS];
+  __shared__ float sM[4][16], sL[4][16];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int group = a.nq / a.nkv;
+  const int R = a.Sq * group;
+  const int S0p = (a.S0 + 31) / 32 * 32, S1p = (a.S1 + 31) / 32 * 32;
+  const int nblk = (S0p + S1p) / 32;
+  const int total = a.rtiles * a.nkv;
+  const T dummy = T();
+
+  for (int w = blockIdx.x; w < total; w += gridDim.x) {
+    const int rt = w % a.rtiles, j = w / a.rtiles;
+    const Rsrc rq = rsrc(a.q, span(a.Sq, a.ldq, a.nq * a.hd, sizeof(T)));
+    const Rsrc rk0 = rsrc(a.k0, span(a.S0, a.ldk, a.nkv * a.hd, sizeof(T)));
+    const Rsrc rv0 = rsrc(a.vt0, (size_t)a.nkv * a.hd * a.ldvt0 * sizeof(T));
+    const Rsrc rk1 = rsrc(a.k1 ? a.k1 : a.k0, a.k1 ? span(a.S1, a.ldk, a.nkv * a.hd, sizeof(T)) : 0);
+    const Rsrc rv1 = rsrc(a.vt1 ? a.vt1 : a.vt0, a.vt1 ? (size_t)a.nkv * a.hd * a.ldvt1 * sizeof(T) : 0);
+
+    uint4 qf[NQF];
+    {
+      const int r = rt * 16 + (lane & 15);
+      const int sq = r / group, h = j * group + r % group;
+#pragma unroll
+      for (int ks = 0; ks < NQF; ++ks) {
+        const int d = ks * SW + (lane >> 4) * VEC;
+        const bool ok = r < R && d < a.hd;
+        qf[ks] = bld16(rq, ok ? (uint32_t)(((size_t)sq * a.ldq + h * a.hd + d) * sizeof(T)) : OOB);
+      }
+    }
+
+    // fragment loads of one 32-key block
+    auto load_k = [&](int b, uint4 (&kf)[2][NQF]) {
+      const int kb = b * 32;
+      const bool seg1 = kb >= S0p;
+      const int kloc = seg1 ? kb - S0p : kb;
+      const int slen = seg1 ? a.S1 : a.S0;
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) {
+        const int key = kloc + nt * 16 + (lane & 15);
+#pragma unroll
+        for (int ks = 0; ks < NQF; ++ks) {
+          const int d = ks * SW + (lane >> 4) * VEC;
+          const bool ok = key < slen && d < a.hd;
+          const uint32_t off = ok ? (uint32_t)(((size_t)key * a.ldk + j * a.hd + d) * sizeof(T)) : OOB;
+          kf[nt][ks] = seg1 ? bld16(rk1, off) : bld16(rk0, off);
+        }
+      }
+    };
+    auto load_v = [&](int b, uint4 (&vf)[NOT][PVS]) {
+      const int kb = b * 32;
+      const bool seg1 = kb >= S0p;
+      const int ldvt = seg1 ? a.ldvt1 : a.ldvt0;
+      const int kloc = seg1 ? kb - S0p : kb;
+#pragma unroll
+      for (int dt = 0; dt < NOT; ++dt) {
+        const int d = dt * 16 + (lane & 15);
+#pragma unroll
+        for (int kk = 0; kk < PVS; ++kk) {
+          const int key = kloc + kk * SW + (lane >> 4) * VEC;
+          const bool ok = d < a.hd;
+          const uint32_t off = ok ? (uint32_t)(((size_t)(j * a.hd + d) * ldvt + key) * sizeof(T)) : OOB;
+          vf[dt][kk] = seg1 ? bld16(rv1, off) : bld16(rv0, off);
+        }
+      }
+    };
+
+    float mrow[4], lrow[4];
+    f32x4 o[NOT];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      mrow[r] = -INFINITY;
+      lrow[r] = 0.f;
+    }
+#pragma unroll
+    for (int d = 0; d < NOT; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    float* myP = sP[wave];
+    // one 32-key block: scores, online softmax, P through LDS, P V
+    // The next block's K is requested as soon as the scores are formed and its V
+    // as soon as P V is done, so loads overlap the rest of the block.
+    uint4 kf[2][NQF], vf[NOT][PVS];
+    auto process = [&](int b) {
+      const int kb = b * 32;
+      const bool seg1 = kb >= S0p;
+      const int kloc = seg1 ? kb - S0p : kb;
+      const int slen = seg1 ? a.S1 : a.S0;
+      f32x4 sacc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+        for (int ks = 0; ks < NQF; ++ks) sacc[nt] = mfma_step(qf[ks], kf[nt][ks], sacc[nt], dummy);
+      if (b + 4 < nblk) load_k(b + 4, kf);
+      float p[2][4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float mx = -INFINITY;
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          const int key = kloc + nt * 16 + (lane & 15);
+          const float sv = key < slen ? sacc[nt][r] * a.scale_log2 : -INFINITY;
+          p[nt][r] = sv;
+          mx = fmaxf(mx, sv);
+        }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+        const float mnew = fmaxf(mrow[r], mx);
+        // a block can be entirely padding: keep everything at zero then
+        const float alpha = mnew == -INFINITY ? 1.f : exp2f(mrow[r] - mnew);
+        float sum = 0.f;
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) {
+          p[nt][r] = mnew == -INFINITY ? 0.f : exp2f(p[nt][r] - mnew);
+          sum += p[nt][r];
+        }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off);
+        lrow[r] = lrow[r] * alpha + sum;
+        mrow[r] = mnew;
+#pragma unroll
+        for (int d = 0; d < NOT; ++d) o[d][r] *= alpha;
+      }
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) myP[((lane >> 4) * 4 + r) * PS + nt * 16 + (lane & 15)] = p[nt][r];
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
+      __builtin_amdgcn_wave_barrier();
+#pragma unroll
+      for (int kk = 0; kk < PVS; ++kk) {
+        const float* pr = myP + (lane & 15) * PS + kk * SW + (lane >> 4) * VEC;
+        if constexpr (sizeof(T) == 2) {
+          uint32_t hi[4], lo[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float x0 = pr[2 * q], x1 = pr[2 * q + 1];
+            const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
+            const uint16_t l0 = f2bf(x0 - bf2f(h0)), l1 = f2bf(x1 - bf2f(h1));
+            hi[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+            lo[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+          }
+          const uint4 phi = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+          const uint4 plo = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+#pragma unroll
+          for (int d = 0; d < NOT; ++d) {
+            o[d] = mfma_step(phi, vf[d][kk], o[d], dummy);
+            o[d] = mfma_step(plo, vf[d][kk], o[d], dummy);
+          }
+        } else {
+          const uint4 pf = make_uint4(__float_as_uint(pr[0]), __float_as_uint(pr[1]),
+                                      __float_as_uint(pr[2]), __float_as_uint(pr[3]));
+#pragma unroll
+          for (int d = 0; d < NOT; ++d) o[d] = mfma_step(pf, vf[d][kk], o[d], dummy);
+        }
+      }
+      if (b + 4 < nblk) load_v(b + 4, vf);
+      __builtin_amdgcn_wave_barrier();
+    };
+
+    for (int b = wave; b < nblk; b += 4) {
+      if (b == wave) {
+        load_k(b, kf);
+        load_v(b, vf);
+      }
+      process(b);
+    }
+
+    // merge the four waves in order
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int rr = (lane >> 4) * 4 + r;
+#pragma unroll
+      for (int d = 0; d < NOT; ++d) sO[wave][rr * OS + d * 16 + (lane & 15)] = o[d][r];
+      if ((lane & 15) == 0) {
+        sM[wave][rr] = mrow[r];
+        sL[wave][rr] = lrow[r];
+      }
+    }
+    __syncthreads();
+    for (int idx = tid; idx < 16 * HDP; idx += 256) {
+      const int rr = idx / HDP, d = idx % HDP;
+      const int prow = rt * 16 + rr;
+      if (prow >= R || d >= a.hd) continue;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) mx = fmaxf(mx, sM[u][rr]);
+      float num = 0.f, den = 0.f;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const float wgt = sM[u][rr] == -INFINITY ? 0.f : exp2f(sM[u][rr] - mx);
+        num += wgt * sO[u][rr * OS + d];
+        den += wgt * sL[u][rr];
+      }
+      const int sq = prow / group, h = j * group + prow % group;
+      TT<T>::st((T*)a.out + (size_t)sq * a.ldo + h * a.hd + d, num / den);
+    }
+    __syncthreads();
+  }
+}
+
+template <typename T>
+static hipError_t run_attn2_t(const Attn2Args& a, int hdp, const LaunchCaps& caps, hipStream_t st) {
+  if (sizeof(T) == 4 && hdp > 128) return hipErrorInvalidValue;  // fp32: head dim <= 128
+  int grid = a.rtiles * a.nkv;
+  if (caps.max_wgs > 0) grid = std::min(grid, caps.max_wgs);
+#define VLA_ATTN2(H)                                                                           \
+  hipExtLaunchKernelGGL((k_attn2<T, H>), dim3(grid), dim3(256), 0, st, caps.ev_start, caps.ev_stop, \
+                        0, a)
+  switch (hdp) {
+    case 32: VLA_ATTN2(32); break;
+    case 64: VLA_ATTN2(64); break;
+    case 96: VLA_ATTN2(96); break;
+    case 128: VLA_ATTN2(128); break;
+    case 256: VLA_ATTN2(256); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef VLA_ATTN2
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_vt(const AttnVtDesc& d, const LaunchCaps& caps, hipStream_t st) {
+  const int hdp = attn_hdp(d.hd, d.dtype);
+  if (hdp < 0 || d.nq % d.nkv != 0 || d.S0 <= 0 || d.S1 < 0 || d.Sq <= 0 ||
+      (d.S1 > 0 && (!d.k1 || !d.vt1)) || d.ldvt0 < (d.S0 + 31) / 32 * 32 ||
+      (d.S1 > 0 && d.ldvt1 < (d.S1 + 31) / 32 * 32))
+    return hipErrorInvalidValue;
+  Attn2Args a{};
+  a.q = d.q;
+  a.k0 = d.k0;
+  a.vt0 = d.vt0;
+  a.k1 = d.S1 > 0 ? d.k1 : nullptr;
+  a.vt1 = d.S1 > 0 ? d.vt1 : nullptr;
+  a.out = d.out;
+  a.ldq = d.ldq;
+  a.ldk = d.ldk;
+  a.ldvt0 = d.ldvt0;
+  a.ldvt1 = d.ldvt1;
+  a.ldo = d.ldo;
+  a.Sq = d.Sq;
+  a.nq = d.nq;
+  a.nkv = d.nkv;
+  a.hd = d.hd;
+  a.S0 = d.S0;
+  a.S1 = d.S1;
+  a.rtiles = (d.Sq * (d.nq / d.nkv) + 15) / 16;
+  a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.hd));
+  if (d.dtype == DT_BF16) return run_attn2_t<uint16_t>(a, hdp, caps, st);
+  return run_attn2_t<float>(a, hdp, caps, st);
+}
+
+// ---------------------------------------------------------------------------
 // Row norms (LayerNorm with biased variance, or RMSNorm), fp32 statistics,
 // one workgroup per row, fixed-order tree reduction.
 // ---------------------------------------------------------------------------
@@ -938,18 +1263,22 @@ __global__ __launch_bounds__(256) void k_norm(float* __restrict__ x, int ldx, in
                                               int ldo) {
   __shared__ float red[4];
   const size_t pstride = (size_t)rows * d;
+  const Rsrc rx = rsrc(x, span(rows, ldx, d, 4));
+  const Rsrc rp = rsrc(part ? part : x, part ? (size_t)splits * pstride * 4 : 0);
+  const Rsrc rb = rsrc(bias ? bias : x, bias ? (size_t)d * 4 : 0);
   for (int row = blockIdx.x; row < rows; row += gridDim.x) {
     float* xr = x + (size_t)row * ldx;
     float v[NORM_NPT], add[NORM_NPT];
 #pragma unroll
     for (int q = 0; q < NORM_NPT; ++q) {
       const int i = threadIdx.x + q * 256;
-      v[q] = i < d ? xr[i] : 0.f;
-      add[q] = (bias && i < d) ? bias[i] : 0.f;
+      const bool ok = i < d;
+      v[q] = bld1(rx, ok ? (uint32_t)(((size_t)row * ldx + i) * 4) : OOB);
+      add[q] = bias ? bld1(rb, ok ? (uint32_t)(i * 4) : OOB) : 0.f;
     }
     if (splits > 0) {
       // partials in split order; four splits' loads are issued together
-      const float* pr = part + (size_t)row * d + threadIdx.x;
+      const size_t pbase = (size_t)row * d + threadIdx.x;
       int sp = 0;
       for (; sp + 4 <= splits; sp += 4) {
         float t[4][NORM_NPT];
@@ -957,7 +1286,8 @@ __global__ __launch_bounds__(256) void k_norm(float* __restrict__ x, int ldx, in
         for (int u = 0; u < 4; ++u)
 #pragma unroll
           for (int q = 0; q < NORM_NPT; ++q)
-            t[u][q] = threadIdx.x + q * 256 < d ? pr[(sp + u) * pstride + q * 256] : 0.f;
+            t[u][q] = bld1(rp, threadIdx.x + q * 256 < d
+                                   ? (uint32_t)((pbase + (sp + u) * pstride + q * 256) * 4) : OOB);
 #pragma unroll
         for (int u = 0; u < 4; ++u)
 #pragma unroll
@@ -966,7 +1296,8 @@ __global__ __launch_bounds__(256) void k_norm(float* __restrict__ x, int ldx, in
       for (; sp < splits; ++sp)
 #pragma unroll
         for (int q = 0; q < NORM_NPT; ++q)
-          if (threadIdx.x + q * 256 < d) add[q] += pr[sp * pstride + q * 256];
+          add[q] += bld1(rp, threadIdx.x + q * 256 < d
+                                 ? (uint32_t)((pbase + sp * pstride + q * 256) * 4) : OOB);
     }
     float s1 = 0.f;
 #pragma unroll

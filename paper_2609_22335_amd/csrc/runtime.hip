@@ -58,6 +58,7 @@ static inline int rnd_up(int x, int m) { return (x + m - 1) / m * m; }
 
 struct Dims {
   int gh, gw, tview, nimg, prefix, kp, kp_pad, a_pad, s_pad, rows_v, kvd, qd, qkv_n, vhd;
+  int prefix_pad, chunk_pad;  // key lengths rounded up to 32 (transposed V rows)
 };
 
 static Dims derive(const vla_config& c) {
@@ -76,6 +77,8 @@ static Dims derive(const vla_config& c) {
   d.qd = c.lm_heads * c.head_dim;
   d.qkv_n = d.qd + 2 * d.kvd;
   d.vhd = c.vit_dim / c.vit_heads;
+  d.prefix_pad = rnd_up(d.prefix, 32);
+  d.chunk_pad = rnd_up(c.chunk_len, 32);
   return d;
 }
 
@@ -96,6 +99,8 @@ static int validate(const vla_config* c) {
   if (vhd % 8 || vhd > 256) return bad("ViT head dim must be a multiple of 8 and <= 256");
   if (c->lm_heads % c->lm_kv_heads) return bad("lm_heads % lm_kv_heads != 0");
   if (c->head_dim % 32 || c->head_dim > 256) return bad("head_dim must be a multiple of 32, <= 256");
+  if (c->dtype == VLA_F32 && (c->head_dim > 128 || vhd > 128))
+    return bad("fp32 configurations need head dims <= 128");
   if (c->ex_layers != c->lm_layers) return bad("ex_layers must equal lm_layers (layer-wise KV sharing)");
   if (c->lm_mlp % 16 || c->ex_mlp % 16) return bad("lm_mlp / ex_mlp must be multiples of 16");
   if (c->vit_dim % 8 || c->lm_dim % 8 || c->ex_dim % 8 || c->vit_mlp % 8)
@@ -175,14 +180,27 @@ struct DecLayer {
   int rms1, qkv, o, rms2, gu, down;  // tensor ids (-1 when absent)
 };
 
+constexpr int MAX_ACT_STREAMS = 4;
+
 struct Streams {
-  hipStream_t v = nullptr, a = nullptr;
+  hipStream_t v = nullptr;
+  hipStream_t a[MAX_ACT_STREAMS] = {};
+};
+
+// Scratch of one action lane (one denoise at a time per lane).
+struct ActWs {
+  float* u = nullptr;
+  void *xop = nullptr, *a = nullptr, *hid = nullptr, *h = nullptr, *q = nullptr;
+  void *kown = nullptr, *vown = nullptr, *att = nullptr, *mlp = nullptr;
+  float* xg = nullptr;      // chunk written by graph replays, copied out afterwards
+  float* nstage = nullptr;  // noise staged for graph replays
+  Scratch scr;
 };
 
 struct vla_ctx {
   vla_model* m = nullptr;
   void* K = nullptr;  // [L][P][kvd]
-  void* V = nullptr;
+  void* V = nullptr;  // transposed: [L][kvd][P rounded up to 32], padding zero
 };
 
 struct vla_model {
@@ -217,18 +235,21 @@ struct vla_model {
     void *h, *qkv, *att, *mlp, *sbuf;
     Scratch scr;
   } vw{};
-  struct ActWs {
-    float* u;
-    void *xop, *a, *hid, *h, *q, *kown, *vown, *att, *mlp;
-    Scratch scr;
-  } aw{};
+  std::vector<std::unique_ptr<ActWs>> aws;  // action lanes; lane 0 serves standalone calls
   std::vector<void*> allocs;
 
   // pipeline
-  vla_ctx* pctx[2] = {nullptr, nullptr};
+  std::vector<vla_ctx*> pctx;  // ring of act_streams + 1 contexts
   std::map<std::pair<int, int>, Streams> mask_streams;
   Streams plain{};
   std::vector<hipEvent_t> ev;
+  // graph replay: frame inputs staged into fixed buffers, graphs cached per
+  // (context, VLM grid cap) and (action lane, context)
+  float* pstage = nullptr;
+  int32_t* istage = nullptr;
+  float* sstage = nullptr;
+  std::map<std::pair<int, int>, hipGraphExec_t> pre_graphs;
+  std::map<std::pair<int, int>, hipGraphExec_t> den_graphs;
   std::mutex mu;
 
   // per-tag kernel timer: every launch whose tag matches is bracketed by
@@ -394,6 +415,7 @@ struct Run {
   hipStream_t st;
   LaunchCaps caps;
   const Scratch* scr;
+  ActWs* aw = nullptr;  // action phase only
 };
 
 // Kernel timer: a launch whose tag matches gets a pair of events that its
@@ -436,6 +458,14 @@ static int gemm(const Run& r, const char* tag, const void* A, int lda, int W, in
   if (err != hipSuccess)
     return fail(VLA_EHIP, std::string("gemm ") + std::to_string(M) + "x" + std::to_string(N) + "x" +
                               std::to_string(K) + ": " + hipGetErrorString(err));
+  return VLA_OK;
+}
+
+static int attn_vt(const Run& r, const char* tag, const AttnVtDesc& a) {
+  LaunchCaps caps = r.caps;
+  VLA_TRY(timer_events(r, tag, &caps));
+  hipError_t err = launch_attention_vt(a, caps, r.st);
+  if (err != hipSuccess) return fail(VLA_EHIP, std::string("attention: ") + hipGetErrorString(err));
   return VLA_OK;
 }
 
@@ -506,33 +536,36 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   e.pos0 = pos0;
   e.rope_cos = m->rope_cos;
   e.rope_sin = m->rope_sin;
+  e.ldvt = lm ? d.prefix_pad : d.chunk_pad;
   VLA_TRY(gemm(r, lm ? "lm.qkv" : "ex.qkv", h, dim, L.qkv, rows, d.qkv_n, dim, e));
   if (kv_only) return VLA_OK;
-  AttnDesc a{};
+  AttnVtDesc a{};
   a.dtype = m->dt;
   a.q = q;
   a.ldq = d.qd;
+  a.ldk = d.kvd;
   if (kpast) {
     a.k0 = kpast;
-    a.v0 = vpast;
+    a.vt0 = vpast;
     a.S0 = npast;
+    a.ldvt0 = d.prefix_pad;
     a.k1 = kout;
-    a.v1 = vout;
+    a.vt1 = vout;
     a.S1 = rows;
+    a.ldvt1 = d.chunk_pad;
   } else {
     a.k0 = kout;
-    a.v0 = vout;
+    a.vt0 = vout;
     a.S0 = rows;
+    a.ldvt0 = d.prefix_pad;
   }
-  a.ldkv = d.kvd;
   a.out = att;
   a.ldo = d.qd;
   a.Sq = rows;
   a.nq = c.lm_heads;
   a.nkv = c.lm_kv_heads;
   a.hd = c.head_dim;
-  a.segs = 1;
-  VLA_TRY(attn(r, lm ? "lm.attn" : "ex.attn", a));
+  VLA_TRY(attn_vt(r, lm ? "lm.attn" : "ex.attn", a));
   int so = 0;
   VLA_TRY(gemm_part(r, lm ? "lm.o" : "ex.o", att, d.qd, L.o, rows, dim, d.qd, &so));
   VLA_TRY(norm(r, x, rows, dim, so, nullptr, L.rms2, -1, true, h));
@@ -598,11 +631,12 @@ static int run_prefill(const Run& r, const vla_frame* f, vla_ctx* ctx) {
                  epi_kind(EPI_F32, w.xl + (size_t)(d.prefix - 1) * dl, dl, m->f32(m->state_b))));
   }
   // LM prefill writing the cache
-  const size_t layer_kv = (size_t)d.prefix * d.kvd * m->esz;
+  const size_t layer_k = (size_t)d.prefix * d.kvd * m->esz;
+  const size_t layer_v = (size_t)d.prefix_pad * d.kvd * m->esz;
   pend = 0;
   for (int l = 0; l < c.lm_layers; ++l) {
-    void* K = (char*)ctx->K + l * layer_kv;
-    void* V = (char*)ctx->V + l * layer_kv;
+    void* K = (char*)ctx->K + l * layer_k;
+    void* V = (char*)ctx->V + l * layer_v;
     VLA_TRY(decoder_layer(r, true, m->lm[l], w.xl, d.prefix, dl, c.lm_mlp, w.h, w.qkv, K, V, 0, nullptr,
                           nullptr, 0, w.att, w.mlp, l == c.lm_layers - 1, &pend));
   }
@@ -613,11 +647,12 @@ static int run_denoise(const Run& r, const vla_ctx* ctx, const float* noise, flo
   vla_model* m = r.m;
   const vla_config& c = m->c;
   const Dims& d = m->d;
-  auto& w = m->aw;
+  ActWs& w = *r.aw;
   const int H = c.chunk_len, de = c.ex_dim, A = c.action_dim;
   const float dt = -1.0f / (float)c.n_steps;
   HIP_TRY(launch_cvt_pad(m->dt, noise, H, A, w.xop, d.a_pad, x, r.st));
-  const size_t layer_kv = (size_t)d.prefix * d.kvd * m->esz;
+  const size_t layer_k = (size_t)d.prefix * d.kvd * m->esz;
+  const size_t layer_v = (size_t)d.prefix_pad * d.kvd * m->esz;
   for (int k = 0; k < c.n_steps; ++k) {
     // action embedding and time conditioning
     VLA_TRY(gemm(r, "ex.in", w.xop, d.a_pad, m->in_w, H, de, d.a_pad, epi_kind(EPI_T, w.a, de, m->f32(m->in_b))));
@@ -625,8 +660,8 @@ static int run_denoise(const Run& r, const vla_ctx* ctx, const float* noise, flo
     VLA_TRY(gemm(r, "ex.time2", w.hid, de, m->t2_w, H, de, de, epi_kind(EPI_F32, w.u, de, m->f32(m->t2_b))));
     int pend = 0;
     for (int l = 0; l < c.ex_layers; ++l) {
-      const void* K = (const char*)ctx->K + l * layer_kv;
-      const void* V = (const char*)ctx->V + l * layer_kv;
+      const void* K = (const char*)ctx->K + l * layer_k;
+      const void* V = (const char*)ctx->V + l * layer_v;
       VLA_TRY(decoder_layer(r, false, m->ex[l], w.u, H, de, c.ex_mlp, w.h, w.q, w.kown, w.vown, d.prefix,
                             K, V, d.prefix, w.att, w.mlp, false, &pend));
     }
@@ -720,6 +755,45 @@ static int setup_tables(vla_model* m) {
   return VLA_OK;
 }
 
+// One action lane's scratch (activations of the chunk rows, own K / V^T,
+// partial sums, staging for graph replays).
+static int add_act_lane(vla_model* m) {
+  const vla_config& c = m->c;
+  const Dims& d = m->d;
+  const int dt = m->dt;
+  const size_t e = m->esz;
+  const int P = d.prefix, H = c.chunk_len, de = c.ex_dim;
+  auto upd = [](ScratchNeed& s, ScratchNeed x) { s.floats = std::max(s.floats, x.floats); };
+  std::unique_ptr<ActWs> lane(new ActWs());
+  ActWs& a = *lane;
+  VLA_TRY(dmalloc(m, (void**)&a.u, (size_t)H * de * 4));
+  VLA_TRY(dmalloc(m, &a.xop, (size_t)H * d.a_pad * e));
+  VLA_TRY(dmalloc(m, &a.a, (size_t)H * de * e));
+  VLA_TRY(dmalloc(m, &a.hid, (size_t)H * de * e));
+  VLA_TRY(dmalloc(m, &a.h, (size_t)H * de * e));
+  VLA_TRY(dmalloc(m, &a.q, (size_t)H * d.qd * e));
+  VLA_TRY(dmalloc(m, &a.kown, (size_t)H * d.kvd * e));
+  VLA_TRY(dmalloc(m, &a.vown, (size_t)d.chunk_pad * d.kvd * e));
+  HIP_TRY(hipMemset(a.vown, 0, (size_t)d.chunk_pad * d.kvd * e));  // padding keys stay zero
+  VLA_TRY(dmalloc(m, &a.att, (size_t)H * d.qd * e));
+  VLA_TRY(dmalloc(m, &a.mlp, (size_t)H * c.ex_mlp * e));
+  ScratchNeed sa;
+  upd(sa, gemm_scratch(dt, H, de, d.a_pad, false, true));
+  upd(sa, gemm_scratch(dt, H, de, de, false, true));
+  upd(sa, gemm_scratch(dt, c.n_steps, de, de, false, true));
+  upd(sa, gemm_scratch(dt, H, d.qkv_n, de, false, true));
+  upd(sa, gemm_scratch(dt, H, de, d.qd, true, true));
+  upd(sa, gemm_scratch(dt, H, 2 * c.ex_mlp, de, false, true));
+  upd(sa, gemm_scratch(dt, H, de, c.ex_mlp, true, true));
+  upd(sa, gemm_scratch(dt, H, c.action_dim, de, false, true));
+  upd(sa, attn_scratch(dt, H, c.lm_heads, c.lm_kv_heads, c.head_dim, P, H, 1));
+  VLA_TRY(alloc_scratch(m, sa, &a.scr));
+  VLA_TRY(dmalloc(m, (void**)&a.xg, (size_t)H * c.action_dim * 4));
+  VLA_TRY(dmalloc(m, (void**)&a.nstage, (size_t)H * c.action_dim * 4));
+  m->aws.push_back(std::move(lane));
+  return VLA_OK;
+}
+
 static int setup_workspaces(vla_model* m) {
   const vla_config& c = m->c;
   const Dims& d = m->d;
@@ -753,28 +827,10 @@ static int setup_workspaces(vla_model* m) {
   upd(sv, attn_scratch(dt, P, c.lm_heads, c.lm_kv_heads, c.head_dim, P, 0, 1));
   VLA_TRY(alloc_scratch(m, sv, &v.scr));
 
-  auto& a = m->aw;
-  VLA_TRY(dmalloc(m, (void**)&a.u, (size_t)H * de * 4));
-  VLA_TRY(dmalloc(m, &a.xop, (size_t)H * d.a_pad * e));
-  VLA_TRY(dmalloc(m, &a.a, (size_t)H * de * e));
-  VLA_TRY(dmalloc(m, &a.hid, (size_t)H * de * e));
-  VLA_TRY(dmalloc(m, &a.h, (size_t)H * de * e));
-  VLA_TRY(dmalloc(m, &a.q, (size_t)H * d.qd * e));
-  VLA_TRY(dmalloc(m, &a.kown, (size_t)H * d.kvd * e));
-  VLA_TRY(dmalloc(m, &a.vown, (size_t)H * d.kvd * e));
-  VLA_TRY(dmalloc(m, &a.att, (size_t)H * d.qd * e));
-  VLA_TRY(dmalloc(m, &a.mlp, (size_t)H * c.ex_mlp * e));
-  ScratchNeed sa;
-  upd(sa, gemm_scratch(dt, H, de, d.a_pad, false, true));
-  upd(sa, gemm_scratch(dt, H, de, de, false, true));
-  upd(sa, gemm_scratch(dt, c.n_steps, de, de, false, true));
-  upd(sa, gemm_scratch(dt, H, d.qkv_n, de, false, true));
-  upd(sa, gemm_scratch(dt, H, de, d.qd, true, true));
-  upd(sa, gemm_scratch(dt, H, 2 * c.ex_mlp, de, false, true));
-  upd(sa, gemm_scratch(dt, H, de, c.ex_mlp, true, true));
-  upd(sa, gemm_scratch(dt, H, c.action_dim, de, false, true));
-  upd(sa, attn_scratch(dt, H, c.lm_heads, c.lm_kv_heads, c.head_dim, P, H, 1));
-  VLA_TRY(alloc_scratch(m, sa, &a.scr));
+  VLA_TRY(dmalloc(m, (void**)&m->pstage, (size_t)c.n_views * c.img_h * c.img_w * 3 * 4));
+  VLA_TRY(dmalloc(m, (void**)&m->istage, (size_t)std::max(c.n_text, 1) * 4));
+  VLA_TRY(dmalloc(m, (void**)&m->sstage, (size_t)std::max(c.state_dim, 1) * 4));
+  VLA_TRY(add_act_lane(m));
   return VLA_OK;
 }
 
@@ -812,7 +868,7 @@ static int create_impl(const vla_config* cfg, uint64_t seed, vla_model** out) {
   if (rc == VLA_OK) rc = setup_workspaces(m.get());
   if (rc == VLA_OK) {
     // c_k = W_2[:, d_e:] phi(t_k) + b_2 for every step (depends on the step only)
-    Run r{m.get(), nullptr, LaunchCaps{}, &m->aw.scr};
+    Run r{m.get(), nullptr, LaunchCaps{}, &m->aws[0]->scr, m->aws[0].get()};
     const int de = m->c.ex_dim;
     rc = gemm(r, "ex.ck", m->phi, de, m->t1_w, m->c.n_steps, de, de,
               epi_kind(EPI_F32, m->ck, de, m->f32(m->t1_b)), de);
@@ -837,13 +893,16 @@ static int create_impl(const vla_config* cfg, uint64_t seed, vla_model** out) {
 static int ctx_create_impl(vla_model* m, vla_ctx** out) {
   std::unique_ptr<vla_ctx> c(new vla_ctx());
   c->m = m;
-  const size_t bytes = (size_t)m->c.lm_layers * m->d.prefix * m->d.kvd * m->esz;
-  hipError_t e = hipMalloc(&c->K, bytes);
+  const size_t kbytes = (size_t)m->c.lm_layers * m->d.prefix * m->d.kvd * m->esz;
+  const size_t vbytes = (size_t)m->c.lm_layers * m->d.prefix_pad * m->d.kvd * m->esz;
+  hipError_t e = hipMalloc(&c->K, kbytes);
   if (e != hipSuccess) return fail(VLA_ENOMEM, "ctx K: hipMalloc failed");
-  e = hipMalloc(&c->V, bytes);
+  e = hipMalloc(&c->V, vbytes);
+  if (e == hipSuccess) e = hipMemset(c->V, 0, vbytes);  // padding keys stay zero
   if (e != hipSuccess) {
     hipFree(c->K);
-    return fail(VLA_ENOMEM, "ctx V: hipMalloc failed");
+    hipFree(c->V);
+    return fail(VLA_ENOMEM, "ctx V: allocation failed");
   }
   *out = c.release();
   return VLA_OK;
@@ -861,13 +920,14 @@ static int get_streams(vla_model* m, const vla_sched& s, Streams* out) {
     if (it == m->mask_streams.end()) {
       // Bits are spread over the XCDs by the driver (bit i -> XCD i % 8), so
       // contiguous ranges whose sizes are multiples of 8 give every XCD CUs
-      // of both phases.
+      // of both phases. All action streams share the action CU set.
       Streams st;
       std::vector<uint32_t> mv, ma;
       cu_mask(0, s.vlm_cus, m->num_cus, mv);
       cu_mask(s.vlm_cus, s.act_cus, m->num_cus, ma);
       HIP_TRY(hipExtStreamCreateWithCUMask(&st.v, (uint32_t)mv.size(), mv.data()));
-      HIP_TRY(hipExtStreamCreateWithCUMask(&st.a, (uint32_t)ma.size(), ma.data()));
+      for (int i = 0; i < MAX_ACT_STREAMS; ++i)
+        HIP_TRY(hipExtStreamCreateWithCUMask(&st.a[i], (uint32_t)ma.size(), ma.data()));
       it = m->mask_streams.emplace(key, st).first;
     }
     *out = it->second;
@@ -875,9 +935,28 @@ static int get_streams(vla_model* m, const vla_sched& s, Streams* out) {
   }
   if (!m->plain.v) {
     HIP_TRY(hipStreamCreateWithFlags(&m->plain.v, hipStreamNonBlocking));
-    HIP_TRY(hipStreamCreateWithFlags(&m->plain.a, hipStreamNonBlocking));
+    for (int i = 0; i < MAX_ACT_STREAMS; ++i)
+      HIP_TRY(hipStreamCreateWithFlags(&m->plain.a[i], hipStreamNonBlocking));
   }
   *out = m->plain;
+  return VLA_OK;
+}
+
+// Capture one phase on `st` into an executable graph.
+template <typename F>
+static int capture(hipStream_t st, F&& body, hipGraphExec_t* out) {
+  HIP_TRY(hipStreamBeginCapture(st, hipStreamCaptureModeThreadLocal));
+  const int rc = body();
+  hipGraph_t g = nullptr;
+  const hipError_t e = hipStreamEndCapture(st, &g);
+  if (rc != VLA_OK) {
+    if (g) hipGraphDestroy(g);
+    return rc;
+  }
+  if (e != hipSuccess) return fail(VLA_EHIP, std::string("graph capture: ") + hipGetErrorString(e));
+  const hipError_t ie = hipGraphInstantiate(out, g, nullptr, nullptr, 0);
+  hipGraphDestroy(g);
+  if (ie != hipSuccess) return fail(VLA_EHIP, std::string("graph instantiate: ") + hipGetErrorString(ie));
   return VLA_OK;
 }
 
@@ -894,12 +973,25 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
                                   std::to_string(m->num_cus) + ")");
   }
   if (s.mode == VLA_MODE_WG_CAPPED && s.vlm_wg_cap < 1) return fail(VLA_EINVAL, "vlm_wg_cap must be >= 1");
+  const int lanes = std::max(1, s.act_streams);
+  if (lanes > MAX_ACT_STREAMS) return fail(VLA_EINVAL, "act_streams must be <= 4");
+  if (lanes > 1 && s.mode == VLA_MODE_SERIAL) return fail(VLA_EINVAL, "act_streams > 1 needs a concurrent mode");
+  const vla_config& c = m->c;
+  for (int r = 0; r < R; ++r)
+    if (!frames[r].pixels || (c.n_text > 0 && !frames[r].text_ids) || (c.state_dim > 0 && !frames[r].state))
+      return fail(VLA_EINVAL, "frame " + std::to_string(r) + " has a NULL input");
   std::lock_guard<std::mutex> lock(m->mu);
-  for (int i = 0; i < 2; ++i)
-    if (!m->pctx[i]) VLA_TRY(ctx_create_impl(m, &m->pctx[i]));
+  const int nctx = lanes + 1;
+  while ((int)m->pctx.size() < nctx) {
+    vla_ctx* cx = nullptr;
+    VLA_TRY(ctx_create_impl(m, &cx));
+    m->pctx.push_back(cx);
+  }
+  while ((int)m->aws.size() < lanes) VLA_TRY(add_act_lane(m));
   Streams st;
   VLA_TRY(get_streams(m, s, &st));
-  if (s.mode == VLA_MODE_SERIAL) st.a = st.v;
+  if (s.mode == VLA_MODE_SERIAL) st.a[0] = st.v;
+  const bool graphs = s.graphs != 0 && m->timer_tag.empty();
   const size_t need = (size_t)4 * R;
   while (m->ev.size() < need) {
     hipEvent_t e;
@@ -909,29 +1001,72 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
   // events: [4r] VLM start, [4r+1] VLM end, [4r+2] action start, [4r+3] action end
   LaunchCaps vcaps{}, acaps{};
   if (s.mode == VLA_MODE_WG_CAPPED) vcaps.max_wgs = s.vlm_wg_cap * m->num_cus;
-  const size_t chunk = (size_t)m->c.chunk_len * m->c.action_dim;
+  const size_t chunk = (size_t)c.chunk_len * c.action_dim;
+  const size_t pix_bytes = (size_t)c.n_views * c.img_h * c.img_w * 3 * 4;
   HIP_TRY(hipDeviceSynchronize());
+
+  if (graphs) {  // capture what is missing (outside the timed loop)
+    vla_frame staged{m->pstage, m->istage, c.state_dim > 0 ? m->sstage : nullptr};
+    for (int ci = 0; ci < nctx; ++ci) {
+      const auto key = std::make_pair(ci, vcaps.max_wgs);
+      if (m->pre_graphs.count(key)) continue;
+      Run rv{m, st.v, vcaps, &m->vw.scr};
+      hipGraphExec_t ge = nullptr;
+      VLA_TRY(capture(st.v, [&] { return run_prefill(rv, &staged, m->pctx[ci]); }, &ge));
+      m->pre_graphs[key] = ge;
+    }
+    for (int li = 0; li < lanes; ++li)
+      for (int ci = 0; ci < nctx; ++ci) {
+        const auto key = std::make_pair(li, ci);
+        if (m->den_graphs.count(key)) continue;
+        ActWs* aw = m->aws[li].get();
+        Run ra{m, st.a[li], acaps, &aw->scr, aw};
+        hipGraphExec_t ge = nullptr;
+        VLA_TRY(capture(st.a[li], [&] { return run_denoise(ra, m->pctx[ci], aw->nstage, aw->xg); }, &ge));
+        m->den_graphs[key] = ge;
+      }
+  }
+
   const auto t0 = std::chrono::steady_clock::now();
   for (int r = 0; r < R; ++r) {
-    vla_ctx* ctx = m->pctx[r % 2];
-    if (r >= 2 && st.v != st.a) HIP_TRY(hipStreamWaitEvent(st.v, m->ev[4 * (r - 2) + 3], 0));
+    const int ci = r % nctx, li = r % lanes;
+    vla_ctx* ctx = m->pctx[ci];
+    hipStream_t sa = st.a[li];
+    // the context is free once the action phase that last read it is done
+    if (r >= nctx && st.v != sa) HIP_TRY(hipStreamWaitEvent(st.v, m->ev[4 * (r - nctx) + 3], 0));
     HIP_TRY(hipEventRecord(m->ev[4 * r], st.v));
-    Run rv{m, st.v, vcaps, &m->vw.scr};
-    VLA_TRY(run_prefill(rv, &frames[r], ctx));
+    if (graphs) {
+      HIP_TRY(hipMemcpyAsync(m->pstage, frames[r].pixels, pix_bytes, hipMemcpyDeviceToDevice, st.v));
+      if (c.n_text > 0)
+        HIP_TRY(hipMemcpyAsync(m->istage, frames[r].text_ids, (size_t)c.n_text * 4, hipMemcpyDeviceToDevice, st.v));
+      if (c.state_dim > 0)
+        HIP_TRY(hipMemcpyAsync(m->sstage, frames[r].state, (size_t)c.state_dim * 4, hipMemcpyDeviceToDevice, st.v));
+      HIP_TRY(hipGraphLaunch(m->pre_graphs[std::make_pair(ci, vcaps.max_wgs)], st.v));
+    } else {
+      Run rv{m, st.v, vcaps, &m->vw.scr};
+      VLA_TRY(run_prefill(rv, &frames[r], ctx));
+    }
     HIP_TRY(hipEventRecord(m->ev[4 * r + 1], st.v));
-    if (st.v != st.a) HIP_TRY(hipStreamWaitEvent(st.a, m->ev[4 * r + 1], 0));
-    HIP_TRY(hipEventRecord(m->ev[4 * r + 2], st.a));
-    Run ra{m, st.a, acaps, &m->aw.scr};
-    VLA_TRY(run_denoise(ra, ctx, noise + r * chunk, actions + r * chunk));
-    HIP_TRY(hipEventRecord(m->ev[4 * r + 3], st.a));
+    if (st.v != sa) HIP_TRY(hipStreamWaitEvent(sa, m->ev[4 * r + 1], 0));
+    HIP_TRY(hipEventRecord(m->ev[4 * r + 2], sa));
+    ActWs* aw = m->aws[li].get();
+    if (graphs) {
+      HIP_TRY(hipMemcpyAsync(aw->nstage, noise + r * chunk, chunk * 4, hipMemcpyDeviceToDevice, sa));
+      HIP_TRY(hipGraphLaunch(m->den_graphs[std::make_pair(li, ci)], sa));
+      HIP_TRY(hipMemcpyAsync(actions + r * chunk, aw->xg, chunk * 4, hipMemcpyDeviceToDevice, sa));
+    } else {
+      Run ra{m, sa, acaps, &aw->scr, aw};
+      VLA_TRY(run_denoise(ra, ctx, noise + r * chunk, actions + r * chunk));
+    }
+    HIP_TRY(hipEventRecord(m->ev[4 * r + 3], sa));
   }
   HIP_TRY(hipStreamSynchronize(st.v));
-  HIP_TRY(hipStreamSynchronize(st.a));
+  for (int li = 0; li < lanes; ++li) HIP_TRY(hipStreamSynchronize(st.a[li]));
   const auto t1 = std::chrono::steady_clock::now();
   if (t) {
     t->wall_ms = std::chrono::duration<double, std::milli>(t1 - t0).count();
     t->frames_per_s = R / (t->wall_ms * 1e-3);
-    t->actions_per_s = t->frames_per_s * m->c.chunk_len;
+    t->actions_per_s = t->frames_per_s * c.chunk_len;
     t->vlm_ms = t->act_ms = 0;
     for (int r = 0; r < R; ++r) {
       float a = 0, b = 0;
@@ -983,20 +1118,20 @@ int vla_destroy(vla_model* m) {
   ABI_GUARD({
     if (!m) return VLA_OK;
     hipDeviceSynchronize();
-    for (int i = 0; i < 2; ++i)
-      if (m->pctx[i]) {
-        hipFree(m->pctx[i]->K);
-        hipFree(m->pctx[i]->V);
-        delete m->pctx[i];
-      }
-    for (auto& kv : m->mask_streams) {
-      hipStreamDestroy(kv.second.v);
-      hipStreamDestroy(kv.second.a);
+    for (auto& kv : m->pre_graphs) hipGraphExecDestroy(kv.second);
+    for (auto& kv : m->den_graphs) hipGraphExecDestroy(kv.second);
+    for (vla_ctx* cx : m->pctx) {
+      hipFree(cx->K);
+      hipFree(cx->V);
+      delete cx;
     }
-    if (m->plain.v) {
-      hipStreamDestroy(m->plain.v);
-      hipStreamDestroy(m->plain.a);
-    }
+    auto drop = [](Streams& st) {
+      if (st.v) hipStreamDestroy(st.v);
+      for (hipStream_t a : st.a)
+        if (a) hipStreamDestroy(a);
+    };
+    for (auto& kv : m->mask_streams) drop(kv.second);
+    drop(m->plain);
     for (auto e : m->ev) hipEventDestroy(e);
     for (auto e : m->timer_ev) hipEventDestroy(e);
     for (void* p : m->allocs) hipFree(p);
@@ -1039,7 +1174,7 @@ int vla_action_denoise(vla_model* m, const vla_ctx* ctx, const float* noise, flo
   ABI_GUARD({
     if (!m || !ctx || !noise || !actions) return fail(VLA_EINVAL, "NULL argument");
     if (ctx->m != m) return fail(VLA_ESTATE, "context belongs to another model");
-    Run r{m, (hipStream_t)stream, LaunchCaps{}, &m->aw.scr};
+    Run r{m, (hipStream_t)stream, LaunchCaps{}, &m->aws[0]->scr, m->aws[0].get()};
     return run_denoise(r, ctx, noise, actions);
   })
 }
@@ -1098,15 +1233,19 @@ int vla_ctx_export_kv(vla_model* m, const vla_ctx* c, int32_t layer, float* host
     if (!m || !c || !host_k || !host_v) return fail(VLA_EINVAL, "NULL argument");
     if (layer < 0 || layer >= m->c.lm_layers) return fail(VLA_EINVAL, "layer out of range");
     if (c->m != m) return fail(VLA_ESTATE, "context belongs to another model");
-    const size_t n = (size_t)m->d.prefix * m->d.kvd;
+    const int P = m->d.prefix, Pp = m->d.prefix_pad, kvd = m->d.kvd;
+    const size_t n = (size_t)P * kvd;
+    auto val = [&](const std::vector<uint8_t>& img, size_t i) {
+      return m->dt == DT_BF16 ? bf16_value(((const uint16_t*)img.data())[i]) : ((const float*)img.data())[i];
+    };
     std::vector<uint8_t> img(n * m->esz);
-    for (int w = 0; w < 2; ++w) {
-      const char* src = (const char*)(w ? c->V : c->K) + layer * n * m->esz;
-      HIP_TRY(hipMemcpy(img.data(), src, img.size(), hipMemcpyDeviceToHost));
-      float* dst = w ? host_v : host_k;
-      for (size_t i = 0; i < n; ++i)
-        dst[i] = m->dt == DT_BF16 ? bf16_value(((uint16_t*)img.data())[i]) : ((float*)img.data())[i];
-    }
+    HIP_TRY(hipMemcpy(img.data(), (const char*)c->K + layer * n * m->esz, img.size(), hipMemcpyDeviceToHost));
+    for (size_t i = 0; i < n; ++i) host_k[i] = val(img, i);
+    const size_t nv = (size_t)Pp * kvd;
+    std::vector<uint8_t> vimg(nv * m->esz);
+    HIP_TRY(hipMemcpy(vimg.data(), (const char*)c->V + layer * nv * m->esz, vimg.size(), hipMemcpyDeviceToHost));
+    for (int p = 0; p < P; ++p)
+      for (int j = 0; j < kvd; ++j) host_v[(size_t)p * kvd + j] = val(vimg, (size_t)j * Pp + p);
     return VLA_OK;
   })
 }
@@ -1177,6 +1316,41 @@ int vla_debug_attention(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int3
       hipStreamSynchronize((hipStream_t)stream);
       hipFree(s.ptr);
     }
+    if (e != hipSuccess) return fail(VLA_EHIP, std::string("attention: ") + hipGetErrorString(e));
+    return VLA_OK;
+  })
+}
+
+int vla_debug_attention_vt(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int32_t hd,
+                           const void* q, const void* k0, const void* vt0, int32_t S0, int32_t ldvt0,
+                           const void* k1, const void* vt1, int32_t S1, int32_t ldvt1, void* out,
+                           void* stream) {
+  ABI_GUARD({
+    if (dtype != VLA_F32 && dtype != VLA_BF16) return fail(VLA_EINVAL, "dtype");
+    if (Sq <= 0 || nq <= 0 || nkv <= 0 || nq % nkv || hd <= 0 || hd % 8 || hd > 256 || S0 <= 0 ||
+        S1 < 0 || ldvt0 < (S0 + 31) / 32 * 32 || (S1 > 0 && ldvt1 < (S1 + 31) / 32 * 32))
+      return fail(VLA_EINVAL, "shape");
+    if (!q || !k0 || !vt0 || !out || (S1 > 0 && (!k1 || !vt1))) return fail(VLA_EINVAL, "NULL argument");
+    AttnVtDesc a{};
+    a.dtype = dtype == VLA_BF16 ? DT_BF16 : DT_F32;
+    a.q = q;
+    a.ldq = nq * hd;
+    a.k0 = k0;
+    a.vt0 = vt0;
+    a.S0 = S0;
+    a.ldvt0 = ldvt0;
+    a.k1 = k1;
+    a.vt1 = vt1;
+    a.S1 = S1;
+    a.ldvt1 = ldvt1;
+    a.ldk = nkv * hd;
+    a.out = out;
+    a.ldo = nq * hd;
+    a.Sq = Sq;
+    a.nq = nq;
+    a.nkv = nkv;
+    a.hd = hd;
+    hipError_t e = launch_attention_vt(a, LaunchCaps{}, (hipStream_t)stream);
     if (e != hipSuccess) return fail(VLA_EHIP, std::string("attention: ") + hipGetErrorString(e));
     return VLA_OK;
   })

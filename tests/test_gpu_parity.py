@@ -103,6 +103,53 @@ def test_attention_vs_oracle(V, case):
     assert np.all(err <= bound), float((err / bound).max())
 
 
+ATTN_VT_CASES = [  # dtype, Sq, nq, nkv, hd, S0, S1
+    (1, 50, 8, 1, 256, 305, 50),   # expert joint attention over [prefix; own]
+    (1, 50, 8, 1, 256, 833, 50),   # three-view prefix
+    (1, 305, 8, 1, 256, 305, 0),   # LM prefill, multi-query
+    (1, 5, 2, 1, 32, 21, 5),
+    (1, 64, 4, 4, 128, 96, 0),     # multi-head, head dim 128
+    (1, 1, 1, 1, 48, 883, 0),      # one query, long keys, head dim 48
+    (0, 8, 4, 1, 64, 80, 8),
+    (0, 80, 4, 1, 64, 80, 0),
+    (0, 3, 2, 2, 32, 1, 0),        # single key
+    (0, 17, 3, 1, 96, 40, 33),
+]
+
+
+@pytest.mark.parametrize("case", ATTN_VT_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_attention_vt_vs_oracle(V, case):
+    g = G()
+    dtype, Sq, nq, nkv, hd, S0, S1 = case
+    g.say(f"attention (transposed V) {case}")
+    q = RNG.standard_normal((Sq, nq, hd))
+    k0, v0 = RNG.standard_normal((S0, nkv, hd)), RNG.standard_normal((S0, nkv, hd))
+    k1, v1 = RNG.standard_normal((max(S1, 1), nkv, hd)), RNG.standard_normal((max(S1, 1), nkv, hd))
+
+    def vt(v, S):  # [S, nkv, hd] -> [nkv * hd, round32(S)], zero padding
+        ld = (S + 31) // 32 * 32
+        t = np.zeros((nkv * hd, ld))
+        t[:, :S] = v[:S].reshape(S, -1).T
+        return t, ld
+
+    vt0, ld0 = vt(v0, S0)
+    vt1, ld1 = vt(v1, max(S1, 1))
+    dv = lambda x: g.operand_dev(x.reshape(x.shape[0], -1), dtype)
+    out = torch.empty((Sq, nq * hd), dtype=torch.bfloat16 if dtype else torch.float32, device="cuda")
+    k1d, vt1d = dv(k1), g.operand_dev(vt1, dtype)
+    V.vla_debug_attention_vt(dtype, Sq, nq, nkv, hd, dv(q), dv(k0), g.operand_dev(vt0, dtype), S0, ld0,
+                             k1d if S1 else None, vt1d if S1 else None, S1, ld1, out)
+    torch.cuda.synchronize()
+    val = lambda x: g.operand_values(x, dtype)
+    kk = np.concatenate([val(k0), val(k1)[:S1]], 0)
+    vv = np.concatenate([val(v0), val(v1)[:S1]], 0)
+    ref = O.attention(val(q), kk, vv).reshape(Sq, -1)
+    got = out.float().cpu().numpy()
+    bound = (2.0 ** -8 * np.abs(ref) + 1e-4) if dtype else (2e-5 + 1e-5 * np.abs(ref))
+    err = np.abs(got - ref)
+    assert np.all(err <= bound), float((err / bound).max())
+
+
 @pytest.mark.parametrize("cfg", [synth.micro(synth.F32), synth.micro(synth.BF16), synth.TINY],
                          ids=["micro-f32", "micro-bf16", "tiny"])
 def test_weights_on_device_equal_seeded_generator(V, cfg):
@@ -184,8 +231,12 @@ def test_pi0_full_size_vs_oracle(V):
 
 @pytest.mark.parametrize("cfg", [synth.micro(synth.BF16), synth.TINY], ids=["micro-bf16", "tiny"])
 def test_pipeline_modes_bit_identical(V, cfg):
+    """Every schedule (one stream, two streams, CU masks, workgroup caps,
+    several action streams, graph replay) gives the same bits as standalone
+    prefill + denoise calls; graph schedules are replayed three times with
+    eager work in between."""
     g = G()
-    R = 5
+    R = 7
     g.say(f"pipeline modes dtype={cfg['dtype']} R={R}")
     frames = [synth.make_frame(cfg, 11, r) for r in range(R)]
     dfs = [g.DevFrame(f) for f in frames]
@@ -193,23 +244,32 @@ def test_pipeline_modes_bit_identical(V, cfg):
     results = {}
     with g.model(cfg, 11) as m:
         ncu = torch.cuda.get_device_properties(0).multi_processor_count
-        modes = [("serial", {}), ("concurrent", {}), ("cu_masked", dict(vlm_cus=(ncu // 2) // 8 * 8, act_cus=16)),
-                 ("wg_capped", dict(vlm_wg_cap=1))]
-        for mode, kw in modes:
-            out = torch.full_like(noise, float("nan"))
-            t = V.vla_pipeline_run(m, [d.c for d in dfs], noise, R, mode=mode, actions=out, **kw)
-            assert t["frames_per_s"] > 0
-            results[mode] = out.cpu().numpy()
+        split = dict(vlm_cus=(ncu // 2) // 8 * 8, act_cus=16)
+        modes = [("serial", {}), ("concurrent", {}), ("cu_masked", split), ("wg_capped", dict(vlm_wg_cap=1)),
+                 ("serial", dict(graphs=True)), ("concurrent", dict(graphs=True)),
+                 ("concurrent", dict(act_streams=2)), ("concurrent", dict(act_streams=3, graphs=True)),
+                 ("cu_masked", dict(split, act_streams=2, graphs=True)),
+                 ("wg_capped", dict(vlm_wg_cap=1, graphs=True))]
         standalone = [g.run_frame(m, cfg, f)[0] for f in frames]
-    for mode, r in results.items():
-        assert np.array_equal(r, results["serial"]), mode
+        for mode, kw in modes:
+            name = mode + "".join(f"/{k}={v}" for k, v in kw.items() if k not in ("vlm_cus", "act_cus"))
+            for rep in range(3 if kw.get("graphs") else 1):
+                g.say(f"pipeline {name} replay {rep}")
+                out = torch.full_like(noise, float("nan"))
+                t = V.vla_pipeline_run(m, [d.c for d in dfs], noise, R, mode=mode, actions=out, **kw)
+                assert t["frames_per_s"] > 0
+                results[f"{name}#{rep}"] = out.cpu().numpy()
+                g.run_frame(m, cfg, frames[rep])  # eager work between replays
+    ref = results["serial#0"]
+    for key, r in results.items():
+        assert np.array_equal(r, ref), key
     for i in range(R):
-        assert np.array_equal(results["serial"][i].astype(np.float64), standalone[i])
+        assert np.array_equal(ref[i].astype(np.float64), standalone[i])
     # and the pipeline is the oracle's function of each frame
     P = synth.make_params(cfg, 11)
     for i in (0, R - 1):
         want = O.forward(P, cfg, frames[i])
-        assert np.abs(results["serial"][i] - want).max() <= CHUNK_TOL[cfg["dtype"]]
+        assert np.abs(ref[i] - want).max() <= CHUNK_TOL[cfg["dtype"]]
 
 
 def test_abi_errors_on_device(V):
