@@ -60,7 +60,20 @@ class VlaError(RuntimeError):
         self.code = code
 
 
+def _share_hip_runtime_with_torch():
+    # PyTorch ships its own copy of the HIP runtime under the same soname as
+    # the ROCm one the library links. One copy serves both only when torch
+    # loads first (libvla's dependency then resolves to it by soname);
+    # loading libvla first would bring in a second runtime and leave torch
+    # without a device. So torch, when present, is imported first.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
+
+
 def _load():
+    _share_hip_runtime_with_torch()
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python paper_2609_22335_amd/build.py`")
     lib = ctypes.CDLL(LIB_PATH)

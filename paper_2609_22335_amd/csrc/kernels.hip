@@ -187,7 +187,7 @@ __device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int 
 // visited grid-stride so a capped grid computes the same tiles.
 // ---------------------------------------------------------------------------
 
-template <typename T, int BM, int BN, int BK>
+template <typename T, int BM, int BN, int BK, int WGM>
 struct GemmSmem {
   static constexpr int VEC = 16 / sizeof(T);
   static constexpr int LDS = BK + VEC;
@@ -197,29 +197,31 @@ struct GemmSmem {
       T a[2][BM * LDS];
       T b[2][BN * LDS];
     } ld;
-    float c[BM * CLD];
+    float c[WGM * 16 * CLD];  // one 16-row slice of every wave row
   };
 };
 
-template <typename T, int BM, int BN, int BK>
-__global__ __launch_bounds__(256) void k_gemm(const T* __restrict__ A, int lda,
+template <typename T, int BM, int BN, int BK, int WGM = 2, int WGN = 2, int PD = 1>
+__global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A, int lda,
                                               const T* __restrict__ W, int ldw, int M, int N,
                                               int K, int kchunk, int splits, int tiles_m,
                                               int tiles_n, Epi e, float* __restrict__ part) {
-  using SM = GemmSmem<T, BM, BN, BK>;
+  using SM = GemmSmem<T, BM, BN, BK, WGM>;
   constexpr int VEC = SM::VEC;
   constexpr int SW = 4 * VEC;  // K covered by one MFMA step across the 4 lane groups
   constexpr int LDS = SM::LDS;
   constexpr int CLD = SM::CLD;
-  constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 16, TN = WN / 16;
+  constexpr int NT = 64 * WGM * WGN;  // threads: a WGM x WGN grid of waves
+  constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 16, TN = WN / 16;
   constexpr int KV = BK / VEC;
-  constexpr int AV = BM * KV / 256, BV = BN * KV / 256;
-  static_assert(AV >= 1 && BV >= 1 && (BM * KV) % 256 == 0 && (BN * KV) % 256 == 0, "tile");
+  constexpr int AV = BM * KV / NT, BV = BN * KV / NT;
+  static_assert(AV >= 1 && BV >= 1 && (BM * KV) % NT == 0 && (BN * KV) % NT == 0, "tile");
+  static_assert(WM % 16 == 0 && WN % 16 == 0, "wave tile");
   static_assert(BN % 32 == 0, "paired epilogues need 32-column groups");
   __shared__ __attribute__((aligned(16))) SM sm;
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WGN, wn = wave % WGN;
   const int ntiles = tiles_m * tiles_n * splits;
   const T dummy = T();
   const Rsrc ra_r = rsrc(A, span(M, lda, K, sizeof(T)));
@@ -239,49 +241,39 @@ __global__ __launch_bounds__(256) void k_gemm(const T* __restrict__ A, int lda,
 #pragma unroll
       for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    uint4 ra[AV], rb[BV];
-    auto gload = [&](int k0) {
+    // K-tiles it+1 .. it+PD are in registers (ring of PD buffers) while tile
+    // it is multiplied from LDS; the loop is unrolled by PD so every buffer
+    // index is a compile-time constant.
+    uint4 ra[PD][AV], rb[PD][BV];
+    auto gload = [&](int k0, uint4 (&xa)[AV], uint4 (&xb)[BV]) {
 #pragma unroll
       for (int i = 0; i < AV; ++i) {
-        const int c = tid + i * 256, r = c / KV, kc = (c % KV) * VEC;
+        const int c = tid + i * NT, r = c / KV, kc = (c % KV) * VEC;
         const int gm = m0 + r, gk = k0 + kc;
         const bool ok = gm < M && gk < kend;
-        ra[i] = bld16(ra_r, ok ? (uint32_t)(((size_t)gm * lda + gk) * sizeof(T)) : OOB);
+        xa[i] = bld16(ra_r, ok ? (uint32_t)(((size_t)gm * lda + gk) * sizeof(T)) : OOB);
       }
 #pragma unroll
       for (int i = 0; i < BV; ++i) {
-        const int c = tid + i * 256, r = c / KV, kc = (c % KV) * VEC;
+        const int c = tid + i * NT, r = c / KV, kc = (c % KV) * VEC;
         const int gn = n0 + r, gk = k0 + kc;
         const bool ok = gn < N && gk < kend;
-        rb[i] = bld16(rb_r, ok ? (uint32_t)(((size_t)gn * ldw + gk) * sizeof(T)) : OOB);
+        xb[i] = bld16(rb_r, ok ? (uint32_t)(((size_t)gn * ldw + gk) * sizeof(T)) : OOB);
       }
     };
-    auto sstore = [&](int buf) {
+    auto sstore = [&](int buf, const uint4 (&xa)[AV], const uint4 (&xb)[BV]) {
 #pragma unroll
       for (int i = 0; i < AV; ++i) {
-        const int c = tid + i * 256, r = c / KV, kc = (c % KV) * VEC;
-        *(uint4*)(sm.ld.a[buf] + r * LDS + kc) = ra[i];
+        const int c = tid + i * NT, r = c / KV, kc = (c % KV) * VEC;
+        *(uint4*)(sm.ld.a[buf] + r * LDS + kc) = xa[i];
       }
 #pragma unroll
       for (int i = 0; i < BV; ++i) {
-        const int c = tid + i * 256, r = c / KV, kc = (c % KV) * VEC;
-        *(uint4*)(sm.ld.b[buf] + r * LDS + kc) = rb[i];
+        const int c = tid + i * NT, r = c / KV, kc = (c % KV) * VEC;
+        *(uint4*)(sm.ld.b[buf] + r * LDS + kc) = xb[i];
       }
     };
-
-    __syncthreads();  // the previous tile's epilogue is done with the LDS
-    if (nk > 0) {
-      gload(kbeg);
-      sstore(0);
-      if (nk > 1) gload(kbeg + BK);
-    }
-    for (int it = 0; it < nk; ++it) {
-      __syncthreads();
-      const int buf = it & 1;
-      if (it + 1 < nk) {
-        sstore(buf ^ 1);
-        if (it + 2 < nk) gload(kbeg + (it + 2) * BK);
-      }
+    auto compute = [&](int buf) {
       const T* sa = sm.ld.a[buf];
       const T* sb = sm.ld.b[buf];
 #pragma unroll
@@ -300,34 +292,62 @@ __global__ __launch_bounds__(256) void k_gemm(const T* __restrict__ A, int lda,
 #pragma unroll
           for (int j = 0; j < TN; ++j) acc[i][j] = mfma_step(af[i], bfg[j], acc[i][j], dummy);
       }
+    };
+    // iteration it: tile it+1 (ring slot (it+1) % PD) goes to LDS, tile
+    // it+1+PD is requested into the freed slot, tile it is multiplied. Loads
+    // and stores are issued unconditionally (tiles past the end read as zero
+    // through the buffer range check), so every path has the same loads in
+    // flight and each wait covers only the oldest ring slot.
+    auto step = [&](int it, uint4 (&xa)[AV], uint4 (&xb)[BV]) {
+      __syncthreads();
+      sstore((it + 1) & 1, xa, xb);
+      gload(kbeg + (it + 1 + PD) * BK, xa, xb);
+      if (it < nk) compute(it & 1);
+    };
+
+    __syncthreads();  // the previous tile's epilogue is done with the LDS
+    gload(kbeg, ra[0], rb[0]);
+    sstore(0, ra[0], rb[0]);
+    // the ring slots must be requested in the order the loop consumes them:
+    // the scheduler may not interleave them
+#pragma unroll
+    for (int q = 0; q < PD; ++q) {
+      gload(kbeg + (1 + q) * BK, ra[(1 + q) % PD], rb[(1 + q) % PD]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    for (int it = 0; it < nk; it += PD) {
+#pragma unroll
+      for (int q = 0; q < PD; ++q) step(it + q, ra[(q + 1) % PD], rb[(q + 1) % PD]);
     }
 
-    // accumulators -> LDS tile [BM][BN]
-    __syncthreads();
+    // epilogue in 16-row slices: slice i of every wave row goes through LDS,
+    // then all threads apply the epilogue with row-contiguous stores
+    float* P = (e.kind == EPI_PART ? (float*)e.out : part) + (size_t)s * M * N;
+    const bool direct = splits == 1 && e.kind != EPI_PART;
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+    for (int i = 0; i < TM; ++i) {
+      __syncthreads();
 #pragma unroll
       for (int j = 0; j < TN; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          sm.c[(wm * WM + i * 16 + (lane >> 4) * 4 + r) * CLD + wn * WN + j * 16 + (lane & 15)] =
-              acc[i][j][r];
-    __syncthreads();
-
-    constexpr int PAIRS = BM * (BN / 2);  // (row, 32-column group, j < 16)
-    if (splits == 1 && e.kind != EPI_PART) {
-      for (int p = tid; p < PAIRS; p += 256) {
-        const int row = p / (BN / 2), q = p % (BN / 2);
-        const int col = (q >> 4) * 32 + (q & 15);
-        epi_pair<T>(e, M, N, m0 + row, n0 + col, sm.c[row * CLD + col], sm.c[row * CLD + col + 16]);
-      }
-    } else {
-      // raw fp32 partial of split s: [splits][M][N]
-      float* P = (e.kind == EPI_PART ? (float*)e.out : part) + (size_t)s * M * N;
-      for (int p = tid; p < BM * BN; p += 256) {
-        const int row = p / BN, col = p % BN;
-        const int m = m0 + row, n = n0 + col;
-        if (m < M && n < N) P[(size_t)m * N + n] = sm.c[row * CLD + col];
+          sm.c[(wm * 16 + (lane >> 4) * 4 + r) * CLD + wn * WN + j * 16 + (lane & 15)] = acc[i][j][r];
+      __syncthreads();
+      if (direct) {
+        constexpr int PAIRS = WGM * 16 * (BN / 2);  // (row, 32-column group, j < 16)
+        for (int p = tid; p < PAIRS; p += NT) {
+          const int row = p / (BN / 2), q = p % (BN / 2);
+          const int col = (q >> 4) * 32 + (q & 15);
+          const int m = m0 + (row >> 4) * WM + i * 16 + (row & 15);
+          epi_pair<T>(e, M, N, m, n0 + col, sm.c[row * CLD + col], sm.c[row * CLD + col + 16]);
+        }
+      } else {
+        // raw fp32 partial of split s: [splits][M][N]
+        for (int p = tid; p < WGM * 16 * BN; p += NT) {
+          const int row = p / BN, col = p % BN;
+          const int m = m0 + (row >> 4) * WM + i * 16 + (row & 15), n = n0 + col;
+          if (m < M && n < N) P[(size_t)m * N + n] = sm.c[row * CLD + col];
+        }
       }
     }
   }
@@ -376,7 +396,7 @@ __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, int lda
   constexpr int VEC = 16 / sizeof(T);
   constexpr int SW = 4 * VEC;
   __shared__ float red[4][8][4][64];  // [wave][n-block * 4 + m-tile][r][lane]
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int npairs = (N + 31) / 32;
   const int nslab = (K + SW - 1) / SW;
   const int total = npairs * splits;
@@ -501,8 +521,10 @@ static hipError_t launch_skinny(const GemmDesc& g, const Scratch& s, const Launc
 struct TileCfg {
   int bm, bn, bk;
 };
-// bf16 configurations, then fp32 ones.
-static const TileCfg kBf16Cfg[] = {{128, 128, 64}, {64, 128, 64}, {64, 64, 64}, {32, 64, 64}};
+// bf16 configurations, then fp32 ones. Wide GEMMs (enough 128 x 128 tiles to
+// cover every CU) take the large tile; everything else takes 64 x 64 tiles,
+// which keep more loads in flight per CU for these M ~ 256..320 shapes.
+static const TileCfg kBf16Cfg[] = {{128, 128, 64}, {64, 64, 64}, {32, 64, 64}};
 static const TileCfg kF32Cfg[] = {{64, 64, 32}, {32, 64, 32}};
 
 GemmPlan plan_gemm(const GemmDesc& g) {
@@ -517,26 +539,27 @@ GemmPlan plan_gemm(const GemmDesc& g) {
   const TileCfg* cfgs = g.dtype == DT_BF16 ? kBf16Cfg : kF32Cfg;
   int c;
   if (g.dtype == DT_BF16) {
-    if (g.M >= 256) {
-      const int t128 = ((g.M + 127) / 128) * ((g.N + 127) / 128);
-      c = t128 >= NUM_CU_PLAN ? 0 : 1;
-    } else if (g.M > 32) {
-      c = 2;
-    } else {
-      c = 3;
-    }
+    const int t128 = ((g.M + 127) / 128) * ((g.N + 127) / 128);
+    if (g.M >= 256 && t128 >= NUM_CU_PLAN) c = 0;
+    else if (g.M > 32) c = 1;
+    else c = 2;
   } else {
     c = g.M > 32 ? 0 : 1;
   }
   const TileCfg t = cfgs[c];
   const int tm = (g.M + t.bm - 1) / t.bm, tn = (g.N + t.bn - 1) / t.bn;
   const int tiles = tm * tn;
-  int splits = 1;
   const int kblocks = (g.K + t.bk - 1) / t.bk;
-  if (tiles < NUM_CU_PLAN && kblocks >= 4) {
-    splits = std::min((NUM_CU_PLAN + tiles - 1) / tiles, kblocks / 2);
-    splits = std::max(splits, 1);
-  }
+  // Split K where it is free: partial sums (EPI_PART) are added by their
+  // consumer, so aim for two workgroups per CU with at least four K-blocks
+  // each. Other epilogues need a separate reduction pass, so only very
+  // small tile counts are split.
+  int splits = 1;
+  if (g.epi.kind == EPI_PART && tiles < 2 * NUM_CU_PLAN)
+    splits = std::min((2 * NUM_CU_PLAN + tiles - 1) / tiles, std::max(1, kblocks / 4));
+  else if (tiles < 32 && kblocks >= 16)
+    splits = std::min(NUM_CU_PLAN / tiles, kblocks / 4);
+  splits = std::max(splits, 1);
   const int kchunk_blocks = (kblocks + splits - 1) / splits;
   splits = (kblocks + kchunk_blocks - 1) / kchunk_blocks;
   p.cfg = c;
@@ -546,7 +569,7 @@ GemmPlan plan_gemm(const GemmDesc& g) {
   return p;
 }
 
-template <typename T, int BM, int BN, int BK>
+template <typename T, int BM, int BN, int BK, int WGM = 2, int WGN = 2, int PD = 1>
 static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch& s,
                              const LaunchCaps& caps, hipStream_t st) {
   const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
@@ -554,7 +577,8 @@ static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch
   const int kchunk = ((kblocks + p.splits - 1) / p.splits) * BK;
   int grid = p.tiles;
   if (caps.max_wgs > 0) grid = std::min(grid, caps.max_wgs);
-  hipExtLaunchKernelGGL((k_gemm<T, BM, BN, BK>), dim3(grid), dim3(256), 0, st, caps.ev_start,
+  hipExtLaunchKernelGGL((k_gemm<T, BM, BN, BK, WGM, WGN, PD>), dim3(grid), dim3(64 * WGM * WGN), 0, st,
+                        caps.ev_start,
                         caps.ev_stop, 0, (const T*)g.A, g.lda, (const T*)g.W, g.ldw, g.M, g.N,
                         g.K, kchunk, p.splits, tiles_m, tiles_n, g.epi, s.ptr);
   if (p.splits > 1 && g.epi.kind != EPI_PART) {
@@ -577,15 +601,14 @@ hipError_t launch_gemm(const GemmDesc& g, const Scratch& s, const LaunchCaps& ca
   }
   if (g.dtype == DT_BF16) {
     switch (p.cfg) {
-      case 0: return run_gemm_t<uint16_t, 128, 128, 64>(g, p, s, caps, st);
-      case 1: return run_gemm_t<uint16_t, 64, 128, 64>(g, p, s, caps, st);
-      case 2: return run_gemm_t<uint16_t, 64, 64, 64>(g, p, s, caps, st);
-      default: return run_gemm_t<uint16_t, 32, 64, 64>(g, p, s, caps, st);
+      case 0: return run_gemm_t<uint16_t, 128, 128, 64, 2, 2, 3>(g, p, s, caps, st);
+      case 1: return run_gemm_t<uint16_t, 64, 64, 64, 2, 2, 2>(g, p, s, caps, st);
+      default: return run_gemm_t<uint16_t, 32, 64, 64, 2, 2, 2>(g, p, s, caps, st);
     }
   }
   switch (p.cfg) {
-    case 0: return run_gemm_t<float, 64, 64, 32>(g, p, s, caps, st);
-    default: return run_gemm_t<float, 32, 64, 32>(g, p, s, caps, st);
+    case 0: return run_gemm_t<float, 64, 64, 32, 2, 2, 2>(g, p, s, caps, st);
+    default: return run_gemm_t<float, 32, 64, 32, 2, 2, 2>(g, p, s, caps, st);
   }
 }
 
@@ -630,7 +653,7 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) T sVt[HDP * VS];
   __shared__ __attribute__((aligned(16))) float sP[4 * 16 * PS];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int group = a.nq / a.nkv;
   const int R = a.Sq * group;
   const int Skv = a.S0 + a.S1;
@@ -686,6 +709,10 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
     for (int b = b0; b < b1; ++b) {
       __syncthreads();
       constexpr int NV = ATT_BKV * (HDP / VEC);
+      // a block inside segment 0 reads one buffer; a block that reaches into
+      // segment 1 reads both with the other one's offset out of range (zero)
+      // and merges them, so the buffer choice never depends on the lane
+      const bool only0 = (b + 1) * ATT_BKV <= a.S0;
       for (int c = tid; c < NV; c += 256) {
         const int kk = c / (HDP / VEC), d = (c % (HDP / VEC)) * VEC;
         const int key = b * ATT_BKV + kk;
@@ -694,8 +721,17 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
         const uint32_t off = ok ? (uint32_t)(((size_t)(s0 ? key : key - a.S0) * a.ldkv + j * a.hd + d) *
                                              sizeof(T))
                                 : OOB;
-        const uint4 kv = s0 ? bld16(rk0, off) : bld16(rk1, off);
-        const uint4 vv = s0 ? bld16(rv0, off) : bld16(rv1, off);
+        uint4 kv, vv;
+        if (only0) {
+          kv = bld16(rk0, off);
+          vv = bld16(rv0, off);
+        } else {
+          const uint32_t o0 = s0 ? off : OOB, o1 = s0 ? OOB : off;
+          const uint4 ka = bld16(rk0, o0), kb = bld16(rk1, o1);
+          const uint4 va = bld16(rv0, o0), vb = bld16(rv1, o1);
+          kv = make_uint4(ka.x | kb.x, ka.y | kb.y, ka.z | kb.z, ka.w | kb.w);
+          vv = make_uint4(va.x | vb.x, va.y | vb.y, va.z | vb.z, va.w | vb.w);
+        }
         *(uint4*)(sK + kk * KS + d) = kv;
         const T* ve = (const T*)&vv;
 #pragma unroll
@@ -954,11 +990,20 @@ hipError_t launch_attention(const AttnDesc& d, const Scratch& s, const LaunchCap
 // so 16-byte loads stay aligned). The key space is [segment 0 padded to a
 // multiple of 32; segment 1 padded likewise]; keys past a segment's length
 // get a -inf score. A workgroup owns 16 packed query rows (row r <-> query
-// r / group, head r % group of one KV head); its four waves take every
-// fourth 32-key block, with the next block's K and V prefetched into
-// registers, and keep an fp32 online softmax. P V runs on MFMA with P split
-// into bf16 high and remainder parts (bf16) or directly (fp32). The four
-// waves' (max, sum, O) are merged through LDS in wave order.
+// r / group, head r % group of one KV head) and its NW waves take every
+// NW-th 32-key block, with the next block's K and V prefetched into
+// registers.
+//
+// Everything is computed transposed, so the probabilities never leave the
+// registers: S^T = K Q^T puts one query per lane column and keys on the
+// rows, and O^T += V^T P^T takes P^T as the B operand straight from the
+// score registers. For that the K rows of a 16-key tile are loaded in the
+// order that makes each lane's score registers hold exactly the keys its
+// B-operand slice needs, which are also the keys one 16-byte V^T load
+// returns. The online softmax is fp32 with one running max per query
+// (reduced across the four lane groups) and per-lane partial sums, reduced
+// once at the end; P is split into bf16 high and remainder parts for the
+// bf16 MFMA. The waves' (max, sum, O) are merged through LDS in wave order.
 // ---------------------------------------------------------------------------
 
 struct Attn2Args {
@@ -974,62 +1019,79 @@ struct Attn2Args {
   float scale_log2;
 };
 
+// waves per workgroup: eight, or four where a wave needs more than the 256
+// registers eight waves leave it
 template <typename T, int HDP>
-__global__ __launch_bounds__(256) void k_attn2(Attn2Args a) {
+constexpr int att2_waves() {
+  return HDP * (int)sizeof(T) >= 512 ? 4 : 8;
+}
+
+// Key (within its 32-key block) held in score row i (0..15) of tile nt, so
+// that lane group g's rows {4g..4g+3} of both tiles are the keys of its
+// B-operand slice of P^T: keys 8g..8g+7 for bf16 (one 32-key slab), keys
+// 16 nt + 4g..4g+3 for fp32 (two 16-key slabs).
+template <typename T>
+__device__ __forceinline__ int att2_key(int nt, int i) {
+  if constexpr (sizeof(T) == 2) return 8 * (i >> 2) + 4 * nt + (i & 3);
+  return 16 * nt + i;
+}
+
+template <typename T, int HDP, int NW>
+__global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
   constexpr int VEC = 16 / sizeof(T);
   constexpr int SW = 4 * VEC;
   constexpr int NQF = HDP / SW;   // Q fragments (also K fragments per 16-key tile)
-  constexpr int NOT = HDP / 16;   // output column tiles
+  constexpr int NOT = HDP / 16;   // 16-row tiles of O^T
   constexpr int PVS = 32 / SW;    // P V slabs per 32-key block
-  constexpr int PS = 36;          // sP row stride
-  constexpr int OS = HDP + 4;     // sO row stride
-  __shared__ __attribute__((aligned(16))) float sP[4][16 * PS];
-  __shared__ float sO[4][16 * OS];
-  __shared__ float sM[4][16], sL[4][16];
+  constexpr int OS = HDP + 4;     // sO row stride (floats)
+  constexpr int NT = 64 * NW;
+  __shared__ __attribute__((aligned(16))) float sO[NW][16 * OS];
+  __shared__ float sM[NW][16], sL[NW][16];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int g4 = lane >> 4;  // lane group
   const int group = a.nq / a.nkv;
   const int R = a.Sq * group;
   const int S0p = (a.S0 + 31) / 32 * 32, S1p = (a.S1 + 31) / 32 * 32;
   const int nblk = (S0p + S1p) / 32;
   const int total = a.rtiles * a.nkv;
   const T dummy = T();
+  const Rsrc rq = rsrc(a.q, span(a.Sq, a.ldq, a.nq * a.hd, sizeof(T)));
+  const Rsrc rk0 = rsrc(a.k0, span(a.S0, a.ldk, a.nkv * a.hd, sizeof(T)));
+  const Rsrc rv0 = rsrc(a.vt0, (size_t)a.nkv * a.hd * a.ldvt0 * sizeof(T));
+  const Rsrc rk1 = rsrc(a.k1 ? a.k1 : a.k0, a.k1 ? span(a.S1, a.ldk, a.nkv * a.hd, sizeof(T)) : 0);
+  const Rsrc rv1 = rsrc(a.vt1 ? a.vt1 : a.vt0, a.vt1 ? (size_t)a.nkv * a.hd * a.ldvt1 * sizeof(T) : 0);
 
   for (int w = blockIdx.x; w < total; w += gridDim.x) {
     const int rt = w % a.rtiles, j = w / a.rtiles;
-    const Rsrc rq = rsrc(a.q, span(a.Sq, a.ldq, a.nq * a.hd, sizeof(T)));
-    const Rsrc rk0 = rsrc(a.k0, span(a.S0, a.ldk, a.nkv * a.hd, sizeof(T)));
-    const Rsrc rv0 = rsrc(a.vt0, (size_t)a.nkv * a.hd * a.ldvt0 * sizeof(T));
-    const Rsrc rk1 = rsrc(a.k1 ? a.k1 : a.k0, a.k1 ? span(a.S1, a.ldk, a.nkv * a.hd, sizeof(T)) : 0);
-    const Rsrc rv1 = rsrc(a.vt1 ? a.vt1 : a.vt0, a.vt1 ? (size_t)a.nkv * a.hd * a.ldvt1 * sizeof(T) : 0);
 
+    // Q^T as the B operand: lane column = packed row, 16-byte slice of d
     uint4 qf[NQF];
     {
       const int r = rt * 16 + (lane & 15);
       const int sq = r / group, h = j * group + r % group;
 #pragma unroll
       for (int ks = 0; ks < NQF; ++ks) {
-        const int d = ks * SW + (lane >> 4) * VEC;
+        const int d = ks * SW + g4 * VEC;
         const bool ok = r < R && d < a.hd;
         qf[ks] = bld16(rq, ok ? (uint32_t)(((size_t)sq * a.ldq + h * a.hd + d) * sizeof(T)) : OOB);
       }
     }
 
-    // fragment loads of one 32-key block
     auto load_k = [&](int b, uint4 (&kf)[2][NQF]) {
       const int kb = b * 32;
       const bool seg1 = kb >= S0p;
       const int kloc = seg1 ? kb - S0p : kb;
       const int slen = seg1 ? a.S1 : a.S0;
+      const Rsrc rk = seg1 ? rk1 : rk0;
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt) {
-        const int key = kloc + nt * 16 + (lane & 15);
+        const int key = kloc + att2_key<T>(nt, lane & 15);
 #pragma unroll
         for (int ks = 0; ks < NQF; ++ks) {
-          const int d = ks * SW + (lane >> 4) * VEC;
-          const bool ok = key < slen && d < a.hd;
-          const uint32_t off = ok ? (uint32_t)(((size_t)key * a.ldk + j * a.hd + d) * sizeof(T)) : OOB;
-          kf[nt][ks] = seg1 ? bld16(rk1, off) : bld16(rk0, off);
+          const int d = ks * SW + g4 * VEC;
+          const bool ok = b < nblk && key < slen && d < a.hd;
+          kf[nt][ks] = bld16(rk, ok ? (uint32_t)(((size_t)key * a.ldk + j * a.hd + d) * sizeof(T)) : OOB);
         }
       }
     };
@@ -1038,147 +1100,151 @@ __global__ __launch_bounds__(256) void k_attn2(Attn2Args a) {
       const bool seg1 = kb >= S0p;
       const int ldvt = seg1 ? a.ldvt1 : a.ldvt0;
       const int kloc = seg1 ? kb - S0p : kb;
+      const Rsrc rv = seg1 ? rv1 : rv0;
 #pragma unroll
       for (int dt = 0; dt < NOT; ++dt) {
         const int d = dt * 16 + (lane & 15);
 #pragma unroll
         for (int kk = 0; kk < PVS; ++kk) {
-          const int key = kloc + kk * SW + (lane >> 4) * VEC;
-          const bool ok = d < a.hd;
-          const uint32_t off = ok ? (uint32_t)(((size_t)(j * a.hd + d) * ldvt + key) * sizeof(T)) : OOB;
-          vf[dt][kk] = seg1 ? bld16(rv1, off) : bld16(rv0, off);
+          const int key = kloc + kk * SW + g4 * VEC;
+          const bool ok = b < nblk && d < a.hd;
+          vf[dt][kk] = bld16(rv, ok ? (uint32_t)(((size_t)(j * a.hd + d) * ldvt + key) * sizeof(T)) : OOB);
         }
       }
     };
 
-    float mrow[4], lrow[4];
+    float mrun = -INFINITY, lpart = 0.f;  // running max of this lane's query; partial sum
     f32x4 o[NOT];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      mrow[r] = -INFINITY;
-      lrow[r] = 0.f;
-    }
 #pragma unroll
     for (int d = 0; d < NOT; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    float* myP = sP[wave];
-    // one 32-key block: scores, online softmax, P through LDS, P V
-    // The next block's K is requested as soon as the scores are formed and its V
-    // as soon as P V is done, so loads overlap the rest of the block.
     uint4 kf[2][NQF], vf[NOT][PVS];
     auto process = [&](int b) {
       const int kb = b * 32;
       const bool seg1 = kb >= S0p;
       const int kloc = seg1 ? kb - S0p : kb;
       const int slen = seg1 ? a.S1 : a.S0;
-      f32x4 sacc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+      // S^T for 32 keys x 16 queries, two accumulators per tile
+      f32x4 sacc[2][2];
+#pragma unroll
+      for (int nt = 0; nt < 2; ++nt) sacc[nt][0] = sacc[nt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < NQF; ++ks)
+#pragma unroll
+        for (int nt = 0; nt < 2; ++nt) sacc[nt][ks & 1] = mfma_step(kf[nt][ks], qf[ks], sacc[nt][ks & 1], dummy);
+      load_k(b + NW, kf);
+      float p[2][4];
+      float mx = -INFINITY;
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
-        for (int ks = 0; ks < NQF; ++ks) sacc[nt] = mfma_step(qf[ks], kf[nt][ks], sacc[nt], dummy);
-      if (b + 4 < nblk) load_k(b + 4, kf);
-      float p[2][4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float mx = -INFINITY;
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-          const int key = kloc + nt * 16 + (lane & 15);
-          const float sv = key < slen ? sacc[nt][r] * a.scale_log2 : -INFINITY;
+        for (int r = 0; r < 4; ++r) {
+          const int key = kloc + att2_key<T>(nt, 4 * g4 + r);
+          const float sv = key < slen ? (sacc[nt][0][r] + sacc[nt][1][r]) * a.scale_log2 : -INFINITY;
           p[nt][r] = sv;
           mx = fmaxf(mx, sv);
         }
-#pragma unroll
-        for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
-        const float mnew = fmaxf(mrow[r], mx);
-        // a block can be entirely padding: keep everything at zero then
-        const float alpha = mnew == -INFINITY ? 1.f : exp2f(mrow[r] - mnew);
-        float sum = 0.f;
-#pragma unroll
-        for (int nt = 0; nt < 2; ++nt) {
-          p[nt][r] = mnew == -INFINITY ? 0.f : exp2f(p[nt][r] - mnew);
-          sum += p[nt][r];
-        }
-#pragma unroll
-        for (int off = 1; off < 16; off <<= 1) sum += __shfl_xor(sum, off);
-        lrow[r] = lrow[r] * alpha + sum;
-        mrow[r] = mnew;
-#pragma unroll
-        for (int d = 0; d < NOT; ++d) o[d][r] *= alpha;
-      }
+      mx = fmaxf(mx, __shfl_xor(mx, 16));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mnew = fmaxf(mrun, mx);
+      // a block can be entirely padding: keep everything at zero then
+      const float alpha = mnew == -INFINITY ? 1.f : exp2f(mrun - mnew);
+      float sum = 0.f;
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) myP[((lane >> 4) * 4 + r) * PS + nt * 16 + (lane & 15)] = p[nt][r];
-      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's LDS writes are done
-      __builtin_amdgcn_wave_barrier();
+        for (int r = 0; r < 4; ++r) {
+          p[nt][r] = mnew == -INFINITY ? 0.f : exp2f(p[nt][r] - mnew);
+          sum += p[nt][r];
+        }
+      lpart = lpart * alpha + sum;
+      mrun = mnew;
 #pragma unroll
-      for (int kk = 0; kk < PVS; ++kk) {
-        const float* pr = myP + (lane & 15) * PS + kk * SW + (lane >> 4) * VEC;
-        if constexpr (sizeof(T) == 2) {
-          uint32_t hi[4], lo[4];
+      for (int d = 0; d < NOT; ++d) o[d] *= alpha;
+      if constexpr (sizeof(T) == 2) {
+        uint32_t hi[4], lo[4];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float x0 = pr[2 * q], x1 = pr[2 * q + 1];
-            const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
-            const uint16_t l0 = f2bf(x0 - bf2f(h0)), l1 = f2bf(x1 - bf2f(h1));
-            hi[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-            lo[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
-          }
-          const uint4 phi = make_uint4(hi[0], hi[1], hi[2], hi[3]);
-          const uint4 plo = make_uint4(lo[0], lo[1], lo[2], lo[3]);
+        for (int q = 0; q < 4; ++q) {
+          const float x0 = p[q >> 1][2 * (q & 1)], x1 = p[q >> 1][2 * (q & 1) + 1];
+          const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
+          const uint16_t l0 = f2bf(x0 - bf2f(h0)), l1 = f2bf(x1 - bf2f(h1));
+          hi[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+          lo[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+        }
+        const uint4 phi = make_uint4(hi[0], hi[1], hi[2], hi[3]);
+        const uint4 plo = make_uint4(lo[0], lo[1], lo[2], lo[3]);
 #pragma unroll
-          for (int d = 0; d < NOT; ++d) {
-            o[d] = mfma_step(phi, vf[d][kk], o[d], dummy);
-            o[d] = mfma_step(plo, vf[d][kk], o[d], dummy);
-          }
-        } else {
-          const uint4 pf = make_uint4(__float_as_uint(pr[0]), __float_as_uint(pr[1]),
-                                      __float_as_uint(pr[2]), __float_as_uint(pr[3]));
+        for (int d = 0; d < NOT; ++d) {
+          o[d] = mfma_step(vf[d][0], phi, o[d], dummy);
+          o[d] = mfma_step(vf[d][0], plo, o[d], dummy);
+        }
+      } else {
 #pragma unroll
-          for (int d = 0; d < NOT; ++d) o[d] = mfma_step(pf, vf[d][kk], o[d], dummy);
+        for (int kk = 0; kk < PVS; ++kk) {
+          const uint4 pf = make_uint4(__float_as_uint(p[kk][0]), __float_as_uint(p[kk][1]),
+                                      __float_as_uint(p[kk][2]), __float_as_uint(p[kk][3]));
+#pragma unroll
+          for (int d = 0; d < NOT; ++d) o[d] = mfma_step(vf[d][kk], pf, o[d], dummy);
         }
       }
-      if (b + 4 < nblk) load_v(b + 4, vf);
-      __builtin_amdgcn_wave_barrier();
+      load_v(b + NW, vf);
     };
 
-    for (int b = wave; b < nblk; b += 4) {
-      if (b == wave) {
-        load_k(b, kf);
-        load_v(b, vf);
-      }
-      process(b);
-    }
+    // Loads are issued unconditionally (blocks past the end read as zero
+    // through the range check): with the same loads in flight on every path
+    // each wait covers only the oldest group.
+    load_k(wave, kf);
+    load_v(wave, vf);
+    for (int b = wave; b < nblk; b += NW) process(b);
 
-    // merge the four waves in order
+    // the four lane groups' partial sums of one query
+    lpart += __shfl_xor(lpart, 16);
+    lpart += __shfl_xor(lpart, 32);
+    // O^T registers: lane column = packed row (lane & 15), rows d = 16 dt + 4 g4 + r
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int rr = (lane >> 4) * 4 + r;
-#pragma unroll
-      for (int d = 0; d < NOT; ++d) sO[wave][rr * OS + d * 16 + (lane & 15)] = o[d][r];
-      if ((lane & 15) == 0) {
-        sM[wave][rr] = mrow[r];
-        sL[wave][rr] = lrow[r];
-      }
+    for (int d = 0; d < NOT; ++d)
+      *(f32x4*)&sO[wave][(lane & 15) * OS + d * 16 + 4 * g4] = o[d];
+    if (g4 == 0) {
+      sM[wave][lane] = mrun;
+      sL[wave][lane] = lpart;
     }
     __syncthreads();
-    for (int idx = tid; idx < 16 * HDP; idx += 256) {
-      const int rr = idx / HDP, d = idx % HDP;
+    // merge the waves in order; eight consecutive outputs per thread
+    for (int idx = tid * 8; idx < 16 * HDP; idx += NT * 8) {
+      const int rr = idx / HDP, d0 = idx % HDP;
       const int prow = rt * 16 + rr;
-      if (prow >= R || d >= a.hd) continue;
+      if (prow >= R || d0 >= a.hd) continue;
       float mx = -INFINITY;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) mx = fmaxf(mx, sM[u][rr]);
-      float num = 0.f, den = 0.f;
+      for (int u = 0; u < NW; ++u) mx = fmaxf(mx, sM[u][rr]);
+      float num[8], den = 0.f;
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
+      for (int e = 0; e < 8; ++e) num[e] = 0.f;
+#pragma unroll
+      for (int u = 0; u < NW; ++u) {
         const float wgt = sM[u][rr] == -INFINITY ? 0.f : exp2f(sM[u][rr] - mx);
-        num += wgt * sO[u][rr * OS + d];
+        const f32x4 v0 = *(const f32x4*)&sO[u][rr * OS + d0];
+        const f32x4 v1 = *(const f32x4*)&sO[u][rr * OS + d0 + 4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          num[e] += wgt * v0[e];
+          num[4 + e] += wgt * v1[e];
+        }
         den += wgt * sL[u][rr];
       }
+      const float inv = 1.f / den;
       const int sq = prow / group, h = j * group + prow % group;
-      TT<T>::st((T*)a.out + (size_t)sq * a.ldo + h * a.hd + d, num / den);
+      T* op = (T*)a.out + (size_t)sq * a.ldo + h * a.hd + d0;
+      if constexpr (sizeof(T) == 2) {
+        uint32_t pk[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          pk[e] = (uint32_t)f2bf(num[2 * e] * inv) | ((uint32_t)f2bf(num[2 * e + 1] * inv) << 16);
+        *(uint4*)op = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+      } else {
+        *(float4*)op = make_float4(num[0] * inv, num[1] * inv, num[2] * inv, num[3] * inv);
+        *(float4*)(op + 4) = make_float4(num[4] * inv, num[5] * inv, num[6] * inv, num[7] * inv);
+      }
     }
     __syncthreads();
   }
@@ -1190,14 +1256,16 @@ static hipError_t run_attn2_t(const Attn2Args& a, int hdp, const LaunchCaps& cap
   int grid = a.rtiles * a.nkv;
   if (caps.max_wgs > 0) grid = std::min(grid, caps.max_wgs);
 #define VLA_ATTN2(H)                                                                           \
-  hipExtLaunchKernelGGL((k_attn2<T, H>), dim3(grid), dim3(256), 0, st, caps.ev_start, caps.ev_stop, \
-                        0, a)
+  hipExtLaunchKernelGGL((k_attn2<T, H, att2_waves<T, H>()>), dim3(grid),                        \
+                        dim3(64 * att2_waves<T, H>()), 0, st, caps.ev_start, caps.ev_stop, 0, a)
   switch (hdp) {
     case 32: VLA_ATTN2(32); break;
     case 64: VLA_ATTN2(64); break;
     case 96: VLA_ATTN2(96); break;
     case 128: VLA_ATTN2(128); break;
-    case 256: VLA_ATTN2(256); break;
+    case 256:
+      if constexpr (sizeof(T) == 2) VLA_ATTN2(256);
+      break;
     default: return hipErrorInvalidValue;
   }
 #undef VLA_ATTN2
@@ -1208,7 +1276,8 @@ hipError_t launch_attention_vt(const AttnVtDesc& d, const LaunchCaps& caps, hipS
   const int hdp = attn_hdp(d.hd, d.dtype);
   if (hdp < 0 || d.nq % d.nkv != 0 || d.S0 <= 0 || d.S1 < 0 || d.Sq <= 0 ||
       (d.S1 > 0 && (!d.k1 || !d.vt1)) || d.ldvt0 < (d.S0 + 31) / 32 * 32 ||
-      (d.S1 > 0 && d.ldvt1 < (d.S1 + 31) / 32 * 32))
+      (d.S1 > 0 && d.ldvt1 < (d.S1 + 31) / 32 * 32) || d.hd % 8 != 0 ||
+      ((size_t)d.ldo * (d.dtype == DT_BF16 ? 2 : 4)) % 16 != 0 || ((uintptr_t)d.out & 15) != 0)
     return hipErrorInvalidValue;
   Attn2Args a{};
   a.q = d.q;
@@ -1242,7 +1311,7 @@ hipError_t launch_attention_vt(const AttnVtDesc& d, const LaunchCaps& caps, hipS
 __device__ __forceinline__ float block_sum(float v, float* red) {
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   __syncthreads();
   if (lane == 0) red[wave] = v;
   __syncthreads();

@@ -37,7 +37,7 @@ RNG = np.random.default_rng(7)
 GEMM_SHAPES = [
     (1, 64, 8), (7, 3, 16), (21, 136, 64), (40, 100, 592), (50, 2560, 1024), (50, 1024, 4096),
     (64, 64, 64), (33, 128, 256), (256, 3456, 1152), (305, 2048, 2048), (512, 8192, 256),
-    (833, 200, 72),
+    (833, 200, 72), (300, 33000, 200),
 ]
 
 
@@ -177,10 +177,14 @@ PHASE_CFGS = [
 def _kv_tol(cfg, ref):
     if cfg["dtype"] == synth.F32:
         return 1e-4
-    # both sides store K/V in bf16; fp32-vs-fp64 differences before the
-    # rounding flip an element by one bf16 ulp (2^-7 relative at most) and
-    # such flips propagate through later layers at the same order
-    return 2.0 ** -5 * np.abs(ref) + 2e-3
+    # Both sides store K/V in bf16 and round every operand at the same
+    # points; fp32-vs-fp64 accumulation differences flip roundings by one
+    # bf16 ulp (2^-8 relative) and those flips travel through every earlier
+    # layer, so an element's deviation scales with the tensor's magnitude
+    # rather than its own: bound it by 2^-5 of its value plus 2^-4 of the
+    # tensor's rms (a structural mistake moves elements by ~ the rms).
+    rms = float(np.sqrt(np.mean(np.square(ref))))
+    return 2.0 ** -5 * np.abs(ref) + 2.0 ** -4 * rms
 
 
 @pytest.mark.parametrize("name,cfg", PHASE_CFGS, ids=[p[0] for p in PHASE_CFGS])
