@@ -123,9 +123,10 @@ int vla_create(const vla_config* cfg, uint64_t seed, vla_model** out);
 int vla_destroy(vla_model* m);
 
 /* Phase-1 -> phase-2 hand-off: the per-layer KV cache of the model's storage
- * type, K [lm_layers][prefix][lm_kv_heads * head_dim] and V transposed
- * [lm_layers][lm_kv_heads * head_dim][prefix rounded up to 32]. Caller-owned
- * via these two calls; destroy NULL is a no-op. */
+ * type, in the layout the attention kernel reads (MFMA fragment order, keys
+ * in blocks of 32; documented at vla_debug_attention_cache), prefix rounded
+ * up to 32 keys per KV head; vla_ctx_export_kv returns it row-major.
+ * Caller-owned via these two calls; destroy NULL is a no-op. */
 int vla_ctx_create(vla_model* m, vla_ctx** out);
 int vla_ctx_destroy(vla_ctx* c);
 
@@ -183,13 +184,22 @@ int vla_debug_attention(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int3
                         const void* v1, int32_t S1, void* out, void* stream);
 
 /* Test entry point for the attention kernel of the LM and the expert: as
- * vla_debug_attention, but V is passed transposed and zero-padded: vt0
- * [nkv*hd][ldvt0 >= S0 rounded up to 32], vt1 [nkv*hd][ldvt1 >= S1 rounded
- * up to 32] (padding columns must hold zeros). All pointers device. */
-int vla_debug_attention_vt(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int32_t hd,
-                           const void* q, const void* k0, const void* vt0, int32_t S0, int32_t ldvt0,
-                           const void* k1, const void* vt1, int32_t S1, int32_t ldvt1, void* out,
-                           void* stream);
+ * vla_debug_attention (q and out row-major, out 16-byte aligned), but K and V
+ * of each segment are in the KV-cache layout, with nb = ceil(S / 32) blocks
+ * per KV head. With VEC = 8 (bf16) or 4 (fp32) elements per 16 bytes,
+ * SW = 4 VEC, NS = ceil(hd / SW), NDT = ceil(hd / 16), PVS = 32 / SW, key
+ * p = 32 b + kin (kin < 32) and head-dim index d of KV head j sit at
+ *   K: ((((j nb + b) 2 + nt) NS + d / SW) 64 + 16 ((d % SW) / VEC) + i) VEC + d % VEC
+ *      with (nt, i) = ((kin / 4) % 2, 4 (kin / 8) + kin % 4) for bf16 and
+ *      (kin / 16, kin % 16) for fp32;
+ *   V: ((((j nb + b) NDT + d / 16) PVS + kin / SW) 64 + 16 ((kin % SW) / VEC)
+ *      + d % 16) VEC + kin % VEC.
+ * Each 64 x VEC run is one MFMA operand load. V must be zero at keys
+ * S .. 32 nb - 1; other unused positions are never read into the result.
+ * fp32 needs hd <= 128. All pointers device. */
+int vla_debug_attention_cache(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int32_t hd,
+                              const void* q, const void* k0, const void* v0, int32_t S0, const void* k1,
+                              const void* v1, int32_t S1, void* out, void* stream);
 
 /* Kernel timer for measurement: while `tag` is set, every launch of the
  * kernels behind that call site (tags: "vit.patch", "vit.qkv", "vit.attn",

@@ -96,7 +96,7 @@ def _load():
         "vla_debug_gemm": [I32, I32, I32, I32, P, I32, P, I32, P, P, P],
         "vla_debug_attention": [I32, I32, I32, I32, I32, P, P, P, I32, P, P, I32, P, P],
         "vla_debug_generate": [U64, ctypes.c_char_p, I64, D, D, P],
-        "vla_debug_attention_vt": [I32, I32, I32, I32, I32, P, P, P, I32, I32, P, P, I32, I32, P, P],
+        "vla_debug_attention_cache": [I32, I32, I32, I32, I32, P, P, P, I32, P, P, I32, P, P],
         "vla_kernel_timer": [P, ctypes.c_char_p],
         "vla_kernel_timer_read": [P, ctypes.POINTER(D), ctypes.POINTER(I64)],
     }
@@ -226,10 +226,10 @@ def vla_debug_attention(dtype: int, Sq: int, nq: int, nkv: int, hd: int, q, k0, 
                                     _ptr(k1), _ptr(v1), S1, _ptr(out), stream or None))
 
 
-def vla_debug_attention_vt(dtype: int, Sq: int, nq: int, nkv: int, hd: int, q, k0, vt0, S0: int,
-                           ldvt0: int, k1, vt1, S1: int, ldvt1: int, out, stream: int = 0) -> None:
-    _check(_lib.vla_debug_attention_vt(dtype, Sq, nq, nkv, hd, _ptr(q), _ptr(k0), _ptr(vt0), S0, ldvt0,
-                                       _ptr(k1), _ptr(vt1), S1, ldvt1, _ptr(out), stream or None))
+def vla_debug_attention_cache(dtype: int, Sq: int, nq: int, nkv: int, hd: int, q, k0, v0, S0: int,
+                              k1, v1, S1: int, out, stream: int = 0) -> None:
+    _check(_lib.vla_debug_attention_cache(dtype, Sq, nq, nkv, hd, _ptr(q), _ptr(k0), _ptr(v0), S0,
+                                          _ptr(k1), _ptr(v1), S1, _ptr(out), stream or None))
 
 
 def vla_kernel_timer(model: int, tag: Optional[str]) -> None:
@@ -254,6 +254,6 @@ def exported_symbols() -> Iterable[str]:
     return ["vla_preset", "vla_validate", "vla_create", "vla_destroy", "vla_ctx_create",
             "vla_ctx_destroy", "vla_vlm_prefill", "vla_action_denoise", "vla_pipeline_run",
             "vla_param_count", "vla_param_info", "vla_export_param", "vla_ctx_export_kv",
-            "vla_debug_gemm", "vla_debug_attention", "vla_debug_attention_vt", "vla_debug_generate",
+            "vla_debug_gemm", "vla_debug_attention", "vla_debug_attention_cache", "vla_debug_generate",
             "vla_kernel_timer",
             "vla_kernel_timer_read", "vla_last_error"]

@@ -24,6 +24,47 @@ enum EpiKind {
                  // the consumer sums the splits in order
 };
 
+// KV-cache layout ("MFMA fragment order"). Keys go in blocks of 32; every
+// 1 KB chunk holds exactly the 64 lanes x 16 bytes one MFMA operand load of
+// the attention kernel reads, so those loads are contiguous. VEC is the
+// elements per 16 bytes (8 bf16, 4 fp32), SW = 4 VEC the K-extent of one
+// MFMA step. Per KV head j, nb blocks:
+//  K (the A operand of S^T = K Q^T): chunk (block b, 16-key tile nt, d-slab
+//    s of SW) = 64 lanes; lane (g, i) = 16 g + i holds d = s SW + g VEC ..
+//    + VEC - 1 of the key in row i of tile nt, which is key
+//    32 b + 8 (i / 4) + 4 nt + i % 4 (bf16) or 32 b + 16 nt + i (fp32), so
+//    that a lane group's score rows are the keys of its P^T slice.
+//  V (the A operand of O^T += V^T P^T): chunk (block b, 16-row d-tile dt,
+//    key slab kk of SW) = 64 lanes; lane (g, i) holds keys
+//    32 b + kk SW + g VEC .. + VEC - 1 of d = 16 dt + i.
+// Elements outside [0, S) x [0, hd) are never written (buffers start zeroed;
+// V there must stay zero, since a zero probability times a non-finite value
+// would not vanish).
+__host__ __device__ inline int kv_vec(int dtype) { return dtype == DT_BF16 ? 8 : 4; }
+__host__ __device__ inline size_t kv_kidx(int dtype, int nb, int hd, int j, int key, int d) {
+  const int vec = kv_vec(dtype), sw = 4 * vec, ns = (hd + sw - 1) / sw;
+  const int b = key >> 5, kin = key & 31;
+  const int nt = dtype == DT_BF16 ? (kin >> 2) & 1 : kin >> 4;
+  const int i = dtype == DT_BF16 ? 4 * (kin >> 3) + (kin & 3) : kin & 15;
+  const int s = d / sw, g = (d % sw) / vec, e = d % vec;
+  return ((((size_t)j * nb + b) * 2 + nt) * ns + s) * 64 * vec + (size_t)(16 * g + i) * vec + e;
+}
+__host__ __device__ inline size_t kv_vidx(int dtype, int nb, int hd, int j, int key, int d) {
+  const int vec = kv_vec(dtype), sw = 4 * vec, ndt = (hd + 15) / 16, pvs = 32 / sw;
+  const int b = key >> 5, kin = key & 31;
+  const int kk = kin / sw, g = (kin % sw) / vec, e = kin % vec;
+  const int dt = d >> 4, i = d & 15;
+  return ((((size_t)j * nb + b) * ndt + dt) * pvs + kk) * 64 * vec + (size_t)(16 * g + i) * vec + e;
+}
+// elements of one K or V buffer (all nkv heads)
+inline size_t kv_kelems(int dtype, int nb, int hd, int nkv) {
+  const int sw = 4 * kv_vec(dtype);
+  return (size_t)nkv * nb * 32 * ((hd + sw - 1) / sw) * sw;
+}
+inline size_t kv_velems(int dtype, int nb, int hd, int nkv) {
+  return (size_t)nkv * nb * 32 * ((hd + 15) / 16) * 16;
+}
+
 struct Epi {
   int kind = EPI_F32;
   void* out = nullptr;
@@ -34,13 +75,13 @@ struct Epi {
   int ldra = 0;
   float* resid = nullptr;
   int ldr = 0;
-  // EPI_QKV_ROPE
+  // EPI_QKV_ROPE: q row-major [m][ldq]; k and v in the KV-cache layout
+  // (kv_kidx / kv_vidx) with kv_nb 32-key blocks per KV head, row m = key m
   void* q = nullptr;
   int ldq = 0;
   void* k = nullptr;
   void* v = nullptr;
-  int ldkv = 0;
-  int ldvt = 0;  // > 0: V is stored transposed, element (m, c) at v[c * ldvt + m]
+  int kv_nb = 0;
   int nq = 0, nkv = 0, hd = 0, pos0 = 0;
   const float* rope_cos = nullptr;  // [pos][hd/2]
   const float* rope_sin = nullptr;
@@ -117,26 +158,24 @@ struct AttnDesc {
 
 size_t attn_scratch_floats(const AttnDesc& a);
 
-// Attention over keys [k0 (S0 rows); k1 (S1 rows)] with V stored transposed:
-// vt0 [n_kv * hd][ldvt0 >= round32(S0)], vt1 [n_kv * hd][ldvt1 >= round32(S1)],
-// padding columns zero. K rows have ldk elements (head j at column j * hd).
-// q and out as in AttnDesc (one segment). No scratch.
-struct AttnVtDesc {
+// Attention over keys [k0 (S0 keys); k1 (S1 keys)], both in the KV-cache
+// layout with ceil(S / 32) blocks per KV head (see kv_kidx / kv_vidx). q and
+// out row-major as in AttnDesc (one segment). No scratch.
+struct AttnKvDesc {
   int dtype;
   const void* q;
   int ldq;
   const void* k0;
-  const void* vt0;
-  int S0, ldvt0;
+  const void* v0;
+  int S0;
   const void* k1;
-  const void* vt1;
-  int S1, ldvt1;
-  int ldk;
+  const void* v1;
+  int S1;
   void* out;
   int ldo;
   int Sq, nq, nkv, hd;
 };
-hipError_t launch_attention_vt(const AttnVtDesc& d, const LaunchCaps& caps, hipStream_t st);
+hipError_t launch_attention_kv(const AttnKvDesc& d, const LaunchCaps& caps, hipStream_t st);
 hipError_t launch_attention(const AttnDesc& a, const Scratch& s, const LaunchCaps& caps, hipStream_t st);
 
 // Residual add + row norm: x[m] += bias + sum_s part[s][m] in split order

@@ -25,10 +25,30 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int NUM_CU_PLAN = 256;  // planner constant; never the live CU count
 
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);  // round to nearest, ties to even (finite values)
-  return (uint16_t)(u >> 16);
+// round to nearest, ties to even (the hardware conversion)
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
+__device__ __forceinline__ uint32_t f2bf2(float lo, float hi) {
+  return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+}
+
+// Cross-lane reductions over lanes l ^ 16 and l ^ 32 with the lane-swap
+// instructions (no LDS round trip). Both lanes of a pair compute the same
+// expression on the same operands, so they hold identical results.
+__device__ __forceinline__ float wave_max_x16_x32(float x) {
+  const uint32_t u = __float_as_uint(x);
+  auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const uint32_t v = __float_as_uint(x);
+  auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float wave_sum_x16_x32(float x) {
+  const uint32_t u = __float_as_uint(x);
+  auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const uint32_t v = __float_as_uint(x);
+  auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 template <typename T>
@@ -153,20 +173,22 @@ __device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int 
       const int i = 16 * (p >> 5) + (p & 15);  // rotate-half pair (i, i + hd/2)
       const size_t t = (size_t)(e.pos0 + m) * (hd / 2) + i;
       const float c = e.rope_cos[t], s = e.rope_sin[t];
-      T* dst = (isq ? (T*)e.q + (size_t)m * e.ldq : (T*)e.k + (size_t)m * e.ldkv) + head * hd;
-      TT<T>::st(dst + i, v0 * c - v1 * s);
-      TT<T>::st(dst + i + hd / 2, v1 * c + v0 * s);
-    } else {
-      const int c0 = n - qcols - kcols;
-      if (e.ldvt > 0) {
-        T* dst = (T*)e.v + m;
-        TT<T>::st(dst + (size_t)c0 * e.ldvt, v0);
-        TT<T>::st(dst + (size_t)(c0 + 16) * e.ldvt, v1);
+      if (isq) {
+        T* dst = (T*)e.q + (size_t)m * e.ldq + head * hd;
+        TT<T>::st(dst + i, v0 * c - v1 * s);
+        TT<T>::st(dst + i + hd / 2, v1 * c + v0 * s);
       } else {
-        T* dst = (T*)e.v + (size_t)m * e.ldkv;
-        TT<T>::st(dst + c0, v0);
-        TT<T>::st(dst + c0 + 16, v1);
+        constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
+        T* dst = (T*)e.k;
+        TT<T>::st(dst + kv_kidx(DT, e.kv_nb, hd, head, m, i), v0 * c - v1 * s);
+        TT<T>::st(dst + kv_kidx(DT, e.kv_nb, hd, head, m, i + hd / 2), v1 * c + v0 * s);
       }
+    } else {
+      constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
+      const int c0 = n - qcols - kcols, c1 = c0 + 16;
+      T* dst = (T*)e.v;
+      TT<T>::st(dst + kv_vidx(DT, e.kv_nb, hd, c0 / hd, m, c0 % hd), v0);
+      TT<T>::st(dst + kv_vidx(DT, e.kv_nb, hd, c1 / hd, m, c1 % hd), v1);
     }
     return;
   }
@@ -984,56 +1006,47 @@ hipError_t launch_attention(const AttnDesc& d, const Scratch& s, const LaunchCap
 }
 
 // ---------------------------------------------------------------------------
-// Attention with K and V read straight into MFMA registers (no LDS staging):
-// K row-major [keys][ldk] and V transposed [n_kv * hd][ldvt] (keys
-// contiguous per head-dim column, padded to a multiple of 32 keys with zeros
-// so 16-byte loads stay aligned). The key space is [segment 0 padded to a
-// multiple of 32; segment 1 padded likewise]; keys past a segment's length
-// get a -inf score. A workgroup owns 16 packed query rows (row r <-> query
-// r / group, head r % group of one KV head) and its NW waves take every
-// NW-th 32-key block, with the next block's K and V prefetched into
-// registers.
+// Attention over the KV cache. K and V sit in MFMA fragment order (see
+// kv_kidx / kv_vidx), so every operand load is one contiguous 1 KB per wave
+// straight into registers; the 16 packed query rows of a workgroup (row r <->
+// query r / group, head r % group of one KV head) are staged once through
+// LDS. The key space is [segment 0 padded to a multiple of 32; segment 1
+// padded likewise]; keys past a segment's length get a -inf score. The NW
+// waves take every NW-th 32-key block, with the next block's K and V
+// prefetched into registers.
 //
 // Everything is computed transposed, so the probabilities never leave the
 // registers: S^T = K Q^T puts one query per lane column and keys on the
 // rows, and O^T += V^T P^T takes P^T as the B operand straight from the
-// score registers. For that the K rows of a 16-key tile are loaded in the
-// order that makes each lane's score registers hold exactly the keys its
-// B-operand slice needs, which are also the keys one 16-byte V^T load
-// returns. The online softmax is fp32 with one running max per query
-// (reduced across the four lane groups) and per-lane partial sums, reduced
-// once at the end; P is split into bf16 high and remainder parts for the
-// bf16 MFMA. The waves' (max, sum, O) are merged through LDS in wave order.
+// score registers (the cache layout puts in each lane group's score rows
+// exactly the keys of its B-operand slice). The online softmax is fp32 with
+// one running max per query (reduced across the four lane groups) and
+// per-lane partial sums, reduced once at the end; P is split into bf16 high
+// and remainder parts for the bf16 MFMA. The waves' (max, sum, O) are merged
+// through LDS in wave order.
 // ---------------------------------------------------------------------------
 
 struct Attn2Args {
   const void* q;
   const void* k0;
-  const void* vt0;
+  const void* v0;
   const void* k1;
-  const void* vt1;
+  const void* v1;
   void* out;
-  int ldq, ldk, ldvt0, ldvt1, ldo;
+  int ldq, ldo;
   int Sq, nq, nkv, hd, S0, S1;
-  int rtiles;  // 16-row tiles of packed rows per KV head
+  int nb0, nb1;  // 32-key blocks per KV head in each segment's buffers
+  int rtiles;    // 16-row tiles of packed rows per KV head
   float scale_log2;
 };
+
+constexpr float ATT_TAU = 8.f;  // lazy-rescaling slack, log2 units
 
 // waves per workgroup: eight, or four where a wave needs more than the 256
 // registers eight waves leave it
 template <typename T, int HDP>
 constexpr int att2_waves() {
   return HDP * (int)sizeof(T) >= 512 ? 4 : 8;
-}
-
-// Key (within its 32-key block) held in score row i (0..15) of tile nt, so
-// that lane group g's rows {4g..4g+3} of both tiles are the keys of its
-// B-operand slice of P^T: keys 8g..8g+7 for bf16 (one 32-key slab), keys
-// 16 nt + 4g..4g+3 for fp32 (two 16-key slabs).
-template <typename T>
-__device__ __forceinline__ int att2_key(int nt, int i) {
-  if constexpr (sizeof(T) == 2) return 8 * (i >> 2) + 4 * nt + (i & 3);
-  return 16 * nt + i;
 }
 
 template <typename T, int HDP, int NW>
@@ -1044,85 +1057,97 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
   constexpr int NOT = HDP / 16;   // 16-row tiles of O^T
   constexpr int PVS = 32 / SW;    // P V slabs per 32-key block
   constexpr int OS = HDP + 4;     // sO row stride (floats)
+  constexpr int QS = HDP + VEC;   // sQ row stride (elements)
   constexpr int NT = 64 * NW;
+  constexpr int FRAG = 64 * VEC;  // elements of one 1 KB fragment chunk
   __shared__ __attribute__((aligned(16))) float sO[NW][16 * OS];
   __shared__ float sM[NW][16], sL[NW][16];
+  __shared__ __attribute__((aligned(16))) T sQ[16 * QS];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int g4 = lane >> 4;  // lane group
   const int group = a.nq / a.nkv;
   const int R = a.Sq * group;
-  const int S0p = (a.S0 + 31) / 32 * 32, S1p = (a.S1 + 31) / 32 * 32;
-  const int nblk = (S0p + S1p) / 32;
+  const int nblk = a.nb0 + a.nb1;
   const int total = a.rtiles * a.nkv;
+  const int ns = (a.hd + SW - 1) / SW, ndt = (a.hd + 15) / 16;
   const T dummy = T();
   const Rsrc rq = rsrc(a.q, span(a.Sq, a.ldq, a.nq * a.hd, sizeof(T)));
-  const Rsrc rk0 = rsrc(a.k0, span(a.S0, a.ldk, a.nkv * a.hd, sizeof(T)));
-  const Rsrc rv0 = rsrc(a.vt0, (size_t)a.nkv * a.hd * a.ldvt0 * sizeof(T));
-  const Rsrc rk1 = rsrc(a.k1 ? a.k1 : a.k0, a.k1 ? span(a.S1, a.ldk, a.nkv * a.hd, sizeof(T)) : 0);
-  const Rsrc rv1 = rsrc(a.vt1 ? a.vt1 : a.vt0, a.vt1 ? (size_t)a.nkv * a.hd * a.ldvt1 * sizeof(T) : 0);
+  const Rsrc rk0 = rsrc(a.k0, (size_t)a.nkv * a.nb0 * 2 * ns * FRAG * sizeof(T));
+  const Rsrc rv0 = rsrc(a.v0, (size_t)a.nkv * a.nb0 * ndt * PVS * FRAG * sizeof(T));
+  const Rsrc rk1 = rsrc(a.k1 ? a.k1 : a.k0, a.k1 ? (size_t)a.nkv * a.nb1 * 2 * ns * FRAG * sizeof(T) : 0);
+  const Rsrc rv1 = rsrc(a.v1 ? a.v1 : a.v0, a.v1 ? (size_t)a.nkv * a.nb1 * ndt * PVS * FRAG * sizeof(T) : 0);
 
   for (int w = blockIdx.x; w < total; w += gridDim.x) {
     const int rt = w % a.rtiles, j = w / a.rtiles;
 
-    // Q^T as the B operand: lane column = packed row, 16-byte slice of d
-    uint4 qf[NQF];
-    {
-      const int r = rt * 16 + (lane & 15);
-      const int sq = r / group, h = j * group + r % group;
+    // the workgroup's 16 packed query rows, row-contiguous loads (issued
+    // before K and V so that waiting for them does not wait for K and V)
+    constexpr int QCH = 16 * (HDP / VEC), QPT = (QCH + NT - 1) / NT;
+    uint4 qld[QPT];
 #pragma unroll
-      for (int ks = 0; ks < NQF; ++ks) {
-        const int d = ks * SW + g4 * VEC;
-        const bool ok = r < R && d < a.hd;
-        qf[ks] = bld16(rq, ok ? (uint32_t)(((size_t)sq * a.ldq + h * a.hd + d) * sizeof(T)) : OOB);
-      }
+    for (int u = 0; u < QPT; ++u) {
+      const int c = tid + u * NT;
+      const int rr = c / (HDP / VEC), d = (c % (HDP / VEC)) * VEC;
+      const int r = rt * 16 + rr;
+      const int sq = r / group, h = j * group + r % group;
+      const bool ok = c < QCH && r < R && d < a.hd;
+      qld[u] = bld16(rq, ok ? (uint32_t)(((size_t)sq * a.ldq + h * a.hd + d) * sizeof(T)) : OOB);
     }
 
+    // fragment loads of one 32-key block (b past the end reads zeros)
     auto load_k = [&](int b, uint4 (&kf)[2][NQF]) {
-      const int kb = b * 32;
-      const bool seg1 = kb >= S0p;
-      const int kloc = seg1 ? kb - S0p : kb;
-      const int slen = seg1 ? a.S1 : a.S0;
+      const bool seg1 = b >= a.nb0;
+      const int bl = seg1 ? b - a.nb0 : b, nb = seg1 ? a.nb1 : a.nb0;
       const Rsrc rk = seg1 ? rk1 : rk0;
 #pragma unroll
-      for (int nt = 0; nt < 2; ++nt) {
-        const int key = kloc + att2_key<T>(nt, lane & 15);
+      for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
         for (int ks = 0; ks < NQF; ++ks) {
-          const int d = ks * SW + g4 * VEC;
-          const bool ok = b < nblk && key < slen && d < a.hd;
-          kf[nt][ks] = bld16(rk, ok ? (uint32_t)(((size_t)key * a.ldk + j * a.hd + d) * sizeof(T)) : OOB);
+          const bool ok = b < nblk && ks * SW + g4 * VEC < a.hd;
+          const size_t off = ((((size_t)j * nb + bl) * 2 + nt) * ns + ks) * FRAG + lane * VEC;
+          kf[nt][ks] = bld16(rk, ok ? (uint32_t)(off * sizeof(T)) : OOB);
         }
-      }
     };
     auto load_v = [&](int b, uint4 (&vf)[NOT][PVS]) {
-      const int kb = b * 32;
-      const bool seg1 = kb >= S0p;
-      const int ldvt = seg1 ? a.ldvt1 : a.ldvt0;
-      const int kloc = seg1 ? kb - S0p : kb;
+      const bool seg1 = b >= a.nb0;
+      const int bl = seg1 ? b - a.nb0 : b, nb = seg1 ? a.nb1 : a.nb0;
       const Rsrc rv = seg1 ? rv1 : rv0;
 #pragma unroll
-      for (int dt = 0; dt < NOT; ++dt) {
-        const int d = dt * 16 + (lane & 15);
+      for (int dt = 0; dt < NOT; ++dt)
 #pragma unroll
         for (int kk = 0; kk < PVS; ++kk) {
-          const int key = kloc + kk * SW + g4 * VEC;
-          const bool ok = b < nblk && d < a.hd;
-          vf[dt][kk] = bld16(rv, ok ? (uint32_t)(((size_t)(j * a.hd + d) * ldvt + key) * sizeof(T)) : OOB);
+          const bool ok = b < nblk && dt * 16 + (lane & 15) < a.hd;
+          const size_t off = ((((size_t)j * nb + bl) * ndt + dt) * PVS + kk) * FRAG + lane * VEC;
+          vf[dt][kk] = bld16(rv, ok ? (uint32_t)(off * sizeof(T)) : OOB);
         }
-      }
     };
+
+    // Loads are issued unconditionally: with the same loads in flight on
+    // every path each wait covers only the oldest group.
+    uint4 kf[2][NQF], vf[NOT][PVS];
+    load_k(wave, kf);
+    load_v(wave, vf);
 
     float mrun = -INFINITY, lpart = 0.f;  // running max of this lane's query; partial sum
     f32x4 o[NOT];
 #pragma unroll
     for (int d = 0; d < NOT; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    uint4 kf[2][NQF], vf[NOT][PVS];
+#pragma unroll
+    for (int u = 0; u < QPT; ++u) {
+      const int c = tid + u * NT;
+      if (c < QCH) *(uint4*)&sQ[(c / (HDP / VEC)) * QS + (c % (HDP / VEC)) * VEC] = qld[u];
+    }
+    __syncthreads();
+    // Q^T as the B operand: lane column = packed row, 16-byte slice of d
+    uint4 qf[NQF];
+#pragma unroll
+    for (int ks = 0; ks < NQF; ++ks) qf[ks] = *(const uint4*)&sQ[(lane & 15) * QS + ks * SW + g4 * VEC];
+
     auto process = [&](int b) {
-      const int kb = b * 32;
-      const bool seg1 = kb >= S0p;
-      const int kloc = seg1 ? kb - S0p : kb;
+      const bool seg1 = b >= a.nb0;
+      const int kloc = (seg1 ? b - a.nb0 : b) * 32;
       const int slen = seg1 ? a.S1 : a.S0;
       // S^T for 32 keys x 16 queries, two accumulators per tile
       f32x4 sacc[2][2];
@@ -1139,37 +1164,43 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
       for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int key = kloc + att2_key<T>(nt, 4 * g4 + r);
-          const float sv = key < slen ? (sacc[nt][0][r] + sacc[nt][1][r]) * a.scale_log2 : -INFINITY;
+          // key of score row 4 g4 + r in tile nt (the cache layout's order)
+          const int kin = sizeof(T) == 2 ? 8 * g4 + 4 * nt + r : 16 * nt + 4 * g4 + r;
+          const float sv = kloc + kin < slen ? (sacc[nt][0][r] + sacc[nt][1][r]) * a.scale_log2 : -INFINITY;
           p[nt][r] = sv;
           mx = fmaxf(mx, sv);
         }
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mnew = fmaxf(mrun, mx);
-      // a block can be entirely padding: keep everything at zero then
-      const float alpha = mnew == -INFINITY ? 1.f : exp2f(mrun - mnew);
+      mx = wave_max_x16_x32(mx);
+      // Lazy rescaling: the reference point mrun only moves when a score
+      // exceeds it by more than 2^ATT_TAU (or on the first finite score), so
+      // the O rescale is skipped for most blocks; probabilities stay below
+      // 2^ATT_TAU and the final normalisation is unchanged.
+      const bool move = mx > mrun + ATT_TAU;
+      if (__any(move)) {
+        const float mnew = move ? mx : mrun;
+        const float alpha = mrun == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mrun - mnew);
+        lpart *= alpha;
+#pragma unroll
+        for (int d = 0; d < NOT; ++d) o[d] *= alpha;
+        mrun = mnew;
+      }
       float sum = 0.f;
 #pragma unroll
       for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          p[nt][r] = mnew == -INFINITY ? 0.f : exp2f(p[nt][r] - mnew);
+          p[nt][r] = p[nt][r] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(p[nt][r] - mrun);
           sum += p[nt][r];
         }
-      lpart = lpart * alpha + sum;
-      mrun = mnew;
-#pragma unroll
-      for (int d = 0; d < NOT; ++d) o[d] *= alpha;
+      lpart += sum;
       if constexpr (sizeof(T) == 2) {
+        // P^T slice of lane group g4: keys 8 g4 .. 8 g4 + 7 = rows 4 g4 + r of tiles 0, 1
         uint32_t hi[4], lo[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const float x0 = p[q >> 1][2 * (q & 1)], x1 = p[q >> 1][2 * (q & 1) + 1];
-          const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
-          const uint16_t l0 = f2bf(x0 - bf2f(h0)), l1 = f2bf(x1 - bf2f(h1));
-          hi[q] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-          lo[q] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+          hi[q] = f2bf2(x0, x1);
+          lo[q] = f2bf2(x0 - bf2f((uint16_t)hi[q]), x1 - bf2f((uint16_t)(hi[q] >> 16)));
         }
         const uint4 phi = make_uint4(hi[0], hi[1], hi[2], hi[3]);
         const uint4 plo = make_uint4(lo[0], lo[1], lo[2], lo[3]);
@@ -1179,6 +1210,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
           o[d] = mfma_step(vf[d][0], plo, o[d], dummy);
         }
       } else {
+        // slab kk = tile kk: keys 16 kk + 4 g4 .. + 3
 #pragma unroll
         for (int kk = 0; kk < PVS; ++kk) {
           const uint4 pf = make_uint4(__float_as_uint(p[kk][0]), __float_as_uint(p[kk][1]),
@@ -1190,16 +1222,10 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
       load_v(b + NW, vf);
     };
 
-    // Loads are issued unconditionally (blocks past the end read as zero
-    // through the range check): with the same loads in flight on every path
-    // each wait covers only the oldest group.
-    load_k(wave, kf);
-    load_v(wave, vf);
     for (int b = wave; b < nblk; b += NW) process(b);
 
     // the four lane groups' partial sums of one query
-    lpart += __shfl_xor(lpart, 16);
-    lpart += __shfl_xor(lpart, 32);
+    lpart = wave_sum_x16_x32(lpart);
     // O^T registers: lane column = packed row (lane & 15), rows d = 16 dt + 4 g4 + r
 #pragma unroll
     for (int d = 0; d < NOT; ++d)
@@ -1222,7 +1248,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
       for (int e = 0; e < 8; ++e) num[e] = 0.f;
 #pragma unroll
       for (int u = 0; u < NW; ++u) {
-        const float wgt = sM[u][rr] == -INFINITY ? 0.f : exp2f(sM[u][rr] - mx);
+        const float wgt = sM[u][rr] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(sM[u][rr] - mx);
         const f32x4 v0 = *(const f32x4*)&sO[u][rr * OS + d0];
         const f32x4 v1 = *(const f32x4*)&sO[u][rr * OS + d0 + 4];
 #pragma unroll
@@ -1272,24 +1298,20 @@ static hipError_t run_attn2_t(const Attn2Args& a, int hdp, const LaunchCaps& cap
   return hipGetLastError();
 }
 
-hipError_t launch_attention_vt(const AttnVtDesc& d, const LaunchCaps& caps, hipStream_t st) {
+hipError_t launch_attention_kv(const AttnKvDesc& d, const LaunchCaps& caps, hipStream_t st) {
   const int hdp = attn_hdp(d.hd, d.dtype);
   if (hdp < 0 || d.nq % d.nkv != 0 || d.S0 <= 0 || d.S1 < 0 || d.Sq <= 0 ||
-      (d.S1 > 0 && (!d.k1 || !d.vt1)) || d.ldvt0 < (d.S0 + 31) / 32 * 32 ||
-      (d.S1 > 0 && d.ldvt1 < (d.S1 + 31) / 32 * 32) || d.hd % 8 != 0 ||
+      (d.S1 > 0 && (!d.k1 || !d.v1)) || d.hd % 8 != 0 ||
       ((size_t)d.ldo * (d.dtype == DT_BF16 ? 2 : 4)) % 16 != 0 || ((uintptr_t)d.out & 15) != 0)
     return hipErrorInvalidValue;
   Attn2Args a{};
   a.q = d.q;
   a.k0 = d.k0;
-  a.vt0 = d.vt0;
+  a.v0 = d.v0;
   a.k1 = d.S1 > 0 ? d.k1 : nullptr;
-  a.vt1 = d.S1 > 0 ? d.vt1 : nullptr;
+  a.v1 = d.S1 > 0 ? d.v1 : nullptr;
   a.out = d.out;
   a.ldq = d.ldq;
-  a.ldk = d.ldk;
-  a.ldvt0 = d.ldvt0;
-  a.ldvt1 = d.ldvt1;
   a.ldo = d.ldo;
   a.Sq = d.Sq;
   a.nq = d.nq;
@@ -1297,6 +1319,8 @@ hipError_t launch_attention_vt(const AttnVtDesc& d, const LaunchCaps& caps, hipS
   a.hd = d.hd;
   a.S0 = d.S0;
   a.S1 = d.S1;
+  a.nb0 = (d.S0 + 31) / 32;
+  a.nb1 = (d.S1 + 31) / 32;
   a.rtiles = (d.Sq * (d.nq / d.nkv) + 15) / 16;
   a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.hd));
   if (d.dtype == DT_BF16) return run_attn2_t<uint16_t>(a, hdp, caps, st);

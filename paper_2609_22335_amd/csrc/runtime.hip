@@ -58,7 +58,7 @@ static inline int rnd_up(int x, int m) { return (x + m - 1) / m * m; }
 
 struct Dims {
   int gh, gw, tview, nimg, prefix, kp, kp_pad, a_pad, s_pad, rows_v, kvd, qd, qkv_n, vhd;
-  int prefix_pad, chunk_pad;  // key lengths rounded up to 32 (transposed V rows)
+  int prefix_pad, chunk_pad;  // key lengths rounded up to 32 (KV-cache blocks)
 };
 
 static Dims derive(const vla_config& c) {
@@ -199,8 +199,10 @@ struct ActWs {
 
 struct vla_ctx {
   vla_model* m = nullptr;
-  void* K = nullptr;  // [L][P][kvd]
-  void* V = nullptr;  // transposed: [L][kvd][P rounded up to 32], padding zero
+  // per layer, the KV-cache layout (kv_kidx / kv_vidx) with prefix_pad / 32
+  // blocks per KV head; zeroed at creation, so unwritten padding stays zero
+  void* K = nullptr;
+  void* V = nullptr;
 };
 
 struct vla_model {
@@ -261,6 +263,20 @@ struct vla_model {
   char* tptr(int t) const { return (char*)arena + T[t].offset; }
   float* f32(int t) const { return (float*)tptr(t); }
 };
+
+// elements per layer of a context's K and V, and of an action lane's own K, V
+static size_t ctx_layer_k(const vla_model* m) {
+  return kv_kelems(m->dt, m->d.prefix_pad / 32, m->c.head_dim, m->c.lm_kv_heads);
+}
+static size_t ctx_layer_v(const vla_model* m) {
+  return kv_velems(m->dt, m->d.prefix_pad / 32, m->c.head_dim, m->c.lm_kv_heads);
+}
+static size_t own_k(const vla_model* m) {
+  return kv_kelems(m->dt, m->d.chunk_pad / 32, m->c.head_dim, m->c.lm_kv_heads);
+}
+static size_t own_v(const vla_model* m) {
+  return kv_velems(m->dt, m->d.chunk_pad / 32, m->c.head_dim, m->c.lm_kv_heads);
+}
 
 static size_t dsz(int dt) { return dt == DT_BF16 ? 2 : 4; }
 
@@ -461,10 +477,10 @@ static int gemm(const Run& r, const char* tag, const void* A, int lda, int W, in
   return VLA_OK;
 }
 
-static int attn_vt(const Run& r, const char* tag, const AttnVtDesc& a) {
+static int attn_kv(const Run& r, const char* tag, const AttnKvDesc& a) {
   LaunchCaps caps = r.caps;
   VLA_TRY(timer_events(r, tag, &caps));
-  hipError_t err = launch_attention_vt(a, caps, r.st);
+  hipError_t err = launch_attention_kv(a, caps, r.st);
   if (err != hipSuccess) return fail(VLA_EHIP, std::string("attention: ") + hipGetErrorString(err));
   return VLA_OK;
 }
@@ -529,35 +545,30 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   e.ldq = d.qd;
   e.k = kout;
   e.v = vout;
-  e.ldkv = d.kvd;
+  e.kv_nb = (lm ? d.prefix_pad : d.chunk_pad) / 32;
   e.nq = c.lm_heads;
   e.nkv = c.lm_kv_heads;
   e.hd = c.head_dim;
   e.pos0 = pos0;
   e.rope_cos = m->rope_cos;
   e.rope_sin = m->rope_sin;
-  e.ldvt = lm ? d.prefix_pad : d.chunk_pad;
   VLA_TRY(gemm(r, lm ? "lm.qkv" : "ex.qkv", h, dim, L.qkv, rows, d.qkv_n, dim, e));
   if (kv_only) return VLA_OK;
-  AttnVtDesc a{};
+  AttnKvDesc a{};
   a.dtype = m->dt;
   a.q = q;
   a.ldq = d.qd;
-  a.ldk = d.kvd;
   if (kpast) {
     a.k0 = kpast;
-    a.vt0 = vpast;
+    a.v0 = vpast;
     a.S0 = npast;
-    a.ldvt0 = d.prefix_pad;
     a.k1 = kout;
-    a.vt1 = vout;
+    a.v1 = vout;
     a.S1 = rows;
-    a.ldvt1 = d.chunk_pad;
   } else {
     a.k0 = kout;
-    a.vt0 = vout;
+    a.v0 = vout;
     a.S0 = rows;
-    a.ldvt0 = d.prefix_pad;
   }
   a.out = att;
   a.ldo = d.qd;
@@ -565,7 +576,7 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   a.nq = c.lm_heads;
   a.nkv = c.lm_kv_heads;
   a.hd = c.head_dim;
-  VLA_TRY(attn_vt(r, lm ? "lm.attn" : "ex.attn", a));
+  VLA_TRY(attn_kv(r, lm ? "lm.attn" : "ex.attn", a));
   int so = 0;
   VLA_TRY(gemm_part(r, lm ? "lm.o" : "ex.o", att, d.qd, L.o, rows, dim, d.qd, &so));
   VLA_TRY(norm(r, x, rows, dim, so, nullptr, L.rms2, -1, true, h));
@@ -631,8 +642,8 @@ static int run_prefill(const Run& r, const vla_frame* f, vla_ctx* ctx) {
                  epi_kind(EPI_F32, w.xl + (size_t)(d.prefix - 1) * dl, dl, m->f32(m->state_b))));
   }
   // LM prefill writing the cache
-  const size_t layer_k = (size_t)d.prefix * d.kvd * m->esz;
-  const size_t layer_v = (size_t)d.prefix_pad * d.kvd * m->esz;
+  const size_t layer_k = ctx_layer_k(m) * m->esz;
+  const size_t layer_v = ctx_layer_v(m) * m->esz;
   pend = 0;
   for (int l = 0; l < c.lm_layers; ++l) {
     void* K = (char*)ctx->K + l * layer_k;
@@ -651,8 +662,8 @@ static int run_denoise(const Run& r, const vla_ctx* ctx, const float* noise, flo
   const int H = c.chunk_len, de = c.ex_dim, A = c.action_dim;
   const float dt = -1.0f / (float)c.n_steps;
   HIP_TRY(launch_cvt_pad(m->dt, noise, H, A, w.xop, d.a_pad, x, r.st));
-  const size_t layer_k = (size_t)d.prefix * d.kvd * m->esz;
-  const size_t layer_v = (size_t)d.prefix_pad * d.kvd * m->esz;
+  const size_t layer_k = ctx_layer_k(m) * m->esz;
+  const size_t layer_v = ctx_layer_v(m) * m->esz;
   for (int k = 0; k < c.n_steps; ++k) {
     // action embedding and time conditioning
     VLA_TRY(gemm(r, "ex.in", w.xop, d.a_pad, m->in_w, H, de, d.a_pad, epi_kind(EPI_T, w.a, de, m->f32(m->in_b))));
@@ -772,9 +783,10 @@ static int add_act_lane(vla_model* m) {
   VLA_TRY(dmalloc(m, &a.hid, (size_t)H * de * e));
   VLA_TRY(dmalloc(m, &a.h, (size_t)H * de * e));
   VLA_TRY(dmalloc(m, &a.q, (size_t)H * d.qd * e));
-  VLA_TRY(dmalloc(m, &a.kown, (size_t)H * d.kvd * e));
-  VLA_TRY(dmalloc(m, &a.vown, (size_t)d.chunk_pad * d.kvd * e));
-  HIP_TRY(hipMemset(a.vown, 0, (size_t)d.chunk_pad * d.kvd * e));  // padding keys stay zero
+  VLA_TRY(dmalloc(m, &a.kown, own_k(m) * e));
+  VLA_TRY(dmalloc(m, &a.vown, own_v(m) * e));
+  HIP_TRY(hipMemset(a.kown, 0, own_k(m) * e));  // padding stays zero
+  HIP_TRY(hipMemset(a.vown, 0, own_v(m) * e));
   VLA_TRY(dmalloc(m, &a.att, (size_t)H * d.qd * e));
   VLA_TRY(dmalloc(m, &a.mlp, (size_t)H * c.ex_mlp * e));
   ScratchNeed sa;
@@ -893,12 +905,16 @@ static int create_impl(const vla_config* cfg, uint64_t seed, vla_model** out) {
 static int ctx_create_impl(vla_model* m, vla_ctx** out) {
   std::unique_ptr<vla_ctx> c(new vla_ctx());
   c->m = m;
-  const size_t kbytes = (size_t)m->c.lm_layers * m->d.prefix * m->d.kvd * m->esz;
-  const size_t vbytes = (size_t)m->c.lm_layers * m->d.prefix_pad * m->d.kvd * m->esz;
+  const size_t kbytes = (size_t)m->c.lm_layers * ctx_layer_k(m) * m->esz;
+  const size_t vbytes = (size_t)m->c.lm_layers * ctx_layer_v(m) * m->esz;
   hipError_t e = hipMalloc(&c->K, kbytes);
-  if (e != hipSuccess) return fail(VLA_ENOMEM, "ctx K: hipMalloc failed");
+  if (e == hipSuccess) e = hipMemset(c->K, 0, kbytes);  // padding stays zero
+  if (e != hipSuccess) {
+    hipFree(c->K);
+    return fail(VLA_ENOMEM, "ctx K: allocation failed");
+  }
   e = hipMalloc(&c->V, vbytes);
-  if (e == hipSuccess) e = hipMemset(c->V, 0, vbytes);  // padding keys stay zero
+  if (e == hipSuccess) e = hipMemset(c->V, 0, vbytes);
   if (e != hipSuccess) {
     hipFree(c->K);
     hipFree(c->V);
@@ -1233,19 +1249,21 @@ int vla_ctx_export_kv(vla_model* m, const vla_ctx* c, int32_t layer, float* host
     if (!m || !c || !host_k || !host_v) return fail(VLA_EINVAL, "NULL argument");
     if (layer < 0 || layer >= m->c.lm_layers) return fail(VLA_EINVAL, "layer out of range");
     if (c->m != m) return fail(VLA_ESTATE, "context belongs to another model");
-    const int P = m->d.prefix, Pp = m->d.prefix_pad, kvd = m->d.kvd;
-    const size_t n = (size_t)P * kvd;
+    const int P = m->d.prefix, nb = m->d.prefix_pad / 32, hd = m->c.head_dim;
+    const int nkv = m->c.lm_kv_heads, kvd = m->d.kvd;
     auto val = [&](const std::vector<uint8_t>& img, size_t i) {
       return m->dt == DT_BF16 ? bf16_value(((const uint16_t*)img.data())[i]) : ((const float*)img.data())[i];
     };
-    std::vector<uint8_t> img(n * m->esz);
-    HIP_TRY(hipMemcpy(img.data(), (const char*)c->K + layer * n * m->esz, img.size(), hipMemcpyDeviceToHost));
-    for (size_t i = 0; i < n; ++i) host_k[i] = val(img, i);
-    const size_t nv = (size_t)Pp * kvd;
-    std::vector<uint8_t> vimg(nv * m->esz);
+    const size_t nk = ctx_layer_k(m), nv = ctx_layer_v(m);
+    std::vector<uint8_t> kimg(nk * m->esz), vimg(nv * m->esz);
+    HIP_TRY(hipMemcpy(kimg.data(), (const char*)c->K + layer * nk * m->esz, kimg.size(), hipMemcpyDeviceToHost));
     HIP_TRY(hipMemcpy(vimg.data(), (const char*)c->V + layer * nv * m->esz, vimg.size(), hipMemcpyDeviceToHost));
     for (int p = 0; p < P; ++p)
-      for (int j = 0; j < kvd; ++j) host_v[(size_t)p * kvd + j] = val(vimg, (size_t)j * Pp + p);
+      for (int j = 0; j < nkv; ++j)
+        for (int dd = 0; dd < hd; ++dd) {
+          host_k[(size_t)p * kvd + j * hd + dd] = val(kimg, kv_kidx(m->dt, nb, hd, j, p, dd));
+          host_v[(size_t)p * kvd + j * hd + dd] = val(vimg, kv_vidx(m->dt, nb, hd, j, p, dd));
+        }
     return VLA_OK;
   })
 }
@@ -1321,36 +1339,33 @@ int vla_debug_attention(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int3
   })
 }
 
-int vla_debug_attention_vt(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int32_t hd,
-                           const void* q, const void* k0, const void* vt0, int32_t S0, int32_t ldvt0,
-                           const void* k1, const void* vt1, int32_t S1, int32_t ldvt1, void* out,
-                           void* stream) {
+int vla_debug_attention_cache(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int32_t hd,
+                              const void* q, const void* k0, const void* v0, int32_t S0, const void* k1,
+                              const void* v1, int32_t S1, void* out, void* stream) {
   ABI_GUARD({
     if (dtype != VLA_F32 && dtype != VLA_BF16) return fail(VLA_EINVAL, "dtype");
-    if (Sq <= 0 || nq <= 0 || nkv <= 0 || nq % nkv || hd <= 0 || hd % 8 || hd > 256 || S0 <= 0 ||
-        S1 < 0 || ldvt0 < (S0 + 31) / 32 * 32 || (S1 > 0 && ldvt1 < (S1 + 31) / 32 * 32))
+    if (Sq <= 0 || nq <= 0 || nkv <= 0 || nq % nkv || hd <= 0 || hd % 8 || hd > 256 || S0 <= 0 || S1 < 0)
       return fail(VLA_EINVAL, "shape");
-    if (!q || !k0 || !vt0 || !out || (S1 > 0 && (!k1 || !vt1))) return fail(VLA_EINVAL, "NULL argument");
-    AttnVtDesc a{};
+    if (dtype == VLA_F32 && hd > 128) return fail(VLA_EINVAL, "fp32 head dim above 128");
+    if (!q || !k0 || !v0 || !out || (S1 > 0 && (!k1 || !v1))) return fail(VLA_EINVAL, "NULL argument");
+    if (((uintptr_t)out & 15) != 0) return fail(VLA_EINVAL, "out must be 16-byte aligned");
+    AttnKvDesc a{};
     a.dtype = dtype == VLA_BF16 ? DT_BF16 : DT_F32;
     a.q = q;
     a.ldq = nq * hd;
     a.k0 = k0;
-    a.vt0 = vt0;
+    a.v0 = v0;
     a.S0 = S0;
-    a.ldvt0 = ldvt0;
     a.k1 = k1;
-    a.vt1 = vt1;
+    a.v1 = v1;
     a.S1 = S1;
-    a.ldvt1 = ldvt1;
-    a.ldk = nkv * hd;
     a.out = out;
     a.ldo = nq * hd;
     a.Sq = Sq;
     a.nq = nq;
     a.nkv = nkv;
     a.hd = hd;
-    hipError_t e = launch_attention_vt(a, LaunchCaps{}, (hipStream_t)stream);
+    hipError_t e = launch_attention_kv(a, LaunchCaps{}, (hipStream_t)stream);
     if (e != hipSuccess) return fail(VLA_EHIP, std::string("attention: ") + hipGetErrorString(e));
     return VLA_OK;
   })

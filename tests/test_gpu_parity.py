@@ -103,7 +103,7 @@ def test_attention_vs_oracle(V, case):
     assert np.all(err <= bound), float((err / bound).max())
 
 
-ATTN_VT_CASES = [  # dtype, Sq, nq, nkv, hd, S0, S1
+ATTN_CACHE_CASES = [  # dtype, Sq, nq, nkv, hd, S0, S1
     (1, 50, 8, 1, 256, 305, 50),   # expert joint attention over [prefix; own]
     (1, 50, 8, 1, 256, 833, 50),   # three-view prefix
     (1, 305, 8, 1, 256, 305, 0),   # LM prefill, multi-query
@@ -117,28 +117,44 @@ ATTN_VT_CASES = [  # dtype, Sq, nq, nkv, hd, S0, S1
 ]
 
 
-@pytest.mark.parametrize("case", ATTN_VT_CASES, ids=lambda c: "-".join(map(str, c)))
-def test_attention_vt_vs_oracle(V, case):
+def cache_layout(x, dtype, kind):
+    """[S, nkv, hd] -> flat buffer in the KV-cache layout that include/vla.h
+    documents at vla_debug_attention_cache (zeros where nothing is stored)."""
+    S, nkv, hd = x.shape
+    vec = 8 if dtype else 4
+    sw, nb = 4 * vec, -(-S // 32)
+    ns, ndt, pvs = -(-hd // sw), -(-hd // 16), 32 // sw
+    p, j, d = np.meshgrid(np.arange(S), np.arange(nkv), np.arange(hd), indexing="ij")
+    b, kin = p // 32, p % 32
+    if kind == "k":
+        nt = (kin // 4) % 2 if dtype else kin // 16
+        i = 4 * (kin // 8) + kin % 4 if dtype else kin % 16
+        idx = ((((j * nb + b) * 2 + nt) * ns + d // sw) * 64 + 16 * ((d % sw) // vec) + i) * vec + d % vec
+        size = nkv * nb * 32 * ns * sw
+    else:
+        idx = ((((j * nb + b) * ndt + d // 16) * pvs + kin // sw) * 64 + 16 * ((kin % sw) // vec)
+               + d % 16) * vec + kin % vec
+        size = nkv * nb * 32 * ndt * 16
+    assert np.unique(idx).size == idx.size and idx.max() < size
+    buf = np.zeros(size)
+    buf[idx.ravel()] = x.ravel()
+    return buf
+
+
+@pytest.mark.parametrize("case", ATTN_CACHE_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_attention_cache_vs_oracle(V, case):
     g = G()
     dtype, Sq, nq, nkv, hd, S0, S1 = case
-    g.say(f"attention (transposed V) {case}")
+    g.say(f"attention (KV-cache layout) {case}")
     q = RNG.standard_normal((Sq, nq, hd))
     k0, v0 = RNG.standard_normal((S0, nkv, hd)), RNG.standard_normal((S0, nkv, hd))
     k1, v1 = RNG.standard_normal((max(S1, 1), nkv, hd)), RNG.standard_normal((max(S1, 1), nkv, hd))
-
-    def vt(v, S):  # [S, nkv, hd] -> [nkv * hd, round32(S)], zero padding
-        ld = (S + 31) // 32 * 32
-        t = np.zeros((nkv * hd, ld))
-        t[:, :S] = v[:S].reshape(S, -1).T
-        return t, ld
-
-    vt0, ld0 = vt(v0, S0)
-    vt1, ld1 = vt(v1, max(S1, 1))
-    dv = lambda x: g.operand_dev(x.reshape(x.shape[0], -1), dtype)
+    lay = lambda x, kind: g.operand_dev(cache_layout(x, dtype, kind), dtype)
     out = torch.empty((Sq, nq * hd), dtype=torch.bfloat16 if dtype else torch.float32, device="cuda")
-    k1d, vt1d = dv(k1), g.operand_dev(vt1, dtype)
-    V.vla_debug_attention_vt(dtype, Sq, nq, nkv, hd, dv(q), dv(k0), g.operand_dev(vt0, dtype), S0, ld0,
-                             k1d if S1 else None, vt1d if S1 else None, S1, ld1, out)
+    k1d, v1d = lay(k1[:max(S1, 1)], "k"), lay(v1[:max(S1, 1)], "v")
+    V.vla_debug_attention_cache(dtype, Sq, nq, nkv, hd, g.operand_dev(q.reshape(Sq, -1), dtype),
+                                lay(k0, "k"), lay(v0, "v"), S0, k1d if S1 else None, v1d if S1 else None,
+                                S1, out)
     torch.cuda.synchronize()
     val = lambda x: g.operand_values(x, dtype)
     kk = np.concatenate([val(k0), val(k1)[:S1]], 0)
