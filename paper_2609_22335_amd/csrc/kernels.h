@@ -23,6 +23,8 @@ enum EpiKind {
   EPI_PART,      // raw fp32 result into out = [splits][M][N] (ldo = its capacity in floats);
                  // the consumer sums the splits in order
 };
+// With Epi::afrag set, the operand-type outputs (out, xop) are written in
+// the row-block operand layout (afrag_index) instead of row-major.
 
 // KV-cache layout ("MFMA fragment order"). Keys go in blocks of 32; every
 // 1 KB chunk holds exactly the 64 lanes x 16 bytes one MFMA operand load of
@@ -65,8 +67,24 @@ inline size_t kv_velems(int dtype, int nb, int hd, int nkv) {
   return (size_t)nkv * nb * 32 * ((hd + 15) / 16) * 16;
 }
 
+// Row-block operand layout of the skinny GEMM's A (at most 64 rows): chunk
+// (K-slab ks of SW, 16-row tile mt) is 1 KB, lane (g, i) = 16 g + i holding
+// row 16 mt + i, columns SW ks + g VEC .. + VEC - 1; chunks go K-slab-major,
+// so the four row tiles of a slab are adjacent. Producers of such operands
+// write it directly; every load of the skinny kernel is then contiguous.
+__host__ __device__ inline size_t afrag_index(int dtype, int m, int k) {
+  const int vec = kv_vec(dtype), sw = 4 * vec;
+  const int lane = (m & 15) + 16 * ((k % sw) / vec);
+  return (((size_t)(k / sw) * 4 + (m >> 4)) * 64 + lane) * vec + k % vec;
+}
+inline size_t afrag_elems(int dtype, int K) {
+  const int sw = 4 * kv_vec(dtype);
+  return (size_t)((K + sw - 1) / sw) * sw * 64;
+}
+
 struct Epi {
   int kind = EPI_F32;
+  int afrag = 0;
   void* out = nullptr;
   int ldo = 0;
   const float* bias = nullptr;
@@ -103,6 +121,8 @@ struct GemmDesc {
   Epi epi;
   // Fragment-ordered weights (skinny kernel, M <= 64): K-slabs per n-block in
   // the stored tensor and the first slab used; frag_ks == 0 means row-major W.
+  // With fragment-ordered weights A is in the row-block operand layout
+  // (afrag_index) and lda is unused.
   int frag_ks = 0;
   int frag_ks0 = 0;
 };
@@ -173,6 +193,7 @@ struct AttnKvDesc {
   int S1;
   void* out;
   int ldo;
+  int out_afrag;  // out in the row-block operand layout (Sq <= 64), ldo unused
   int Sq, nq, nkv, hd;
 };
 hipError_t launch_attention_kv(const AttnKvDesc& d, const LaunchCaps& caps, hipStream_t st);
@@ -181,10 +202,11 @@ hipError_t launch_attention(const AttnDesc& a, const Scratch& s, const LaunchCap
 // Residual add + row norm: x[m] += bias + sum_s part[s][m] in split order
 // (part [splits][rows][d]; nothing is added when splits is 0), then
 // out[m] = LayerNorm (biased variance) or RMSNorm of x[m], times g (+ b),
-// in the operand type. d <= 2048.
+// in the operand type (row-major with ldo, or the row-block operand layout
+// when afrag, rows <= 64). d <= 2048.
 hipError_t launch_norm(int dtype, float* x, int ldx, int rows, int d, const float* part,
                        int splits, const float* bias, const float* g, const float* b, bool rms,
-                       void* out, int ldo, hipStream_t st);
+                       void* out, int ldo, bool afrag, hipStream_t st);
 
 // Image [views][H][W][3] fp32 -> patches [views * T][ldo] of the operand type,
 // columns beyond 3 p^2 zero.
@@ -196,10 +218,11 @@ hipError_t launch_patchify(int dtype, const float* pix, int views, int H, int W,
 hipError_t launch_embed(int dtype, const void* E, int d, int vocab, const int32_t* ids, int n,
                         float scale, float* x, int ldx, hipStream_t st);
 
-// dst_T[r, c] = T(src[r, c]) for c < cols, 0 for cols <= c < ld_dst;
+// dst_T[r, c] = T(src[r, c]) for c < cols, 0 for cols <= c < ld_dst (row-major
+// with ld_dst, or the row-block operand layout with K = ld_dst when afrag);
 // optionally also copies src into dst_f32 (fp32, ld = cols).
 hipError_t launch_cvt_pad(int dtype, const float* src, int rows, int cols, void* dst, int ld_dst,
-                          float* dst_f32, hipStream_t st);
+                          bool afrag, float* dst_f32, hipStream_t st);
 
 // dst[r, :] = row (operand type) for every r < rows.
 hipError_t launch_bcast_row(int dtype, const void* row, int cols, void* dst, int ld_dst, int rows,

@@ -110,6 +110,13 @@ __device__ __forceinline__ float bld1(Rsrc r, uint32_t off) {
 // GEMM epilogues
 // ---------------------------------------------------------------------------
 
+// Index of output element (m, n) of an operand-type epilogue output.
+template <typename T>
+__device__ __forceinline__ size_t out_at(const Epi& e, int m, int n, int ld) {
+  constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
+  return e.afrag ? afrag_index(DT, m, n) : (size_t)m * ld + n;
+}
+
 template <typename T>
 __device__ __forceinline__ void epi_one(const Epi& e, int m, int n, float v) {
   switch (e.kind) {
@@ -121,7 +128,7 @@ __device__ __forceinline__ void epi_one(const Epi& e, int m, int n, float v) {
     }
     case EPI_T: {
       if (e.bias) v += e.bias[n];
-      TT<T>::st((T*)e.out + (size_t)m * e.ldo + n, v);
+      TT<T>::st((T*)e.out + out_at<T>(e, m, n, e.ldo), v);
       break;
     }
     case EPI_RESID: {
@@ -131,12 +138,12 @@ __device__ __forceinline__ void epi_one(const Epi& e, int m, int n, float v) {
     }
     case EPI_GELU: {
       if (e.bias) v += e.bias[n];
-      TT<T>::st((T*)e.out + (size_t)m * e.ldo + n, gelu_tanh(v));
+      TT<T>::st((T*)e.out + out_at<T>(e, m, n, e.ldo), gelu_tanh(v));
       break;
     }
     case EPI_SWISH: {
       if (e.bias) v += e.bias[n];
-      TT<T>::st((T*)e.out + (size_t)m * e.ldo + n, swishf(v));
+      TT<T>::st((T*)e.out + out_at<T>(e, m, n, e.ldo), swishf(v));
       break;
     }
     case EPI_EULER: {
@@ -144,7 +151,7 @@ __device__ __forceinline__ void epi_one(const Epi& e, int m, int n, float v) {
       float* xp = e.x + (size_t)m * e.ldx + n;
       const float xn = *xp + e.dt * v;
       *xp = xn;
-      TT<T>::st((T*)e.xop + (size_t)m * e.ldxop + n, xn);
+      TT<T>::st((T*)e.xop + out_at<T>(e, m, n, e.ldxop), xn);
       break;
     }
     default:
@@ -160,7 +167,7 @@ __device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int 
   if (e.kind == EPI_GEGLU) {
     if (n + 16 >= N) return;
     const int g = n >> 5, j = n & 15;
-    TT<T>::st((T*)e.out + (size_t)m * e.ldo + 16 * g + j, gelu_tanh(v0) * v1);
+    TT<T>::st((T*)e.out + out_at<T>(e, m, 16 * g + j, e.ldo), gelu_tanh(v0) * v1);
     return;
   }
   if (e.kind == EPI_QKV_ROPE) {
@@ -401,7 +408,9 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__
 // Skinny GEMM for M <= 64 (the action expert's rows): C[M, N] = A[M, K] W^T
 // with W stored in MFMA fragment order (see frag_index): the 16 x SW fragment
 // of n-block nb and K-slab ks is 1 KB contiguous, lane l holding W[16 nb +
-// l % 16][SW ks + VEC (l / 16) ...]. A workgroup owns 32 columns (two
+// l % 16][SW ks + VEC (l / 16) ...], and A in the row-block operand layout
+// (afrag_index), so both operands load as contiguous 1 KB chunks (lda is
+// unused). A workgroup owns 32 columns (two
 // n-blocks, so the paired epilogues stay inside it) and a K-range of
 // 4 * SPW slabs; each wave takes SPW consecutive slabs and issues every load
 // of its range at once (one memory round trip), then the four waves' partial
@@ -424,7 +433,7 @@ __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, int lda
   const int total = npairs * splits;
   const T dummy = T();
   const Rsrc rw = rsrc(Wf, (size_t)npairs * 2 * KS * 64 * VEC * sizeof(T));
-  const Rsrc ra = rsrc(A, span(M, lda, K, sizeof(T)));
+  const Rsrc ra = rsrc(A, (size_t)nslab * 4 * 64 * VEC * sizeof(T));  // row-block operand layout
   for (int w = blockIdx.x; w < total; w += gridDim.x) {
     const int s = w % splits, np = w / splits;
     const int sb = (s * 4 + wave) * SPW;
@@ -442,7 +451,7 @@ __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, int lda
       for (int mt = 0; mt < 4; ++mt) {
         const int row = mt * 16 + (lane & 15);
         const bool oka = ok && row < M && k < K;
-        af[q][mt] = bld16(ra, oka ? (uint32_t)(((size_t)row * lda + k) * sizeof(T)) : OOB);
+        af[q][mt] = bld16(ra, oka ? (uint32_t)((((size_t)ks * 4 + mt) * 64 + lane) * VEC * sizeof(T)) : OOB);
       }
     }
     f32x4 acc[2][4];
@@ -1033,7 +1042,7 @@ struct Attn2Args {
   const void* k1;
   const void* v1;
   void* out;
-  int ldq, ldo;
+  int ldq, ldo, out_afrag;
   int Sq, nq, nkv, hd, S0, S1;
   int nb0, nb1;  // 32-key blocks per KV head in each segment's buffers
   int rtiles;    // 16-row tiles of packed rows per KV head
@@ -1259,17 +1268,20 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
         den += wgt * sL[u][rr];
       }
       const float inv = 1.f / den;
-      const int sq = prow / group, h = j * group + prow % group;
-      T* op = (T*)a.out + (size_t)sq * a.ldo + h * a.hd + d0;
+      const int sq = prow / group, col = (j * group + prow % group) * a.hd + d0;
+      // 16-byte pieces: one VEC group each in the row-block operand layout
+      auto at = [&](int c) {
+        constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
+        return (T*)a.out + (a.out_afrag ? afrag_index(DT, sq, c) : (size_t)sq * a.ldo + c);
+      };
       if constexpr (sizeof(T) == 2) {
         uint32_t pk[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          pk[e] = (uint32_t)f2bf(num[2 * e] * inv) | ((uint32_t)f2bf(num[2 * e + 1] * inv) << 16);
-        *(uint4*)op = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+        for (int e = 0; e < 4; ++e) pk[e] = f2bf2(num[2 * e] * inv, num[2 * e + 1] * inv);
+        *(uint4*)at(col) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
       } else {
-        *(float4*)op = make_float4(num[0] * inv, num[1] * inv, num[2] * inv, num[3] * inv);
-        *(float4*)(op + 4) = make_float4(num[4] * inv, num[5] * inv, num[6] * inv, num[7] * inv);
+        *(float4*)at(col) = make_float4(num[0] * inv, num[1] * inv, num[2] * inv, num[3] * inv);
+        *(float4*)at(col + 4) = make_float4(num[4] * inv, num[5] * inv, num[6] * inv, num[7] * inv);
       }
     }
     __syncthreads();
@@ -1301,8 +1313,9 @@ static hipError_t run_attn2_t(const Attn2Args& a, int hdp, const LaunchCaps& cap
 hipError_t launch_attention_kv(const AttnKvDesc& d, const LaunchCaps& caps, hipStream_t st) {
   const int hdp = attn_hdp(d.hd, d.dtype);
   if (hdp < 0 || d.nq % d.nkv != 0 || d.S0 <= 0 || d.S1 < 0 || d.Sq <= 0 ||
-      (d.S1 > 0 && (!d.k1 || !d.v1)) || d.hd % 8 != 0 ||
-      ((size_t)d.ldo * (d.dtype == DT_BF16 ? 2 : 4)) % 16 != 0 || ((uintptr_t)d.out & 15) != 0)
+      (d.S1 > 0 && (!d.k1 || !d.v1)) || d.hd % 8 != 0 || (d.out_afrag && d.Sq > 64) ||
+      (!d.out_afrag && ((size_t)d.ldo * (d.dtype == DT_BF16 ? 2 : 4)) % 16 != 0) ||
+      ((uintptr_t)d.out & 15) != 0)
     return hipErrorInvalidValue;
   Attn2Args a{};
   a.q = d.q;
@@ -1313,6 +1326,7 @@ hipError_t launch_attention_kv(const AttnKvDesc& d, const LaunchCaps& caps, hipS
   a.out = d.out;
   a.ldq = d.ldq;
   a.ldo = d.ldo;
+  a.out_afrag = d.out_afrag;
   a.Sq = d.Sq;
   a.nq = d.nq;
   a.nkv = d.nkv;
@@ -1353,7 +1367,8 @@ __global__ __launch_bounds__(256) void k_norm(float* __restrict__ x, int ldx, in
                                               const float* __restrict__ bias,
                                               const float* __restrict__ g,
                                               const float* __restrict__ b, int rms, T* out,
-                                              int ldo) {
+                                              int ldo, int afrag) {
+  constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
   __shared__ float red[4];
   const size_t pstride = (size_t)rows * d;
   const Rsrc rx = rsrc(x, span(rows, ldx, d, 4));
@@ -1415,14 +1430,13 @@ __global__ __launch_bounds__(256) void k_norm(float* __restrict__ x, int ldx, in
       }
     }
     const float inv = 1.f / sqrtf(block_sum(s2, red) / d + 1e-6f);
-    T* orow = out + (size_t)row * ldo;
 #pragma unroll
     for (int q = 0; q < NORM_NPT; ++q) {
       const int i = threadIdx.x + q * 256;
       if (i < d) {
         float y = (v[q] - mean) * inv * g[i];
         if (b) y += b[i];
-        TT<T>::st(orow + i, y);
+        TT<T>::st(out + (afrag ? afrag_index(DT, row, i) : (size_t)row * ldo + i), y);
       }
     }
   }
@@ -1430,15 +1444,15 @@ __global__ __launch_bounds__(256) void k_norm(float* __restrict__ x, int ldx, in
 
 hipError_t launch_norm(int dtype, float* x, int ldx, int rows, int d, const float* part,
                        int splits, const float* bias, const float* g, const float* b, bool rms,
-                       void* out, int ldo, hipStream_t st) {
-  if (d > 256 * NORM_NPT) return hipErrorInvalidValue;
+                       void* out, int ldo, bool afrag, hipStream_t st) {
+  if (d > 256 * NORM_NPT || (afrag && rows > 64)) return hipErrorInvalidValue;
   const int grid = std::min(rows, 4096);
   if (dtype == DT_BF16)
     k_norm<uint16_t><<<grid, 256, 0, st>>>(x, ldx, rows, d, part, splits, bias, g, b, rms,
-                                           (uint16_t*)out, ldo);
+                                           (uint16_t*)out, ldo, afrag);
   else
     k_norm<float><<<grid, 256, 0, st>>>(x, ldx, rows, d, part, splits, bias, g, b, rms,
-                                        (float*)out, ldo);
+                                        (float*)out, ldo, afrag);
   return hipGetLastError();
 }
 
@@ -1500,26 +1514,28 @@ hipError_t launch_embed(int dtype, const void* E, int d, int vocab, const int32_
 
 template <typename T>
 __global__ void k_cvt_pad(const float* __restrict__ src, int rows, int cols, T* __restrict__ dst,
-                          int ld, float* __restrict__ dst32) {
+                          int ld, int afrag, float* __restrict__ dst32) {
+  constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
   const long long total = (long long)rows * ld;
   for (long long idx = blockIdx.x * (long long)blockDim.x + threadIdx.x; idx < total;
        idx += (long long)gridDim.x * blockDim.x) {
     const int c = (int)(idx % ld);
     const long long r = idx / ld;
     const float v = c < cols ? src[r * cols + c] : 0.f;
-    TT<T>::st(dst + idx, v);
+    TT<T>::st(dst + (afrag ? afrag_index(DT, (int)r, c) : (size_t)idx), v);
     if (dst32 && c < cols) dst32[r * cols + c] = v;
   }
 }
 
 hipError_t launch_cvt_pad(int dtype, const float* src, int rows, int cols, void* dst, int ld_dst,
-                          float* dst_f32, hipStream_t st) {
+                          bool afrag, float* dst_f32, hipStream_t st) {
+  if (afrag && rows > 64) return hipErrorInvalidValue;
   const long long total = (long long)rows * ld_dst;
   const int grid = (int)std::min<long long>((total + 255) / 256, 1024);
   if (dtype == DT_BF16)
-    k_cvt_pad<uint16_t><<<grid, 256, 0, st>>>(src, rows, cols, (uint16_t*)dst, ld_dst, dst_f32);
+    k_cvt_pad<uint16_t><<<grid, 256, 0, st>>>(src, rows, cols, (uint16_t*)dst, ld_dst, afrag, dst_f32);
   else
-    k_cvt_pad<float><<<grid, 256, 0, st>>>(src, rows, cols, (float*)dst, ld_dst, dst_f32);
+    k_cvt_pad<float><<<grid, 256, 0, st>>>(src, rows, cols, (float*)dst, ld_dst, afrag, dst_f32);
   return hipGetLastError();
 }
 

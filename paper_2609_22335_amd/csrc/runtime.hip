@@ -228,7 +228,7 @@ struct vla_model {
   // constant tables
   float* rope_cos = nullptr;
   float* rope_sin = nullptr;
-  void* phi = nullptr;  // [n_steps][ex_dim] operand type
+  void* phi = nullptr;  // [n_steps][ex_dim] operand type, row-block operand layout
   float* ck = nullptr;  // [n_steps][ex_dim]: W_2 phi(t_k) + b_2
 
   // phase scratch
@@ -495,11 +495,13 @@ static int attn(const Run& r, const char* tag, const AttnDesc& a) {
 
 // Residual add of `splits` pending partials (from the phase scratch) + bias,
 // then LayerNorm / RMSNorm into `out`.
+// out: row-major [rows][d], or the row-block operand layout when it feeds a
+// skinny GEMM (afrag)
 static int norm(const Run& r, float* x, int rows, int d, int splits, const float* bias, int g, int b,
-                bool rms, void* out) {
+                bool rms, void* out, bool afrag = false) {
   vla_model* m = r.m;
   hipError_t err = launch_norm(m->dt, x, d, rows, d, r.scr->ptr, splits, bias, m->f32(g),
-                               b >= 0 ? m->f32(b) : nullptr, rms, out, d, r.st);
+                               b >= 0 ? m->f32(b) : nullptr, rms, out, d, afrag, r.st);
   if (err != hipSuccess) return fail(VLA_EHIP, std::string("norm: ") + hipGetErrorString(err));
   return VLA_OK;
 }
@@ -537,7 +539,9 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   vla_model* m = r.m;
   const vla_config& c = m->c;
   const Dims& d = m->d;
-  VLA_TRY(norm(r, x, rows, dim, *pend, nullptr, L.rms1, -1, true, h));
+  // the expert's activations feed skinny GEMMs: row-block operand layout
+  const bool af = !lm;
+  VLA_TRY(norm(r, x, rows, dim, *pend, nullptr, L.rms1, -1, true, h, af));
   *pend = 0;
   Epi e;
   e.kind = EPI_QKV_ROPE;
@@ -572,6 +576,7 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   }
   a.out = att;
   a.ldo = d.qd;
+  a.out_afrag = af;
   a.Sq = rows;
   a.nq = c.lm_heads;
   a.nkv = c.lm_kv_heads;
@@ -579,9 +584,10 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   VLA_TRY(attn_kv(r, lm ? "lm.attn" : "ex.attn", a));
   int so = 0;
   VLA_TRY(gemm_part(r, lm ? "lm.o" : "ex.o", att, d.qd, L.o, rows, dim, d.qd, &so));
-  VLA_TRY(norm(r, x, rows, dim, so, nullptr, L.rms2, -1, true, h));
-  VLA_TRY(gemm(r, lm ? "lm.gateup" : "ex.gateup", h, dim, L.gu, rows, 2 * mlp, dim,
-               epi_kind(EPI_GEGLU, mlpbuf, mlp)));
+  VLA_TRY(norm(r, x, rows, dim, so, nullptr, L.rms2, -1, true, h, af));
+  Epi eg = epi_kind(EPI_GEGLU, mlpbuf, mlp);
+  eg.afrag = af;
+  VLA_TRY(gemm(r, lm ? "lm.gateup" : "ex.gateup", h, dim, L.gu, rows, 2 * mlp, dim, eg));
   VLA_TRY(gemm_part(r, lm ? "lm.down" : "ex.down", mlpbuf, mlp, L.down, rows, dim, mlp, pend));
   return VLA_OK;
 }
@@ -637,7 +643,7 @@ static int run_prefill(const Run& r, const vla_frame* f, vla_ctx* ctx) {
   HIP_TRY(launch_embed(m->dt, m->tptr(m->embed), dl, c.vocab, f->text_ids, c.n_text, std::sqrt((float)dl),
                        w.xl + (size_t)d.nimg * dl, dl, r.st));
   if (c.state_dim > 0) {
-    HIP_TRY(launch_cvt_pad(m->dt, f->state, 1, c.state_dim, w.sbuf, d.s_pad, nullptr, r.st));
+    HIP_TRY(launch_cvt_pad(m->dt, f->state, 1, c.state_dim, w.sbuf, d.s_pad, false, nullptr, r.st));
     VLA_TRY(gemm(r, "state", w.sbuf, d.s_pad, m->state_w, 1, dl, d.s_pad,
                  epi_kind(EPI_F32, w.xl + (size_t)(d.prefix - 1) * dl, dl, m->f32(m->state_b))));
   }
@@ -661,13 +667,18 @@ static int run_denoise(const Run& r, const vla_ctx* ctx, const float* noise, flo
   ActWs& w = *r.aw;
   const int H = c.chunk_len, de = c.ex_dim, A = c.action_dim;
   const float dt = -1.0f / (float)c.n_steps;
-  HIP_TRY(launch_cvt_pad(m->dt, noise, H, A, w.xop, d.a_pad, x, r.st));
+  // every operand of the expert's GEMMs is in the row-block operand layout
+  HIP_TRY(launch_cvt_pad(m->dt, noise, H, A, w.xop, d.a_pad, true, x, r.st));
   const size_t layer_k = ctx_layer_k(m) * m->esz;
   const size_t layer_v = ctx_layer_v(m) * m->esz;
   for (int k = 0; k < c.n_steps; ++k) {
     // action embedding and time conditioning
-    VLA_TRY(gemm(r, "ex.in", w.xop, d.a_pad, m->in_w, H, de, d.a_pad, epi_kind(EPI_T, w.a, de, m->f32(m->in_b))));
-    VLA_TRY(gemm(r, "ex.time1", w.a, de, m->t1_w, H, de, de, epi_kind(EPI_SWISH, w.hid, de, m->ck + (size_t)k * de)));
+    Epi ein = epi_kind(EPI_T, w.a, de, m->f32(m->in_b));
+    ein.afrag = 1;
+    VLA_TRY(gemm(r, "ex.in", w.xop, d.a_pad, m->in_w, H, de, d.a_pad, ein));
+    Epi et1 = epi_kind(EPI_SWISH, w.hid, de, m->ck + (size_t)k * de);
+    et1.afrag = 1;
+    VLA_TRY(gemm(r, "ex.time1", w.a, de, m->t1_w, H, de, de, et1));
     VLA_TRY(gemm(r, "ex.time2", w.hid, de, m->t2_w, H, de, de, epi_kind(EPI_F32, w.u, de, m->f32(m->t2_b))));
     int pend = 0;
     for (int l = 0; l < c.ex_layers; ++l) {
@@ -676,9 +687,10 @@ static int run_denoise(const Run& r, const vla_ctx* ctx, const float* noise, flo
       VLA_TRY(decoder_layer(r, false, m->ex[l], w.u, H, de, c.ex_mlp, w.h, w.q, w.kown, w.vown, d.prefix,
                             K, V, d.prefix, w.att, w.mlp, false, &pend));
     }
-    VLA_TRY(norm(r, w.u, H, de, pend, nullptr, m->fin_g, -1, true, w.h));
+    VLA_TRY(norm(r, w.u, H, de, pend, nullptr, m->fin_g, -1, true, w.h, true));
     Epi e;
     e.kind = EPI_EULER;
+    e.afrag = 1;
     e.bias = m->f32(m->out_b);
     e.x = x;
     e.ldx = A;
@@ -754,13 +766,19 @@ static int setup_tables(vla_model* m) {
       phi[(size_t)k * de + dh + i] = (float)std::cos(x);
     }
   }
-  VLA_TRY(dmalloc(m, &m->phi, phi.size() * m->esz));
+  // phi feeds a skinny GEMM: row-block operand layout (n_steps <= 64 rows)
+  const size_t nphi = afrag_elems(m->dt, de);
+  VLA_TRY(dmalloc(m, &m->phi, nphi * m->esz));
   if (m->dt == DT_BF16) {
-    std::vector<uint16_t> hb(phi.size());
-    for (size_t i = 0; i < phi.size(); ++i) hb[i] = bf16_bits(phi[i]);
+    std::vector<uint16_t> hb(nphi, 0);
+    for (int k = 0; k < c.n_steps; ++k)
+      for (int i = 0; i < de; ++i) hb[afrag_index(m->dt, k, i)] = bf16_bits(phi[(size_t)k * de + i]);
     HIP_TRY(hipMemcpy(m->phi, hb.data(), hb.size() * 2, hipMemcpyHostToDevice));
   } else {
-    HIP_TRY(hipMemcpy(m->phi, phi.data(), phi.size() * 4, hipMemcpyHostToDevice));
+    std::vector<float> hf(nphi, 0.f);
+    for (int k = 0; k < c.n_steps; ++k)
+      for (int i = 0; i < de; ++i) hf[afrag_index(m->dt, k, i)] = phi[(size_t)k * de + i];
+    HIP_TRY(hipMemcpy(m->phi, hf.data(), hf.size() * 4, hipMemcpyHostToDevice));
   }
   VLA_TRY(dmalloc(m, (void**)&m->ck, (size_t)c.n_steps * de * 4));
   return VLA_OK;
@@ -778,17 +796,20 @@ static int add_act_lane(vla_model* m) {
   std::unique_ptr<ActWs> lane(new ActWs());
   ActWs& a = *lane;
   VLA_TRY(dmalloc(m, (void**)&a.u, (size_t)H * de * 4));
-  VLA_TRY(dmalloc(m, &a.xop, (size_t)H * d.a_pad * e));
-  VLA_TRY(dmalloc(m, &a.a, (size_t)H * de * e));
-  VLA_TRY(dmalloc(m, &a.hid, (size_t)H * de * e));
-  VLA_TRY(dmalloc(m, &a.h, (size_t)H * de * e));
+  // skinny-GEMM operands: row-block operand layout (64 rows), zeroed so the
+  // padding columns of xop stay zero
+  VLA_TRY(dmalloc(m, &a.xop, afrag_elems(dt, d.a_pad) * e));
+  HIP_TRY(hipMemset(a.xop, 0, afrag_elems(dt, d.a_pad) * e));
+  VLA_TRY(dmalloc(m, &a.a, afrag_elems(dt, de) * e));
+  VLA_TRY(dmalloc(m, &a.hid, afrag_elems(dt, de) * e));
+  VLA_TRY(dmalloc(m, &a.h, afrag_elems(dt, de) * e));
   VLA_TRY(dmalloc(m, &a.q, (size_t)H * d.qd * e));
   VLA_TRY(dmalloc(m, &a.kown, own_k(m) * e));
   VLA_TRY(dmalloc(m, &a.vown, own_v(m) * e));
   HIP_TRY(hipMemset(a.kown, 0, own_k(m) * e));  // padding stays zero
   HIP_TRY(hipMemset(a.vown, 0, own_v(m) * e));
-  VLA_TRY(dmalloc(m, &a.att, (size_t)H * d.qd * e));
-  VLA_TRY(dmalloc(m, &a.mlp, (size_t)H * c.ex_mlp * e));
+  VLA_TRY(dmalloc(m, &a.att, afrag_elems(dt, d.qd) * e));
+  VLA_TRY(dmalloc(m, &a.mlp, afrag_elems(dt, c.ex_mlp) * e));
   ScratchNeed sa;
   upd(sa, gemm_scratch(dt, H, de, d.a_pad, false, true));
   upd(sa, gemm_scratch(dt, H, de, de, false, true));
