@@ -61,7 +61,18 @@ typedef struct vla_config {
   int32_t vocab, n_text, state_dim;              /* state_dim 0 = no state token */
   int32_t ex_dim, ex_mlp, ex_layers;             /* ex_layers must equal lm_layers */
   int32_t chunk_len, action_dim, n_steps;        /* action chunk H x A, Euler steps */
+  int32_t head;     /* VLA_HEAD_PI0 or VLA_HEAD_DIT                                  */
+  int32_t shuffle;  /* pixel-shuffle factor of the ViT grid before the projector (1: none) */
+  int32_t ex_heads; /* VLA_HEAD_DIT: attention heads of the DiT (head dim ex_dim / ex_heads) */
 } vla_config;
+
+/* Action-head families (Section 2.1): the pi0-style expert runs its own
+ * decoder layers over [the LM's per-layer KV cache; its own K/V]
+ * (ex_layers == lm_layers); the GR00T-style DiT (adaLN-conditioned, even
+ * layers cross-attending to the LM's final normalised hidden states, odd
+ * layers self-attending) reads per-frame cross K/V made from those features. */
+#define VLA_HEAD_PI0 0
+#define VLA_HEAD_DIT 1
 
 typedef struct vla_model vla_model;
 typedef struct vla_ctx vla_ctx;

@@ -27,6 +27,15 @@ with ``_op`` (round to fp32, then to bf16, nearest-even):
 Residual stream, norm statistics, softmax probabilities, velocities and the
 Euler state stay exact (fp64 here). For fp32 configurations ``_op`` is the
 identity and the oracle is the exact-arithmetic model.
+
+Two action-head families (Section 2.1 names both flow-matching heads that
+read the VLM's KV cache, as in pi0, and diffusion-transformer heads that read
+the VLM's features): ``head == 0`` is the pi0-style expert sharing the LM
+cache; ``head == 1`` is a GR00T-style DiT whose even layers cross-attend to
+the LM's final normalised hidden states (the features) and whose odd layers
+self-attend, conditioned on the flow time through adaLN. The DiT config also
+pixel-shuffles the ViT grid 2x2 before the projector and runs every LM layer
+(the features need the last layer's output).
 """
 from __future__ import annotations
 
@@ -163,6 +172,24 @@ def sinusoid(t, dim):
     return np.concatenate([np.sin(x), np.cos(x)])
 
 
+def positions_sinusoid(n, dim):
+    """Fixed token positions of the DiT: row p is [sin(p w_i)]_i ++ [cos(p w_i)]_i
+    with w_i = 10000^(-i / (dim/2)), i < dim/2."""
+    half = dim // 2
+    w = ROPE_BASE ** (-np.arange(half, dtype=np.float64) / half)
+    ang = np.arange(n, dtype=np.float64)[:, None] * w[None, :]
+    return np.concatenate([np.sin(ang), np.cos(ang)], axis=1)
+
+
+def pixel_shuffle(x, grid_h, grid_w, s):
+    """Space-to-depth of a raster token grid: [gh gw, c] -> [(gh/s)(gw/s), s^2 c];
+    coarse token (i, j) concatenates fine tokens (s i + dy, s j + dx) in
+    (dy, dx) order, channels fastest."""
+    c = x.shape[1]
+    t = x.reshape(grid_h // s, s, grid_w // s, s, c).transpose(0, 2, 1, 3, 4)
+    return t.reshape((grid_h // s) * (grid_w // s), s * s * c)
+
+
 def flow_times(n_steps) -> Tuple[List[float], float]:
     """Euler schedule of the flow-matching head: noise sits at t = 1 and the
     data at t = 0; t_k = (N - k) / N and dt = -1 / N, each one fp32 division."""
@@ -214,11 +241,15 @@ def vit_view(P, cfg, img):
 
 
 def image_tokens(P, cfg, pixels):
-    """Views encoded independently, projected to the LM width, view-major."""
+    """Views encoded independently, pixel-shuffled when the config asks for it,
+    projected to the LM width, view-major."""
     outs = []
+    gh, gw, s = cfg["img_h"] // cfg["patch"], cfg["img_w"] // cfg["patch"], cfg.get("shuffle", 1)
     for v in range(cfg["n_views"]):
-        y = _op(vit_view(P, cfg, pixels[v]), cfg)
-        outs.append(linear(y, _w(P, "proj.w"), _w(P, "proj.b")))
+        y = vit_view(P, cfg, pixels[v])
+        if s > 1:
+            y = pixel_shuffle(y, gh, gw, s)
+        outs.append(linear(_op(y, cfg), _w(P, "proj.w"), _w(P, "proj.b")))
     return np.concatenate(outs, axis=0)
 
 
@@ -285,15 +316,52 @@ def lm_prefill(P, cfg, x0):
     return cache
 
 
+def lm_features(P, cfg, x0):
+    """Every LM layer over the prefix (positions 0 .. P-1, no mask), then the
+    final RMSNorm: the features a DiT head reads. Returns (features, cache)."""
+    x = np.asarray(x0, dtype=np.float64)
+    pos = np.arange(x.shape[0])
+    cache = []
+    for l in range(cfg["lm_layers"]):
+        x, k, v = decoder_layer(P, cfg, f"lm.{l}.", x, pos)
+        cache.append((k, v))
+    return rms_norm(x, _w(P, "lm.final.g")), cache
+
+
+def dit_cross_kv(P, cfg, feats):
+    """K, V of every cross-attention (even) DiT layer from the features, once
+    per frame: [S, heads, hd] each, no biases."""
+    s, nh = feats.shape[0], cfg["ex_heads"]
+    hd = cfg["ex_dim"] // nh
+    f = _op(feats, cfg)
+    out = {}
+    for l in range(0, cfg["ex_layers"], 2):
+        p = f"ex.{l}."
+        out[l] = (_op(linear(f, _w(P, p + "k.w")), cfg).reshape(s, nh, hd),
+                  _op(linear(f, _w(P, p + "v.w")), cfg).reshape(s, nh, hd))
+    return out
+
+
 def vlm_prefill(P, cfg, frame, capture: Optional[dict] = None):
+    """Phase 1. pi0 head: the per-layer KV cache. DiT head: the cross K/V of
+    the DiT's even layers (from the LM features)."""
     img = image_tokens(P, cfg, frame["pixels"])
     x0 = prefix(P, cfg, frame, img)
-    cache = lm_prefill(P, cfg, x0)
+    feats = None
+    if cfg.get("head", 0) == 1:
+        feats, cache = lm_features(P, cfg, x0)
+        out = dit_cross_kv(P, cfg, feats)
+    else:
+        cache = lm_prefill(P, cfg, x0)
+        out = cache
     if capture is not None:
         capture["image_tokens"] = img
         capture["prefix"] = x0
         capture["kv"] = cache
-    return cache
+        if feats is not None:
+            capture["features"] = feats
+            capture["cross_kv"] = out
+    return out
 
 
 # ---------------------------------------------------------------------------
@@ -322,10 +390,63 @@ def expert_velocity(P, cfg, cache, x, t):
     return linear(h, _w(P, "ex.out.w"), _w(P, "ex.out.b"))
 
 
+def dit_condition(P, cfg, t):
+    """c = W_t2 swish(W_t1 phi_256(t) + b_t1) + b_t2 (the timestep embedder);
+    returns the adaLN input swish(c) as stored for its GEMMs."""
+    phi = _op(sinusoid(t, P["ex.time1.w"].shape[1])[None, :], cfg)
+    hid = _op(swish(linear(phi, _w(P, "ex.time1.w"), _w(P, "ex.time1.b"))), cfg)
+    c = linear(hid, _w(P, "ex.time2.w"), _w(P, "ex.time2.b"))
+    return _op(swish(c), cfg)
+
+
+def adaln(x, shift, scale):
+    """LayerNorm without affine parameters, then x (1 + scale) + shift."""
+    return layer_norm(x, 1.0 + scale, shift)
+
+
+def dit_velocity(P, cfg, cross, x, t):
+    """v(x_t, t) of the GR00T-style DiT head.
+
+    X = W_a x + b_a + pos (fixed sinusoid positions); per layer l, from
+    (shift1, scale1, gate1, shift2, scale2, gate2) = W_l swish(c) + b_l:
+    X += gate1 * W_o MHA(adaLN(X; shift1, scale1)) -- cross-attention to the
+    features' K/V on even layers, self-attention on odd ones, no mask, no
+    biases -- then X += gate2 * W_2 GELU(W_1 adaLN(X; shift2, scale2)).
+    Finally (shift, scale) = W_f swish(c) + b_f and v = W_out adaLN(X) + b_out."""
+    hlen, de, nh = x.shape[0], cfg["ex_dim"], cfg["ex_heads"]
+    hd = de // nh
+    X = linear(_op(x, cfg), _w(P, "ex.in.w"), _w(P, "ex.in.b")) + positions_sinusoid(hlen, de)
+    sc = dit_condition(P, cfg, t)
+    for l in range(cfg["ex_layers"]):
+        p = f"ex.{l}."
+        mod = linear(sc, _w(P, p + "ada.w"), _w(P, p + "ada.b"))[0].reshape(6, de)
+        sh1, sc1, g1, sh2, sc2, g2 = mod
+        h = _op(adaln(X, sh1, sc1), cfg)
+        q = _op(linear(h, _w(P, p + "q.w")), cfg).reshape(hlen, nh, hd)
+        if l % 2 == 0:
+            k, v = cross[l]
+        else:
+            k = _op(linear(h, _w(P, p + "k.w")), cfg).reshape(hlen, nh, hd)
+            v = _op(linear(h, _w(P, p + "v.w")), cfg).reshape(hlen, nh, hd)
+        a = _op(attention(q, k, v).reshape(hlen, de), cfg)
+        X = X + g1 * linear(a, _w(P, p + "o.w"))
+        h2 = _op(adaln(X, sh2, sc2), cfg)
+        f = _op(gelu_tanh(linear(h2, _w(P, p + "fc1.w"))), cfg)
+        X = X + g2 * linear(f, _w(P, p + "fc2.w"))
+    sh, scl = linear(sc, _w(P, "ex.final.ada.w"), _w(P, "ex.final.ada.b"))[0].reshape(2, de)
+    h = _op(adaln(X, sh, scl), cfg)
+    return linear(h, _w(P, "ex.out.w"), _w(P, "ex.out.b"))
+
+
 def action_denoise(P, cfg, cache, noise):
-    """Euler integration of the expert's velocity from x_0 = noise (t = 1) to
-    t = 0; returns the action chunk [chunk_len, action_dim]."""
-    return euler_integrate(noise, lambda x, t: expert_velocity(P, cfg, cache, x, t), cfg["n_steps"])
+    """Euler integration of the head's velocity from x_0 = noise (t = 1) to
+    t = 0; returns the action chunk [chunk_len, action_dim]. ``cache`` is the
+    phase-1 hand-off (KV cache, or the DiT's cross K/V)."""
+    if cfg.get("head", 0) == 1:
+        vel = lambda x, t: dit_velocity(P, cfg, cache, x, t)
+    else:
+        vel = lambda x, t: expert_velocity(P, cfg, cache, x, t)
+    return euler_integrate(noise, vel, cfg["n_steps"])
 
 
 def forward(P, cfg, frame, capture: Optional[dict] = None):

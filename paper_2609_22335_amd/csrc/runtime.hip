@@ -101,7 +101,18 @@ static int validate(const vla_config* c) {
   if (c->head_dim % 32 || c->head_dim > 256) return bad("head_dim must be a multiple of 32, <= 256");
   if (c->dtype == VLA_F32 && (c->head_dim > 128 || vhd > 128))
     return bad("fp32 configurations need head dims <= 128");
-  if (c->ex_layers != c->lm_layers) return bad("ex_layers must equal lm_layers (layer-wise KV sharing)");
+  if (c->head != VLA_HEAD_PI0 && c->head != VLA_HEAD_DIT) return bad("head");
+  if (c->shuffle < 1 || (c->img_h / c->patch) % c->shuffle || (c->img_w / c->patch) % c->shuffle)
+    return bad("shuffle must be >= 1 and divide the patch grid");
+  if (c->head == VLA_HEAD_PI0) {
+    if (c->ex_layers != c->lm_layers) return bad("ex_layers must equal lm_layers (layer-wise KV sharing)");
+  } else {
+    if (c->ex_heads <= 0 || c->ex_dim % c->ex_heads) return bad("ex_heads must divide ex_dim");
+    const int ehd = c->ex_dim / c->ex_heads;
+    if (ehd % 8 || ehd > 256 || (c->dtype == VLA_F32 && ehd > 128))
+      return bad("DiT head dim must be a multiple of 8, <= 256 (<= 128 in fp32)");
+    if (c->ex_dim % 2) return bad("ex_dim must be even");
+  }
   if (c->lm_mlp % 16 || c->ex_mlp % 16) return bad("lm_mlp / ex_mlp must be multiples of 16");
   if (c->vit_dim % 8 || c->lm_dim % 8 || c->ex_dim % 8 || c->vit_mlp % 8)
     return bad("model widths must be multiples of 8");
@@ -115,12 +126,22 @@ static bool preset(const char* name, vla_config* o) {
   const std::string n(name);
   if (n == "tiny") {
     *o = vla_config{VLA_F32, 1, 128, 128, 16, 256, 4, 1024, 2, 256, 4, 1, 64, 1024, 2,
-                    1024, 16, 0, 128, 512, 2, 8, 7, 4};
+                    1024, 16, 0, 128, 512, 2, 8, 7, 4, VLA_HEAD_PI0, 1, 0};
+    return true;
+  }
+  if (n == "tiny_dit") {
+    *o = vla_config{VLA_F32, 1, 128, 128, 16, 256, 4, 1024, 2, 256, 4, 4, 64, 1024, 2,
+                    1024, 16, 0, 192, 768, 4, 8, 7, 4, VLA_HEAD_DIT, 2, 4};
+    return true;
+  }
+  if (n == "gr00t") {
+    *o = vla_config{VLA_BF16, 1, 448, 448, 28, 1152, 16, 4304, 27, 2048, 16, 16, 128, 8192, 12,
+                    1024, 32, 0, 1536, 6144, 16, 16, 32, 4, VLA_HEAD_DIT, 2, 32};
     return true;
   }
   if (n == "pi0" || n == "pi0_3view") {
     *o = vla_config{VLA_BF16, 1, 224, 224, 14, 1152, 16, 4304, 27, 2048, 8, 1, 256, 16384, 18,
-                    1024, 48, 32, 1024, 4096, 18, 50, 32, 10};
+                    1024, 48, 32, 1024, 4096, 18, 50, 32, 10, VLA_HEAD_PI0, 1, 0};
     if (n == "pi0_3view") {
       o->n_views = 3;
       o->n_text = 64;
@@ -869,6 +890,7 @@ static int setup_workspaces(vla_model* m) {
 
 static int create_impl(const vla_config* cfg, uint64_t seed, vla_model** out) {
   VLA_TRY(validate(cfg));
+  if (cfg->head == VLA_HEAD_DIT) return fail(VLA_EUNSUPPORTED, "the DiT head is not built yet");
   std::unique_ptr<vla_model> m(new vla_model());
   m->c = *cfg;
   m->d = derive(*cfg);

@@ -172,10 +172,16 @@ CONFIG_FIELDS = (
     "lm_dim", "lm_heads", "lm_kv_heads", "head_dim", "lm_mlp", "lm_layers",
     "vocab", "n_text", "state_dim",
     "ex_dim", "ex_mlp", "ex_layers", "chunk_len", "action_dim", "n_steps",
+    "head", "shuffle", "ex_heads",
 )
+
+#: Action-head families: the pi0-style expert that shares the LM's KV cache,
+#: and the GR00T-style DiT that cross-attends to the LM's final features.
+HEAD_PI0, HEAD_DIT = 0, 1
 
 
 def _cfg(**kw) -> Dict[str, int]:
+    kw = dict(dict(head=HEAD_PI0, shuffle=1, ex_heads=0), **kw)
     missing = [f for f in CONFIG_FIELDS if f not in kw]
     assert not missing, missing
     return {f: int(kw[f]) for f in CONFIG_FIELDS}
@@ -208,7 +214,39 @@ def micro(dtype: int = F32) -> Dict[str, int]:
                 ex_dim=32, ex_mlp=64, ex_layers=1, chunk_len=5, action_dim=3, n_steps=2)
 
 
-PRESETS = {"tiny": TINY, "pi0": PI0, "pi0_3view": PI0_3VIEW}
+#: GR00T-shaped VLA: the ViT on 448x448 with 28x28 patches (256 patches),
+#: 2x2 pixel shuffle to 64 tokens, a 12-layer multi-head LM whose final
+#: normalised hidden states are the features, and a 16-layer DiT action head
+#: (even layers cross-attend to the features, odd layers self-attend; adaLN
+#: timestep conditioning), chunk 16x32, 4 Euler steps.
+GR00T = _cfg(dtype=BF16, n_views=1, img_h=448, img_w=448, patch=28,
+             vit_dim=1152, vit_heads=16, vit_mlp=4304, vit_layers=27,
+             lm_dim=2048, lm_heads=16, lm_kv_heads=16, head_dim=128, lm_mlp=8192, lm_layers=12,
+             vocab=1024, n_text=32, state_dim=0,
+             ex_dim=1536, ex_mlp=6144, ex_layers=16, chunk_len=16, action_dim=32, n_steps=4,
+             head=HEAD_DIT, shuffle=2, ex_heads=32)
+
+
+def micro_dit(dtype: int = F32) -> Dict[str, int]:
+    """Smallest DiT-head model: 4x4 patches shuffled to 2x2 tokens, head dim 48."""
+    return _cfg(dtype=dtype, n_views=1, img_h=32, img_w=32, patch=8,
+                vit_dim=64, vit_heads=2, vit_mlp=136, vit_layers=1,
+                lm_dim=64, lm_heads=2, lm_kv_heads=2, head_dim=32, lm_mlp=128, lm_layers=2,
+                vocab=1024, n_text=5, state_dim=0,
+                ex_dim=96, ex_mlp=192, ex_layers=2, chunk_len=5, action_dim=3, n_steps=2,
+                head=HEAD_DIT, shuffle=2, ex_heads=2)
+
+
+#: GR00T-shaped wiring at tiny sizes (fp32): 8x8 patches -> 16 tokens,
+#: 4 DiT layers of width 192 (4 heads of 48).
+TINY_DIT = _cfg(dtype=F32, n_views=1, img_h=128, img_w=128, patch=16,
+                vit_dim=256, vit_heads=4, vit_mlp=1024, vit_layers=2,
+                lm_dim=256, lm_heads=4, lm_kv_heads=4, head_dim=64, lm_mlp=1024, lm_layers=2,
+                vocab=1024, n_text=16, state_dim=0,
+                ex_dim=192, ex_mlp=768, ex_layers=4, chunk_len=8, action_dim=7, n_steps=4,
+                head=HEAD_DIT, shuffle=2, ex_heads=4)
+
+PRESETS = {"tiny": TINY, "pi0": PI0, "pi0_3view": PI0_3VIEW, "gr00t": GR00T, "tiny_dit": TINY_DIT}
 
 
 def derived(cfg: Dict[str, int]) -> Dict[str, int]:
@@ -216,7 +254,7 @@ def derived(cfg: Dict[str, int]) -> Dict[str, int]:
     length P, key length of the expert's joint attention."""
     ph, pw = cfg["img_h"] // cfg["patch"], cfg["img_w"] // cfg["patch"]
     t_view = ph * pw
-    n_img = cfg["n_views"] * t_view
+    n_img = cfg["n_views"] * t_view // cfg["shuffle"] ** 2
     prefix = n_img + cfg["n_text"] + (1 if cfg["state_dim"] > 0 else 0)
     return {"grid_h": ph, "grid_w": pw, "tokens_per_view": t_view, "n_img": n_img,
             "prefix": prefix, "patch_dim": 3 * cfg["patch"] ** 2,
@@ -228,6 +266,7 @@ def derived(cfg: Dict[str, int]) -> Dict[str, int]:
 # --------------------------------------------------------------------------
 
 WEIGHT_STD = 0.02
+DIT_TIME_DIM = 256  # width of the DiT's sinusoidal timestep embedding
 
 
 def param_specs(cfg: Dict[str, int]) -> List[Tuple[str, Tuple[int, ...], float, float]]:
@@ -256,7 +295,7 @@ def param_specs(cfg: Dict[str, int]) -> List[Tuple[str, Tuple[int, ...], float, 
         w(p + "fc1.w", (cfg["vit_mlp"], dv)); w(p + "fc1.b", (cfg["vit_mlp"],))
         w(p + "fc2.w", (dv, cfg["vit_mlp"])); w(p + "fc2.b", (dv,))
     g("vit.post.g", dv); w("vit.post.b", (dv,))
-    w("proj.w", (dl, dv)); w("proj.b", (dl,))
+    w("proj.w", (dl, dv * cfg["shuffle"] ** 2)); w("proj.b", (dl,))
     w("lm.embed", (cfg["vocab"], dl))
     if cfg["state_dim"] > 0:
         w("state.w", (dl, cfg["state_dim"])); w("state.b", (dl,))
@@ -264,13 +303,28 @@ def param_specs(cfg: Dict[str, int]) -> List[Tuple[str, Tuple[int, ...], float, 
         p = f"lm.{l}."
         g(p + "rms1.g", dl)
         w(p + "q.w", (nq * hd, dl)); w(p + "k.w", (nkv * hd, dl)); w(p + "v.w", (nkv * hd, dl))
-        if l == cfg["lm_layers"] - 1:
+        if l == cfg["lm_layers"] - 1 and cfg["head"] == HEAD_PI0:
             break  # the last layer's attention output and MLP never reach the KV cache
         w(p + "o.w", (dl, nq * hd))
         g(p + "rms2.g", dl)
         w(p + "gate.w", (cfg["lm_mlp"], dl)); w(p + "up.w", (cfg["lm_mlp"], dl))
         w(p + "down.w", (dl, cfg["lm_mlp"]))
     a = cfg["action_dim"]
+    if cfg["head"] == HEAD_DIT:
+        g("lm.final.g", dl)
+        w("ex.in.w", (de, a)); w("ex.in.b", (de,))
+        w("ex.time1.w", (de, DIT_TIME_DIM)); w("ex.time1.b", (de,))
+        w("ex.time2.w", (de, de)); w("ex.time2.b", (de,))
+        for l in range(cfg["ex_layers"]):
+            p = f"ex.{l}."
+            w(p + "ada.w", (6 * de, de)); w(p + "ada.b", (6 * de,))
+            kv_in = dl if l % 2 == 0 else de  # even layers cross-attend to the features
+            w(p + "q.w", (de, de)); w(p + "k.w", (de, kv_in)); w(p + "v.w", (de, kv_in))
+            w(p + "o.w", (de, de))
+            w(p + "fc1.w", (cfg["ex_mlp"], de)); w(p + "fc2.w", (de, cfg["ex_mlp"]))
+        w("ex.final.ada.w", (2 * de, de)); w("ex.final.ada.b", (2 * de,))
+        w("ex.out.w", (a, de)); w("ex.out.b", (a,))
+        return out
     w("ex.in.w", (de, a)); w("ex.in.b", (de,))
     w("ex.time1.w", (de, 2 * de)); w("ex.time1.b", (de,))
     w("ex.time2.w", (de, de)); w("ex.time2.b", (de,))

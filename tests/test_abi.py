@@ -34,6 +34,8 @@ def test_presets_match_shapes():
     assert V.vla_preset("tiny") == synth.TINY
     assert V.vla_preset("pi0") == synth.PI0
     assert V.vla_preset("pi0_3view") == synth.PI0_3VIEW
+    assert V.vla_preset("gr00t") == synth.GR00T
+    assert V.vla_preset("tiny_dit") == synth.TINY_DIT
     with pytest.raises(V.VlaError) as e:
         V.vla_preset("nope")
     assert e.value.code == -1

@@ -428,3 +428,141 @@ def test_multi_view_is_view_major_and_independent():
     for v in range(2):
         want = O.image_tokens(P, single, fr["pixels"][v:v + 1])
         assert np.allclose(toks[v * 16:(v + 1) * 16], want, rtol=1e-13)
+
+
+# ------------------------------------------------------------ DiT action head
+
+def test_pixel_shuffle_hand_example_and_vs_torch():
+    # 4x4 grid of one-channel tokens numbered in raster order: coarse token
+    # (i, j) holds fine tokens (2i, 2j), (2i, 2j+1), (2i+1, 2j), (2i+1, 2j+1)
+    x = np.arange(16, dtype=np.float64)[:, None]
+    want = np.array([[0, 1, 4, 5], [2, 3, 6, 7], [8, 9, 12, 13], [10, 11, 14, 15]], dtype=np.float64)
+    assert np.array_equal(O.pixel_shuffle(x, 4, 4, 2), want)
+    assert np.array_equal(O.pixel_shuffle(x, 4, 4, 1), x)
+    # channels fastest: torch's space-to-depth orders channels (c, dy, dx)
+    gh, gw, c, s = 6, 4, 5, 2
+    y = rnd(gh * gw, c)
+    t = F.pixel_unshuffle(t64(y).T.reshape(1, c, gh, gw), s)[0]  # [c s s, gh/s, gw/s]
+    t = t.reshape(c, s * s, gh // s, gw // s).permute(2, 3, 1, 0).reshape(-1, s * s * c)
+    assert np.array_equal(O.pixel_shuffle(y, gh, gw, s), t.numpy())
+
+
+def test_positions_sinusoid_closed_form():
+    pos = O.positions_sinusoid(3, 4)  # w = [1, 10000^-1/2]
+    w1 = 10000.0 ** -0.5
+    want = np.array([[0, 0, 1, 1], [math.sin(1), math.sin(w1), math.cos(1), math.cos(w1)],
+                     [math.sin(2), math.sin(2 * w1), math.cos(2), math.cos(2 * w1)]])
+    assert np.allclose(pos, want, rtol=0, atol=1e-15)
+
+
+def _dit_torch(P, cfg, cross, x, t):
+    """The DiT velocity assembled from torch primitives: LayerNorm without
+    affine, SDPA (multi-head), tanh-GELU, SiLU."""
+    de, nh, H = cfg["ex_dim"], cfg["ex_heads"], x.shape[0]
+    hd = de // nh
+    lin = lambda z, w, b=None: F.linear(z, t64(P[w]), None if b is None else t64(P[b]))
+    ln = lambda z, shift, scale: F.layer_norm(z, (de,), eps=1e-6) * (1 + scale) + shift
+    half = de // 2
+    ang = torch.arange(H, dtype=torch.float64)[:, None] * 10000.0 ** (-torch.arange(half, dtype=torch.float64) / half)
+    X = lin(t64(x), "ex.in.w", "ex.in.b") + torch.cat([ang.sin(), ang.cos()], 1)
+    phi = t64(O.sinusoid(t, 256))[None]
+    c = lin(F.silu(lin(phi, "ex.time1.w", "ex.time1.b")), "ex.time2.w", "ex.time2.b")
+    sc = F.silu(c)
+    heads = lambda z: z.reshape(-1, nh, hd).transpose(0, 1)[None]
+    for l in range(cfg["ex_layers"]):
+        p = f"ex.{l}."
+        sh1, sc1, g1, sh2, sc2, g2 = lin(sc, p + "ada.w", p + "ada.b")[0].reshape(6, de)
+        h = ln(X, sh1, sc1)
+        q = lin(h, p + "q.w")
+        if l % 2 == 0:
+            k, v = (t64(a).reshape(a.shape[0], de) for a in cross[l])
+        else:
+            k, v = lin(h, p + "k.w"), lin(h, p + "v.w")
+        a = F.scaled_dot_product_attention(heads(q), heads(k), heads(v))[0].transpose(0, 1).reshape(H, de)
+        X = X + g1 * lin(a, p + "o.w")
+        X = X + g2 * lin(F.gelu(lin(ln(X, sh2, sc2), p + "fc1.w"), approximate="tanh"), p + "fc2.w")
+    sh, scl = lin(sc, "ex.final.ada.w", "ex.final.ada.b")[0].reshape(2, de)
+    return lin(ln(X, sh, scl), "ex.out.w", "ex.out.b").numpy()
+
+
+def test_dit_velocity_vs_torch_assembly():
+    cfg = dict(synth.micro_dit(), ex_layers=3)  # cross, self, cross
+    P = synth.make_params(cfg, 0)
+    de, nh = cfg["ex_dim"], cfg["ex_heads"]
+    cross = {l: (rnd(9, nh, de // nh), rnd(9, nh, de // nh)) for l in (0, 2)}
+    x, t = rnd(cfg["chunk_len"], cfg["action_dim"]), 0.5
+    got = O.dit_velocity(P, cfg, cross, x, t)
+    with torch.no_grad():
+        ref = _dit_torch(P, cfg, cross, x, t)
+    assert np.allclose(got, ref, rtol=1e-10, atol=1e-10)
+
+
+def _zero_ada(P, cfg, bias_for=None):
+    for l in range(cfg["ex_layers"]):
+        P[f"ex.{l}.ada.w"] = np.zeros_like(P[f"ex.{l}.ada.w"])
+        P[f"ex.{l}.ada.b"] = np.zeros_like(P[f"ex.{l}.ada.b"]) if bias_for is None else bias_for(l)
+    P["ex.final.ada.w"] = np.zeros_like(P["ex.final.ada.w"])
+    P["ex.final.ada.b"] = np.zeros_like(P["ex.final.ada.b"])
+
+
+def test_dit_with_zero_gates_is_embedding_then_final_projection():
+    """All adaLN outputs zero: every gated residual vanishes, so
+    v = W_out LN(W_a x + b_a + pos) + b_out."""
+    cfg = synth.micro_dit()
+    P = synth.make_params(cfg, 0)
+    _zero_ada(P, cfg)
+    x = rnd(cfg["chunk_len"], cfg["action_dim"])
+    cross = {0: (rnd(4, 2, 48), rnd(4, 2, 48))}
+    X0 = x @ P["ex.in.w"].T.astype(np.float64) + P["ex.in.b"] + O.positions_sinusoid(x.shape[0], cfg["ex_dim"])
+    mu = X0.mean(1, keepdims=True)
+    xn = (X0 - mu) / np.sqrt(((X0 - mu) ** 2).mean(1, keepdims=True) + 1e-6)
+    want = xn @ P["ex.out.w"].T.astype(np.float64) + P["ex.out.b"]
+    assert np.allclose(O.dit_velocity(P, cfg, cross, x, 0.5), want, rtol=1e-12, atol=1e-12)
+
+
+def test_dit_cross_attention_to_identical_features():
+    """Identical feature rows make every cross-attention output the common V
+    row (the softmax weights only mix equal rows); with gate1 = 1 and
+    gate2 = 0 the layer adds exactly W_o (W_v f)."""
+    cfg = dict(synth.micro_dit(), ex_layers=1)
+    P = synth.make_params(cfg, 0)
+    de = cfg["ex_dim"]
+    _zero_ada(P, cfg, bias_for=lambda l: np.concatenate([np.zeros(2 * de), np.ones(de), np.zeros(3 * de)]))
+    f = np.tile(rnd(1, cfg["lm_dim"]), (7, 1))
+    cross = O.dit_cross_kv(P, cfg, f)
+    x = rnd(cfg["chunk_len"], cfg["action_dim"])
+    X0 = x @ P["ex.in.w"].T.astype(np.float64) + P["ex.in.b"] + O.positions_sinusoid(x.shape[0], de)
+    vrow = f[0] @ P["ex.0.v.w"].T.astype(np.float64)
+    X1 = X0 + vrow @ P["ex.0.o.w"].T.astype(np.float64)
+    want = O.layer_norm(X1, np.ones(de), np.zeros(de)) @ P["ex.out.w"].T.astype(np.float64) + P["ex.out.b"]
+    assert np.allclose(O.dit_velocity(P, cfg, cross, x, 0.25), want, rtol=1e-10, atol=1e-10)
+
+
+def test_dit_zero_out_projection_gives_noise_minus_bias():
+    cfg = synth.micro_dit()
+    P = synth.make_params(cfg, 0)
+    P["ex.out.w"] = np.zeros_like(P["ex.out.w"])
+    fr = synth.make_frame(cfg, 0, 0)
+    chunk = O.forward(P, cfg, fr)
+    assert np.allclose(chunk, fr["noise"] - P["ex.out.b"], atol=1e-6)
+
+
+def test_dit_phase1_hand_off():
+    """Features are the final RMSNorm of the last LM layer (RMS just below 1
+    before the gain); the hand-off holds the cross K/V of the even DiT layers only, and
+    the shuffled ViT grid gives a quarter of the image tokens."""
+    cfg = dict(synth.micro_dit(), ex_layers=4)
+    P = synth.make_params(cfg, 0)
+    fr = synth.make_frame(cfg, 0, 0)
+    cap = {}
+    out = O.vlm_prefill(P, cfg, fr, cap)
+    d = synth.derived(cfg)
+    assert cap["image_tokens"].shape == (d["n_img"], cfg["lm_dim"]) and d["n_img"] == 4
+    f = cap["features"] / P["lm.final.g"]
+    rms = np.sqrt((f ** 2).mean(1))  # m / (m + eps) with m the row's mean square
+    assert np.all(rms <= 1.0) and np.all(rms > 0.99)
+    assert sorted(out) == [0, 2]
+    for l in (0, 2):
+        assert out[l][0].shape == (d["prefix"], cfg["ex_heads"], cfg["ex_dim"] // cfg["ex_heads"])
+    # the last LM layer now runs in full: the features differ from its input
+    assert len(cap["kv"]) == cfg["lm_layers"]
