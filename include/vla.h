@@ -178,6 +178,11 @@ int vla_export_param(vla_model* m, const char* name, float* host_dst, int64_t nu
  * [prefix, lm_kv_heads * head_dim] each (logical head-dim order). Blocking. */
 int vla_ctx_export_kv(vla_model* m, const vla_ctx* c, int32_t layer, float* host_k, float* host_v);
 
+/* VLA_HEAD_DIT only: copy the cross K and V of even DiT layer `layer` (made
+ * from the LM features in the prefill) to host fp32 buffers of [prefix,
+ * ex_dim] each (head-major columns). Blocking. */
+int vla_ctx_export_cross(vla_model* m, const vla_ctx* c, int32_t layer, float* host_k, float* host_v);
+
 /* Test entry points for single kernels (same kernels and launch planner as
  * the phases). dtype VLA_F32 or VLA_BF16 selects the operand type of A and W
  * (bf16 passed as uint16 bit patterns). All pointers device.
@@ -216,7 +221,8 @@ int vla_debug_attention_cache(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv
  * kernels behind that call site (tags: "vit.patch", "vit.qkv", "vit.attn",
  * "vit.o", "vit.fc1", "vit.fc2", "proj", "state", "lm.qkv", "lm.attn", "lm.o",
  * "lm.gateup", "lm.down", "ex.in", "ex.time1", "ex.time2", "ex.qkv",
- * "ex.attn", "ex.o", "ex.gateup", "ex.down", "ex.out") records a pair of
+ * "ex.attn", "ex.o", "ex.gateup", "ex.down", "ex.out"; DiT head also
+ * "dit.cross_kv", "ex.q", "ex.fc1", "ex.fc2") records a pair of
  * HIP events at the start and end of its main kernel (hipExtLaunchKernel
  * start/stop events, on the launching stream; a separate split-K reduce or
  * attention-combine kernel is not included). NULL or "" turns it off.

@@ -95,6 +95,7 @@ def _load():
         "vla_param_info": [P, I32, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(I64)],
         "vla_export_param": [P, ctypes.c_char_p, P, I64],
         "vla_ctx_export_kv": [P, P, I32, P, P],
+        "vla_ctx_export_cross": [P, P, I32, P, P],
         "vla_debug_gemm": [I32, I32, I32, I32, P, I32, P, I32, P, P, P],
         "vla_debug_attention": [I32, I32, I32, I32, I32, P, P, P, I32, P, P, I32, P, P],
         "vla_debug_generate": [U64, ctypes.c_char_p, I64, D, D, P],
@@ -216,6 +217,13 @@ def vla_ctx_export_kv(model: int, ctx: int, layer: int, n: int) -> Tuple[np.ndar
     return k, v
 
 
+def vla_ctx_export_cross(model: int, ctx: int, layer: int, n: int) -> Tuple[np.ndarray, np.ndarray]:
+    k = np.empty(n, dtype=np.float32)
+    v = np.empty(n, dtype=np.float32)
+    _check(_lib.vla_ctx_export_cross(model, ctx, layer, k.ctypes.data, v.ctypes.data))
+    return k, v
+
+
 def vla_debug_gemm(dtype: int, M: int, N: int, K: int, A, lda: int, W, ldw: int, bias, C,
                    stream: int = 0) -> None:
     _check(_lib.vla_debug_gemm(dtype, M, N, K, _ptr(A), lda, _ptr(W), ldw, _ptr(bias), _ptr(C),
@@ -255,7 +263,7 @@ def exported_symbols() -> Iterable[str]:
     """Names of the C entry points this binding wraps."""
     return ["vla_preset", "vla_validate", "vla_create", "vla_destroy", "vla_ctx_create",
             "vla_ctx_destroy", "vla_vlm_prefill", "vla_action_denoise", "vla_pipeline_run",
-            "vla_param_count", "vla_param_info", "vla_export_param", "vla_ctx_export_kv",
+            "vla_param_count", "vla_param_info", "vla_export_param", "vla_ctx_export_kv", "vla_ctx_export_cross",
             "vla_debug_gemm", "vla_debug_attention", "vla_debug_attention_cache", "vla_debug_generate",
             "vla_kernel_timer",
             "vla_kernel_timer_read", "vla_last_error"]

@@ -19,6 +19,7 @@ enum EpiKind {
   EPI_SWISH,     // out_T[m, n] = T(swish(v + bias[n]))
   EPI_GEGLU,     // gate/up interleaved in 16-row blocks: out_T[m, 16g+j] = T(gelu(gate) * up)
   EPI_QKV_ROPE,  // q/k rotated pairs (rotate-half, permuted rows), v plain; written to q / k / v
+  EPI_QKV_PLAIN, // columns [q (nq*hd) | k (nkv*hd) | v (nkv*hd)] without rotation, any hd
   EPI_EULER,     // x[m, n] += dt * (v + bias[n]); xop[m, n] = T(x[m, n])
   EPI_PART,      // raw fp32 result into out = [splits][M][N] (ldo = its capacity in floats);
                  // the consumer sums the splits in order
@@ -199,14 +200,33 @@ struct AttnKvDesc {
 hipError_t launch_attention_kv(const AttnKvDesc& d, const LaunchCaps& caps, hipStream_t st);
 hipError_t launch_attention(const AttnDesc& a, const Scratch& s, const LaunchCaps& caps, hipStream_t st);
 
-// Residual add + row norm: x[m] += bias + sum_s part[s][m] in split order
-// (part [splits][rows][d]; nothing is added when splits is 0), then
-// out[m] = LayerNorm (biased variance) or RMSNorm of x[m], times g (+ b),
-// in the operand type (row-major with ldo, or the row-block operand layout
-// when afrag, rows <= 64). d <= 2048.
-hipError_t launch_norm(int dtype, float* x, int ldx, int rows, int d, const float* part,
-                       int splits, const float* bias, const float* g, const float* b, bool rms,
-                       void* out, int ldo, bool afrag, hipStream_t st);
+// Residual add + row norm: x[m] += bias + colscale * sum_s part[s][m] (split
+// order; nothing is added when splits is 0, colscale NULL means 1), stored
+// back, then out[m] = LayerNorm (biased variance) or RMSNorm of x[m], times
+// gain (g, or 1 + g when g_plus_one) plus b, in the operand type: row-major
+// with ldo, the row-block operand layout (afrag, rows <= 64), or pixel
+// shuffled (shuffle > 1: row = view * tview + y * grid_w + x of a raster
+// patch grid goes to coarse row view * tview / s^2 + (y / s) * (grid_w / s)
+// + x / s, columns offset by ((y % s) * s + x % s) * d; ldo = s^2 d).
+// d <= 2048.
+struct NormDesc {
+  int dtype = DT_F32;
+  float* x = nullptr;
+  int ldx = 0, rows = 0, d = 0;
+  const float* part = nullptr;
+  int splits = 0;
+  const float* bias = nullptr;
+  const float* colscale = nullptr;
+  const float* g = nullptr;
+  int g_plus_one = 0;
+  const float* b = nullptr;
+  int rms = 0;
+  void* out = nullptr;
+  int ldo = 0;
+  int afrag = 0;
+  int shuffle = 1, grid_w = 0, tview = 0;
+};
+hipError_t launch_norm(const NormDesc& n, hipStream_t st);
 
 // Image [views][H][W][3] fp32 -> patches [views * T][ldo] of the operand type,
 // columns beyond 3 p^2 zero.

@@ -146,6 +146,20 @@ __device__ __forceinline__ void epi_one(const Epi& e, int m, int n, float v) {
       TT<T>::st((T*)e.out + out_at<T>(e, m, n, e.ldo), swishf(v));
       break;
     }
+    case EPI_QKV_PLAIN: {
+      constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
+      const int qcols = e.nq * e.hd, kcols = e.nkv * e.hd;
+      if (n < qcols) {
+        TT<T>::st((T*)e.q + (size_t)m * e.ldq + n, v);
+      } else if (n < qcols + kcols) {
+        const int c = n - qcols;
+        TT<T>::st((T*)e.k + kv_kidx(DT, e.kv_nb, e.hd, c / e.hd, m, c % e.hd), v);
+      } else {
+        const int c = n - qcols - kcols;
+        TT<T>::st((T*)e.v + kv_vidx(DT, e.kv_nb, e.hd, c / e.hd, m, c % e.hd), v);
+      }
+      break;
+    }
     case EPI_EULER: {
       if (e.bias) v += e.bias[n];
       float* xp = e.x + (size_t)m * e.ldx + n;
@@ -1356,37 +1370,37 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return (red[0] + red[1]) + (red[2] + red[3]);
 }
 
-// x[m, :] += bias + sum_s part[s, m, :] (split order; skipped when splits is
-// 0), stored back, then out[m, :] = norm(x[m, :]) * g (+ b). Row values stay
-// in registers (d <= 256 * NORM_NPT).
+// One workgroup per row; row values stay in registers (d <= 256 * NORM_NPT).
 constexpr int NORM_NPT = 8;
 
 template <typename T>
-__global__ __launch_bounds__(256) void k_norm(float* __restrict__ x, int ldx, int rows, int d,
-                                              const float* __restrict__ part, int splits,
-                                              const float* __restrict__ bias,
-                                              const float* __restrict__ g,
-                                              const float* __restrict__ b, int rms, T* out,
-                                              int ldo, int afrag) {
+__global__ __launch_bounds__(256) void k_norm(NormDesc n) {
   constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
   __shared__ float red[4];
+  const int rows = n.rows, d = n.d, ldx = n.ldx, splits = n.splits;
+  float* __restrict__ x = n.x;
   const size_t pstride = (size_t)rows * d;
   const Rsrc rx = rsrc(x, span(rows, ldx, d, 4));
-  const Rsrc rp = rsrc(part ? part : x, part ? (size_t)splits * pstride * 4 : 0);
-  const Rsrc rb = rsrc(bias ? bias : x, bias ? (size_t)d * 4 : 0);
+  const Rsrc rp = rsrc(n.part ? n.part : x, n.part ? (size_t)splits * pstride * 4 : 0);
+  const Rsrc rb = rsrc(n.bias ? n.bias : x, n.bias ? (size_t)d * 4 : 0);
+  const Rsrc rc = rsrc(n.colscale ? n.colscale : x, n.colscale ? (size_t)d * 4 : 0);
   for (int row = blockIdx.x; row < rows; row += gridDim.x) {
     float* xr = x + (size_t)row * ldx;
-    float v[NORM_NPT], add[NORM_NPT];
+    float v[NORM_NPT], add[NORM_NPT], cs[NORM_NPT];
 #pragma unroll
     for (int q = 0; q < NORM_NPT; ++q) {
       const int i = threadIdx.x + q * 256;
       const bool ok = i < d;
       v[q] = bld1(rx, ok ? (uint32_t)(((size_t)row * ldx + i) * 4) : OOB);
-      add[q] = bias ? bld1(rb, ok ? (uint32_t)(i * 4) : OOB) : 0.f;
+      add[q] = n.bias ? bld1(rb, ok ? (uint32_t)(i * 4) : OOB) : 0.f;
+      cs[q] = n.colscale ? bld1(rc, ok ? (uint32_t)(i * 4) : OOB) : 1.f;
     }
     if (splits > 0) {
       // partials in split order; four splits' loads are issued together
       const size_t pbase = (size_t)row * d + threadIdx.x;
+      float sum[NORM_NPT];
+#pragma unroll
+      for (int q = 0; q < NORM_NPT; ++q) sum[q] = 0.f;
       int sp = 0;
       for (; sp + 4 <= splits; sp += 4) {
         float t[4][NORM_NPT];
@@ -1399,13 +1413,15 @@ __global__ __launch_bounds__(256) void k_norm(float* __restrict__ x, int ldx, in
 #pragma unroll
         for (int u = 0; u < 4; ++u)
 #pragma unroll
-          for (int q = 0; q < NORM_NPT; ++q) add[q] += t[u][q];
+          for (int q = 0; q < NORM_NPT; ++q) sum[q] += t[u][q];
       }
       for (; sp < splits; ++sp)
 #pragma unroll
         for (int q = 0; q < NORM_NPT; ++q)
-          add[q] += bld1(rp, threadIdx.x + q * 256 < d
+          sum[q] += bld1(rp, threadIdx.x + q * 256 < d
                                  ? (uint32_t)((pbase + sp * pstride + q * 256) * 4) : OOB);
+#pragma unroll
+      for (int q = 0; q < NORM_NPT; ++q) add[q] += n.colscale ? cs[q] * sum[q] : sum[q];
     }
     float s1 = 0.f;
 #pragma unroll
@@ -1419,7 +1435,7 @@ __global__ __launch_bounds__(256) void k_norm(float* __restrict__ x, int ldx, in
         s1 += v[q];
       }
     }
-    const float mean = rms ? 0.f : block_sum(s1, red) / d;
+    const float mean = n.rms ? 0.f : block_sum(s1, red) / d;
     float s2 = 0.f;
 #pragma unroll
     for (int q = 0; q < NORM_NPT; ++q) {
@@ -1430,29 +1446,36 @@ __global__ __launch_bounds__(256) void k_norm(float* __restrict__ x, int ldx, in
       }
     }
     const float inv = 1.f / sqrtf(block_sum(s2, red) / d + 1e-6f);
+    // output row and column offset (pixel shuffle moves whole rows)
+    size_t obase = (size_t)row * n.ldo;
+    if (n.shuffle > 1) {
+      const int s = n.shuffle, view = row / n.tview, t = row % n.tview;
+      const int y = t / n.grid_w, xx = t % n.grid_w;
+      const int orow = view * (n.tview / (s * s)) + (y / s) * (n.grid_w / s) + xx / s;
+      obase = (size_t)orow * n.ldo + (size_t)((y % s) * s + xx % s) * d;
+    }
 #pragma unroll
     for (int q = 0; q < NORM_NPT; ++q) {
       const int i = threadIdx.x + q * 256;
       if (i < d) {
-        float y = (v[q] - mean) * inv * g[i];
-        if (b) y += b[i];
-        TT<T>::st(out + (afrag ? afrag_index(DT, row, i) : (size_t)row * ldo + i), y);
+        const float gi = n.g_plus_one ? 1.f + n.g[i] : n.g[i];
+        float y = (v[q] - mean) * inv * gi;
+        if (n.b) y += n.b[i];
+        TT<T>::st((T*)n.out + (n.afrag ? afrag_index(DT, row, i) : obase + i), y);
       }
     }
   }
 }
 
-hipError_t launch_norm(int dtype, float* x, int ldx, int rows, int d, const float* part,
-                       int splits, const float* bias, const float* g, const float* b, bool rms,
-                       void* out, int ldo, bool afrag, hipStream_t st) {
-  if (d > 256 * NORM_NPT || (afrag && rows > 64)) return hipErrorInvalidValue;
-  const int grid = std::min(rows, 4096);
-  if (dtype == DT_BF16)
-    k_norm<uint16_t><<<grid, 256, 0, st>>>(x, ldx, rows, d, part, splits, bias, g, b, rms,
-                                           (uint16_t*)out, ldo, afrag);
+hipError_t launch_norm(const NormDesc& n, hipStream_t st) {
+  if (n.d > 256 * NORM_NPT || (n.afrag && n.rows > 64) || !n.x || !n.g || !n.out ||
+      (n.shuffle > 1 && (n.grid_w % n.shuffle || n.tview % (n.shuffle * n.grid_w) || n.afrag)))
+    return hipErrorInvalidValue;
+  const int grid = std::min(n.rows, 4096);
+  if (n.dtype == DT_BF16)
+    k_norm<uint16_t><<<grid, 256, 0, st>>>(n);
   else
-    k_norm<float><<<grid, 256, 0, st>>>(x, ldx, rows, d, part, splits, bias, g, b, rms,
-                                        (float*)out, ldo, afrag);
+    k_norm<float><<<grid, 256, 0, st>>>(n);
   return hipGetLastError();
 }
 

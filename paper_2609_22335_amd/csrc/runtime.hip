@@ -58,6 +58,8 @@ static inline int rnd_up(int x, int m) { return (x + m - 1) / m * m; }
 
 struct Dims {
   int gh, gw, tview, nimg, prefix, kp, kp_pad, a_pad, s_pad, rows_v, kvd, qd, qkv_n, vhd;
+  int kproj;  // projector input width (ViT width times the pixel-shuffle factor squared)
+  int ehd;    // DiT head dim
   int prefix_pad, chunk_pad;  // key lengths rounded up to 32 (KV-cache blocks)
 };
 
@@ -66,13 +68,15 @@ static Dims derive(const vla_config& c) {
   d.gh = c.img_h / c.patch;
   d.gw = c.img_w / c.patch;
   d.tview = d.gh * d.gw;
-  d.nimg = c.n_views * d.tview;
+  d.nimg = c.n_views * d.tview / (c.shuffle * c.shuffle);
   d.prefix = d.nimg + c.n_text + (c.state_dim > 0 ? 1 : 0);
   d.kp = 3 * c.patch * c.patch;
   d.kp_pad = rnd_up(d.kp, 8);
   d.a_pad = rnd_up(c.action_dim, 8);
   d.s_pad = rnd_up(std::max(c.state_dim, 1), 8);
-  d.rows_v = d.nimg;
+  d.rows_v = c.n_views * d.tview;
+  d.kproj = c.vit_dim * c.shuffle * c.shuffle;
+  d.ehd = c.head == VLA_HEAD_DIT ? c.ex_dim / c.ex_heads : c.head_dim;
   d.kvd = c.lm_kv_heads * c.head_dim;
   d.qd = c.lm_heads * c.head_dim;
   d.qkv_n = d.qd + 2 * d.kvd;
@@ -157,6 +161,7 @@ static bool preset(const char* name, vla_config* o) {
 // ---------------------------------------------------------------------------
 
 enum RowMap { MAP_IDENT = 0, MAP_ROPE, MAP_GATE, MAP_UP };
+constexpr int DIT_TIME_DIM = 256;  // width of the DiT's sinusoidal timestep embedding
 
 struct DevTensor {
   size_t offset = 0;  // into the weight arena
@@ -200,6 +205,11 @@ struct VitLayer {
 struct DecLayer {
   int rms1, qkv, o, rms2, gu, down;  // tensor ids (-1 when absent)
 };
+// DiT layer: cross layers (even) have q and kv (row-major, features -> K|V),
+// self layers (odd) a fused q|k|v.
+struct DitLayer {
+  int ada_w = -1, ada_b = -1, q = -1, kv = -1, qkv = -1, o = -1, fc1 = -1, fc2 = -1;
+};
 
 constexpr int MAX_ACT_STREAMS = 4;
 
@@ -224,6 +234,9 @@ struct vla_ctx {
   // blocks per KV head; zeroed at creation, so unwritten padding stays zero
   void* K = nullptr;
   void* V = nullptr;
+  // DiT head: cross K/V of every even DiT layer (same layout, ex_heads heads)
+  void* XK = nullptr;
+  void* XV = nullptr;
 };
 
 struct vla_model {
@@ -244,13 +257,22 @@ struct vla_model {
   int patch_w, patch_b, pos, post_g, post_b, proj_w, proj_b, embed, state_w = -1, state_b = -1;
   std::vector<VitLayer> vit;
   std::vector<DecLayer> lm, ex;
-  int in_w, in_b, t1_w, t1_b, t2_w, t2_b, fin_g, out_w, out_b;
+  int in_w, in_b, t1_w, t1_b, t2_w, t2_b, fin_g = -1, out_w, out_b;
+  // DiT head
+  int lm_fin_g = -1, fada_w = -1, fada_b = -1;
+  std::vector<DitLayer> dit;
 
   // constant tables
   float* rope_cos = nullptr;
   float* rope_sin = nullptr;
   void* phi = nullptr;  // [n_steps][ex_dim] operand type, row-block operand layout
   float* ck = nullptr;  // [n_steps][ex_dim]: W_2 phi(t_k) + b_2
+  // DiT head: adaLN vectors per step, [n_steps][ex_layers][6][ex_dim]
+  // (shift1, scale1, gate1, shift2, scale2, gate2), final [n_steps][2][ex_dim]
+  // (shift, scale), token positions [chunk_len][ex_dim]
+  float* ada = nullptr;
+  float* fada = nullptr;
+  float* dpos = nullptr;
 
   // phase scratch
   struct VlmWs {
@@ -292,11 +314,19 @@ static size_t ctx_layer_k(const vla_model* m) {
 static size_t ctx_layer_v(const vla_model* m) {
   return kv_velems(m->dt, m->d.prefix_pad / 32, m->c.head_dim, m->c.lm_kv_heads);
 }
+static int own_heads(const vla_model* m) {
+  return m->c.head == VLA_HEAD_DIT ? m->c.ex_heads : m->c.lm_kv_heads;
+}
 static size_t own_k(const vla_model* m) {
-  return kv_kelems(m->dt, m->d.chunk_pad / 32, m->c.head_dim, m->c.lm_kv_heads);
+  return kv_kelems(m->dt, m->d.chunk_pad / 32, m->d.ehd, own_heads(m));
 }
 static size_t own_v(const vla_model* m) {
-  return kv_velems(m->dt, m->d.chunk_pad / 32, m->c.head_dim, m->c.lm_kv_heads);
+  return kv_velems(m->dt, m->d.chunk_pad / 32, m->d.ehd, own_heads(m));
+}
+// one even DiT layer's cross K or V (prefix keys, ex_heads heads)
+static size_t cross_elems(const vla_model* m) {
+  return std::max(kv_kelems(m->dt, m->d.prefix_pad / 32, m->d.ehd, m->c.ex_heads),
+                  kv_velems(m->dt, m->d.prefix_pad / 32, m->d.ehd, m->c.ex_heads));
 }
 
 static size_t dsz(int dt) { return dt == DT_BF16 ? 2 : 4; }
@@ -365,7 +395,7 @@ static void build_inventory(vla_model* m) {
   }
   m->post_g = add_vec(m, "vit.post.g", c.vit_dim, 1.0);
   m->post_b = add_vec(m, "vit.post.b", c.vit_dim);
-  m->proj_w = add_mat(m, "proj.w", c.lm_dim, c.vit_dim);
+  m->proj_w = add_mat(m, "proj.w", c.lm_dim, d.kproj);
   m->proj_b = add_vec(m, "proj.b", c.lm_dim);
   m->embed = add_mat(m, "lm.embed", c.vocab, c.lm_dim);
   if (c.state_dim > 0) {
@@ -381,7 +411,7 @@ static void build_inventory(vla_model* m) {
       add_param(m, p + "q.w", d.qd, dim, 0.0, L.qkv, MAP_ROPE, 0, c.head_dim);
       add_param(m, p + "k.w", d.kvd, dim, 0.0, L.qkv, MAP_ROPE, d.qd, c.head_dim);
       add_param(m, p + "v.w", d.kvd, dim, 0.0, L.qkv, MAP_IDENT, d.qd + d.kvd);
-      if (lm && l == layers - 1) {  // the last LM layer only feeds the cache
+      if (lm && l == layers - 1 && c.head == VLA_HEAD_PI0) {  // the last LM layer only feeds the cache
         out.push_back(L);
         break;
       }
@@ -395,6 +425,42 @@ static void build_inventory(vla_model* m) {
     }
   };
   dec("lm.", c.lm_layers, c.lm_dim, c.lm_mlp, true, m->lm);
+  if (c.head == VLA_HEAD_DIT) {
+    const int de = c.ex_dim;
+    m->lm_fin_g = add_vec(m, "lm.final.g", c.lm_dim, 1.0);
+    m->in_w = add_mat(m, "ex.in.w", de, c.action_dim, true);
+    m->in_b = add_vec(m, "ex.in.b", de);
+    m->t1_w = add_mat(m, "ex.time1.w", de, DIT_TIME_DIM, true);
+    m->t1_b = add_vec(m, "ex.time1.b", de);
+    m->t2_w = add_mat(m, "ex.time2.w", de, de, true);
+    m->t2_b = add_vec(m, "ex.time2.b", de);
+    for (int l = 0; l < c.ex_layers; ++l) {
+      const std::string p = "ex." + std::to_string(l) + ".";
+      DitLayer L;
+      L.ada_w = add_mat(m, p + "ada.w", 6 * de, de, true);
+      L.ada_b = add_vec(m, p + "ada.b", 6 * de);
+      if (l % 2 == 0) {  // cross-attention: K / V from the features (M = prefix rows)
+        L.q = add_mat(m, p + "q.w", de, de, true);
+        L.kv = add_tensor(m, 2 * de, rnd_up(c.lm_dim, 8), m->dt);
+        add_param(m, p + "k.w", de, c.lm_dim, 0.0, L.kv, MAP_IDENT, 0);
+        add_param(m, p + "v.w", de, c.lm_dim, 0.0, L.kv, MAP_IDENT, de);
+      } else {
+        L.qkv = add_tensor(m, 3 * de, de, m->dt, false, true);
+        add_param(m, p + "q.w", de, de, 0.0, L.qkv, MAP_IDENT, 0);
+        add_param(m, p + "k.w", de, de, 0.0, L.qkv, MAP_IDENT, de);
+        add_param(m, p + "v.w", de, de, 0.0, L.qkv, MAP_IDENT, 2 * de);
+      }
+      L.o = add_mat(m, p + "o.w", de, de, true);
+      L.fc1 = add_mat(m, p + "fc1.w", c.ex_mlp, de, true);
+      L.fc2 = add_mat(m, p + "fc2.w", de, c.ex_mlp, true);
+      m->dit.push_back(L);
+    }
+    m->fada_w = add_mat(m, "ex.final.ada.w", 2 * de, de, true);
+    m->fada_b = add_vec(m, "ex.final.ada.b", 2 * de);
+    m->out_w = add_mat(m, "ex.out.w", c.action_dim, de, true);
+    m->out_b = add_vec(m, "ex.out.b", c.action_dim);
+    return;
+  }
   m->in_w = add_mat(m, "ex.in.w", c.ex_dim, c.action_dim, true);
   m->in_b = add_vec(m, "ex.in.b", c.ex_dim);
   m->t1_w = add_mat(m, "ex.time1.w", c.ex_dim, 2 * c.ex_dim, true);
@@ -516,15 +582,32 @@ static int attn(const Run& r, const char* tag, const AttnDesc& a) {
 
 // Residual add of `splits` pending partials (from the phase scratch) + bias,
 // then LayerNorm / RMSNorm into `out`.
+static int run_norm(const Run& r, NormDesc n) {
+  n.dtype = r.m->dt;
+  n.part = r.scr->ptr;
+  hipError_t err = launch_norm(n, r.st);
+  if (err != hipSuccess) return fail(VLA_EHIP, std::string("norm: ") + hipGetErrorString(err));
+  return VLA_OK;
+}
+
 // out: row-major [rows][d], or the row-block operand layout when it feeds a
 // skinny GEMM (afrag)
 static int norm(const Run& r, float* x, int rows, int d, int splits, const float* bias, int g, int b,
                 bool rms, void* out, bool afrag = false) {
-  vla_model* m = r.m;
-  hipError_t err = launch_norm(m->dt, x, d, rows, d, r.scr->ptr, splits, bias, m->f32(g),
-                               b >= 0 ? m->f32(b) : nullptr, rms, out, d, afrag, r.st);
-  if (err != hipSuccess) return fail(VLA_EHIP, std::string("norm: ") + hipGetErrorString(err));
-  return VLA_OK;
+  NormDesc n;
+  n.x = x;
+  n.ldx = d;
+  n.rows = rows;
+  n.d = d;
+  n.splits = splits;
+  n.bias = bias;
+  n.g = r.m->f32(g);
+  n.b = b >= 0 ? r.m->f32(b) : nullptr;
+  n.rms = rms;
+  n.out = out;
+  n.ldo = d;
+  n.afrag = afrag;
+  return run_norm(r, n);
 }
 
 // GEMM whose result is added to the residual stream by the next norm: the raw
@@ -658,9 +741,27 @@ static int run_prefill(const Run& r, const vla_frame* f, vla_ctx* ctx) {
     VLA_TRY(gemm_part(r, "vit.fc2", w.mlp, c.vit_mlp, L.fc2_w, rows, dv, c.vit_mlp, &pend));
     pbias = m->f32(L.fc2_b);
   }
-  VLA_TRY(norm(r, w.xv, rows, dv, pend, pbias, m->post_g, m->post_b, false, w.h));
+  {
+    // final LayerNorm; the pixel shuffle (if any) is the norm's output placement
+    NormDesc n;
+    n.x = w.xv;
+    n.ldx = dv;
+    n.rows = rows;
+    n.d = dv;
+    n.splits = pend;
+    n.bias = pbias;
+    n.g = m->f32(m->post_g);
+    n.b = m->f32(m->post_b);
+    n.out = w.h;
+    n.ldo = d.kproj;
+    n.shuffle = c.shuffle;
+    n.grid_w = d.gw;
+    n.tview = d.tview;
+    VLA_TRY(run_norm(r, n));
+  }
   // prefix: [projected image tokens; text * sqrt(d); state projection]
-  VLA_TRY(gemm(r, "proj", w.h, dv, m->proj_w, rows, dl, dv, epi_kind(EPI_F32, w.xl, dl, m->f32(m->proj_b))));
+  VLA_TRY(gemm(r, "proj", w.h, d.kproj, m->proj_w, d.nimg, dl, d.kproj,
+               epi_kind(EPI_F32, w.xl, dl, m->f32(m->proj_b))));
   HIP_TRY(launch_embed(m->dt, m->tptr(m->embed), dl, c.vocab, f->text_ids, c.n_text, std::sqrt((float)dl),
                        w.xl + (size_t)d.nimg * dl, dl, r.st));
   if (c.state_dim > 0) {
@@ -672,17 +773,138 @@ static int run_prefill(const Run& r, const vla_frame* f, vla_ctx* ctx) {
   const size_t layer_k = ctx_layer_k(m) * m->esz;
   const size_t layer_v = ctx_layer_v(m) * m->esz;
   pend = 0;
+  const bool dit = c.head == VLA_HEAD_DIT;
   for (int l = 0; l < c.lm_layers; ++l) {
     void* K = (char*)ctx->K + l * layer_k;
     void* V = (char*)ctx->V + l * layer_v;
     VLA_TRY(decoder_layer(r, true, m->lm[l], w.xl, d.prefix, dl, c.lm_mlp, w.h, w.qkv, K, V, 0, nullptr,
-                          nullptr, 0, w.att, w.mlp, l == c.lm_layers - 1, &pend));
+                          nullptr, 0, w.att, w.mlp, !dit && l == c.lm_layers - 1, &pend));
+  }
+  if (dit) {
+    // features = final RMSNorm of the last layer; then the cross K/V of every
+    // even DiT layer, once per frame
+    VLA_TRY(norm(r, w.xl, d.prefix, dl, pend, nullptr, m->lm_fin_g, -1, true, w.h));
+    const size_t xe = cross_elems(m) * m->esz;
+    for (int l = 0; l < c.ex_layers; l += 2) {
+      Epi e;
+      e.kind = EPI_QKV_PLAIN;
+      e.nq = 0;
+      e.nkv = c.ex_heads;
+      e.hd = d.ehd;
+      e.k = (char*)ctx->XK + (l / 2) * xe;
+      e.v = (char*)ctx->XV + (l / 2) * xe;
+      e.kv_nb = d.prefix_pad / 32;
+      VLA_TRY(gemm(r, "dit.cross_kv", w.h, dl, m->dit[l].kv, d.prefix, 2 * c.ex_dim, dl, e));
+    }
+  }
+  return VLA_OK;
+}
+
+// GR00T-style DiT head (Euler steps as in run_denoise): tokens = W_a x + b_a +
+// positions; per layer, adaLN-modulated LayerNorm (gain 1 + scale, shift
+// from the per-step table) -> attention (even layers: queries over the
+// frame's cross K/V; odd layers: self-attention) -> out-projection whose
+// partial sums the next norm adds with gate1 -> adaLN LayerNorm -> GELU MLP
+// -> down-projection added with gate2 by the next norm; final adaLN +
+// out-projection fused with the Euler update.
+static int run_denoise_dit(const Run& r, const vla_ctx* ctx, const float* noise, float* x) {
+  vla_model* m = r.m;
+  const vla_config& c = m->c;
+  const Dims& d = m->d;
+  ActWs& w = *r.aw;
+  const int H = c.chunk_len, de = c.ex_dim, A = c.action_dim, L = c.ex_layers;
+  const float dt = -1.0f / (float)c.n_steps;
+  const size_t xe = cross_elems(m) * m->esz;
+  HIP_TRY(launch_cvt_pad(m->dt, noise, H, A, w.xop, d.a_pad, true, x, r.st));
+  auto adanorm = [&](int pend, const float* gate, const float* shift, const float* scale) {
+    NormDesc n;
+    n.x = w.u;
+    n.ldx = de;
+    n.rows = H;
+    n.d = de;
+    n.splits = pend;
+    n.colscale = gate;
+    n.g = scale;
+    n.g_plus_one = 1;
+    n.b = shift;
+    n.out = w.h;
+    n.ldo = de;
+    n.afrag = 1;
+    return run_norm(r, n);
+  };
+  for (int k = 0; k < c.n_steps; ++k) {
+    {
+      Epi e = epi_kind(EPI_F32, w.u, de, m->f32(m->in_b));
+      e.rowadd = m->dpos;
+      e.rowadd_period = H;
+      e.ldra = de;
+      VLA_TRY(gemm(r, "ex.in", w.xop, d.a_pad, m->in_w, H, de, d.a_pad, e));
+    }
+    int pend = 0;
+    const float* pgate = nullptr;
+    for (int l = 0; l < L; ++l) {
+      const DitLayer& D = m->dit[l];
+      const float* ad = m->ada + ((size_t)k * L + l) * 6 * de;
+      VLA_TRY(adanorm(pend, pgate, ad, ad + de));
+      AttnKvDesc a{};
+      a.dtype = m->dt;
+      a.q = w.q;
+      a.ldq = de;
+      a.nq = a.nkv = c.ex_heads;
+      a.hd = d.ehd;
+      a.Sq = H;
+      a.out = w.att;
+      a.out_afrag = 1;
+      if (l % 2 == 0) {
+        VLA_TRY(gemm(r, "ex.q", w.h, de, D.q, H, de, de, epi_kind(EPI_T, w.q, de)));
+        a.k0 = (const char*)ctx->XK + (l / 2) * xe;
+        a.v0 = (const char*)ctx->XV + (l / 2) * xe;
+        a.S0 = d.prefix;
+      } else {
+        Epi e;
+        e.kind = EPI_QKV_PLAIN;
+        e.q = w.q;
+        e.ldq = de;
+        e.nq = c.ex_heads;
+        e.nkv = c.ex_heads;
+        e.hd = d.ehd;
+        e.k = w.kown;
+        e.v = w.vown;
+        e.kv_nb = d.chunk_pad / 32;
+        VLA_TRY(gemm(r, "ex.qkv", w.h, de, D.qkv, H, 3 * de, de, e));
+        a.k0 = w.kown;
+        a.v0 = w.vown;
+        a.S0 = H;
+      }
+      VLA_TRY(attn_kv(r, "ex.attn", a));
+      int so = 0;
+      VLA_TRY(gemm_part(r, "ex.o", w.att, de, D.o, H, de, de, &so));
+      VLA_TRY(adanorm(so, ad + 2 * de, ad + 3 * de, ad + 4 * de));
+      Epi e1 = epi_kind(EPI_GELU, w.mlp, c.ex_mlp);
+      e1.afrag = 1;
+      VLA_TRY(gemm(r, "ex.fc1", w.h, de, D.fc1, H, c.ex_mlp, de, e1));
+      VLA_TRY(gemm_part(r, "ex.fc2", w.mlp, c.ex_mlp, D.fc2, H, de, c.ex_mlp, &pend));
+      pgate = ad + 5 * de;
+    }
+    const float* fa = m->fada + (size_t)k * 2 * de;
+    VLA_TRY(adanorm(pend, pgate, fa, fa + de));
+    Epi e;
+    e.kind = EPI_EULER;
+    e.afrag = 1;
+    e.bias = m->f32(m->out_b);
+    e.x = x;
+    e.ldx = A;
+    e.xop = w.xop;
+    e.ldxop = d.a_pad;
+    e.dt = dt;
+    VLA_TRY(gemm(r, "ex.out", w.h, de, m->out_w, H, A, de, e));
   }
   return VLA_OK;
 }
 
 static int run_denoise(const Run& r, const vla_ctx* ctx, const float* noise, float* x) {
   vla_model* m = r.m;
+  if (m->c.head == VLA_HEAD_DIT) return run_denoise_dit(r, ctx, noise, x);
   const vla_config& c = m->c;
   const Dims& d = m->d;
   ActWs& w = *r.aw;
@@ -774,8 +996,10 @@ static int setup_tables(vla_model* m) {
   VLA_TRY(dmalloc(m, (void**)&m->rope_sin, sn.size() * 4));
   HIP_TRY(hipMemcpy(m->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice));
   HIP_TRY(hipMemcpy(m->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice));
-  // sinusoid phi(t_k): periods log-spaced on [4e-3, 4]; t_k = (N - k) / N in fp32
-  const int de = c.ex_dim, dh = de / 2;
+  // sinusoid phi(t_k): periods log-spaced on [4e-3, 4]; t_k = (N - k) / N in
+  // fp32; the DiT's timestep embedder takes a 256-wide phi
+  const bool dit = c.head == VLA_HEAD_DIT;
+  const int de = dit ? DIT_TIME_DIM : c.ex_dim, dh = de / 2;
   std::vector<float> phi((size_t)c.n_steps * de);
   for (int k = 0; k < c.n_steps; ++k) {
     const float t = (float)(c.n_steps - k) / (float)c.n_steps;
@@ -801,7 +1025,46 @@ static int setup_tables(vla_model* m) {
       for (int i = 0; i < de; ++i) hf[afrag_index(m->dt, k, i)] = phi[(size_t)k * de + i];
     HIP_TRY(hipMemcpy(m->phi, hf.data(), hf.size() * 4, hipMemcpyHostToDevice));
   }
-  VLA_TRY(dmalloc(m, (void**)&m->ck, (size_t)c.n_steps * de * 4));
+  if (!dit) {
+    VLA_TRY(dmalloc(m, (void**)&m->ck, (size_t)c.n_steps * de * 4));
+    return VLA_OK;
+  }
+  // DiT: adaLN tables (filled at create) and the fixed token positions,
+  // [sin(p w_i)]_i ++ [cos(p w_i)]_i with w_i = 10000^(-i / (d/2))
+  const int dx = c.ex_dim, hx = dx / 2;
+  VLA_TRY(dmalloc(m, (void**)&m->ada, (size_t)c.n_steps * c.ex_layers * 6 * dx * 4));
+  VLA_TRY(dmalloc(m, (void**)&m->fada, (size_t)c.n_steps * 2 * dx * 4));
+  std::vector<float> pos((size_t)c.chunk_len * dx);
+  for (int p = 0; p < c.chunk_len; ++p)
+    for (int i = 0; i < hx; ++i) {
+      const double ang = p * std::pow(10000.0, -(double)i / hx);
+      pos[(size_t)p * dx + i] = (float)std::sin(ang);
+      pos[(size_t)p * dx + hx + i] = (float)std::cos(ang);
+    }
+  VLA_TRY(dmalloc(m, (void**)&m->dpos, pos.size() * 4));
+  HIP_TRY(hipMemcpy(m->dpos, pos.data(), pos.size() * 4, hipMemcpyHostToDevice));
+  return VLA_OK;
+}
+
+// DiT: adaLN vectors of every step from the timestep embedder,
+// W_l swish(W_t2 swish(W_t1 phi(t_k) + b_t1) + b_t2) + b_l (they depend on
+// the step only), computed once with the library's GEMMs.
+static int setup_dit_tables(vla_model* m) {
+  const vla_config& c = m->c;
+  const int de = c.ex_dim, N = c.n_steps, L = c.ex_layers;
+  ActWs& w = *m->aws[0];
+  Run r{m, nullptr, LaunchCaps{}, &w.scr, &w};
+  Epi e1 = epi_kind(EPI_SWISH, w.a, de, m->f32(m->t1_b));
+  e1.afrag = 1;
+  VLA_TRY(gemm(r, "dit.time1", m->phi, DIT_TIME_DIM, m->t1_w, N, de, DIT_TIME_DIM, e1));
+  Epi e2 = epi_kind(EPI_SWISH, w.hid, de, m->f32(m->t2_b));
+  e2.afrag = 1;
+  VLA_TRY(gemm(r, "dit.time2", w.a, de, m->t2_w, N, de, de, e2));
+  for (int l = 0; l < L; ++l)
+    VLA_TRY(gemm(r, "dit.ada", w.hid, de, m->dit[l].ada_w, N, 6 * de, de,
+                 epi_kind(EPI_F32, m->ada + (size_t)l * 6 * de, L * 6 * de, m->f32(m->dit[l].ada_b))));
+  VLA_TRY(gemm(r, "dit.ada", w.hid, de, m->fada_w, N, 2 * de, de,
+               epi_kind(EPI_F32, m->fada, 2 * de, m->f32(m->fada_b))));
   return VLA_OK;
 }
 
@@ -824,14 +1087,29 @@ static int add_act_lane(vla_model* m) {
   VLA_TRY(dmalloc(m, &a.a, afrag_elems(dt, de) * e));
   VLA_TRY(dmalloc(m, &a.hid, afrag_elems(dt, de) * e));
   VLA_TRY(dmalloc(m, &a.h, afrag_elems(dt, de) * e));
-  VLA_TRY(dmalloc(m, &a.q, (size_t)H * d.qd * e));
+  const int qw = std::max(d.qd, de);  // query width (LM heads, or the DiT's)
+  VLA_TRY(dmalloc(m, &a.q, (size_t)H * qw * e));
   VLA_TRY(dmalloc(m, &a.kown, own_k(m) * e));
   VLA_TRY(dmalloc(m, &a.vown, own_v(m) * e));
   HIP_TRY(hipMemset(a.kown, 0, own_k(m) * e));  // padding stays zero
   HIP_TRY(hipMemset(a.vown, 0, own_v(m) * e));
-  VLA_TRY(dmalloc(m, &a.att, afrag_elems(dt, d.qd) * e));
+  VLA_TRY(dmalloc(m, &a.att, afrag_elems(dt, qw) * e));
   VLA_TRY(dmalloc(m, &a.mlp, afrag_elems(dt, c.ex_mlp) * e));
   ScratchNeed sa;
+  if (c.head == VLA_HEAD_DIT) {
+    const int N = c.n_steps;
+    upd(sa, gemm_scratch(dt, H, de, d.a_pad, false, true));
+    upd(sa, gemm_scratch(dt, N, de, DIT_TIME_DIM, false, true));
+    upd(sa, gemm_scratch(dt, N, de, de, false, true));
+    upd(sa, gemm_scratch(dt, N, 6 * de, de, false, true));
+    upd(sa, gemm_scratch(dt, N, 2 * de, de, false, true));
+    upd(sa, gemm_scratch(dt, H, de, de, false, true));
+    upd(sa, gemm_scratch(dt, H, 3 * de, de, false, true));
+    upd(sa, gemm_scratch(dt, H, de, de, true, true));
+    upd(sa, gemm_scratch(dt, H, c.ex_mlp, de, false, true));
+    upd(sa, gemm_scratch(dt, H, de, c.ex_mlp, true, true));
+    upd(sa, gemm_scratch(dt, H, c.action_dim, de, false, true));
+  }
   upd(sa, gemm_scratch(dt, H, de, d.a_pad, false, true));
   upd(sa, gemm_scratch(dt, H, de, de, false, true));
   upd(sa, gemm_scratch(dt, c.n_steps, de, de, false, true));
@@ -871,7 +1149,8 @@ static int setup_workspaces(vla_model* m) {
   upd(sv, gemm_scratch(dt, rv, dv, dv, true));
   upd(sv, gemm_scratch(dt, rv, c.vit_mlp, dv));
   upd(sv, gemm_scratch(dt, rv, dv, c.vit_mlp, true));
-  upd(sv, gemm_scratch(dt, rv, dl, dv));
+  upd(sv, gemm_scratch(dt, d.nimg, dl, d.kproj));
+  if (c.head == VLA_HEAD_DIT) upd(sv, gemm_scratch(dt, P, 2 * c.ex_dim, dl));
   upd(sv, gemm_scratch(dt, 1, dl, d.s_pad));
   upd(sv, gemm_scratch(dt, P, d.qkv_n, dl));
   upd(sv, gemm_scratch(dt, P, dl, d.qd, true));
@@ -890,7 +1169,6 @@ static int setup_workspaces(vla_model* m) {
 
 static int create_impl(const vla_config* cfg, uint64_t seed, vla_model** out) {
   VLA_TRY(validate(cfg));
-  if (cfg->head == VLA_HEAD_DIT) return fail(VLA_EUNSUPPORTED, "the DiT head is not built yet");
   std::unique_ptr<vla_model> m(new vla_model());
   m->c = *cfg;
   m->d = derive(*cfg);
@@ -921,7 +1199,9 @@ static int create_impl(const vla_config* cfg, uint64_t seed, vla_model** out) {
   }
   int rc = setup_tables(m.get());
   if (rc == VLA_OK) rc = setup_workspaces(m.get());
-  if (rc == VLA_OK) {
+  if (rc == VLA_OK && m->c.head == VLA_HEAD_DIT) {
+    rc = setup_dit_tables(m.get());
+  } else if (rc == VLA_OK) {
     // c_k = W_2[:, d_e:] phi(t_k) + b_2 for every step (depends on the step only)
     Run r{m.get(), nullptr, LaunchCaps{}, &m->aws[0]->scr, m->aws[0].get()};
     const int de = m->c.ex_dim;
@@ -958,10 +1238,19 @@ static int ctx_create_impl(vla_model* m, vla_ctx** out) {
   }
   e = hipMalloc(&c->V, vbytes);
   if (e == hipSuccess) e = hipMemset(c->V, 0, vbytes);
+  if (e == hipSuccess && m->c.head == VLA_HEAD_DIT) {
+    const size_t xbytes = (size_t)((m->c.ex_layers + 1) / 2) * cross_elems(m) * m->esz;
+    e = hipMalloc(&c->XK, xbytes);
+    if (e == hipSuccess) e = hipMemset(c->XK, 0, xbytes);
+    if (e == hipSuccess) e = hipMalloc(&c->XV, xbytes);
+    if (e == hipSuccess) e = hipMemset(c->XV, 0, xbytes);
+  }
   if (e != hipSuccess) {
     hipFree(c->K);
     hipFree(c->V);
-    return fail(VLA_ENOMEM, "ctx V: allocation failed");
+    hipFree(c->XK);
+    hipFree(c->XV);
+    return fail(VLA_ENOMEM, "ctx V / cross K/V: allocation failed");
   }
   *out = c.release();
   return VLA_OK;
@@ -1182,6 +1471,8 @@ int vla_destroy(vla_model* m) {
     for (vla_ctx* cx : m->pctx) {
       hipFree(cx->K);
       hipFree(cx->V);
+      hipFree(cx->XK);
+      hipFree(cx->XV);
       delete cx;
     }
     auto drop = [](Streams& st) {
@@ -1213,6 +1504,8 @@ int vla_ctx_destroy(vla_ctx* c) {
     if (!c) return VLA_OK;
     hipFree(c->K);
     hipFree(c->V);
+    hipFree(c->XK);
+    hipFree(c->XV);
     delete c;
     return VLA_OK;
   })
@@ -1306,6 +1599,31 @@ int vla_ctx_export_kv(vla_model* m, const vla_ctx* c, int32_t layer, float* host
         for (int dd = 0; dd < hd; ++dd) {
           host_k[(size_t)p * kvd + j * hd + dd] = val(kimg, kv_kidx(m->dt, nb, hd, j, p, dd));
           host_v[(size_t)p * kvd + j * hd + dd] = val(vimg, kv_vidx(m->dt, nb, hd, j, p, dd));
+        }
+    return VLA_OK;
+  })
+}
+
+int vla_ctx_export_cross(vla_model* m, const vla_ctx* c, int32_t layer, float* host_k, float* host_v) {
+  ABI_GUARD({
+    if (!m || !c || !host_k || !host_v) return fail(VLA_EINVAL, "NULL argument");
+    if (c->m != m) return fail(VLA_ESTATE, "context belongs to another model");
+    if (m->c.head != VLA_HEAD_DIT) return fail(VLA_EINVAL, "the model has no DiT head");
+    if (layer < 0 || layer >= m->c.ex_layers || layer % 2) return fail(VLA_EINVAL, "layer must be an even DiT layer");
+    const int P = m->d.prefix, nb = m->d.prefix_pad / 32, hd = m->d.ehd, nh = m->c.ex_heads;
+    const size_t n = cross_elems(m);
+    std::vector<uint8_t> kimg(n * m->esz), vimg(n * m->esz);
+    const size_t off = (size_t)(layer / 2) * n * m->esz;
+    HIP_TRY(hipMemcpy(kimg.data(), (const char*)c->XK + off, kimg.size(), hipMemcpyDeviceToHost));
+    HIP_TRY(hipMemcpy(vimg.data(), (const char*)c->XV + off, vimg.size(), hipMemcpyDeviceToHost));
+    auto val = [&](const std::vector<uint8_t>& img, size_t i) {
+      return m->dt == DT_BF16 ? bf16_value(((const uint16_t*)img.data())[i]) : ((const float*)img.data())[i];
+    };
+    for (int p = 0; p < P; ++p)
+      for (int j = 0; j < nh; ++j)
+        for (int dd = 0; dd < hd; ++dd) {
+          host_k[(size_t)p * nh * hd + j * hd + dd] = val(kimg, kv_kidx(m->dt, nb, hd, j, p, dd));
+          host_v[(size_t)p * nh * hd + j * hd + dd] = val(vimg, kv_vidx(m->dt, nb, hd, j, p, dd));
         }
     return VLA_OK;
   })

@@ -72,8 +72,10 @@ def context(m):
         V.vla_ctx_destroy(c)
 
 
-def run_frame(m, cfg, fr, stream=0):
-    """Prefill + denoise of one frame on one stream; returns (chunk, ctx-kv list)."""
+def run_frame(m, cfg, fr, stream=0, cross=None):
+    """Prefill + denoise of one frame on one stream; returns (chunk, ctx-kv
+    list). For a DiT head, ``cross`` (a dict) receives the cross K/V of every
+    even DiT layer."""
     d = synth.derived(cfg)
     df = DevFrame(fr)
     out = torch.empty_like(df.noise)
@@ -83,4 +85,7 @@ def run_frame(m, cfg, fr, stream=0):
         torch.cuda.synchronize()
         n = d["prefix"] * cfg["lm_kv_heads"] * cfg["head_dim"]
         kv = [V.vla_ctx_export_kv(m, c, l, n) for l in range(cfg["lm_layers"])]
+        if cross is not None and cfg.get("head", 0) == synth.HEAD_DIT:
+            for l in range(0, cfg["ex_layers"], 2):
+                cross[l] = V.vla_ctx_export_cross(m, c, l, d["prefix"] * cfg["ex_dim"])
     return out.cpu().numpy().astype(np.float64), kv

@@ -249,7 +249,49 @@ def test_pi0_full_size_vs_oracle(V):
     assert err <= CHUNK_TOL[synth.BF16]
 
 
-@pytest.mark.parametrize("cfg", [synth.micro(synth.BF16), synth.TINY], ids=["micro-bf16", "tiny"])
+DIT_CFGS = [
+    ("micro-dit-f32", synth.micro_dit(synth.F32)),
+    ("micro-dit-bf16", synth.micro_dit(synth.BF16)),
+    ("micro-dit-2view", dict(synth.micro_dit(synth.F32), n_views=2, ex_layers=3)),
+    ("tiny-dit", synth.TINY_DIT),
+    ("tiny-dit-bf16", dict(synth.TINY_DIT, dtype=synth.BF16)),
+]
+
+
+@pytest.mark.parametrize("name,cfg", DIT_CFGS, ids=[p[0] for p in DIT_CFGS])
+def test_dit_phases_vs_oracle(V, name, cfg):
+    """GR00T-style head: LM cache and the DiT's cross K/V (phase 1) and the
+    chunk (phase 2) against the oracle."""
+    g = G()
+    g.say(f"dit phases {name}")
+    P = synth.make_params(cfg, 0)
+    fr = synth.make_frame(cfg, 0, 0)
+    cap = {}
+    want = O.forward(P, cfg, fr, cap)
+    with g.model(cfg, 0) as m:
+        cross = {}
+        got, kv = g.run_frame(m, cfg, fr, cross=cross)
+        got2, _ = g.run_frame(m, cfg, fr)
+    assert np.array_equal(got, got2), "not deterministic"
+    nkvd = cfg["lm_kv_heads"] * cfg["head_dim"]
+    for l, (k, v) in enumerate(kv):
+        rk = cap["kv"][l][0].reshape(-1, nkvd).ravel()
+        rv = cap["kv"][l][1].reshape(-1, nkvd).ravel()
+        assert np.all(np.abs(k - rk) <= _kv_tol(cfg, rk)), ("lm", l, float(np.abs(k - rk).max()))
+        assert np.all(np.abs(v - rv) <= _kv_tol(cfg, rv)), ("lm", l, float(np.abs(v - rv).max()))
+    assert sorted(cross) == sorted(cap["cross_kv"])
+    for l, (k, v) in cross.items():
+        rk = cap["cross_kv"][l][0].ravel()
+        rv = cap["cross_kv"][l][1].ravel()
+        assert np.all(np.abs(k - rk) <= _kv_tol(cfg, rk)), ("cross", l, float(np.abs(k - rk).max()))
+        assert np.all(np.abs(v - rv) <= _kv_tol(cfg, rv)), ("cross", l, float(np.abs(v - rv).max()))
+    err = float(np.abs(got - want).max())
+    print(f"[gpu] {name}: chunk max abs err {err:.3e}", flush=True)
+    assert err <= CHUNK_TOL[cfg["dtype"]]
+
+
+@pytest.mark.parametrize("cfg", [synth.micro(synth.BF16), synth.TINY, synth.micro_dit(synth.BF16)],
+                         ids=["micro-bf16", "tiny", "micro-dit-bf16"])
 def test_pipeline_modes_bit_identical(V, cfg):
     """Every schedule (one stream, two streams, CU masks, workgroup caps,
     several action streams, graph replay) gives the same bits as standalone
