@@ -10,6 +10,10 @@ stream). One step = vla_pipeline_run over the R frames: the VLM prefill of
 frame r+1 overlaps the action denoising of frame r. Inputs are resident in
 HBM before the timed region.
 
+Further workloads of the same pipeline (``--extra``; by default the
+GR00T-shaped VLA with its DiT action head, R=8) are measured the same way
+and reported under ``other_workloads``; the headline stays the one above.
+
 Prints one JSON line: frames/s of the fastest schedule as `value` (named in
 config.schedule),
 actions/s, every schedule's throughput and its speedup over the serialized
@@ -97,6 +101,9 @@ def main():
     ap.add_argument("--kernel", default="ex.gateup", help="tag of the kernel timed for the roofline")
     ap.add_argument("--preset", default="pi0")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--extra", default="gr00t:8:serial,concurrent,cu_masked,lanes2_graph,lanes3_graph",
+                    help="further workloads, ';'-separated preset:R:schedule,schedule,...")
+    ap.add_argument("--extra-steps", type=int, default=5)
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -120,18 +127,6 @@ def main():
         modes.append(args.mode)
     vlm_cus, act_cus = (int(x) for x in args.split.split(","))
 
-    print(f"[bench] creating {args.preset} model (seed {seed})", file=sys.stderr, flush=True)
-    m = V.vla_create(cfg, seed)
-    frames_np = [synth.make_frame(cfg, seed, r) for r in range(R)]
-    dev = []
-    for f in frames_np:
-        pix = torch.from_numpy(f["pixels"]).cuda()
-        ids = torch.from_numpy(f["ids"]).cuda()
-        st = torch.from_numpy(f["state"]).cuda() if f["state"].size else None
-        dev.append((pix, ids, st))
-    cframes = [V.make_frame(p, i, s) for p, i, s in dev]
-    noise = torch.from_numpy(np.stack([f["noise"] for f in frames_np])).cuda().contiguous()
-    actions = torch.empty_like(noise)
     # schedules: the paper's serialized and naive two-stream ones, the two
     # MI355X levers (CU masks, workgroup caps), graph replay, and several
     # action streams for the independent robots' action phases
@@ -144,31 +139,55 @@ def main():
           "lanes2_graph": dict(mode="concurrent", act_streams=2, graphs=True),
           "lanes3_graph": dict(mode="concurrent", act_streams=3, graphs=True),
           "lanes4_graph": dict(mode="concurrent", act_streams=4, graphs=True)}
+    for a_, b_ in ((224, 32), (192, 64), (160, 96)):  # CU-split sweep entries
+        kw[f"cu_{a_}_{b_}"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_)
+        kw[f"cu_{a_}_{b_}_lanes3"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_, act_streams=3, graphs=True)
+    for c_ in (1, 2, 4):
+        kw[f"wg_cap{c_}"] = dict(mode="wg_capped", vlm_wg_cap=c_)
 
-    results, outputs = {}, {}
-    for mode in modes:
-        print(f"[bench] mode {mode}: {args.warmup} warmup + {args.steps} timed steps of R={R}",
-              file=sys.stderr, flush=True)
-        for _ in range(args.warmup):
-            V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **kw[mode])
-        torch.cuda.synchronize()
-        lib_ms = []
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            t = V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **kw[mode])
-            lib_ms.append(t["wall_ms"])
-        torch.cuda.synchronize()
-        el = time.perf_counter() - t0
-        fps = args.steps * R / el
-        results[mode] = {"frames_per_s": fps, "actions_per_s": fps * cfg["chunk_len"],
-                         "ms_per_step": 1e3 * el / args.steps,
-                         "median_step_ms": float(np.median(lib_ms)), "min_step_ms": float(np.min(lib_ms)),
-                         "vlm_ms_per_frame": t["vlm_ms"] / R, "action_ms_per_frame": t["act_ms"] / R}
-        outputs[mode] = actions.cpu().numpy().copy()
-    ser = results.get("serial", {}).get("frames_per_s")
-    for mode in results:
-        results[mode]["speedup_vs_serialized"] = (results[mode]["frames_per_s"] / ser) if ser else None
-    identical = all(np.array_equal(outputs[m0], outputs[modes[0]]) for m0 in outputs)
+    def measure(preset, R, modes, steps, warmup):
+        """vla_pipeline_run over R seeded frames of `preset` in each schedule."""
+        cfg = V.vla_preset(preset)
+        print(f"[bench] creating {preset} model (seed {seed})", file=sys.stderr, flush=True)
+        m = V.vla_create(cfg, seed)
+        frames_np = [synth.make_frame(cfg, seed, r) for r in range(R)]
+        dev = []
+        for f in frames_np:
+            pix = torch.from_numpy(f["pixels"]).cuda()
+            ids = torch.from_numpy(f["ids"]).cuda()
+            st = torch.from_numpy(f["state"]).cuda() if f["state"].size else None
+            dev.append((pix, ids, st))
+        cframes = [V.make_frame(p, i, s) for p, i, s in dev]
+        noise = torch.from_numpy(np.stack([f["noise"] for f in frames_np])).cuda().contiguous()
+        actions = torch.empty_like(noise)
+        results, outputs = {}, {}
+        for mode in modes:
+            print(f"[bench] {preset} mode {mode}: {warmup} warmup + {steps} timed steps of R={R}",
+                  file=sys.stderr, flush=True)
+            for _ in range(warmup):
+                V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **kw[mode])
+            torch.cuda.synchronize()
+            lib_ms = []
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                t = V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **kw[mode])
+                lib_ms.append(t["wall_ms"])
+            torch.cuda.synchronize()
+            el = time.perf_counter() - t0
+            fps = steps * R / el
+            results[mode] = {"frames_per_s": fps, "actions_per_s": fps * cfg["chunk_len"],
+                             "ms_per_step": 1e3 * el / steps,
+                             "median_step_ms": float(np.median(lib_ms)), "min_step_ms": float(np.min(lib_ms)),
+                             "vlm_ms_per_frame": t["vlm_ms"] / R, "action_ms_per_frame": t["act_ms"] / R}
+            outputs[mode] = actions.cpu().numpy().copy()
+        ser = results.get("serial", {}).get("frames_per_s")
+        for mode in results:
+            results[mode]["speedup_vs_serialized"] = (results[mode]["frames_per_s"] / ser) if ser else None
+        identical = all(np.array_equal(outputs[m0], outputs[modes[0]]) for m0 in outputs)
+        return cfg, m, results, outputs, identical, (cframes, noise, actions)
+
+    cfg, m, results, outputs, identical, (cframes, noise, actions) = measure(
+        args.preset, R, modes, args.steps, args.warmup)
     if args.mode == "auto":
         args.mode = max(results, key=lambda k: results[k]["frames_per_s"])
 
@@ -192,6 +211,24 @@ def main():
                 "algorithmic_bytes": byts, "flops": flops}
     outs = outputs[args.mode]
     V.vla_destroy(m)
+    del cframes, noise, actions
+
+    # further workloads of the same pipeline: preset:R:schedules (a short
+    # summary each; the first config above is the headline)
+    others = {}
+    for spec in [x for x in args.extra.split(";") if x]:
+        preset, r_, sched = spec.split(":")
+        ms_ = sched.split(",")
+        ocfg, om, ores, _, oid, _ = measure(preset, int(r_), ms_, args.extra_steps, 1)
+        V.vla_destroy(om)
+        best = max(ores, key=lambda k: ores[k]["frames_per_s"])
+        others[f"{preset}_R{r_}"] = {
+            "workload": f"{preset}, R={r_} robot request streams", "best_schedule": best,
+            "frames_per_s": ores[best]["frames_per_s"], "actions_per_s": ores[best]["actions_per_s"],
+            "speedup_vs_serialized": ores[best]["speedup_vs_serialized"],
+            "chunk": [ocfg["chunk_len"], ocfg["action_dim"]], "euler_steps": ocfg["n_steps"],
+            "prefix_tokens": synth.derived(ocfg)["prefix"], "steps": args.extra_steps,
+            "outputs_identical_across_modes": oid, "modes": ores}
 
     main_r = results[args.mode]
     line = {
@@ -210,6 +247,8 @@ def main():
         "modes": results, "outputs_identical_across_modes": identical,
         "roofline": roofline,
     }
+    if others:
+        line["other_workloads"] = others
     if not args.no_cpu_baseline:
         cb, chunk = cpu_baseline(cfg, seed)
         cb["max_abs_err_gpu_vs_oracle_frame0"] = float(np.abs(outs[0].astype(np.float64) - chunk).max())
