@@ -270,10 +270,19 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
   const Rsrc ra_r = rsrc(A, span(M, lda, K, sizeof(T)));
   const Rsrc rb_r = rsrc(W, span(N, ldw, K, sizeof(T)));
 
-  for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-    const int s = tile % splits;
-    const int t2 = tile / splits;
-    const int tm = t2 % tiles_m, tn = t2 / tiles_m;
+  // Workgroups are dispatched round-robin over the 8 XCDs (workgroup b on
+  // XCD b % 8), each with its own L2. Giving every XCD a contiguous range of
+  // tiles keeps the row tiles that share a weight block (consecutive tile
+  // indices) on one XCD, so the block comes from HBM once. Any bijection of
+  // the workgroup index gives the same results.
+  const int G = gridDim.x;
+  const int first = G % 8 == 0 ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
+  for (int tile = first; tile < ntiles; tile += G) {
+    // row tile fastest, then column tile, then K split: an XCD's range holds
+    // whole column blocks (each weight block read once) of few K splits
+    // (so it reads only those K ranges of A)
+    const int tm = tile % tiles_m, t2 = tile / tiles_m;
+    const int tn = t2 % tiles_n, s = t2 / tiles_n;
     const int m0 = tm * BM, n0 = tn * BN;
     const int kbeg = s * kchunk, kend = min(K, kbeg + kchunk);
     const int nk = (kend - kbeg + BK - 1) / BK;
