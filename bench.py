@@ -151,7 +151,10 @@ def main():
           "cu_masked_graph": dict(mode="cu_masked", vlm_cus=vlm_cus, act_cus=act_cus, graphs=True),
           "lanes2_graph": dict(mode="concurrent", act_streams=2, graphs=True),
           "lanes3_graph": dict(mode="concurrent", act_streams=3, graphs=True),
-          "lanes4_graph": dict(mode="concurrent", act_streams=4, graphs=True)}
+          "lanes4_graph": dict(mode="concurrent", act_streams=4, graphs=True),
+          "v2_lanes2_graph": dict(mode="concurrent", vlm_streams=2, act_streams=2, graphs=True),
+          "v2_lanes3_graph": dict(mode="concurrent", vlm_streams=2, act_streams=3, graphs=True),
+          "v2_lanes4_graph": dict(mode="concurrent", vlm_streams=2, act_streams=4, graphs=True)}
     for a_, b_ in ((224, 32), (192, 64), (160, 96)):  # CU-split sweep entries
         kw[f"cu_{a_}_{b_}"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_)
         kw[f"cu_{a_}_{b_}_lanes3"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_, act_streams=3, graphs=True)

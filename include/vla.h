@@ -100,8 +100,11 @@ typedef struct vla_sched {
                       /*   action phases of k consecutive frames (different robots)  */
                       /*   run concurrently on k streams; not with VLA_MODE_SERIAL   */
   int32_t graphs;     /* 1: replay each phase as a captured HIP graph (captured on   */
-                      /*   first use and cached per context / action stream)         */
-  int32_t reserved[2];
+                      /*   first use and cached per context / stream)                */
+  int32_t vlm_streams;/* VLM streams (0 or 1: one; at most 2). With 2, the prefills  */
+                      /*   of consecutive frames alternate between two streams and   */
+                      /*   may overlap each other; not with VLA_MODE_SERIAL          */
+  int32_t reserved;
 } vla_sched;
 
 typedef struct vla_timing {

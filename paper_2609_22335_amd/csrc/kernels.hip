@@ -230,10 +230,14 @@ __device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int 
 // visited grid-stride so a capped grid computes the same tiles.
 // ---------------------------------------------------------------------------
 
+#ifndef VLA_GEMM_LDS_PAD
+#define VLA_GEMM_LDS_PAD 2  // LDS row padding of the GEMM tiles, in 16-byte units (32 B: fewest bank conflicts measured)
+#endif
+
 template <typename T, int BM, int BN, int BK, int WGM>
 struct GemmSmem {
   static constexpr int VEC = 16 / sizeof(T);
-  static constexpr int LDS = BK + VEC;
+  static constexpr int LDS = BK + VEC * VLA_GEMM_LDS_PAD;
   static constexpr int CLD = BN + 4;
   union {
     struct {

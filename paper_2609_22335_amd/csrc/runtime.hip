@@ -213,9 +213,22 @@ struct DitLayer {
 
 constexpr int MAX_ACT_STREAMS = 4;
 
+constexpr int MAX_VLM_STREAMS = 2;
+
 struct Streams {
-  hipStream_t v = nullptr;
+  hipStream_t v[MAX_VLM_STREAMS] = {};
   hipStream_t a[MAX_ACT_STREAMS] = {};
+};
+
+// Scratch of one VLM lane (one prefill at a time per lane), with staging for
+// graph replays.
+struct VlmWs {
+  float *xv = nullptr, *xl = nullptr;
+  void *h = nullptr, *qkv = nullptr, *att = nullptr, *mlp = nullptr, *sbuf = nullptr;
+  Scratch scr;
+  float* pstage = nullptr;
+  int32_t* istage = nullptr;
+  float* sstage = nullptr;
 };
 
 // Scratch of one action lane (one denoise at a time per lane).
@@ -275,11 +288,7 @@ struct vla_model {
   float* dpos = nullptr;
 
   // phase scratch
-  struct VlmWs {
-    float *xv, *xl;
-    void *h, *qkv, *att, *mlp, *sbuf;
-    Scratch scr;
-  } vw{};
+  std::vector<std::unique_ptr<VlmWs>> vws;  // VLM lanes; lane 0 serves standalone calls
   std::vector<std::unique_ptr<ActWs>> aws;  // action lanes; lane 0 serves standalone calls
   std::vector<void*> allocs;
 
@@ -290,10 +299,7 @@ struct vla_model {
   std::vector<hipEvent_t> ev;
   // graph replay: frame inputs staged into fixed buffers, graphs cached per
   // (context, VLM grid cap) and (action lane, context)
-  float* pstage = nullptr;
-  int32_t* istage = nullptr;
-  float* sstage = nullptr;
-  std::map<std::pair<int, int>, hipGraphExec_t> pre_graphs;
+  std::map<std::tuple<int, int, int>, hipGraphExec_t> pre_graphs;  // (VLM lane, context, WG cap)
   std::map<std::pair<int, int>, hipGraphExec_t> den_graphs;
   std::mutex mu;
 
@@ -519,6 +525,7 @@ struct Run {
   LaunchCaps caps;
   const Scratch* scr;
   ActWs* aw = nullptr;  // action phase only
+  VlmWs* vw = nullptr;  // VLM phase only
 };
 
 // Kernel timer: a launch whose tag matches gets a pair of events that its
@@ -700,7 +707,7 @@ static int run_prefill(const Run& r, const vla_frame* f, vla_ctx* ctx) {
   vla_model* m = r.m;
   const vla_config& c = m->c;
   const Dims& d = m->d;
-  auto& w = m->vw;
+  VlmWs& w = *r.vw;
   const int dv = c.vit_dim, dl = c.lm_dim, rows = d.rows_v;
   // ViT: patch embedding + bias + position
   HIP_TRY(launch_patchify(m->dt, f->pixels, c.n_views, c.img_h, c.img_w, c.patch, w.h, d.kp_pad, r.st));
@@ -1126,14 +1133,15 @@ static int add_act_lane(vla_model* m) {
   return VLA_OK;
 }
 
-static int setup_workspaces(vla_model* m) {
+static int add_vlm_lane(vla_model* m) {
   const vla_config& c = m->c;
   const Dims& d = m->d;
   const int dt = m->dt;
   const size_t e = m->esz;
-  const int rv = d.rows_v, P = d.prefix, H = c.chunk_len;
-  const int dv = c.vit_dim, dl = c.lm_dim, de = c.ex_dim;
-  auto& v = m->vw;
+  const int rv = d.rows_v, P = d.prefix;
+  const int dv = c.vit_dim, dl = c.lm_dim;
+  std::unique_ptr<VlmWs> lane(new VlmWs());
+  VlmWs& v = *lane;
   const int rmax = std::max(rv, P);
   VLA_TRY(dmalloc(m, (void**)&v.xv, (size_t)rv * dv * 4));
   VLA_TRY(dmalloc(m, (void**)&v.xl, (size_t)P * dl * 4));
@@ -1159,10 +1167,15 @@ static int setup_workspaces(vla_model* m) {
   upd(sv, attn_scratch(dt, d.tview, c.vit_heads, c.vit_heads, d.vhd, d.tview, 0, c.n_views));
   upd(sv, attn_scratch(dt, P, c.lm_heads, c.lm_kv_heads, c.head_dim, P, 0, 1));
   VLA_TRY(alloc_scratch(m, sv, &v.scr));
+  VLA_TRY(dmalloc(m, (void**)&v.pstage, (size_t)c.n_views * c.img_h * c.img_w * 3 * 4));
+  VLA_TRY(dmalloc(m, (void**)&v.istage, (size_t)std::max(c.n_text, 1) * 4));
+  VLA_TRY(dmalloc(m, (void**)&v.sstage, (size_t)std::max(c.state_dim, 1) * 4));
+  m->vws.push_back(std::move(lane));
+  return VLA_OK;
+}
 
-  VLA_TRY(dmalloc(m, (void**)&m->pstage, (size_t)c.n_views * c.img_h * c.img_w * 3 * 4));
-  VLA_TRY(dmalloc(m, (void**)&m->istage, (size_t)std::max(c.n_text, 1) * 4));
-  VLA_TRY(dmalloc(m, (void**)&m->sstage, (size_t)std::max(c.state_dim, 1) * 4));
+static int setup_workspaces(vla_model* m) {
+  VLA_TRY(add_vlm_lane(m));
   VLA_TRY(add_act_lane(m));
   return VLA_OK;
 }
@@ -1273,7 +1286,8 @@ static int get_streams(vla_model* m, const vla_sched& s, Streams* out) {
       std::vector<uint32_t> mv, ma;
       cu_mask(0, s.vlm_cus, m->num_cus, mv);
       cu_mask(s.vlm_cus, s.act_cus, m->num_cus, ma);
-      HIP_TRY(hipExtStreamCreateWithCUMask(&st.v, (uint32_t)mv.size(), mv.data()));
+      for (int i = 0; i < MAX_VLM_STREAMS; ++i)
+        HIP_TRY(hipExtStreamCreateWithCUMask(&st.v[i], (uint32_t)mv.size(), mv.data()));
       for (int i = 0; i < MAX_ACT_STREAMS; ++i)
         HIP_TRY(hipExtStreamCreateWithCUMask(&st.a[i], (uint32_t)ma.size(), ma.data()));
       it = m->mask_streams.emplace(key, st).first;
@@ -1281,8 +1295,9 @@ static int get_streams(vla_model* m, const vla_sched& s, Streams* out) {
     *out = it->second;
     return VLA_OK;
   }
-  if (!m->plain.v) {
-    HIP_TRY(hipStreamCreateWithFlags(&m->plain.v, hipStreamNonBlocking));
+  if (!m->plain.v[0]) {
+    for (int i = 0; i < MAX_VLM_STREAMS; ++i)
+      HIP_TRY(hipStreamCreateWithFlags(&m->plain.v[i], hipStreamNonBlocking));
     for (int i = 0; i < MAX_ACT_STREAMS; ++i)
       HIP_TRY(hipStreamCreateWithFlags(&m->plain.a[i], hipStreamNonBlocking));
   }
@@ -1324,21 +1339,26 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
   const int lanes = std::max(1, s.act_streams);
   if (lanes > MAX_ACT_STREAMS) return fail(VLA_EINVAL, "act_streams must be <= 4");
   if (lanes > 1 && s.mode == VLA_MODE_SERIAL) return fail(VLA_EINVAL, "act_streams > 1 needs a concurrent mode");
+  const int vlanes = std::max(1, s.vlm_streams);
+  if (vlanes > MAX_VLM_STREAMS) return fail(VLA_EINVAL, "vlm_streams must be <= 2");
+  if (vlanes > 1 && s.mode == VLA_MODE_SERIAL) return fail(VLA_EINVAL, "vlm_streams > 1 needs a concurrent mode");
   const vla_config& c = m->c;
   for (int r = 0; r < R; ++r)
     if (!frames[r].pixels || (c.n_text > 0 && !frames[r].text_ids) || (c.state_dim > 0 && !frames[r].state))
       return fail(VLA_EINVAL, "frame " + std::to_string(r) + " has a NULL input");
   std::lock_guard<std::mutex> lock(m->mu);
-  const int nctx = lanes + 1;
+  // a context is in flight from its prefill until its action phase ends
+  const int nctx = lanes + vlanes;
   while ((int)m->pctx.size() < nctx) {
     vla_ctx* cx = nullptr;
     VLA_TRY(ctx_create_impl(m, &cx));
     m->pctx.push_back(cx);
   }
   while ((int)m->aws.size() < lanes) VLA_TRY(add_act_lane(m));
+  while ((int)m->vws.size() < vlanes) VLA_TRY(add_vlm_lane(m));
   Streams st;
   VLA_TRY(get_streams(m, s, &st));
-  if (s.mode == VLA_MODE_SERIAL) st.a[0] = st.v;
+  if (s.mode == VLA_MODE_SERIAL) st.a[0] = st.v[0];
   const bool graphs = s.graphs != 0 && m->timer_tag.empty();
   const size_t need = (size_t)4 * R;
   while (m->ev.size() < need) {
@@ -1354,14 +1374,17 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
   HIP_TRY(hipDeviceSynchronize());
 
   if (graphs) {  // capture what is missing (outside the timed loop)
-    vla_frame staged{m->pstage, m->istage, c.state_dim > 0 ? m->sstage : nullptr};
-    for (int ci = 0; ci < nctx; ++ci) {
-      const auto key = std::make_pair(ci, vcaps.max_wgs);
-      if (m->pre_graphs.count(key)) continue;
-      Run rv{m, st.v, vcaps, &m->vw.scr};
-      hipGraphExec_t ge = nullptr;
-      VLA_TRY(capture(st.v, [&] { return run_prefill(rv, &staged, m->pctx[ci]); }, &ge));
-      m->pre_graphs[key] = ge;
+    for (int vi = 0; vi < vlanes; ++vi) {
+      VlmWs* vw = m->vws[vi].get();
+      vla_frame staged{vw->pstage, vw->istage, c.state_dim > 0 ? vw->sstage : nullptr};
+      for (int ci = 0; ci < nctx; ++ci) {
+        const auto key = std::make_tuple(vi, ci, vcaps.max_wgs);
+        if (m->pre_graphs.count(key)) continue;
+        Run rv{m, st.v[vi], vcaps, &vw->scr, nullptr, vw};
+        hipGraphExec_t ge = nullptr;
+        VLA_TRY(capture(st.v[vi], [&] { return run_prefill(rv, &staged, m->pctx[ci]); }, &ge));
+        m->pre_graphs[key] = ge;
+      }
     }
     for (int li = 0; li < lanes; ++li)
       for (int ci = 0; ci < nctx; ++ci) {
@@ -1377,25 +1400,26 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
 
   const auto t0 = std::chrono::steady_clock::now();
   for (int r = 0; r < R; ++r) {
-    const int ci = r % nctx, li = r % lanes;
+    const int ci = r % nctx, li = r % lanes, vi = r % vlanes;
     vla_ctx* ctx = m->pctx[ci];
-    hipStream_t sa = st.a[li];
+    hipStream_t sv = st.v[vi], sa = st.a[li];
+    VlmWs* vw = m->vws[vi].get();
     // the context is free once the action phase that last read it is done
-    if (r >= nctx && st.v != sa) HIP_TRY(hipStreamWaitEvent(st.v, m->ev[4 * (r - nctx) + 3], 0));
-    HIP_TRY(hipEventRecord(m->ev[4 * r], st.v));
+    if (r >= nctx && sv != sa) HIP_TRY(hipStreamWaitEvent(sv, m->ev[4 * (r - nctx) + 3], 0));
+    HIP_TRY(hipEventRecord(m->ev[4 * r], sv));
     if (graphs) {
-      HIP_TRY(hipMemcpyAsync(m->pstage, frames[r].pixels, pix_bytes, hipMemcpyDeviceToDevice, st.v));
+      HIP_TRY(hipMemcpyAsync(vw->pstage, frames[r].pixels, pix_bytes, hipMemcpyDeviceToDevice, sv));
       if (c.n_text > 0)
-        HIP_TRY(hipMemcpyAsync(m->istage, frames[r].text_ids, (size_t)c.n_text * 4, hipMemcpyDeviceToDevice, st.v));
+        HIP_TRY(hipMemcpyAsync(vw->istage, frames[r].text_ids, (size_t)c.n_text * 4, hipMemcpyDeviceToDevice, sv));
       if (c.state_dim > 0)
-        HIP_TRY(hipMemcpyAsync(m->sstage, frames[r].state, (size_t)c.state_dim * 4, hipMemcpyDeviceToDevice, st.v));
-      HIP_TRY(hipGraphLaunch(m->pre_graphs[std::make_pair(ci, vcaps.max_wgs)], st.v));
+        HIP_TRY(hipMemcpyAsync(vw->sstage, frames[r].state, (size_t)c.state_dim * 4, hipMemcpyDeviceToDevice, sv));
+      HIP_TRY(hipGraphLaunch(m->pre_graphs[std::make_tuple(vi, ci, vcaps.max_wgs)], sv));
     } else {
-      Run rv{m, st.v, vcaps, &m->vw.scr};
+      Run rv{m, sv, vcaps, &vw->scr, nullptr, vw};
       VLA_TRY(run_prefill(rv, &frames[r], ctx));
     }
-    HIP_TRY(hipEventRecord(m->ev[4 * r + 1], st.v));
-    if (st.v != sa) HIP_TRY(hipStreamWaitEvent(sa, m->ev[4 * r + 1], 0));
+    HIP_TRY(hipEventRecord(m->ev[4 * r + 1], sv));
+    if (sv != sa) HIP_TRY(hipStreamWaitEvent(sa, m->ev[4 * r + 1], 0));
     HIP_TRY(hipEventRecord(m->ev[4 * r + 2], sa));
     ActWs* aw = m->aws[li].get();
     if (graphs) {
@@ -1408,7 +1432,7 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
     }
     HIP_TRY(hipEventRecord(m->ev[4 * r + 3], sa));
   }
-  HIP_TRY(hipStreamSynchronize(st.v));
+  for (int vi = 0; vi < vlanes; ++vi) HIP_TRY(hipStreamSynchronize(st.v[vi]));
   for (int li = 0; li < lanes; ++li) HIP_TRY(hipStreamSynchronize(st.a[li]));
   const auto t1 = std::chrono::steady_clock::now();
   if (t) {
@@ -1476,7 +1500,8 @@ int vla_destroy(vla_model* m) {
       delete cx;
     }
     auto drop = [](Streams& st) {
-      if (st.v) hipStreamDestroy(st.v);
+      for (hipStream_t v : st.v)
+        if (v) hipStreamDestroy(v);
       for (hipStream_t a : st.a)
         if (a) hipStreamDestroy(a);
     };
@@ -1517,7 +1542,7 @@ int vla_vlm_prefill(vla_model* m, const vla_frame* in, vla_ctx* ctx, void* strea
       return fail(VLA_EINVAL, "NULL argument");
     if (m->c.state_dim > 0 && !in->state) return fail(VLA_EINVAL, "state is NULL but state_dim > 0");
     if (ctx->m != m) return fail(VLA_ESTATE, "context belongs to another model");
-    Run r{m, (hipStream_t)stream, LaunchCaps{}, &m->vw.scr};
+    Run r{m, (hipStream_t)stream, LaunchCaps{}, &m->vws[0]->scr, nullptr, m->vws[0].get()};
     return run_prefill(r, in, ctx);
   })
 }

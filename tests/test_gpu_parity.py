@@ -341,6 +341,8 @@ def test_pipeline_modes_bit_identical(V, cfg):
                  ("serial", dict(graphs=True)), ("concurrent", dict(graphs=True)),
                  ("concurrent", dict(act_streams=2)), ("concurrent", dict(act_streams=3, graphs=True)),
                  ("cu_masked", dict(split, act_streams=2, graphs=True)),
+                 ("concurrent", dict(vlm_streams=2, act_streams=2)),
+                 ("concurrent", dict(vlm_streams=2, act_streams=3, graphs=True)),
                  ("wg_capped", dict(vlm_wg_cap=1, graphs=True))]
         standalone = [g.run_frame(m, cfg, f)[0] for f in frames]
         for mode, kw in modes:
