@@ -62,6 +62,50 @@ def kernel_work(cfg, tag):
     return byts, 2.0 * M * N * K
 
 
+def cu_residency(rec, window=None):
+    """Per-CU residency from workgroup start/end records (vla_wavelog_read).
+
+    CU = (XCC, shader engine, shader array, CU) from the hardware-id
+    registers; the phase of a record is that of its hardware queue (the
+    VLM's queues are those that ran the VLM-only kernel kinds). Returns the
+    mean over CUs of the fraction of the window in which the CU hosts at
+    least one workgroup, and in which it hosts workgroups of both phases."""
+    import numpy as np
+    hw = rec["hwid"].astype(np.int64)
+    cu = rec["xcc"].astype(np.int64) * 256 + ((hw >> 13) & 7) * 32 + ((hw >> 12) & 1) * 16 + ((hw >> 8) & 15)
+    queue = ((hw >> 30) & 3) * 64 + ((hw >> 6) & 3) * 8 + ((hw >> 24) & 7)
+    vlm_q = np.unique(queue[np.isin(rec["kind"], (1, 8, 9))])  # GEMM, patchify, embed
+    is_vlm = np.isin(queue, vlm_q)
+    t = rec["t"].astype(np.int64)
+    d = np.where(rec["end"] == 1, -1, 1)
+    if window is None:
+        if is_vlm.any() and (~is_vlm).any():
+            lo = max(t[is_vlm].min(), t[~is_vlm].min())
+            hi = min(t[is_vlm].max(), t[~is_vlm].max())
+        else:
+            lo, hi = t.min(), t.max()
+    else:
+        lo, hi = window
+    order = np.lexsort((d, t, cu))  # ends before starts at equal times
+    cu, t, dv, da = cu[order], t[order], (d * is_vlm)[order], (d * ~is_vlm)[order]
+    cv, ca = np.cumsum(dv), np.cumsum(da)
+    # restart the running counts at each CU boundary
+    first = np.r_[True, cu[1:] != cu[:-1]]
+    seg = np.cumsum(first) - 1
+    base_v = (cv - dv)[first][seg]
+    base_a = (ca - da)[first][seg]
+    nv, na = cv - base_v, ca - base_a
+    nxt = np.r_[t[1:], t[-1]]
+    same = np.r_[cu[1:] == cu[:-1], False]
+    dur = np.clip(np.minimum(nxt, hi) - np.maximum(t, lo), 0, None) * same
+    ncu = len(np.unique(cu))
+    span = max(hi - lo, 1)
+    busy = float(((nv + na) > 0) @ dur) / (span * ncu)
+    both = float(((nv > 0) & (na > 0)) @ dur) / (span * ncu)
+    return {"cus": int(ncu), "window_ms": float(span) * 1e-5, "busy_frac": float(busy),
+            "both_phases_frac": float(both), "vlm_queues": int(len(vlm_q))}
+
+
 def cpu_baseline(cfg, seed):
     """The fp64 oracle on one frame of the same workload (full VLM prefill
     and the 10-step denoising of that frame); frames/s = 1 / its time."""
@@ -104,6 +148,8 @@ def main():
     ap.add_argument("--extra", default="gr00t:8:serial,concurrent,cu_masked,lanes2_graph,lanes3_graph",
                     help="further workloads, ';'-separated preset:R:schedule,schedule,...")
     ap.add_argument("--extra-steps", type=int, default=5)
+    ap.add_argument("--residency", type=int, default=8_000_000,
+                    help="capacity of the workgroup residency log (0: skip the residency runs)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB five times (the reference "
                          "kernel for scaling the HBM byte counters) and exit")
@@ -207,6 +253,21 @@ def main():
     if args.mode == "auto":
         args.mode = max(results, key=lambda k: results[k]["frames_per_s"])
 
+    # per-CU residency (workgroup start/end log), serialized vs the reported
+    # schedule, one logged pipeline run each (not part of the timed steps)
+    residency = {}
+    if args.residency:
+        print("[bench] residency logs", file=sys.stderr, flush=True)
+        V.vla_wavelog_enable(m, args.residency)
+        for name in dict.fromkeys(["serial", args.mode]):
+            V.vla_wavelog_read(m, 0)
+            V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **kw[name])
+            rec, n = V.vla_wavelog_read(m, args.residency)
+            full = cu_residency(rec, window=(int(rec["t"].min()), int(rec["t"].max())))
+            ovl = cu_residency(rec)
+            residency[name] = {"whole_run": full, "overlap_window": ovl, "records": int(n)}
+        V.vla_wavelog_enable(m, 0)
+
     # dominant kernel, timed live with HIP events on its stream (serial schedule)
     print(f"[bench] kernel timer on {args.kernel}", file=sys.stderr, flush=True)
     V.vla_kernel_timer(m, args.kernel)
@@ -263,6 +324,8 @@ def main():
         "modes": results, "outputs_identical_across_modes": identical,
         "roofline": roofline,
     }
+    if residency:
+        line["cu_residency"] = residency
     if others:
         line["other_workloads"] = others
     if not args.no_cpu_baseline:

@@ -234,6 +234,23 @@ int vla_debug_attention_cache(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv
 int vla_kernel_timer(vla_model* m, const char* tag);
 int vla_kernel_timer_read(vla_model* m, double* total_ms, int64_t* launches);
 
+/* Measurement: workgroup residency log. _enable allocates room for
+ * `capacity` records and points every instrumented kernel of the process at
+ * it (capacity 0 turns logging off and frees the buffer); call it with no
+ * work in flight. While on, the first lane of each workgroup appends a
+ * record when the workgroup starts and when it ends; each record is 24
+ * bytes: uint64 time (100 MHz constant clock), uint32 HW_ID register (CU,
+ * shader array, shader engine, queue), uint32 XCC_ID register, uint32
+ * kernel kind (1 GEMM, 2 split-K reduce, 3 skinny GEMM, 4 LDS attention,
+ * 5 attention combine, 6 cache attention, 7 norm, 8 patchify, 9 embed,
+ * 10 convert), uint32 end flag. _read waits for the device, copies up to
+ * max_records records written since the last read to host_dst, sets *n to
+ * the number copied and restarts the log; it returns VLA_ESTATE when the
+ * log overflowed (records past the capacity are lost).
+ * One log per process and device: the last model to enable it owns it. */
+int vla_wavelog_enable(vla_model* m, int64_t capacity);
+int vla_wavelog_read(vla_model* m, void* host_dst, int64_t max_records, int64_t* n);
+
 /* Host-only: values start .. start+n-1 of the library's parameter generator
  * for (seed, name) with the given mean and std, as fp32 (before any bf16
  * rounding) into host_dst. Needs no GPU. */

@@ -96,6 +96,8 @@ def _load():
         "vla_export_param": [P, ctypes.c_char_p, P, I64],
         "vla_ctx_export_kv": [P, P, I32, P, P],
         "vla_ctx_export_cross": [P, P, I32, P, P],
+        "vla_wavelog_enable": [P, I64],
+        "vla_wavelog_read": [P, P, I64, ctypes.POINTER(I64)],
         "vla_debug_gemm": [I32, I32, I32, I32, P, I32, P, I32, P, P, P],
         "vla_debug_attention": [I32, I32, I32, I32, I32, P, P, P, I32, P, P, I32, P, P],
         "vla_debug_generate": [U64, ctypes.c_char_p, I64, D, D, P],
@@ -224,6 +226,21 @@ def vla_ctx_export_cross(model: int, ctx: int, layer: int, n: int) -> Tuple[np.n
     return k, v
 
 
+WAVE_REC = np.dtype([("t", "<u8"), ("hwid", "<u4"), ("xcc", "<u4"), ("kind", "<u4"), ("end", "<u4")])
+
+
+def vla_wavelog_enable(model: int, capacity: int) -> None:
+    _check(_lib.vla_wavelog_enable(model, int(capacity)))
+
+
+def vla_wavelog_read(model: int, max_records: int) -> Tuple[np.ndarray, int]:
+    buf = np.empty(int(max_records), dtype=WAVE_REC)
+    n = ctypes.c_int64()
+    _check(_lib.vla_wavelog_read(model, buf.ctypes.data if max_records else None, int(max_records),
+                                 ctypes.byref(n)))
+    return buf[:min(n.value, max_records)], n.value
+
+
 def vla_debug_gemm(dtype: int, M: int, N: int, K: int, A, lda: int, W, ldw: int, bias, C,
                    stream: int = 0) -> None:
     _check(_lib.vla_debug_gemm(dtype, M, N, K, _ptr(A), lda, _ptr(W), ldw, _ptr(bias), _ptr(C),
@@ -263,7 +280,7 @@ def exported_symbols() -> Iterable[str]:
     """Names of the C entry points this binding wraps."""
     return ["vla_preset", "vla_validate", "vla_create", "vla_destroy", "vla_ctx_create",
             "vla_ctx_destroy", "vla_vlm_prefill", "vla_action_denoise", "vla_pipeline_run",
-            "vla_param_count", "vla_param_info", "vla_export_param", "vla_ctx_export_kv", "vla_ctx_export_cross",
+            "vla_param_count", "vla_param_info", "vla_export_param", "vla_ctx_export_kv", "vla_ctx_export_cross", "vla_wavelog_enable", "vla_wavelog_read",
             "vla_debug_gemm", "vla_debug_attention", "vla_debug_attention_cache", "vla_debug_generate",
             "vla_kernel_timer",
             "vla_kernel_timer_read", "vla_last_error"]

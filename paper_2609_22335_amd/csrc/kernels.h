@@ -248,4 +248,29 @@ hipError_t launch_cvt_pad(int dtype, const float* src, int rows, int cols, void*
 hipError_t launch_bcast_row(int dtype, const void* row, int cols, void* dst, int ld_dst, int rows,
                             hipStream_t st);
 
+// Per-workgroup residency log (measurement only). While a log is set, the
+// first lane of every workgroup of the instrumented kernels appends one
+// record when the workgroup starts and one when it ends: the time on the
+// 100 MHz constant clock, the hardware-id register (CU, shader array and
+// engine, and the queue the work came from), the XCC id, the kernel kind
+// and whether it is the end.
+struct WaveRec {
+  uint64_t t;
+  uint32_t hwid, xcc, kind, end;
+};
+// Eight slices (one per XCC, counters 256 bytes apart to keep the atomics
+// of different XCCs off one cache line), cap records each.
+constexpr int WAVELOG_SLICES = 8;
+struct WaveLog {
+  uint32_t cap, pad[63];
+  uint32_t count[WAVELOG_SLICES * 64];  // slice x counts at count[64 x]
+  WaveRec rec[1];                        // WAVELOG_SLICES * cap records follow
+};
+enum KernelKind {
+  KK_GEMM = 1, KK_SPLITK, KK_SKINNY, KK_ATTN, KK_ATTN_COMBINE, KK_ATTN2, KK_NORM,
+  KK_PATCHIFY, KK_EMBED, KK_CVT
+};
+// Point the kernels at a log (nullptr: off). Not while kernels run.
+hipError_t wavelog_set(WaveLog* dev);
+
 }  // namespace vla

@@ -25,6 +25,42 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int NUM_CU_PLAN = 256;  // planner constant; never the live CU count
 
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+// Residency log (see WaveLog): one load of the log pointer at the start and
+// at the end of a workgroup; one vector atomic per record while logging. No
+// register is held between the two points.
+__device__ WaveLog* g_wavelog = nullptr;
+
+__device__ __forceinline__ void wave_event(uint32_t kind, uint32_t end) {
+  WaveLog* L = g_wavelog;
+  if (threadIdx.x != 0) return;
+  const uint64_t t = wall_clock64();
+  const uint32_t xcc = __builtin_amdgcn_s_getreg((31 << 11) | 20);  // XCC_ID
+  const uint32_t x = xcc & (WAVELOG_SLICES - 1);
+  const uint32_t i = atomicAdd(&L->count[64 * x], 1u);
+  if (i < L->cap) {
+    WaveRec r;
+    r.t = t;
+    r.hwid = __builtin_amdgcn_s_getreg((31 << 11) | 4);  // HW_ID
+    r.xcc = xcc;
+    r.kind = kind;
+    r.end = end;
+    L->rec[(size_t)x * L->cap + i] = r;
+  }
+}
+
+#define VLA_WAVE_BEGIN(kind)                \
+  do {                                      \
+    if (g_wavelog) wave_event((kind), 0u);  \
+  } while (0)
+#define VLA_WAVE_END(kind)                  \
+  do {                                      \
+    if (g_wavelog) wave_event((kind), 1u);  \
+  } while (0)
+
+hipError_t wavelog_set(WaveLog* dev) {
+  return hipMemcpyToSymbol(HIP_SYMBOL(g_wavelog), &dev, sizeof(dev));
+}
+
 // round to nearest, ties to even (the hardware conversion)
 __device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 __device__ __forceinline__ uint32_t f2bf2(float lo, float hi) {
@@ -253,6 +289,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
                                               const T* __restrict__ W, int ldw, int M, int N,
                                               int K, int kchunk, int splits, int tiles_m,
                                               int tiles_n, Epi e, float* __restrict__ part) {
+  VLA_WAVE_BEGIN(KK_GEMM);
   using SM = GemmSmem<T, BM, BN, BK, WGM>;
   constexpr int VEC = SM::VEC;
   constexpr int SW = 4 * VEC;  // K covered by one MFMA step across the 4 lane groups
@@ -407,12 +444,14 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
       }
     }
   }
+  VLA_WAVE_END(KK_GEMM);
 }
 
 // Sum of split-K partials in split order, then the epilogue.
 template <typename T>
 __global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__ part, int splits,
                                                        int M, int N, Epi e) {
+  VLA_WAVE_BEGIN(KK_SPLITK);
   const int groups = (N + 31) / 32;
   const long long total = (long long)M * groups * 16;
   for (long long idx = blockIdx.x * (long long)blockDim.x + threadIdx.x; idx < total;
@@ -429,6 +468,7 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__
     }
     epi_pair<T>(e, M, N, m, n, v0, v1);
   }
+  VLA_WAVE_END(KK_SPLITK);
 }
 
 // ---------------------------------------------------------------------------
@@ -451,6 +491,7 @@ __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, int lda
                                                 const T* __restrict__ Wf, int KS, int ks0, int M,
                                                 int N, int K, int splits, Epi e,
                                                 float* __restrict__ part) {
+  VLA_WAVE_BEGIN(KK_SKINNY);
   constexpr int VEC = 16 / sizeof(T);
   constexpr int SW = 4 * VEC;
   __shared__ float red[4][8][4][64];  // [wave][n-block * 4 + m-tile][r][lane]
@@ -522,6 +563,7 @@ __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, int lda
       }
     }
   }
+  VLA_WAVE_END(KK_SKINNY);
 }
 
 size_t frag_index(int n, int k, int KS, int dtype) {
@@ -700,6 +742,7 @@ struct AttnArgs {
 
 template <typename T, int HDP>
 __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
+  VLA_WAVE_BEGIN(KK_ATTN);
   constexpr int VEC = 16 / sizeof(T);
   constexpr int SW = 4 * VEC;
   constexpr int KS = HDP + VEC;          // sK row stride
@@ -906,10 +949,12 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
       }
     }
   }
+  VLA_WAVE_END(KK_ATTN);
 }
 
 template <typename T, int HDP>
 __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
+  VLA_WAVE_BEGIN(KK_ATTN_COMBINE);
   const int group = a.nq / a.nkv;
   const int R = a.Sq * group;
   const int nwork = a.qblocks * a.nkv * a.segs;
@@ -942,6 +987,7 @@ __global__ __launch_bounds__(256) void k_attn_combine(AttnArgs a) {
     T* op = (T*)a.out + seg * a.seg_o + (size_t)sq * a.ldo + h * a.hd;
     TT<T>::st(op + d, num / den);
   }
+  VLA_WAVE_END(KK_ATTN_COMBINE);
 }
 
 static int attn_hdp(int hd, int dtype) {
@@ -1087,6 +1133,7 @@ constexpr int att2_waves() {
 
 template <typename T, int HDP, int NW>
 __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
+  VLA_WAVE_BEGIN(KK_ATTN2);
   constexpr int VEC = 16 / sizeof(T);
   constexpr int SW = 4 * VEC;
   constexpr int NQF = HDP / SW;   // Q fragments (also K fragments per 16-key tile)
@@ -1313,6 +1360,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
     }
     __syncthreads();
   }
+  VLA_WAVE_END(KK_ATTN2);
 }
 
 template <typename T>
@@ -1388,6 +1436,7 @@ constexpr int NORM_NPT = 8;
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_norm(NormDesc n) {
+  VLA_WAVE_BEGIN(KK_NORM);
   constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
   __shared__ float red[4];
   const int rows = n.rows, d = n.d, ldx = n.ldx, splits = n.splits;
@@ -1478,6 +1527,7 @@ __global__ __launch_bounds__(256) void k_norm(NormDesc n) {
       }
     }
   }
+  VLA_WAVE_END(KK_NORM);
 }
 
 hipError_t launch_norm(const NormDesc& n, hipStream_t st) {
@@ -1499,6 +1549,7 @@ hipError_t launch_norm(const NormDesc& n, hipStream_t st) {
 template <typename T>
 __global__ void k_patchify(const float* __restrict__ pix, int views, int H, int W, int p,
                            T* __restrict__ out, int ldo) {
+  VLA_WAVE_BEGIN(KK_PATCHIFY);
   const int gw = W / p, gh = H / p, T_ = gh * gw, kp = 3 * p * p;
   const long long total = (long long)views * T_ * ldo;
   for (long long idx = blockIdx.x * (long long)blockDim.x + threadIdx.x; idx < total;
@@ -1514,6 +1565,7 @@ __global__ void k_patchify(const float* __restrict__ pix, int views, int H, int 
     }
     TT<T>::st(out + idx, v);
   }
+  VLA_WAVE_END(KK_PATCHIFY);
 }
 
 hipError_t launch_patchify(int dtype, const float* pix, int views, int H, int W, int p, void* out,
@@ -1530,11 +1582,13 @@ hipError_t launch_patchify(int dtype, const float* pix, int views, int H, int W,
 template <typename T>
 __global__ void k_embed(const T* __restrict__ E, int d, int vocab, const int32_t* __restrict__ ids,
                         int n, float scale, float* __restrict__ x, int ldx) {
+  VLA_WAVE_BEGIN(KK_EMBED);
   for (int row = blockIdx.x; row < n; row += gridDim.x) {
     const int id = min(max(ids[row], 0), vocab - 1);  // out-of-range ids are clamped
     const T* er = E + (size_t)id * d;
     for (int i = threadIdx.x; i < d; i += blockDim.x) x[(size_t)row * ldx + i] = TT<T>::ld(er + i) * scale;
   }
+  VLA_WAVE_END(KK_EMBED);
 }
 
 hipError_t launch_embed(int dtype, const void* E, int d, int vocab, const int32_t* ids, int n,
@@ -1551,6 +1605,7 @@ hipError_t launch_embed(int dtype, const void* E, int d, int vocab, const int32_
 template <typename T>
 __global__ void k_cvt_pad(const float* __restrict__ src, int rows, int cols, T* __restrict__ dst,
                           int ld, int afrag, float* __restrict__ dst32) {
+  VLA_WAVE_BEGIN(KK_CVT);
   constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
   const long long total = (long long)rows * ld;
   for (long long idx = blockIdx.x * (long long)blockDim.x + threadIdx.x; idx < total;
@@ -1561,6 +1616,7 @@ __global__ void k_cvt_pad(const float* __restrict__ src, int rows, int cols, T* 
     TT<T>::st(dst + (afrag ? afrag_index(DT, (int)r, c) : (size_t)idx), v);
     if (dst32 && c < cols) dst32[r * cols + c] = v;
   }
+  VLA_WAVE_END(KK_CVT);
 }
 
 hipError_t launch_cvt_pad(int dtype, const float* src, int rows, int cols, void* dst, int ld_dst,

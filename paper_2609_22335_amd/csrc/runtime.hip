@@ -289,6 +289,8 @@ struct vla_model {
 
   // phase scratch
   std::vector<std::unique_ptr<VlmWs>> vws;  // VLM lanes; lane 0 serves standalone calls
+  WaveLog* wlog = nullptr;                  // residency log (measurement), device memory
+  size_t wlog_cap = 0;
   std::vector<std::unique_ptr<ActWs>> aws;  // action lanes; lane 0 serves standalone calls
   std::vector<void*> allocs;
 
@@ -1509,6 +1511,10 @@ int vla_destroy(vla_model* m) {
     drop(m->plain);
     for (auto e : m->ev) hipEventDestroy(e);
     for (auto e : m->timer_ev) hipEventDestroy(e);
+    if (m->wlog) {
+      wavelog_set(nullptr);
+      hipFree(m->wlog);
+    }
     for (void* p : m->allocs) hipFree(p);
     hipFree(m->arena);
     delete m;
@@ -1650,6 +1656,60 @@ int vla_ctx_export_cross(vla_model* m, const vla_ctx* c, int32_t layer, float* h
           host_k[(size_t)p * nh * hd + j * hd + dd] = val(kimg, kv_kidx(m->dt, nb, hd, j, p, dd));
           host_v[(size_t)p * nh * hd + j * hd + dd] = val(vimg, kv_vidx(m->dt, nb, hd, j, p, dd));
         }
+    return VLA_OK;
+  })
+}
+
+int vla_wavelog_enable(vla_model* m, int64_t capacity) {
+  ABI_GUARD({
+    if (!m) return fail(VLA_EINVAL, "model is NULL");
+    if (capacity < 0 || capacity > (int64_t)1 << 30) return fail(VLA_EINVAL, "capacity out of range");
+    std::lock_guard<std::mutex> lock(m->mu);
+    HIP_TRY(hipDeviceSynchronize());
+    HIP_TRY(wavelog_set(nullptr));
+    if (m->wlog) {
+      HIP_TRY(hipFree(m->wlog));
+      m->wlog = nullptr;
+      m->wlog_cap = 0;
+    }
+    if (capacity == 0) return VLA_OK;
+    const size_t per = ((size_t)capacity + WAVELOG_SLICES - 1) / WAVELOG_SLICES;
+    const size_t bytes = sizeof(WaveLog) + per * WAVELOG_SLICES * sizeof(WaveRec);
+    hipError_t e = hipMalloc(&m->wlog, bytes);
+    if (e != hipSuccess) return fail(VLA_ENOMEM, "wave log: hipMalloc failed");
+    std::vector<uint8_t> head(offsetof(WaveLog, rec), 0);
+    ((WaveLog*)head.data())->cap = (uint32_t)per;
+    HIP_TRY(hipMemcpy(m->wlog, head.data(), head.size(), hipMemcpyHostToDevice));
+    m->wlog_cap = per;
+    HIP_TRY(wavelog_set(m->wlog));
+    return VLA_OK;
+  })
+}
+
+int vla_wavelog_read(vla_model* m, void* host_dst, int64_t max_records, int64_t* n) {
+  ABI_GUARD({
+    if (!m || !n || (!host_dst && max_records > 0)) return fail(VLA_EINVAL, "NULL argument");
+    if (!m->wlog) return fail(VLA_ESTATE, "the wave log is not enabled");
+    std::lock_guard<std::mutex> lock(m->mu);
+    HIP_TRY(hipDeviceSynchronize());
+    std::vector<uint8_t> head(offsetof(WaveLog, rec));
+    HIP_TRY(hipMemcpy(head.data(), m->wlog, head.size(), hipMemcpyDeviceToHost));
+    WaveLog* h = (WaveLog*)head.data();
+    int64_t total = 0, got = 0;
+    const int64_t room = std::max<int64_t>(max_records, 0);
+    for (int x = 0; x < WAVELOG_SLICES; ++x) {
+      const int64_t c = h->count[64 * x];
+      total += c;
+      const int64_t k = std::min<int64_t>({c, (int64_t)m->wlog_cap, room - got});
+      if (k > 0)
+        HIP_TRY(hipMemcpy((WaveRec*)host_dst + got, m->wlog->rec + (size_t)x * m->wlog_cap,
+                          (size_t)k * sizeof(WaveRec), hipMemcpyDeviceToHost));
+      got += std::max<int64_t>(k, 0);
+      h->count[64 * x] = 0;
+    }
+    *n = got;
+    if (total > got && room > got) return fail(VLA_ESTATE, "wave log overflowed: raise the capacity");
+    HIP_TRY(hipMemcpy(m->wlog, head.data(), head.size(), hipMemcpyHostToDevice));
     return VLA_OK;
   })
 }
