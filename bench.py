@@ -130,6 +130,31 @@ def cpu_baseline(cfg, seed):
                       f"denoising, fp64 NumPy, {dt:.1f} s", "seconds": dt}, chunk
 
 
+def measured_traffic(preset, R, kernel):
+    """HBM bytes per launch of `kernel` from the committed counter record
+    (FETCH_SIZE + WRITE_SIZE, each scaled by a plain copy's reading), or
+    None when the record is for another workload or the kernel source has
+    changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{kernel.replace('.', '_')}_{preset}_R{R}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if kernel_source_digest() != rec["kernels_code_sha256"]:
+        return None
+    return rec["traffic_bytes_per_launch"]
+
+
+def kernel_source_digest():
+    """sha256 of the kernel source with comments and whitespace removed: any
+    code change (in any kernel) changes it, a comment edit does not."""
+    import hashlib
+    import re
+    src = open(os.path.join(ROOT, "paper_2609_22335_amd", "csrc", "kernels.hip")).read()
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return hashlib.sha256(" ".join(src.split()).encode()).hexdigest()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -283,7 +308,7 @@ def main():
     else:
         ach, peak, unit = flops / avg_s / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"
     roofline = {"bound": "hbm" if hbm_bound else "mfma", "achieved": ach, "peak": peak, "unit": unit,
-                "frac": ach / peak, "traffic": None, "kernel": args.kernel,
+                "frac": ach / peak, "traffic": measured_traffic(args.preset, R, args.kernel), "kernel": args.kernel,
                 "avg_us": avg_s * 1e6, "launches": launches,
                 "algorithmic_bytes": byts, "flops": flops}
     outs = outputs[args.mode]

@@ -257,13 +257,13 @@ __device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int 
 // GEMM: C[M, N] = A[M, K] W[N, K]^T, both operands K-contiguous.
 // 256 threads = 4 waves in a 2 x 2 arrangement; each wave owns a
 // (BM/2) x (BN/2) block of 16 x 16 MFMA tiles. A and W tiles go through a
-// two-stage LDS ring (rows padded by 16 bytes against bank conflicts) with the
-// next K-tile prefetched into registers, one barrier per K-step. The
-// accumulators are staged through LDS for the epilogue, so epilogue stores are
-// row-contiguous. Split-K partials are summed inside the kernel: the last
-// workgroup to finish a tile (per-tile arrival counter) adds the partials in
-// split order, so the result does not depend on arrival order. Tiles are
-// visited grid-stride so a capped grid computes the same tiles.
+// two-stage LDS ring (rows padded against bank conflicts) fed by a ring of PD
+// K-tiles held in registers, one barrier per K-step. The accumulators are
+// staged through LDS for the epilogue, so epilogue stores are row-contiguous.
+// With split-K each split writes its raw fp32 partial ([split][M][N]); a
+// second kernel sums the partials in split order and applies the epilogue, so
+// the result does not depend on which split finishes first. Tiles are visited
+// grid-stride so a capped grid computes the same tiles.
 // ---------------------------------------------------------------------------
 
 #ifndef VLA_GEMM_LDS_PAD
