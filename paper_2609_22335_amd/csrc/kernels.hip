@@ -1431,80 +1431,92 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
   return (red[0] + red[1]) + (red[2] + red[3]);
 }
 
-// One workgroup per row; row values stay in registers (d <= 256 * NORM_NPT).
-constexpr int NORM_NPT = 8;
+// One workgroup per row. Thread t owns the four-column groups starting at
+// columns 4 t, 4 t + 1024, ... (16-byte accesses), and every load of the row
+// (x, the split partials, bias, column scale, gain and shift) is issued before
+// the first use, so a row costs one memory round trip.
+constexpr int NORM_VPT = 2;  // four-column groups per thread: d <= 2048
+
+__device__ __forceinline__ f32x4 bld4f(Rsrc r, uint32_t off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_norm(NormDesc n) {
   VLA_WAVE_BEGIN(KK_NORM);
   constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
+  constexpr int SPL = 8;  // split partials requested together
   __shared__ float red[4];
   const int rows = n.rows, d = n.d, ldx = n.ldx, splits = n.splits;
   float* __restrict__ x = n.x;
   const size_t pstride = (size_t)rows * d;
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f}, one4 = {1.f, 1.f, 1.f, 1.f};
+  // absent vectors get an empty range: their loads return zeros
   const Rsrc rx = rsrc(x, span(rows, ldx, d, 4));
   const Rsrc rp = rsrc(n.part ? n.part : x, n.part ? (size_t)splits * pstride * 4 : 0);
   const Rsrc rb = rsrc(n.bias ? n.bias : x, n.bias ? (size_t)d * 4 : 0);
   const Rsrc rc = rsrc(n.colscale ? n.colscale : x, n.colscale ? (size_t)d * 4 : 0);
+  const Rsrc rg = rsrc(n.g, (size_t)d * 4);
+  const Rsrc rs = rsrc(n.b ? n.b : x, n.b ? (size_t)d * 4 : 0);
   for (int row = blockIdx.x; row < rows; row += gridDim.x) {
-    float* xr = x + (size_t)row * ldx;
-    float v[NORM_NPT], add[NORM_NPT], cs[NORM_NPT];
+    f32x4 v[NORM_VPT], add[NORM_VPT], cs[NORM_VPT], gn[NORM_VPT], sh[NORM_VPT];
 #pragma unroll
-    for (int q = 0; q < NORM_NPT; ++q) {
-      const int i = threadIdx.x + q * 256;
-      const bool ok = i < d;
-      v[q] = bld1(rx, ok ? (uint32_t)(((size_t)row * ldx + i) * 4) : OOB);
-      add[q] = n.bias ? bld1(rb, ok ? (uint32_t)(i * 4) : OOB) : 0.f;
-      cs[q] = n.colscale ? bld1(rc, ok ? (uint32_t)(i * 4) : OOB) : 1.f;
+    for (int q = 0; q < NORM_VPT; ++q) {
+      const int c = (threadIdx.x + q * 256) * 4;
+      const bool ok = c < d;
+      v[q] = bld4f(rx, ok ? (uint32_t)(((size_t)row * ldx + c) * 4) : OOB);
+      add[q] = bld4f(rb, ok ? (uint32_t)(c * 4) : OOB);
+      cs[q] = bld4f(rc, ok ? (uint32_t)(c * 4) : OOB);
+      gn[q] = bld4f(rg, ok ? (uint32_t)(c * 4) : OOB);
+      sh[q] = bld4f(rs, ok ? (uint32_t)(c * 4) : OOB);
     }
     if (splits > 0) {
-      // partials in split order; four splits' loads are issued together
-      const size_t pbase = (size_t)row * d + threadIdx.x;
-      float sum[NORM_NPT];
+      // partials summed in split order, SPL splits' loads in flight at once
+      f32x4 sum[NORM_VPT];
 #pragma unroll
-      for (int q = 0; q < NORM_NPT; ++q) sum[q] = 0.f;
-      int sp = 0;
-      for (; sp + 4 <= splits; sp += 4) {
-        float t[4][NORM_NPT];
+      for (int q = 0; q < NORM_VPT; ++q) sum[q] = zero4;
+      for (int sp = 0; sp < splits; sp += SPL) {
+        f32x4 t[SPL][NORM_VPT];
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < SPL; ++u)
 #pragma unroll
-          for (int q = 0; q < NORM_NPT; ++q)
-            t[u][q] = bld1(rp, threadIdx.x + q * 256 < d
-                                   ? (uint32_t)((pbase + (sp + u) * pstride + q * 256) * 4) : OOB);
+          for (int q = 0; q < NORM_VPT; ++q) {
+            const int c = (threadIdx.x + q * 256) * 4;
+            const bool ok = c < d && sp + u < splits;
+            t[u][q] = bld4f(rp, ok ? (uint32_t)(((size_t)row * d + (sp + u) * pstride + c) * 4) : OOB);
+          }
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < SPL; ++u)
 #pragma unroll
-          for (int q = 0; q < NORM_NPT; ++q) sum[q] += t[u][q];
+          for (int q = 0; q < NORM_VPT; ++q)
+            if (sp + u < splits) sum[q] += t[u][q];
       }
-      for (; sp < splits; ++sp)
 #pragma unroll
-        for (int q = 0; q < NORM_NPT; ++q)
-          sum[q] += bld1(rp, threadIdx.x + q * 256 < d
-                                 ? (uint32_t)((pbase + sp * pstride + q * 256) * 4) : OOB);
-#pragma unroll
-      for (int q = 0; q < NORM_NPT; ++q) add[q] += n.colscale ? cs[q] * sum[q] : sum[q];
+      for (int q = 0; q < NORM_VPT; ++q) add[q] += n.colscale ? cs[q] * sum[q] : sum[q];
     }
     float s1 = 0.f;
 #pragma unroll
-    for (int q = 0; q < NORM_NPT; ++q) {
-      const int i = threadIdx.x + q * 256;
-      if (i < d) {
+    for (int q = 0; q < NORM_VPT; ++q) {
+      const int c = (threadIdx.x + q * 256) * 4;
+      if (c < d) {
         if (splits > 0) {
           v[q] += add[q];
-          xr[i] = v[q];
+          *(f32x4*)(x + (size_t)row * ldx + c) = v[q];
         }
-        s1 += v[q];
+        s1 += (v[q][0] + v[q][1]) + (v[q][2] + v[q][3]);
       }
     }
     const float mean = n.rms ? 0.f : block_sum(s1, red) / d;
     float s2 = 0.f;
 #pragma unroll
-    for (int q = 0; q < NORM_NPT; ++q) {
-      const int i = threadIdx.x + q * 256;
-      if (i < d) {
-        const float c = v[q] - mean;
-        s2 += c * c;
+    for (int q = 0; q < NORM_VPT; ++q) {
+      const int c = (threadIdx.x + q * 256) * 4;
+      if (c < d) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float cd = v[q][e] - mean;
+          s2 += cd * cd;
+        }
       }
     }
     const float inv = 1.f / sqrtf(block_sum(s2, red) / d + 1e-6f);
@@ -1517,13 +1529,18 @@ __global__ __launch_bounds__(256) void k_norm(NormDesc n) {
       obase = (size_t)orow * n.ldo + (size_t)((y % s) * s + xx % s) * d;
     }
 #pragma unroll
-    for (int q = 0; q < NORM_NPT; ++q) {
-      const int i = threadIdx.x + q * 256;
-      if (i < d) {
-        const float gi = n.g_plus_one ? 1.f + n.g[i] : n.g[i];
-        float y = (v[q] - mean) * inv * gi;
-        if (n.b) y += n.b[i];
-        TT<T>::st((T*)n.out + (n.afrag ? afrag_index(DT, row, i) : obase + i), y);
+    for (int q = 0; q < NORM_VPT; ++q) {
+      const int c = (threadIdx.x + q * 256) * 4;
+      if (c < d) {
+        const f32x4 gi = n.g_plus_one ? one4 + gn[q] : gn[q];
+        f32x4 y = (v[q] - mean) * inv * gi;
+        if (n.b) y += sh[q];
+        // four consecutive columns are contiguous in both output layouts
+        T* dst = (T*)n.out + (n.afrag ? afrag_index(DT, row, c) : obase + c);
+        if constexpr (sizeof(T) == 2)
+          *(uint2*)dst = make_uint2(f2bf2(y[0], y[1]), f2bf2(y[2], y[3]));
+        else
+          *(f32x4*)dst = y;
       }
     }
   }
@@ -1531,7 +1548,13 @@ __global__ __launch_bounds__(256) void k_norm(NormDesc n) {
 }
 
 hipError_t launch_norm(const NormDesc& n, hipStream_t st) {
-  if (n.d > 256 * NORM_NPT || (n.afrag && n.rows > 64) || !n.x || !n.g || !n.out ||
+  // four-column accesses: 16-byte fp32 loads and stores, 8-byte bf16 stores
+  auto mis = [](const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) != 0; };
+  if (mis(n.x, 16) || mis(n.part, 16) || mis(n.bias, 16) || mis(n.colscale, 16) ||
+      mis(n.g, 16) || mis(n.b, 16) || mis(n.out, n.dtype == DT_BF16 ? 8 : 16))
+    return hipErrorInvalidValue;
+  if (n.d > 1024 * NORM_VPT || n.d % 4 || n.ldx % 4 || (!n.afrag && n.ldo % 4) ||
+      (n.afrag && n.rows > 64) || !n.x || !n.g || !n.out ||
       (n.shuffle > 1 && (n.grid_w % n.shuffle || n.tview % (n.shuffle * n.grid_w) || n.afrag)))
     return hipErrorInvalidValue;
   const int grid = std::min(n.rows, 4096);
