@@ -238,6 +238,11 @@ def test_pi0_full_size_vs_oracle(V):
     fr = synth.make_frame(cfg, 0, 0)
     with g.model(cfg, 0) as m:
         got, kv = g.run_frame(m, cfg, fr)
+        # the schedule the benchmark reports (two action lanes, graph replay)
+        # gives the same bits as the standalone calls
+        g.say("pi0 full size: pipeline, two action lanes, graphs")
+        piped = _pipeline_frames(g, m, cfg, [fr, synth.make_frame(cfg, 0, 1)])
+        assert np.array_equal(piped[0].astype(np.float64), got)
     g.say("pi0 full size: oracle")
     P = synth.make_params(cfg, 0)
     cap = {}
@@ -248,6 +253,48 @@ def test_pi0_full_size_vs_oracle(V):
         assert np.all(np.abs(kv[l][0] - rk) <= _kv_tol(cfg, rk)), l
     err = float(np.abs(got - want).max())
     print(f"[gpu] pi0 chunk max abs err {err:.3e}", flush=True)
+    assert err <= CHUNK_TOL[synth.BF16]
+
+
+def _pipeline_frames(g, m, cfg, frames):
+    """Chunks of `frames` from one pipeline run in the two-action-lane graph
+    schedule."""
+    dfs = [g.DevFrame(f) for f in frames]
+    noise = torch.stack([d.noise for d in dfs]).contiguous()
+    out = torch.full_like(noise, float("nan"))
+    V_ = g.V
+    V_.vla_pipeline_run(m, [d.c for d in dfs], noise, len(frames), mode="concurrent", actions=out,
+                        act_streams=2, graphs=True)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+@pytest.mark.timeout(900)
+def test_pi0_three_views_full_size_vs_oracle(V):
+    """The stress shape at its real sizes: three camera views (768 image
+    tokens, attention within each view) and 64 text tokens, so an 833-token
+    prefix and 883 keys for the expert. Frame 0 of seed 0 from a pipeline run
+    in the benchmark's schedule against the oracle, and against the
+    standalone prefill + denoise bit for bit."""
+    g = G()
+    cfg = synth.PI0_3VIEW
+    g.say("pi0 three views full size: GPU")
+    frames = [synth.make_frame(cfg, 0, r) for r in range(2)]
+    with g.model(cfg, 0) as m:
+        got, kv = g.run_frame(m, cfg, frames[0])
+        g.say("pi0 three views full size: pipeline, two action lanes, graphs")
+        piped = _pipeline_frames(g, m, cfg, frames)
+    assert np.array_equal(piped[0].astype(np.float64), got)
+    g.say("pi0 three views full size: oracle")
+    P = synth.make_params(cfg, 0)
+    cap = {}
+    want = O.forward(P, cfg, frames[0], cap)
+    nkvd = cfg["lm_kv_heads"] * cfg["head_dim"]
+    for l in (0, cfg["lm_layers"] - 1):
+        rk = cap["kv"][l][0].reshape(-1, nkvd).ravel()
+        assert np.all(np.abs(kv[l][0] - rk) <= _kv_tol(cfg, rk)), l
+    err = float(np.abs(got - want).max())
+    print(f"[gpu] pi0 three views chunk max abs err {err:.3e}", flush=True)
     assert err <= CHUNK_TOL[synth.BF16]
 
 
