@@ -11,8 +11,10 @@ frame r+1 overlaps the action denoising of frame r. Inputs are resident in
 HBM before the timed region.
 
 Further workloads of the same pipeline (``--extra``; by default the
-GR00T-shaped VLA with its DiT action head, R=8) are measured the same way
-and reported under ``other_workloads``; the headline stays the one above.
+GR00T-shaped VLA with its DiT action head at R=8, and the three-view stress
+shape at R=32 with its sweep of CU splits 224/32, 192/64, 160/96 and VLM
+workgroup caps of 1 and 2 per CU) are measured the same way and reported
+under ``other_workloads``; the headline stays the one above.
 
 Prints one JSON line: frames/s of the fastest schedule as `value` (named in
 config.schedule),
@@ -170,7 +172,9 @@ def main():
     ap.add_argument("--kernel", default="ex.gateup", help="tag of the kernel timed for the roofline")
     ap.add_argument("--preset", default="pi0")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--extra", default="gr00t:8:serial,concurrent,cu_masked,lanes2_graph,lanes3_graph",
+    ap.add_argument("--extra", default="gr00t:8:serial,concurrent,cu_masked,lanes2_graph,v2_lanes2_graph;"
+                                       "pi0_3view:32:serial,concurrent,cu_224_32,cu_192_64,cu_160_96,"
+                                       "wg_cap1,wg_cap2,lanes2_graph,cu_160_96_lanes2",
                     help="further workloads, ';'-separated preset:R:schedule,schedule,...")
     ap.add_argument("--extra-steps", type=int, default=5)
     ap.add_argument("--residency", type=int, default=8_000_000,
@@ -228,6 +232,7 @@ def main():
           "v2_lanes4_graph": dict(mode="concurrent", vlm_streams=2, act_streams=4, graphs=True)}
     for a_, b_ in ((224, 32), (192, 64), (160, 96)):  # CU-split sweep entries
         kw[f"cu_{a_}_{b_}"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_)
+        kw[f"cu_{a_}_{b_}_lanes2"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_, act_streams=2, graphs=True)
         kw[f"cu_{a_}_{b_}_lanes3"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_, act_streams=3, graphs=True)
     for c_ in (1, 2, 4):
         kw[f"wg_cap{c_}"] = dict(mode="wg_capped", vlm_wg_cap=c_)
