@@ -166,7 +166,8 @@ def main():
     ap.add_argument("--mode", default="auto",
                     help="schedule reported as `value` (auto: the fastest measured one)")
     ap.add_argument("--modes", default="serial,concurrent,cu_masked,wg_capped,serial_graph,"
-                                       "concurrent_graph,lanes2_graph,lanes3_graph")
+                                       "concurrent_graph,lanes2_graph,lanes3_graph,batch2_graph,"
+                                       "batch2_lanes2_graph")
     ap.add_argument("--split", default="192,64", help="CU split VLM,action for cu_masked")
     ap.add_argument("--wg-cap", type=int, default=2, help="VLM workgroups per CU for wg_capped")
     ap.add_argument("--kernel", default="ex.gateup", help="tag of the kernel timed for the roofline")
@@ -229,7 +230,11 @@ def main():
           "lanes4_graph": dict(mode="concurrent", act_streams=4, graphs=True),
           "v2_lanes2_graph": dict(mode="concurrent", vlm_streams=2, act_streams=2, graphs=True),
           "v2_lanes3_graph": dict(mode="concurrent", vlm_streams=2, act_streams=3, graphs=True),
-          "v2_lanes4_graph": dict(mode="concurrent", vlm_streams=2, act_streams=4, graphs=True)}
+          "v2_lanes4_graph": dict(mode="concurrent", vlm_streams=2, act_streams=4, graphs=True),
+          # two robots' action phases as one loop that reads the weights once
+          "batch2_graph": dict(mode="concurrent", act_batch=2, graphs=True),
+          "batch2_lanes2_graph": dict(mode="concurrent", act_batch=2, act_streams=2, graphs=True),
+          "batch2_v2_graph": dict(mode="concurrent", act_batch=2, vlm_streams=2, graphs=True)}
     for a_, b_ in ((224, 32), (192, 64), (160, 96)):  # CU-split sweep entries
         kw[f"cu_{a_}_{b_}"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_)
         kw[f"cu_{a_}_{b_}_lanes2"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_, act_streams=2, graphs=True)

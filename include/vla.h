@@ -104,7 +104,12 @@ typedef struct vla_sched {
   int32_t vlm_streams;/* VLM streams (0 or 1: one; at most 2). With 2, the prefills  */
                       /*   of consecutive frames alternate between two streams and   */
                       /*   may overlap each other; not with VLA_MODE_SERIAL          */
-  int32_t reserved;
+  int32_t act_batch;  /* frames per action phase (0 or 1: one; at most 2). With 2,   */
+                      /*   the action phases of two consecutive frames (different    */
+                      /*   robots) run as one denoising loop that reads the weights  */
+                      /*   once for both; it starts when both prefills are done. A   */
+                      /*   final odd frame runs alone. Every frame's chunk is bit    */
+                      /*   identical to its own run. VLA_HEAD_PI0 models only.       */
 } vla_sched;
 
 typedef struct vla_timing {

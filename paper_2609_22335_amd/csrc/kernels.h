@@ -82,6 +82,13 @@ inline size_t afrag_elems(int dtype, int K) {
   const int sw = 4 * kv_vec(dtype);
   return (size_t)((K + sw - 1) / sw) * sw * 64;
 }
+// Frame blocks: an operand of several frames' rows (a batched action phase)
+// holds each frame's blk_rows rows (<= 64) in its own row-block layout,
+// blk_elems elements apart; blk_rows == 0 means one block (m < 64).
+__host__ __device__ inline size_t afrag_index_blk(int dtype, int m, int k, int blk_rows, size_t blk_elems) {
+  if (blk_rows <= 0) return afrag_index(dtype, m, k);
+  return (size_t)(m / blk_rows) * blk_elems + afrag_index(dtype, m % blk_rows, k);
+}
 
 struct Epi {
   int kind = EPI_F32;
@@ -110,6 +117,13 @@ struct Epi {
   void* xop = nullptr;
   int ldxop = 0;
   float dt = 0.f;
+  // Frame blocks (batched action phase): with blk_rows > 0, row m is row
+  // m % blk_rows of frame m / blk_rows. Row-block-layout outputs (out, xop)
+  // of frame b start b * blk_out elements in (see afrag_index_blk), its own
+  // K / V b * blk_k / b * blk_v elements in, with that frame's rows as keys
+  // and RoPE positions pos0 + m % blk_rows. Row-major outputs use row m.
+  int blk_rows = 0;
+  size_t blk_out = 0, blk_xop = 0, blk_k = 0, blk_v = 0;
 };
 
 struct GemmDesc {
@@ -126,6 +140,12 @@ struct GemmDesc {
   // (afrag_index) and lda is unused.
   int frag_ks = 0;
   int frag_ks0 = 0;
+  // Skinny kernel only: `frames` row blocks of M rows each (a batched action
+  // phase), block f of A at A + f * a_blk elements; the weights are loaded
+  // once for all of them and every row is computed exactly as in a
+  // one-frame call. The epilogue sees rows f * M + m (Epi::blk_rows = M).
+  int frames = 1;
+  size_t a_blk = 0;
 };
 
 // Offset of element (n, k) of a weight stored in MFMA fragment order with KS
@@ -196,6 +216,13 @@ struct AttnKvDesc {
   int ldo;
   int out_afrag;  // out in the row-block operand layout (Sq <= 64), ldo unused
   int Sq, nq, nkv, hd;
+  // Several frames in one launch (batched action phase): frame f has queries
+  // q + f Sq ldq, keys [k0f[f] (S0); k1 + f k1_blk (S1)] (values alike) and
+  // output out + f out_blk; frame 0 uses k0 / v0.
+  int frames = 1;
+  const void* k0f[2] = {nullptr, nullptr};
+  const void* v0f[2] = {nullptr, nullptr};
+  size_t k1_blk = 0, v1_blk = 0, out_blk = 0;
 };
 hipError_t launch_attention_kv(const AttnKvDesc& d, const LaunchCaps& caps, hipStream_t st);
 hipError_t launch_attention(const AttnDesc& a, const Scratch& s, const LaunchCaps& caps, hipStream_t st);
@@ -204,7 +231,7 @@ hipError_t launch_attention(const AttnDesc& a, const Scratch& s, const LaunchCap
 // order; nothing is added when splits is 0, colscale NULL means 1), stored
 // back, then out[m] = LayerNorm (biased variance) or RMSNorm of x[m], times
 // gain (g, or 1 + g when g_plus_one) plus b, in the operand type: row-major
-// with ldo, the row-block operand layout (afrag, rows <= 64), or pixel
+// with ldo, the row-block operand layout (afrag, rows <= 64 per frame block), or pixel
 // shuffled (shuffle > 1: row = view * tview + y * grid_w + x of a raster
 // patch grid goes to coarse row view * tview / s^2 + (y / s) * (grid_w / s)
 // + x / s, columns offset by ((y % s) * s + x % s) * d; ldo = s^2 d).
@@ -225,6 +252,8 @@ struct NormDesc {
   int ldo = 0;
   int afrag = 0;
   int shuffle = 1, grid_w = 0, tview = 0;
+  int blk_rows = 0;     // afrag output in frame blocks (afrag_index_blk)
+  size_t blk_out = 0;
 };
 hipError_t launch_norm(const NormDesc& n, hipStream_t st);
 
@@ -239,10 +268,12 @@ hipError_t launch_embed(int dtype, const void* E, int d, int vocab, const int32_
                         float scale, float* x, int ldx, hipStream_t st);
 
 // dst_T[r, c] = T(src[r, c]) for c < cols, 0 for cols <= c < ld_dst (row-major
-// with ld_dst, or the row-block operand layout with K = ld_dst when afrag);
+// with ld_dst, or the row-block operand layout with K = ld_dst when afrag,
+// in frame blocks of blk_rows rows blk_elems apart when blk_rows > 0);
 // optionally also copies src into dst_f32 (fp32, ld = cols).
 hipError_t launch_cvt_pad(int dtype, const float* src, int rows, int cols, void* dst, int ld_dst,
-                          bool afrag, float* dst_f32, hipStream_t st);
+                          bool afrag, float* dst_f32, hipStream_t st, int blk_rows = 0,
+                          size_t blk_elems = 0);
 
 // dst[r, :] = row (operand type) for every r < rows.
 hipError_t launch_bcast_row(int dtype, const void* row, int cols, void* dst, int ld_dst, int rows,

@@ -138,6 +138,10 @@ __device__ __forceinline__ size_t span(int rows, size_t ld, int len, size_t esz)
 __device__ __forceinline__ uint4 bld16(Rsrc r, uint32_t off) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
 }
+// the same with a wave-uniform byte offset added (in a scalar register)
+__device__ __forceinline__ uint4 bld16s(Rsrc r, uint32_t off, uint32_t soff) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, soff, 0));
+}
 __device__ __forceinline__ float bld1(Rsrc r, uint32_t off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
@@ -148,9 +152,14 @@ __device__ __forceinline__ float bld1(Rsrc r, uint32_t off) {
 
 // Index of output element (m, n) of an operand-type epilogue output.
 template <typename T>
-__device__ __forceinline__ size_t out_at(const Epi& e, int m, int n, int ld) {
+__device__ __forceinline__ size_t out_at(const Epi& e, int m, int n, int ld, size_t blk) {
   constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
-  return e.afrag ? afrag_index(DT, m, n) : (size_t)m * ld + n;
+  return e.afrag ? afrag_index_blk(DT, m, n, e.blk_rows, blk) : (size_t)m * ld + n;
+}
+// key index and element offset of row m's own K / V (frame blocks)
+__device__ __forceinline__ int epi_key(const Epi& e, int m) { return e.blk_rows > 0 ? m % e.blk_rows : m; }
+__device__ __forceinline__ size_t epi_kblk(const Epi& e, int m, size_t blk) {
+  return e.blk_rows > 0 ? (size_t)(m / e.blk_rows) * blk : 0;
 }
 
 template <typename T>
@@ -164,7 +173,7 @@ __device__ __forceinline__ void epi_one(const Epi& e, int m, int n, float v) {
     }
     case EPI_T: {
       if (e.bias) v += e.bias[n];
-      TT<T>::st((T*)e.out + out_at<T>(e, m, n, e.ldo), v);
+      TT<T>::st((T*)e.out + out_at<T>(e, m, n, e.ldo, e.blk_out), v);
       break;
     }
     case EPI_RESID: {
@@ -174,12 +183,12 @@ __device__ __forceinline__ void epi_one(const Epi& e, int m, int n, float v) {
     }
     case EPI_GELU: {
       if (e.bias) v += e.bias[n];
-      TT<T>::st((T*)e.out + out_at<T>(e, m, n, e.ldo), gelu_tanh(v));
+      TT<T>::st((T*)e.out + out_at<T>(e, m, n, e.ldo, e.blk_out), gelu_tanh(v));
       break;
     }
     case EPI_SWISH: {
       if (e.bias) v += e.bias[n];
-      TT<T>::st((T*)e.out + out_at<T>(e, m, n, e.ldo), swishf(v));
+      TT<T>::st((T*)e.out + out_at<T>(e, m, n, e.ldo, e.blk_out), swishf(v));
       break;
     }
     case EPI_QKV_PLAIN: {
@@ -189,10 +198,10 @@ __device__ __forceinline__ void epi_one(const Epi& e, int m, int n, float v) {
         TT<T>::st((T*)e.q + (size_t)m * e.ldq + n, v);
       } else if (n < qcols + kcols) {
         const int c = n - qcols;
-        TT<T>::st((T*)e.k + kv_kidx(DT, e.kv_nb, e.hd, c / e.hd, m, c % e.hd), v);
+        TT<T>::st((T*)e.k + epi_kblk(e, m, e.blk_k) + kv_kidx(DT, e.kv_nb, e.hd, c / e.hd, epi_key(e, m), c % e.hd), v);
       } else {
         const int c = n - qcols - kcols;
-        TT<T>::st((T*)e.v + kv_vidx(DT, e.kv_nb, e.hd, c / e.hd, m, c % e.hd), v);
+        TT<T>::st((T*)e.v + epi_kblk(e, m, e.blk_v) + kv_vidx(DT, e.kv_nb, e.hd, c / e.hd, epi_key(e, m), c % e.hd), v);
       }
       break;
     }
@@ -201,7 +210,7 @@ __device__ __forceinline__ void epi_one(const Epi& e, int m, int n, float v) {
       float* xp = e.x + (size_t)m * e.ldx + n;
       const float xn = *xp + e.dt * v;
       *xp = xn;
-      TT<T>::st((T*)e.xop + out_at<T>(e, m, n, e.ldxop), xn);
+      TT<T>::st((T*)e.xop + out_at<T>(e, m, n, e.ldxop, e.blk_xop), xn);
       break;
     }
     default:
@@ -217,7 +226,7 @@ __device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int 
   if (e.kind == EPI_GEGLU) {
     if (n + 16 >= N) return;
     const int g = n >> 5, j = n & 15;
-    TT<T>::st((T*)e.out + out_at<T>(e, m, 16 * g + j, e.ldo), gelu_tanh(v0) * v1);
+    TT<T>::st((T*)e.out + out_at<T>(e, m, 16 * g + j, e.ldo, e.blk_out), gelu_tanh(v0) * v1);
     return;
   }
   if (e.kind == EPI_QKV_ROPE) {
@@ -228,7 +237,8 @@ __device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int 
       const int rn = isq ? n : n - qcols;
       const int head = rn / hd, p = rn - head * hd;
       const int i = 16 * (p >> 5) + (p & 15);  // rotate-half pair (i, i + hd/2)
-      const size_t t = (size_t)(e.pos0 + m) * (hd / 2) + i;
+      const int key = epi_key(e, m);
+      const size_t t = (size_t)(e.pos0 + key) * (hd / 2) + i;
       const float c = e.rope_cos[t], s = e.rope_sin[t];
       if (isq) {
         T* dst = (T*)e.q + (size_t)m * e.ldq + head * hd;
@@ -236,16 +246,16 @@ __device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int 
         TT<T>::st(dst + i + hd / 2, v1 * c + v0 * s);
       } else {
         constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
-        T* dst = (T*)e.k;
-        TT<T>::st(dst + kv_kidx(DT, e.kv_nb, hd, head, m, i), v0 * c - v1 * s);
-        TT<T>::st(dst + kv_kidx(DT, e.kv_nb, hd, head, m, i + hd / 2), v1 * c + v0 * s);
+        T* dst = (T*)e.k + epi_kblk(e, m, e.blk_k);
+        TT<T>::st(dst + kv_kidx(DT, e.kv_nb, hd, head, key, i), v0 * c - v1 * s);
+        TT<T>::st(dst + kv_kidx(DT, e.kv_nb, hd, head, key, i + hd / 2), v1 * c + v0 * s);
       }
     } else {
       constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
-      const int c0 = n - qcols - kcols, c1 = c0 + 16;
-      T* dst = (T*)e.v;
-      TT<T>::st(dst + kv_vidx(DT, e.kv_nb, hd, c0 / hd, m, c0 % hd), v0);
-      TT<T>::st(dst + kv_vidx(DT, e.kv_nb, hd, c1 / hd, m, c1 % hd), v1);
+      const int c0 = n - qcols - kcols, c1 = c0 + 16, key = epi_key(e, m);
+      T* dst = (T*)e.v + epi_kblk(e, m, e.blk_v);
+      TT<T>::st(dst + kv_vidx(DT, e.kv_nb, hd, c0 / hd, key, c0 % hd), v0);
+      TT<T>::st(dst + kv_vidx(DT, e.kv_nb, hd, c1 / hd, key, c1 % hd), v1);
     }
     return;
   }
@@ -486,8 +496,14 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__
 // epilogues go through the split-K reduce kernel.
 // ---------------------------------------------------------------------------
 
+// Frames (a batched action phase): `frames` row blocks of M rows, block f of
+// A at A + f a_blk elements. Every (column pair, K-range) tile is computed
+// once per frame by its own workgroup, exactly as in a one-frame call; the
+// frames of a tile are consecutive tile indices, and with the XCD-aware
+// order below they run on one XCD at the same time, so the weights come
+// from HBM once and from that XCD's L2 for the other frame.
 template <typename T, int SPW>
-__global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, int lda,
+__global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, size_t a_blk, int frames,
                                                 const T* __restrict__ Wf, int KS, int ks0, int M,
                                                 int N, int K, int splits, Epi e,
                                                 float* __restrict__ part) {
@@ -498,13 +514,20 @@ __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, int lda
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int npairs = (N + 31) / 32;
   const int nslab = (K + SW - 1) / SW;
-  const int total = npairs * splits;
+  const int total = npairs * splits * frames;
+  const int Mt = M * frames;  // rows of all frames
   const T dummy = T();
   const Rsrc rw = rsrc(Wf, (size_t)npairs * 2 * KS * 64 * VEC * sizeof(T));
-  const Rsrc ra = rsrc(A, (size_t)nslab * 4 * 64 * VEC * sizeof(T));  // row-block operand layout
-  for (int w = blockIdx.x; w < total; w += gridDim.x) {
-    const int s = w % splits, np = w / splits;
+  // row-block operand layout, one block per frame
+  const Rsrc ra = rsrc(A, ((size_t)(frames - 1) * a_blk + (size_t)nslab * 4 * 64 * VEC) * sizeof(T));
+  const int G = gridDim.x;
+  const int first = frames > 1 && G % 8 == 0 ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8)
+                                             : (int)blockIdx.x;
+  for (int w = first; w < total; w += G) {
+    const int f = w % frames, wt = w / frames;
+    const int s = wt % splits, np = wt / splits;
     const int sb = (s * 4 + wave) * SPW;
+    const uint32_t aoff = (uint32_t)((size_t)f * a_blk * sizeof(T));  // frame f's block
     uint4 bf[SPW][2], af[SPW][4];
 #pragma unroll
     for (int q = 0; q < SPW; ++q) {
@@ -519,7 +542,7 @@ __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, int lda
       for (int mt = 0; mt < 4; ++mt) {
         const int row = mt * 16 + (lane & 15);
         const bool oka = ok && row < M && k < K;
-        af[q][mt] = bld16(ra, oka ? (uint32_t)((((size_t)ks * 4 + mt) * 64 + lane) * VEC * sizeof(T)) : OOB);
+        af[q][mt] = bld16s(ra, oka ? (uint32_t)((((size_t)ks * 4 + mt) * 64 + lane) * VEC * sizeof(T)) : OOB, aoff);
       }
     }
     f32x4 acc[2][4];
@@ -554,10 +577,11 @@ __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, int lda
       const int m = mt * 16 + (lane >> 4) * 4 + r;
       const int n = np * 32 + (lane & 15);
       if (m >= M) continue;
+      const int mg = f * M + m;  // row over all frames
       if (splits == 1 && e.kind != EPI_PART) {
-        epi_pair<T>(e, M, N, m, n, v[0], v[1]);
+        epi_pair<T>(e, Mt, N, mg, n, v[0], v[1]);
       } else {
-        float* P = (e.kind == EPI_PART ? (float*)e.out : part) + (size_t)s * M * N + (size_t)m * N;
+        float* P = (e.kind == EPI_PART ? (float*)e.out : part) + (size_t)s * Mt * N + (size_t)mg * N;
         if (n < N) P[n] = v[0];
         if (n + 16 < N) P[n + 16] = v[1];
       }
@@ -586,25 +610,28 @@ int skinny_splits(const GemmDesc& g) {
 template <typename T, int SPW>
 static hipError_t run_skinny_t(const GemmDesc& g, int splits, const Scratch& s,
                                const LaunchCaps& caps, hipStream_t st) {
-  int grid = ((g.N + 31) / 32) * splits;
+  int grid = ((g.N + 31) / 32) * splits * g.frames;
   if (caps.max_wgs > 0) grid = std::min(grid, caps.max_wgs);
   hipExtLaunchKernelGGL((k_skinny<T, SPW>), dim3(grid), dim3(256), 0, st, caps.ev_start,
-                        caps.ev_stop, 0, (const T*)g.A, g.lda, (const T*)g.W, g.frag_ks,
+                        caps.ev_stop, 0, (const T*)g.A, g.a_blk, g.frames, (const T*)g.W, g.frag_ks,
                         g.frag_ks0, g.M, g.N, g.K, splits, g.epi, s.ptr);
   if (splits > 1 && g.epi.kind != EPI_PART) {
-    const long long total = (long long)g.M * ((g.N + 31) / 32) * 16;
+    const int Mt = g.M * g.frames;
+    const long long total = (long long)Mt * ((g.N + 31) / 32) * 16;
     int rgrid = (int)std::min<long long>((total + 255) / 256, 4096);
     if (caps.max_wgs > 0) rgrid = std::min(rgrid, caps.max_wgs);
-    k_splitk_reduce<T><<<rgrid, 256, 0, st>>>(s.ptr, splits, g.M, g.N, g.epi);
+    k_splitk_reduce<T><<<rgrid, 256, 0, st>>>(s.ptr, splits, Mt, g.N, g.epi);
   }
   return hipGetLastError();
 }
 
 static hipError_t launch_skinny(const GemmDesc& g, const Scratch& s, const LaunchCaps& caps,
                                 hipStream_t st) {
-  if (g.M > 64) return hipErrorInvalidValue;
+  if (g.M > 64 || g.frames < 1 || g.frames > 2 ||
+      (g.frames > 1 && (g.epi.blk_rows != g.M || g.a_blk < afrag_elems(g.dtype, g.K))))
+    return hipErrorInvalidValue;
   const int splits = skinny_splits(g);
-  const size_t need = (size_t)splits * g.M * g.N;
+  const size_t need = (size_t)splits * g.M * g.frames * g.N;
   if (g.epi.kind == EPI_PART) {
     if (!g.epi.out || need > (size_t)g.epi.ldo) return hipErrorInvalidValue;
   } else if (splits > 1 && need > s.floats) {
@@ -632,8 +659,8 @@ GemmPlan plan_gemm(const GemmDesc& g) {
   if (g.frag_ks > 0) {  // fragment-ordered weights: skinny kernel
     p.cfg = -1;
     p.splits = skinny_splits(g);
-    p.tiles = ((g.N + 31) / 32) * p.splits;
-    p.scratch_floats = (p.splits > 1 || g.epi.kind == EPI_PART) ? (size_t)p.splits * g.M * g.N : 0;
+    p.tiles = ((g.N + 31) / 32) * p.splits * g.frames;
+    p.scratch_floats = (p.splits > 1 || g.epi.kind == EPI_PART) ? (size_t)p.splits * g.M * g.frames * g.N : 0;
     return p;
   }
   const TileCfg* cfgs = g.dtype == DT_BF16 ? kBf16Cfg : kF32Cfg;
@@ -1110,11 +1137,13 @@ hipError_t launch_attention(const AttnDesc& d, const Scratch& s, const LaunchCap
 
 struct Attn2Args {
   const void* q;
-  const void* k0;
-  const void* v0;
-  const void* k1;
+  const void* k0[2];  // per frame
+  const void* v0[2];
+  const void* k1;     // frame f: k1 + f k1_blk (elements)
   const void* v1;
-  void* out;
+  void* out;          // frame f: out + f out_blk
+  size_t k1_blk, v1_blk, out_blk;
+  int frames;
   int ldq, ldo, out_afrag;
   int Sq, nq, nkv, hd, S0, S1;
   int nb0, nb1;  // 32-key blocks per KV head in each segment's buffers
@@ -1155,14 +1184,18 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
   const int total = a.rtiles * a.nkv;
   const int ns = (a.hd + SW - 1) / SW, ndt = (a.hd + 15) / 16;
   const T dummy = T();
-  const Rsrc rq = rsrc(a.q, span(a.Sq, a.ldq, a.nq * a.hd, sizeof(T)));
-  const Rsrc rk0 = rsrc(a.k0, (size_t)a.nkv * a.nb0 * 2 * ns * FRAG * sizeof(T));
-  const Rsrc rv0 = rsrc(a.v0, (size_t)a.nkv * a.nb0 * ndt * PVS * FRAG * sizeof(T));
-  const Rsrc rk1 = rsrc(a.k1 ? a.k1 : a.k0, a.k1 ? (size_t)a.nkv * a.nb1 * 2 * ns * FRAG * sizeof(T) : 0);
-  const Rsrc rv1 = rsrc(a.v1 ? a.v1 : a.v0, a.v1 ? (size_t)a.nkv * a.nb1 * ndt * PVS * FRAG * sizeof(T) : 0);
+  const Rsrc rq = rsrc(a.q, span(a.Sq * a.frames, a.ldq, a.nq * a.hd, sizeof(T)));
 
-  for (int w = blockIdx.x; w < total; w += gridDim.x) {
-    const int rt = w % a.rtiles, j = w / a.rtiles;
+  for (int w = blockIdx.x; w < total * a.frames; w += gridDim.x) {
+    // frame f: its queries, its two key segments and its output block
+    const int f = __builtin_amdgcn_readfirstlane(w / total), wl = w % total;
+    const int rt = wl % a.rtiles, j = wl / a.rtiles;
+    const Rsrc rk0 = rsrc(a.k0[f], (size_t)a.nkv * a.nb0 * 2 * ns * FRAG * sizeof(T));
+    const Rsrc rv0 = rsrc(a.v0[f], (size_t)a.nkv * a.nb0 * ndt * PVS * FRAG * sizeof(T));
+    const Rsrc rk1 = rsrc(a.k1 ? (const T*)a.k1 + f * a.k1_blk : a.k0[f],
+                          a.k1 ? (size_t)a.nkv * a.nb1 * 2 * ns * FRAG * sizeof(T) : 0);
+    const Rsrc rv1 = rsrc(a.v1 ? (const T*)a.v1 + f * a.v1_blk : a.v0[f],
+                          a.v1 ? (size_t)a.nkv * a.nb1 * ndt * PVS * FRAG * sizeof(T) : 0);
 
     // the workgroup's 16 packed query rows, row-contiguous loads (issued
     // before K and V so that waiting for them does not wait for K and V)
@@ -1173,7 +1206,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
       const int c = tid + u * NT;
       const int rr = c / (HDP / VEC), d = (c % (HDP / VEC)) * VEC;
       const int r = rt * 16 + rr;
-      const int sq = r / group, h = j * group + r % group;
+      const int sq = f * a.Sq + r / group, h = j * group + r % group;
       const bool ok = c < QCH && r < R && d < a.hd;
       qld[u] = bld16(rq, ok ? (uint32_t)(((size_t)sq * a.ldq + h * a.hd + d) * sizeof(T)) : OOB);
     }
@@ -1346,7 +1379,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
       // 16-byte pieces: one VEC group each in the row-block operand layout
       auto at = [&](int c) {
         constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
-        return (T*)a.out + (a.out_afrag ? afrag_index(DT, sq, c) : (size_t)sq * a.ldo + c);
+        return (T*)a.out + f * a.out_blk + (a.out_afrag ? afrag_index(DT, sq, c) : (size_t)sq * a.ldo + c);
       };
       if constexpr (sizeof(T) == 2) {
         uint32_t pk[4];
@@ -1366,7 +1399,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
 template <typename T>
 static hipError_t run_attn2_t(const Attn2Args& a, int hdp, const LaunchCaps& caps, hipStream_t st) {
   if (sizeof(T) == 4 && hdp > 128) return hipErrorInvalidValue;  // fp32: head dim <= 128
-  int grid = a.rtiles * a.nkv;
+  int grid = a.rtiles * a.nkv * a.frames;
   if (caps.max_wgs > 0) grid = std::min(grid, caps.max_wgs);
 #define VLA_ATTN2(H)                                                                           \
   hipExtLaunchKernelGGL((k_attn2<T, H, att2_waves<T, H>()>), dim3(grid),                        \
@@ -1390,14 +1423,21 @@ hipError_t launch_attention_kv(const AttnKvDesc& d, const LaunchCaps& caps, hipS
   if (hdp < 0 || d.nq % d.nkv != 0 || d.S0 <= 0 || d.S1 < 0 || d.Sq <= 0 ||
       (d.S1 > 0 && (!d.k1 || !d.v1)) || d.hd % 8 != 0 || (d.out_afrag && d.Sq > 64) ||
       (!d.out_afrag && ((size_t)d.ldo * (d.dtype == DT_BF16 ? 2 : 4)) % 16 != 0) ||
-      ((uintptr_t)d.out & 15) != 0)
+      ((uintptr_t)d.out & 15) != 0 || d.frames < 1 || d.frames > 2 ||
+      (d.frames > 1 && (!d.k0f[1] || !d.v0f[1] || (d.out_blk * (d.dtype == DT_BF16 ? 2 : 4)) % 16 != 0)))
     return hipErrorInvalidValue;
   Attn2Args a{};
   a.q = d.q;
-  a.k0 = d.k0;
-  a.v0 = d.v0;
+  a.k0[0] = d.k0;
+  a.v0[0] = d.v0;
+  a.k0[1] = d.frames > 1 ? d.k0f[1] : d.k0;
+  a.v0[1] = d.frames > 1 ? d.v0f[1] : d.v0;
   a.k1 = d.S1 > 0 ? d.k1 : nullptr;
   a.v1 = d.S1 > 0 ? d.v1 : nullptr;
+  a.k1_blk = d.k1_blk;
+  a.v1_blk = d.v1_blk;
+  a.out_blk = d.out_blk;
+  a.frames = d.frames;
   a.out = d.out;
   a.ldq = d.ldq;
   a.ldo = d.ldo;
@@ -1536,7 +1576,7 @@ __global__ __launch_bounds__(256) void k_norm(NormDesc n) {
         f32x4 y = (v[q] - mean) * inv * gi;
         if (n.b) y += sh[q];
         // four consecutive columns are contiguous in both output layouts
-        T* dst = (T*)n.out + (n.afrag ? afrag_index(DT, row, c) : obase + c);
+        T* dst = (T*)n.out + (n.afrag ? afrag_index_blk(DT, row, c, n.blk_rows, n.blk_out) : obase + c);
         if constexpr (sizeof(T) == 2)
           *(uint2*)dst = make_uint2(f2bf2(y[0], y[1]), f2bf2(y[2], y[3]));
         else
@@ -1554,7 +1594,7 @@ hipError_t launch_norm(const NormDesc& n, hipStream_t st) {
       mis(n.g, 16) || mis(n.b, 16) || mis(n.out, n.dtype == DT_BF16 ? 8 : 16))
     return hipErrorInvalidValue;
   if (n.d > 1024 * NORM_VPT || n.d % 4 || n.ldx % 4 || (!n.afrag && n.ldo % 4) ||
-      (n.afrag && n.rows > 64) || !n.x || !n.g || !n.out ||
+      (n.afrag && (n.blk_rows > 0 ? n.blk_rows > 64 : n.rows > 64)) || !n.x || !n.g || !n.out ||
       (n.shuffle > 1 && (n.grid_w % n.shuffle || n.tview % (n.shuffle * n.grid_w) || n.afrag)))
     return hipErrorInvalidValue;
   const int grid = std::min(n.rows, 4096);
@@ -1627,7 +1667,7 @@ hipError_t launch_embed(int dtype, const void* E, int d, int vocab, const int32_
 
 template <typename T>
 __global__ void k_cvt_pad(const float* __restrict__ src, int rows, int cols, T* __restrict__ dst,
-                          int ld, int afrag, float* __restrict__ dst32) {
+                          int ld, int afrag, float* __restrict__ dst32, int blk_rows, size_t blk_elems) {
   VLA_WAVE_BEGIN(KK_CVT);
   constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
   const long long total = (long long)rows * ld;
@@ -1636,21 +1676,23 @@ __global__ void k_cvt_pad(const float* __restrict__ src, int rows, int cols, T* 
     const int c = (int)(idx % ld);
     const long long r = idx / ld;
     const float v = c < cols ? src[r * cols + c] : 0.f;
-    TT<T>::st(dst + (afrag ? afrag_index(DT, (int)r, c) : (size_t)idx), v);
+    TT<T>::st(dst + (afrag ? afrag_index_blk(DT, (int)r, c, blk_rows, blk_elems) : (size_t)idx), v);
     if (dst32 && c < cols) dst32[r * cols + c] = v;
   }
   VLA_WAVE_END(KK_CVT);
 }
 
 hipError_t launch_cvt_pad(int dtype, const float* src, int rows, int cols, void* dst, int ld_dst,
-                          bool afrag, float* dst_f32, hipStream_t st) {
-  if (afrag && rows > 64) return hipErrorInvalidValue;
+                          bool afrag, float* dst_f32, hipStream_t st, int blk_rows, size_t blk_elems) {
+  if (afrag && (blk_rows > 0 ? blk_rows > 64 : rows > 64)) return hipErrorInvalidValue;
   const long long total = (long long)rows * ld_dst;
   const int grid = (int)std::min<long long>((total + 255) / 256, 1024);
   if (dtype == DT_BF16)
-    k_cvt_pad<uint16_t><<<grid, 256, 0, st>>>(src, rows, cols, (uint16_t*)dst, ld_dst, afrag, dst_f32);
+    k_cvt_pad<uint16_t><<<grid, 256, 0, st>>>(src, rows, cols, (uint16_t*)dst, ld_dst, afrag, dst_f32,
+                                              blk_rows, blk_elems);
   else
-    k_cvt_pad<float><<<grid, 256, 0, st>>>(src, rows, cols, (float*)dst, ld_dst, afrag, dst_f32);
+    k_cvt_pad<float><<<grid, 256, 0, st>>>(src, rows, cols, (float*)dst, ld_dst, afrag, dst_f32,
+                                           blk_rows, blk_elems);
   return hipGetLastError();
 }
 

@@ -214,6 +214,7 @@ struct DitLayer {
 constexpr int MAX_ACT_STREAMS = 4;
 
 constexpr int MAX_VLM_STREAMS = 2;
+constexpr int MAX_ACT_BATCH = 2;  // frames one action phase can run together
 
 struct Streams {
   hipStream_t v[MAX_VLM_STREAMS] = {};
@@ -232,12 +233,16 @@ struct VlmWs {
 };
 
 // Scratch of one action lane (one denoise at a time per lane).
+// Action-phase workspace, sized for MAX_ACT_BATCH frames: row-major buffers
+// hold the frames' rows one after another; row-block-layout operands hold
+// one block per frame, the blk_* elements apart.
 struct ActWs {
   float* u = nullptr;
   void *xop = nullptr, *a = nullptr, *hid = nullptr, *h = nullptr, *q = nullptr;
   void *kown = nullptr, *vown = nullptr, *att = nullptr, *mlp = nullptr;
-  float* xg = nullptr;      // chunk written by graph replays, copied out afterwards
+  float* xg = nullptr;      // chunks written by graph replays, copied out afterwards
   float* nstage = nullptr;  // noise staged for graph replays
+  size_t blk_xop = 0, blk_de = 0, blk_att = 0, blk_mlp = 0, blk_k = 0, blk_v = 0;
   Scratch scr;
 };
 
@@ -302,7 +307,7 @@ struct vla_model {
   // graph replay: frame inputs staged into fixed buffers, graphs cached per
   // (context, VLM grid cap) and (action lane, context)
   std::map<std::tuple<int, int, int>, hipGraphExec_t> pre_graphs;  // (VLM lane, context, WG cap)
-  std::map<std::pair<int, int>, hipGraphExec_t> den_graphs;
+  std::map<std::tuple<int, int, int>, hipGraphExec_t> den_graphs;  // (lane, first context, frames)
   std::mutex mu;
 
   // per-tag kernel timer: every launch whose tag matches is bracketed by
@@ -546,9 +551,16 @@ static int timer_events(const Run& r, const char* tag, LaunchCaps* caps) {
   return VLA_OK;
 }
 
+// Frames of a batched action phase: `n` frames of M rows; the A operand's
+// per-frame blocks are a_blk elements apart.
+struct Frames {
+  int n = 1;
+  size_t a_blk = 0;
+};
+
 // C = A W[:, koff : koff + K]^T with the epilogue e; W is a weight tensor id.
 static GemmDesc gemm_desc(vla_model* m, const void* A, int lda, int W, int M, int N, int K,
-                          const Epi& e, int koff = 0) {
+                          const Epi& e, int koff = 0, Frames fr = Frames()) {
   const DevTensor& t = m->T[W];
   GemmDesc g{m->dt, A, lda, m->tptr(W), t.ld, M, N, K, e};
   if (t.fks > 0) {
@@ -557,13 +569,15 @@ static GemmDesc gemm_desc(vla_model* m, const void* A, int lda, int W, int M, in
   } else {
     g.W = m->tptr(W) + (size_t)koff * m->esz;
   }
+  g.frames = fr.n;
+  g.a_blk = fr.a_blk;
   return g;
 }
 
 static int gemm(const Run& r, const char* tag, const void* A, int lda, int W, int M, int N, int K,
-                const Epi& e, int koff = 0) {
+                const Epi& e, int koff = 0, Frames fr = Frames()) {
   vla_model* m = r.m;
-  const GemmDesc g = gemm_desc(m, A, lda, W, M, N, K, e, koff);
+  const GemmDesc g = gemm_desc(m, A, lda, W, M, N, K, e, koff, fr);
   LaunchCaps caps = r.caps;
   VLA_TRY(timer_events(r, tag, &caps));
   hipError_t err = launch_gemm(g, *r.scr, caps, r.st);
@@ -602,8 +616,10 @@ static int run_norm(const Run& r, NormDesc n) {
 // out: row-major [rows][d], or the row-block operand layout when it feeds a
 // skinny GEMM (afrag)
 static int norm(const Run& r, float* x, int rows, int d, int splits, const float* bias, int g, int b,
-                bool rms, void* out, bool afrag = false) {
+                bool rms, void* out, bool afrag = false, int blk_rows = 0, size_t blk_out = 0) {
   NormDesc n;
+  n.blk_rows = blk_rows;
+  n.blk_out = blk_out;
   n.x = x;
   n.ldx = d;
   n.rows = rows;
@@ -622,14 +638,15 @@ static int norm(const Run& r, float* x, int rows, int d, int splits, const float
 // GEMM whose result is added to the residual stream by the next norm: the raw
 // result (or its split-K partials) goes to the phase scratch.
 static int gemm_part(const Run& r, const char* tag, const void* A, int lda, int W, int M, int N,
-                     int K, int* splits) {
+                     int K, int* splits, Frames fr = Frames()) {
   vla_model* m = r.m;
   Epi e;
   e.kind = EPI_PART;
   e.out = r.scr->ptr;
   e.ldo = (int)std::min<size_t>(r.scr->floats, (size_t)INT32_MAX);
-  *splits = plan_gemm(gemm_desc(m, A, lda, W, M, N, K, e)).splits;
-  return gemm(r, tag, A, lda, W, M, N, K, e);
+  if (fr.n > 1) e.blk_rows = M;
+  *splits = plan_gemm(gemm_desc(m, A, lda, W, M, N, K, e, 0, fr)).splits;
+  return gemm(r, tag, A, lda, W, M, N, K, e, 0, fr);
 }
 
 static Epi epi_kind(int kind, void* out = nullptr, int ldo = 0, const float* bias = nullptr) {
@@ -645,16 +662,24 @@ static Epi epi_kind(int kind, void* out = nullptr, int ldo = 0, const float* bia
 // partials) -> QKV (+RoPE, K/V stored) -> attention over [past; own] -> O ->
 // RMSNorm (after adding O) -> GeGLU -> down. The down projection is left
 // pending in the scratch (*pend = its split count) for the next norm.
+// Expert layers may run `frames` frames together (a batched action phase):
+// `rows` rows each, frame f reading the past K/V kpast[f] / vpast[f] and the
+// action workspace's per-frame blocks.
 static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int rows, int dim, int mlp,
-                         void* h, void* q, void* kout, void* vout, int pos0, const void* kpast,
-                         const void* vpast, int npast, void* att, void* mlpbuf, bool kv_only,
-                         int* pend) {
+                         void* h, void* q, void* kout, void* vout, int pos0, const void* const* kpast,
+                         const void* const* vpast, int npast, void* att, void* mlpbuf, bool kv_only,
+                         int* pend, int frames = 1) {
   vla_model* m = r.m;
   const vla_config& c = m->c;
   const Dims& d = m->d;
   // the expert's activations feed skinny GEMMs: row-block operand layout
   const bool af = !lm;
-  VLA_TRY(norm(r, x, rows, dim, *pend, nullptr, L.rms1, -1, true, h, af));
+  const bool fb = frames > 1;  // frame blocks
+  const ActWs* aw = r.aw;
+  if (fb && (lm || !aw)) return fail(VLA_EINVAL, "batched frames: expert layers only");
+  const int blk = fb ? rows : 0;
+  auto frm = [&](size_t a_blk) { Frames f; f.n = frames; f.a_blk = fb ? a_blk : 0; return f; };
+  VLA_TRY(norm(r, x, frames * rows, dim, *pend, nullptr, L.rms1, -1, true, h, af, blk, fb ? aw->blk_de : 0));
   *pend = 0;
   Epi e;
   e.kind = EPI_QKV_ROPE;
@@ -669,15 +694,20 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   e.pos0 = pos0;
   e.rope_cos = m->rope_cos;
   e.rope_sin = m->rope_sin;
-  VLA_TRY(gemm(r, lm ? "lm.qkv" : "ex.qkv", h, dim, L.qkv, rows, d.qkv_n, dim, e));
+  if (fb) {
+    e.blk_rows = rows;
+    e.blk_k = aw->blk_k;
+    e.blk_v = aw->blk_v;
+  }
+  VLA_TRY(gemm(r, lm ? "lm.qkv" : "ex.qkv", h, dim, L.qkv, rows, d.qkv_n, dim, e, 0, frm(fb ? aw->blk_de : 0)));
   if (kv_only) return VLA_OK;
   AttnKvDesc a{};
   a.dtype = m->dt;
   a.q = q;
   a.ldq = d.qd;
   if (kpast) {
-    a.k0 = kpast;
-    a.v0 = vpast;
+    a.k0 = kpast[0];
+    a.v0 = vpast[0];
     a.S0 = npast;
     a.k1 = kout;
     a.v1 = vout;
@@ -694,14 +724,28 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   a.nq = c.lm_heads;
   a.nkv = c.lm_kv_heads;
   a.hd = c.head_dim;
+  if (fb) {
+    if (!kpast) return fail(VLA_EINVAL, "batched frames need past K/V");
+    a.frames = frames;
+    a.k0f[1] = kpast[1];
+    a.v0f[1] = vpast[1];
+    a.k1_blk = aw->blk_k;
+    a.v1_blk = aw->blk_v;
+    a.out_blk = aw->blk_att;
+  }
   VLA_TRY(attn_kv(r, lm ? "lm.attn" : "ex.attn", a));
   int so = 0;
-  VLA_TRY(gemm_part(r, lm ? "lm.o" : "ex.o", att, d.qd, L.o, rows, dim, d.qd, &so));
-  VLA_TRY(norm(r, x, rows, dim, so, nullptr, L.rms2, -1, true, h, af));
+  VLA_TRY(gemm_part(r, lm ? "lm.o" : "ex.o", att, d.qd, L.o, rows, dim, d.qd, &so, frm(fb ? aw->blk_att : 0)));
+  VLA_TRY(norm(r, x, frames * rows, dim, so, nullptr, L.rms2, -1, true, h, af, blk, fb ? aw->blk_de : 0));
   Epi eg = epi_kind(EPI_GEGLU, mlpbuf, mlp);
   eg.afrag = af;
-  VLA_TRY(gemm(r, lm ? "lm.gateup" : "ex.gateup", h, dim, L.gu, rows, 2 * mlp, dim, eg));
-  VLA_TRY(gemm_part(r, lm ? "lm.down" : "ex.down", mlpbuf, mlp, L.down, rows, dim, mlp, pend));
+  if (fb) {
+    eg.blk_rows = rows;
+    eg.blk_out = aw->blk_mlp;
+  }
+  VLA_TRY(gemm(r, lm ? "lm.gateup" : "ex.gateup", h, dim, L.gu, rows, 2 * mlp, dim, eg, 0, frm(fb ? aw->blk_de : 0)));
+  VLA_TRY(gemm_part(r, lm ? "lm.down" : "ex.down", mlpbuf, mlp, L.down, rows, dim, mlp, pend,
+                    frm(fb ? aw->blk_mlp : 0)));
   return VLA_OK;
 }
 
@@ -911,35 +955,55 @@ static int run_denoise_dit(const Run& r, const vla_ctx* ctx, const float* noise,
   return VLA_OK;
 }
 
-static int run_denoise(const Run& r, const vla_ctx* ctx, const float* noise, float* x) {
+// The flow-matching loop of `frames` frames together (frames <= 2; noise
+// and x hold the frames' chunks one after another): the frames' rows share
+// every weight load, and each frame's result equals its own run bit for bit.
+static int run_denoise_n(const Run& r, const vla_ctx* const* ctxs, int frames, const float* noise, float* x) {
   vla_model* m = r.m;
-  if (m->c.head == VLA_HEAD_DIT) return run_denoise_dit(r, ctx, noise, x);
+  if (m->c.head == VLA_HEAD_DIT) {
+    if (frames != 1) return fail(VLA_EINVAL, "batched action phases: pi0-style head only");
+    return run_denoise_dit(r, ctxs[0], noise, x);
+  }
+  if (frames < 1 || frames > MAX_ACT_BATCH) return fail(VLA_EINVAL, "frames per action phase: 1 or 2");
   const vla_config& c = m->c;
   const Dims& d = m->d;
   ActWs& w = *r.aw;
   const int H = c.chunk_len, de = c.ex_dim, A = c.action_dim;
   const float dt = -1.0f / (float)c.n_steps;
+  const bool fb = frames > 1;
+  const int blk = fb ? H : 0;
+  auto frm = [&](size_t a_blk) { Frames f; f.n = frames; f.a_blk = fb ? a_blk : 0; return f; };
   // every operand of the expert's GEMMs is in the row-block operand layout
-  HIP_TRY(launch_cvt_pad(m->dt, noise, H, A, w.xop, d.a_pad, true, x, r.st));
+  HIP_TRY(launch_cvt_pad(m->dt, noise, frames * H, A, w.xop, d.a_pad, true, x, r.st, blk, w.blk_xop));
   const size_t layer_k = ctx_layer_k(m) * m->esz;
   const size_t layer_v = ctx_layer_v(m) * m->esz;
   for (int k = 0; k < c.n_steps; ++k) {
     // action embedding and time conditioning
     Epi ein = epi_kind(EPI_T, w.a, de, m->f32(m->in_b));
     ein.afrag = 1;
-    VLA_TRY(gemm(r, "ex.in", w.xop, d.a_pad, m->in_w, H, de, d.a_pad, ein));
+    ein.blk_rows = blk;
+    ein.blk_out = w.blk_de;
+    VLA_TRY(gemm(r, "ex.in", w.xop, d.a_pad, m->in_w, H, de, d.a_pad, ein, 0, frm(w.blk_xop)));
     Epi et1 = epi_kind(EPI_SWISH, w.hid, de, m->ck + (size_t)k * de);
     et1.afrag = 1;
-    VLA_TRY(gemm(r, "ex.time1", w.a, de, m->t1_w, H, de, de, et1));
-    VLA_TRY(gemm(r, "ex.time2", w.hid, de, m->t2_w, H, de, de, epi_kind(EPI_F32, w.u, de, m->f32(m->t2_b))));
+    et1.blk_rows = blk;
+    et1.blk_out = w.blk_de;
+    VLA_TRY(gemm(r, "ex.time1", w.a, de, m->t1_w, H, de, de, et1, 0, frm(w.blk_de)));
+    Epi et2 = epi_kind(EPI_F32, w.u, de, m->f32(m->t2_b));
+    et2.blk_rows = blk;
+    VLA_TRY(gemm(r, "ex.time2", w.hid, de, m->t2_w, H, de, de, et2, 0, frm(w.blk_de)));
     int pend = 0;
     for (int l = 0; l < c.ex_layers; ++l) {
-      const void* K = (const char*)ctx->K + l * layer_k;
-      const void* V = (const char*)ctx->V + l * layer_v;
+      const void* K[MAX_ACT_BATCH] = {nullptr, nullptr};
+      const void* V[MAX_ACT_BATCH] = {nullptr, nullptr};
+      for (int f = 0; f < frames; ++f) {
+        K[f] = (const char*)ctxs[f]->K + l * layer_k;
+        V[f] = (const char*)ctxs[f]->V + l * layer_v;
+      }
       VLA_TRY(decoder_layer(r, false, m->ex[l], w.u, H, de, c.ex_mlp, w.h, w.q, w.kown, w.vown, d.prefix,
-                            K, V, d.prefix, w.att, w.mlp, false, &pend));
+                            K, V, d.prefix, w.att, w.mlp, false, &pend, frames));
     }
-    VLA_TRY(norm(r, w.u, H, de, pend, nullptr, m->fin_g, -1, true, w.h, true));
+    VLA_TRY(norm(r, w.u, frames * H, de, pend, nullptr, m->fin_g, -1, true, w.h, true, blk, w.blk_de));
     Epi e;
     e.kind = EPI_EULER;
     e.afrag = 1;
@@ -949,9 +1013,15 @@ static int run_denoise(const Run& r, const vla_ctx* ctx, const float* noise, flo
     e.xop = w.xop;
     e.ldxop = d.a_pad;
     e.dt = dt;
-    VLA_TRY(gemm(r, "ex.out", w.h, de, m->out_w, H, A, de, e));
+    e.blk_rows = blk;
+    e.blk_xop = w.blk_xop;
+    VLA_TRY(gemm(r, "ex.out", w.h, de, m->out_w, H, A, de, e, 0, frm(w.blk_de)));
   }
   return VLA_OK;
+}
+
+static int run_denoise(const Run& r, const vla_ctx* ctx, const float* noise, float* x) {
+  return run_denoise_n(r, &ctx, 1, noise, x);
 }
 
 // ---------------------------------------------------------------------------
@@ -1088,22 +1158,29 @@ static int add_act_lane(vla_model* m) {
   auto upd = [](ScratchNeed& s, ScratchNeed x) { s.floats = std::max(s.floats, x.floats); };
   std::unique_ptr<ActWs> lane(new ActWs());
   ActWs& a = *lane;
-  VLA_TRY(dmalloc(m, (void**)&a.u, (size_t)H * de * 4));
-  // skinny-GEMM operands: row-block operand layout (64 rows), zeroed so the
-  // padding columns of xop stay zero
-  VLA_TRY(dmalloc(m, &a.xop, afrag_elems(dt, d.a_pad) * e));
-  HIP_TRY(hipMemset(a.xop, 0, afrag_elems(dt, d.a_pad) * e));
-  VLA_TRY(dmalloc(m, &a.a, afrag_elems(dt, de) * e));
-  VLA_TRY(dmalloc(m, &a.hid, afrag_elems(dt, de) * e));
-  VLA_TRY(dmalloc(m, &a.h, afrag_elems(dt, de) * e));
+  const int F = MAX_ACT_BATCH;
   const int qw = std::max(d.qd, de);  // query width (LM heads, or the DiT's)
-  VLA_TRY(dmalloc(m, &a.q, (size_t)H * qw * e));
-  VLA_TRY(dmalloc(m, &a.kown, own_k(m) * e));
-  VLA_TRY(dmalloc(m, &a.vown, own_v(m) * e));
-  HIP_TRY(hipMemset(a.kown, 0, own_k(m) * e));  // padding stays zero
-  HIP_TRY(hipMemset(a.vown, 0, own_v(m) * e));
-  VLA_TRY(dmalloc(m, &a.att, afrag_elems(dt, qw) * e));
-  VLA_TRY(dmalloc(m, &a.mlp, afrag_elems(dt, c.ex_mlp) * e));
+  a.blk_xop = afrag_elems(dt, d.a_pad);
+  a.blk_de = afrag_elems(dt, de);
+  a.blk_att = afrag_elems(dt, qw);
+  a.blk_mlp = afrag_elems(dt, c.ex_mlp);
+  a.blk_k = own_k(m);
+  a.blk_v = own_v(m);
+  VLA_TRY(dmalloc(m, (void**)&a.u, (size_t)F * H * de * 4));
+  // skinny-GEMM operands: row-block operand layout (64 rows per frame),
+  // zeroed so the padding columns of xop stay zero
+  VLA_TRY(dmalloc(m, &a.xop, F * a.blk_xop * e));
+  HIP_TRY(hipMemset(a.xop, 0, F * a.blk_xop * e));
+  VLA_TRY(dmalloc(m, &a.a, F * a.blk_de * e));
+  VLA_TRY(dmalloc(m, &a.hid, F * a.blk_de * e));
+  VLA_TRY(dmalloc(m, &a.h, F * a.blk_de * e));
+  VLA_TRY(dmalloc(m, &a.q, (size_t)F * H * qw * e));
+  VLA_TRY(dmalloc(m, &a.kown, F * a.blk_k * e));
+  VLA_TRY(dmalloc(m, &a.vown, F * a.blk_v * e));
+  HIP_TRY(hipMemset(a.kown, 0, F * a.blk_k * e));  // padding stays zero
+  HIP_TRY(hipMemset(a.vown, 0, F * a.blk_v * e));
+  VLA_TRY(dmalloc(m, &a.att, F * a.blk_att * e));
+  VLA_TRY(dmalloc(m, &a.mlp, F * a.blk_mlp * e));
   ScratchNeed sa;
   if (c.head == VLA_HEAD_DIT) {
     const int N = c.n_steps;
@@ -1119,18 +1196,19 @@ static int add_act_lane(vla_model* m) {
     upd(sa, gemm_scratch(dt, H, de, c.ex_mlp, true, true));
     upd(sa, gemm_scratch(dt, H, c.action_dim, de, false, true));
   }
-  upd(sa, gemm_scratch(dt, H, de, d.a_pad, false, true));
-  upd(sa, gemm_scratch(dt, H, de, de, false, true));
+  // (split partials of all frames of a batched action phase)
+  upd(sa, gemm_scratch(dt, F * H, de, d.a_pad, false, true));
+  upd(sa, gemm_scratch(dt, F * H, de, de, false, true));
   upd(sa, gemm_scratch(dt, c.n_steps, de, de, false, true));
-  upd(sa, gemm_scratch(dt, H, d.qkv_n, de, false, true));
-  upd(sa, gemm_scratch(dt, H, de, d.qd, true, true));
-  upd(sa, gemm_scratch(dt, H, 2 * c.ex_mlp, de, false, true));
-  upd(sa, gemm_scratch(dt, H, de, c.ex_mlp, true, true));
-  upd(sa, gemm_scratch(dt, H, c.action_dim, de, false, true));
+  upd(sa, gemm_scratch(dt, F * H, d.qkv_n, de, false, true));
+  upd(sa, gemm_scratch(dt, F * H, de, d.qd, true, true));
+  upd(sa, gemm_scratch(dt, F * H, 2 * c.ex_mlp, de, false, true));
+  upd(sa, gemm_scratch(dt, F * H, de, c.ex_mlp, true, true));
+  upd(sa, gemm_scratch(dt, F * H, c.action_dim, de, false, true));
   upd(sa, attn_scratch(dt, H, c.lm_heads, c.lm_kv_heads, c.head_dim, P, H, 1));
   VLA_TRY(alloc_scratch(m, sa, &a.scr));
-  VLA_TRY(dmalloc(m, (void**)&a.xg, (size_t)H * c.action_dim * 4));
-  VLA_TRY(dmalloc(m, (void**)&a.nstage, (size_t)H * c.action_dim * 4));
+  VLA_TRY(dmalloc(m, (void**)&a.xg, (size_t)F * H * c.action_dim * 4));
+  VLA_TRY(dmalloc(m, (void**)&a.nstage, (size_t)F * H * c.action_dim * 4));
   m->aws.push_back(std::move(lane));
   return VLA_OK;
 }
@@ -1344,13 +1422,17 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
   const int vlanes = std::max(1, s.vlm_streams);
   if (vlanes > MAX_VLM_STREAMS) return fail(VLA_EINVAL, "vlm_streams must be <= 2");
   if (vlanes > 1 && s.mode == VLA_MODE_SERIAL) return fail(VLA_EINVAL, "vlm_streams > 1 needs a concurrent mode");
+  const int B = std::max(1, s.act_batch);
+  if (B > MAX_ACT_BATCH) return fail(VLA_EINVAL, "act_batch must be <= 2");
+  if (B > 1 && m->c.head != VLA_HEAD_PI0) return fail(VLA_EINVAL, "act_batch > 1: pi0-style action head only");
   const vla_config& c = m->c;
   for (int r = 0; r < R; ++r)
     if (!frames[r].pixels || (c.n_text > 0 && !frames[r].text_ids) || (c.state_dim > 0 && !frames[r].state))
       return fail(VLA_EINVAL, "frame " + std::to_string(r) + " has a NULL input");
   std::lock_guard<std::mutex> lock(m->mu);
-  // a context is in flight from its prefill until its action phase ends
-  const int nctx = lanes + vlanes;
+  // a context is in flight from its prefill until its action phase ends;
+  // frames go to action phases in groups of B consecutive frames
+  const int nctx = B * (lanes + vlanes);
   while ((int)m->pctx.size() < nctx) {
     vla_ctx* cx = nullptr;
     VLA_TRY(ctx_create_impl(m, &cx));
@@ -1388,21 +1470,25 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
         m->pre_graphs[key] = ge;
       }
     }
+    // one graph per (lane, first context, frames): a group of n frames uses
+    // contexts ci .. ci + n - 1 (groups start at multiples of B)
     for (int li = 0; li < lanes; ++li)
-      for (int ci = 0; ci < nctx; ++ci) {
-        const auto key = std::make_pair(li, ci);
-        if (m->den_graphs.count(key)) continue;
-        ActWs* aw = m->aws[li].get();
-        Run ra{m, st.a[li], acaps, &aw->scr, aw};
-        hipGraphExec_t ge = nullptr;
-        VLA_TRY(capture(st.a[li], [&] { return run_denoise(ra, m->pctx[ci], aw->nstage, aw->xg); }, &ge));
-        m->den_graphs[key] = ge;
-      }
+      for (int ci = 0; ci < nctx; ci += B)
+        for (int n = 1; n <= B; ++n) {
+          const auto key = std::make_tuple(li, ci, n);
+          if (m->den_graphs.count(key)) continue;
+          ActWs* aw = m->aws[li].get();
+          Run ra{m, st.a[li], acaps, &aw->scr, aw};
+          const vla_ctx* cs[MAX_ACT_BATCH] = {m->pctx[ci], n > 1 ? m->pctx[ci + 1] : nullptr};
+          hipGraphExec_t ge = nullptr;
+          VLA_TRY(capture(st.a[li], [&] { return run_denoise_n(ra, cs, n, aw->nstage, aw->xg); }, &ge));
+          m->den_graphs[key] = ge;
+        }
   }
 
   const auto t0 = std::chrono::steady_clock::now();
   for (int r = 0; r < R; ++r) {
-    const int ci = r % nctx, li = r % lanes, vi = r % vlanes;
+    const int ci = r % nctx, li = (r / B) % lanes, vi = r % vlanes;
     vla_ctx* ctx = m->pctx[ci];
     hipStream_t sv = st.v[vi], sa = st.a[li];
     VlmWs* vw = m->vws[vi].get();
@@ -1421,18 +1507,30 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
       VLA_TRY(run_prefill(rv, &frames[r], ctx));
     }
     HIP_TRY(hipEventRecord(m->ev[4 * r + 1], sv));
-    if (sv != sa) HIP_TRY(hipStreamWaitEvent(sa, m->ev[4 * r + 1], 0));
-    HIP_TRY(hipEventRecord(m->ev[4 * r + 2], sa));
+    // the action phase of a group starts when its last frame's prefill ends
+    const int g0 = r / B * B, n = std::min(B, R - g0);
+    if (r != g0 + n - 1) continue;
+    for (int q = g0; q <= r; ++q)
+      if (st.v[q % vlanes] != sa) HIP_TRY(hipStreamWaitEvent(sa, m->ev[4 * q + 1], 0));
+    HIP_TRY(hipEventRecord(m->ev[4 * g0 + 2], sa));
     ActWs* aw = m->aws[li].get();
+    const int c0 = g0 % nctx;
     if (graphs) {
-      HIP_TRY(hipMemcpyAsync(aw->nstage, noise + r * chunk, chunk * 4, hipMemcpyDeviceToDevice, sa));
-      HIP_TRY(hipGraphLaunch(m->den_graphs[std::make_pair(li, ci)], sa));
-      HIP_TRY(hipMemcpyAsync(actions + r * chunk, aw->xg, chunk * 4, hipMemcpyDeviceToDevice, sa));
+      HIP_TRY(hipMemcpyAsync(aw->nstage, noise + g0 * chunk, n * chunk * 4, hipMemcpyDeviceToDevice, sa));
+      HIP_TRY(hipGraphLaunch(m->den_graphs[std::make_tuple(li, c0, n)], sa));
+      HIP_TRY(hipMemcpyAsync(actions + g0 * chunk, aw->xg, n * chunk * 4, hipMemcpyDeviceToDevice, sa));
     } else {
       Run ra{m, sa, acaps, &aw->scr, aw};
-      VLA_TRY(run_denoise(ra, ctx, noise + r * chunk, actions + r * chunk));
+      const vla_ctx* cs[MAX_ACT_BATCH] = {m->pctx[c0], n > 1 ? m->pctx[c0 + 1] : nullptr};
+      VLA_TRY(run_denoise_n(ra, cs, n, noise + g0 * chunk, actions + g0 * chunk));
     }
-    HIP_TRY(hipEventRecord(m->ev[4 * r + 3], sa));
+    HIP_TRY(hipEventRecord(m->ev[4 * g0 + 3], sa));
+    // the group's other frames get an empty action interval at its end (the
+    // group's time is counted once) and the same end for context reuse
+    for (int q = g0 + 1; q <= r; ++q) {
+      HIP_TRY(hipEventRecord(m->ev[4 * q + 2], sa));
+      HIP_TRY(hipEventRecord(m->ev[4 * q + 3], sa));
+    }
   }
   for (int vi = 0; vi < vlanes; ++vi) HIP_TRY(hipStreamSynchronize(st.v[vi]));
   for (int li = 0; li < lanes; ++li) HIP_TRY(hipStreamSynchronize(st.a[li]));

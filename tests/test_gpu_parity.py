@@ -241,8 +241,13 @@ def test_pi0_full_size_vs_oracle(V):
         # the schedule the benchmark reports (two action lanes, graph replay)
         # gives the same bits as the standalone calls
         g.say("pi0 full size: pipeline, two action lanes, graphs")
-        piped = _pipeline_frames(g, m, cfg, [fr, synth.make_frame(cfg, 0, 1)])
+        fr1 = synth.make_frame(cfg, 0, 1)
+        piped = _pipeline_frames(g, m, cfg, [fr, fr1])
         assert np.array_equal(piped[0].astype(np.float64), got)
+        # the two frames' action phases as one batched loop
+        g.say("pi0 full size: pipeline, batched action phases, graphs")
+        batched = _pipeline_frames(g, m, cfg, [fr, fr1], act_batch=2, act_streams=1)
+        assert np.array_equal(batched, piped)
     g.say("pi0 full size: oracle")
     P = synth.make_params(cfg, 0)
     cap = {}
@@ -256,15 +261,15 @@ def test_pi0_full_size_vs_oracle(V):
     assert err <= CHUNK_TOL[synth.BF16]
 
 
-def _pipeline_frames(g, m, cfg, frames):
-    """Chunks of `frames` from one pipeline run in the two-action-lane graph
-    schedule."""
+def _pipeline_frames(g, m, cfg, frames, **kw):
+    """Chunks of `frames` from one pipeline run in a graph schedule (by
+    default the two-action-lane one)."""
     dfs = [g.DevFrame(f) for f in frames]
     noise = torch.stack([d.noise for d in dfs]).contiguous()
     out = torch.full_like(noise, float("nan"))
-    V_ = g.V
-    V_.vla_pipeline_run(m, [d.c for d in dfs], noise, len(frames), mode="concurrent", actions=out,
-                        act_streams=2, graphs=True)
+    kw = dict(dict(act_streams=2), **kw)
+    g.V.vla_pipeline_run(m, [d.c for d in dfs], noise, len(frames), mode="concurrent", actions=out,
+                         graphs=True, **kw)
     torch.cuda.synchronize()
     return out.cpu().numpy()
 
@@ -391,6 +396,18 @@ def test_pipeline_modes_bit_identical(V, cfg):
                  ("concurrent", dict(vlm_streams=2, act_streams=2)),
                  ("concurrent", dict(vlm_streams=2, act_streams=3, graphs=True)),
                  ("wg_capped", dict(vlm_wg_cap=1, graphs=True))]
+        if cfg["head"] == synth.HEAD_PI0:
+            # two robots' action phases as one batched loop (R = 7: the last
+            # frame runs alone)
+            modes += [("serial", dict(act_batch=2)), ("concurrent", dict(act_batch=2)),
+                      ("concurrent", dict(act_batch=2, graphs=True)),
+                      ("concurrent", dict(act_batch=2, act_streams=2, graphs=True)),
+                      ("cu_masked", dict(split, act_batch=2, graphs=True)),
+                      ("concurrent", dict(act_batch=2, vlm_streams=2, act_streams=2))]
+        else:
+            with pytest.raises(V.VlaError):
+                V.vla_pipeline_run(m, [d.c for d in dfs], noise, R, mode="concurrent", act_batch=2,
+                                   actions=torch.empty_like(noise))
         standalone = [g.run_frame(m, cfg, f)[0] for f in frames]
         for mode, kw in modes:
             name = mode + "".join(f"/{k}={v}" for k, v in kw.items() if k not in ("vlm_cus", "act_cus"))
