@@ -241,12 +241,12 @@ def test_pi0_full_size_vs_oracle(V):
         # the schedule the benchmark reports (two action lanes, graph replay)
         # gives the same bits as the standalone calls
         g.say("pi0 full size: pipeline, two action lanes, graphs")
-        fr1 = synth.make_frame(cfg, 0, 1)
-        piped = _pipeline_frames(g, m, cfg, [fr, fr1])
+        frs = [fr] + [synth.make_frame(cfg, 0, r) for r in (1, 2)]
+        piped = _pipeline_frames(g, m, cfg, frs)
         assert np.array_equal(piped[0].astype(np.float64), got)
-        # the two frames' action phases as one batched loop
+        # frames 0 and 1 as one batched action loop (the last frame runs alone)
         g.say("pi0 full size: pipeline, batched action phases, graphs")
-        batched = _pipeline_frames(g, m, cfg, [fr, fr1], act_batch=2, act_streams=1)
+        batched = _pipeline_frames(g, m, cfg, frs, act_batch=2, act_streams=1)
         assert np.array_equal(batched, piped)
     g.say("pi0 full size: oracle")
     P = synth.make_params(cfg, 0)
