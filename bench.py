@@ -167,7 +167,9 @@ def main():
                     help="schedule reported as `value` (auto: the fastest measured one)")
     ap.add_argument("--modes", default="serial,concurrent,cu_masked,wg_capped,serial_graph,"
                                        "concurrent_graph,lanes2_graph,lanes3_graph,batch2_graph,"
-                                       "batch2_lanes2_graph")
+                                       "batch2_lanes2_graph,batch4_graph,batch4_lanes2_graph,batch8_graph,"
+                                       "vb2_ab2_graph,vb2_ab2_lanes2_graph,vb2_ab4_graph,vb4_ab4_graph,"
+                                       "vb4_ab2_lanes2_graph,vb4_ab4_lanes2_graph,vb8_ab8_graph")
     ap.add_argument("--split", default="192,64", help="CU split VLM,action for cu_masked")
     ap.add_argument("--wg-cap", type=int, default=2, help="VLM workgroups per CU for wg_capped")
     ap.add_argument("--kernel", default="ex.gateup", help="tag of the kernel timed for the roofline")
@@ -175,7 +177,7 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--extra", default="gr00t:8:serial,concurrent,cu_masked,lanes2_graph,v2_lanes2_graph;"
                                        "pi0_3view:32:serial,concurrent,cu_224_32,cu_192_64,cu_160_96,"
-                                       "wg_cap1,wg_cap2,lanes2_graph,cu_160_96_lanes2",
+                                       "wg_cap1,wg_cap2,lanes2_graph,cu_160_96_lanes2,batch4_lanes2_graph,batch8_lanes2_graph",
                     help="further workloads, ';'-separated preset:R:schedule,schedule,...")
     ap.add_argument("--extra-steps", type=int, default=5)
     ap.add_argument("--residency", type=int, default=8_000_000,
@@ -235,6 +237,17 @@ def main():
           "batch2_graph": dict(mode="concurrent", act_batch=2, graphs=True),
           "batch2_lanes2_graph": dict(mode="concurrent", act_batch=2, act_streams=2, graphs=True),
           "batch2_v2_graph": dict(mode="concurrent", act_batch=2, vlm_streams=2, graphs=True)}
+    for v_ in (2, 4, 8):  # several robots' prefills as one pass, with action groups
+        for a_ in (1, 2, 4, 8):
+            kw[f"vb{v_}_ab{a_}_graph"] = dict(mode="concurrent", vlm_batch=v_, act_batch=a_, graphs=True)
+            kw[f"vb{v_}_ab{a_}_lanes2_graph"] = dict(mode="concurrent", vlm_batch=v_, act_batch=a_,
+                                                     act_streams=2, graphs=True)
+            kw[f"vb{v_}_ab{a_}_cu_192_64"] = dict(mode="cu_masked", vlm_cus=192, act_cus=64, vlm_batch=v_,
+                                                  act_batch=a_, graphs=True)
+    for b_ in (4, 8):  # larger groups of robots per action loop
+        kw[f"batch{b_}_graph"] = dict(mode="concurrent", act_batch=b_, graphs=True)
+        kw[f"batch{b_}_lanes2_graph"] = dict(mode="concurrent", act_batch=b_, act_streams=2, graphs=True)
+        kw[f"batch{b_}_v2_graph"] = dict(mode="concurrent", act_batch=b_, vlm_streams=2, graphs=True)
     for a_, b_ in ((224, 32), (192, 64), (160, 96)):  # CU-split sweep entries
         kw[f"cu_{a_}_{b_}"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_)
         kw[f"cu_{a_}_{b_}_lanes2"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_, act_streams=2, graphs=True)

@@ -104,12 +104,20 @@ typedef struct vla_sched {
   int32_t vlm_streams;/* VLM streams (0 or 1: one; at most 2). With 2, the prefills  */
                       /*   of consecutive frames alternate between two streams and   */
                       /*   may overlap each other; not with VLA_MODE_SERIAL          */
-  int32_t act_batch;  /* frames per action phase (0 or 1: one; at most 2). With 2,   */
-                      /*   the action phases of two consecutive frames (different    */
-                      /*   robots) run as one denoising loop that reads the weights  */
-                      /*   once for both; it starts when both prefills are done. A   */
-                      /*   final odd frame runs alone. Every frame's chunk is bit    */
+  int32_t act_batch;  /* frames per action phase (0 or 1: one; at most 8). With     */
+                      /*   k > 1, the action phases of k consecutive frames          */
+                      /*   (different robots) run as one denoising loop that reads   */
+                      /*   the weights once for all of them; it starts when their    */
+                      /*   prefills are done. A final group of fewer than k frames   */
+                      /*   runs with as many as remain. Every frame's chunk is bit   */
                       /*   identical to its own run. VLA_HEAD_PI0 models only.       */
+  int32_t vlm_batch;  /* frames per VLM prefill (0 or 1: one; else 2, 4 or 8). With  */
+                      /*   k > 1, the prefills of k consecutive frames (different    */
+                      /*   robots) run as one pass: their views stacked for the ViT  */
+                      /*   and their prefixes for the LM, so every weight is read    */
+                      /*   once for all k; a final group of fewer than k frames runs */
+                      /*   with as many as remain. Every frame's cache and chunk are */
+                      /*   bit identical to its own run.                             */
 } vla_sched;
 
 typedef struct vla_timing {

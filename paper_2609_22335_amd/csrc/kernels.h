@@ -8,6 +8,10 @@ namespace vla {
 
 enum Dtype { DT_F32 = 0, DT_BF16 = 1 };
 
+// Most frames (robots' action phases) one skinny GEMM, norm or cache
+// attention launch can carry as frame blocks.
+constexpr int MAX_FRAMES = 8;
+
 // GEMM epilogues. Physical output column n of a GEMM is row n of its weight
 // matrix as stored on the device; paired kinds read columns n and n + 16 of
 // every 32-column group together.
@@ -146,6 +150,10 @@ struct GemmDesc {
   // one-frame call. The epilogue sees rows f * M + m (Epi::blk_rows = M).
   int frames = 1;
   size_t a_blk = 0;
+  // Rows of one frame when M stacks several frames' rows (a batched
+  // prefill): the split-K factor is planned for plan_m rows, so every row
+  // gets the same reduction as in a one-frame call (0: plan for M).
+  int plan_m = 0;
 };
 
 // Offset of element (n, k) of a weight stored in MFMA fragment order with KS
@@ -195,6 +203,10 @@ struct AttnDesc {
   int Sq, nq, nkv, hd;
   int segs;  // independent segments (camera views) with their own Q/K/V rows
   long long seg_q, seg_kv, seg_o;  // element strides between segments
+  // segments of one frame when several frames' views are stacked: the KV
+  // split is planned for plan_segs segments, so every segment is reduced
+  // as in a one-frame call (0: plan for segs)
+  int plan_segs = 0;
 };
 
 size_t attn_scratch_floats(const AttnDesc& a);
@@ -220,8 +232,8 @@ struct AttnKvDesc {
   // q + f Sq ldq, keys [k0f[f] (S0); k1 + f k1_blk (S1)] (values alike) and
   // output out + f out_blk; frame 0 uses k0 / v0.
   int frames = 1;
-  const void* k0f[2] = {nullptr, nullptr};
-  const void* v0f[2] = {nullptr, nullptr};
+  const void* k0f[MAX_FRAMES] = {};
+  const void* v0f[MAX_FRAMES] = {};
   size_t k1_blk = 0, v1_blk = 0, out_blk = 0;
 };
 hipError_t launch_attention_kv(const AttnKvDesc& d, const LaunchCaps& caps, hipStream_t st);

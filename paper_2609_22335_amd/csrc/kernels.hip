@@ -627,7 +627,7 @@ static hipError_t run_skinny_t(const GemmDesc& g, int splits, const Scratch& s,
 
 static hipError_t launch_skinny(const GemmDesc& g, const Scratch& s, const LaunchCaps& caps,
                                 hipStream_t st) {
-  if (g.M > 64 || g.frames < 1 || g.frames > 2 ||
+  if (g.M > 64 || g.frames < 1 || g.frames > MAX_FRAMES ||
       (g.frames > 1 && (g.epi.blk_rows != g.M || g.a_blk < afrag_elems(g.dtype, g.K))))
     return hipErrorInvalidValue;
   const int splits = skinny_splits(g);
@@ -664,18 +664,21 @@ GemmPlan plan_gemm(const GemmDesc& g) {
     return p;
   }
   const TileCfg* cfgs = g.dtype == DT_BF16 ? kBf16Cfg : kF32Cfg;
-  int c;
-  if (g.dtype == DT_BF16) {
-    const int t128 = ((g.M + 127) / 128) * ((g.N + 127) / 128);
-    if (g.M >= 256 && t128 >= NUM_CU_PLAN) c = 0;
-    else if (g.M > 32) c = 1;
-    else c = 2;
-  } else {
-    c = g.M > 32 ? 0 : 1;
-  }
-  const TileCfg t = cfgs[c];
-  const int tm = (g.M + t.bm - 1) / t.bm, tn = (g.N + t.bn - 1) / t.bn;
-  const int tiles = tm * tn;
+  auto choose = [&](int M) {
+    if (g.dtype == DT_BF16) {
+      const int t128 = ((M + 127) / 128) * ((g.N + 127) / 128);
+      if (M >= 256 && t128 >= NUM_CU_PLAN) return 0;
+      return M > 32 ? 1 : 2;
+    }
+    return M > 32 ? 0 : 1;
+  };
+  // The split factor comes from the rows of one frame (plan_m), the tile
+  // from all M rows; every configuration of a dtype has the same BK, so the
+  // K range of each split (and every sum) is the same as in a one-frame call.
+  const int Mp = g.plan_m > 0 ? std::min(g.plan_m, g.M) : g.M;
+  const int c = choose(g.M);
+  const TileCfg t = cfgs[c], tp = cfgs[choose(Mp)];
+  const int tiles = ((Mp + tp.bm - 1) / tp.bm) * ((g.N + tp.bn - 1) / tp.bn);
   const int kblocks = (g.K + t.bk - 1) / t.bk;
   // Split K where it is free: partial sums (EPI_PART) are added by their
   // consumer, so aim for two workgroups per CU with at least four K-blocks
@@ -691,7 +694,7 @@ GemmPlan plan_gemm(const GemmDesc& g) {
   splits = (kblocks + kchunk_blocks - 1) / kchunk_blocks;
   p.cfg = c;
   p.splits = splits;
-  p.tiles = tiles * splits;
+  p.tiles = ((g.M + t.bm - 1) / t.bm) * ((g.N + t.bn - 1) / t.bn) * splits;
   p.scratch_floats = (splits > 1 || g.epi.kind == EPI_PART) ? (size_t)splits * g.M * g.N : 0;
   return p;
 }
@@ -1031,7 +1034,7 @@ static int attn_hdp(int hd, int dtype) {
 static void attn_split(const AttnDesc& d, int* qblocks, int* splits) {
   const int group = d.nq / d.nkv;
   *qblocks = (d.Sq * group + ATT_BQ - 1) / ATT_BQ;
-  const int base = *qblocks * d.nkv * d.segs;
+  const int base = *qblocks * d.nkv * (d.plan_segs > 0 ? std::min(d.plan_segs, d.segs) : d.segs);
   const int nblk = (d.S0 + d.S1 + ATT_BKV - 1) / ATT_BKV;
   int s = 1;
   if (base < 128 && nblk >= 4) s = std::min((128 + base - 1) / base, nblk / 2);
@@ -1137,8 +1140,8 @@ hipError_t launch_attention(const AttnDesc& d, const Scratch& s, const LaunchCap
 
 struct Attn2Args {
   const void* q;
-  const void* k0[2];  // per frame
-  const void* v0[2];
+  const void* k0[MAX_FRAMES];  // per frame
+  const void* v0[MAX_FRAMES];
   const void* k1;     // frame f: k1 + f k1_blk (elements)
   const void* v1;
   void* out;          // frame f: out + f out_blk
@@ -1423,15 +1426,19 @@ hipError_t launch_attention_kv(const AttnKvDesc& d, const LaunchCaps& caps, hipS
   if (hdp < 0 || d.nq % d.nkv != 0 || d.S0 <= 0 || d.S1 < 0 || d.Sq <= 0 ||
       (d.S1 > 0 && (!d.k1 || !d.v1)) || d.hd % 8 != 0 || (d.out_afrag && d.Sq > 64) ||
       (!d.out_afrag && ((size_t)d.ldo * (d.dtype == DT_BF16 ? 2 : 4)) % 16 != 0) ||
-      ((uintptr_t)d.out & 15) != 0 || d.frames < 1 || d.frames > 2 ||
-      (d.frames > 1 && (!d.k0f[1] || !d.v0f[1] || (d.out_blk * (d.dtype == DT_BF16 ? 2 : 4)) % 16 != 0)))
+      ((uintptr_t)d.out & 15) != 0 || d.frames < 1 || d.frames > MAX_FRAMES ||
+      (d.frames > 1 && (d.out_blk * (d.dtype == DT_BF16 ? 2 : 4)) % 16 != 0))
     return hipErrorInvalidValue;
+  for (int f = 1; f < d.frames; ++f)
+    if (!d.k0f[f] || !d.v0f[f]) return hipErrorInvalidValue;
   Attn2Args a{};
   a.q = d.q;
   a.k0[0] = d.k0;
   a.v0[0] = d.v0;
-  a.k0[1] = d.frames > 1 ? d.k0f[1] : d.k0;
-  a.v0[1] = d.frames > 1 ? d.v0f[1] : d.v0;
+  for (int f = 1; f < MAX_FRAMES; ++f) {
+    a.k0[f] = f < d.frames ? d.k0f[f] : d.k0;
+    a.v0[f] = f < d.frames ? d.v0f[f] : d.v0;
+  }
   a.k1 = d.S1 > 0 ? d.k1 : nullptr;
   a.v1 = d.S1 > 0 ? d.v1 : nullptr;
   a.k1_blk = d.k1_blk;

@@ -214,22 +214,31 @@ struct DitLayer {
 constexpr int MAX_ACT_STREAMS = 4;
 
 constexpr int MAX_VLM_STREAMS = 2;
-constexpr int MAX_ACT_BATCH = 2;  // frames one action phase can run together
+constexpr int MAX_ACT_BATCH = MAX_FRAMES;  // frames one action phase can run together
 
 struct Streams {
   hipStream_t v[MAX_VLM_STREAMS] = {};
   hipStream_t a[MAX_ACT_STREAMS] = {};
 };
 
+constexpr int MAX_VLM_BATCH = 8;  // frames one prefill can run together
+constexpr int CTX_BLOCK = 8;      // pipeline contexts are allocated in blocks of this many
+
 // Scratch of one VLM lane (one prefill at a time per lane), with staging for
-// graph replays.
+// graph replays, sized for `cap` frames prefilled together (each buffer holds
+// the frames' rows one after another).
 struct VlmWs {
+  int cap = 1;
   float *xv = nullptr, *xl = nullptr;
   void *h = nullptr, *qkv = nullptr, *att = nullptr, *mlp = nullptr, *sbuf = nullptr;
   Scratch scr;
   float* pstage = nullptr;
   int32_t* istage = nullptr;
   float* sstage = nullptr;
+  std::vector<void*> mem;  // this lane's allocations
+  ~VlmWs() {
+    for (void* p : mem) hipFree(p);
+  }
 };
 
 // Scratch of one action lane (one denoise at a time per lane).
@@ -248,6 +257,9 @@ struct ActWs {
 
 struct vla_ctx {
   vla_model* m = nullptr;
+  // contexts made together share one allocation per buffer (context i of a
+  // block at i times the context size); the block's first context owns it
+  bool own = true;
   // per layer, the KV-cache layout (kv_kidx / kv_vidx) with prefix_pad / 32
   // blocks per KV head; zeroed at creation, so unwritten padding stays zero
   void* K = nullptr;
@@ -306,7 +318,7 @@ struct vla_model {
   std::vector<hipEvent_t> ev;
   // graph replay: frame inputs staged into fixed buffers, graphs cached per
   // (context, VLM grid cap) and (action lane, context)
-  std::map<std::tuple<int, int, int>, hipGraphExec_t> pre_graphs;  // (VLM lane, context, WG cap)
+  std::map<std::tuple<int, int, int, int>, hipGraphExec_t> pre_graphs;  // (VLM lane, first context, WG cap, frames)
   std::map<std::tuple<int, int, int>, hipGraphExec_t> den_graphs;  // (lane, first context, frames)
   std::mutex mu;
 
@@ -340,6 +352,22 @@ static size_t own_v(const vla_model* m) {
 static size_t cross_elems(const vla_model* m) {
   return std::max(kv_kelems(m->dt, m->d.prefix_pad / 32, m->d.ehd, m->c.ex_heads),
                   kv_velems(m->dt, m->d.prefix_pad / 32, m->d.ehd, m->c.ex_heads));
+}
+
+// bytes of one context's K, V and DiT cross K / V buffers
+static size_t ctx_kbytes(const vla_model* m) { return (size_t)m->c.lm_layers * ctx_layer_k(m) * m->esz; }
+static size_t ctx_vbytes(const vla_model* m) { return (size_t)m->c.lm_layers * ctx_layer_v(m) * m->esz; }
+static size_t ctx_xbytes(const vla_model* m) {
+  return m->c.head == VLA_HEAD_DIT ? (size_t)((m->c.ex_layers + 1) / 2) * cross_elems(m) * m->esz : 0;
+}
+
+// True when c[0 .. n-1] are consecutive contexts of one block.
+static bool ctx_consecutive(const vla_model* m, vla_ctx* const* c, int n) {
+  for (int i = 1; i < n; ++i)
+    if (c[i]->K != (char*)c[0]->K + i * ctx_kbytes(m) || c[i]->V != (char*)c[0]->V + i * ctx_vbytes(m) ||
+        c[i]->XK != (ctx_xbytes(m) ? (char*)c[0]->XK + i * ctx_xbytes(m) : nullptr))
+      return false;
+  return true;
 }
 
 static size_t dsz(int dt) { return dt == DT_BF16 ? 2 : 4; }
@@ -556,6 +584,7 @@ static int timer_events(const Run& r, const char* tag, LaunchCaps* caps) {
 struct Frames {
   int n = 1;
   size_t a_blk = 0;
+  int plan_m = 0;  // rows of one frame when M stacks several frames (0: M)
 };
 
 // C = A W[:, koff : koff + K]^T with the epilogue e; W is a weight tensor id.
@@ -571,6 +600,7 @@ static GemmDesc gemm_desc(vla_model* m, const void* A, int lda, int W, int M, in
   }
   g.frames = fr.n;
   g.a_blk = fr.a_blk;
+  g.plan_m = fr.plan_m;
   return g;
 }
 
@@ -662,13 +692,16 @@ static Epi epi_kind(int kind, void* out = nullptr, int ldo = 0, const float* bia
 // partials) -> QKV (+RoPE, K/V stored) -> attention over [past; own] -> O ->
 // RMSNorm (after adding O) -> GeGLU -> down. The down projection is left
 // pending in the scratch (*pend = its split count) for the next norm.
-// Expert layers may run `frames` frames together (a batched action phase):
-// `rows` rows each, frame f reading the past K/V kpast[f] / vpast[f] and the
-// action workspace's per-frame blocks.
+// Several frames may run together, `rows` rows each:
+//  * expert layers (a batched action phase): frame f reads the past K/V
+//    kpast[f] / vpast[f] and the action workspace's per-frame blocks;
+//  * LM layers (a batched prefill): x holds the frames' rows one after
+//    another, frame f's own K/V (its cache) sit kstride / vstride elements
+//    after frame f - 1's, and the split-K factors are those of one frame.
 static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int rows, int dim, int mlp,
                          void* h, void* q, void* kout, void* vout, int pos0, const void* const* kpast,
                          const void* const* vpast, int npast, void* att, void* mlpbuf, bool kv_only,
-                         int* pend, int frames = 1) {
+                         int* pend, int frames = 1, size_t kstride = 0, size_t vstride = 0) {
   vla_model* m = r.m;
   const vla_config& c = m->c;
   const Dims& d = m->d;
@@ -676,10 +709,24 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   const bool af = !lm;
   const bool fb = frames > 1;  // frame blocks
   const ActWs* aw = r.aw;
-  if (fb && (lm || !aw)) return fail(VLA_EINVAL, "batched frames: expert layers only");
-  const int blk = fb ? rows : 0;
-  auto frm = [&](size_t a_blk) { Frames f; f.n = frames; f.a_blk = fb ? a_blk : 0; return f; };
-  VLA_TRY(norm(r, x, frames * rows, dim, *pend, nullptr, L.rms1, -1, true, h, af, blk, fb ? aw->blk_de : 0));
+  if (fb && !lm && !aw) return fail(VLA_EINVAL, "batched frames: expert layers need an action workspace");
+  if (fb && lm && (kstride == 0 || vstride == 0)) return fail(VLA_EINVAL, "batched prefill: cache strides");
+  // GEMM rows and frames: the LM stacks the frames' rows into one M (splits
+  // planned for one frame); the skinny expert GEMMs take frame blocks
+  const int gm = lm ? frames * rows : rows;
+  auto frm = [&](size_t a_blk) {
+    Frames f;
+    if (lm) {
+      f.plan_m = rows;
+    } else {
+      f.n = frames;
+      f.a_blk = fb ? a_blk : 0;
+    }
+    return f;
+  };
+  const int nblk = fb && !lm ? rows : 0;  // norm output frame blocks (operand layout)
+  const size_t nblk_out = fb && !lm ? aw->blk_de : 0;
+  VLA_TRY(norm(r, x, frames * rows, dim, *pend, nullptr, L.rms1, -1, true, h, af, nblk, nblk_out));
   *pend = 0;
   Epi e;
   e.kind = EPI_QKV_ROPE;
@@ -696,10 +743,10 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   e.rope_sin = m->rope_sin;
   if (fb) {
     e.blk_rows = rows;
-    e.blk_k = aw->blk_k;
-    e.blk_v = aw->blk_v;
+    e.blk_k = lm ? kstride : aw->blk_k;
+    e.blk_v = lm ? vstride : aw->blk_v;
   }
-  VLA_TRY(gemm(r, lm ? "lm.qkv" : "ex.qkv", h, dim, L.qkv, rows, d.qkv_n, dim, e, 0, frm(fb ? aw->blk_de : 0)));
+  VLA_TRY(gemm(r, lm ? "lm.qkv" : "ex.qkv", h, dim, L.qkv, gm, d.qkv_n, dim, e, 0, frm(fb && !lm ? aw->blk_de : 0)));
   if (kv_only) return VLA_OK;
   AttnKvDesc a{};
   a.dtype = m->dt;
@@ -724,52 +771,80 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   a.nq = c.lm_heads;
   a.nkv = c.lm_kv_heads;
   a.hd = c.head_dim;
-  if (fb) {
+  if (fb && lm) {
+    // frame f: queries f * rows .., its own cache, output rows f * rows ..
+    a.frames = frames;
+    for (int f = 1; f < frames; ++f) {
+      a.k0f[f] = (const char*)kout + f * kstride * m->esz;
+      a.v0f[f] = (const char*)vout + f * vstride * m->esz;
+    }
+    a.out_blk = (size_t)rows * d.qd;
+  } else if (fb) {
     if (!kpast) return fail(VLA_EINVAL, "batched frames need past K/V");
     a.frames = frames;
-    a.k0f[1] = kpast[1];
-    a.v0f[1] = vpast[1];
+    for (int f = 1; f < frames; ++f) {
+      a.k0f[f] = kpast[f];
+      a.v0f[f] = vpast[f];
+    }
     a.k1_blk = aw->blk_k;
     a.v1_blk = aw->blk_v;
     a.out_blk = aw->blk_att;
   }
   VLA_TRY(attn_kv(r, lm ? "lm.attn" : "ex.attn", a));
   int so = 0;
-  VLA_TRY(gemm_part(r, lm ? "lm.o" : "ex.o", att, d.qd, L.o, rows, dim, d.qd, &so, frm(fb ? aw->blk_att : 0)));
-  VLA_TRY(norm(r, x, frames * rows, dim, so, nullptr, L.rms2, -1, true, h, af, blk, fb ? aw->blk_de : 0));
+  VLA_TRY(gemm_part(r, lm ? "lm.o" : "ex.o", att, d.qd, L.o, gm, dim, d.qd, &so, frm(fb && !lm ? aw->blk_att : 0)));
+  VLA_TRY(norm(r, x, frames * rows, dim, so, nullptr, L.rms2, -1, true, h, af, nblk, nblk_out));
   Epi eg = epi_kind(EPI_GEGLU, mlpbuf, mlp);
   eg.afrag = af;
-  if (fb) {
+  if (fb && !lm) {
     eg.blk_rows = rows;
     eg.blk_out = aw->blk_mlp;
   }
-  VLA_TRY(gemm(r, lm ? "lm.gateup" : "ex.gateup", h, dim, L.gu, rows, 2 * mlp, dim, eg, 0, frm(fb ? aw->blk_de : 0)));
-  VLA_TRY(gemm_part(r, lm ? "lm.down" : "ex.down", mlpbuf, mlp, L.down, rows, dim, mlp, pend,
-                    frm(fb ? aw->blk_mlp : 0)));
+  VLA_TRY(gemm(r, lm ? "lm.gateup" : "ex.gateup", h, dim, L.gu, gm, 2 * mlp, dim, eg, 0,
+               frm(fb && !lm ? aw->blk_de : 0)));
+  VLA_TRY(gemm_part(r, lm ? "lm.down" : "ex.down", mlpbuf, mlp, L.down, gm, dim, mlp, pend,
+                    frm(fb && !lm ? aw->blk_mlp : 0)));
   return VLA_OK;
 }
 
-static int run_prefill(const Run& r, const vla_frame* f, vla_ctx* ctx) {
+// The VLM prefill of `n` frames together (a batched prefill; n <= the lane's
+// capacity): their views are stacked as n * n_views views for the ViT and
+// their prefixes as n * prefix rows for the LM, each frame writing its own
+// context ctxs[f] (consecutive contexts of one block when n > 1). Splits
+// and reductions are planned for one frame, so every frame's cache equals
+// its own prefill bit for bit.
+static int run_prefill_n(const Run& r, const vla_frame* f, int n, vla_ctx* const* ctxs) {
   vla_model* m = r.m;
   const vla_config& c = m->c;
   const Dims& d = m->d;
   VlmWs& w = *r.vw;
-  const int dv = c.vit_dim, dl = c.lm_dim, rows = d.rows_v;
+  if (n < 1 || n > w.cap) return fail(VLA_EINVAL, "frames per prefill exceed the lane's capacity");
+  if (n > 1 && !ctx_consecutive(m, ctxs, n)) return fail(VLA_EINVAL, "batched prefill: contexts not consecutive");
+  const int dv = c.vit_dim, dl = c.lm_dim, rows = d.rows_v, P = d.prefix;
+  const int nv = n * c.n_views;  // views of all frames
+  auto fr1 = [&](int rows1) {  // splits of one frame's rows
+    Frames x;
+    x.plan_m = rows1;
+    return x;
+  };
   // ViT: patch embedding + bias + position
-  HIP_TRY(launch_patchify(m->dt, f->pixels, c.n_views, c.img_h, c.img_w, c.patch, w.h, d.kp_pad, r.st));
+  for (int i = 0; i < n; ++i)
+    HIP_TRY(launch_patchify(m->dt, f[i].pixels, c.n_views, c.img_h, c.img_w, c.patch,
+                            (char*)w.h + (size_t)i * rows * d.kp_pad * m->esz, d.kp_pad, r.st));
   {
     Epi e = epi_kind(EPI_F32, w.xv, dv, m->f32(m->patch_b));
     e.rowadd = m->f32(m->pos);
     e.rowadd_period = d.tview;
     e.ldra = dv;
-    VLA_TRY(gemm(r, "vit.patch", w.h, d.kp_pad, m->patch_w, rows, dv, d.kp_pad, e));
+    VLA_TRY(gemm(r, "vit.patch", w.h, d.kp_pad, m->patch_w, n * rows, dv, d.kp_pad, e, 0, fr1(rows)));
   }
   int pend = 0;
   const float* pbias = nullptr;
   for (int l = 0; l < c.vit_layers; ++l) {
     const VitLayer& L = m->vit[l];
-    VLA_TRY(norm(r, w.xv, rows, dv, pend, pbias, L.ln1_g, L.ln1_b, false, w.h));
-    VLA_TRY(gemm(r, "vit.qkv", w.h, dv, L.qkv_w, rows, 3 * dv, dv, epi_kind(EPI_T, w.qkv, 3 * dv, m->f32(L.qkv_b))));
+    VLA_TRY(norm(r, w.xv, n * rows, dv, pend, pbias, L.ln1_g, L.ln1_b, false, w.h));
+    VLA_TRY(gemm(r, "vit.qkv", w.h, dv, L.qkv_w, n * rows, 3 * dv, dv,
+                 epi_kind(EPI_T, w.qkv, 3 * dv, m->f32(L.qkv_b)), 0, fr1(rows)));
     AttnDesc a{};
     a.dtype = m->dt;
     a.q = w.qkv;
@@ -783,60 +858,69 @@ static int run_prefill(const Run& r, const vla_frame* f, vla_ctx* ctx) {
     a.Sq = d.tview;
     a.nq = a.nkv = c.vit_heads;
     a.hd = d.vhd;
-    a.segs = c.n_views;
+    a.segs = nv;
+    a.plan_segs = c.n_views;
     a.seg_q = a.seg_kv = (long long)d.tview * 3 * dv;
     a.seg_o = (long long)d.tview * dv;
     VLA_TRY(attn(r, "vit.attn", a));
     int so = 0;
-    VLA_TRY(gemm_part(r, "vit.o", w.att, dv, L.o_w, rows, dv, dv, &so));
-    VLA_TRY(norm(r, w.xv, rows, dv, so, m->f32(L.o_b), L.ln2_g, L.ln2_b, false, w.h));
-    VLA_TRY(gemm(r, "vit.fc1", w.h, dv, L.fc1_w, rows, c.vit_mlp, dv, epi_kind(EPI_GELU, w.mlp, c.vit_mlp, m->f32(L.fc1_b))));
-    VLA_TRY(gemm_part(r, "vit.fc2", w.mlp, c.vit_mlp, L.fc2_w, rows, dv, c.vit_mlp, &pend));
+    VLA_TRY(gemm_part(r, "vit.o", w.att, dv, L.o_w, n * rows, dv, dv, &so, fr1(rows)));
+    VLA_TRY(norm(r, w.xv, n * rows, dv, so, m->f32(L.o_b), L.ln2_g, L.ln2_b, false, w.h));
+    VLA_TRY(gemm(r, "vit.fc1", w.h, dv, L.fc1_w, n * rows, c.vit_mlp, dv,
+                 epi_kind(EPI_GELU, w.mlp, c.vit_mlp, m->f32(L.fc1_b)), 0, fr1(rows)));
+    VLA_TRY(gemm_part(r, "vit.fc2", w.mlp, c.vit_mlp, L.fc2_w, n * rows, dv, c.vit_mlp, &pend, fr1(rows)));
     pbias = m->f32(L.fc2_b);
   }
   {
     // final LayerNorm; the pixel shuffle (if any) is the norm's output placement
-    NormDesc n;
-    n.x = w.xv;
-    n.ldx = dv;
-    n.rows = rows;
-    n.d = dv;
-    n.splits = pend;
-    n.bias = pbias;
-    n.g = m->f32(m->post_g);
-    n.b = m->f32(m->post_b);
-    n.out = w.h;
-    n.ldo = d.kproj;
-    n.shuffle = c.shuffle;
-    n.grid_w = d.gw;
-    n.tview = d.tview;
-    VLA_TRY(run_norm(r, n));
+    NormDesc nd;
+    nd.x = w.xv;
+    nd.ldx = dv;
+    nd.rows = n * rows;
+    nd.d = dv;
+    nd.splits = pend;
+    nd.bias = pbias;
+    nd.g = m->f32(m->post_g);
+    nd.b = m->f32(m->post_b);
+    nd.out = w.h;
+    nd.ldo = d.kproj;
+    nd.shuffle = c.shuffle;
+    nd.grid_w = d.gw;
+    nd.tview = d.tview;
+    VLA_TRY(run_norm(r, nd));
   }
-  // prefix: [projected image tokens; text * sqrt(d); state projection]
-  VLA_TRY(gemm(r, "proj", w.h, d.kproj, m->proj_w, d.nimg, dl, d.kproj,
-               epi_kind(EPI_F32, w.xl, dl, m->f32(m->proj_b))));
-  HIP_TRY(launch_embed(m->dt, m->tptr(m->embed), dl, c.vocab, f->text_ids, c.n_text, std::sqrt((float)dl),
-                       w.xl + (size_t)d.nimg * dl, dl, r.st));
-  if (c.state_dim > 0) {
-    HIP_TRY(launch_cvt_pad(m->dt, f->state, 1, c.state_dim, w.sbuf, d.s_pad, false, nullptr, r.st));
-    VLA_TRY(gemm(r, "state", w.sbuf, d.s_pad, m->state_w, 1, dl, d.s_pad,
-                 epi_kind(EPI_F32, w.xl + (size_t)(d.prefix - 1) * dl, dl, m->f32(m->state_b))));
+  // prefix of frame i at rows i * P: [projected image tokens; text * sqrt(d);
+  // state projection]
+  for (int i = 0; i < n; ++i) {
+    float* xl = w.xl + (size_t)i * P * dl;
+    VLA_TRY(gemm(r, "proj", (char*)w.h + (size_t)i * d.nimg * d.kproj * m->esz, d.kproj, m->proj_w, d.nimg,
+                 dl, d.kproj, epi_kind(EPI_F32, xl, dl, m->f32(m->proj_b))));
+    HIP_TRY(launch_embed(m->dt, m->tptr(m->embed), dl, c.vocab, f[i].text_ids, c.n_text, std::sqrt((float)dl),
+                         xl + (size_t)d.nimg * dl, dl, r.st));
+    if (c.state_dim > 0) {
+      void* sb = (char*)w.sbuf + (size_t)i * d.s_pad * m->esz;
+      HIP_TRY(launch_cvt_pad(m->dt, f[i].state, 1, c.state_dim, sb, d.s_pad, false, nullptr, r.st));
+      VLA_TRY(gemm(r, "state", sb, d.s_pad, m->state_w, 1, dl, d.s_pad,
+                   epi_kind(EPI_F32, xl + (size_t)(P - 1) * dl, dl, m->f32(m->state_b))));
+    }
   }
-  // LM prefill writing the cache
+  // LM prefill writing the caches
   const size_t layer_k = ctx_layer_k(m) * m->esz;
   const size_t layer_v = ctx_layer_v(m) * m->esz;
+  const size_t kstride = ctx_kbytes(m) / m->esz, vstride = ctx_vbytes(m) / m->esz;
   pend = 0;
   const bool dit = c.head == VLA_HEAD_DIT;
+  vla_ctx* ctx = ctxs[0];
   for (int l = 0; l < c.lm_layers; ++l) {
     void* K = (char*)ctx->K + l * layer_k;
     void* V = (char*)ctx->V + l * layer_v;
-    VLA_TRY(decoder_layer(r, true, m->lm[l], w.xl, d.prefix, dl, c.lm_mlp, w.h, w.qkv, K, V, 0, nullptr,
-                          nullptr, 0, w.att, w.mlp, !dit && l == c.lm_layers - 1, &pend));
+    VLA_TRY(decoder_layer(r, true, m->lm[l], w.xl, P, dl, c.lm_mlp, w.h, w.qkv, K, V, 0, nullptr, nullptr, 0,
+                          w.att, w.mlp, !dit && l == c.lm_layers - 1, &pend, n, kstride, vstride));
   }
   if (dit) {
     // features = final RMSNorm of the last layer; then the cross K/V of every
     // even DiT layer, once per frame
-    VLA_TRY(norm(r, w.xl, d.prefix, dl, pend, nullptr, m->lm_fin_g, -1, true, w.h));
+    VLA_TRY(norm(r, w.xl, n * P, dl, pend, nullptr, m->lm_fin_g, -1, true, w.h));
     const size_t xe = cross_elems(m) * m->esz;
     for (int l = 0; l < c.ex_layers; l += 2) {
       Epi e;
@@ -847,11 +931,17 @@ static int run_prefill(const Run& r, const vla_frame* f, vla_ctx* ctx) {
       e.k = (char*)ctx->XK + (l / 2) * xe;
       e.v = (char*)ctx->XV + (l / 2) * xe;
       e.kv_nb = d.prefix_pad / 32;
-      VLA_TRY(gemm(r, "dit.cross_kv", w.h, dl, m->dit[l].kv, d.prefix, 2 * c.ex_dim, dl, e));
+      if (n > 1) {
+        e.blk_rows = P;
+        e.blk_k = e.blk_v = ctx_xbytes(m) / m->esz;
+      }
+      VLA_TRY(gemm(r, "dit.cross_kv", w.h, dl, m->dit[l].kv, n * P, 2 * c.ex_dim, dl, e, 0, fr1(P)));
     }
   }
   return VLA_OK;
 }
+
+static int run_prefill(const Run& r, const vla_frame* f, vla_ctx* ctx) { return run_prefill_n(r, f, 1, &ctx); }
 
 // GR00T-style DiT head (Euler steps as in run_denoise): tokens = W_a x + b_a +
 // positions; per layer, adaLN-modulated LayerNorm (gain 1 + scale, shift
@@ -955,7 +1045,7 @@ static int run_denoise_dit(const Run& r, const vla_ctx* ctx, const float* noise,
   return VLA_OK;
 }
 
-// The flow-matching loop of `frames` frames together (frames <= 2; noise
+// The flow-matching loop of `frames` frames together (at most MAX_ACT_BATCH; noise
 // and x hold the frames' chunks one after another): the frames' rows share
 // every weight load, and each frame's result equals its own run bit for bit.
 static int run_denoise_n(const Run& r, const vla_ctx* const* ctxs, int frames, const float* noise, float* x) {
@@ -964,7 +1054,7 @@ static int run_denoise_n(const Run& r, const vla_ctx* const* ctxs, int frames, c
     if (frames != 1) return fail(VLA_EINVAL, "batched action phases: pi0-style head only");
     return run_denoise_dit(r, ctxs[0], noise, x);
   }
-  if (frames < 1 || frames > MAX_ACT_BATCH) return fail(VLA_EINVAL, "frames per action phase: 1 or 2");
+  if (frames < 1 || frames > MAX_ACT_BATCH) return fail(VLA_EINVAL, "frames per action phase: 1 to " + std::to_string(MAX_ACT_BATCH));
   const vla_config& c = m->c;
   const Dims& d = m->d;
   ActWs& w = *r.aw;
@@ -994,8 +1084,8 @@ static int run_denoise_n(const Run& r, const vla_ctx* const* ctxs, int frames, c
     VLA_TRY(gemm(r, "ex.time2", w.hid, de, m->t2_w, H, de, de, et2, 0, frm(w.blk_de)));
     int pend = 0;
     for (int l = 0; l < c.ex_layers; ++l) {
-      const void* K[MAX_ACT_BATCH] = {nullptr, nullptr};
-      const void* V[MAX_ACT_BATCH] = {nullptr, nullptr};
+      const void* K[MAX_ACT_BATCH] = {};
+      const void* V[MAX_ACT_BATCH] = {};
       for (int f = 0; f < frames; ++f) {
         K[f] = (const char*)ctxs[f]->K + l * layer_k;
         V[f] = (const char*)ctxs[f]->V + l * layer_v;
@@ -1032,15 +1122,19 @@ struct ScratchNeed {
   size_t floats = 0;
 };
 
-static ScratchNeed gemm_scratch(int dt, int M, int N, int K, bool part = false, bool frag = false) {
-  GemmDesc g{dt, nullptr, K, nullptr, K, M, N, K, Epi()};
+// (frames: that many frames' rows stacked, split-K planned for one frame)
+static ScratchNeed gemm_scratch(int dt, int M, int N, int K, bool part = false, bool frag = false,
+                                int frames = 1) {
+  GemmDesc g{dt, nullptr, K, nullptr, K, M * frames, N, K, Epi()};
+  g.plan_m = M;
   if (part) g.epi.kind = EPI_PART;
   if (frag) g.frag_ks = (K + frag_slab(dt) - 1) / frag_slab(dt);
   const GemmPlan p = plan_gemm(g);
   return ScratchNeed{p.scratch_floats};
 }
 
-static ScratchNeed attn_scratch(int dt, int Sq, int nq, int nkv, int hd, int S0, int S1, int segs) {
+static ScratchNeed attn_scratch(int dt, int Sq, int nq, int nkv, int hd, int S0, int S1, int segs,
+                                int plan_segs = 0) {
   AttnDesc a{};
   a.dtype = dt;
   a.Sq = Sq;
@@ -1050,6 +1144,7 @@ static ScratchNeed attn_scratch(int dt, int Sq, int nq, int nkv, int hd, int S0,
   a.S0 = S0;
   a.S1 = S1;
   a.segs = segs;
+  a.plan_segs = plan_segs;
   return ScratchNeed{attn_scratch_floats(a)};
 }
 
@@ -1213,46 +1308,75 @@ static int add_act_lane(vla_model* m) {
   return VLA_OK;
 }
 
-static int add_vlm_lane(vla_model* m) {
+// A VLM lane for up to `cap` frames per prefill. Lane `slot` is replaced when
+// it exists (after the device is idle); its cached prefill graphs go with it.
+static int make_vlm_lane(vla_model* m, int cap, int slot) {
   const vla_config& c = m->c;
   const Dims& d = m->d;
   const int dt = m->dt;
   const size_t e = m->esz;
-  const int rv = d.rows_v, P = d.prefix;
+  const size_t rv = (size_t)cap * d.rows_v, P = (size_t)cap * d.prefix;
   const int dv = c.vit_dim, dl = c.lm_dim;
   std::unique_ptr<VlmWs> lane(new VlmWs());
   VlmWs& v = *lane;
-  const int rmax = std::max(rv, P);
-  VLA_TRY(dmalloc(m, (void**)&v.xv, (size_t)rv * dv * 4));
-  VLA_TRY(dmalloc(m, (void**)&v.xl, (size_t)P * dl * 4));
-  VLA_TRY(dmalloc(m, &v.h, (size_t)rmax * std::max({d.kp_pad, dv, dl}) * e));
-  VLA_TRY(dmalloc(m, &v.qkv, (size_t)std::max((size_t)rv * 3 * dv, (size_t)P * d.qd) * e));
-  VLA_TRY(dmalloc(m, &v.att, (size_t)std::max((size_t)rv * dv, (size_t)P * d.qd) * e));
-  VLA_TRY(dmalloc(m, &v.mlp, (size_t)std::max((size_t)rv * c.vit_mlp, (size_t)P * c.lm_mlp) * e));
-  VLA_TRY(dmalloc(m, &v.sbuf, (size_t)d.s_pad * e));
+  v.cap = cap;
+  auto alloc = [&](void** p, size_t bytes) {
+    hipError_t err = hipMalloc(p, std::max<size_t>(bytes, 256));
+    if (err != hipSuccess) return fail(VLA_ENOMEM, std::string("hipMalloc: ") + hipGetErrorString(err));
+    v.mem.push_back(*p);
+    return VLA_OK;
+  };
+  const size_t rmax = std::max(rv, P);
+  VLA_TRY(alloc((void**)&v.xv, rv * dv * 4));
+  VLA_TRY(alloc((void**)&v.xl, P * dl * 4));
+  VLA_TRY(alloc(&v.h, rmax * std::max({d.kp_pad, dv, dl}) * e));
+  VLA_TRY(alloc(&v.qkv, std::max(rv * 3 * dv, P * d.qd) * e));
+  VLA_TRY(alloc(&v.att, std::max(rv * dv, P * d.qd) * e));
+  VLA_TRY(alloc(&v.mlp, std::max(rv * c.vit_mlp, P * c.lm_mlp) * e));
+  VLA_TRY(alloc(&v.sbuf, (size_t)cap * d.s_pad * e));
+  // split partials of all frames' rows (splits planned for one frame)
   ScratchNeed sv;
   auto upd = [](ScratchNeed& s, ScratchNeed x) { s.floats = std::max(s.floats, x.floats); };
-  upd(sv, gemm_scratch(dt, rv, dv, d.kp_pad));
-  upd(sv, gemm_scratch(dt, rv, 3 * dv, dv));
-  upd(sv, gemm_scratch(dt, rv, dv, dv, true));
-  upd(sv, gemm_scratch(dt, rv, c.vit_mlp, dv));
-  upd(sv, gemm_scratch(dt, rv, dv, c.vit_mlp, true));
+  const int r1 = d.rows_v, p1 = d.prefix;
+  upd(sv, gemm_scratch(dt, r1, dv, d.kp_pad, false, false, cap));
+  upd(sv, gemm_scratch(dt, r1, 3 * dv, dv, false, false, cap));
+  upd(sv, gemm_scratch(dt, r1, dv, dv, true, false, cap));
+  upd(sv, gemm_scratch(dt, r1, c.vit_mlp, dv, false, false, cap));
+  upd(sv, gemm_scratch(dt, r1, dv, c.vit_mlp, true, false, cap));
   upd(sv, gemm_scratch(dt, d.nimg, dl, d.kproj));
-  if (c.head == VLA_HEAD_DIT) upd(sv, gemm_scratch(dt, P, 2 * c.ex_dim, dl));
+  if (c.head == VLA_HEAD_DIT) upd(sv, gemm_scratch(dt, p1, 2 * c.ex_dim, dl, false, false, cap));
   upd(sv, gemm_scratch(dt, 1, dl, d.s_pad));
-  upd(sv, gemm_scratch(dt, P, d.qkv_n, dl));
-  upd(sv, gemm_scratch(dt, P, dl, d.qd, true));
-  upd(sv, gemm_scratch(dt, P, 2 * c.lm_mlp, dl));
-  upd(sv, gemm_scratch(dt, P, dl, c.lm_mlp, true));
-  upd(sv, attn_scratch(dt, d.tview, c.vit_heads, c.vit_heads, d.vhd, d.tview, 0, c.n_views));
-  upd(sv, attn_scratch(dt, P, c.lm_heads, c.lm_kv_heads, c.head_dim, P, 0, 1));
-  VLA_TRY(alloc_scratch(m, sv, &v.scr));
-  VLA_TRY(dmalloc(m, (void**)&v.pstage, (size_t)c.n_views * c.img_h * c.img_w * 3 * 4));
-  VLA_TRY(dmalloc(m, (void**)&v.istage, (size_t)std::max(c.n_text, 1) * 4));
-  VLA_TRY(dmalloc(m, (void**)&v.sstage, (size_t)std::max(c.state_dim, 1) * 4));
-  m->vws.push_back(std::move(lane));
+  upd(sv, gemm_scratch(dt, p1, d.qkv_n, dl, false, false, cap));
+  upd(sv, gemm_scratch(dt, p1, dl, d.qd, true, false, cap));
+  upd(sv, gemm_scratch(dt, p1, 2 * c.lm_mlp, dl, false, false, cap));
+  upd(sv, gemm_scratch(dt, p1, dl, c.lm_mlp, true, false, cap));
+  upd(sv, attn_scratch(dt, d.tview, c.vit_heads, c.vit_heads, d.vhd, d.tview, 0, cap * c.n_views, c.n_views));
+  upd(sv, attn_scratch(dt, p1, c.lm_heads, c.lm_kv_heads, c.head_dim, p1, 0, 1));
+  if (sv.floats) {
+    VLA_TRY(alloc((void**)&v.scr.ptr, sv.floats * 4));
+    v.scr.floats = sv.floats;
+  }
+  VLA_TRY(alloc((void**)&v.pstage, (size_t)cap * c.n_views * c.img_h * c.img_w * 3 * 4));
+  VLA_TRY(alloc((void**)&v.istage, (size_t)cap * std::max(c.n_text, 1) * 4));
+  VLA_TRY(alloc((void**)&v.sstage, (size_t)cap * std::max(c.state_dim, 1) * 4));
+  if (slot < (int)m->vws.size()) {
+    HIP_TRY(hipDeviceSynchronize());
+    for (auto it = m->pre_graphs.begin(); it != m->pre_graphs.end();) {
+      if (std::get<0>(it->first) == slot) {
+        hipGraphExecDestroy(it->second);
+        it = m->pre_graphs.erase(it);
+      } else {
+        ++it;
+      }
+    }
+    m->vws[slot] = std::move(lane);
+  } else {
+    m->vws.push_back(std::move(lane));
+  }
   return VLA_OK;
 }
+
+static int add_vlm_lane(vla_model* m) { return make_vlm_lane(m, 1, (int)m->vws.size()); }
 
 static int setup_workspaces(vla_model* m) {
   VLA_TRY(add_vlm_lane(m));
@@ -1318,36 +1442,53 @@ static int create_impl(const vla_config* cfg, uint64_t seed, vla_model** out) {
 // Pipeline
 // ---------------------------------------------------------------------------
 
-static int ctx_create_impl(vla_model* m, vla_ctx** out) {
-  std::unique_ptr<vla_ctx> c(new vla_ctx());
-  c->m = m;
-  const size_t kbytes = (size_t)m->c.lm_layers * ctx_layer_k(m) * m->esz;
-  const size_t vbytes = (size_t)m->c.lm_layers * ctx_layer_v(m) * m->esz;
-  hipError_t e = hipMalloc(&c->K, kbytes);
-  if (e == hipSuccess) e = hipMemset(c->K, 0, kbytes);  // padding stays zero
-  if (e != hipSuccess) {
-    hipFree(c->K);
-    return fail(VLA_ENOMEM, "ctx K: allocation failed");
-  }
-  e = hipMalloc(&c->V, vbytes);
-  if (e == hipSuccess) e = hipMemset(c->V, 0, vbytes);
-  if (e == hipSuccess && m->c.head == VLA_HEAD_DIT) {
-    const size_t xbytes = (size_t)((m->c.ex_layers + 1) / 2) * cross_elems(m) * m->esz;
-    e = hipMalloc(&c->XK, xbytes);
-    if (e == hipSuccess) e = hipMemset(c->XK, 0, xbytes);
-    if (e == hipSuccess) e = hipMalloc(&c->XV, xbytes);
-    if (e == hipSuccess) e = hipMemset(c->XV, 0, xbytes);
-  }
-  if (e != hipSuccess) {
+static void ctx_free(vla_ctx* c) {
+  if (!c) return;
+  if (c->own) {
     hipFree(c->K);
     hipFree(c->V);
     hipFree(c->XK);
     hipFree(c->XV);
-    return fail(VLA_ENOMEM, "ctx V / cross K/V: allocation failed");
   }
-  *out = c.release();
+  delete c;
+}
+
+// n contexts whose buffers are consecutive slices of one zeroed allocation
+// each (context i at i times the context size), so a batched prefill reaches
+// frame i's cache at a fixed stride. out[0] owns the allocations.
+static int ctx_create_n(vla_model* m, int n, vla_ctx** out) {
+  const size_t kb = ctx_kbytes(m), vb = ctx_vbytes(m), xb = ctx_xbytes(m);
+  void *K = nullptr, *V = nullptr, *XK = nullptr, *XV = nullptr;
+  auto zalloc = [](void** p, size_t bytes) {
+    hipError_t e = hipMalloc(p, bytes);
+    if (e == hipSuccess) e = hipMemset(*p, 0, bytes);  // padding stays zero
+    return e;
+  };
+  hipError_t e = zalloc(&K, n * kb);
+  if (e == hipSuccess) e = zalloc(&V, n * vb);
+  if (e == hipSuccess && xb) e = zalloc(&XK, n * xb);
+  if (e == hipSuccess && xb) e = zalloc(&XV, n * xb);
+  if (e != hipSuccess) {
+    hipFree(K);
+    hipFree(V);
+    hipFree(XK);
+    hipFree(XV);
+    return fail(VLA_ENOMEM, std::string("context buffers: ") + hipGetErrorString(e));
+  }
+  for (int i = 0; i < n; ++i) {
+    vla_ctx* c = new vla_ctx();
+    c->m = m;
+    c->own = i == 0;
+    c->K = (char*)K + i * kb;
+    c->V = (char*)V + i * vb;
+    c->XK = xb ? (char*)XK + i * xb : nullptr;
+    c->XV = xb ? (char*)XV + i * xb : nullptr;
+    out[i] = c;
+  }
   return VLA_OK;
 }
+
+static int ctx_create_impl(vla_model* m, vla_ctx** out) { return ctx_create_n(m, 1, out); }
 
 static void cu_mask(int first, int count, int total, std::vector<uint32_t>& mask) {
   mask.assign((total + 31) / 32, 0u);
@@ -1423,23 +1564,29 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
   if (vlanes > MAX_VLM_STREAMS) return fail(VLA_EINVAL, "vlm_streams must be <= 2");
   if (vlanes > 1 && s.mode == VLA_MODE_SERIAL) return fail(VLA_EINVAL, "vlm_streams > 1 needs a concurrent mode");
   const int B = std::max(1, s.act_batch);
-  if (B > MAX_ACT_BATCH) return fail(VLA_EINVAL, "act_batch must be <= 2");
+  if (B > MAX_ACT_BATCH) return fail(VLA_EINVAL, "act_batch must be <= " + std::to_string(MAX_ACT_BATCH));
   if (B > 1 && m->c.head != VLA_HEAD_PI0) return fail(VLA_EINVAL, "act_batch > 1: pi0-style action head only");
+  const int Bv = std::max(1, s.vlm_batch);
+  if (Bv > MAX_VLM_BATCH || CTX_BLOCK % Bv) return fail(VLA_EINVAL, "vlm_batch must be 1, 2, 4 or 8");
   const vla_config& c = m->c;
   for (int r = 0; r < R; ++r)
     if (!frames[r].pixels || (c.n_text > 0 && !frames[r].text_ids) || (c.state_dim > 0 && !frames[r].state))
       return fail(VLA_EINVAL, "frame " + std::to_string(r) + " has a NULL input");
   std::lock_guard<std::mutex> lock(m->mu);
-  // a context is in flight from its prefill until its action phase ends;
-  // frames go to action phases in groups of B consecutive frames
-  const int nctx = B * (lanes + vlanes);
+  // A context is in flight from its prefill until its action phase ends.
+  // Prefills go in groups of Bv consecutive frames (consecutive contexts of
+  // one block), action phases in groups of B. The ring holds whole blocks and
+  // at least Bv + B contexts, so a prefill only ever waits for action phases
+  // of frames before its own group.
+  const int nctx = rnd_up(Bv * vlanes + B * lanes + std::max(Bv, B), CTX_BLOCK);
   while ((int)m->pctx.size() < nctx) {
-    vla_ctx* cx = nullptr;
-    VLA_TRY(ctx_create_impl(m, &cx));
-    m->pctx.push_back(cx);
+    vla_ctx* blk[CTX_BLOCK];
+    VLA_TRY(ctx_create_n(m, CTX_BLOCK, blk));
+    for (vla_ctx* cx : blk) m->pctx.push_back(cx);
   }
   while ((int)m->aws.size() < lanes) VLA_TRY(add_act_lane(m));
-  while ((int)m->vws.size() < vlanes) VLA_TRY(add_vlm_lane(m));
+  for (int vi = 0; vi < vlanes; ++vi)
+    if (vi >= (int)m->vws.size() || m->vws[vi]->cap < Bv) VLA_TRY(make_vlm_lane(m, Bv, vi));
   Streams st;
   VLA_TRY(get_streams(m, s, &st));
   if (s.mode == VLA_MODE_SERIAL) st.a[0] = st.v[0];
@@ -1450,86 +1597,106 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
     HIP_TRY(hipEventCreate(&e));
     m->ev.push_back(e);
   }
-  // events: [4r] VLM start, [4r+1] VLM end, [4r+2] action start, [4r+3] action end
+  // events: [4r] VLM start, [4r+1] VLM end, [4r+2] action start, [4r+3]
+  // action end; a group's time is recorded on its first frame, the others
+  // get an empty interval at the group's end
   LaunchCaps vcaps{}, acaps{};
   if (s.mode == VLA_MODE_WG_CAPPED) vcaps.max_wgs = s.vlm_wg_cap * m->num_cus;
   const size_t chunk = (size_t)c.chunk_len * c.action_dim;
   const size_t pix_bytes = (size_t)c.n_views * c.img_h * c.img_w * 3 * 4;
+  auto vlane = [&](int r) { return (r / Bv) % vlanes; };  // VLM lane of frame r
+  auto alane = [&](int r) { return (r / B) % lanes; };    // action lane of frame r
   HIP_TRY(hipDeviceSynchronize());
 
-  if (graphs) {  // capture what is missing (outside the timed loop)
-    for (int vi = 0; vi < vlanes; ++vi) {
+  if (graphs) {  // capture what this run needs and is missing (outside the timed loop)
+    for (int g0 = 0; g0 < R; g0 += Bv) {
+      const int n = std::min(Bv, R - g0), vi = vlane(g0), ci = g0 % nctx;
+      const auto key = std::make_tuple(vi, ci, vcaps.max_wgs, n);
+      if (m->pre_graphs.count(key)) continue;
       VlmWs* vw = m->vws[vi].get();
-      vla_frame staged{vw->pstage, vw->istage, c.state_dim > 0 ? vw->sstage : nullptr};
-      for (int ci = 0; ci < nctx; ++ci) {
-        const auto key = std::make_tuple(vi, ci, vcaps.max_wgs);
-        if (m->pre_graphs.count(key)) continue;
-        Run rv{m, st.v[vi], vcaps, &vw->scr, nullptr, vw};
-        hipGraphExec_t ge = nullptr;
-        VLA_TRY(capture(st.v[vi], [&] { return run_prefill(rv, &staged, m->pctx[ci]); }, &ge));
-        m->pre_graphs[key] = ge;
-      }
+      vla_frame staged[MAX_VLM_BATCH];
+      for (int i = 0; i < n; ++i)
+        staged[i] = vla_frame{vw->pstage + i * pix_bytes / 4, vw->istage + (size_t)i * std::max(c.n_text, 1),
+                              c.state_dim > 0 ? vw->sstage + (size_t)i * c.state_dim : nullptr};
+      Run rv{m, st.v[vi], vcaps, &vw->scr, nullptr, vw};
+      hipGraphExec_t ge = nullptr;
+      VLA_TRY(capture(st.v[vi], [&] { return run_prefill_n(rv, staged, n, &m->pctx[ci]); }, &ge));
+      m->pre_graphs[key] = ge;
     }
-    // one graph per (lane, first context, frames): a group of n frames uses
-    // contexts ci .. ci + n - 1 (groups start at multiples of B)
-    for (int li = 0; li < lanes; ++li)
-      for (int ci = 0; ci < nctx; ci += B)
-        for (int n = 1; n <= B; ++n) {
-          const auto key = std::make_tuple(li, ci, n);
-          if (m->den_graphs.count(key)) continue;
-          ActWs* aw = m->aws[li].get();
-          Run ra{m, st.a[li], acaps, &aw->scr, aw};
-          const vla_ctx* cs[MAX_ACT_BATCH] = {m->pctx[ci], n > 1 ? m->pctx[ci + 1] : nullptr};
-          hipGraphExec_t ge = nullptr;
-          VLA_TRY(capture(st.a[li], [&] { return run_denoise_n(ra, cs, n, aw->nstage, aw->xg); }, &ge));
-          m->den_graphs[key] = ge;
-        }
+    // one graph per (lane, first context, frames): the group of frames
+    // g0 .. g0 + n - 1 uses contexts g0 % nctx .. + n - 1
+    for (int g0 = 0; g0 < R; g0 += B) {
+      const int n = std::min(B, R - g0), li = alane(g0), ci = g0 % nctx;
+      const auto key = std::make_tuple(li, ci, n);
+      if (m->den_graphs.count(key)) continue;
+      ActWs* aw = m->aws[li].get();
+      Run ra{m, st.a[li], acaps, &aw->scr, aw};
+      const vla_ctx* cs[MAX_ACT_BATCH] = {};
+      for (int f = 0; f < n; ++f) cs[f] = m->pctx[ci + f];
+      hipGraphExec_t ge = nullptr;
+      VLA_TRY(capture(st.a[li], [&] { return run_denoise_n(ra, cs, n, aw->nstage, aw->xg); }, &ge));
+      m->den_graphs[key] = ge;
+    }
   }
 
   const auto t0 = std::chrono::steady_clock::now();
-  for (int r = 0; r < R; ++r) {
-    const int ci = r % nctx, li = (r / B) % lanes, vi = r % vlanes;
-    vla_ctx* ctx = m->pctx[ci];
-    hipStream_t sv = st.v[vi], sa = st.a[li];
+  int next_act = 0;  // first frame whose action phase is not issued yet
+  for (int g0 = 0; g0 < R; g0 += Bv) {
+    const int n = std::min(Bv, R - g0), vi = vlane(g0), ci = g0 % nctx;
+    hipStream_t sv = st.v[vi];
     VlmWs* vw = m->vws[vi].get();
-    // the context is free once the action phase that last read it is done
-    if (r >= nctx && sv != sa) HIP_TRY(hipStreamWaitEvent(sv, m->ev[4 * (r - nctx) + 3], 0));
-    HIP_TRY(hipEventRecord(m->ev[4 * r], sv));
+    // a context is free once the action phase that last read it is done
+    for (int q = g0; q < g0 + n; ++q)
+      if (q >= nctx && sv != st.a[alane(q - nctx)]) HIP_TRY(hipStreamWaitEvent(sv, m->ev[4 * (q - nctx) + 3], 0));
+    HIP_TRY(hipEventRecord(m->ev[4 * g0], sv));
     if (graphs) {
-      HIP_TRY(hipMemcpyAsync(vw->pstage, frames[r].pixels, pix_bytes, hipMemcpyDeviceToDevice, sv));
-      if (c.n_text > 0)
-        HIP_TRY(hipMemcpyAsync(vw->istage, frames[r].text_ids, (size_t)c.n_text * 4, hipMemcpyDeviceToDevice, sv));
-      if (c.state_dim > 0)
-        HIP_TRY(hipMemcpyAsync(vw->sstage, frames[r].state, (size_t)c.state_dim * 4, hipMemcpyDeviceToDevice, sv));
-      HIP_TRY(hipGraphLaunch(m->pre_graphs[std::make_tuple(vi, ci, vcaps.max_wgs)], sv));
+      for (int i = 0; i < n; ++i) {
+        const vla_frame& fr = frames[g0 + i];
+        HIP_TRY(hipMemcpyAsync(vw->pstage + i * pix_bytes / 4, fr.pixels, pix_bytes, hipMemcpyDeviceToDevice, sv));
+        if (c.n_text > 0)
+          HIP_TRY(hipMemcpyAsync(vw->istage + (size_t)i * c.n_text, fr.text_ids, (size_t)c.n_text * 4,
+                                 hipMemcpyDeviceToDevice, sv));
+        if (c.state_dim > 0)
+          HIP_TRY(hipMemcpyAsync(vw->sstage + (size_t)i * c.state_dim, fr.state, (size_t)c.state_dim * 4,
+                                 hipMemcpyDeviceToDevice, sv));
+      }
+      HIP_TRY(hipGraphLaunch(m->pre_graphs[std::make_tuple(vi, ci, vcaps.max_wgs, n)], sv));
     } else {
       Run rv{m, sv, vcaps, &vw->scr, nullptr, vw};
-      VLA_TRY(run_prefill(rv, &frames[r], ctx));
+      VLA_TRY(run_prefill_n(rv, &frames[g0], n, &m->pctx[ci]));
     }
-    HIP_TRY(hipEventRecord(m->ev[4 * r + 1], sv));
-    // the action phase of a group starts when its last frame's prefill ends
-    const int g0 = r / B * B, n = std::min(B, R - g0);
-    if (r != g0 + n - 1) continue;
-    for (int q = g0; q <= r; ++q)
-      if (st.v[q % vlanes] != sa) HIP_TRY(hipStreamWaitEvent(sa, m->ev[4 * q + 1], 0));
-    HIP_TRY(hipEventRecord(m->ev[4 * g0 + 2], sa));
-    ActWs* aw = m->aws[li].get();
-    const int c0 = g0 % nctx;
-    if (graphs) {
-      HIP_TRY(hipMemcpyAsync(aw->nstage, noise + g0 * chunk, n * chunk * 4, hipMemcpyDeviceToDevice, sa));
-      HIP_TRY(hipGraphLaunch(m->den_graphs[std::make_tuple(li, c0, n)], sa));
-      HIP_TRY(hipMemcpyAsync(actions + g0 * chunk, aw->xg, n * chunk * 4, hipMemcpyDeviceToDevice, sa));
-    } else {
-      Run ra{m, sa, acaps, &aw->scr, aw};
-      const vla_ctx* cs[MAX_ACT_BATCH] = {m->pctx[c0], n > 1 ? m->pctx[c0 + 1] : nullptr};
-      VLA_TRY(run_denoise_n(ra, cs, n, noise + g0 * chunk, actions + g0 * chunk));
+    HIP_TRY(hipEventRecord(m->ev[4 * g0 + 1], sv));
+    for (int q = g0 + 1; q < g0 + n; ++q) {
+      HIP_TRY(hipEventRecord(m->ev[4 * q], sv));
+      HIP_TRY(hipEventRecord(m->ev[4 * q + 1], sv));
     }
-    HIP_TRY(hipEventRecord(m->ev[4 * g0 + 3], sa));
-    // the group's other frames get an empty action interval at its end (the
-    // group's time is counted once) and the same end for context reuse
-    for (int q = g0 + 1; q <= r; ++q) {
-      HIP_TRY(hipEventRecord(m->ev[4 * q + 2], sa));
-      HIP_TRY(hipEventRecord(m->ev[4 * q + 3], sa));
+    // every action group whose frames are all prefilled starts now
+    while (next_act < R) {
+      const int a0 = next_act, na = std::min(B, R - a0);
+      if (a0 + na > g0 + n) break;
+      next_act += na;
+      const int li = alane(a0);
+      hipStream_t sa = st.a[li];
+      for (int q = a0; q < a0 + na; ++q)
+        if (st.v[vlane(q)] != sa) HIP_TRY(hipStreamWaitEvent(sa, m->ev[4 * q + 1], 0));
+      HIP_TRY(hipEventRecord(m->ev[4 * a0 + 2], sa));
+      ActWs* aw = m->aws[li].get();
+      const int c0 = a0 % nctx;
+      if (graphs) {
+        HIP_TRY(hipMemcpyAsync(aw->nstage, noise + a0 * chunk, na * chunk * 4, hipMemcpyDeviceToDevice, sa));
+        HIP_TRY(hipGraphLaunch(m->den_graphs[std::make_tuple(li, c0, na)], sa));
+        HIP_TRY(hipMemcpyAsync(actions + a0 * chunk, aw->xg, na * chunk * 4, hipMemcpyDeviceToDevice, sa));
+      } else {
+        Run ra{m, sa, acaps, &aw->scr, aw};
+        const vla_ctx* cs[MAX_ACT_BATCH] = {};
+        for (int f = 0; f < na; ++f) cs[f] = m->pctx[c0 + f];
+        VLA_TRY(run_denoise_n(ra, cs, na, noise + a0 * chunk, actions + a0 * chunk));
+      }
+      HIP_TRY(hipEventRecord(m->ev[4 * a0 + 3], sa));
+      for (int q = a0 + 1; q < a0 + na; ++q) {
+        HIP_TRY(hipEventRecord(m->ev[4 * q + 2], sa));
+        HIP_TRY(hipEventRecord(m->ev[4 * q + 3], sa));
+      }
     }
   }
   for (int vi = 0; vi < vlanes; ++vi) HIP_TRY(hipStreamSynchronize(st.v[vi]));
@@ -1592,13 +1759,8 @@ int vla_destroy(vla_model* m) {
     hipDeviceSynchronize();
     for (auto& kv : m->pre_graphs) hipGraphExecDestroy(kv.second);
     for (auto& kv : m->den_graphs) hipGraphExecDestroy(kv.second);
-    for (vla_ctx* cx : m->pctx) {
-      hipFree(cx->K);
-      hipFree(cx->V);
-      hipFree(cx->XK);
-      hipFree(cx->XV);
-      delete cx;
-    }
+    // members of a block first, its owner last
+    for (auto it = m->pctx.rbegin(); it != m->pctx.rend(); ++it) ctx_free(*it);
     auto drop = [](Streams& st) {
       for (hipStream_t v : st.v)
         if (v) hipStreamDestroy(v);
@@ -1631,11 +1793,7 @@ int vla_ctx_create(vla_model* m, vla_ctx** out) {
 int vla_ctx_destroy(vla_ctx* c) {
   ABI_GUARD({
     if (!c) return VLA_OK;
-    hipFree(c->K);
-    hipFree(c->V);
-    hipFree(c->XK);
-    hipFree(c->XV);
-    delete c;
+    ctx_free(c);
     return VLA_OK;
   })
 }

@@ -248,6 +248,17 @@ def test_pi0_full_size_vs_oracle(V):
         g.say("pi0 full size: pipeline, batched action phases, graphs")
         batched = _pipeline_frames(g, m, cfg, frs, act_batch=2, act_streams=1)
         assert np.array_equal(batched, piped)
+        # all three frames in one action loop (a group of four cut short)
+        g.say("pi0 full size: pipeline, three frames in one action loop, graphs")
+        batched = _pipeline_frames(g, m, cfg, frs, act_batch=4, act_streams=1)
+        assert np.array_equal(batched, piped)
+        # and in one prefill pass as well (every cache and chunk bit for bit)
+        g.say("pi0 full size: pipeline, three frames in one prefill and one action loop, graphs")
+        batched = _pipeline_frames(g, m, cfg, frs, act_batch=4, vlm_batch=4, act_streams=1)
+        assert np.array_equal(batched, piped)
+        g.say("pi0 full size: pipeline, prefills in pairs, no graphs")
+        batched = _pipeline_frames(g, m, cfg, frs, vlm_batch=2, graphs=False)
+        assert np.array_equal(batched, piped)
     g.say("pi0 full size: oracle")
     P = synth.make_params(cfg, 0)
     cap = {}
@@ -267,9 +278,8 @@ def _pipeline_frames(g, m, cfg, frames, **kw):
     dfs = [g.DevFrame(f) for f in frames]
     noise = torch.stack([d.noise for d in dfs]).contiguous()
     out = torch.full_like(noise, float("nan"))
-    kw = dict(dict(act_streams=2), **kw)
-    g.V.vla_pipeline_run(m, [d.c for d in dfs], noise, len(frames), mode="concurrent", actions=out,
-                         graphs=True, **kw)
+    kw = dict(dict(act_streams=2, graphs=True), **kw)
+    g.V.vla_pipeline_run(m, [d.c for d in dfs], noise, len(frames), mode="concurrent", actions=out, **kw)
     torch.cuda.synchronize()
     return out.cpu().numpy()
 
@@ -289,7 +299,10 @@ def test_pi0_three_views_full_size_vs_oracle(V):
         got, kv = g.run_frame(m, cfg, frames[0])
         g.say("pi0 three views full size: pipeline, two action lanes, graphs")
         piped = _pipeline_frames(g, m, cfg, frames)
+        g.say("pi0 three views full size: pipeline, both frames in one prefill and one action loop")
+        batched = _pipeline_frames(g, m, cfg, frames, vlm_batch=2, act_batch=2, act_streams=1)
     assert np.array_equal(piped[0].astype(np.float64), got)
+    assert np.array_equal(batched, piped)
     g.say("pi0 three views full size: oracle")
     P = synth.make_params(cfg, 0)
     cap = {}
@@ -315,6 +328,13 @@ def test_gr00t_full_size_vs_oracle(V):
     with g.model(cfg, 0) as m:
         cross = {}
         got, kv = g.run_frame(m, cfg, fr, cross=cross)
+        # two frames in one prefill pass (features and cross K/V per frame)
+        g.say("gr00t full size: pipeline, two frames in one prefill, graphs")
+        frs = [fr, synth.make_frame(cfg, 0, 1)]
+        got1, _ = g.run_frame(m, cfg, frs[1])
+        batched = _pipeline_frames(g, m, cfg, frs, vlm_batch=2)
+        assert np.array_equal(batched[0].astype(np.float64), got)
+        assert np.array_equal(batched[1].astype(np.float64), got1)
     g.say("gr00t full size: oracle")
     P = synth.make_params(cfg, 0)
     cap = {}
@@ -395,7 +415,13 @@ def test_pipeline_modes_bit_identical(V, cfg):
                  ("cu_masked", dict(split, act_streams=2, graphs=True)),
                  ("concurrent", dict(vlm_streams=2, act_streams=2)),
                  ("concurrent", dict(vlm_streams=2, act_streams=3, graphs=True)),
-                 ("wg_capped", dict(vlm_wg_cap=1, graphs=True))]
+                 ("wg_capped", dict(vlm_wg_cap=1, graphs=True)),
+                 # several robots' prefills as one pass (R = 7: groups of two
+                 # and a last single frame; four and three; all seven)
+                 ("serial", dict(vlm_batch=2)), ("concurrent", dict(vlm_batch=4, graphs=True)),
+                 ("concurrent", dict(vlm_batch=2, vlm_streams=2, act_streams=2, graphs=True)),
+                 ("cu_masked", dict(split, vlm_batch=4)), ("wg_capped", dict(vlm_wg_cap=1, vlm_batch=2)),
+                 ("concurrent", dict(vlm_batch=8))]
         if cfg["head"] == synth.HEAD_PI0:
             # two robots' action phases as one batched loop (R = 7: the last
             # frame runs alone)
@@ -403,10 +429,26 @@ def test_pipeline_modes_bit_identical(V, cfg):
                       ("concurrent", dict(act_batch=2, graphs=True)),
                       ("concurrent", dict(act_batch=2, act_streams=2, graphs=True)),
                       ("cu_masked", dict(split, act_batch=2, graphs=True)),
-                      ("concurrent", dict(act_batch=2, vlm_streams=2, act_streams=2))]
+                      ("concurrent", dict(act_batch=2, vlm_streams=2, act_streams=2)),
+                      # groups of four (the last one of three) and all seven at once
+                      ("concurrent", dict(act_batch=4, graphs=True)),
+                      ("concurrent", dict(act_batch=4, act_streams=2, graphs=True)),
+                      ("serial", dict(act_batch=8)),
+                      ("concurrent", dict(act_batch=8, graphs=True)),
+                      # both phases batched, groups of different sizes
+                      ("concurrent", dict(act_batch=4, vlm_batch=4, graphs=True)),
+                      ("concurrent", dict(act_batch=4, vlm_batch=2, act_streams=2, graphs=True)),
+                      ("concurrent", dict(act_batch=2, vlm_batch=4, act_streams=2))]
+            with pytest.raises(V.VlaError):
+                V.vla_pipeline_run(m, [d.c for d in dfs], noise, R, mode="concurrent", act_batch=9,
+                                   actions=torch.empty_like(noise))
         else:
             with pytest.raises(V.VlaError):
                 V.vla_pipeline_run(m, [d.c for d in dfs], noise, R, mode="concurrent", act_batch=2,
+                                   actions=torch.empty_like(noise))
+        for bad in (3, 16):
+            with pytest.raises(V.VlaError):
+                V.vla_pipeline_run(m, [d.c for d in dfs], noise, R, mode="concurrent", vlm_batch=bad,
                                    actions=torch.empty_like(noise))
         standalone = [g.run_frame(m, cfg, f)[0] for f in frames]
         for mode, kw in modes:
