@@ -38,13 +38,15 @@ HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 MFMA, TFLOP/s
 
 
-def kernel_work(cfg, tag):
+def kernel_work(cfg, tag, vlm_frames=1, act_frames=1):
     """Algorithmic bytes and flops of one launch of a tagged kernel: weights,
     the A operand and the output (plus the fp32 residual read and write for
-    residual epilogues) each moved once; flops = 2 M N K."""
+    residual epilogues) each moved once; flops = 2 M N K. A batched prefill
+    stacks vlm_frames frames' rows into M, a batched action loop act_frames."""
     import synth
     d = synth.derived(cfg)
-    H, P = cfg["chunk_len"], d["prefix"]
+    H, P = cfg["chunk_len"] * act_frames, d["prefix"] * vlm_frames
+    vit_rows = cfg["n_views"] * d["tokens_per_view"] * vlm_frames  # ViT rows (before any pixel shuffle)
     qd, kvd = cfg["lm_heads"] * cfg["head_dim"], cfg["lm_kv_heads"] * cfg["head_dim"]
     shapes = {  # tag: (M, N, K, output bytes per element, residual?)
         "ex.gateup": (H, 2 * cfg["ex_mlp"], cfg["ex_dim"], 2, False),
@@ -55,8 +57,8 @@ def kernel_work(cfg, tag):
         "lm.down": (P, cfg["lm_dim"], cfg["lm_mlp"], 4, True),
         "lm.qkv": (P, qd + 2 * kvd, cfg["lm_dim"], 2, False),
         "lm.o": (P, cfg["lm_dim"], qd, 4, True),
-        "vit.fc1": (d["n_img"], cfg["vit_mlp"], cfg["vit_dim"], 2, False),
-        "vit.fc2": (d["n_img"], cfg["vit_dim"], cfg["vit_mlp"], 4, True),
+        "vit.fc1": (vit_rows, cfg["vit_mlp"], cfg["vit_dim"], 2, False),
+        "vit.fc2": (vit_rows, cfg["vit_dim"], cfg["vit_mlp"], 4, True),
     }
     M, N, K, ob, resid = shapes[tag]
     nout = N // 2 if tag.endswith("gateup") else N
@@ -132,12 +134,12 @@ def cpu_baseline(cfg, seed):
                       f"denoising, fp64 NumPy, {dt:.1f} s", "seconds": dt}, chunk
 
 
-def measured_traffic(preset, R, kernel):
+def measured_traffic(preset, R, kernel, schedule):
     """HBM bytes per launch of `kernel` from the committed counter record
     (FETCH_SIZE + WRITE_SIZE, each scaled by a plain copy's reading), or
-    None when the record is for another workload or the kernel source has
-    changed since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", f"{kernel.replace('.', '_')}_{preset}_R{R}_traffic.json")
+    None when the record is for another workload or schedule, or the kernel
+    source has changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"{kernel.replace('.', '_')}_{preset}_R{R}_{schedule}_traffic.json")
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
@@ -169,10 +171,13 @@ def main():
                                        "concurrent_graph,lanes2_graph,lanes3_graph,batch2_graph,"
                                        "batch2_lanes2_graph,batch4_graph,batch4_lanes2_graph,batch8_graph,"
                                        "vb2_ab2_graph,vb2_ab2_lanes2_graph,vb2_ab4_graph,vb4_ab4_graph,"
-                                       "vb4_ab2_lanes2_graph,vb4_ab4_lanes2_graph,vb8_ab8_graph")
+                                       "vb4_ab2_lanes2_graph,vb4_ab4_lanes2_graph,vb8_ab8_graph,"
+                                       "vb8_ab4_lanes2_graph,vb4_ab4_v2_lanes2_graph")
     ap.add_argument("--split", default="192,64", help="CU split VLM,action for cu_masked")
     ap.add_argument("--wg-cap", type=int, default=2, help="VLM workgroups per CU for wg_capped")
-    ap.add_argument("--kernel", default="ex.gateup", help="tag of the kernel timed for the roofline")
+    ap.add_argument("--kernel", default="auto",
+                    help="tag of the kernel timed for the roofline (auto: of the candidate tags, the one "
+                         "with the most GPU time in the reported schedule)")
     ap.add_argument("--preset", default="pi0")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--extra", default="gr00t:8:serial,concurrent,cu_masked,lanes2_graph,v2_lanes2_graph;"
@@ -244,6 +249,11 @@ def main():
                                                      act_streams=2, graphs=True)
             kw[f"vb{v_}_ab{a_}_cu_192_64"] = dict(mode="cu_masked", vlm_cus=192, act_cus=64, vlm_batch=v_,
                                                   act_batch=a_, graphs=True)
+            for l_ in (3, 4):
+                kw[f"vb{v_}_ab{a_}_lanes{l_}_graph"] = dict(mode="concurrent", vlm_batch=v_, act_batch=a_,
+                                                           act_streams=l_, graphs=True)
+            kw[f"vb{v_}_ab{a_}_v2_lanes2_graph"] = dict(mode="concurrent", vlm_batch=v_, act_batch=a_,
+                                                        vlm_streams=2, act_streams=2, graphs=True)
     for b_ in (4, 8):  # larger groups of robots per action loop
         kw[f"batch{b_}_graph"] = dict(mode="concurrent", act_batch=b_, graphs=True)
         kw[f"batch{b_}_lanes2_graph"] = dict(mode="concurrent", act_batch=b_, act_streams=2, graphs=True)
@@ -293,7 +303,21 @@ def main():
         ser = results.get("serial", {}).get("frames_per_s")
         for mode in results:
             results[mode]["speedup_vs_serialized"] = (results[mode]["frames_per_s"] / ser) if ser else None
-        identical = all(np.array_equal(outputs[m0], outputs[modes[0]]) for m0 in outputs)
+        # Batched action loops (groups of >= 2 frames) run tiled GEMMs over
+        # the stacked rows: identical among themselves, within the oracle
+        # tolerance of the one-frame path; every other schedule is identical
+        # to the one-frame path.
+        def grp(mode):
+            b = kw[mode].get("act_batch", 1)
+            return "batched" if b > 1 and R % b != 1 else "one_frame"
+        identical = {}
+        for g_ in ("one_frame", "batched"):
+            ms_ = [m0 for m0 in outputs if grp(m0) == g_]
+            if ms_:
+                identical[g_] = all(np.array_equal(outputs[m0], outputs[ms_[0]]) for m0 in ms_)
+        a_, b_ = [[outputs[m0] for m0 in outputs if grp(m0) == g_] for g_ in ("one_frame", "batched")]
+        if a_ and b_:
+            identical["max_abs_diff_batched_vs_one_frame"] = float(np.abs(a_[0] - b_[0]).max())
         return cfg, m, results, outputs, identical, (cframes, noise, actions)
 
     cfg, m, results, outputs, identical, (cframes, noise, actions) = measure(
@@ -316,24 +340,35 @@ def main():
             residency[name] = {"whole_run": full, "overlap_window": ovl, "records": int(n)}
         V.vla_wavelog_enable(m, 0)
 
-    # dominant kernel, timed live with HIP events on its stream (serial schedule)
-    print(f"[bench] kernel timer on {args.kernel}", file=sys.stderr, flush=True)
-    V.vla_kernel_timer(m, args.kernel)
-    for _ in range(args.steps):
-        V.vla_pipeline_run(m, cframes, noise, R, mode="serial", actions=actions)
-    tot_ms, launches = V.vla_kernel_timer_read(m)
-    V.vla_kernel_timer(m, None)
+    # dominant kernel of the reported schedule, timed live with HIP events
+    # on its own stream (the timer replays the schedule without graphs; the
+    # kernels and their grids are the same)
+    sargs = kw[args.mode]
+    tags = [args.kernel] if args.kernel != "auto" else ["lm.gateup", "lm.down", "ex.gateup", "ex.down", "vit.fc1"]
+    timed = {}
+    for tag in tags:
+        print(f"[bench] kernel timer on {tag} in {args.mode}", file=sys.stderr, flush=True)
+        V.vla_kernel_timer(m, tag)
+        for _ in range(args.steps):
+            V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **sargs)
+        timed[tag] = V.vla_kernel_timer_read(m)
+        V.vla_kernel_timer(m, None)
+    kernel = max(timed, key=lambda k: timed[k][0])
+    tot_ms, launches = timed[kernel]
     avg_s = tot_ms * 1e-3 / max(launches, 1)
-    byts, flops = kernel_work(cfg, args.kernel)
+    vfr, afr = max(1, sargs.get("vlm_batch", 1)), max(1, sargs.get("act_batch", 1))
+    byts, flops = kernel_work(cfg, kernel, vfr if kernel.startswith(("lm.", "vit.")) else 1,
+                              afr if kernel.startswith("ex.") else 1)
     hbm_bound = flops / byts < BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
     if hbm_bound:
         ach, peak, unit = byts / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
     else:
         ach, peak, unit = flops / avg_s / 1e12, BF16_PEAK_TFLOPS, "TFLOP/s"
     roofline = {"bound": "hbm" if hbm_bound else "mfma", "achieved": ach, "peak": peak, "unit": unit,
-                "frac": ach / peak, "traffic": measured_traffic(args.preset, R, args.kernel), "kernel": args.kernel,
-                "avg_us": avg_s * 1e6, "launches": launches,
-                "algorithmic_bytes": byts, "flops": flops}
+                "frac": ach / peak, "traffic": measured_traffic(args.preset, R, kernel, args.mode),
+                "kernel": kernel, "schedule": args.mode, "avg_us": avg_s * 1e6, "launches": launches,
+                "algorithmic_bytes": byts, "flops": flops,
+                "gpu_ms_per_step_by_tag": {k: v[0] / args.steps for k, v in timed.items()}}
     outs = outputs[args.mode]
     V.vla_destroy(m)
     del cframes, noise, actions

@@ -287,6 +287,10 @@ hipError_t launch_cvt_pad(int dtype, const float* src, int rows, int cols, void*
                           bool afrag, float* dst_f32, hipStream_t st, int blk_rows = 0,
                           size_t blk_elems = 0);
 
+// Row-major copy of a weight stored in MFMA fragment order: out[n * K + k] =
+// W[frag_index(n, k, KS)] for n < N, k < K (operand type; K a multiple of 8).
+hipError_t launch_unfrag(int dtype, const void* frag, int N, int K, int KS, void* out, hipStream_t st);
+
 // dst[r, :] = row (operand type) for every r < rows.
 hipError_t launch_bcast_row(int dtype, const void* row, int cols, void* dst, int ld_dst, int rows,
                             hipStream_t st);

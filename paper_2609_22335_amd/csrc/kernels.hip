@@ -590,6 +590,35 @@ __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, size_t 
   VLA_WAVE_END(KK_SKINNY);
 }
 
+// Row-major copy of a fragment-ordered weight: one thread per 16-byte piece
+// (VEC consecutive k of one row n, which the fragment order keeps together).
+template <typename T>
+__global__ __launch_bounds__(256) void k_unfrag(const T* __restrict__ Wf, int N, int K, int KS,
+                                                T* __restrict__ out) {
+  constexpr int VEC = 16 / sizeof(T), SW = 4 * VEC;
+  const int kv = K / VEC;
+  const long long total = (long long)N * kv;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    const int n = (int)(i / kv), k = (int)(i % kv) * VEC;
+    const size_t frag = (size_t)(n / 16) * KS + k / SW;
+    const int lane = n % 16 + 16 * ((k % SW) / VEC);
+    *(uint4*)(out + (size_t)n * K + k) = *(const uint4*)(Wf + (frag * 64 + lane) * VEC);
+  }
+}
+
+hipError_t launch_unfrag(int dtype, const void* frag, int N, int K, int KS, void* out, hipStream_t st) {
+  const int vec = dtype == DT_BF16 ? 8 : 4;
+  if (N <= 0 || K <= 0 || K % vec || KS * frag_slab(dtype) < K) return hipErrorInvalidValue;
+  const long long total = (long long)N * (K / vec);
+  const int grid = (int)std::min<long long>((total + 255) / 256, 8192);
+  if (dtype == DT_BF16)
+    k_unfrag<uint16_t><<<grid, 256, 0, st>>>((const uint16_t*)frag, N, K, KS, (uint16_t*)out);
+  else
+    k_unfrag<float><<<grid, 256, 0, st>>>((const float*)frag, N, K, KS, (float*)out);
+  return hipGetLastError();
+}
+
 size_t frag_index(int n, int k, int KS, int dtype) {
   const int vec = dtype == DT_BF16 ? 8 : 4, sw = 4 * vec;
   const size_t frag = (size_t)(n / 16) * KS + k / sw;

@@ -304,6 +304,15 @@ struct vla_model {
   float* fada = nullptr;
   float* dpos = nullptr;
 
+  // Row-major copies of the expert layers' matrices (qkv, o, gate/up, down)
+  // for batched action loops, made on first use from the fragment-ordered
+  // weights; one allocation.
+  struct WideLayer {
+    const void *qkv = nullptr, *o = nullptr, *gu = nullptr, *down = nullptr;
+  };
+  std::vector<WideLayer> exw;
+  void* exw_mem = nullptr;
+
   // phase scratch
   std::vector<std::unique_ptr<VlmWs>> vws;  // VLM lanes; lane 0 serves standalone calls
   WaveLog* wlog = nullptr;                  // residency log (measurement), device memory
@@ -617,6 +626,22 @@ static int gemm(const Run& r, const char* tag, const void* A, int lda, int W, in
   return VLA_OK;
 }
 
+// C = A W^T with W a row-major [N][ldw] matrix in device memory (not a model
+// tensor id): the batched action loop's row-major expert weights.
+static int gemm_rm(const Run& r, const char* tag, const void* A, int lda, const void* W, int ldw, int M, int N,
+                   int K, const Epi& e, Frames fr = Frames()) {
+  vla_model* m = r.m;
+  GemmDesc g{m->dt, A, lda, W, ldw, M, N, K, e};
+  g.plan_m = fr.plan_m;
+  LaunchCaps caps = r.caps;
+  VLA_TRY(timer_events(r, tag, &caps));
+  hipError_t err = launch_gemm(g, *r.scr, caps, r.st);
+  if (err != hipSuccess)
+    return fail(VLA_EHIP, std::string("gemm ") + std::to_string(M) + "x" + std::to_string(N) + "x" +
+                              std::to_string(K) + ": " + hipGetErrorString(err));
+  return VLA_OK;
+}
+
 static int attn_kv(const Run& r, const char* tag, const AttnKvDesc& a) {
   LaunchCaps caps = r.caps;
   VLA_TRY(timer_events(r, tag, &caps));
@@ -667,6 +692,19 @@ static int norm(const Run& r, float* x, int rows, int d, int splits, const float
 
 // GEMM whose result is added to the residual stream by the next norm: the raw
 // result (or its split-K partials) goes to the phase scratch.
+static int gemm_part_rm(const Run& r, const char* tag, const void* A, int lda, const void* W, int ldw, int M,
+                        int N, int K, int* splits, Frames fr) {
+  vla_model* m = r.m;
+  Epi e;
+  e.kind = EPI_PART;
+  e.out = r.scr->ptr;
+  e.ldo = (int)std::min<size_t>(r.scr->floats, (size_t)INT32_MAX);
+  GemmDesc g{m->dt, A, lda, W, ldw, M, N, K, e};
+  g.plan_m = fr.plan_m;
+  *splits = plan_gemm(g).splits;
+  return gemm_rm(r, tag, A, lda, W, ldw, M, N, K, e, fr);
+}
+
 static int gemm_part(const Run& r, const char* tag, const void* A, int lda, int W, int M, int N,
                      int K, int* splits, Frames fr = Frames()) {
   vla_model* m = r.m;
@@ -693,30 +731,37 @@ static Epi epi_kind(int kind, void* out = nullptr, int ldo = 0, const float* bia
 // RMSNorm (after adding O) -> GeGLU -> down. The down projection is left
 // pending in the scratch (*pend = its split count) for the next norm.
 // Several frames may run together, `rows` rows each:
-//  * expert layers (a batched action phase): frame f reads the past K/V
-//    kpast[f] / vpast[f] and the action workspace's per-frame blocks;
 //  * LM layers (a batched prefill): x holds the frames' rows one after
 //    another, frame f's own K/V (its cache) sit kstride / vstride elements
-//    after frame f - 1's, and the split-K factors are those of one frame.
+//    after frame f - 1's;
+//  * expert layers of a batched action loop, wide (wl set): the same
+//    stacked rows and row-major operands, the tiled GEMM over all frames'
+//    rows with the row-major copies of the layer's matrices in *wl;
+//  * otherwise expert layers take frame blocks in the row-block operand
+//    layout (skinny GEMMs, one launch for all frames).
+// Frame f of a batched expert layer reads the past K/V kpast[f] / vpast[f]
+// and the action workspace's per-frame blocks. Stacked rows get the split-K
+// factors of one frame, so a frame's result does not depend on how many
+// frames share the launch.
 static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int rows, int dim, int mlp,
                          void* h, void* q, void* kout, void* vout, int pos0, const void* const* kpast,
                          const void* const* vpast, int npast, void* att, void* mlpbuf, bool kv_only,
-                         int* pend, int frames = 1, size_t kstride = 0, size_t vstride = 0) {
+                         int* pend, int frames = 1, size_t kstride = 0, size_t vstride = 0,
+                         const vla_model::WideLayer* wl = nullptr) {
   vla_model* m = r.m;
   const vla_config& c = m->c;
   const Dims& d = m->d;
-  // the expert's activations feed skinny GEMMs: row-block operand layout
-  const bool af = !lm;
-  const bool fb = frames > 1;  // frame blocks
+  const bool wide = !lm && wl;
+  const bool stacked = lm || wide;  // row-major operands, frames' rows stacked into M
+  const bool af = !stacked;         // skinny operands: row-block operand layout
+  const bool fb = frames > 1;       // frame blocks
   const ActWs* aw = r.aw;
-  if (fb && !lm && !aw) return fail(VLA_EINVAL, "batched frames: expert layers need an action workspace");
-  if (fb && lm && (kstride == 0 || vstride == 0)) return fail(VLA_EINVAL, "batched prefill: cache strides");
-  // GEMM rows and frames: the LM stacks the frames' rows into one M (splits
-  // planned for one frame); the skinny expert GEMMs take frame blocks
-  const int gm = lm ? frames * rows : rows;
+  if (!lm && fb && !aw) return fail(VLA_EINVAL, "batched frames: expert layers need an action workspace");
+  if (lm && fb && (kstride == 0 || vstride == 0)) return fail(VLA_EINVAL, "batched prefill: cache strides");
+  const int gm = stacked ? frames * rows : rows;
   auto frm = [&](size_t a_blk) {
     Frames f;
-    if (lm) {
+    if (stacked) {
       f.plan_m = rows;
     } else {
       f.n = frames;
@@ -724,8 +769,9 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
     }
     return f;
   };
-  const int nblk = fb && !lm ? rows : 0;  // norm output frame blocks (operand layout)
-  const size_t nblk_out = fb && !lm ? aw->blk_de : 0;
+  const bool skin_fb = fb && !stacked;  // skinny frame blocks
+  const int nblk = skin_fb ? rows : 0;   // norm output frame blocks (operand layout)
+  const size_t nblk_out = skin_fb ? aw->blk_de : 0;
   VLA_TRY(norm(r, x, frames * rows, dim, *pend, nullptr, L.rms1, -1, true, h, af, nblk, nblk_out));
   *pend = 0;
   Epi e;
@@ -746,7 +792,11 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
     e.blk_k = lm ? kstride : aw->blk_k;
     e.blk_v = lm ? vstride : aw->blk_v;
   }
-  VLA_TRY(gemm(r, lm ? "lm.qkv" : "ex.qkv", h, dim, L.qkv, gm, d.qkv_n, dim, e, 0, frm(fb && !lm ? aw->blk_de : 0)));
+  const char* tq = lm ? "lm.qkv" : "ex.qkv";
+  if (wide)
+    VLA_TRY(gemm_rm(r, tq, h, dim, wl->qkv, dim, gm, d.qkv_n, dim, e, frm(0)));
+  else
+    VLA_TRY(gemm(r, tq, h, dim, L.qkv, gm, d.qkv_n, dim, e, 0, frm(skin_fb ? aw->blk_de : 0)));
   if (kv_only) return VLA_OK;
   AttnKvDesc a{};
   a.dtype = m->dt;
@@ -788,22 +838,32 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
     }
     a.k1_blk = aw->blk_k;
     a.v1_blk = aw->blk_v;
-    a.out_blk = aw->blk_att;
+    a.out_blk = wide ? (size_t)rows * d.qd : aw->blk_att;
   }
   VLA_TRY(attn_kv(r, lm ? "lm.attn" : "ex.attn", a));
   int so = 0;
-  VLA_TRY(gemm_part(r, lm ? "lm.o" : "ex.o", att, d.qd, L.o, gm, dim, d.qd, &so, frm(fb && !lm ? aw->blk_att : 0)));
+  const char* to = lm ? "lm.o" : "ex.o";
+  if (wide)
+    VLA_TRY(gemm_part_rm(r, to, att, d.qd, wl->o, d.qd, gm, dim, d.qd, &so, frm(0)));
+  else
+    VLA_TRY(gemm_part(r, to, att, d.qd, L.o, gm, dim, d.qd, &so, frm(skin_fb ? aw->blk_att : 0)));
   VLA_TRY(norm(r, x, frames * rows, dim, so, nullptr, L.rms2, -1, true, h, af, nblk, nblk_out));
   Epi eg = epi_kind(EPI_GEGLU, mlpbuf, mlp);
   eg.afrag = af;
-  if (fb && !lm) {
+  if (skin_fb) {
     eg.blk_rows = rows;
     eg.blk_out = aw->blk_mlp;
   }
-  VLA_TRY(gemm(r, lm ? "lm.gateup" : "ex.gateup", h, dim, L.gu, gm, 2 * mlp, dim, eg, 0,
-               frm(fb && !lm ? aw->blk_de : 0)));
-  VLA_TRY(gemm_part(r, lm ? "lm.down" : "ex.down", mlpbuf, mlp, L.down, gm, dim, mlp, pend,
-                    frm(fb && !lm ? aw->blk_mlp : 0)));
+  const char* tg = lm ? "lm.gateup" : "ex.gateup";
+  if (wide)
+    VLA_TRY(gemm_rm(r, tg, h, dim, wl->gu, dim, gm, 2 * mlp, dim, eg, frm(0)));
+  else
+    VLA_TRY(gemm(r, tg, h, dim, L.gu, gm, 2 * mlp, dim, eg, 0, frm(skin_fb ? aw->blk_de : 0)));
+  const char* td = lm ? "lm.down" : "ex.down";
+  if (wide)
+    VLA_TRY(gemm_part_rm(r, td, mlpbuf, mlp, wl->down, mlp, gm, dim, mlp, pend, frm(0)));
+  else
+    VLA_TRY(gemm_part(r, td, mlpbuf, mlp, L.down, gm, dim, mlp, pend, frm(skin_fb ? aw->blk_mlp : 0)));
   return VLA_OK;
 }
 
@@ -1045,6 +1105,48 @@ static int run_denoise_dit(const Run& r, const vla_ctx* ctx, const float* noise,
   return VLA_OK;
 }
 
+// Row-major copies of the expert layers' matrices for batched action loops
+// (converted on the device from the fragment-ordered weights, once). Not
+// while a graph is being captured.
+static int ensure_wide(vla_model* m) {
+  if (!m->exw.empty()) return VLA_OK;
+  const vla_config& c = m->c;
+  struct Item {
+    int t, N, K;
+  };
+  std::vector<Item> items;
+  for (const DecLayer& L : m->ex) {
+    const int de = c.ex_dim;
+    items.push_back({L.qkv, m->d.qkv_n, de});
+    items.push_back({L.o, de, m->d.qd});
+    items.push_back({L.gu, 2 * c.ex_mlp, de});
+    items.push_back({L.down, de, c.ex_mlp});
+  }
+  std::vector<size_t> off;
+  size_t total = 0;
+  for (const Item& it : items) {
+    off.push_back(total);
+    total += ((size_t)it.N * it.K * m->esz + 255) / 256 * 256;
+  }
+  HIP_TRY(hipMalloc(&m->exw_mem, total));
+  for (size_t i = 0; i < items.size(); ++i) {
+    const Item& it = items[i];
+    const DevTensor& t = m->T[it.t];
+    if (t.fks <= 0 || t.rows != it.N || t.ld != it.K) return fail(VLA_ESTATE, "expert weight layout");
+    HIP_TRY(launch_unfrag(m->dt, m->tptr(it.t), it.N, it.K, t.fks, (char*)m->exw_mem + off[i], nullptr));
+  }
+  HIP_TRY(hipDeviceSynchronize());
+  for (size_t l = 0; l < m->ex.size(); ++l) {
+    vla_model::WideLayer w;
+    w.qkv = (char*)m->exw_mem + off[4 * l];
+    w.o = (char*)m->exw_mem + off[4 * l + 1];
+    w.gu = (char*)m->exw_mem + off[4 * l + 2];
+    w.down = (char*)m->exw_mem + off[4 * l + 3];
+    m->exw.push_back(w);
+  }
+  return VLA_OK;
+}
+
 // The flow-matching loop of `frames` frames together (at most MAX_ACT_BATCH; noise
 // and x hold the frames' chunks one after another): the frames' rows share
 // every weight load, and each frame's result equals its own run bit for bit.
@@ -1055,6 +1157,7 @@ static int run_denoise_n(const Run& r, const vla_ctx* const* ctxs, int frames, c
     return run_denoise_dit(r, ctxs[0], noise, x);
   }
   if (frames < 1 || frames > MAX_ACT_BATCH) return fail(VLA_EINVAL, "frames per action phase: 1 to " + std::to_string(MAX_ACT_BATCH));
+  if (frames > 1 && m->exw.size() != m->ex.size()) return fail(VLA_ESTATE, "row-major expert weights missing");
   const vla_config& c = m->c;
   const Dims& d = m->d;
   ActWs& w = *r.aw;
@@ -1091,7 +1194,8 @@ static int run_denoise_n(const Run& r, const vla_ctx* const* ctxs, int frames, c
         V[f] = (const char*)ctxs[f]->V + l * layer_v;
       }
       VLA_TRY(decoder_layer(r, false, m->ex[l], w.u, H, de, c.ex_mlp, w.h, w.q, w.kown, w.vown, d.prefix,
-                            K, V, d.prefix, w.att, w.mlp, false, &pend, frames));
+                            K, V, d.prefix, w.att, w.mlp, false, &pend, frames, 0, 0,
+                            fb ? &m->exw[l] : nullptr));
     }
     VLA_TRY(norm(r, w.u, frames * H, de, pend, nullptr, m->fin_g, -1, true, w.h, true, blk, w.blk_de));
     Epi e;
@@ -1299,6 +1403,11 @@ static int add_act_lane(vla_model* m) {
   upd(sa, gemm_scratch(dt, F * H, de, d.qd, true, true));
   upd(sa, gemm_scratch(dt, F * H, 2 * c.ex_mlp, de, false, true));
   upd(sa, gemm_scratch(dt, F * H, de, c.ex_mlp, true, true));
+  // batched loops: tiled GEMMs over all frames' rows, splits of one frame
+  upd(sa, gemm_scratch(dt, H, d.qkv_n, de, false, false, F));
+  upd(sa, gemm_scratch(dt, H, de, d.qd, true, false, F));
+  upd(sa, gemm_scratch(dt, H, 2 * c.ex_mlp, de, false, false, F));
+  upd(sa, gemm_scratch(dt, H, de, c.ex_mlp, true, false, F));
   upd(sa, gemm_scratch(dt, F * H, c.action_dim, de, false, true));
   upd(sa, attn_scratch(dt, H, c.lm_heads, c.lm_kv_heads, c.head_dim, P, H, 1));
   VLA_TRY(alloc_scratch(m, sa, &a.scr));
@@ -1431,6 +1540,7 @@ static int create_impl(const vla_config* cfg, uint64_t seed, vla_model** out) {
   }
   if (rc != VLA_OK) {
     for (void* p : m->allocs) hipFree(p);
+    hipFree(m->exw_mem);
     hipFree(m->arena);
     return rc;
   }
@@ -1587,6 +1697,7 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
   while ((int)m->aws.size() < lanes) VLA_TRY(add_act_lane(m));
   for (int vi = 0; vi < vlanes; ++vi)
     if (vi >= (int)m->vws.size() || m->vws[vi]->cap < Bv) VLA_TRY(make_vlm_lane(m, Bv, vi));
+  if (B > 1) VLA_TRY(ensure_wide(m));
   Streams st;
   VLA_TRY(get_streams(m, s, &st));
   if (s.mode == VLA_MODE_SERIAL) st.a[0] = st.v[0];
@@ -1776,6 +1887,7 @@ int vla_destroy(vla_model* m) {
       hipFree(m->wlog);
     }
     for (void* p : m->allocs) hipFree(p);
+    hipFree(m->exw_mem);
     hipFree(m->arena);
     delete m;
     return VLA_OK;

@@ -244,25 +244,27 @@ def test_pi0_full_size_vs_oracle(V):
         frs = [fr] + [synth.make_frame(cfg, 0, r) for r in (1, 2)]
         piped = _pipeline_frames(g, m, cfg, frs)
         assert np.array_equal(piped[0].astype(np.float64), got)
-        # frames 0 and 1 as one batched action loop (the last frame runs alone)
-        g.say("pi0 full size: pipeline, batched action phases, graphs")
-        batched = _pipeline_frames(g, m, cfg, frs, act_batch=2, act_streams=1)
-        assert np.array_equal(batched, piped)
-        # all three frames in one action loop (a group of four cut short)
-        g.say("pi0 full size: pipeline, three frames in one action loop, graphs")
-        batched = _pipeline_frames(g, m, cfg, frs, act_batch=4, act_streams=1)
-        assert np.array_equal(batched, piped)
-        # and in one prefill pass as well (every cache and chunk bit for bit)
-        g.say("pi0 full size: pipeline, three frames in one prefill and one action loop, graphs")
-        batched = _pipeline_frames(g, m, cfg, frs, act_batch=4, vlm_batch=4, act_streams=1)
-        assert np.array_equal(batched, piped)
+        # prefills of several frames in one pass: every cache and chunk bit
+        # for bit
         g.say("pi0 full size: pipeline, prefills in pairs, no graphs")
-        batched = _pipeline_frames(g, m, cfg, frs, vlm_batch=2, graphs=False)
-        assert np.array_equal(batched, piped)
+        vb = _pipeline_frames(g, m, cfg, frs, vlm_batch=2, graphs=False)
+        assert np.array_equal(vb, piped)
+        # batched action loops (tiled GEMMs over the stacked rows): the same
+        # bits for a group of three (of four) and a pair, with or without a
+        # batched prefill; frame 2 of the pair schedule runs alone
+        g.say("pi0 full size: pipeline, three frames in one prefill and one action loop, graphs")
+        b4 = _pipeline_frames(g, m, cfg, frs, act_batch=4, vlm_batch=4, act_streams=1)
+        g.say("pi0 full size: pipeline, action loops in pairs, graphs")
+        b2 = _pipeline_frames(g, m, cfg, frs, act_batch=2, act_streams=1)
+        assert np.array_equal(b4[:2], b2[:2])
+        assert np.array_equal(b2[2], piped[2])
     g.say("pi0 full size: oracle")
     P = synth.make_params(cfg, 0)
     cap = {}
     want = O.forward(P, cfg, fr, cap)
+    err_b = float(np.abs(b4[0] - want).max())
+    print(f"[gpu] pi0 batched-loop chunk max abs err {err_b:.3e}", flush=True)
+    assert err_b <= CHUNK_TOL[synth.BF16]
     nkvd = cfg["lm_kv_heads"] * cfg["head_dim"]
     for l in (0, cfg["lm_layers"] - 1):
         rk = cap["kv"][l][0].reshape(-1, nkvd).ravel()
@@ -299,10 +301,12 @@ def test_pi0_three_views_full_size_vs_oracle(V):
         got, kv = g.run_frame(m, cfg, frames[0])
         g.say("pi0 three views full size: pipeline, two action lanes, graphs")
         piped = _pipeline_frames(g, m, cfg, frames)
+        g.say("pi0 three views full size: pipeline, both frames in one prefill")
+        vb = _pipeline_frames(g, m, cfg, frames, vlm_batch=2)
         g.say("pi0 three views full size: pipeline, both frames in one prefill and one action loop")
         batched = _pipeline_frames(g, m, cfg, frames, vlm_batch=2, act_batch=2, act_streams=1)
     assert np.array_equal(piped[0].astype(np.float64), got)
-    assert np.array_equal(batched, piped)
+    assert np.array_equal(vb, piped)
     g.say("pi0 three views full size: oracle")
     P = synth.make_params(cfg, 0)
     cap = {}
@@ -312,8 +316,10 @@ def test_pi0_three_views_full_size_vs_oracle(V):
         rk = cap["kv"][l][0].reshape(-1, nkvd).ravel()
         assert np.all(np.abs(kv[l][0] - rk) <= _kv_tol(cfg, rk)), l
     err = float(np.abs(got - want).max())
-    print(f"[gpu] pi0 three views chunk max abs err {err:.3e}", flush=True)
+    err_b = float(np.abs(batched[0] - want).max())
+    print(f"[gpu] pi0 three views chunk max abs err {err:.3e} (batched loop {err_b:.3e})", flush=True)
     assert err <= CHUNK_TOL[synth.BF16]
+    assert err_b <= CHUNK_TOL[synth.BF16]
 
 
 @pytest.mark.timeout(900)
@@ -460,16 +466,33 @@ def test_pipeline_modes_bit_identical(V, cfg):
                 assert t["frames_per_s"] > 0
                 results[f"{name}#{rep}"] = out.cpu().numpy()
                 g.run_frame(m, cfg, frames[rep])  # eager work between replays
+    # Frames of batched action loops (act_batch >= 2) run the tiled GEMMs
+    # over all frames' rows with one frame's splits: the same bits for every
+    # group size and schedule (a final group may hold a single frame, which
+    # runs the one-frame path); everything else equals the standalone calls.
     ref = results["serial#0"]
+    bref, bmulti = None, None
     for key, r in results.items():
-        assert np.array_equal(r, ref), key
+        if "act_batch=" not in key:
+            assert np.array_equal(r, ref), key
+            continue
+        b = int(key.split("act_batch=")[1].split("/")[0].split("#")[0])
+        multi = {i for i in range(R) if not (R % b == 1 and i == R - 1)}  # frames in groups of >= 2
+        if bref is None:
+            bref, bmulti = r, multi
+        both = sorted(multi & bmulti)
+        assert np.array_equal(r[both], bref[both]), key
+        alone = sorted(set(range(R)) - multi)
+        assert np.array_equal(r[alone], ref[alone]), key
     for i in range(R):
         assert np.array_equal(ref[i].astype(np.float64), standalone[i])
-    # and the pipeline is the oracle's function of each frame
+    # and the pipeline is the oracle's function of each frame, batched or not
     P = synth.make_params(cfg, 11)
     for i in (0, R - 1):
         want = O.forward(P, cfg, frames[i])
         assert np.abs(ref[i] - want).max() <= CHUNK_TOL[cfg["dtype"]]
+        if bref is not None:
+            assert np.abs(bref[i] - want).max() <= CHUNK_TOL[cfg["dtype"]]
 
 
 def test_abi_errors_on_device(V):
