@@ -298,7 +298,7 @@ template <typename T, int BM, int BN, int BK, int WGM = 2, int WGN = 2, int PD =
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A, int lda,
                                               const T* __restrict__ W, int ldw, int M, int N,
                                               int K, int kchunk, int splits, int tiles_m,
-                                              int tiles_n, Epi e, float* __restrict__ part) {
+                                              int tiles_n, int group_m, Epi e, float* __restrict__ part) {
   VLA_WAVE_BEGIN(KK_GEMM);
   using SM = GemmSmem<T, BM, BN, BK, WGM>;
   constexpr int VEC = SM::VEC;
@@ -328,12 +328,17 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
   // the workgroup index gives the same results.
   const int G = gridDim.x;
   const int first = G % 8 == 0 ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
+  const int plane = tiles_m * tiles_n;
   for (int tile = first; tile < ntiles; tile += G) {
-    // row tile fastest, then column tile, then K split: an XCD's range holds
-    // whole column blocks (each weight block read once) of few K splits
-    // (so it reads only those K ranges of A)
-    const int tm = tile % tiles_m, t2 = tile / tiles_m;
-    const int tn = t2 % tiles_n, s = t2 / tiles_n;
+    // K split slowest. Within a split, bands of group_m row tiles in turn;
+    // inside a band the row tile is fastest, then the column tile. The ~32
+    // tiles an XCD runs at once then share group_m row tiles of A and a few
+    // column tiles of W in its L2 (group_m = tiles_m, one band, when all of
+    // A fits in L2: each weight block is then read once per XCD).
+    const int s = tile / plane, r = tile % plane;
+    const int band = r / (group_m * tiles_n), tm0 = band * group_m;
+    const int gm = min(group_m, tiles_m - tm0), q = r - band * group_m * tiles_n;
+    const int tm = tm0 + q % gm, tn = q / gm;
     const int m0 = tm * BM, n0 = tn * BN;
     const int kbeg = s * kchunk, kend = min(K, kbeg + kchunk);
     const int nk = (kend - kbeg + BK - 1) / BK;
@@ -396,16 +401,17 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
           for (int j = 0; j < TN; ++j) acc[i][j] = mfma_step(af[i], bfg[j], acc[i][j], dummy);
       }
     };
-    // iteration it: tile it+1 (ring slot (it+1) % PD) goes to LDS, tile
-    // it+1+PD is requested into the freed slot, tile it is multiplied. Loads
-    // and stores are issued unconditionally (tiles past the end read as zero
-    // through the buffer range check), so every path has the same loads in
-    // flight and each wait covers only the oldest ring slot.
+    // iteration it: tile it is multiplied from LDS buffer it & 1 (its MFMAs
+    // run while the wave goes on), tile it+1 (ring slot (it+1) % PD) goes to
+    // the other buffer, tile it+1+PD is requested into the freed slot, then
+    // one barrier. Loads and stores are issued unconditionally (tiles past
+    // the end read as zero through the buffer range check), so every path has
+    // the same loads in flight and each wait covers only the oldest ring slot.
     auto step = [&](int it, uint4 (&xa)[AV], uint4 (&xb)[BV]) {
-      __syncthreads();
+      if (it < nk) compute(it & 1);
       sstore((it + 1) & 1, xa, xb);
       gload(kbeg + (it + 1 + PD) * BK, xa, xb);
-      if (it < nk) compute(it & 1);
+      __syncthreads();
     };
 
     __syncthreads();  // the previous tile's epilogue is done with the LDS
@@ -418,6 +424,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
       gload(kbeg + (1 + q) * BK, ra[(1 + q) % PD], rb[(1 + q) % PD]);
       __builtin_amdgcn_sched_barrier(0);
     }
+    __syncthreads();  // tile 0 is in LDS
     for (int it = 0; it < nk; it += PD) {
 #pragma unroll
       for (int q = 0; q < PD; ++q) step(it + q, ra[(q + 1) % PD], rb[(q + 1) % PD]);
@@ -736,10 +743,14 @@ static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch
   const int kchunk = ((kblocks + p.splits - 1) / p.splits) * BK;
   int grid = p.tiles;
   if (caps.max_wgs > 0) grid = std::min(grid, caps.max_wgs);
+  // row-tile bands sized so a band's A K-range takes about half of an XCD's
+  // 4 MB L2
+  const size_t band_bytes = (size_t)BM * kchunk * sizeof(T);
+  const int group_m = std::max(1, std::min(tiles_m, (int)((2u << 20) / std::max<size_t>(band_bytes, 1))));
   hipExtLaunchKernelGGL((k_gemm<T, BM, BN, BK, WGM, WGN, PD>), dim3(grid), dim3(64 * WGM * WGN), 0, st,
                         caps.ev_start,
                         caps.ev_stop, 0, (const T*)g.A, g.lda, (const T*)g.W, g.ldw, g.M, g.N,
-                        g.K, kchunk, p.splits, tiles_m, tiles_n, g.epi, s.ptr);
+                        g.K, kchunk, p.splits, tiles_m, tiles_n, group_m, g.epi, s.ptr);
   if (p.splits > 1 && g.epi.kind != EPI_PART) {
     const long long total = (long long)g.M * ((g.N + 31) / 32) * 16;
     int rgrid = (int)std::min<long long>((total + 255) / 256, 4096);
