@@ -71,14 +71,15 @@ def cu_residency(rec, window=None):
 
     CU = (XCC, shader engine, shader array, CU) from the hardware-id
     registers; the phase of a record is that of its hardware queue (the
-    VLM's queues are those that ran the VLM-only kernel kinds). Returns the
+    VLM's queues are those that ran a kernel kind only the prefill has:
+    ViT attention and its combine, patchify, text embedding). Returns the
     mean over CUs of the fraction of the window in which the CU hosts at
     least one workgroup, and in which it hosts workgroups of both phases."""
     import numpy as np
     hw = rec["hwid"].astype(np.int64)
     cu = rec["xcc"].astype(np.int64) * 256 + ((hw >> 13) & 7) * 32 + ((hw >> 12) & 1) * 16 + ((hw >> 8) & 15)
     queue = ((hw >> 30) & 3) * 64 + ((hw >> 6) & 3) * 8 + ((hw >> 24) & 7)
-    vlm_q = np.unique(queue[np.isin(rec["kind"], (1, 8, 9))])  # GEMM, patchify, embed
+    vlm_q = np.unique(queue[np.isin(rec["kind"], (4, 5, 8, 9))])  # ViT attention, combine, patchify, embed
     is_vlm = np.isin(queue, vlm_q)
     t = rec["t"].astype(np.int64)
     d = np.where(rec["end"] == 1, -1, 1)
@@ -180,9 +181,12 @@ def main():
                          "with the most GPU time in the reported schedule)")
     ap.add_argument("--preset", default="pi0")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--extra", default="gr00t:8:serial,concurrent,cu_masked,lanes2_graph,v2_lanes2_graph;"
+    ap.add_argument("--extra", default="gr00t:8:serial,concurrent,cu_masked,lanes2_graph,v2_lanes2_graph,"
+                                       "vb4_ab1_lanes2_graph,vb8_ab1_lanes4_graph,vb4_ab1_v2_lanes2_graph;"
                                        "pi0_3view:32:serial,concurrent,cu_224_32,cu_192_64,cu_160_96,"
-                                       "wg_cap1,wg_cap2,lanes2_graph,cu_160_96_lanes2,batch4_lanes2_graph,batch8_lanes2_graph",
+                                       "wg_cap1,wg_cap2,lanes2_graph,cu_160_96_lanes2,batch4_lanes2_graph,"
+                                       "batch8_lanes2_graph,vb4_ab4_lanes2_graph,vb8_ab4_lanes2_graph,"
+                                       "vb8_ab8_lanes2_graph",
                     help="further workloads, ';'-separated preset:R:schedule,schedule,...")
     ap.add_argument("--extra-steps", type=int, default=5)
     ap.add_argument("--residency", type=int, default=8_000_000,
