@@ -81,3 +81,26 @@ def test_null_arguments_are_errors_not_crashes():
     assert lib.vla_pipeline_run(None, None, None, 1, None, None, None) == -1
     assert "NULL" in V.vla_last_error() or "model" in V.vla_last_error()
     assert lib.vla_debug_gemm(0, 4, 4, 7, None, 8, None, 8, None, None, None) == -1
+
+
+@pytest.mark.parametrize("struct", ["vla_config", "vla_frame", "vla_sched", "vla_timing"])
+def test_binding_structs_match_header(struct):
+    """The ctypes structures pass the header's fields in the header's order
+    and types (a field added on one side only would shift every later one)."""
+    import ctypes as C
+    import paper_2609_22335_amd as V
+    src = open(os.path.join(ROOT, "include", "vla.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    body = re.search(r"typedef struct " + struct + r"\s*\{(.*?)\}\s*" + struct + ";", src, flags=re.S).group(1)
+    fields = []
+    for t, names in re.findall(r"^\s*((?:const\s+)?\w+\s*\*?)\s*([\w\s,]+);", body, flags=re.M):
+        fields += [(t.strip(), n.strip()) for n in names.split(",")]
+    ctype = {"int32_t": C.c_int32, "double": C.c_double, "float": C.c_float}
+    got = getattr(V, struct)._fields_
+    assert [n for _, n in fields] == [n for n, _ in got], struct
+    for (t, n), (gn, gt) in zip(fields, got):
+        t = t.replace("const", "").strip()
+        if t.endswith("*"):
+            assert gt in (C.c_void_p,), (struct, n, gt)
+        else:
+            assert gt is ctype[t], (struct, n, t, gt)
