@@ -280,10 +280,21 @@ __device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int 
 #define VLA_GEMM_LDS_PAD 2  // LDS row padding of the GEMM tiles, in 16-byte units (32 B: fewest bank conflicts measured)
 #endif
 
-template <typename T, int BM, int BN, int BK, int WGM>
+// Compile-time loop: f(integral_constant<int, I>) for I = B .. E-1, so that
+// register arrays are indexed by constants even where the loop body is too
+// large for the unroller.
+template <int B, int E, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
+template <typename T, int BM, int BN, int BK, int WGM, int PAD = VLA_GEMM_LDS_PAD>
 struct GemmSmem {
   static constexpr int VEC = 16 / sizeof(T);
-  static constexpr int LDS = BK + VEC * VLA_GEMM_LDS_PAD;
+  static constexpr int LDS = BK + VEC * PAD;
   static constexpr int CLD = BN + 4;
   union {
     struct {
@@ -294,13 +305,13 @@ struct GemmSmem {
   };
 };
 
-template <typename T, int BM, int BN, int BK, int WGM = 2, int WGN = 2, int PD = 1>
+template <typename T, int BM, int BN, int BK, int WGM = 2, int WGN = 2, int PD = 1, int PAD = VLA_GEMM_LDS_PAD>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A, int lda,
                                               const T* __restrict__ W, int ldw, int M, int N,
                                               int K, int kchunk, int splits, int tiles_m,
                                               int tiles_n, int group_m, Epi e, float* __restrict__ part) {
   VLA_WAVE_BEGIN(KK_GEMM);
-  using SM = GemmSmem<T, BM, BN, BK, WGM>;
+  using SM = GemmSmem<T, BM, BN, BK, WGM, PAD>;
   constexpr int VEC = SM::VEC;
   constexpr int SW = 4 * VEC;  // K covered by one MFMA step across the 4 lane groups
   constexpr int LDS = SM::LDS;
@@ -434,8 +445,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
     // then all threads apply the epilogue with row-contiguous stores
     float* P = (e.kind == EPI_PART ? (float*)e.out : part) + (size_t)s * M * N;
     const bool direct = splits == 1 && e.kind != EPI_PART;
-#pragma unroll
-    for (int i = 0; i < TM; ++i) {
+    auto slice = [&](auto ic) {
+      const int i = ic;
       __syncthreads();
 #pragma unroll
       for (int j = 0; j < TN; ++j)
@@ -459,6 +470,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
           if (m < M && n < N) P[(size_t)m * N + n] = sm.c[row * CLD + col];
         }
       }
+    };
+    // many row slices: a compile-time loop keeps acc indexed by constants
+    if constexpr (TM > 4) {
+      static_for<0, TM>(slice);
+    } else {
+#pragma unroll
+      for (int i = 0; i < TM; ++i) slice(i);
     }
   }
   VLA_WAVE_END(KK_GEMM);
@@ -687,7 +705,7 @@ struct TileCfg {
 // bf16 configurations, then fp32 ones. Wide GEMMs (enough 128 x 128 tiles to
 // cover every CU) take the large tile; everything else takes 64 x 64 tiles,
 // which keep more loads in flight per CU for these M ~ 256..320 shapes.
-static const TileCfg kBf16Cfg[] = {{128, 128, 64}, {64, 64, 64}, {32, 64, 64}};
+static const TileCfg kBf16Cfg[] = {{128, 128, 64}, {64, 64, 64}, {32, 64, 64}, {256, 256, 64}};
 static const TileCfg kF32Cfg[] = {{64, 64, 32}, {32, 64, 32}};
 
 GemmPlan plan_gemm(const GemmDesc& g) {
@@ -703,6 +721,8 @@ GemmPlan plan_gemm(const GemmDesc& g) {
   auto choose = [&](int M) {
     if (g.dtype == DT_BF16) {
       const int t128 = ((M + 127) / 128) * ((g.N + 127) / 128);
+      const int t256 = ((M + 255) / 256) * ((g.N + 255) / 256);
+      if (M >= 1024 && t256 >= NUM_CU_PLAN) return 3;
       if (M >= 256 && t128 >= NUM_CU_PLAN) return 0;
       return M > 32 ? 1 : 2;
     }
@@ -735,7 +755,7 @@ GemmPlan plan_gemm(const GemmDesc& g) {
   return p;
 }
 
-template <typename T, int BM, int BN, int BK, int WGM = 2, int WGN = 2, int PD = 1>
+template <typename T, int BM, int BN, int BK, int WGM = 2, int WGN = 2, int PD = 1, int PAD = VLA_GEMM_LDS_PAD>
 static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch& s,
                              const LaunchCaps& caps, hipStream_t st) {
   const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
@@ -747,7 +767,7 @@ static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch
   // 4 MB L2
   const size_t band_bytes = (size_t)BM * kchunk * sizeof(T);
   const int group_m = std::max(1, std::min(tiles_m, (int)((2u << 20) / std::max<size_t>(band_bytes, 1))));
-  hipExtLaunchKernelGGL((k_gemm<T, BM, BN, BK, WGM, WGN, PD>), dim3(grid), dim3(64 * WGM * WGN), 0, st,
+  hipExtLaunchKernelGGL((k_gemm<T, BM, BN, BK, WGM, WGN, PD, PAD>), dim3(grid), dim3(64 * WGM * WGN), 0, st,
                         caps.ev_start,
                         caps.ev_stop, 0, (const T*)g.A, g.lda, (const T*)g.W, g.ldw, g.M, g.N,
                         g.K, kchunk, p.splits, tiles_m, tiles_n, group_m, g.epi, s.ptr);
@@ -773,6 +793,7 @@ hipError_t launch_gemm(const GemmDesc& g, const Scratch& s, const LaunchCaps& ca
     switch (p.cfg) {
       case 0: return run_gemm_t<uint16_t, 128, 128, 64, 2, 2, 3>(g, p, s, caps, st);
       case 1: return run_gemm_t<uint16_t, 64, 64, 64, 2, 2, 2>(g, p, s, caps, st);
+      case 3: return run_gemm_t<uint16_t, 256, 256, 64, 2, 4, 1, 1>(g, p, s, caps, st);
       default: return run_gemm_t<uint16_t, 32, 64, 64, 2, 2, 2>(g, p, s, caps, st);
     }
   }

@@ -38,6 +38,9 @@ GEMM_SHAPES = [
     (1, 64, 8), (7, 3, 16), (21, 136, 64), (40, 100, 592), (50, 2560, 1024), (50, 1024, 4096),
     (64, 64, 64), (33, 128, 256), (256, 3456, 1152), (305, 2048, 2048), (512, 8192, 256),
     (833, 200, 72), (300, 33000, 200),
+    # stacked-frame shapes: the 256 x 256 tile (ragged M, N and K) and
+    # several row-tile bands
+    (1030, 16400, 96), (2440, 16640, 136),
 ]
 
 
