@@ -150,9 +150,10 @@ struct GemmDesc {
   // one-frame call. The epilogue sees rows f * M + m (Epi::blk_rows = M).
   int frames = 1;
   size_t a_blk = 0;
-  // Rows of one frame when M stacks several frames' rows (a batched
-  // prefill): the split-K factor is planned for plan_m rows, so every row
-  // gets the same reduction as in a one-frame call (0: plan for M).
+  // Row count the split-K factor is planned for (0: M). A batched prefill
+  // passes one frame's rows, so every row gets the same reduction as in a
+  // one-frame call; batched action loops pass a fixed reference (the largest
+  // group), so the reduction does not depend on the group size.
   int plan_m = 0;
 };
 

@@ -731,7 +731,7 @@ GemmPlan plan_gemm(const GemmDesc& g) {
   // The split factor comes from the rows of one frame (plan_m), the tile
   // from all M rows; every configuration of a dtype has the same BK, so the
   // K range of each split (and every sum) is the same as in a one-frame call.
-  const int Mp = g.plan_m > 0 ? std::min(g.plan_m, g.M) : g.M;
+  const int Mp = g.plan_m > 0 ? g.plan_m : g.M;  // may exceed M (a fixed reference row count)
   const int c = choose(g.M);
   const TileCfg t = cfgs[c], tp = cfgs[choose(Mp)];
   const int tiles = ((Mp + tp.bm - 1) / tp.bm) * ((g.N + tp.bn - 1) / tp.bn);

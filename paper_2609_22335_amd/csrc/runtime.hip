@@ -740,9 +740,10 @@ static Epi epi_kind(int kind, void* out = nullptr, int ldo = 0, const float* bia
 //  * otherwise expert layers take frame blocks in the row-block operand
 //    layout (skinny GEMMs, one launch for all frames).
 // Frame f of a batched expert layer reads the past K/V kpast[f] / vpast[f]
-// and the action workspace's per-frame blocks. Stacked rows get the split-K
-// factors of one frame, so a frame's result does not depend on how many
-// frames share the launch.
+// and the action workspace's per-frame blocks. Stacked rows get split-K
+// factors planned for a fixed row count (one frame's prefix in the LM, the
+// largest batched loop in the expert), so a frame's result does not depend
+// on how many frames share the launch.
 static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int rows, int dim, int mlp,
                          void* h, void* q, void* kout, void* vout, int pos0, const void* const* kpast,
                          const void* const* vpast, int npast, void* att, void* mlpbuf, bool kv_only,
@@ -762,7 +763,9 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   auto frm = [&](size_t a_blk) {
     Frames f;
     if (stacked) {
-      f.plan_m = rows;
+      // splits: those of one frame's prefix rows (LM), or of the largest
+      // batched action loop (expert): fixed for every group size
+      f.plan_m = lm ? rows : MAX_ACT_BATCH * rows;
     } else {
       f.n = frames;
       f.a_blk = fb ? a_blk : 0;
