@@ -186,7 +186,9 @@ def main():
                                        "pi0_3view:32:serial,concurrent,cu_224_32,cu_192_64,cu_160_96,"
                                        "wg_cap1,wg_cap2,lanes2_graph,cu_160_96_lanes2,batch4_lanes2_graph,"
                                        "batch8_lanes2_graph,vb4_ab4_lanes2_graph,vb8_ab4_lanes2_graph,"
-                                       "vb8_ab8_lanes2_graph",
+                                       "vb8_ab8_lanes2_graph;"
+                                       "pi0:8:async2_serial,async2_lanes2_graph,async2_vb8_ab4_lanes2_graph,"
+                                       "async2_vb8_ab8_lanes2_graph,async4_serial,async4_vb8_ab8_lanes2_graph",
                     help="further workloads, ';'-separated preset:R:schedule,schedule,...")
     ap.add_argument("--extra-steps", type=int, default=5)
     ap.add_argument("--residency", type=int, default=8_000_000,
@@ -247,7 +249,7 @@ def main():
           "batch2_lanes2_graph": dict(mode="concurrent", act_batch=2, act_streams=2, graphs=True),
           "batch2_v2_graph": dict(mode="concurrent", act_batch=2, vlm_streams=2, graphs=True)}
     for v_ in (2, 4, 8):  # several robots' prefills as one pass, with action groups
-        for a_ in (1, 2, 4, 8):
+        for a_ in (1, 2, 3, 4, 8):
             kw[f"vb{v_}_ab{a_}_graph"] = dict(mode="concurrent", vlm_batch=v_, act_batch=a_, graphs=True)
             kw[f"vb{v_}_ab{a_}_lanes2_graph"] = dict(mode="concurrent", vlm_batch=v_, act_batch=a_,
                                                      act_streams=2, graphs=True)
@@ -258,6 +260,14 @@ def main():
                                                            act_streams=l_, graphs=True)
             kw[f"vb{v_}_ab{a_}_v2_lanes2_graph"] = dict(mode="concurrent", vlm_batch=v_, act_batch=a_,
                                                         vlm_streams=2, act_streams=2, graphs=True)
+    # asynchronous inference: k action chunks per VLM output
+    for k_ in (2, 4):
+        kw[f"async{k_}_serial"] = dict(mode="serial", act_chunks=k_)
+        kw[f"async{k_}_lanes2_graph"] = dict(mode="concurrent", act_streams=2, graphs=True, act_chunks=k_)
+        kw[f"async{k_}_vb8_ab4_lanes2_graph"] = dict(mode="concurrent", vlm_batch=8, act_batch=4, act_streams=2,
+                                                   graphs=True, act_chunks=k_)
+        kw[f"async{k_}_vb8_ab8_lanes2_graph"] = dict(mode="concurrent", vlm_batch=8, act_batch=8, act_streams=2,
+                                                   graphs=True, act_chunks=k_)
     for b_ in (4, 8):  # larger groups of robots per action loop
         kw[f"batch{b_}_graph"] = dict(mode="concurrent", act_batch=b_, graphs=True)
         kw[f"batch{b_}_lanes2_graph"] = dict(mode="concurrent", act_batch=b_, act_streams=2, graphs=True)
@@ -284,8 +294,18 @@ def main():
         cframes = [V.make_frame(p, i, s) for p, i, s in dev]
         noise = torch.from_numpy(np.stack([f["noise"] for f in frames_np])).cuda().contiguous()
         actions = torch.empty_like(noise)
+        chunk_bufs = {1: (noise, actions)}  # k chunks per frame -> (noise, actions) [R k, H, A]
+
+        def bufs(k):
+            if k not in chunk_bufs:
+                nk = np.stack([synth.chunk_noise(cfg, seed, r, j) for r in range(R) for j in range(k)])
+                nt = torch.from_numpy(nk).cuda().contiguous()
+                chunk_bufs[k] = (nt, torch.empty_like(nt))
+            return chunk_bufs[k]
         results, outputs = {}, {}
         for mode in modes:
+            kc = kw[mode].get("act_chunks", 1)
+            noise, actions = bufs(kc)
             print(f"[bench] {preset} mode {mode}: {warmup} warmup + {steps} timed steps of R={R}",
                   file=sys.stderr, flush=True)
             for _ in range(warmup):
@@ -299,29 +319,33 @@ def main():
             torch.cuda.synchronize()
             el = time.perf_counter() - t0
             fps = steps * R / el
-            results[mode] = {"frames_per_s": fps, "actions_per_s": fps * cfg["chunk_len"],
+            results[mode] = {"frames_per_s": fps, "actions_per_s": fps * kc * cfg["chunk_len"],
+                             "chunks_per_frame": kc,
                              "ms_per_step": 1e3 * el / steps,
                              "median_step_ms": float(np.median(lib_ms)), "min_step_ms": float(np.min(lib_ms)),
                              "vlm_ms_per_frame": t["vlm_ms"] / R, "action_ms_per_frame": t["act_ms"] / R}
             outputs[mode] = actions.cpu().numpy().copy()
-        ser = results.get("serial", {}).get("frames_per_s")
+        # speedup over the serialized schedule with as many chunks per frame
         for mode in results:
+            kc = kw[mode].get("act_chunks", 1)
+            ser = results.get("serial" if kc == 1 else f"async{kc}_serial", {}).get("frames_per_s")
             results[mode]["speedup_vs_serialized"] = (results[mode]["frames_per_s"] / ser) if ser else None
         # Batched action loops (groups of >= 2 frames) run tiled GEMMs over
         # the stacked rows: identical among themselves, within the oracle
         # tolerance of the one-frame path; every other schedule is identical
         # to the one-frame path.
         def grp(mode):
-            b = kw[mode].get("act_batch", 1)
-            return "batched" if b > 1 and R % b != 1 else "one_frame"
+            b, kc = kw[mode].get("act_batch", 1), kw[mode].get("act_chunks", 1)
+            g_ = "batched" if b > 1 and (R * kc) % b != 1 else "one_frame"
+            return g_ if kc == 1 else f"{g_}_{kc}_chunks"
         identical = {}
-        for g_ in ("one_frame", "batched"):
+        for g_ in sorted({grp(m0) for m0 in outputs}):
             ms_ = [m0 for m0 in outputs if grp(m0) == g_]
-            if ms_:
-                identical[g_] = all(np.array_equal(outputs[m0], outputs[ms_[0]]) for m0 in ms_)
+            identical[g_] = all(np.array_equal(outputs[m0], outputs[ms_[0]]) for m0 in ms_)
         a_, b_ = [[outputs[m0] for m0 in outputs if grp(m0) == g_] for g_ in ("one_frame", "batched")]
         if a_ and b_:
             identical["max_abs_diff_batched_vs_one_frame"] = float(np.abs(a_[0] - b_[0]).max())
+        noise, actions = chunk_bufs[1]
         return cfg, m, results, outputs, identical, (cframes, noise, actions)
 
     cfg, m, results, outputs, identical, (cframes, noise, actions) = measure(
@@ -385,9 +409,14 @@ def main():
         ms_ = sched.split(",")
         ocfg, om, ores, _, oid, _ = measure(preset, int(r_), ms_, args.extra_steps, 1)
         V.vla_destroy(om)
-        best = max(ores, key=lambda k: ores[k]["frames_per_s"])
-        others[f"{preset}_R{r_}"] = {
-            "workload": f"{preset}, R={r_} robot request streams", "best_schedule": best,
+        kmax = max(kw[m0].get("act_chunks", 1) for m0 in ms_)
+        # asynchronous workloads differ in chunks per frame: best by actions/s
+        best = max(ores, key=lambda k: ores[k]["actions_per_s" if kmax > 1 else "frames_per_s"])
+        name = f"{preset}_R{r_}" + ("_async" if kmax > 1 else "")
+        others[name] = {
+            "workload": f"{preset}, R={r_} robot request streams"
+                        + (", asynchronous inference (several action chunks per VLM output)" if kmax > 1 else ""),
+            "best_schedule": best,
             "frames_per_s": ores[best]["frames_per_s"], "actions_per_s": ores[best]["actions_per_s"],
             "speedup_vs_serialized": ores[best]["speedup_vs_serialized"],
             "chunk": [ocfg["chunk_len"], ocfg["action_dim"]], "euler_steps": ocfg["n_steps"],

@@ -118,6 +118,10 @@ typedef struct vla_sched {
                       /*   once for all k; a final group of fewer than k frames runs */
                       /*   with as many as remain. Every frame's cache and chunk are */
                       /*   bit identical to its own run.                             */
+  int32_t act_chunks; /* action chunks per VLM output (0 or 1: one; at most 64):     */
+                      /*   asynchronous inference. Each frame's context feeds k      */
+                      /*   action phases (items), each from its own noise; item i is */
+                      /*   chunk i % k of frame i / k. act_batch then counts items.  */
 } vla_sched;
 
 typedef struct vla_timing {
@@ -172,12 +176,16 @@ int vla_action_denoise(vla_model* m, const vla_ctx* ctx, const float* noise, flo
 
 /* Run R frames through the two-stage pipeline and wait for it. frames:
  * host array of R vla_frame (device pointers inside); noise: device fp32
- * [R, chunk_len, action_dim]; actions: device fp32 [R, chunk_len,
- * action_dim]. The VLM prefill of frame r+1 overlaps the action phase of
- * frame r (a ring of act_streams + 1 model-owned contexts, events between the
+ * [R * k, chunk_len, action_dim] with k = max(1, act_chunks), item i = chunk
+ * i % k of frame i / k; actions: device fp32 of the same shape. The VLM
+ * prefill of later frames overlaps the action phases of earlier ones (a ring
+ * of model-owned contexts, allocated in blocks of 8, and events between the
  * streams) except in VLA_MODE_SERIAL. Results are bit-identical across
- * modes, action-stream counts and graph replay. t may be NULL. Calls on one
- * model are serialised. */
+ * modes, stream counts, prefill batching and graph replay; batched action
+ * loops (act_batch >= 2) are bit-identical among themselves and within the
+ * chunk tolerance of one-item loops. t may be NULL (frames_per_s counts
+ * frames, actions_per_s counts chunk rows of every item). Calls on one model
+ * are serialised. */
 int vla_pipeline_run(vla_model* m, const vla_frame* frames, const float* noise, int32_t R,
                      const vla_sched* sched, float* actions, vla_timing* t);
 

@@ -48,7 +48,7 @@ class vla_sched(ctypes.Structure):
     _fields_ = [("mode", ctypes.c_int32), ("vlm_cus", ctypes.c_int32), ("act_cus", ctypes.c_int32),
                 ("vlm_wg_cap", ctypes.c_int32), ("act_streams", ctypes.c_int32), ("graphs", ctypes.c_int32),
                 ("vlm_streams", ctypes.c_int32), ("act_batch", ctypes.c_int32),
-                ("vlm_batch", ctypes.c_int32)]
+                ("vlm_batch", ctypes.c_int32), ("act_chunks", ctypes.c_int32)]
 
 
 class vla_timing(ctypes.Structure):
@@ -185,10 +185,10 @@ def vla_action_denoise(model: int, ctx: int, noise, actions, stream: int = 0) ->
 def vla_pipeline_run(model: int, frames: Sequence[vla_frame], noise, R: int, mode="serial",
                      vlm_cus: int = 0, act_cus: int = 0, vlm_wg_cap: int = 0, actions=None,
                      act_streams: int = 1, graphs: bool = False, vlm_streams: int = 1,
-                     act_batch: int = 1, vlm_batch: int = 1) -> Dict[str, float]:
+                     act_batch: int = 1, vlm_batch: int = 1, act_chunks: int = 1) -> Dict[str, float]:
     arr = (vla_frame * len(frames))(*frames)
     s = vla_sched(MODES[mode] if isinstance(mode, str) else int(mode), vlm_cus, act_cus, vlm_wg_cap,
-                  act_streams, 1 if graphs else 0, vlm_streams, act_batch, vlm_batch)
+                  act_streams, 1 if graphs else 0, vlm_streams, act_batch, vlm_batch, act_chunks)
     t = vla_timing()
     _check(_lib.vla_pipeline_run(model, arr, _ptr(noise), int(R), ctypes.byref(s), _ptr(actions),
                                  ctypes.byref(t)))

@@ -324,11 +324,12 @@ struct vla_model {
   std::vector<vla_ctx*> pctx;  // ring of act_streams + 1 contexts
   std::map<std::pair<int, int>, Streams> mask_streams;
   Streams plain{};
-  std::vector<hipEvent_t> ev;
+  std::vector<hipEvent_t> ev;   // per frame: VLM start, end
+  std::vector<hipEvent_t> eva;  // per action item: start, end
   // graph replay: frame inputs staged into fixed buffers, graphs cached per
   // (context, VLM grid cap) and (action lane, context)
   std::map<std::tuple<int, int, int, int>, hipGraphExec_t> pre_graphs;  // (VLM lane, first context, WG cap, frames)
-  std::map<std::tuple<int, int, int>, hipGraphExec_t> den_graphs;  // (lane, first context, frames)
+  std::map<std::pair<int, std::vector<int>>, hipGraphExec_t> den_graphs;  // (lane, contexts of the items)
   std::mutex mu;
 
   // per-tag kernel timer: every launch whose tag matches is bracketed by
@@ -1679,6 +1680,7 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
   const int B = std::max(1, s.act_batch);
   if (B > MAX_ACT_BATCH) return fail(VLA_EINVAL, "act_batch must be <= " + std::to_string(MAX_ACT_BATCH));
   if (B > 1 && m->c.head != VLA_HEAD_PI0) return fail(VLA_EINVAL, "act_batch > 1: pi0-style action head only");
+  if (s.act_chunks < 0 || s.act_chunks > 64) return fail(VLA_EINVAL, "act_chunks must be in 0 .. 64");
   const int Bv = std::max(1, s.vlm_batch);
   if (Bv > MAX_VLM_BATCH || CTX_BLOCK % Bv) return fail(VLA_EINVAL, "vlm_batch must be 1, 2, 4 or 8");
   const vla_config& c = m->c;
@@ -1705,23 +1707,38 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
   VLA_TRY(get_streams(m, s, &st));
   if (s.mode == VLA_MODE_SERIAL) st.a[0] = st.v[0];
   const bool graphs = s.graphs != 0 && m->timer_tag.empty();
-  const size_t need = (size_t)4 * R;
-  while (m->ev.size() < need) {
-    hipEvent_t e;
-    HIP_TRY(hipEventCreate(&e));
-    m->ev.push_back(e);
-  }
-  // events: [4r] VLM start, [4r+1] VLM end, [4r+2] action start, [4r+3]
-  // action end; a group's time is recorded on its first frame, the others
-  // get an empty interval at the group's end
+  // Asynchronous inference: k action chunks (items) per VLM output. Item i
+  // is chunk i % k of frame i / k, with its own noise and output rows.
+  const int k = std::max(1, s.act_chunks);
+  const int items = R * k;
+  auto grow = [&](std::vector<hipEvent_t>& v, size_t n) -> int {
+    while (v.size() < n) {
+      hipEvent_t e;
+      HIP_TRY(hipEventCreate(&e));
+      v.push_back(e);
+    }
+    return VLA_OK;
+  };
+  // events: ev[2r] / ev[2r+1] VLM start / end of frame r; eva[2i] / eva[2i+1]
+  // action start / end of item i. A group's time is recorded on its first
+  // member, the others get an empty interval at the group's end; a frame's
+  // context is free again at the end event of its last item.
+  VLA_TRY(grow(m->ev, (size_t)2 * R));
+  VLA_TRY(grow(m->eva, (size_t)2 * items));
   LaunchCaps vcaps{}, acaps{};
   if (s.mode == VLA_MODE_WG_CAPPED) vcaps.max_wgs = s.vlm_wg_cap * m->num_cus;
   const size_t chunk = (size_t)c.chunk_len * c.action_dim;
   const size_t pix_bytes = (size_t)c.n_views * c.img_h * c.img_w * 3 * 4;
   auto vlane = [&](int r) { return (r / Bv) % vlanes; };  // VLM lane of frame r
-  auto alane = [&](int r) { return (r / B) % lanes; };    // action lane of frame r
+  auto alane = [&](int i) { return (i / B) % lanes; };    // action lane of item i
+  auto actx = [&](int i) { return (i / k) % nctx; };      // context of item i
   HIP_TRY(hipDeviceSynchronize());
 
+  auto den_key = [&](int li, int a0, int na) {
+    std::vector<int> cs;
+    for (int f = 0; f < na; ++f) cs.push_back(actx(a0 + f));
+    return std::make_pair(li, cs);
+  };
   if (graphs) {  // capture what this run needs and is missing (outside the timed loop)
     for (int g0 = 0; g0 < R; g0 += Bv) {
       const int n = std::min(Bv, R - g0), vi = vlane(g0), ci = g0 % nctx;
@@ -1737,32 +1754,34 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
       VLA_TRY(capture(st.v[vi], [&] { return run_prefill_n(rv, staged, n, &m->pctx[ci]); }, &ge));
       m->pre_graphs[key] = ge;
     }
-    // one graph per (lane, first context, frames): the group of frames
-    // g0 .. g0 + n - 1 uses contexts g0 % nctx .. + n - 1
-    for (int g0 = 0; g0 < R; g0 += B) {
-      const int n = std::min(B, R - g0), li = alane(g0), ci = g0 % nctx;
-      const auto key = std::make_tuple(li, ci, n);
+    // one graph per (lane, contexts of the group's items)
+    for (int a0 = 0; a0 < items; a0 += B) {
+      const int na = std::min(B, items - a0), li = alane(a0);
+      const auto key = den_key(li, a0, na);
       if (m->den_graphs.count(key)) continue;
       ActWs* aw = m->aws[li].get();
       Run ra{m, st.a[li], acaps, &aw->scr, aw};
       const vla_ctx* cs[MAX_ACT_BATCH] = {};
-      for (int f = 0; f < n; ++f) cs[f] = m->pctx[ci + f];
+      for (int f = 0; f < na; ++f) cs[f] = m->pctx[actx(a0 + f)];
       hipGraphExec_t ge = nullptr;
-      VLA_TRY(capture(st.a[li], [&] { return run_denoise_n(ra, cs, n, aw->nstage, aw->xg); }, &ge));
+      VLA_TRY(capture(st.a[li], [&] { return run_denoise_n(ra, cs, na, aw->nstage, aw->xg); }, &ge));
       m->den_graphs[key] = ge;
     }
   }
 
   const auto t0 = std::chrono::steady_clock::now();
-  int next_act = 0;  // first frame whose action phase is not issued yet
+  int next_item = 0;  // first item whose action phase is not issued yet
   for (int g0 = 0; g0 < R; g0 += Bv) {
     const int n = std::min(Bv, R - g0), vi = vlane(g0), ci = g0 % nctx;
     hipStream_t sv = st.v[vi];
     VlmWs* vw = m->vws[vi].get();
-    // a context is free once the action phase that last read it is done
-    for (int q = g0; q < g0 + n; ++q)
-      if (q >= nctx && sv != st.a[alane(q - nctx)]) HIP_TRY(hipStreamWaitEvent(sv, m->ev[4 * (q - nctx) + 3], 0));
-    HIP_TRY(hipEventRecord(m->ev[4 * g0], sv));
+    // a context is free once the action phases that read it are done
+    for (int q = g0; q < g0 + n; ++q) {
+      if (q < nctx) continue;
+      const int last = (q - nctx) * k + k - 1;  // the previous user's last item
+      if (sv != st.a[alane(last)]) HIP_TRY(hipStreamWaitEvent(sv, m->eva[2 * last + 1], 0));
+    }
+    HIP_TRY(hipEventRecord(m->ev[2 * g0], sv));
     if (graphs) {
       for (int i = 0; i < n; ++i) {
         const vla_frame& fr = frames[g0 + i];
@@ -1779,37 +1798,37 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
       Run rv{m, sv, vcaps, &vw->scr, nullptr, vw};
       VLA_TRY(run_prefill_n(rv, &frames[g0], n, &m->pctx[ci]));
     }
-    HIP_TRY(hipEventRecord(m->ev[4 * g0 + 1], sv));
+    HIP_TRY(hipEventRecord(m->ev[2 * g0 + 1], sv));
     for (int q = g0 + 1; q < g0 + n; ++q) {
-      HIP_TRY(hipEventRecord(m->ev[4 * q], sv));
-      HIP_TRY(hipEventRecord(m->ev[4 * q + 1], sv));
+      HIP_TRY(hipEventRecord(m->ev[2 * q], sv));
+      HIP_TRY(hipEventRecord(m->ev[2 * q + 1], sv));
     }
     // every action group whose frames are all prefilled starts now
-    while (next_act < R) {
-      const int a0 = next_act, na = std::min(B, R - a0);
-      if (a0 + na > g0 + n) break;
-      next_act += na;
+    while (next_item < items) {
+      const int a0 = next_item, na = std::min(B, items - a0);
+      const int f_first = a0 / k, f_last = (a0 + na - 1) / k;
+      if (f_last >= g0 + n) break;
+      next_item += na;
       const int li = alane(a0);
       hipStream_t sa = st.a[li];
-      for (int q = a0; q < a0 + na; ++q)
-        if (st.v[vlane(q)] != sa) HIP_TRY(hipStreamWaitEvent(sa, m->ev[4 * q + 1], 0));
-      HIP_TRY(hipEventRecord(m->ev[4 * a0 + 2], sa));
+      for (int q = f_first; q <= f_last; ++q)
+        if (st.v[vlane(q)] != sa) HIP_TRY(hipStreamWaitEvent(sa, m->ev[2 * q + 1], 0));
+      HIP_TRY(hipEventRecord(m->eva[2 * a0], sa));
       ActWs* aw = m->aws[li].get();
-      const int c0 = a0 % nctx;
       if (graphs) {
         HIP_TRY(hipMemcpyAsync(aw->nstage, noise + a0 * chunk, na * chunk * 4, hipMemcpyDeviceToDevice, sa));
-        HIP_TRY(hipGraphLaunch(m->den_graphs[std::make_tuple(li, c0, na)], sa));
+        HIP_TRY(hipGraphLaunch(m->den_graphs[den_key(li, a0, na)], sa));
         HIP_TRY(hipMemcpyAsync(actions + a0 * chunk, aw->xg, na * chunk * 4, hipMemcpyDeviceToDevice, sa));
       } else {
         Run ra{m, sa, acaps, &aw->scr, aw};
         const vla_ctx* cs[MAX_ACT_BATCH] = {};
-        for (int f = 0; f < na; ++f) cs[f] = m->pctx[c0 + f];
+        for (int f = 0; f < na; ++f) cs[f] = m->pctx[actx(a0 + f)];
         VLA_TRY(run_denoise_n(ra, cs, na, noise + a0 * chunk, actions + a0 * chunk));
       }
-      HIP_TRY(hipEventRecord(m->ev[4 * a0 + 3], sa));
+      HIP_TRY(hipEventRecord(m->eva[2 * a0 + 1], sa));
       for (int q = a0 + 1; q < a0 + na; ++q) {
-        HIP_TRY(hipEventRecord(m->ev[4 * q + 2], sa));
-        HIP_TRY(hipEventRecord(m->ev[4 * q + 3], sa));
+        HIP_TRY(hipEventRecord(m->eva[2 * q], sa));
+        HIP_TRY(hipEventRecord(m->eva[2 * q + 1], sa));
       }
     }
   }
@@ -1819,13 +1838,16 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
   if (t) {
     t->wall_ms = std::chrono::duration<double, std::milli>(t1 - t0).count();
     t->frames_per_s = R / (t->wall_ms * 1e-3);
-    t->actions_per_s = t->frames_per_s * c.chunk_len;
+    t->actions_per_s = t->frames_per_s * k * c.chunk_len;
     t->vlm_ms = t->act_ms = 0;
     for (int r = 0; r < R; ++r) {
-      float a = 0, b = 0;
-      HIP_TRY(hipEventElapsedTime(&a, m->ev[4 * r], m->ev[4 * r + 1]));
-      HIP_TRY(hipEventElapsedTime(&b, m->ev[4 * r + 2], m->ev[4 * r + 3]));
+      float a = 0;
+      HIP_TRY(hipEventElapsedTime(&a, m->ev[2 * r], m->ev[2 * r + 1]));
       t->vlm_ms += a;
+    }
+    for (int i = 0; i < items; ++i) {
+      float b = 0;
+      HIP_TRY(hipEventElapsedTime(&b, m->eva[2 * i], m->eva[2 * i + 1]));
       t->act_ms += b;
     }
   }
@@ -1884,6 +1906,7 @@ int vla_destroy(vla_model* m) {
     for (auto& kv : m->mask_streams) drop(kv.second);
     drop(m->plain);
     for (auto e : m->ev) hipEventDestroy(e);
+    for (auto e : m->eva) hipEventDestroy(e);
     for (auto e : m->timer_ev) hipEventDestroy(e);
     if (m->wlog) {
       wavelog_set(nullptr);

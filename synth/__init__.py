@@ -382,3 +382,13 @@ def make_frame(cfg: Dict[str, int], seed: int, r: int) -> Dict[str, np.ndarray]:
     fr["state"] = (normal(fs, "frame.state", cfg["state_dim"], 1.0) if cfg["state_dim"] > 0
                    else np.zeros(0, np.float32))
     return fr
+
+
+def chunk_noise(cfg: Dict[str, int], seed: int, r: int, j: int) -> np.ndarray:
+    """Start noise x_0 of action chunk ``j`` of frame ``r`` under asynchronous
+    inference (several chunks from one VLM output): chunk 0 is the frame's own
+    noise, chunk j > 0 an independent N(0, 1) draw of the same shape."""
+    if j == 0:
+        return make_frame(cfg, seed, r)["noise"]
+    return normal(frame_seed(seed, r), f"frame.noise.{j}", cfg["chunk_len"] * cfg["action_dim"], 1.0).reshape(
+        cfg["chunk_len"], cfg["action_dim"])

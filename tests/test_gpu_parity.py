@@ -459,6 +459,9 @@ def test_pipeline_modes_bit_identical(V, cfg):
             with pytest.raises(V.VlaError):
                 V.vla_pipeline_run(m, [d.c for d in dfs], noise, R, mode="concurrent", vlm_batch=bad,
                                    actions=torch.empty_like(noise))
+        with pytest.raises(V.VlaError):
+            V.vla_pipeline_run(m, [d.c for d in dfs], noise, R, mode="concurrent", act_chunks=65,
+                               actions=torch.empty_like(noise))
         standalone = [g.run_frame(m, cfg, f)[0] for f in frames]
         for mode, kw in modes:
             name = mode + "".join(f"/{k}={v}" for k, v in kw.items() if k not in ("vlm_cus", "act_cus"))
@@ -514,3 +517,55 @@ def test_abi_errors_on_device(V):
             with pytest.raises(V.VlaError) as e:
                 V.vla_action_denoise(m, c2, torch.zeros(15, device="cuda"), torch.zeros(15, device="cuda"))
             assert e.value.code == -5
+
+
+@pytest.mark.parametrize("cfg", [synth.micro(synth.BF16), synth.TINY, synth.micro_dit(synth.BF16)],
+                         ids=["micro-bf16", "tiny", "micro-dit-bf16"])
+def test_async_inference_chunks(V, cfg):
+    """Asynchronous inference: k action chunks from each VLM output, each from
+    its own noise. One-item loops equal standalone denoise calls on the
+    frame's context bit for bit in every schedule; batched loops (pi0 head)
+    are identical among themselves; chunks match the oracle."""
+    g = G()
+    R, k = 3, 3
+    g.say(f"async chunks dtype={cfg['dtype']} R={R} k={k}")
+    frames = [synth.make_frame(cfg, 5, r) for r in range(R)]
+    noise_np = np.stack([synth.chunk_noise(cfg, 5, r, j) for r in range(R) for j in range(k)])
+    dfs = [g.DevFrame(f) for f in frames]
+    noise = g.to_dev(noise_np.astype(np.float32)).contiguous()
+    with g.model(cfg, 5) as m:
+        want = np.empty(noise_np.shape, np.float64)
+        for r in range(R):  # standalone: one prefill, k denoise calls
+            with g.context(m) as c:
+                V.vla_vlm_prefill(m, dfs[r].c, c, 0)
+                for j in range(k):
+                    out = torch.empty_like(dfs[r].noise)
+                    V.vla_action_denoise(m, c, noise[r * k + j], out, 0)
+                    torch.cuda.synchronize()
+                    want[r * k + j] = out.cpu().numpy()
+        one = [("serial", {}), ("concurrent", dict(graphs=True)), ("concurrent", dict(act_streams=2)),
+               ("concurrent", dict(vlm_batch=2, act_streams=2, graphs=True))]
+        batched = [("concurrent", dict(act_batch=4, graphs=True)),
+                   ("concurrent", dict(act_batch=2, act_streams=2, vlm_batch=2)),
+                   ("serial", dict(act_batch=8))] if cfg["head"] == synth.HEAD_PI0 else []
+        bref = None
+        for mode, kw in one + batched:
+            g.say(f"async {mode} {kw}")
+            out = torch.full_like(noise, float("nan"))
+            t = V.vla_pipeline_run(m, [d.c for d in dfs], noise, R, mode=mode, actions=out, act_chunks=k, **kw)
+            assert t["actions_per_s"] == pytest.approx(t["frames_per_s"] * k * cfg["chunk_len"])
+            got = out.cpu().numpy().astype(np.float64)
+            b = kw.get("act_batch", 1)
+            if b == 1:
+                assert np.array_equal(got, want), (mode, kw)
+            else:
+                multi = [i for i in range(R * k) if not ((R * k) % b == 1 and i == R * k - 1)]
+                if bref is None:
+                    bref = got
+                assert np.array_equal(got[multi], bref[multi]), (mode, kw)
+    P = synth.make_params(cfg, 5)
+    for r, j in ((0, 1), (R - 1, k - 1)):
+        ref = O.forward(P, cfg, dict(frames[r], noise=noise_np[r * k + j]))
+        assert np.abs(want[r * k + j] - ref).max() <= CHUNK_TOL[cfg["dtype"]]
+        if bref is not None:
+            assert np.abs(bref[r * k + j] - ref).max() <= CHUNK_TOL[cfg["dtype"]]
