@@ -364,21 +364,30 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
     // it is multiplied from LDS; the loop is unrolled by PD so every buffer
     // index is a compile-time constant.
     uint4 ra[PD][AV], rb[PD][BV];
+    // Per-thread load offsets, fixed for the tile: thread tid loads the
+    // 16-byte column slice kc of rows (tid + i NT) / KV (NT is a multiple of
+    // KV, so kc is the same for every i). Each K-step then adds the uniform
+    // k0 as the scalar offset; rows past M / N and columns past kend read as
+    // zero (out-of-range buffer offset).
+    const int kc = (tid % KV) * VEC;
+    uint32_t aoff[AV], boff[BV];
+#pragma unroll
+    for (int i = 0; i < AV; ++i) {
+      const int gm = m0 + (tid + i * NT) / KV;
+      aoff[i] = gm < M ? (uint32_t)(((size_t)gm * lda + kc) * sizeof(T)) : OOB;
+    }
+#pragma unroll
+    for (int i = 0; i < BV; ++i) {
+      const int gn = n0 + (tid + i * NT) / KV;
+      boff[i] = gn < N ? (uint32_t)(((size_t)gn * ldw + kc) * sizeof(T)) : OOB;
+    }
     auto gload = [&](int k0, uint4 (&xa)[AV], uint4 (&xb)[BV]) {
+      const bool kok = kc < kend - k0;  // this thread's slice lies before kend
+      const uint32_t soff = (uint32_t)k0 * sizeof(T);
 #pragma unroll
-      for (int i = 0; i < AV; ++i) {
-        const int c = tid + i * NT, r = c / KV, kc = (c % KV) * VEC;
-        const int gm = m0 + r, gk = k0 + kc;
-        const bool ok = gm < M && gk < kend;
-        xa[i] = bld16(ra_r, ok ? (uint32_t)(((size_t)gm * lda + gk) * sizeof(T)) : OOB);
-      }
+      for (int i = 0; i < AV; ++i) xa[i] = bld16s(ra_r, kok ? aoff[i] : OOB, soff);
 #pragma unroll
-      for (int i = 0; i < BV; ++i) {
-        const int c = tid + i * NT, r = c / KV, kc = (c % KV) * VEC;
-        const int gn = n0 + r, gk = k0 + kc;
-        const bool ok = gn < N && gk < kend;
-        xb[i] = bld16(rb_r, ok ? (uint32_t)(((size_t)gn * ldw + gk) * sizeof(T)) : OOB);
-      }
+      for (int i = 0; i < BV; ++i) xb[i] = bld16s(rb_r, kok ? boff[i] : OOB, soff);
     };
     auto sstore = [&](int buf, const uint4 (&xa)[AV], const uint4 (&xb)[BV]) {
 #pragma unroll
