@@ -14,6 +14,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <type_traits>
 
 #include "kernels.h"
 
@@ -142,6 +143,15 @@ __device__ __forceinline__ uint4 bld16(Rsrc r, uint32_t off) {
 __device__ __forceinline__ uint4 bld16s(Rsrc r, uint32_t off, uint32_t soff) {
   return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, off, soff, 0));
 }
+// 16 bytes per lane from the buffer straight into the LDS: lane l writes
+// bytes [16 l, 16 l + 16) after `dst` (which must be the same in every lane);
+// an out-of-range lane writes zeros
+__device__ __forceinline__ void bld16_lds(Rsrc r, void* dst, uint32_t off, uint32_t soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)dst, 16, off, soff, 0, 0);
+}
+// s_waitcnt operand that waits for every outstanding vector memory load
+// (vmcnt 0; expcnt and lgkmcnt left at their maxima)
+constexpr int VMCNT0 = 0x0F70;
 __device__ __forceinline__ float bld1(Rsrc r, uint32_t off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
@@ -304,17 +314,30 @@ struct GemmSmem {
     float c[WGM * 16 * CLD];  // one 16-row slice of every wave row
   };
 };
+// Direct-load variant: stage 0 of the operand ring shares this object with the
+// epilogue slice; stage 1 is a separate __shared__ array, so the compiler can
+// tell the two stages apart and lets the LDS reads of one stage run while
+// loads into the other are in flight.
+template <typename T, int BM, int BN, int BK, int WGM>
+struct GemmSmemDL {
+  static constexpr int CLD = BN + 4;
+  union {
+    T d[(BM + BN) * BK];
+    float c[WGM * 16 * CLD];
+  };
+};
 
-template <typename T, int BM, int BN, int BK, int WGM = 2, int WGN = 2, int PD = 1, int PAD = VLA_GEMM_LDS_PAD>
+template <typename T, int BM, int BN, int BK, int WGM = 2, int WGN = 2, int PD = 1, int PAD = VLA_GEMM_LDS_PAD,
+          bool DL = false>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A, int lda,
                                               const T* __restrict__ W, int ldw, int M, int N,
                                               int K, int kchunk, int splits, int tiles_m,
                                               int tiles_n, int group_m, Epi e, float* __restrict__ part) {
   VLA_WAVE_BEGIN(KK_GEMM);
-  using SM = GemmSmem<T, BM, BN, BK, WGM, PAD>;
-  constexpr int VEC = SM::VEC;
+  using SM = std::conditional_t<DL, GemmSmemDL<T, BM, BN, BK, WGM>, GemmSmem<T, BM, BN, BK, WGM, PAD>>;
+  constexpr int VEC = 16 / sizeof(T);
   constexpr int SW = 4 * VEC;  // K covered by one MFMA step across the 4 lane groups
-  constexpr int LDS = SM::LDS;
+  constexpr int LDS = BK + VEC * PAD;
   constexpr int CLD = SM::CLD;
   constexpr int NT = 64 * WGM * WGN;  // threads: a WGM x WGN grid of waves
   constexpr int WM = BM / WGM, WN = BN / WGN, TM = WM / 16, TN = WN / 16;
@@ -360,100 +383,200 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
 #pragma unroll
       for (int j = 0; j < TN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // K-tiles it+1 .. it+PD are in registers (ring of PD buffers) while tile
-    // it is multiplied from LDS; the loop is unrolled by PD so every buffer
-    // index is a compile-time constant.
-    uint4 ra[PD][AV], rb[PD][BV];
-    // Per-thread load offsets, fixed for the tile: thread tid loads the
-    // 16-byte column slice kc of rows (tid + i NT) / KV (NT is a multiple of
-    // KV, so kc is the same for every i). Each K-step then adds the uniform
-    // k0 as the scalar offset; rows past M / N and columns past kend read as
-    // zero (out-of-range buffer offset).
-    const int kc = (tid % KV) * VEC;
-    uint32_t aoff[AV], boff[BV];
+    if constexpr (DL) {
+      // Operands go from global memory straight into LDS (buffer loads with
+      // the LDS as destination: each wave instruction writes 1 KB, lane l at
+      // byte 16 l), two stages. A K-tile row is BK elements = 8 chunks of 16
+      // bytes with no padding; chunk c of tile row r sits at chunk position
+      // c ^ (r % 8), so the 16-byte fragment reads of 8 consecutive rows hit
+      // distinct banks. Lane l of an instruction covering rows 8g .. 8g + 7
+      // loads row 8g + l / 8, chunk (l % 8) ^ (l / 8): each row is still read
+      // as one contiguous 128-byte line. Out-of-range rows and chunks read as
+      // zero through the buffer range check.
+      static_assert(sizeof(T) == 2 && BK / VEC == 8, "direct loads: 8 chunks per tile row");
+      static_assert((BM / 8) % (NT / 64) == 0 && (BN / 8) % (NT / 64) == 0, "direct loads per wave");
+      __shared__ __attribute__((aligned(16))) T d1[(BM + BN) * BK];
+      constexpr int LA = BM / 8 / (NT / 64), LB = BN / 8 / (NT / 64);  // instructions per wave
+      const int lr = lane >> 3, lcol = ((lane & 7) ^ lr) * VEC;
+      uint32_t aoff[LA], boff[LB];
 #pragma unroll
-    for (int i = 0; i < AV; ++i) {
-      const int gm = m0 + (tid + i * NT) / KV;
-      aoff[i] = gm < M ? (uint32_t)(((size_t)gm * lda + kc) * sizeof(T)) : OOB;
-    }
+      for (int i = 0; i < LA; ++i) {
+        const int gm = m0 + (wave * LA + i) * 8 + lr;
+        aoff[i] = gm < M ? (uint32_t)(((size_t)gm * lda + lcol) * sizeof(T)) : OOB;
+      }
 #pragma unroll
-    for (int i = 0; i < BV; ++i) {
-      const int gn = n0 + (tid + i * NT) / KV;
-      boff[i] = gn < N ? (uint32_t)(((size_t)gn * ldw + kc) * sizeof(T)) : OOB;
-    }
-    auto gload = [&](int k0, uint4 (&xa)[AV], uint4 (&xb)[BV]) {
-      const bool kok = kc < kend - k0;  // this thread's slice lies before kend
-      const uint32_t soff = (uint32_t)k0 * sizeof(T);
+      for (int i = 0; i < LB; ++i) {
+        const int gn = n0 + (wave * LB + i) * 8 + lr;
+        boff[i] = gn < N ? (uint32_t)(((size_t)gn * ldw + lcol) * sizeof(T)) : OOB;
+      }
+      auto issue = [&](T* d, int k0) {
+        const bool kok = lcol < kend - k0;
+        const uint32_t soff = (uint32_t)k0 * sizeof(T);
 #pragma unroll
-      for (int i = 0; i < AV; ++i) xa[i] = bld16s(ra_r, kok ? aoff[i] : OOB, soff);
+        for (int i = 0; i < LA; ++i)
+          bld16_lds(ra_r, d + (wave * LA + i) * 8 * BK, kok ? aoff[i] : OOB, soff);
 #pragma unroll
-      for (int i = 0; i < BV; ++i) xb[i] = bld16s(rb_r, kok ? boff[i] : OOB, soff);
-    };
-    auto sstore = [&](int buf, const uint4 (&xa)[AV], const uint4 (&xb)[BV]) {
+        for (int i = 0; i < LB; ++i)
+          bld16_lds(rb_r, d + (BM + (wave * LB + i) * 8) * BK, kok ? boff[i] : OOB, soff);
+      };
+      // fragment reads: tile row (lane % 16) + 16 i of the wave's rows, chunk
+      // 4 ks + lane / 16, at chunk position chunk ^ (lane % 8)
+      const int fr = lane & 15, fp = ((lane >> 4) ^ (lane & 7)) * VEC;
+      auto compute_dl = [&](const T* d) {
+        const T* sa = d + (wm * WM + fr) * BK;
+        const T* sb = d + (BM + wn * WN + fr) * BK;
+#pragma unroll
+        for (int ks = 0; ks < BK / SW; ++ks) {
+          const int cp = fp ^ (ks * 4 * VEC);
+          uint4 af[TM], bfg[TN];
+#pragma unroll
+          for (int j = 0; j < TN; ++j) bfg[j] = *(const uint4*)(sb + j * 16 * BK + cp);
+#pragma unroll
+          for (int i = 0; i < TM; ++i) af[i] = *(const uint4*)(sa + i * 16 * BK + cp);
+          // all fragment reads of the K-slab go out before its first MFMA
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = mfma_step(af[i], bfg[j], acc[i][j], dummy);
+        }
+      };
+      // step: request the next K-tile into the other stage, multiply this
+      // one, wait for this wave's loads, one barrier
+      T* d0 = sm.d;
+      __syncthreads();  // the previous tile's epilogue is done with the LDS
+      issue(d0, kbeg);
+      __builtin_amdgcn_s_waitcnt(VMCNT0);
+      __syncthreads();  // tile 0 is in LDS
+      for (int it = 0; it < nk; it += 2) {
+        if (it + 1 < nk) issue(d1, kbeg + (it + 1) * BK);
+        compute_dl(d0);
+        __builtin_amdgcn_s_waitcnt(VMCNT0);
+        __syncthreads();
+        if (it + 1 < nk) {
+          if (it + 2 < nk) issue(d0, kbeg + (it + 2) * BK);
+          compute_dl(d1);
+          __builtin_amdgcn_s_waitcnt(VMCNT0);
+          __syncthreads();
+        }
+      }
+    } else {
+      auto compute = [&](int buf) {
+        const T* sa = sm.ld.a[buf];
+        const T* sb = sm.ld.b[buf];
+#pragma unroll
+        for (int ks = 0; ks < BK / SW; ++ks) {
+          uint4 af[TM], bfg[TN];
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+            af[i] = *(const uint4*)(sa + (wm * WM + i * 16 + (lane & 15)) * LDS + ks * SW +
+                                    (lane >> 4) * VEC);
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            bfg[j] = *(const uint4*)(sb + (wn * WN + j * 16 + (lane & 15)) * LDS + ks * SW +
+                                     (lane >> 4) * VEC);
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = mfma_step(af[i], bfg[j], acc[i][j], dummy);
+        }
+      };
+
+      // K-tiles it+1 .. it+PD are in registers (ring of PD buffers) while tile
+      // it is multiplied from LDS; the loop is unrolled by PD so every buffer
+      // index is a compile-time constant.
+      uint4 ra[PD][AV], rb[PD][BV];
+      // Per-thread load offsets, fixed for the tile: thread tid loads the
+      // 16-byte column slice kc of rows (tid + i NT) / KV (NT is a multiple of
+      // KV, so kc is the same for every i). Each K-step then adds the uniform
+      // k0 as the scalar offset; rows past M / N and columns past kend read as
+      // zero (out-of-range buffer offset).
+      const int kc = (tid % KV) * VEC;
+      uint32_t aoff[AV], boff[BV];
 #pragma unroll
       for (int i = 0; i < AV; ++i) {
-        const int c = tid + i * NT, r = c / KV, kc = (c % KV) * VEC;
-        *(uint4*)(sm.ld.a[buf] + r * LDS + kc) = xa[i];
+        const int gm = m0 + (tid + i * NT) / KV;
+        aoff[i] = gm < M ? (uint32_t)(((size_t)gm * lda + kc) * sizeof(T)) : OOB;
       }
 #pragma unroll
       for (int i = 0; i < BV; ++i) {
-        const int c = tid + i * NT, r = c / KV, kc = (c % KV) * VEC;
-        *(uint4*)(sm.ld.b[buf] + r * LDS + kc) = xb[i];
+        const int gn = n0 + (tid + i * NT) / KV;
+        boff[i] = gn < N ? (uint32_t)(((size_t)gn * ldw + kc) * sizeof(T)) : OOB;
       }
-    };
-    auto compute = [&](int buf) {
-      const T* sa = sm.ld.a[buf];
-      const T* sb = sm.ld.b[buf];
+      auto gload = [&](int k0, uint4 (&xa)[AV], uint4 (&xb)[BV]) {
+        const bool kok = kc < kend - k0;  // this thread's slice lies before kend
+        const uint32_t soff = (uint32_t)k0 * sizeof(T);
 #pragma unroll
-      for (int ks = 0; ks < BK / SW; ++ks) {
-        uint4 af[TM], bfg[TN];
+        for (int i = 0; i < AV; ++i) xa[i] = bld16s(ra_r, kok ? aoff[i] : OOB, soff);
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
-          af[i] = *(const uint4*)(sa + (wm * WM + i * 16 + (lane & 15)) * LDS + ks * SW +
-                                  (lane >> 4) * VEC);
+        for (int i = 0; i < BV; ++i) xb[i] = bld16s(rb_r, kok ? boff[i] : OOB, soff);
+      };
+      auto sstore = [&](int buf, const uint4 (&xa)[AV], const uint4 (&xb)[BV]) {
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
-          bfg[j] = *(const uint4*)(sb + (wn * WN + j * 16 + (lane & 15)) * LDS + ks * SW +
-                                   (lane >> 4) * VEC);
+        for (int i = 0; i < AV; ++i) {
+          const int c = tid + i * NT, r = c / KV, kc = (c % KV) * VEC;
+          *(uint4*)(sm.ld.a[buf] + r * LDS + kc) = xa[i];
+        }
 #pragma unroll
-        for (int i = 0; i < TM; ++i)
-#pragma unroll
-          for (int j = 0; j < TN; ++j) acc[i][j] = mfma_step(af[i], bfg[j], acc[i][j], dummy);
-      }
-    };
-    // iteration it: tile it is multiplied from LDS buffer it & 1 (its MFMAs
-    // run while the wave goes on), tile it+1 (ring slot (it+1) % PD) goes to
-    // the other buffer, tile it+1+PD is requested into the freed slot, then
-    // one barrier. Loads and stores are issued unconditionally (tiles past
-    // the end read as zero through the buffer range check), so every path has
-    // the same loads in flight and each wait covers only the oldest ring slot.
-    auto step = [&](int it, uint4 (&xa)[AV], uint4 (&xb)[BV]) {
-      if (it < nk) compute(it & 1);
-      sstore((it + 1) & 1, xa, xb);
-      gload(kbeg + (it + 1 + PD) * BK, xa, xb);
-      __syncthreads();
-    };
+        for (int i = 0; i < BV; ++i) {
+          const int c = tid + i * NT, r = c / KV, kc = (c % KV) * VEC;
+          *(uint4*)(sm.ld.b[buf] + r * LDS + kc) = xb[i];
+        }
+      };
+      // iteration it: tile it is multiplied from LDS buffer it & 1 (its MFMAs
+      // run while the wave goes on), tile it+1 (ring slot (it+1) % PD) goes to
+      // the other buffer, tile it+1+PD is requested into the freed slot, then
+      // one barrier. Loads and stores are issued unconditionally (tiles past
+      // the end read as zero through the buffer range check), so every path has
+      // the same loads in flight and each wait covers only the oldest ring slot.
+      auto step = [&](int it, uint4 (&xa)[AV], uint4 (&xb)[BV]) {
+        if (it < nk) compute(it & 1);
+        sstore((it + 1) & 1, xa, xb);
+        gload(kbeg + (it + 1 + PD) * BK, xa, xb);
+        __syncthreads();
+      };
 
-    __syncthreads();  // the previous tile's epilogue is done with the LDS
-    gload(kbeg, ra[0], rb[0]);
-    sstore(0, ra[0], rb[0]);
-    // the ring slots must be requested in the order the loop consumes them:
-    // the scheduler may not interleave them
+      __syncthreads();  // the previous tile's epilogue is done with the LDS
+      gload(kbeg, ra[0], rb[0]);
+      sstore(0, ra[0], rb[0]);
+      // the ring slots must be requested in the order the loop consumes them:
+      // the scheduler may not interleave them
 #pragma unroll
-    for (int q = 0; q < PD; ++q) {
-      gload(kbeg + (1 + q) * BK, ra[(1 + q) % PD], rb[(1 + q) % PD]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    __syncthreads();  // tile 0 is in LDS
-    for (int it = 0; it < nk; it += PD) {
+      for (int q = 0; q < PD; ++q) {
+        gload(kbeg + (1 + q) * BK, ra[(1 + q) % PD], rb[(1 + q) % PD]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      __syncthreads();  // tile 0 is in LDS
+      for (int it = 0; it < nk; it += PD) {
 #pragma unroll
-      for (int q = 0; q < PD; ++q) step(it + q, ra[(q + 1) % PD], rb[(q + 1) % PD]);
+        for (int q = 0; q < PD; ++q) step(it + q, ra[(q + 1) % PD], rb[(q + 1) % PD]);
+      }
+
     }
 
     // epilogue in 16-row slices: slice i of every wave row goes through LDS,
     // then all threads apply the epilogue with row-contiguous stores
     float* P = (e.kind == EPI_PART ? (float*)e.out : part) + (size_t)s * M * N;
     const bool direct = splits == 1 && e.kind != EPI_PART;
+    // In the direct epilogue thread tid always owns the same two columns,
+    // na and na + 16 (pair index tid % (BN / 2), since NT is a multiple of
+    // BN / 2). Epilogues that only store, or that read nothing but the bias,
+    // take a short path: the bias is loaded once per tile, and each slice's
+    // stores go out back to back. (A load issued between stores would wait
+    // for all of them: the vector memory counter keeps loads and stores in
+    // one issue order.)
+    static_assert(NT % (BN / 2) == 0, "fixed columns per thread");
+    const int qc = tid % (BN / 2), colc = (qc >> 4) * 32 + (qc & 15);
+    const int na = n0 + colc, nb = na + 16;
+    const int ek = e.kind;
+    const bool fast = direct && (ek == EPI_GEGLU || ek == EPI_T || ek == EPI_GELU || ek == EPI_SWISH ||
+                                 (ek == EPI_F32 && !e.rowadd));
+    const bool hasb = fast && ek != EPI_GEGLU && e.bias;
+    float ba = 0.f, bb = 0.f;
+    if (hasb) {
+      if (na < N) ba = e.bias[na];
+      if (nb < N) bb = e.bias[nb];
+    }
     auto slice = [&](auto ic) {
       const int i = ic;
       __syncthreads();
@@ -463,7 +586,53 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
         for (int r = 0; r < 4; ++r)
           sm.c[(wm * 16 + (lane >> 4) * 4 + r) * CLD + wn * WN + j * 16 + (lane & 15)] = acc[i][j][r];
       __syncthreads();
-      if (direct) {
+      if (fast) {
+        constexpr int PER = WGM * 16 * (BN / 2) / NT;
+        // f(m, v0, v1) for this thread's rows of the slice (same arithmetic
+        // as epi_pair)
+        auto each = [&](auto f) {
+#pragma unroll 2
+          for (int k = 0; k < PER; ++k) {
+            const int row = (tid + k * NT) / (BN / 2);
+            const int m = m0 + (row >> 4) * WM + i * 16 + (row & 15);
+            if (m < M) {
+              float v0 = sm.c[row * CLD + colc], v1 = sm.c[row * CLD + colc + 16];
+              if (hasb) {
+                v0 += ba;
+                v1 += bb;
+              }
+              f(m, v0, v1);
+            }
+          }
+        };
+        T* out = (T*)e.out;
+        if (ek == EPI_GEGLU) {
+          const int gcol = 16 * (na >> 5) + (na & 15);
+          if (nb < N)
+            each([&](int m, float v0, float v1) {
+              TT<T>::st(out + out_at<T>(e, m, gcol, e.ldo, e.blk_out), gelu_tanh(v0) * v1);
+            });
+        } else if (ek == EPI_F32) {
+          each([&](int m, float v0, float v1) {
+            float* o = (float*)e.out + (size_t)m * e.ldo + na;
+            if (na < N) o[0] = v0;
+            if (nb < N) o[16] = v1;
+          });
+        } else {
+          // EPI_T, EPI_GELU, EPI_SWISH
+          each([&](int m, float v0, float v1) {
+            if (ek == EPI_GELU) {
+              v0 = gelu_tanh(v0);
+              v1 = gelu_tanh(v1);
+            } else if (ek == EPI_SWISH) {
+              v0 = swishf(v0);
+              v1 = swishf(v1);
+            }
+            if (na < N) TT<T>::st(out + out_at<T>(e, m, na, e.ldo, e.blk_out), v0);
+            if (nb < N) TT<T>::st(out + out_at<T>(e, m, nb, e.ldo, e.blk_out), v1);
+          });
+        }
+      } else if (direct) {
         constexpr int PAIRS = WGM * 16 * (BN / 2);  // (row, 32-column group, j < 16)
         for (int p = tid; p < PAIRS; p += NT) {
           const int row = p / (BN / 2), q = p % (BN / 2);
@@ -764,7 +933,8 @@ GemmPlan plan_gemm(const GemmDesc& g) {
   return p;
 }
 
-template <typename T, int BM, int BN, int BK, int WGM = 2, int WGN = 2, int PD = 1, int PAD = VLA_GEMM_LDS_PAD>
+template <typename T, int BM, int BN, int BK, int WGM = 2, int WGN = 2, int PD = 1, int PAD = VLA_GEMM_LDS_PAD,
+          bool DL = false>
 static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch& s,
                              const LaunchCaps& caps, hipStream_t st) {
   const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
@@ -776,7 +946,7 @@ static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch
   // 4 MB L2
   const size_t band_bytes = (size_t)BM * kchunk * sizeof(T);
   const int group_m = std::max(1, std::min(tiles_m, (int)((2u << 20) / std::max<size_t>(band_bytes, 1))));
-  hipExtLaunchKernelGGL((k_gemm<T, BM, BN, BK, WGM, WGN, PD, PAD>), dim3(grid), dim3(64 * WGM * WGN), 0, st,
+  hipExtLaunchKernelGGL((k_gemm<T, BM, BN, BK, WGM, WGN, PD, PAD, DL>), dim3(grid), dim3(64 * WGM * WGN), 0, st,
                         caps.ev_start,
                         caps.ev_stop, 0, (const T*)g.A, g.lda, (const T*)g.W, g.ldw, g.M, g.N,
                         g.K, kchunk, p.splits, tiles_m, tiles_n, group_m, g.epi, s.ptr);
@@ -802,7 +972,7 @@ hipError_t launch_gemm(const GemmDesc& g, const Scratch& s, const LaunchCaps& ca
     switch (p.cfg) {
       case 0: return run_gemm_t<uint16_t, 128, 128, 64, 2, 2, 3>(g, p, s, caps, st);
       case 1: return run_gemm_t<uint16_t, 64, 64, 64, 2, 2, 2>(g, p, s, caps, st);
-      case 3: return run_gemm_t<uint16_t, 256, 256, 64, 2, 4, 1, 1>(g, p, s, caps, st);
+      case 3: return run_gemm_t<uint16_t, 256, 256, 64, 2, 4, 1, 0, true>(g, p, s, caps, st);
       default: return run_gemm_t<uint16_t, 32, 64, 64, 2, 2, 2>(g, p, s, caps, st);
     }
   }
