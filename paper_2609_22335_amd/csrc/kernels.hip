@@ -569,9 +569,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
     const int qc = tid % (BN / 2), colc = (qc >> 4) * 32 + (qc & 15);
     const int na = n0 + colc, nb = na + 16;
     const int ek = e.kind;
+    // (the row-operand paths are left out of the largest tile, whose 128
+    // accumulators per thread leave few registers; it runs the FFN GEMMs)
+    constexpr bool ROWK = TM * TN < 32;
     const bool fast = direct && (ek == EPI_GEGLU || ek == EPI_T || ek == EPI_GELU || ek == EPI_SWISH ||
-                                 (ek == EPI_F32 && !e.rowadd));
-    const bool hasb = fast && ek != EPI_GEGLU && e.bias;
+                                 (ek == EPI_F32 && !e.rowadd) ||
+                                 (ROWK && (ek == EPI_QKV_ROPE || ek == EPI_QKV_PLAIN || ek == EPI_EULER)));
+    const bool hasb = fast && ek != EPI_GEGLU && ek != EPI_QKV_ROPE && ek != EPI_QKV_PLAIN && e.bias;
     float ba = 0.f, bb = 0.f;
     if (hasb) {
       if (na < N) ba = e.bias[na];
@@ -605,8 +609,117 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
             }
           }
         };
+        // rows' operands that the epilogue reads (RoPE tables, Euler state)
+        // are loaded for the whole slice before its first store
+        // (in groups of at most 4 rows, for registers)
+        auto rows2 = [&](auto ld, auto st) {
+          constexpr int RC = PER < 4 ? PER : 4;
+#pragma nounroll
+          for (int k0 = 0; k0 < PER; k0 += RC) {
+          float o0[RC], o1[RC];
+#pragma unroll
+          for (int k = 0; k < RC; ++k) {
+            const int row = (tid + (k0 + k) * NT) / (BN / 2);
+            const int m = m0 + (row >> 4) * WM + i * 16 + (row & 15);
+            o0[k] = o1[k] = 0.f;
+            if (m < M) ld(m, o0[k], o1[k]);
+          }
+#pragma unroll
+          for (int k = 0; k < RC; ++k) {
+            const int row = (tid + (k0 + k) * NT) / (BN / 2);
+            const int m = m0 + (row >> 4) * WM + i * 16 + (row & 15);
+            if (m < M) {
+              float v0 = sm.c[row * CLD + colc], v1 = sm.c[row * CLD + colc + 16];
+              if (hasb) {
+                v0 += ba;
+                v1 += bb;
+              }
+              st(m, v0, v1, o0[k], o1[k]);
+            }
+          }
+          }
+        };
+        constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
         T* out = (T*)e.out;
-        if (ek == EPI_GEGLU) {
+        if (ROWK && (ek == EPI_QKV_ROPE || ek == EPI_QKV_PLAIN)) {
+          const int hd = e.hd, qcols = e.nq * hd, kcols = e.nkv * hd;
+          if (ek == EPI_QKV_ROPE && na < qcols + kcols) {
+            // column pair (na, nb) holds a rotate-half pair (ri, ri + hd / 2)
+            const bool isq = na < qcols;
+            const int rn = isq ? na : na - qcols;
+            const int head = rn / hd, pp = rn - head * hd;
+            const int ri = 16 * (pp >> 5) + (pp & 15);
+            if (nb < N)
+              rows2(
+                  [&](int m, float& c, float& sn) {
+                    const size_t t = (size_t)(e.pos0 + epi_key(e, m)) * (hd / 2) + ri;
+                    c = e.rope_cos[t];
+                    sn = e.rope_sin[t];
+                  },
+                  [&](int m, float v0, float v1, float c, float sn) {
+                    const float a = v0 * c - v1 * sn, b = v1 * c + v0 * sn;
+                    if (isq) {
+                      T* dst = (T*)e.q + (size_t)m * e.ldq + head * hd;
+                      TT<T>::st(dst + ri, a);
+                      TT<T>::st(dst + ri + hd / 2, b);
+                    } else {
+                      const int key = epi_key(e, m);
+                      T* dst = (T*)e.k + epi_kblk(e, m, e.blk_k);
+                      TT<T>::st(dst + kv_kidx(DT, e.kv_nb, hd, head, key, ri), a);
+                      TT<T>::st(dst + kv_kidx(DT, e.kv_nb, hd, head, key, ri + hd / 2), b);
+                    }
+                  });
+          } else if (ek == EPI_QKV_ROPE) {
+            // V columns
+            const int c0 = na - qcols - kcols, c1 = c0 + 16;
+            if (nb < N)
+              each([&](int m, float v0, float v1) {
+                const int key = epi_key(e, m);
+                T* dst = (T*)e.v + epi_kblk(e, m, e.blk_v);
+                TT<T>::st(dst + kv_vidx(DT, e.kv_nb, hd, c0 / hd, key, c0 % hd), v0);
+                TT<T>::st(dst + kv_vidx(DT, e.kv_nb, hd, c1 / hd, key, c1 % hd), v1);
+              });
+          } else {
+            // EPI_QKV_PLAIN: column c of q, k or v
+            auto put = [&](int m, int n, float v) {
+              if (n < qcols) {
+                TT<T>::st((T*)e.q + (size_t)m * e.ldq + n, v);
+              } else if (n < qcols + kcols) {
+                const int c = n - qcols;
+                TT<T>::st((T*)e.k + epi_kblk(e, m, e.blk_k) +
+                              kv_kidx(DT, e.kv_nb, hd, c / hd, epi_key(e, m), c % hd), v);
+              } else {
+                const int c = n - qcols - kcols;
+                TT<T>::st((T*)e.v + epi_kblk(e, m, e.blk_v) +
+                              kv_vidx(DT, e.kv_nb, hd, c / hd, epi_key(e, m), c % hd), v);
+              }
+            };
+            each([&](int m, float v0, float v1) {
+              if (na < N) put(m, na, v0);
+              if (nb < N) put(m, nb, v1);
+            });
+          }
+        } else if (ROWK && ek == EPI_EULER) {
+          rows2(
+              [&](int m, float& x0, float& x1) {
+                const float* xp = e.x + (size_t)m * e.ldx + na;
+                if (na < N) x0 = xp[0];
+                if (nb < N) x1 = xp[16];
+              },
+              [&](int m, float v0, float v1, float x0, float x1) {
+                float* xp = e.x + (size_t)m * e.ldx + na;
+                if (na < N) {
+                  const float xn = x0 + e.dt * v0;
+                  xp[0] = xn;
+                  TT<T>::st((T*)e.xop + out_at<T>(e, m, na, e.ldxop, e.blk_xop), xn);
+                }
+                if (nb < N) {
+                  const float xn = x1 + e.dt * v1;
+                  xp[16] = xn;
+                  TT<T>::st((T*)e.xop + out_at<T>(e, m, nb, e.ldxop, e.blk_xop), xn);
+                }
+              });
+        } else if (ek == EPI_GEGLU) {
           const int gcol = 16 * (na >> 5) + (na & 15);
           if (nb < N)
             each([&](int m, float v0, float v1) {
@@ -649,13 +762,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
         }
       }
     };
-    // many row slices: a compile-time loop keeps acc indexed by constants
-    if constexpr (TM > 4) {
-      static_for<0, TM>(slice);
-    } else {
-#pragma unroll
-      for (int i = 0; i < TM; ++i) slice(i);
-    }
+    // a compile-time loop keeps acc indexed by constants
+    static_for<0, TM>(slice);
   }
   VLA_WAVE_END(KK_GEMM);
 }
