@@ -273,6 +273,118 @@ __device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int 
   if (n + 16 < N) epi_one<T>(e, m, n + 16, v1);
 }
 
+// The epilogue of PER column pairs of one thread (pair k: row m[k], columns
+// n[k] and n[k] + 16, values v0[k], v1[k]), with the arithmetic of epi_pair
+// on each pair. Everything the epilogue reads (bias, rowadd, Euler state,
+// RoPE tables) is loaded for all pairs before the first store: the vector
+// memory counter keeps loads and stores in one issue order, so a load placed
+// after a store waits for that store's write to complete, and one epi_pair
+// after another would serialise on them. Rows m[k] >= M are skipped.
+template <typename T, int PER>
+__device__ __forceinline__ void epi_pairs(const Epi& e, int M, int N, const int (&m)[PER],
+                                          const int (&n)[PER], float (&v0)[PER], float (&v1)[PER]) {
+  const int kind = e.kind;
+  const bool biased = kind == EPI_F32 || kind == EPI_T || kind == EPI_RESID || kind == EPI_GELU ||
+                      kind == EPI_SWISH || kind == EPI_EULER;
+  if (biased && e.bias) {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      if (n[k] < N) v0[k] += e.bias[n[k]];
+      if (n[k] + 16 < N) v1[k] += e.bias[n[k] + 16];
+    }
+  }
+  if (kind == EPI_F32 && e.rowadd) {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      if (m[k] >= M) continue;
+      const float* ra = e.rowadd + (size_t)(m[k] % e.rowadd_period) * e.ldra;
+      if (n[k] < N) v0[k] += ra[n[k]];
+      if (n[k] + 16 < N) v1[k] += ra[n[k] + 16];
+    }
+  }
+  if (kind == EPI_RESID || kind == EPI_EULER) {
+    // read-modify-write operands: the residual stream, or the Euler state x
+    float* base = kind == EPI_RESID ? e.resid : e.x;
+    const int ld = kind == EPI_RESID ? e.ldr : e.ldx;
+    float r0[PER], r1[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const bool ok = m[k] < M;
+      r0[k] = ok && n[k] < N ? base[(size_t)m[k] * ld + n[k]] : 0.f;
+      r1[k] = ok && n[k] + 16 < N ? base[(size_t)m[k] * ld + n[k] + 16] : 0.f;
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      if (m[k] >= M) continue;
+      float* p = base + (size_t)m[k] * ld + n[k];
+      if (kind == EPI_RESID) {
+        if (n[k] < N) p[0] = r0[k] + v0[k];
+        if (n[k] + 16 < N) p[16] = r1[k] + v1[k];
+      } else {
+        if (n[k] < N) {
+          const float xn = r0[k] + e.dt * v0[k];
+          p[0] = xn;
+          TT<T>::st((T*)e.xop + out_at<T>(e, m[k], n[k], e.ldxop, e.blk_xop), xn);
+        }
+        if (n[k] + 16 < N) {
+          const float xn = r1[k] + e.dt * v1[k];
+          p[16] = xn;
+          TT<T>::st((T*)e.xop + out_at<T>(e, m[k], n[k] + 16, e.ldxop, e.blk_xop), xn);
+        }
+      }
+    }
+    return;
+  }
+  if (kind == EPI_QKV_ROPE) {
+    const int hd = e.hd, qcols = e.nq * hd, kcols = e.nkv * hd;
+    float c[PER], sn[PER];
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      c[k] = 1.f;
+      sn[k] = 0.f;
+      if (m[k] < M && n[k] + 16 < N && n[k] < qcols + kcols) {
+        const int rn = n[k] < qcols ? n[k] : n[k] - qcols;
+        const int pp = rn % hd;
+        const int i = 16 * (pp >> 5) + (pp & 15);
+        const size_t t = (size_t)(e.pos0 + epi_key(e, m[k])) * (hd / 2) + i;
+        c[k] = e.rope_cos[t];
+        sn[k] = e.rope_sin[t];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      if (m[k] >= M || n[k] + 16 >= N) continue;
+      if (n[k] < qcols + kcols) {
+        const bool isq = n[k] < qcols;
+        const int rn = isq ? n[k] : n[k] - qcols;
+        const int head = rn / hd, pp = rn - head * hd;
+        const int i = 16 * (pp >> 5) + (pp & 15);
+        const float a = v0[k] * c[k] - v1[k] * sn[k], b = v1[k] * c[k] + v0[k] * sn[k];
+        if (isq) {
+          T* dst = (T*)e.q + (size_t)m[k] * e.ldq + head * hd;
+          TT<T>::st(dst + i, a);
+          TT<T>::st(dst + i + hd / 2, b);
+        } else {
+          constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
+          const int key = epi_key(e, m[k]);
+          T* dst = (T*)e.k + epi_kblk(e, m[k], e.blk_k);
+          TT<T>::st(dst + kv_kidx(DT, e.kv_nb, hd, head, key, i), a);
+          TT<T>::st(dst + kv_kidx(DT, e.kv_nb, hd, head, key, i + hd / 2), b);
+        }
+      } else {
+        epi_pair<T>(e, M, N, m[k], n[k], v0[k], v1[k]);  // V columns: stores only
+      }
+    }
+    return;
+  }
+  // the rest only store: bias and rowadd are already in v0 / v1
+  Epi f = e;
+  f.bias = nullptr;
+  f.rowadd = nullptr;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) epi_pair<T>(f, M, N, m[k], n[k], v0[k], v1[k]);
+}
+
 // ---------------------------------------------------------------------------
 // GEMM: C[M, N] = A[M, K] W[N, K]^T, both operands K-contiguous.
 // 256 threads = 4 waves in a 2 x 2 arrangement; each wave owns a
@@ -878,23 +990,27 @@ __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, size_t 
     __syncthreads();
     // wave w finishes m-tile w: sum the four waves in order, then the epilogue
     const int mt = wave;
+    const int n = np * 32 + (lane & 15);
+    int mg[4], nn[4];
+    float v0[4], v1[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      float v[2];
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-        v[nb] = ((red[0][nb * 4 + mt][r][lane] + red[1][nb * 4 + mt][r][lane]) +
-                 red[2][nb * 4 + mt][r][lane]) + red[3][nb * 4 + mt][r][lane];
+      v0[r] = ((red[0][mt][r][lane] + red[1][mt][r][lane]) + red[2][mt][r][lane]) + red[3][mt][r][lane];
+      v1[r] = ((red[0][4 + mt][r][lane] + red[1][4 + mt][r][lane]) + red[2][4 + mt][r][lane]) +
+              red[3][4 + mt][r][lane];
       const int m = mt * 16 + (lane >> 4) * 4 + r;
-      const int n = np * 32 + (lane & 15);
-      if (m >= M) continue;
-      const int mg = f * M + m;  // row over all frames
-      if (splits == 1 && e.kind != EPI_PART) {
-        epi_pair<T>(e, Mt, N, mg, n, v[0], v[1]);
-      } else {
-        float* P = (e.kind == EPI_PART ? (float*)e.out : part) + (size_t)s * Mt * N + (size_t)mg * N;
-        if (n < N) P[n] = v[0];
-        if (n + 16 < N) P[n + 16] = v[1];
+      mg[r] = m < M ? f * M + m : Mt;  // row over all frames (Mt: skipped)
+      nn[r] = n;
+    }
+    if (splits == 1 && e.kind != EPI_PART) {
+      epi_pairs<T, 4>(e, Mt, N, mg, nn, v0, v1);
+    } else {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        if (mg[r] >= Mt) continue;
+        float* P = (e.kind == EPI_PART ? (float*)e.out : part) + (size_t)s * Mt * N + (size_t)mg[r] * N;
+        if (n < N) P[n] = v0[r];
+        if (n + 16 < N) P[n + 16] = v1[r];
       }
     }
   }
