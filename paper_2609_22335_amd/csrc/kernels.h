@@ -291,6 +291,11 @@ hipError_t launch_cvt_pad(int dtype, const float* src, int rows, int cols, void*
 // Row-major copy of a weight stored in MFMA fragment order: out[n * K + k] =
 // W[frag_index(n, k, KS)] for n < N, k < K (operand type; K a multiple of 8).
 hipError_t launch_unfrag(int dtype, const void* frag, int N, int K, int KS, void* out, hipStream_t st);
+// Device-to-device copy of `bytes` bytes as a kernel on stream st. (The
+// runtime's device-to-device copies run as its own copy kernels, which a
+// kernel trace shows on the default stream's hardware queue; this keeps the
+// pipeline's staging copies on the queue of the stream that orders them.)
+hipError_t launch_copy(void* dst, const void* src, size_t bytes, hipStream_t st);
 
 // dst[r, :] = row (operand type) for every r < rows.
 hipError_t launch_bcast_row(int dtype, const void* row, int cols, void* dst, int ld_dst, int rows,

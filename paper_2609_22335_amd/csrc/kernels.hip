@@ -1034,6 +1034,32 @@ __global__ __launch_bounds__(256) void k_unfrag(const T* __restrict__ Wf, int N,
   }
 }
 
+// Copy in 16-byte pieces when both pointers and the size allow it, else in
+// bytes.
+__global__ __launch_bounds__(256) void k_copy16(uint4* __restrict__ dst, const uint4* __restrict__ src, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    dst[i] = src[i];
+}
+__global__ __launch_bounds__(256) void k_copy1(unsigned char* __restrict__ dst, const unsigned char* __restrict__ src,
+                                               size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    dst[i] = src[i];
+}
+
+hipError_t launch_copy(void* dst, const void* src, size_t bytes, hipStream_t st) {
+  if (bytes == 0) return hipSuccess;
+  if (!dst || !src) return hipErrorInvalidValue;
+  if (((uintptr_t)dst | (uintptr_t)src | bytes) % 16 == 0) {
+    const size_t n = bytes / 16;
+    const int grid = (int)std::min<size_t>((n + 255) / 256, 1024);
+    k_copy16<<<grid, 256, 0, st>>>((uint4*)dst, (const uint4*)src, n);
+  } else {
+    const int grid = (int)std::min<size_t>((bytes + 255) / 256, 1024);
+    k_copy1<<<grid, 256, 0, st>>>((unsigned char*)dst, (const unsigned char*)src, bytes);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_unfrag(int dtype, const void* frag, int N, int K, int KS, void* out, hipStream_t st) {
   const int vec = dtype == DT_BF16 ? 8 : 4;
   if (N <= 0 || K <= 0 || K % vec || KS * frag_slab(dtype) < K) return hipErrorInvalidValue;

@@ -1621,20 +1621,31 @@ static int get_streams(vla_model* m, const vla_sched& s, Streams* out) {
       std::vector<uint32_t> mv, ma;
       cu_mask(0, s.vlm_cus, m->num_cus, mv);
       cu_mask(s.vlm_cus, s.act_cus, m->num_cus, ma);
-      for (int i = 0; i < MAX_VLM_STREAMS; ++i)
-        HIP_TRY(hipExtStreamCreateWithCUMask(&st.v[i], (uint32_t)mv.size(), mv.data()));
-      for (int i = 0; i < MAX_ACT_STREAMS; ++i)
+      // creation order: as for the plain streams below
+      HIP_TRY(hipExtStreamCreateWithCUMask(&st.v[0], (uint32_t)mv.size(), mv.data()));
+      for (int i = 0; i < 2; ++i)
         HIP_TRY(hipExtStreamCreateWithCUMask(&st.a[i], (uint32_t)ma.size(), ma.data()));
+      for (int i = 2; i < MAX_ACT_STREAMS; ++i)
+        HIP_TRY(hipExtStreamCreateWithCUMask(&st.a[i], (uint32_t)ma.size(), ma.data()));
+      for (int i = 1; i < MAX_VLM_STREAMS; ++i)
+        HIP_TRY(hipExtStreamCreateWithCUMask(&st.v[i], (uint32_t)mv.size(), mv.data()));
       it = m->mask_streams.emplace(key, st).first;
     }
     *out = it->second;
     return VLA_OK;
   }
   if (!m->plain.v[0]) {
-    for (int i = 0; i < MAX_VLM_STREAMS; ++i)
-      HIP_TRY(hipStreamCreateWithFlags(&m->plain.v[i], hipStreamNonBlocking));
-    for (int i = 0; i < MAX_ACT_STREAMS; ++i)
+    // The HIP runtime maps streams onto a few hardware queues (4 per process
+    // unless GPU_MAX_HW_QUEUES says otherwise) and later streams share them.
+    // The first VLM stream and the first two action streams are created
+    // first, so the common schedules (one VLM lane, one or two action lanes)
+    // get hardware queues of their own next to the default stream's.
+    HIP_TRY(hipStreamCreateWithFlags(&m->plain.v[0], hipStreamNonBlocking));
+    for (int i = 0; i < 2; ++i) HIP_TRY(hipStreamCreateWithFlags(&m->plain.a[i], hipStreamNonBlocking));
+    for (int i = 2; i < MAX_ACT_STREAMS; ++i)
       HIP_TRY(hipStreamCreateWithFlags(&m->plain.a[i], hipStreamNonBlocking));
+    for (int i = 1; i < MAX_VLM_STREAMS; ++i)
+      HIP_TRY(hipStreamCreateWithFlags(&m->plain.v[i], hipStreamNonBlocking));
   }
   *out = m->plain;
   return VLA_OK;
@@ -1785,13 +1796,11 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
     if (graphs) {
       for (int i = 0; i < n; ++i) {
         const vla_frame& fr = frames[g0 + i];
-        HIP_TRY(hipMemcpyAsync(vw->pstage + i * pix_bytes / 4, fr.pixels, pix_bytes, hipMemcpyDeviceToDevice, sv));
+        HIP_TRY(launch_copy(vw->pstage + i * pix_bytes / 4, fr.pixels, pix_bytes, sv));
         if (c.n_text > 0)
-          HIP_TRY(hipMemcpyAsync(vw->istage + (size_t)i * c.n_text, fr.text_ids, (size_t)c.n_text * 4,
-                                 hipMemcpyDeviceToDevice, sv));
+          HIP_TRY(launch_copy(vw->istage + (size_t)i * c.n_text, fr.text_ids, (size_t)c.n_text * 4, sv));
         if (c.state_dim > 0)
-          HIP_TRY(hipMemcpyAsync(vw->sstage + (size_t)i * c.state_dim, fr.state, (size_t)c.state_dim * 4,
-                                 hipMemcpyDeviceToDevice, sv));
+          HIP_TRY(launch_copy(vw->sstage + (size_t)i * c.state_dim, fr.state, (size_t)c.state_dim * 4, sv));
       }
       HIP_TRY(hipGraphLaunch(m->pre_graphs[std::make_tuple(vi, ci, vcaps.max_wgs, n)], sv));
     } else {
@@ -1816,9 +1825,9 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
       HIP_TRY(hipEventRecord(m->eva[2 * a0], sa));
       ActWs* aw = m->aws[li].get();
       if (graphs) {
-        HIP_TRY(hipMemcpyAsync(aw->nstage, noise + a0 * chunk, na * chunk * 4, hipMemcpyDeviceToDevice, sa));
+        HIP_TRY(launch_copy(aw->nstage, noise + a0 * chunk, na * chunk * 4, sa));
         HIP_TRY(hipGraphLaunch(m->den_graphs[den_key(li, a0, na)], sa));
-        HIP_TRY(hipMemcpyAsync(actions + a0 * chunk, aw->xg, na * chunk * 4, hipMemcpyDeviceToDevice, sa));
+        HIP_TRY(launch_copy(actions + a0 * chunk, aw->xg, na * chunk * 4, sa));
       } else {
         Run ra{m, sa, acaps, &aw->scr, aw};
         const vla_ctx* cs[MAX_ACT_BATCH] = {};
