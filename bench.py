@@ -273,7 +273,7 @@ def main():
         kw[f"batch{b_}_graph"] = dict(mode="concurrent", act_batch=b_, graphs=True)
         kw[f"batch{b_}_lanes2_graph"] = dict(mode="concurrent", act_batch=b_, act_streams=2, graphs=True)
         kw[f"batch{b_}_v2_graph"] = dict(mode="concurrent", act_batch=b_, vlm_streams=2, graphs=True)
-    for a_, b_ in ((224, 32), (192, 64), (160, 96)):  # CU-split sweep entries
+    for a_, b_ in ((224, 32), (192, 64), (160, 96), (128, 128), (96, 160)):  # CU-split sweep entries
         kw[f"cu_{a_}_{b_}"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_)
         kw[f"cu_{a_}_{b_}_lanes2"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_, act_streams=2, graphs=True)
         kw[f"cu_{a_}_{b_}_lanes3"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_, act_streams=3, graphs=True)

@@ -1,0 +1,112 @@
+"""Intensity descriptors and the CU-split planner (host logic, no GPU).
+
+The quantisation and the descriptor arithmetic follow the paper's offline
+profiling pass (section on profile metadata, table of intensity fields):
+fraction of peak on the matrix, ALU and DRAM pipelines, quantised to 0..15.
+The planner's cases below are worked by hand."""
+import csv
+import math
+
+import pytest
+
+from paper_2609_22335_amd import intensity as I
+
+
+def test_quantize_levels():
+    assert I.quantize(0.0) == 0
+    assert I.quantize(-0.1) == 0
+    assert I.quantize(float("nan")) == 0
+    assert I.quantize(1.0) == 15
+    assert I.quantize(3.0) == 15
+    assert I.quantize(0.5) == 8          # 7.5 rounds half up
+    assert I.quantize(1 / 30 - 1e-9) == 0  # just below level 1's lower edge (0.5 / 15)
+    assert I.quantize(1 / 30 + 1e-9) == 1
+    assert I.quantize(7 / 15) == 7
+    levels = [I.quantize(i / 1000) for i in range(1001)]
+    assert levels == sorted(levels) and set(levels) == set(range(16))
+
+
+def _write(path, header, rows):
+    with open(path, "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(header)
+        w.writerows(rows)
+
+
+TRACE_H = ["Kernel_Name", "Grid_Size_X", "Workgroup_Size_X", "Start_Timestamp", "End_Timestamp"]
+CTR_H = ["Kernel_Name", "Grid_Size", "Workgroup_Size", "Counter_Name", "Counter_Value"]
+
+
+def test_descriptor_arithmetic(tmp_path):
+    # kernel A: 256 workgroups of 256 threads, 10 us per launch; kernel B:
+    # 8 workgroups of 64 threads, 2 us
+    _write(tmp_path / "t1.csv", TRACE_H, [["A", 65536, 256, 0, 10_000], ["B", 512, 64, 0, 2_000],
+                                          ["S", 64, 64, 0, 1_000]])
+    _write(tmp_path / "t3.csv", TRACE_H, [["A", 65536, 256, 0, 10_000]] * 3 + [["B", 512, 64, 0, 2_000]] * 7 +
+           [["S", 64, 64, 0, 1_000]])
+    small, large = I.read_trace(str(tmp_path / "t1.csv")), I.read_trace(str(tmp_path / "t3.csv"))
+    counts = I.frame_counts(small, large, 2)
+    assert counts == {("A", 256, 256): 1.0, ("B", 8, 64): 3.0}  # set-up kernel S cancels
+    # A: 12.5 GFLOP of bf16 MFMA in 10 us = 1.25 PFLOP/s = half of peak;
+    # B: 0.3146 GFLOP of fp32 VALU in 2 us = 157.3 TFLOP/s = all of peak
+    alu_rows = [["A", 65536, 256, "SQ_INSTS_VALU_MFMA_MOPS_BF16", 12.5e9 / 512],
+                ["A", 65536, 256, "SQ_INSTS_VALU_FLOPS_FP32", 0],
+                ["B", 512, 64, "SQ_INSTS_VALU_MFMA_MOPS_BF16", 0],
+                ["B", 512, 64, "SQ_INSTS_VALU_FLOPS_FP32", 157.3e12 * 2e-6 * 0.75],
+                ["B", 512, 64, "SQ_INSTS_VALU_FLOPS_FP32_TRANS", 157.3e12 * 2e-6 * 0.25]]
+    _write(tmp_path / "alu.csv", CTR_H, alu_rows)
+    # DRAM: A moves 20 MB in 10 us = 2 TB/s = 0.25 of 8 TB/s (counted KiB
+    # are half the true fetched bytes, scale 2; writes counted 1:1)
+    _write(tmp_path / "fe.csv", CTR_H, [["A", 65536, 256, "FETCH_SIZE", 8e6 / 1024 / 2], ["B", 512, 64, "FETCH_SIZE", 0]])
+    _write(tmp_path / "wr.csv", CTR_H, [["A", 65536, 256, "WRITE_SIZE", 12e6 / 1024], ["B", 512, 64, "WRITE_SIZE", 0]])
+    d = I.descriptors(large, I.read_counters(str(tmp_path / "alu.csv")), I.read_counters(str(tmp_path / "fe.csv")),
+                      I.read_counters(str(tmp_path / "wr.csv")), 2.0, 1.0, counts, "vlm")
+    by = {x["kernel"]: x for x in d}
+    assert by["A"]["frac"] == pytest.approx([0.5, 0.0, 0.25])
+    assert by["A"]["tau"] == [8, 0, 4]
+    assert by["B"]["frac"] == pytest.approx([0.0, 1.0, 0.0])
+    assert by["B"]["tau"] == [0, 15, 0]
+    assert by["A"]["us"] == pytest.approx(10.0) and by["B"]["launches_per_frame"] == 3.0
+    assert d[0]["kernel"] == "A"  # ordered by time per frame (10 us vs 6 us)
+
+
+def test_copy_scale(tmp_path):
+    _write(tmp_path / "c.csv", CTR_H, [["void at::elementwise_copy", 1 << 20, 256, "FETCH_SIZE", 131072],
+                                       ["other", 4, 64, "FETCH_SIZE", 10]])
+    c = I.read_counters(str(tmp_path / "c.csv"))
+    assert I.copy_scale(c, "FETCH_SIZE", 262144.0) == pytest.approx(2.0)
+    with pytest.raises(ValueError):
+        I.copy_scale(c, "WRITE_SIZE", 1.0)
+
+
+def _d(phase, wgs, us, lpf=1.0, mem=0.1):
+    return {"kernel": f"{phase}{wgs}", "workgroups": wgs, "wg_threads": 256, "phase": phase,
+            "launches_per_frame": lpf, "us": us, "frac": [0.0, 0.0, mem], "tau": [0, 0, I.quantize(mem)]}
+
+
+def test_planner_worked_case():
+    # VLM: one 256-workgroup kernel, 1 ms alone; action: one 32-workgroup
+    # kernel, 0.5 ms alone. On c VLM CUs the VLM takes 256 / c ms, the
+    # action 0.5 * max(1, 32 / (256 - c)) ms:
+    #   c = 224: max(1.143, 0.5) = 1.143;  c = 232: max(1.103, 0.667) = 1.103
+    #   c = 240: max(1.067, 1.0)  = 1.067;  c = 248: max(1.032, 2.0)   = 2.0
+    desc = [_d("vlm", 256, 1000.0), _d("action", 32, 500.0)]
+    assert I.phase_time(desc, "vlm", 128) == pytest.approx(2e-3)
+    assert I.phase_time(desc, "action", 128) == pytest.approx(0.5e-3)
+    assert I.phase_time(desc, "action", 16) == pytest.approx(1e-3)
+    p = I.plan_cu_split(desc)
+    assert (p["vlm_cus"], p["act_cus"]) == (240, 16)
+    assert p["per_frame_s"] == pytest.approx(256 / 240 * 1e-3)
+    assert p["hbm_share"] == pytest.approx(0.2)
+
+
+def test_planner_hbm_stretch_and_weights():
+    # two launches per frame of the action kernel count twice; DRAM
+    # fractions 0.7 (VLM) and 0.6 (action, time-weighted) exceed 1 together,
+    # so both phases stretch by 1.3
+    desc = [_d("vlm", 64, 100.0, mem=0.7), _d("action", 8, 50.0, lpf=2.0, mem=0.9), _d("action", 8, 100.0, mem=0.3)]
+    assert I.mem_level(desc, "action") == pytest.approx((100 * 0.9 + 100 * 0.3) / 200)
+    p = I.predict_split(desc, 128)
+    assert p["vlm_s"] == pytest.approx(100e-6) and p["action_s"] == pytest.approx(200e-6)
+    assert p["per_frame_s"] == pytest.approx(200e-6 * 1.3)
+    assert math.isclose(p["hbm_share"], 1.3)
