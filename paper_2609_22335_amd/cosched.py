@@ -43,7 +43,7 @@ from __future__ import annotations
 
 import heapq
 import math
-from dataclasses import dataclass, field
+from dataclasses import dataclass
 from typing import Dict, List, Optional, Sequence, Tuple
 
 U_MAX = 255
@@ -73,7 +73,6 @@ class _Run:
     order: int              # dispatcher order (launch time, then stream)
     pending: int
     running: int = 0
-    done_at: float = -1.0
 
 
 @dataclass
@@ -84,6 +83,7 @@ class _WG:
     last: float             # time of the last rate update
     rate: float
     gen: int = 0
+    rid: int = -1           # the run it belongs to
 
 
 def wg_seconds(isolated_s: float, workgroups: int, occupancy: int, num_cus: int) -> float:
@@ -217,8 +217,7 @@ def simulate(launches: Sequence[Launch], num_cus: int, policy: str = "baseline")
                 sim.used[j] += 1.0 / k.occupancy
                 sim.resident[j][rid] = sim.resident[j].get(rid, 0) + 1
                 sim._add(j, k, +1)
-                w = _WG(run, j, k.wg_seconds, t, 1.0)
-                w.rid = rid
+                w = _WG(run, j, k.wg_seconds, t, 1.0, 0, rid)
                 sim.wgs[j].append(w)
                 live[id(w)] = w
                 sim.admitted += 1

@@ -27,13 +27,8 @@ def test_stream_order_and_dependency():
 
 
 def test_head_of_line_blocking_removed():
-    # A: 16 workgroups that fill 2 CUs twice over (occupancy 1, 1 s each);
-    # B (other stream, launched right after): 2 workgroups of 0.1 s at
-    # occupancy 2 (half a CU each). Baseline: B waits until A has issued all
-    # of its workgroups (after round 7, t = 7 s) -> B ends at 7.1 s... but a
-    # CU is full until an A workgroup ends; two-phase: a CU has no room for B
-    # either while A holds it fully, so compare with A at occupancy 2 (half
-    # a CU per workgroup): then B gets a half-CU slot on each CU at once.
+    # A: 16 workgroups at two per CU (1 s each) on 2 CUs: 4 rounds. B (other
+    # stream, launched right after A): 2 workgroups of 0.1 s at two per CU.
     a = K("A", 16, 2, 1.0, (10, 0, 0))
     b = K("B", 2, 2, 0.1, (0, 0, 10))
     L = [C.Launch(a, 0), C.Launch(b, 1)]
@@ -84,23 +79,15 @@ def test_grid_and_reg_scores():
 
 
 def test_contention_slows_shared_pipeline():
-    # two kernels that each saturate HBM alone (tau 15 at occupancy 1) share
-    # one CU at occupancy 2: the CU's memory load is 15 / 2 * 2 = 15 -> rate
-    # 1; at occupancy 1 each they cannot co-reside. With tau 15 at occupancy 2
-    # and two workgroups of each kernel... keep it exact: one CU, a kernel
-    # with tau_mem 15 and occupancy 2 admitted twice: load 15 -> no slowdown;
-    # two different kernels each tau_mem 15 at occupancy 2, one workgroup
-    # each: load 7.5 + 7.5 = 15 -> rate 1.
+    # one CU; a workgroup carries tau / occupancy of its kernel's level.
+    # a and b (memory level 15, two per CU) side by side: load 7.5 + 7.5 = 15,
+    # no slowdown
     a = K("a", 1, 2, 1.0, (0, 0, 15))
     b = K("b", 1, 2, 1.0, (0, 0, 15))
     r = C.simulate([C.Launch(a, 0), C.Launch(b, 1)], 1, "two_phase")
     assert r["makespan"] == pytest.approx(1.0)
-    # a third kernel's workgroup cannot fit; make b occupancy 4 (quarter CU,
-    # tau 15 / 4 each) with 2 workgroups: load 7.5 + 3.75 * 2 = 15 -> rate 1;
-    # with tau_mem 15 at occupancy 1 for a it would not fit at all. Over
-    # subscription: a at occupancy 2 with tau 15 plus b at occupancy 2 with
-    # tau 30 (beyond the 4-bit range, to force it): load 7.5 + 15 = 22.5 ->
-    # rate 1 / 1.5 while both run
+    # b2 at level 30 (beyond the 4-bit range, to oversubscribe): load
+    # 7.5 + 15 = 22.5, both run at rate 1 / 1.5 and end at 1.5 s
     b2 = K("b2", 1, 2, 1.0, (0, 0, 30))
     r = C.simulate([C.Launch(a, 0), C.Launch(b2, 1)], 1, "two_phase")
     assert r["makespan"] == pytest.approx(1.5)
