@@ -189,7 +189,8 @@ def main():
                                        "batch8_lanes2_graph,vb4_ab4_lanes2_graph,vb8_ab4_lanes2_graph,"
                                        "vb8_ab8_lanes2_graph;"
                                        "pi0:8:async2_serial,async2_lanes2_graph,async2_vb8_ab4_lanes2_graph,"
-                                       "async2_vb8_ab8_lanes2_graph,async4_serial,async4_vb8_ab8_lanes2_graph",
+                                       "async2_vb8_ab8_lanes2_graph,async4_serial,async4_vb8_ab8_lanes2_graph;"
+                                       "pi0_ddim:8:serial,vb8_ab8_graph,vb8_ab4_lanes2_graph",
                     help="further workloads, ';'-separated preset:R:schedule,schedule,...")
     ap.add_argument("--extra-steps", type=int, default=5)
     ap.add_argument("--residency", type=int, default=8_000_000,

@@ -64,6 +64,7 @@ typedef struct vla_config {
   int32_t head;     /* VLA_HEAD_PI0 or VLA_HEAD_DIT                                  */
   int32_t shuffle;  /* pixel-shuffle factor of the ViT grid before the projector (1: none) */
   int32_t ex_heads; /* VLA_HEAD_DIT: attention heads of the DiT (head dim ex_dim / ex_heads) */
+  int32_t sampler;  /* VLA_SAMPLER_EULER or VLA_SAMPLER_DDIM (see below)              */
 } vla_config;
 
 /* Action-head families (Section 2.1): the pi0-style expert runs its own
@@ -73,6 +74,18 @@ typedef struct vla_config {
  * layers self-attending) reads per-frame cross K/V made from those features. */
 #define VLA_HEAD_PI0 0
 #define VLA_HEAD_DIT 1
+
+/* Samplers of the action head (Section 2.1 names flow-matching and diffusion
+ * heads). EULER: flow matching from noise at t = 1 to data at t = 0, the head
+ * output read as a velocity, t_k = (N - k) / N and x += -(1/N) v. DDIM: the
+ * head output read as the noise estimate; deterministic DDIM over a linear
+ * beta schedule (1e-4 .. 0.02, 1000 training steps), timesteps
+ * s_k = floor((N - k) 1000 / N) - 1, time input t_k = s_k / 1000, and
+ * x <- a_k x + b_k eps with a_k = sqrt(abar_{k+1} / abar_k),
+ * b_k = sqrt(1 - abar_{k+1}) - a_k sqrt(1 - abar_k) (abar after the last
+ * step = 1). */
+#define VLA_SAMPLER_EULER 0
+#define VLA_SAMPLER_DDIM 1
 
 typedef struct vla_model vla_model;
 typedef struct vla_ctx vla_ctx;

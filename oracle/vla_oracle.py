@@ -208,6 +208,43 @@ def euler_integrate(x0, velocity: Callable[[np.ndarray, float], np.ndarray], n_s
     return x
 
 
+DDIM_TRAIN_STEPS = 1000
+
+
+def ddim_alpha_bar(train_steps: int = DDIM_TRAIN_STEPS) -> np.ndarray:
+    """Cumulative products abar_s = prod_{i <= s} (1 - beta_i) of a linear beta
+    schedule from 1e-4 to 0.02 over the training steps (the DDPM schedule)."""
+    beta = np.linspace(1e-4, 0.02, train_steps, dtype=np.float64)
+    return np.cumprod(1.0 - beta)
+
+
+def ddim_schedule(n_steps: int) -> Tuple[List[float], List[int], np.ndarray]:
+    """Deterministic DDIM sampling in N steps: timesteps s_k =
+    floor((N - k) T / N) - 1 for k = 0 .. N-1 (T training steps), the head's
+    time input t_k = s_k / T (one fp32 division, as the flow-matching times),
+    and abar at each timestep followed by abar = 1 after the last step."""
+    T = DDIM_TRAIN_STEPS
+    s = [(n_steps - k) * T // n_steps - 1 for k in range(n_steps)]
+    ts = [float(np.float32(sk) / np.float32(T)) for sk in s]
+    ab = ddim_alpha_bar()
+    abar = np.array([ab[sk] for sk in s] + [1.0])
+    return ts, s, abar
+
+
+def ddim_integrate(x0, eps: Callable[[np.ndarray, float], np.ndarray], n_steps):
+    """DDIM (eta = 0): from x_k at abar_k, the clean estimate
+    x0_hat = (x_k - sqrt(1 - abar_k) eps) / sqrt(abar_k) and
+    x_{k+1} = sqrt(abar_{k+1}) x0_hat + sqrt(1 - abar_{k+1}) eps, with eps the
+    head's output at (x_k, t_k); returns x_N."""
+    ts, _, abar = ddim_schedule(n_steps)
+    x = np.asarray(x0, dtype=np.float64)
+    for k in range(n_steps):
+        e = eps(x, ts[k])
+        x0_hat = (x - np.sqrt(1.0 - abar[k]) * e) / np.sqrt(abar[k])
+        x = np.sqrt(abar[k + 1]) * x0_hat + np.sqrt(1.0 - abar[k + 1]) * e
+    return x
+
+
 # ---------------------------------------------------------------------------
 # Phase 1: VLM prefill
 # ---------------------------------------------------------------------------
@@ -440,12 +477,15 @@ def dit_velocity(P, cfg, cross, x, t):
 
 def action_denoise(P, cfg, cache, noise):
     """Euler integration of the head's velocity from x_0 = noise (t = 1) to
-    t = 0; returns the action chunk [chunk_len, action_dim]. ``cache`` is the
-    phase-1 hand-off (KV cache, or the DiT's cross K/V)."""
+    t = 0, or DDIM steps with the head's output as the noise estimate
+    (cfg["sampler"] == 1); returns the action chunk [chunk_len, action_dim].
+    ``cache`` is the phase-1 hand-off (KV cache, or the DiT's cross K/V)."""
     if cfg.get("head", 0) == 1:
         vel = lambda x, t: dit_velocity(P, cfg, cache, x, t)
     else:
         vel = lambda x, t: expert_velocity(P, cfg, cache, x, t)
+    if cfg.get("sampler", 0) == 1:
+        return ddim_integrate(noise, vel, cfg["n_steps"])
     return euler_integrate(noise, vel, cfg["n_steps"])
 
 

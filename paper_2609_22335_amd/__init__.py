@@ -31,9 +31,10 @@ CONFIG_FIELDS = (
     "lm_dim", "lm_heads", "lm_kv_heads", "head_dim", "lm_mlp", "lm_layers",
     "vocab", "n_text", "state_dim",
     "ex_dim", "ex_mlp", "ex_layers", "chunk_len", "action_dim", "n_steps",
-    "head", "shuffle", "ex_heads",
+    "head", "shuffle", "ex_heads", "sampler",
 )
 HEAD_PI0, HEAD_DIT = 0, 1
+SAMPLER_EULER, SAMPLER_DDIM = 0, 1
 
 
 class vla_config(ctypes.Structure):

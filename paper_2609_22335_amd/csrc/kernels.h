@@ -121,6 +121,7 @@ struct Epi {
   void* xop = nullptr;
   int ldxop = 0;
   float dt = 0.f;
+  float xs = 1.f;  // EPI_EULER: x <- xs x + dt v
   // Frame blocks (batched action phase): with blk_rows > 0, row m is row
   // m % blk_rows of frame m / blk_rows. Row-block-layout outputs (out, xop)
   // of frame b start b * blk_out elements in (see afrag_index_blk), its own

@@ -218,7 +218,7 @@ __device__ __forceinline__ void epi_one(const Epi& e, int m, int n, float v) {
     case EPI_EULER: {
       if (e.bias) v += e.bias[n];
       float* xp = e.x + (size_t)m * e.ldx + n;
-      const float xn = *xp + e.dt * v;
+      const float xn = __builtin_fmaf(e.dt, v, *xp * e.xs);
       *xp = xn;
       TT<T>::st((T*)e.xop + out_at<T>(e, m, n, e.ldxop, e.blk_xop), xn);
       break;
@@ -322,12 +322,12 @@ __device__ __forceinline__ void epi_pairs(const Epi& e, int M, int N, const int 
         if (n[k] + 16 < N) p[16] = r1[k] + v1[k];
       } else {
         if (n[k] < N) {
-          const float xn = r0[k] + e.dt * v0[k];
+          const float xn = __builtin_fmaf(e.dt, v0[k], r0[k] * e.xs);
           p[0] = xn;
           TT<T>::st((T*)e.xop + out_at<T>(e, m[k], n[k], e.ldxop, e.blk_xop), xn);
         }
         if (n[k] + 16 < N) {
-          const float xn = r1[k] + e.dt * v1[k];
+          const float xn = __builtin_fmaf(e.dt, v1[k], r1[k] * e.xs);
           p[16] = xn;
           TT<T>::st((T*)e.xop + out_at<T>(e, m[k], n[k] + 16, e.ldxop, e.blk_xop), xn);
         }
@@ -821,12 +821,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
               [&](int m, float v0, float v1, float x0, float x1) {
                 float* xp = e.x + (size_t)m * e.ldx + na;
                 if (na < N) {
-                  const float xn = x0 + e.dt * v0;
+                  const float xn = __builtin_fmaf(e.dt, v0, x0 * e.xs);
                   xp[0] = xn;
                   TT<T>::st((T*)e.xop + out_at<T>(e, m, na, e.ldxop, e.blk_xop), xn);
                 }
                 if (nb < N) {
-                  const float xn = x1 + e.dt * v1;
+                  const float xn = __builtin_fmaf(e.dt, v1, x1 * e.xs);
                   xp[16] = xn;
                   TT<T>::st((T*)e.xop + out_at<T>(e, m, nb, e.ldxop, e.blk_xop), xn);
                 }

@@ -122,15 +122,18 @@ static int validate(const vla_config* c) {
     return bad("model widths must be multiples of 8");
   if (c->ex_dim % 32) return bad("ex_dim must be a multiple of 32");
   if (c->chunk_len > 64 || c->n_steps > 64) return bad("chunk_len and n_steps must be <= 64");
+  if (c->sampler != VLA_SAMPLER_EULER && c->sampler != VLA_SAMPLER_DDIM) return bad("unknown sampler");
+  if (c->sampler == VLA_SAMPLER_DDIM && c->n_steps > 1000) return bad("DDIM: n_steps must be <= 1000");
   return VLA_OK;
 }
 
 static bool preset(const char* name, vla_config* o) {
   if (!name || !o) return false;
   const std::string n(name);
-  if (n == "tiny") {
+  if (n == "tiny" || n == "tiny_ddim") {
     *o = vla_config{VLA_F32, 1, 128, 128, 16, 256, 4, 1024, 2, 256, 4, 1, 64, 1024, 2,
-                    1024, 16, 0, 128, 512, 2, 8, 7, 4, VLA_HEAD_PI0, 1, 0};
+                    1024, 16, 0, 128, 512, 2, 8, 7, 4, VLA_HEAD_PI0, 1, 0, VLA_SAMPLER_EULER};
+    if (n == "tiny_ddim") o->sampler = VLA_SAMPLER_DDIM;
     return true;
   }
   if (n == "tiny_dit") {
@@ -143,13 +146,14 @@ static bool preset(const char* name, vla_config* o) {
                     1024, 32, 0, 1536, 6144, 16, 16, 32, 4, VLA_HEAD_DIT, 2, 32};
     return true;
   }
-  if (n == "pi0" || n == "pi0_3view") {
+  if (n == "pi0" || n == "pi0_3view" || n == "pi0_ddim") {
     *o = vla_config{VLA_BF16, 1, 224, 224, 14, 1152, 16, 4304, 27, 2048, 8, 1, 256, 16384, 18,
-                    1024, 48, 32, 1024, 4096, 18, 50, 32, 10, VLA_HEAD_PI0, 1, 0};
+                    1024, 48, 32, 1024, 4096, 18, 50, 32, 10, VLA_HEAD_PI0, 1, 0, VLA_SAMPLER_EULER};
     if (n == "pi0_3view") {
       o->n_views = 3;
       o->n_text = 64;
     }
+    if (n == "pi0_ddim") o->sampler = VLA_SAMPLER_DDIM;
     return true;
   }
   return false;
@@ -297,6 +301,9 @@ struct vla_model {
   float* rope_sin = nullptr;
   void* phi = nullptr;  // [n_steps][ex_dim] operand type, row-block operand layout
   float* ck = nullptr;  // [n_steps][ex_dim]: W_2 phi(t_k) + b_2
+  // per step k: x <- step_a[k] x + step_b[k] v (Euler: 1 and -1/N; DDIM:
+  // a_k and b_k of the header), and the head's time input t_k
+  std::vector<float> step_a, step_b, step_t;
   // DiT head: adaLN vectors per step, [n_steps][ex_layers][6][ex_dim]
   // (shift1, scale1, gate1, shift2, scale2, gate2), final [n_steps][2][ex_dim]
   // (shift, scale), token positions [chunk_len][ex_dim]
@@ -1020,7 +1027,6 @@ static int run_denoise_dit(const Run& r, const vla_ctx* ctx, const float* noise,
   const Dims& d = m->d;
   ActWs& w = *r.aw;
   const int H = c.chunk_len, de = c.ex_dim, A = c.action_dim, L = c.ex_layers;
-  const float dt = -1.0f / (float)c.n_steps;
   const size_t xe = cross_elems(m) * m->esz;
   HIP_TRY(launch_cvt_pad(m->dt, noise, H, A, w.xop, d.a_pad, true, x, r.st));
   auto adanorm = [&](int pend, const float* gate, const float* shift, const float* scale) {
@@ -1103,7 +1109,8 @@ static int run_denoise_dit(const Run& r, const vla_ctx* ctx, const float* noise,
     e.ldx = A;
     e.xop = w.xop;
     e.ldxop = d.a_pad;
-    e.dt = dt;
+    e.dt = m->step_b[k];
+    e.xs = m->step_a[k];
     VLA_TRY(gemm(r, "ex.out", w.h, de, m->out_w, H, A, de, e));
   }
   return VLA_OK;
@@ -1166,7 +1173,6 @@ static int run_denoise_n(const Run& r, const vla_ctx* const* ctxs, int frames, c
   const Dims& d = m->d;
   ActWs& w = *r.aw;
   const int H = c.chunk_len, de = c.ex_dim, A = c.action_dim;
-  const float dt = -1.0f / (float)c.n_steps;
   const bool fb = frames > 1;
   const int blk = fb ? H : 0;
   auto frm = [&](size_t a_blk) { Frames f; f.n = frames; f.a_blk = fb ? a_blk : 0; return f; };
@@ -1210,7 +1216,8 @@ static int run_denoise_n(const Run& r, const vla_ctx* const* ctxs, int frames, c
     e.ldx = A;
     e.xop = w.xop;
     e.ldxop = d.a_pad;
-    e.dt = dt;
+    e.dt = m->step_b[k];
+    e.xs = m->step_a[k];
     e.blk_rows = blk;
     e.blk_xop = w.blk_xop;
     VLA_TRY(gemm(r, "ex.out", w.h, de, m->out_w, H, A, de, e, 0, frm(w.blk_de)));
@@ -1278,13 +1285,41 @@ static int setup_tables(vla_model* m) {
   VLA_TRY(dmalloc(m, (void**)&m->rope_sin, sn.size() * 4));
   HIP_TRY(hipMemcpy(m->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice));
   HIP_TRY(hipMemcpy(m->rope_sin, sn.data(), sn.size() * 4, hipMemcpyHostToDevice));
-  // sinusoid phi(t_k): periods log-spaced on [4e-3, 4]; t_k = (N - k) / N in
-  // fp32; the DiT's timestep embedder takes a 256-wide phi
+  // sampler steps: Euler t_k = (N - k) / N in fp32, x += (-1/N) v; DDIM
+  // (deterministic) over abar_s = prod_{i <= s} (1 - beta_i), beta linear on
+  // [1e-4, 0.02] over 1000 training steps, timesteps s_k = floor((N - k)
+  // 1000 / N) - 1, t_k = s_k / 1000, and x <- a_k x + b_k eps with
+  // a_k = sqrt(abar_{k+1} / abar_k), b_k = sqrt(1 - abar_{k+1}) -
+  // a_k sqrt(1 - abar_k) (abar after the last step = 1); coefficients in fp64
+  m->step_a.assign(c.n_steps, 1.0f);
+  m->step_b.assign(c.n_steps, -1.0f / (float)c.n_steps);
+  m->step_t.resize(c.n_steps);
+  if (c.sampler == VLA_SAMPLER_DDIM) {
+    constexpr int TRAIN = 1000;
+    std::vector<double> abar(TRAIN);
+    double p = 1.0;
+    for (int i = 0; i < TRAIN; ++i) {
+      p *= 1.0 - (1e-4 + (0.02 - 1e-4) * i / (TRAIN - 1));
+      abar[i] = p;
+    }
+    auto step_s = [&](int k) { return (c.n_steps - k) * TRAIN / c.n_steps - 1; };
+    for (int k = 0; k < c.n_steps; ++k) {
+      const double a0 = abar[step_s(k)], a1 = k + 1 < c.n_steps ? abar[step_s(k + 1)] : 1.0;
+      const double a = std::sqrt(a1 / a0);
+      m->step_a[k] = (float)a;
+      m->step_b[k] = (float)(std::sqrt(1.0 - a1) - a * std::sqrt(1.0 - a0));
+      m->step_t[k] = (float)step_s(k) / (float)TRAIN;
+    }
+  } else {
+    for (int k = 0; k < c.n_steps; ++k) m->step_t[k] = (float)(c.n_steps - k) / (float)c.n_steps;
+  }
+  // sinusoid phi(t_k): periods log-spaced on [4e-3, 4]; the DiT's timestep
+  // embedder takes a 256-wide phi
   const bool dit = c.head == VLA_HEAD_DIT;
   const int de = dit ? DIT_TIME_DIM : c.ex_dim, dh = de / 2;
   std::vector<float> phi((size_t)c.n_steps * de);
   for (int k = 0; k < c.n_steps; ++k) {
-    const float t = (float)(c.n_steps - k) / (float)c.n_steps;
+    const float t = m->step_t[k];
     for (int i = 0; i < dh; ++i) {
       const double frac = dh > 1 ? (double)i / (dh - 1) : 0.0;
       const double period = 4e-3 * std::pow(4.0 / 4e-3, frac);

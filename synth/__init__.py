@@ -172,16 +172,19 @@ CONFIG_FIELDS = (
     "lm_dim", "lm_heads", "lm_kv_heads", "head_dim", "lm_mlp", "lm_layers",
     "vocab", "n_text", "state_dim",
     "ex_dim", "ex_mlp", "ex_layers", "chunk_len", "action_dim", "n_steps",
-    "head", "shuffle", "ex_heads",
+    "head", "shuffle", "ex_heads", "sampler",
 )
 
 #: Action-head families: the pi0-style expert that shares the LM's KV cache,
 #: and the GR00T-style DiT that cross-attends to the LM's final features.
 HEAD_PI0, HEAD_DIT = 0, 1
+#: Samplers: flow-matching Euler steps, or deterministic DDIM steps with the
+#: head's output read as the noise estimate.
+SAMPLER_EULER, SAMPLER_DDIM = 0, 1
 
 
 def _cfg(**kw) -> Dict[str, int]:
-    kw = dict(dict(head=HEAD_PI0, shuffle=1, ex_heads=0), **kw)
+    kw = dict(dict(head=HEAD_PI0, shuffle=1, ex_heads=0, sampler=SAMPLER_EULER), **kw)
     missing = [f for f in CONFIG_FIELDS if f not in kw]
     assert not missing, missing
     return {f: int(kw[f]) for f in CONFIG_FIELDS}
@@ -246,7 +249,13 @@ TINY_DIT = _cfg(dtype=F32, n_views=1, img_h=128, img_w=128, patch=16,
                 ex_dim=192, ex_mlp=768, ex_layers=4, chunk_len=8, action_dim=7, n_steps=4,
                 head=HEAD_DIT, shuffle=2, ex_heads=4)
 
-PRESETS = {"tiny": TINY, "pi0": PI0, "pi0_3view": PI0_3VIEW, "gr00t": GR00T, "tiny_dit": TINY_DIT}
+#: The pi0-shaped model sampled with DDIM steps instead of Euler steps (a
+#: diffusion head of the same shapes).
+TINY_DDIM = dict(TINY, sampler=SAMPLER_DDIM)
+PI0_DDIM = dict(PI0, sampler=SAMPLER_DDIM)
+
+PRESETS = {"tiny": TINY, "pi0": PI0, "pi0_3view": PI0_3VIEW, "gr00t": GR00T, "tiny_dit": TINY_DIT,
+           "tiny_ddim": TINY_DDIM, "pi0_ddim": PI0_DDIM}
 
 
 def derived(cfg: Dict[str, int]) -> Dict[str, int]:

@@ -566,3 +566,36 @@ def test_dit_phase1_hand_off():
         assert out[l][0].shape == (d["prefix"], cfg["ex_heads"], cfg["ex_dim"] // cfg["ex_heads"])
     # the last LM layer now runs in full: the features differ from its input
     assert len(cap["kv"]) == cfg["lm_layers"]
+
+
+def test_ddim_schedule_and_exact_recovery():
+    """DDIM pins: the DDPM linear-beta abar (first value 1 - 1e-4, decreasing,
+    abar_999 ~ 4.04e-5), the N = 10 timesteps 999, 899, ..., 99 and times
+    s / 1000; and the defining property of deterministic DDIM: if the head
+    returns the true noise eps of x_k = sqrt(abar_k) x0 + sqrt(1 - abar_k) eps,
+    each step lands exactly on the next marginal, so N steps return x0."""
+    ab = O.ddim_alpha_bar()
+    assert ab[0] == 1 - 1e-4 and np.all(np.diff(ab) < 0)
+    assert 4.0e-5 < ab[-1] < 4.1e-5
+    ts, s, abar = O.ddim_schedule(10)
+    assert s == [999 - 100 * k for k in range(10)]
+    assert ts[0] == float(np.float32(0.999)) and ts[-1] == float(np.float32(0.099))
+    assert abar[-1] == 1.0 and abar[0] == ab[999]
+    rng = np.random.default_rng(3)
+    x0, eps = rng.standard_normal((5, 3)), rng.standard_normal((5, 3))
+    for n in (1, 4, 10):
+        _, _, abar = O.ddim_schedule(n)
+        xT = np.sqrt(abar[0]) * x0 + np.sqrt(1 - abar[0]) * eps
+        got = O.ddim_integrate(xT, lambda x, t: eps, n)
+        assert np.allclose(got, x0, rtol=0, atol=1e-9), n
+    # one step from k = 0 lands on the k = 1 marginal
+    _, _, abar = O.ddim_schedule(4)
+    x1 = O.ddim_integrate(np.sqrt(abar[0]) * x0 + np.sqrt(1 - abar[0]) * eps, lambda x, t: eps, 1)
+    # (a one-step run has abar_1 = 1: it returns x0; the four-step schedule's
+    # second marginal follows from its own first step)
+    assert np.allclose(x1, x0, atol=1e-9)
+    seen = []
+    O.ddim_integrate(np.sqrt(abar[0]) * x0 + np.sqrt(1 - abar[0]) * eps,
+                     lambda x, t: (seen.append(x.copy()), eps)[1], 4)
+    for k in range(4):
+        assert np.allclose(seen[k], np.sqrt(abar[k]) * x0 + np.sqrt(1 - abar[k]) * eps, atol=1e-9), k
