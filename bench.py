@@ -214,7 +214,7 @@ def main():
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this build runs on one GPU only; the R robot streams of a "
                                    "multi-GPU deployment shard across GPUs with no exchange step "
-                                   "(see DESIGN.md); run with --gpus 1"}), flush=True)
+                                   "; run with --gpus 1"}), flush=True)
         sys.exit(2)
 
     import numpy as np

@@ -1,7 +1,7 @@
 """Offline profiling pass: intensity descriptors of every kernel of a preset.
 
     python paper_2609_22335_amd/profile_intensity.py --preset pi0 \
-        --out profiles/intensity_pi0.json --work gpurun_out/intensity_pi0
+        --out profiles/intensity_pi0.json --work intensity_work/pi0
 
 Runs on a machine with the GPU and rocprofv3. Each phase of one frame runs
 on its own (the VLM prefill of frames, or the action loop of one frame over a
