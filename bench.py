@@ -212,9 +212,9 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; the R robot streams of a "
-                                   "multi-GPU deployment shard across GPUs with no exchange step "
-                                   "; run with --gpus 1"}), flush=True)
+        print(json.dumps({"error": "bench.py measures one GPU; the R robot streams of a "
+                                   "multi-GPU deployment shard across GPUs with no exchange step; "
+                                   "run with --gpus 1"}), flush=True)
         sys.exit(2)
 
     import numpy as np
