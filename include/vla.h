@@ -40,7 +40,7 @@ extern "C" {
 #define VLA_EINVAL (-1)       /* invalid argument or configuration            */
 #define VLA_ENOMEM (-2)       /* device or host allocation failed             */
 #define VLA_EHIP (-3)         /* a HIP runtime call failed (message has it)   */
-#define VLA_EUNSUPPORTED (-4) /* valid request this build does not implement  */
+#define VLA_EUNSUPPORTED (-4) /* valid request the library does not implement */
 #define VLA_ESTATE (-5)       /* object in the wrong state (e.g. mismatched)  */
 
 /* ---- number types ---- */

@@ -13,7 +13,7 @@ representation; for the pi-family models this hand-off is the LM's per-layer
 KV cache. Phase 2, a flow-matching action head, integrates a velocity field
 over a few Euler steps to produce an action chunk, every step attending to
 that cache. The paper gives no layer equations, so the layer definitions
-below are the readings fixed for this build (SigLIP-style ViT, Gemma-style
+below are the readings this oracle fixes (SigLIP-style ViT, Gemma-style
 prefix LM with multi-query attention, pi0-style action expert); each function
 names the reading it follows.
 
