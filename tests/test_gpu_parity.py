@@ -421,8 +421,9 @@ def test_dit_phases_vs_oracle(V, name, cfg):
     assert err <= CHUNK_TOL[cfg["dtype"]] * sampler_gain(cfg)
 
 
-@pytest.mark.parametrize("cfg", [synth.micro(synth.BF16), synth.TINY, synth.micro_dit(synth.BF16)],
-                         ids=["micro-bf16", "tiny", "micro-dit-bf16"])
+@pytest.mark.parametrize("cfg", [synth.micro(synth.BF16), synth.TINY, synth.micro_dit(synth.BF16),
+                                 dict(synth.micro(synth.BF16), sampler=synth.SAMPLER_DDIM)],
+                         ids=["micro-bf16", "tiny", "micro-dit-bf16", "micro-ddim-bf16"])
 def test_pipeline_modes_bit_identical(V, cfg):
     """Every schedule (one stream, two streams, CU masks, workgroup caps,
     several action streams, graph replay) gives the same bits as standalone
