@@ -599,3 +599,97 @@ def test_ddim_schedule_and_exact_recovery():
                      lambda x, t: (seen.append(x.copy()), eps)[1], 4)
     for k in range(4):
         assert np.allclose(seen[k], np.sqrt(abar[k]) * x0 + np.sqrt(1 - abar[k]) * eps, atol=1e-9), k
+
+
+# ------------------------------------------- phase-1 hand-off of the DiT head
+
+def test_lm_features_vs_gemma_stack():
+    """The DiT's features: every LM layer runs in full (the last one's
+    attention output and MLP included), then the final RMSNorm; assembled
+    from transformers Gemma decoder layers (multi-head, 3 layers) and torch's
+    RMSNorm, with every layer's K / V read back from the cache."""
+    from transformers.cache_utils import DynamicCache
+    cfg = dict(synth.micro_dit(), lm_layers=3)
+    P = synth.make_params(cfg, 0)
+    n, dl = 11, cfg["lm_dim"]
+    x0 = rnd(n, dl)
+    got, cache_o = O.lm_features(P, cfg, x0)
+    pos = np.arange(n)
+    with torch.no_grad():
+        h = t64(x0)[None]
+        cache = DynamicCache()
+        for l in range(cfg["lm_layers"]):
+            m = _gemma_layer(cfg, P, "lm", l, dl, cfg["lm_mlp"])
+            h = m(h, attention_mask=None, position_ids=torch.arange(n)[None], past_key_values=cache,
+                  use_cache=True, position_embeddings=_rope_tables(cfg["head_dim"], pos))
+            h = h[0] if isinstance(h, tuple) else h
+        ref = F.rms_norm(h[0], (dl,), t64(P["lm.final.g"]), eps=1e-6).numpy()
+    # Gemma's RMSNorm runs in fp32, hence the tolerance
+    assert np.allclose(got, ref, rtol=5e-5, atol=5e-5)
+    assert len(cache_o) == cfg["lm_layers"]
+    for l in range(cfg["lm_layers"]):
+        assert np.allclose(cache_o[l][0], cache.layers[l].keys[0].transpose(0, 1).numpy(), rtol=5e-5, atol=5e-5)
+        assert np.allclose(cache_o[l][1], cache.layers[l].values[0].transpose(0, 1).numpy(), rtol=5e-5, atol=5e-5)
+
+
+def _dit_cross_torch(P, cfg, feats):
+    """Cross K / V of the even DiT layers from the features with F.linear."""
+    nh, hd = cfg["ex_heads"], cfg["ex_dim"] // cfg["ex_heads"]
+    out = {}
+    for l in range(0, cfg["ex_layers"], 2):
+        k = F.linear(t64(feats), t64(P[f"ex.{l}.k.w"])).reshape(-1, nh, hd)
+        v = F.linear(t64(feats), t64(P[f"ex.{l}.v.w"])).reshape(-1, nh, hd)
+        out[l] = (k.numpy(), v.numpy())
+    return out
+
+
+def test_dit_cross_kv_vs_linear_and_velocity_from_features():
+    """dit_cross_kv on distinct feature rows: K and V of every even layer
+    against F.linear, and the DiT velocity fed with them against the torch
+    assembly fed with K / V computed by torch from the same features (so a
+    K projection that differs in any way changes the attention weights)."""
+    cfg = dict(synth.micro_dit(), ex_layers=4)  # cross, self, cross, self
+    P = synth.make_params(cfg, 0)
+    feats = rnd(9, cfg["lm_dim"])
+    got = O.dit_cross_kv(P, cfg, feats)
+    want = _dit_cross_torch(P, cfg, feats)
+    assert sorted(got) == [0, 2]
+    for l in (0, 2):
+        assert np.allclose(got[l][0], want[l][0], rtol=1e-12, atol=1e-12)
+        assert np.allclose(got[l][1], want[l][1], rtol=1e-12, atol=1e-12)
+    x, t = rnd(cfg["chunk_len"], cfg["action_dim"]), 0.75
+    v_got = O.dit_velocity(P, cfg, got, x, t)
+    with torch.no_grad():
+        v_ref = _dit_torch(P, cfg, want, x, t)
+    assert np.allclose(v_got, v_ref, rtol=1e-10, atol=1e-10)
+    # the attention weights depend on K: a swapped projection moves the result
+    swapped = {l: (want[l][1], want[l][0]) for l in want}
+    with torch.no_grad():
+        assert not np.allclose(_dit_torch(P, cfg, swapped, x, t), v_got, rtol=1e-6, atol=1e-6)
+
+
+def test_image_tokens_with_pixel_shuffle_vs_torch_assembly():
+    """Shuffled image tokens (the GR00T-shaped ViT): SigLIP layers, then the
+    final LayerNorm on every fine token, then torch's space-to-depth
+    (pixel_unshuffle, channels reordered to (dy, dx, c)), then the projector."""
+    cfg = dict(synth.micro_dit(), vit_layers=2)
+    P = synth.make_params(cfg, 0)
+    fr = synth.make_frame(cfg, 0, 0)
+    got = O.image_tokens(P, cfg, fr["pixels"])
+    p, dv, s = cfg["patch"], cfg["vit_dim"], cfg["shuffle"]
+    gh, gw = cfg["img_h"] // p, cfg["img_w"] // p
+    with torch.no_grad():
+        img = t64(fr["pixels"][0])
+        patches = img.permute(2, 0, 1).unfold(1, p, p).unfold(2, p, p)
+        patches = patches.permute(1, 2, 3, 4, 0).reshape(gh * gw, p * p * 3)
+        x = F.linear(patches, t64(P["vit.patch.w"]), t64(P["vit.patch.b"])) + t64(P["vit.pos"])
+        for l in range(cfg["vit_layers"]):
+            y = _siglip_layer(cfg, P, l)(x[None], None)
+            x = (y[0] if isinstance(y, tuple) else y)[0]
+        x = F.layer_norm(x, (dv,), t64(P["vit.post.g"]), t64(P["vit.post.b"]), eps=1e-6)
+        g = F.pixel_unshuffle(x.T.reshape(1, dv, gh, gw), s)[0]  # [dv s s, gh/s, gw/s], channels (c, dy, dx)
+        g = g.reshape(dv, s * s, gh // s, gw // s).permute(2, 3, 1, 0).reshape(-1, s * s * dv)
+        ref = F.linear(g, t64(P["proj.w"]), t64(P["proj.b"])).numpy()
+    assert got.shape == ((gh // s) * (gw // s), cfg["lm_dim"])
+    # transformers computes the ViT softmax in fp32, hence 1e-7
+    assert np.allclose(got, ref, rtol=1e-7, atol=1e-7)
