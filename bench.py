@@ -6,21 +6,29 @@ a 224x224 image; 18-layer LM, d=2048, 8 query heads / 1 KV head of 256,
 GeGLU 16384, prefix 256 image + 48 text + 1 state token) with a pi0-shaped
 flow-matching expert (18 layers, d=1024, GeGLU 4096, chunk 50x32, 10 Euler
 steps), bf16, R=8 independent robot request streams (a new seeded frame per
-stream). One step = vla_pipeline_run over the R frames: the VLM prefill of
-frame r+1 overlaps the action denoising of frame r. Inputs are resident in
-HBM before the timed region.
+stream). One step = vla_pipeline_run over the R frames. Inputs are resident
+in HBM before the timed region.
 
-Further workloads of the same pipeline (``--extra``; by default the
-GR00T-shaped VLA with its DiT action head at R=8, and the three-view stress
-shape at R=32 with its sweep of CU splits 224/32, 192/64, 160/96 and VLM
-workgroup caps of 1 and 2 per CU) are measured the same way and reported
-under ``other_workloads``; the headline stays the one above.
+Schedules (``--modes``): the paper's serialized and naive two-stream ones,
+CU masks, VLM workgroup caps, HIP graphs, several action lanes, and batched
+prefills / action loops (several robots' frames through one pass). In a
+schedule whose prefills come in two or more groups (one-frame prefills, or
+groups smaller than R) a later group's prefill runs while an earlier
+group's action loop runs on another stream; with one prefill group of all R
+frames the action loops start after it.
 
-Prints one JSON line: frames/s of the fastest schedule as `value` (named in
-config.schedule),
-actions/s, every schedule's throughput and its speedup over the serialized
-one, the dominant kernel's roofline fraction (timed live with HIP events on
-its own stream) and the fp64 CPU oracle timed on this host as a baseline.
+`value` is the frames/s of the schedule named by ``--mode`` (fixed in
+advance, not the fastest measured one); the line also gives its speedup over
+the one-frame serialized schedule and over the serialized schedule with the
+same batching, and `best_overlapped`: the fastest schedule in which the two
+phases overlap, with the per-CU residency of both phases measured from the
+kernels' workgroup logs.
+
+Output: the last stdout line is a compact JSON headline (a few KB): metric,
+value, roofline of the dominant kernel (timed live with HIP events on its own
+stream), the fp64 CPU oracle timed on this host as a baseline. Every
+schedule's numbers, the residency logs and the further workloads
+(``--extra``) go to ``--detail`` (a JSON file) and to stderr.
 """
 from __future__ import annotations
 
@@ -132,7 +140,8 @@ def cpu_baseline(cfg, seed):
     del P
     return {"value": 1.0 / dt, "unit": "frames/s", "cores": int(threads), "kind": "oracle",
             "sample": f"frame 0 of the workload: full VLM prefill + {cfg['n_steps']}-step action "
-                      f"denoising, fp64 NumPy, {dt:.1f} s", "seconds": dt}, chunk
+                      f"denoising, fp64 NumPy, {dt:.1f} s", "seconds": dt, "blas_threads": int(threads),
+            "os_cpu_count": os.cpu_count()}, chunk
 
 
 def measured_traffic(preset, R, kernel, schedule):
@@ -166,14 +175,17 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--R", type=int, default=8, help="robot request streams (frames per step)")
-    ap.add_argument("--mode", default="auto",
+    ap.add_argument("--mode", default="vb8_ab4_lanes2_graph",
                     help="schedule reported as `value` (auto: the fastest measured one)")
     ap.add_argument("--modes", default="serial,concurrent,cu_masked,wg_capped,serial_graph,"
                                        "concurrent_graph,lanes2_graph,lanes3_graph,batch2_graph,"
                                        "batch2_lanes2_graph,batch4_graph,batch4_lanes2_graph,batch8_graph,"
                                        "vb2_ab2_graph,vb2_ab2_lanes2_graph,vb2_ab4_graph,vb4_ab4_graph,"
                                        "vb4_ab2_lanes2_graph,vb4_ab4_lanes2_graph,vb8_ab8_graph,"
-                                       "vb8_ab4_lanes2_graph,vb4_ab4_v2_lanes2_graph")
+                                       "vb8_ab4_lanes2_graph,vb4_ab4_v2_lanes2_graph,"
+                                       "serial_vb8_ab4_graph,serial_vb4_ab4_graph")
+    ap.add_argument("--detail", default=os.path.join(ROOT, "gpurun_out", "bench_detail.json"),
+                    help="JSON file for every schedule's numbers, residency logs and further workloads")
     ap.add_argument("--split", default="192,64", help="CU split VLM,action for cu_masked")
     ap.add_argument("--wg-cap", type=int, default=2, help="VLM workgroups per CU for wg_capped")
     ap.add_argument("--kernel", default="auto",
@@ -280,6 +292,11 @@ def main():
         kw[f"cu_{a_}_{b_}_lanes3"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_, act_streams=3, graphs=True)
     for c_ in (1, 2, 4):
         kw[f"wg_cap{c_}"] = dict(mode="wg_capped", vlm_wg_cap=c_)
+    # serialized with batching: one stream, groups as in the batched schedules
+    # (the same outputs bit for bit), the baseline of their concurrency gain
+    for v_ in (1, 2, 4, 8):
+        for a_ in (1, 2, 4, 8):
+            kw[f"serial_vb{v_}_ab{a_}_graph"] = dict(mode="serial", vlm_batch=v_, act_batch=a_, graphs=True)
 
     def measure(preset, R, modes, steps, warmup):
         """vla_pipeline_run over R seeded frames of `preset` in each schedule."""
@@ -355,19 +372,43 @@ def main():
     if args.mode == "auto":
         args.mode = max(results, key=lambda k: results[k]["frames_per_s"])
 
-    # per-CU residency (workgroup start/end log), serialized vs the reported
-    # schedule, one logged pipeline run each (not part of the timed steps)
+    def n_prefill_groups(name):
+        return -(-R // max(1, kw[name].get("vlm_batch", 1)))
+
+    def overlaps(name):
+        """Both phases can run at once: two streams, and a later prefill group
+        exists to run beside an earlier group's action loop."""
+        return kw[name].get("mode") != "serial" and n_prefill_groups(name) >= 2
+
+    def same_batching_serial(name):
+        a = kw[name]
+        if a.get("mode") == "serial":
+            return name if a.get("vlm_batch", 1) > 1 or a.get("act_batch", 1) > 1 else "serial"
+        v_, b_ = max(1, a.get("vlm_batch", 1)), max(1, a.get("act_batch", 1))
+        if v_ == 1 and b_ == 1:
+            return "serial"
+        return f"serial_vb{v_}_ab{b_}_graph"
+
+    cands = [k for k in results if overlaps(k) and kw[k].get("act_chunks", 1) == 1]
+    best_ovl = max(cands, key=lambda k: results[k]["frames_per_s"]) if cands else None
+
+    # per-CU residency (workgroup start/end log): one logged pipeline run per
+    # schedule (not part of the timed steps), the serialized one first
     residency = {}
     if args.residency:
         print("[bench] residency logs", file=sys.stderr, flush=True)
         V.vla_wavelog_enable(m, args.residency)
-        for name in dict.fromkeys(["serial", args.mode]):
+        logged = ["serial", "concurrent", "cu_masked", "wg_capped", "lanes2_graph", best_ovl, args.mode]
+        for name in dict.fromkeys(x for x in logged if x and x in kw):
             V.vla_wavelog_read(m, 0)
             V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **kw[name])
             rec, n = V.vla_wavelog_read(m, args.residency)
             full = cu_residency(rec, window=(int(rec["t"].min()), int(rec["t"].max())))
             ovl = cu_residency(rec)
             residency[name] = {"whole_run": full, "overlap_window": ovl, "records": int(n)}
+            print(f"[bench] residency {name}: busy {full['busy_frac']:.3f} whole run; overlap window "
+                  f"{ovl['window_ms']:.2f} ms, busy {ovl['busy_frac']:.3f}, both phases "
+                  f"{ovl['both_phases_frac']:.3f}", file=sys.stderr, flush=True)
         V.vla_wavelog_enable(m, 0)
 
     # dominant kernel of the reported schedule, timed live with HIP events
@@ -401,9 +442,9 @@ def main():
     roofline = {"bound": "hbm" if hbm_bound else "mfma", "achieved": ach, "peak": peak, "unit": unit,
                 "frac": ach / peak, "traffic": measured_traffic(args.preset, R, kernel, args.mode),
                 "kernel": kernel, "schedule": args.mode, "avg_us": avg_s * 1e6, "launches": launches,
-                "algorithmic_bytes": byts, "flops": flops,
-                "gpu_ms_per_step_by_tag": {k: v[0] / args.steps for k, v in timed.items()},
-                "stream_ms_per_step_by_tag": {k: v[0] / args.steps / lanes_of(k) for k, v in timed.items()}}
+                "algorithmic_bytes": byts, "flops": flops}
+    roofline_detail = dict(roofline, gpu_ms_per_step_by_tag={k: v[0] / args.steps for k, v in timed.items()},
+                           stream_ms_per_step_by_tag={k: v[0] / args.steps / lanes_of(k) for k, v in timed.items()})
     outs = outputs[args.mode]
     V.vla_destroy(m)
     del cframes, noise, actions
@@ -429,33 +470,82 @@ def main():
             "chunk": [ocfg["chunk_len"], ocfg["action_dim"]], "euler_steps": ocfg["n_steps"],
             "prefix_tokens": synth.derived(ocfg)["prefix"], "steps": args.extra_steps,
             "outputs_identical_across_modes": oid, "modes": ores}
+        print(f"[bench] {name}: best {best} {ores[best]['frames_per_s']:.1f} frames/s "
+              f"({ores[best]['speedup_vs_serialized'] or 0:.2f}x serialized)", file=sys.stderr, flush=True)
 
     main_r = results[args.mode]
-    line = {
-        "metric": METRIC, "value": main_r["frames_per_s"], "unit": "frames/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": main_r["ms_per_step"],
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
-        "data": "synthetic",
-        "config": {"workload": f"{args.preset}-shaped VLA (PaliGemma-3B-shaped VLM + pi0-shaped "
-                               f"expert), R={R} robot request streams, schedule {args.mode}",
-                   "schedule": args.mode, "schedule_args": {k: v for k, v in kw[args.mode].items()},
-                   "R": R, "global_batch": R, "chunk": [cfg["chunk_len"], cfg["action_dim"]],
-                   "euler_steps": cfg["n_steps"], "prefix_tokens": synth.derived(cfg)["prefix"],
-                   "parallelism": "1 GPU, 2 streams"},
-        "actions_per_s": main_r["actions_per_s"],
-        "speedup_vs_serialized": main_r["speedup_vs_serialized"],
-        "modes": results, "outputs_identical_across_modes": identical,
-        "roofline": roofline,
-    }
-    if residency:
-        line["cu_residency"] = residency
-    if others:
-        line["other_workloads"] = others
+    ser_same = same_batching_serial(args.mode)
+    sp_same = (main_r["frames_per_s"] / results[ser_same]["frames_per_s"]) if ser_same in results else None
+    a_ = kw[args.mode]
+    streams = 1 if a_.get("mode") == "serial" else max(1, a_.get("vlm_streams", 1)) + max(1, a_.get("act_streams", 1))
+    cpu = None
     if not args.no_cpu_baseline:
         cb, chunk = cpu_baseline(cfg, seed)
         cb["max_abs_err_gpu_vs_oracle_frame0"] = float(np.abs(outs[0].astype(np.float64) - chunk).max())
-        line["cpu_baseline"] = cb
-    print(json.dumps(line), flush=True)
+        cpu = cb
+
+    def short_res(name):
+        r_ = residency.get(name)
+        if not r_:
+            return None
+        return {"busy_whole_run": round(r_["whole_run"]["busy_frac"], 4),
+                "overlap_window_ms": round(r_["overlap_window"]["window_ms"], 3),
+                "busy_in_overlap": round(r_["overlap_window"]["busy_frac"], 4),
+                "both_phases_in_overlap": round(r_["overlap_window"]["both_phases_frac"], 4)}
+
+    def rnd(x, n=4):
+        return None if x is None else round(float(x), n)
+
+    headline = {
+        "metric": METRIC, "value": rnd(main_r["frames_per_s"], 3), "unit": "frames/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": rnd(main_r["ms_per_step"], 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded frames and weights of the stated shapes)",
+        "config": {"workload": f"{args.preset}-shaped VLA (PaliGemma-3B-shaped VLM + pi0-shaped expert, "
+                               f"chunk {cfg['chunk_len']}x{cfg['action_dim']}, {cfg['n_steps']} Euler steps), "
+                               f"R={R} robot request streams",
+                   "schedule": args.mode, "R": R, "global_batch": R,
+                   "parallelism": f"1 GPU, {streams} HIP stream{'s' if streams > 1 else ''}"},
+        "actions_per_s": rnd(main_r["actions_per_s"], 1),
+        "speedup_vs_serialized": rnd(main_r["speedup_vs_serialized"]),
+        "serialized_frames_per_s": rnd(results.get("serial", {}).get("frames_per_s"), 3),
+        "speedup_vs_serialized_same_batching": rnd(sp_same),
+        "serialized_same_batching": ser_same if ser_same in results else None,
+        "best_overlapped": None if best_ovl is None else {
+            "schedule": best_ovl, "frames_per_s": rnd(results[best_ovl]["frames_per_s"], 3),
+            "speedup_vs_serialized": rnd(results[best_ovl]["speedup_vs_serialized"]),
+            "speedup_vs_serialized_same_batching": rnd(
+                results[best_ovl]["frames_per_s"] / results[same_batching_serial(best_ovl)]["frames_per_s"]
+                if same_batching_serial(best_ovl) in results else None),
+            "residency": short_res(best_ovl)},
+        "naive_concurrent": None if "concurrent" not in results else {
+            "frames_per_s": rnd(results["concurrent"]["frames_per_s"], 3),
+            "speedup_vs_serialized": rnd(results["concurrent"]["speedup_vs_serialized"]),
+            "residency": short_res("concurrent")},
+        "serialized_residency": short_res("serial"),
+        "outputs_identical_across_modes": identical,
+        "roofline": {k: (rnd(v, 5) if isinstance(v, float) else v) for k, v in roofline.items()},
+        "mfma_util_dominant_kernel": rnd(roofline["frac"]) if roofline["bound"] == "mfma" else None,
+        "cpu_baseline": None if cpu is None else {
+            "value": rnd(cpu["value"], 6), "unit": cpu["unit"], "cores": cpu["cores"], "kind": "oracle",
+            "sample": cpu["sample"], "seconds": rnd(cpu["seconds"], 2), "blas_threads": cpu["blas_threads"],
+            "os_cpu_count": cpu["os_cpu_count"],
+            "max_abs_err_gpu_vs_oracle_frame0": rnd(cpu["max_abs_err_gpu_vs_oracle_frame0"], 6)},
+        "detail_file": os.path.relpath(args.detail, ROOT),
+    }
+    detail = {"headline": headline, "modes": results, "schedule_args": {k: kw[k] for k in results},
+              "roofline": roofline_detail, "cu_residency": residency, "other_workloads": others,
+              "cpu_baseline": cpu}
+    try:
+        os.makedirs(os.path.dirname(os.path.abspath(args.detail)), exist_ok=True)
+        with open(args.detail, "w") as f:
+            json.dump(detail, f, indent=1)
+    except OSError as e:
+        print(f"[bench] could not write {args.detail}: {e}", file=sys.stderr, flush=True)
+    for name, r_ in results.items():
+        print(f"[bench] {name}: {r_['frames_per_s']:.2f} frames/s, {r_['speedup_vs_serialized'] or 0:.3f}x "
+              f"serialized", file=sys.stderr, flush=True)
+    print(json.dumps(headline), flush=True)
 
 
 if __name__ == "__main__":

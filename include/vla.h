@@ -41,7 +41,8 @@ extern "C" {
 #define VLA_ENOMEM (-2)       /* device or host allocation failed             */
 #define VLA_EHIP (-3)         /* a HIP runtime call failed (message has it)   */
 #define VLA_EUNSUPPORTED (-4) /* valid request the library does not implement */
-#define VLA_ESTATE (-5)       /* object in the wrong state (e.g. mismatched)  */
+#define VLA_ESTATE (-5)       /* object in the wrong state (e.g. mismatched), */
+                              /* or an internal error of the library          */
 
 /* ---- number types ---- */
 #define VLA_F32 0  /* every tensor and operand fp32                           */
@@ -122,8 +123,11 @@ typedef struct vla_sched {
                       /*   (different robots) run as one denoising loop that reads   */
                       /*   the weights once for all of them; it starts when their    */
                       /*   prefills are done. A final group of fewer than k frames   */
-                      /*   runs with as many as remain. Every frame's chunk is bit   */
-                      /*   identical to its own run. VLA_HEAD_PI0 models only.       */
+                      /*   runs with as many as remain. A frame's chunk does not     */
+                      /*   depend on k >= 2 or on the group it lands in (every       */
+                      /*   reduction is planned for 8 frames); it differs from the   */
+                      /*   one-frame loop only in rounding order (see                */
+                      /*   vla_pipeline_run). VLA_HEAD_PI0 models only.              */
   int32_t vlm_batch;  /* frames per VLM prefill (0 or 1: one; else 2, 4 or 8). With  */
                       /*   k > 1, the prefills of k consecutive frames (different    */
                       /*   robots) run as one pass: their views stacked for the ViT  */
@@ -163,6 +167,10 @@ int vla_validate(const vla_config* cfg);
  * per-phase scratch memory. Blocking. The library owns *out. */
 int vla_create(const vla_config* cfg, uint64_t seed, vla_model** out);
 
+/* Copy the model's configuration to *out (host). VLA_EINVAL for NULL
+ * pointers. Lets a caller size the device buffers of the calls below. */
+int vla_model_config(const vla_model* m, vla_config* out);
+
 /* Free everything the model owns (waits for its streams). NULL is a no-op. */
 int vla_destroy(vla_model* m);
 
@@ -179,26 +187,33 @@ int vla_ctx_destroy(vla_ctx* c);
  * writing every layer's K (after RoPE) and V into `ctx`. */
 int vla_vlm_prefill(vla_model* m, const vla_frame* in, vla_ctx* ctx, void* stream);
 
-/* Phase 2 for one frame, enqueued on `stream`, asynchronous: n_steps Euler
- * steps x <- x + dt * v(x, t) from x_0 = noise at t = 1 to t = 0, each step a
- * full pass of the expert over [ctx KV; its own KV]. noise and actions are
- * device fp32 [chunk_len, action_dim] and may alias. Must be ordered after
- * the prefill that wrote ctx (same stream, or an event wait). */
+/* Phase 2 for one frame, enqueued on `stream`, asynchronous: n_steps sampler
+ * steps from x_0 = noise, each a full pass of the action head (pi0 expert:
+ * over [ctx KV; its own KV]; DiT: over the ctx cross K/V) whose output
+ * updates x in the output projection's epilogue: x <- x + dt v (Euler, t
+ * from 1 to 0) or x <- a_k x + b_k eps (DDIM; see VLA_SAMPLER_DDIM). noise
+ * and actions are device fp32 [chunk_len, action_dim] and may alias. Must be
+ * ordered after the prefill that wrote ctx (same stream, or an event wait). */
 int vla_action_denoise(vla_model* m, const vla_ctx* ctx, const float* noise, float* actions,
                        void* stream);
 
 /* Run R frames through the two-stage pipeline and wait for it. frames:
- * host array of R vla_frame (device pointers inside); noise: device fp32
- * [R * k, chunk_len, action_dim] with k = max(1, act_chunks), item i = chunk
- * i % k of frame i / k; actions: device fp32 of the same shape. The VLM
- * prefill of later frames overlaps the action phases of earlier ones (a ring
- * of model-owned contexts, allocated in blocks of 8, and events between the
- * streams) except in VLA_MODE_SERIAL. Results are bit-identical across
- * modes, stream counts, prefill batching and graph replay; batched action
- * loops (act_batch >= 2) are bit-identical among themselves and within the
- * chunk tolerance of one-item loops. t may be NULL (frames_per_s counts
- * frames, actions_per_s counts chunk rows of every item). Calls on one model
- * are serialised. */
+ * host array of at least R vla_frame (device pointers inside); noise: device
+ * fp32 [R * k, chunk_len, action_dim] with k = max(1, act_chunks), item i =
+ * chunk i % k of frame i / k; actions: device fp32 of the same shape. The
+ * library cannot check these lengths: shorter buffers are read and written
+ * out of bounds (the Python binding checks tensors before the call). The VLM
+ * prefill of a later prefill group overlaps the action phases of earlier
+ * ones (a ring of model-owned contexts, allocated in blocks of 8, and events
+ * between the streams) except in VLA_MODE_SERIAL. Results are bit-identical
+ * across modes, stream counts, prefill batching and graph replay. Batched
+ * action loops (act_batch >= 2) are bit-identical among themselves and
+ * differ from one-item loops only in the GEMMs' rounding order: for Euler
+ * both are within the chunk tolerance of the exact model; DDIM amplifies a
+ * head-output difference by up to sum_k |b_k| prod_{j>k} |a_j| (about 160 for
+ * 10 steps), so its batched and one-item chunks differ by that factor more.
+ * t may be NULL (frames_per_s counts frames, actions_per_s counts chunk rows
+ * of every item). Calls on one model are serialised. */
 int vla_pipeline_run(vla_model* m, const vla_frame* frames, const float* noise, int32_t R,
                      const vla_sched* sched, float* actions, vla_timing* t);
 

@@ -85,6 +85,7 @@ def _load():
     sig = {
         "vla_preset": [ctypes.c_char_p, ctypes.POINTER(vla_config)],
         "vla_validate": [ctypes.POINTER(vla_config)],
+        "vla_model_config": [P, ctypes.POINTER(vla_config)],
         "vla_create": [ctypes.POINTER(vla_config), U64, ctypes.POINTER(P)],
         "vla_destroy": [P],
         "vla_ctx_create": [P, ctypes.POINTER(P)],
@@ -170,16 +171,67 @@ def vla_ctx_destroy(ctx: Optional[int]) -> None:
     _check(_lib.vla_ctx_destroy(ctx))
 
 
+def vla_model_config(model: int) -> Dict[str, int]:
+    c = vla_config()
+    _check(_lib.vla_model_config(model, ctypes.byref(c)))
+    return {f: int(getattr(c, f)) for f in CONFIG_FIELDS}
+
+
+def _einval(msg: str) -> VlaError:
+    return VlaError(-1, msg)
+
+
+def _check_buffer(x, what: str, numel: int, dtype: str) -> None:
+    """A tensor handed to the library as a device buffer: on the GPU,
+    contiguous, of the element type the entry point reads, and at least
+    `numel` elements long. Raises before anything is launched. Integer
+    pointers cannot be checked and are passed as given."""
+    if x is None:
+        raise _einval(f"{what} is None")
+    if not hasattr(x, "data_ptr"):
+        return
+    if not getattr(x, "is_cuda", False):
+        raise _einval(f"{what} must be a device (cuda) tensor")
+    if str(x.dtype) != f"torch.{dtype}":
+        raise _einval(f"{what} must be {dtype}, got {x.dtype}")
+    if not x.is_contiguous():
+        raise _einval(f"{what} must be contiguous")
+    if x.numel() < numel:
+        raise _einval(f"{what} holds {x.numel()} elements, needs at least {numel}")
+
+
+def _check_frame(cfg: Dict[str, int], fr: vla_frame, i: int) -> None:
+    src = getattr(fr, "_src", None)
+    if src is None:
+        return
+    pixels, ids, state = src
+    _check_buffer(pixels, f"frame {i} pixels", cfg["n_views"] * cfg["img_h"] * cfg["img_w"] * 3, "float32")
+    if cfg["n_text"] > 0:
+        _check_buffer(ids, f"frame {i} text_ids", cfg["n_text"], "int32")
+    if cfg["state_dim"] > 0:
+        _check_buffer(state, f"frame {i} state", cfg["state_dim"], "float32")
+
+
 def make_frame(pixels, text_ids, state=None) -> vla_frame:
-    """A vla_frame from device buffers (tensors or integer pointers)."""
-    return vla_frame(_ptr(pixels), _ptr(text_ids), _ptr(state))
+    """A vla_frame from device buffers (tensors or integer pointers); the
+    tensors are kept with it so the calls below can check them."""
+    f = vla_frame(_ptr(pixels), _ptr(text_ids), _ptr(state))
+    f._src = (pixels, text_ids, state)
+    return f
 
 
 def vla_vlm_prefill(model: int, frame: vla_frame, ctx: int, stream: int = 0) -> None:
+    if model:
+        _check_frame(vla_model_config(model), frame, 0)
     _check(_lib.vla_vlm_prefill(model, ctypes.byref(frame), ctx, stream or None))
 
 
 def vla_action_denoise(model: int, ctx: int, noise, actions, stream: int = 0) -> None:
+    if model:
+        cfg = vla_model_config(model)
+        n = cfg["chunk_len"] * cfg["action_dim"]
+        _check_buffer(noise, "noise", n, "float32")
+        _check_buffer(actions, "actions", n, "float32")
     _check(_lib.vla_action_denoise(model, ctx, _ptr(noise), _ptr(actions), stream or None))
 
 
@@ -187,6 +239,17 @@ def vla_pipeline_run(model: int, frames: Sequence[vla_frame], noise, R: int, mod
                      vlm_cus: int = 0, act_cus: int = 0, vlm_wg_cap: int = 0, actions=None,
                      act_streams: int = 1, graphs: bool = False, vlm_streams: int = 1,
                      act_batch: int = 1, vlm_batch: int = 1, act_chunks: int = 1) -> Dict[str, float]:
+    if model and int(R) >= 1:
+        # the library reads frames[0 .. R-1] and R * k chunks of noise and
+        # actions (k = act_chunks): check them all before anything runs
+        if len(frames) < int(R):
+            raise _einval(f"{len(frames)} frames given for R = {R}")
+        cfg = vla_model_config(model)
+        n = int(R) * max(1, int(act_chunks)) * cfg["chunk_len"] * cfg["action_dim"]
+        _check_buffer(noise, "noise", n, "float32")
+        _check_buffer(actions, "actions", n, "float32")
+        for i in range(int(R)):
+            _check_frame(cfg, frames[i], i)
     arr = (vla_frame * len(frames))(*frames)
     s = vla_sched(MODES[mode] if isinstance(mode, str) else int(mode), vlm_cus, act_cus, vlm_wg_cap,
                   act_streams, 1 if graphs else 0, vlm_streams, act_batch, vlm_batch, act_chunks)
@@ -281,7 +344,7 @@ def vla_debug_generate(seed: int, name: str, n: int, mean: float, std: float) ->
 
 def exported_symbols() -> Iterable[str]:
     """Names of the C entry points this binding wraps."""
-    return ["vla_preset", "vla_validate", "vla_create", "vla_destroy", "vla_ctx_create",
+    return ["vla_preset", "vla_validate", "vla_model_config", "vla_create", "vla_destroy", "vla_ctx_create",
             "vla_ctx_destroy", "vla_vlm_prefill", "vla_action_denoise", "vla_pipeline_run",
             "vla_param_count", "vla_param_info", "vla_export_param", "vla_ctx_export_kv", "vla_ctx_export_cross", "vla_wavelog_enable", "vla_wavelog_read",
             "vla_debug_gemm", "vla_debug_attention", "vla_debug_attention_cache", "vla_debug_generate",

@@ -122,23 +122,26 @@ class Sim:
 
     def choose(self, j: int, active: Sequence[Tuple[int, _Run]]) -> Optional[int]:
         """One admission decision on CU j over the active kernels (run id,
-        run) in dispatcher order; returns the run id to admit or None."""
+        run) in dispatcher order; returns the run id to admit or None.
+
+        Baseline: only the oldest kernel with workgroups left may dispatch.
+        Two-phase policy (Section 3, Algorithm 1): a kernel with no workgroup
+        on this CU yet goes first, so every co-runner gets a foothold;
+        otherwise the kernel whose intensity best fills the CU's idle
+        pipelines, by the score of _score (the first one on a tie)."""
         if self.policy == "baseline":
-            for rid, run in active:
-                if run.pending > 0:
-                    return rid if self._fits(j, run) else None
+            oldest = next((run for _, run in active if run.pending > 0), None)
+            if oldest is None or not self._fits(j, oldest):
+                return None
+            return next(rid for rid, run in active if run is oldest)
+        fitting = [(rid, run) for rid, run in active if self._fits(j, run)]
+        if not fitting:
             return None
-        for rid, run in active:  # phase 1
-            if run.pending > 0 and self.resident[j].get(rid, 0) == 0 and self._fits(j, run):
-                return rid
-        best, best_s = None, -1.0  # phase 2
-        for rid, run in active:
-            if not self._fits(j, run):
-                continue
-            s = self._score(j, run, rid)
-            if s > best_s:
-                best, best_s = rid, s
-        return best
+        newcomer = next((rid for rid, _ in fitting if self.resident[j].get(rid, 0) == 0), None)
+        if newcomer is not None:
+            return newcomer
+        scores = [self._score(j, run, rid) for rid, run in fitting]
+        return fitting[scores.index(max(scores))][0]
 
     # -- contention ----------------------------------------------------------
     def _rate(self, j: int, k: Kernel) -> float:

@@ -17,6 +17,7 @@
 #include <map>
 #include <memory>
 #include <mutex>
+#include <new>
 #include <string>
 #include <vector>
 
@@ -1902,14 +1903,18 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
 // C ABI
 // ---------------------------------------------------------------------------
 
-#define ABI_GUARD(...)                                            \
-  try {                                                           \
-    g_err.clear();                                                \
-    __VA_ARGS__                                                   \
-  } catch (const std::exception& ex) {                            \
-    return fail(VLA_ENOMEM, std::string("exception: ") + ex.what()); \
-  } catch (...) {                                                 \
-    return fail(VLA_EINVAL, "unknown exception");                 \
+// No C++ exception crosses the ABI: an allocation failure is VLA_ENOMEM,
+// any other exception (a library defect, not a caller error) VLA_ESTATE.
+#define ABI_GUARD(...)                                                          \
+  try {                                                                         \
+    g_err.clear();                                                              \
+    __VA_ARGS__                                                                 \
+  } catch (const std::bad_alloc& ex) {                                          \
+    return fail(VLA_ENOMEM, std::string("host allocation failed: ") + ex.what()); \
+  } catch (const std::exception& ex) {                                          \
+    return fail(VLA_ESTATE, std::string("internal exception: ") + ex.what());   \
+  } catch (...) {                                                               \
+    return fail(VLA_ESTATE, "internal exception");                              \
   }
 
 extern "C" {
@@ -1930,6 +1935,14 @@ int vla_create(const vla_config* cfg, uint64_t seed, vla_model** out) {
     if (!out) return fail(VLA_EINVAL, "out is NULL");
     *out = nullptr;
     return create_impl(cfg, seed, out);
+  })
+}
+
+int vla_model_config(const vla_model* m, vla_config* out) {
+  ABI_GUARD({
+    if (!m || !out) return fail(VLA_EINVAL, "NULL argument");
+    *out = m->c;
+    return VLA_OK;
   })
 }
 

@@ -530,8 +530,9 @@ def test_abi_errors_on_device(V):
             V.vla_pipeline_run(m, [], torch.zeros(1, device="cuda"), 0, actions=torch.zeros(1, device="cuda"))
         assert e.value.code == -1
         with pytest.raises(V.VlaError):
-            V.vla_pipeline_run(m, [V.make_frame(1, 1, 1)], torch.zeros(1, device="cuda"), 1,
-                               mode="cu_masked", vlm_cus=4, act_cus=8, actions=torch.zeros(1, device="cuda"))
+            n = cfg["chunk_len"] * cfg["action_dim"]
+            V.vla_pipeline_run(m, [V.make_frame(1, 1, 1)], torch.zeros(n, device="cuda"), 1,
+                               mode="cu_masked", vlm_cus=4, act_cus=8, actions=torch.zeros(n, device="cuda"))
         with pytest.raises(V.VlaError):
             V.vla_export_param(m, "nope", 3)
         with g.model(cfg) as m2, g.context(m2) as c2:
