@@ -251,6 +251,21 @@ int vla_debug_attention(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int3
                         const void* q, const void* k0, const void* v0, int32_t S0, const void* k1,
                         const void* v1, int32_t S1, void* out, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops and harnesses that forbid hipMalloc): the GEMM of
+ * vla_debug_gemm, same arguments, layouts, kernels, plan and result bits,
+ * but it allocates nothing and never synchronises. Its split-K partials go
+ * to a fixed device array of 2^21 floats (8 MiB) that every GPU the library
+ * runs on holds until the process ends; a shape whose plan needs more
+ * returns VLA_EUNSUPPORTED (the planner splits at most 256 64-wide tiles, so
+ * no valid shape needs more than 2^20 floats). Every call on one GPU shares
+ * that array and a later call overwrites it: calls whose executions overlap
+ * on one GPU (two streams, or two host threads) race. Each call writes every
+ * partial it reads, so nothing needs clearing between calls. All pointers
+ * device; asynchronous on `stream`. */
+int vla_gemm_noalloc(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* A, int32_t lda,
+                     const void* W, int32_t ldw, const float* bias, float* C, void* stream);
+
 /* Test entry point for the attention kernel of the LM and the expert: as
  * vla_debug_attention (q and out row-major, out 16-byte aligned), but K and V
  * of each segment are in the KV-cache layout, with nb = ceil(S / 32) blocks

@@ -102,6 +102,7 @@ def _load():
         "vla_wavelog_enable": [P, I64],
         "vla_wavelog_read": [P, P, I64, ctypes.POINTER(I64)],
         "vla_debug_gemm": [I32, I32, I32, I32, P, I32, P, I32, P, P, P],
+        "vla_gemm_noalloc": [I32, I32, I32, I32, P, I32, P, I32, P, P, P],
         "vla_debug_attention": [I32, I32, I32, I32, I32, P, P, P, I32, P, P, I32, P, P],
         "vla_debug_generate": [U64, ctypes.c_char_p, I64, D, D, P],
         "vla_debug_attention_cache": [I32, I32, I32, I32, I32, P, P, P, I32, P, P, I32, P, P],
@@ -313,6 +314,12 @@ def vla_debug_gemm(dtype: int, M: int, N: int, K: int, A, lda: int, W, ldw: int,
                                stream or None))
 
 
+def vla_gemm_noalloc(dtype: int, M: int, N: int, K: int, A, lda: int, W, ldw: int, bias, C,
+                     stream: int = 0) -> None:
+    _check(_lib.vla_gemm_noalloc(dtype, M, N, K, _ptr(A), lda, _ptr(W), ldw, _ptr(bias), _ptr(C),
+                                 stream or None))
+
+
 def vla_debug_attention(dtype: int, Sq: int, nq: int, nkv: int, hd: int, q, k0, v0, S0: int,
                         k1, v1, S1: int, out, stream: int = 0) -> None:
     _check(_lib.vla_debug_attention(dtype, Sq, nq, nkv, hd, _ptr(q), _ptr(k0), _ptr(v0), S0,
@@ -347,6 +354,6 @@ def exported_symbols() -> Iterable[str]:
     return ["vla_preset", "vla_validate", "vla_model_config", "vla_create", "vla_destroy", "vla_ctx_create",
             "vla_ctx_destroy", "vla_vlm_prefill", "vla_action_denoise", "vla_pipeline_run",
             "vla_param_count", "vla_param_info", "vla_export_param", "vla_ctx_export_kv", "vla_ctx_export_cross", "vla_wavelog_enable", "vla_wavelog_read",
-            "vla_debug_gemm", "vla_debug_attention", "vla_debug_attention_cache", "vla_debug_generate",
+            "vla_debug_gemm", "vla_gemm_noalloc", "vla_debug_attention", "vla_debug_attention_cache", "vla_debug_generate",
             "vla_kernel_timer",
             "vla_kernel_timer_read", "vla_last_error"]

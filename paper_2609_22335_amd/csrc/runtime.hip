@@ -1900,6 +1900,38 @@ static int pipeline_impl(vla_model* m, const vla_frame* frames, const float* noi
 }
 
 // ---------------------------------------------------------------------------
+// Allocation-free GEMM: split-K partials in a fixed device array
+// ---------------------------------------------------------------------------
+
+// Split-K partials of vla_gemm_noalloc. Every GPU the library runs on holds
+// its own copy until the process ends. In host code `scratch` only names the
+// symbol: kernels get the device address that hipGetSymbolAddress returns
+// for the current device (noalloc_scratch below), never the name itself.
+constexpr size_t NOALLOC_SCRATCH_FLOATS = (size_t)2 << 20;  // 8 MiB
+static __device__ __align__(256) float scratch[NOALLOC_SCRATCH_FLOATS];
+
+constexpr int NOALLOC_MAX_DEVICES = 64;
+static float* g_noalloc_ptr[NOALLOC_MAX_DEVICES] = {};
+static std::mutex g_noalloc_mu;
+
+// Device address of the current device's copy of `scratch`, looked up on the
+// first call on that device (with it current) and kept.
+static int noalloc_scratch(float** out) {
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= NOALLOC_MAX_DEVICES) return fail(VLA_EUNSUPPORTED, "device index above 63");
+  std::lock_guard<std::mutex> lock(g_noalloc_mu);
+  if (!g_noalloc_ptr[dev]) {
+    void* p = nullptr;
+    HIP_TRY(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(VLA_EHIP, "hipGetSymbolAddress returned NULL for the scratch array");
+    g_noalloc_ptr[dev] = (float*)p;
+  }
+  *out = g_noalloc_ptr[dev];
+  return VLA_OK;
+}
+
+// ---------------------------------------------------------------------------
 // C ABI
 // ---------------------------------------------------------------------------
 
@@ -2188,6 +2220,34 @@ int vla_debug_gemm(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* A
       hipStreamSynchronize((hipStream_t)stream);
       hipFree(s.ptr);
     }
+    if (e != hipSuccess) return fail(VLA_EHIP, std::string("gemm: ") + hipGetErrorString(e));
+    return VLA_OK;
+  })
+}
+
+int vla_gemm_noalloc(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* A, int32_t lda,
+                     const void* W, int32_t ldw, const float* bias, float* C, void* stream) {
+  ABI_GUARD({
+    if (dtype != VLA_F32 && dtype != VLA_BF16) return fail(VLA_EINVAL, "dtype");
+    if (M <= 0 || N <= 0 || K <= 0 || K % 8 || lda < K || ldw < K || lda % 8 || ldw % 8)
+      return fail(VLA_EINVAL, "shape: M, N, K > 0, K, lda, ldw multiples of 8, lda, ldw >= K");
+    if (!A || !W || !C) return fail(VLA_EINVAL, "NULL argument");
+    GemmDesc g{dtype == VLA_BF16 ? DT_BF16 : DT_F32, A, lda, W, ldw, M, N, K, Epi()};
+    g.epi.kind = EPI_F32;
+    g.epi.out = C;
+    g.epi.ldo = N;
+    g.epi.bias = bias;
+    const GemmPlan p = plan_gemm(g);
+    if (p.scratch_floats > NOALLOC_SCRATCH_FLOATS)
+      return fail(VLA_EUNSUPPORTED, "split-K partials of " + std::to_string(p.scratch_floats) +
+                                        " floats exceed the fixed scratch of " +
+                                        std::to_string(NOALLOC_SCRATCH_FLOATS) + " floats");
+    Scratch s;
+    if (p.scratch_floats) {
+      VLA_TRY(noalloc_scratch(&s.ptr));
+      s.floats = NOALLOC_SCRATCH_FLOATS;
+    }
+    hipError_t e = launch_gemm(g, s, LaunchCaps{}, (hipStream_t)stream);
     if (e != hipSuccess) return fail(VLA_EHIP, std::string("gemm: ") + hipGetErrorString(e));
     return VLA_OK;
   })
