@@ -251,6 +251,59 @@ int vla_debug_attention(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int3
                         const void* q, const void* k0, const void* v0, int32_t S0, const void* k1,
                         const void* v1, int32_t S1, void* out, void* stream);
 
+/* Test entry point for the GEMM epilogues (the fused operations of every
+ * phase), on the tiled kernel or the skinny one. A [M][K] and W [N][K] are
+ * row-major device arrays of the operand type (dtype as in vla_debug_gemm;
+ * K a multiple of 8) with W in its logical row order; with v = A W^T:
+ *  BIAS       out fp32 [M][N] = v + bias
+ *  T          out [M][N] = T(v + bias)            (T: round to the operand type)
+ *  GELU       out [M][N] = T(gelu_tanh(v + bias))
+ *  SWISH      out [M][N] = T(swish(v + bias))
+ *  GEGLU      W = [gate (N/2 rows); up (N/2 rows)], N a multiple of 32:
+ *             out [M][N/2] = T(gelu_tanh(v_gate) * v_up)
+ *  QKV_ROPE   W = [q (nq hd rows); k (nkv hd); v (nkv hd)], hd a multiple of
+ *             32: q_out [M][nq hd] and k_out [M][nkv hd] = T(RoPE(v_q or v_k,
+ *             position pos0 + m)) (rotate-half pairs (i, i + hd/2), angle
+ *             p 10000^(-2 i / hd)), v_out [M][nkv hd] = T(v_v); K and V pass
+ *             through the KV-cache layout and are returned row-major
+ *  QKV_PLAIN  as QKV_ROPE without the rotation (hd a multiple of 8)
+ *  STEP       x fp32 [M][N] <- xs x + dt (v + bias); out [M][N] = T(new x)
+ *  RESID_NORM resid fp32 [M][N] += v (split-K partials summed in split
+ *             order); out [M][N] = T(RMSNorm(resid) * gain), N <= 2048
+ * bias may be NULL; GEGLU and QKV take none. skinny = 1 runs the action
+ * head's kernel (M <= 64): W is converted to MFMA fragment order and A to
+ * the row-block operand layout, and operand-type outputs are written in that
+ * layout and returned row-major. skinny = 0 runs the tiled kernel with the
+ * tile the planner picks for M and N. plan_out (host, may be NULL) receives
+ * the tile's rows and columns (0 and 32 for the skinny kernel) and the
+ * split-K factor. Blocking; allocates temporaries. */
+#define VLA_DEBUG_EPI_BIAS 0
+#define VLA_DEBUG_EPI_T 1
+#define VLA_DEBUG_EPI_GELU 2
+#define VLA_DEBUG_EPI_SWISH 3
+#define VLA_DEBUG_EPI_GEGLU 4
+#define VLA_DEBUG_EPI_QKV_ROPE 5
+#define VLA_DEBUG_EPI_QKV_PLAIN 6
+#define VLA_DEBUG_EPI_STEP 7
+#define VLA_DEBUG_EPI_RESID_NORM 8
+typedef struct vla_debug_epi {
+  int32_t kind;           /* VLA_DEBUG_EPI_*                                   */
+  int32_t skinny;         /* 0: tiled kernel, 1: skinny kernel (M <= 64)       */
+  const float* bias;      /* device fp32 [N] or NULL                           */
+  void* out;              /* device, see above                                 */
+  int32_t nq, nkv, hd, pos0; /* QKV_ROPE / QKV_PLAIN                           */
+  void* q_out;            /* device, operand type                              */
+  void* k_out;
+  void* v_out;
+  float* x;               /* STEP: device fp32 [M][N], updated                 */
+  float xs, dt;           /* STEP coefficients                                 */
+  float* resid;           /* RESID_NORM: device fp32 [M][N], updated           */
+  const float* gain;      /* RESID_NORM: device fp32 [N]                       */
+  int32_t* plan_out;      /* host int32[3] or NULL                             */
+} vla_debug_epi;
+int vla_debug_gemm_epi(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* A, const void* W,
+                       const vla_debug_epi* e, void* stream);
+
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, serving loops and harnesses that forbid hipMalloc): the GEMM of
  * vla_debug_gemm, same arguments, layouts, kernels, plan and result bits,

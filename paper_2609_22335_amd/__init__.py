@@ -58,6 +58,19 @@ class vla_timing(ctypes.Structure):
                 ("act_ms", ctypes.c_double)]
 
 
+class vla_debug_epi(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("skinny", ctypes.c_int32), ("bias", ctypes.c_void_p),
+                ("out", ctypes.c_void_p), ("nq", ctypes.c_int32), ("nkv", ctypes.c_int32),
+                ("hd", ctypes.c_int32), ("pos0", ctypes.c_int32), ("q_out", ctypes.c_void_p),
+                ("k_out", ctypes.c_void_p), ("v_out", ctypes.c_void_p), ("x", ctypes.c_void_p),
+                ("xs", ctypes.c_float), ("dt", ctypes.c_float), ("resid", ctypes.c_void_p),
+                ("gain", ctypes.c_void_p), ("plan_out", ctypes.c_void_p)]
+
+
+DEBUG_EPI = {"bias": 0, "t": 1, "gelu": 2, "swish": 3, "geglu": 4, "qkv_rope": 5, "qkv_plain": 6, "step": 7,
+             "resid_norm": 8}
+
+
 class VlaError(RuntimeError):
     def __init__(self, code: int, msg: str):
         super().__init__(f"vla status {code}: {msg}")
@@ -103,6 +116,7 @@ def _load():
         "vla_wavelog_read": [P, P, I64, ctypes.POINTER(I64)],
         "vla_debug_gemm": [I32, I32, I32, I32, P, I32, P, I32, P, P, P],
         "vla_gemm_noalloc": [I32, I32, I32, I32, P, I32, P, I32, P, P, P],
+        "vla_debug_gemm_epi": [I32, I32, I32, I32, P, P, ctypes.POINTER(vla_debug_epi), P],
         "vla_debug_attention": [I32, I32, I32, I32, I32, P, P, P, I32, P, P, I32, P, P],
         "vla_debug_generate": [U64, ctypes.c_char_p, I64, D, D, P],
         "vla_debug_attention_cache": [I32, I32, I32, I32, I32, P, P, P, I32, P, P, I32, P, P],
@@ -314,6 +328,20 @@ def vla_debug_gemm(dtype: int, M: int, N: int, K: int, A, lda: int, W, ldw: int,
                                stream or None))
 
 
+def vla_debug_gemm_epi(dtype: int, M: int, N: int, K: int, A, W, kind: str, skinny: bool = False, bias=None,
+                       out=None, nq: int = 0, nkv: int = 0, hd: int = 0, pos0: int = 0, q_out=None, k_out=None,
+                       v_out=None, x=None, xs: float = 1.0, dt: float = 0.0, resid=None, gain=None,
+                       stream: int = 0) -> Tuple[int, int]:
+    """Returns (tile rows, tile columns, split-K factor) of the launch; the
+    skinny kernel reports 0 rows."""
+    plan = (ctypes.c_int32 * 3)()
+    e = vla_debug_epi(DEBUG_EPI[kind], 1 if skinny else 0, _ptr(bias), _ptr(out), nq, nkv, hd, pos0, _ptr(q_out),
+                      _ptr(k_out), _ptr(v_out), _ptr(x), xs, dt, _ptr(resid), _ptr(gain),
+                      ctypes.cast(plan, ctypes.c_void_p))
+    _check(_lib.vla_debug_gemm_epi(dtype, M, N, K, _ptr(A), _ptr(W), ctypes.byref(e), stream or None))
+    return int(plan[0]), int(plan[1]), int(plan[2])
+
+
 def vla_gemm_noalloc(dtype: int, M: int, N: int, K: int, A, lda: int, W, ldw: int, bias, C,
                      stream: int = 0) -> None:
     _check(_lib.vla_gemm_noalloc(dtype, M, N, K, _ptr(A), lda, _ptr(W), ldw, _ptr(bias), _ptr(C),
@@ -354,6 +382,6 @@ def exported_symbols() -> Iterable[str]:
     return ["vla_preset", "vla_validate", "vla_model_config", "vla_create", "vla_destroy", "vla_ctx_create",
             "vla_ctx_destroy", "vla_vlm_prefill", "vla_action_denoise", "vla_pipeline_run",
             "vla_param_count", "vla_param_info", "vla_export_param", "vla_ctx_export_kv", "vla_ctx_export_cross", "vla_wavelog_enable", "vla_wavelog_read",
-            "vla_debug_gemm", "vla_gemm_noalloc", "vla_debug_attention", "vla_debug_attention_cache", "vla_debug_generate",
+            "vla_debug_gemm", "vla_debug_gemm_epi", "vla_gemm_noalloc", "vla_debug_attention", "vla_debug_attention_cache", "vla_debug_generate",
             "vla_kernel_timer",
             "vla_kernel_timer_read", "vla_last_error"]

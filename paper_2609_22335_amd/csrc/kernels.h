@@ -187,6 +187,9 @@ struct GemmPlan {
 };
 
 GemmPlan plan_gemm(const GemmDesc& g);
+// Rows and columns of the tile of plan p (the skinny kernel: 0 rows, 32
+// columns per workgroup).
+void plan_tile(const GemmDesc& g, const GemmPlan& p, int* bm, int* bn);
 hipError_t launch_gemm(const GemmDesc& g, const Scratch& s, const LaunchCaps& caps, hipStream_t st);
 
 struct AttnDesc {

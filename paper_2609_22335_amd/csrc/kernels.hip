@@ -1183,6 +1183,17 @@ GemmPlan plan_gemm(const GemmDesc& g) {
   return p;
 }
 
+void plan_tile(const GemmDesc& g, const GemmPlan& p, int* bm, int* bn) {
+  if (p.cfg < 0) {
+    *bm = 0;
+    *bn = 32;
+    return;
+  }
+  const TileCfg t = (g.dtype == DT_BF16 ? kBf16Cfg : kF32Cfg)[p.cfg];
+  *bm = t.bm;
+  *bn = t.bn;
+}
+
 template <typename T, int BM, int BN, int BK, int WGM = 2, int WGN = 2, int PD = 1, int PAD = VLA_GEMM_LDS_PAD,
           bool DL = false>
 static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch& s,

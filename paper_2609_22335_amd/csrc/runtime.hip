@@ -1270,18 +1270,27 @@ static int alloc_scratch(vla_model* m, const ScratchNeed& n, Scratch* s) {
   return VLA_OK;
 }
 
-static int setup_tables(vla_model* m) {
-  const vla_config& c = m->c;
-  const Dims& d = m->d;
-  const int npos = d.prefix + c.chunk_len, half = c.head_dim / 2;
-  std::vector<float> cs((size_t)npos * half), sn((size_t)npos * half);
+// RoPE tables [npos][hd / 2]: cos and sin of p 10000^(-2 i / hd), computed in
+// fp64 and rounded to fp32.
+static void rope_tables(int npos, int hd, std::vector<float>& cs, std::vector<float>& sn) {
+  const int half = hd / 2;
+  cs.assign((size_t)npos * half, 0.f);
+  sn.assign((size_t)npos * half, 0.f);
   for (int p = 0; p < npos; ++p)
     for (int i = 0; i < half; ++i) {
-      const double inv = std::pow(10000.0, -2.0 * i / c.head_dim);
+      const double inv = std::pow(10000.0, -2.0 * i / hd);
       const double ang = p * inv;
       cs[(size_t)p * half + i] = (float)std::cos(ang);
       sn[(size_t)p * half + i] = (float)std::sin(ang);
     }
+}
+
+static int setup_tables(vla_model* m) {
+  const vla_config& c = m->c;
+  const Dims& d = m->d;
+  const int npos = d.prefix + c.chunk_len;
+  std::vector<float> cs, sn;
+  rope_tables(npos, c.head_dim, cs, sn);
   VLA_TRY(dmalloc(m, (void**)&m->rope_cos, cs.size() * 4));
   VLA_TRY(dmalloc(m, (void**)&m->rope_sin, sn.size() * 4));
   HIP_TRY(hipMemcpy(m->rope_cos, cs.data(), cs.size() * 4, hipMemcpyHostToDevice));
@@ -2249,6 +2258,245 @@ int vla_gemm_noalloc(int32_t dtype, int32_t M, int32_t N, int32_t K, const void*
     }
     hipError_t e = launch_gemm(g, s, LaunchCaps{}, (hipStream_t)stream);
     if (e != hipSuccess) return fail(VLA_EHIP, std::string("gemm: ") + hipGetErrorString(e));
+    return VLA_OK;
+  })
+}
+
+int vla_debug_gemm_epi(int32_t dtype, int32_t M, int32_t N, int32_t K, const void* A, const void* W,
+                       const vla_debug_epi* ep, void* stream_) {
+  ABI_GUARD({
+    if (dtype != VLA_F32 && dtype != VLA_BF16) return fail(VLA_EINVAL, "dtype");
+    if (!A || !W || !ep) return fail(VLA_EINVAL, "NULL argument");
+    const vla_debug_epi& e = *ep;
+    if (M <= 0 || N <= 0 || K <= 0 || K % 8) return fail(VLA_EINVAL, "shape: M, N, K > 0, K a multiple of 8");
+    if (e.skinny && M > 64) return fail(VLA_EINVAL, "the skinny kernel takes M <= 64");
+    const int dt = dtype == VLA_BF16 ? DT_BF16 : DT_F32;
+    const size_t esz = dt == DT_BF16 ? 2 : 4;
+    hipStream_t st = (hipStream_t)stream_;
+    const int kind = e.kind;
+    const bool rope = kind == VLA_DEBUG_EPI_QKV_ROPE, qkv = rope || kind == VLA_DEBUG_EPI_QKV_PLAIN;
+    if (kind < VLA_DEBUG_EPI_BIAS || kind > VLA_DEBUG_EPI_RESID_NORM) return fail(VLA_EINVAL, "unknown epilogue");
+    if (kind == VLA_DEBUG_EPI_GEGLU && N % 32) return fail(VLA_EINVAL, "GEGLU: N must be a multiple of 32");
+    if (qkv) {
+      if (e.nq < 0 || e.nkv <= 0 || e.hd <= 0 || e.hd % 8 || N != (e.nq + 2 * e.nkv) * e.hd || e.pos0 < 0)
+        return fail(VLA_EINVAL, "QKV: N must be (nq + 2 nkv) hd, hd a multiple of 8");
+      if (rope && e.hd % 32) return fail(VLA_EINVAL, "QKV_ROPE: hd must be a multiple of 32");
+      if (dt == DT_F32 && e.hd > 128) return fail(VLA_EINVAL, "QKV in fp32: hd <= 128");
+      if ((e.nq > 0 && !e.q_out) || !e.k_out || !e.v_out) return fail(VLA_EINVAL, "QKV: NULL output");
+    } else if (kind == VLA_DEBUG_EPI_STEP) {
+      if (!e.x || !e.out) return fail(VLA_EINVAL, "STEP: NULL x or out");
+    } else if (kind == VLA_DEBUG_EPI_RESID_NORM) {
+      if (!e.resid || !e.gain || !e.out || N > 2048) return fail(VLA_EINVAL, "RESID_NORM: NULL buffer or N > 2048");
+    } else if (!e.out) {
+      return fail(VLA_EINVAL, "NULL out");
+    }
+    std::vector<void*> tmp;
+    struct Free {
+      std::vector<void*>& v;
+      ~Free() {
+        for (void* p : v) hipFree(p);
+      }
+    } freer{tmp};
+    // temporaries: zeroed and filled by blocking calls; the device is
+    // synchronised before the launches on `st`
+    auto dalloc = [&](size_t bytes, void** p) -> int {
+      HIP_TRY(hipMalloc(p, std::max<size_t>(bytes, 256)));
+      tmp.push_back(*p);
+      HIP_TRY(hipMemset(*p, 0, std::max<size_t>(bytes, 256)));
+      return VLA_OK;
+    };
+    HIP_TRY(hipStreamSynchronize(st));
+    // host images of the operands (logical row-major)
+    std::vector<uint8_t> hw((size_t)N * K * esz);
+    HIP_TRY(hipMemcpy(hw.data(), W, hw.size(), hipMemcpyDeviceToHost));
+    // physical row of logical weight row r: GeGLU gate / up rows interleaved
+    // in 16-row blocks; Q and K rows of each head permuted so that RoPE
+    // partners (i, i + hd/2) sit 16 columns apart
+    const int qk_rows = rope ? (e.nq + e.nkv) * e.hd : 0;
+    auto prow = [&](int rr) -> int {
+      if (kind == VLA_DEBUG_EPI_GEGLU) {
+        const int F = N / 2;
+        return rr < F ? 32 * (rr / 16) + rr % 16 : 32 * ((rr - F) / 16) + 16 + (rr - F) % 16;
+      }
+      if (rope && rr < qk_rows) {
+        const int hd = e.hd, half = hd / 2, head = rr / hd, i = rr % hd;
+        const int ph = i < half ? 32 * (i / 16) + i % 16 : 32 * ((i - half) / 16) + 16 + (i - half) % 16;
+        return head * hd + ph;
+      }
+      return rr;
+    };
+    const int fks = (K + frag_slab(dt) - 1) / frag_slab(dt);
+    std::vector<uint8_t> pw;
+    if (e.skinny) {
+      pw.assign((size_t)((N + 31) / 32 * 32) * fks * frag_slab(dt) * esz, 0);
+      for (int rr = 0; rr < N; ++rr) {
+        const int p = prow(rr);
+        for (int k = 0; k < K; ++k)
+          std::memcpy(&pw[frag_index(p, k, fks, dt) * esz], &hw[((size_t)rr * K + k) * esz], esz);
+      }
+    } else {
+      pw.assign(hw.size(), 0);
+      for (int rr = 0; rr < N; ++rr)
+        std::memcpy(&pw[(size_t)prow(rr) * K * esz], &hw[(size_t)rr * K * esz], (size_t)K * esz);
+    }
+    void* dW = nullptr;
+    VLA_TRY(dalloc(pw.size(), &dW));
+    HIP_TRY(hipMemcpy(dW, pw.data(), pw.size(), hipMemcpyHostToDevice));
+    const void* dA = A;
+    if (e.skinny) {  // A in the row-block operand layout
+      std::vector<uint8_t> ha((size_t)M * K * esz), pa(afrag_elems(dt, K) * esz, 0);
+      HIP_TRY(hipMemcpy(ha.data(), A, ha.size(), hipMemcpyDeviceToHost));
+      for (int mm = 0; mm < M; ++mm)
+        for (int k = 0; k < K; ++k)
+          std::memcpy(&pa[afrag_index(dt, mm, k) * esz], &ha[((size_t)mm * K + k) * esz], esz);
+      void* p = nullptr;
+      VLA_TRY(dalloc(pa.size(), &p));
+      HIP_TRY(hipMemcpy(p, pa.data(), pa.size(), hipMemcpyHostToDevice));
+      dA = p;
+    }
+    Epi x;
+    x.afrag = e.skinny ? 1 : 0;
+    // operand-type output columns and its device image (row-major, or the
+    // row-block operand layout on the skinny path)
+    const int ocols = kind == VLA_DEBUG_EPI_GEGLU ? N / 2 : N;
+    const bool op_out = kind == VLA_DEBUG_EPI_T || kind == VLA_DEBUG_EPI_GELU || kind == VLA_DEBUG_EPI_SWISH ||
+                        kind == VLA_DEBUG_EPI_GEGLU || kind == VLA_DEBUG_EPI_STEP ||
+                        kind == VLA_DEBUG_EPI_RESID_NORM;
+    const size_t oel = e.skinny ? afrag_elems(dt, ocols) : (size_t)M * ocols;
+    void* dout = nullptr;
+    if (op_out) VLA_TRY(dalloc(oel * esz, &dout));
+    void *dk = nullptr, *dv = nullptr;
+    const int kv_nb = (M + 31) / 32;
+    float *rc = nullptr, *rs = nullptr;
+    switch (kind) {
+      case VLA_DEBUG_EPI_BIAS:
+        x.kind = EPI_F32;
+        x.out = e.out;
+        x.ldo = N;
+        x.bias = e.bias;
+        break;
+      case VLA_DEBUG_EPI_T:
+      case VLA_DEBUG_EPI_GELU:
+      case VLA_DEBUG_EPI_SWISH:
+        x.kind = kind == VLA_DEBUG_EPI_T ? EPI_T : kind == VLA_DEBUG_EPI_GELU ? EPI_GELU : EPI_SWISH;
+        x.out = dout;
+        x.ldo = N;
+        x.bias = e.bias;
+        break;
+      case VLA_DEBUG_EPI_GEGLU:
+        x.kind = EPI_GEGLU;
+        x.out = dout;
+        x.ldo = N / 2;
+        break;
+      case VLA_DEBUG_EPI_QKV_ROPE:
+      case VLA_DEBUG_EPI_QKV_PLAIN: {
+        x.kind = rope ? EPI_QKV_ROPE : EPI_QKV_PLAIN;
+        x.afrag = 0;
+        x.q = e.q_out;
+        x.ldq = e.nq * e.hd;
+        VLA_TRY(dalloc(kv_kelems(dt, kv_nb, e.hd, e.nkv) * esz, &dk));
+        VLA_TRY(dalloc(kv_velems(dt, kv_nb, e.hd, e.nkv) * esz, &dv));
+        x.k = dk;
+        x.v = dv;
+        x.kv_nb = kv_nb;
+        x.nq = e.nq;
+        x.nkv = e.nkv;
+        x.hd = e.hd;
+        x.pos0 = e.pos0;
+        if (rope) {
+          std::vector<float> cs, sn;
+          rope_tables(e.pos0 + M, e.hd, cs, sn);
+          VLA_TRY(dalloc(cs.size() * 4, (void**)&rc));
+          VLA_TRY(dalloc(sn.size() * 4, (void**)&rs));
+          HIP_TRY(hipMemcpy(rc, cs.data(), cs.size() * 4, hipMemcpyHostToDevice));
+          HIP_TRY(hipMemcpy(rs, sn.data(), sn.size() * 4, hipMemcpyHostToDevice));
+          x.rope_cos = rc;
+          x.rope_sin = rs;
+        }
+        break;
+      }
+      case VLA_DEBUG_EPI_STEP:
+        x.kind = EPI_EULER;
+        x.bias = e.bias;
+        x.x = e.x;
+        x.ldx = N;
+        x.xop = dout;
+        x.ldxop = N;
+        x.dt = e.dt;
+        x.xs = e.xs;
+        break;
+      default:  // RESID_NORM: raw split-K partials, summed by the norm
+        x.kind = EPI_PART;
+        x.afrag = 0;
+        break;
+    }
+    GemmDesc g{dt, dA, K, dW, K, M, N, K, x};
+    if (e.skinny) {
+      g.frag_ks = fks;
+      g.frag_ks0 = 0;
+    }
+    const GemmPlan p = plan_gemm(g);
+    Scratch s;
+    if (p.scratch_floats) {
+      VLA_TRY(dalloc(p.scratch_floats * 4, (void**)&s.ptr));
+      s.floats = p.scratch_floats;
+    }
+    if (kind == VLA_DEBUG_EPI_RESID_NORM) {
+      g.epi.out = s.ptr;
+      g.epi.ldo = (int)std::min<size_t>(s.floats, (size_t)INT32_MAX);
+    }
+    if (e.plan_out) {
+      plan_tile(g, p, &e.plan_out[0], &e.plan_out[1]);
+      e.plan_out[2] = p.splits;
+    }
+    HIP_TRY(hipDeviceSynchronize());
+    hipError_t err = launch_gemm(g, s, LaunchCaps{}, st);
+    if (err != hipSuccess) return fail(VLA_EHIP, std::string("gemm: ") + hipGetErrorString(err));
+    if (kind == VLA_DEBUG_EPI_RESID_NORM) {
+      NormDesc n;
+      n.dtype = dt;
+      n.x = e.resid;
+      n.ldx = N;
+      n.rows = M;
+      n.d = N;
+      n.part = s.ptr;
+      n.splits = p.splits;
+      n.g = e.gain;
+      n.rms = 1;
+      n.out = dout;
+      n.ldo = N;
+      n.afrag = e.skinny ? 1 : 0;
+      err = launch_norm(n, st);
+      if (err != hipSuccess) return fail(VLA_EHIP, std::string("norm: ") + hipGetErrorString(err));
+    }
+    HIP_TRY(hipStreamSynchronize(st));
+    // outputs back to the caller's row-major buffers
+    if (op_out) {
+      std::vector<uint8_t> img(oel * esz), rm((size_t)M * ocols * esz);
+      HIP_TRY(hipMemcpy(img.data(), dout, img.size(), hipMemcpyDeviceToHost));
+      for (int mm = 0; mm < M; ++mm)
+        for (int c = 0; c < ocols; ++c) {
+          const size_t at = e.skinny ? afrag_index(dt, mm, c) : (size_t)mm * ocols + c;
+          std::memcpy(&rm[((size_t)mm * ocols + c) * esz], &img[at * esz], esz);
+        }
+      HIP_TRY(hipMemcpy(e.out, rm.data(), rm.size(), hipMemcpyHostToDevice));
+    }
+    if (qkv) {
+      const int kvd = e.nkv * e.hd;
+      std::vector<uint8_t> ki(kv_kelems(dt, kv_nb, e.hd, e.nkv) * esz), vi(kv_velems(dt, kv_nb, e.hd, e.nkv) * esz);
+      std::vector<uint8_t> kr((size_t)M * kvd * esz), vr((size_t)M * kvd * esz);
+      HIP_TRY(hipMemcpy(ki.data(), dk, ki.size(), hipMemcpyDeviceToHost));
+      HIP_TRY(hipMemcpy(vi.data(), dv, vi.size(), hipMemcpyDeviceToHost));
+      for (int mm = 0; mm < M; ++mm)
+        for (int j = 0; j < e.nkv; ++j)
+          for (int d = 0; d < e.hd; ++d) {
+            const size_t o = ((size_t)mm * kvd + j * e.hd + d) * esz;
+            std::memcpy(&kr[o], &ki[kv_kidx(dt, kv_nb, e.hd, j, mm, d) * esz], esz);
+            std::memcpy(&vr[o], &vi[kv_vidx(dt, kv_nb, e.hd, j, mm, d) * esz], esz);
+          }
+      HIP_TRY(hipMemcpy(e.k_out, kr.data(), kr.size(), hipMemcpyHostToDevice));
+      HIP_TRY(hipMemcpy(e.v_out, vr.data(), vr.size(), hipMemcpyHostToDevice));
+    }
     return VLA_OK;
   })
 }

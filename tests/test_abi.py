@@ -83,7 +83,7 @@ def test_null_arguments_are_errors_not_crashes():
     assert lib.vla_debug_gemm(0, 4, 4, 7, None, 8, None, 8, None, None, None) == -1
 
 
-@pytest.mark.parametrize("struct", ["vla_config", "vla_frame", "vla_sched", "vla_timing"])
+@pytest.mark.parametrize("struct", ["vla_config", "vla_frame", "vla_sched", "vla_timing", "vla_debug_epi"])
 def test_binding_structs_match_header(struct):
     """The ctypes structures pass the header's fields in the header's order
     and types (a field added on one side only would shift every later one)."""

@@ -197,34 +197,60 @@ PHASE_CFGS = [
 ]
 
 
-def sampler_gain(cfg):
-    """How much an error in the head's output can grow by the end of the
-    chunk, relative to Euler steps (where the N errors are each scaled by
-    1/N: total 1). DDIM step k scales an error in eps by |b_k| and every later
-    step multiplies the state by a_j, so the bound is
-    sum_k |b_k| prod_{j>k} |a_j| (~157 from abar_999 to 1: 1/sqrt(abar_999))."""
-    if cfg.get("sampler", 0) != synth.SAMPLER_DDIM:
-        return 1.0
-    _, _, ab = O.ddim_schedule(cfg["n_steps"])
-    n = cfg["n_steps"]
-    a = [np.sqrt(ab[k + 1] / ab[k]) for k in range(n)]
-    b = [np.sqrt(1 - ab[k + 1]) - a[k] * np.sqrt(1 - ab[k]) for k in range(n)]
-    return float(sum(abs(b[k]) * np.prod([abs(a[j]) for j in range(k + 1, n)]) for k in range(n)))
+# bf16 DDIM chunks: the bound is relative to the chunk's magnitude (see
+# chunk_bound).
+DDIM_BF16_REL = 5e-3
 
 
-def _kv_tol(cfg, ref):
+def chunk_bound(cfg, want):
+    """Max abs error allowed on an action chunk against the oracle.
+
+    Euler steps: 1e-4 in fp32, 2e-2 in bf16. DDIM in fp32: 1e-4 as well.
+    DDIM in bf16: relative to the chunk. DDIM's last step divides the state
+    by sqrt(abar_999) = 1/157, so the chunk is about 157 times the noise's
+    scale (max |chunk| ~ 390 at tiny sizes), and an error in the head's output
+    grows by sum_k |b_k| prod_{j>k} |a_j| ~ 157 as well: |err| <=
+    DDIM_BF16_REL * max |want| (the Euler bf16 bound is ~0.7% of max |chunk|
+    at full size)."""
+    if cfg.get("sampler", 0) == synth.SAMPLER_DDIM and cfg["dtype"] == synth.BF16:
+        return DDIM_BF16_REL * float(np.abs(want).max())
+    return CHUNK_TOL[cfg["dtype"]]
+
+
+# Intermediate (K / V cache, cross K / V) bounds in bf16; see _kv_check.
+KV_REL_BF16 = 2.0 ** -3
+KV_L2_BF16 = 0.04
+
+
+def _kv_check(cfg, tag, got, ref, depth=1.0):
+    """An intermediate tensor against the oracle. fp32: 1e-4 absolute.
+
+    bf16: both sides store K / V in bf16 and round every operand at the same
+    points; fp32-vs-fp64 accumulation flips single roundings by one bf16 ulp
+    (2^-8 relative) and those flips travel through every earlier layer (up to
+    27 ViT + 18 LM layers), so an element's deviation scales with the
+    tensor's magnitude as well as its own. Two bounds:
+      * pointwise, |got - ref| <= KV_REL_BF16 (|ref| + rms(ref)) (observed
+        worst 0.075, pi0-shaped LM layer 15 of 18);
+      * aggregate, ||got - ref||_2 / ||ref||_2 <= KV_L2_BF16 sqrt(depth),
+        depth = (l + 1) / L for LM layer l of L (cross K / V: 1), since the
+        flips add up like a random walk over the layers (observed at full
+        size: 0.0056 at layer 0 rising to 0.0165 at layer 17 of the
+        pi0-shaped LM, 0.0049 .. 0.011 in the GR00T-shaped one). A
+        systematic error of a few percent on a share of the elements (a wrong
+        RoPE frequency on some head dims, say) shows up here, not in the
+        pointwise bound.
+    Both observed figures are printed for every tensor."""
+    err = np.abs(got - ref)
     if cfg["dtype"] == synth.F32:
-        return 1e-4
-    # Both sides store K/V in bf16 and round every operand at the same
-    # points; fp32-vs-fp64 accumulation differences flip roundings by one
-    # bf16 ulp (2^-8 relative) and those flips travel through every earlier
-    # layer (27 ViT + 18 LM layers at full size), growing like a random walk
-    # with depth. So an element's deviation scales with the tensor's
-    # magnitude rather than its own: the intermediate bound is 2^-3 of
-    # (|value| + rms), a diagnostic that still catches a structural mistake
-    # (which moves elements by ~ the rms); the contract is the chunk bound.
+        assert np.all(err <= 1e-4), (tag, float(err.max()))
+        return
     rms = float(np.sqrt(np.mean(np.square(ref))))
-    return 2.0 ** -3 * (np.abs(ref) + rms)
+    ratio = float((err / (np.abs(ref) + rms)).max())
+    rel_l2 = float(np.sqrt(np.sum(np.square(got - ref)) / np.sum(np.square(ref))))
+    print(f"[gpu] kv-ratio {tag} {ratio:.3e} rel-l2 {rel_l2:.3e} max|d|/rms {float(err.max()) / rms:.3e}", flush=True)
+    assert ratio <= KV_REL_BF16, (tag, ratio)
+    assert rel_l2 <= KV_L2_BF16 * np.sqrt(depth), (tag, rel_l2)
 
 
 @pytest.mark.parametrize("name,cfg", PHASE_CFGS, ids=[p[0] for p in PHASE_CFGS])
@@ -239,15 +265,26 @@ def test_phases_vs_oracle(V, name, cfg):
         got, kv = g.run_frame(m, cfg, fr)
         got2, _ = g.run_frame(m, cfg, fr)
     assert np.array_equal(got, got2), "not deterministic"
-    nkvd = cfg["lm_kv_heads"] * cfg["head_dim"]
-    for l, (k, v) in enumerate(kv):
-        rk = cap["kv"][l][0].reshape(-1, nkvd).ravel()
-        rv = cap["kv"][l][1].reshape(-1, nkvd).ravel()
-        assert np.all(np.abs(k - rk) <= _kv_tol(cfg, rk)), (l, float(np.abs(k - rk).max()))
-        assert np.all(np.abs(v - rv) <= _kv_tol(cfg, rv)), (l, float(np.abs(v - rv).max()))
+    _check_cache(cfg, name, kv, cap)
     err = float(np.abs(got - want).max())
-    print(f"[gpu] {name}: chunk max abs err {err:.3e}", flush=True)
-    assert err <= CHUNK_TOL[cfg["dtype"]] * sampler_gain(cfg)
+    print(f"[gpu] {name}: chunk max abs err {err:.3e} (max|chunk| {float(np.abs(want).max()):.3e})", flush=True)
+    assert err <= chunk_bound(cfg, want)
+
+
+def _check_cache(cfg, name, kv, cap, cross=None):
+    """Every LM layer's K and V (and every cross layer's K and V of a DiT
+    head) against the oracle's."""
+    nkvd = cfg["lm_kv_heads"] * cfg["head_dim"]
+    assert len(kv) == cfg["lm_layers"]
+    L = cfg["lm_layers"]
+    for l, (k, v) in enumerate(kv):
+        _kv_check(cfg, f"{name} lm.{l}.k", k, cap["kv"][l][0].reshape(-1, nkvd).ravel(), (l + 1) / L)
+        _kv_check(cfg, f"{name} lm.{l}.v", v, cap["kv"][l][1].reshape(-1, nkvd).ravel(), (l + 1) / L)
+    if cross is not None:
+        assert sorted(cross) == sorted(cap["cross_kv"])
+        for l, (k, v) in cross.items():
+            _kv_check(cfg, f"{name} cross.{l}.k", k, cap["cross_kv"][l][0].ravel())
+            _kv_check(cfg, f"{name} cross.{l}.v", v, cap["cross_kv"][l][1].ravel())
 
 
 @pytest.mark.timeout(900)
@@ -287,13 +324,35 @@ def test_pi0_full_size_vs_oracle(V):
     err_b = float(np.abs(b4[0] - want).max())
     print(f"[gpu] pi0 batched-loop chunk max abs err {err_b:.3e}", flush=True)
     assert err_b <= CHUNK_TOL[synth.BF16]
-    nkvd = cfg["lm_kv_heads"] * cfg["head_dim"]
-    for l in (0, cfg["lm_layers"] - 1):
-        rk = cap["kv"][l][0].reshape(-1, nkvd).ravel()
-        assert np.all(np.abs(kv[l][0] - rk) <= _kv_tol(cfg, rk)), l
+    _check_cache(cfg, "pi0", kv, cap)
     err = float(np.abs(got - want).max())
     print(f"[gpu] pi0 chunk max abs err {err:.3e}", flush=True)
     assert err <= CHUNK_TOL[synth.BF16]
+
+
+@pytest.mark.timeout(900)
+def test_pi0_ddim_full_size_vs_oracle(V):
+    """The pi0-shaped model sampled with 10 DDIM steps at its real sizes:
+    frames 0 and 1 of seed 0 from the standalone calls and from one batched
+    action loop of both (the tiled GEMMs), against the oracle under the
+    relative DDIM bound."""
+    g = G()
+    cfg = synth.PI0_DDIM
+    g.say("pi0_ddim full size: GPU")
+    frs = [synth.make_frame(cfg, 0, r) for r in range(2)]
+    with g.model(cfg, 0) as m:
+        one = [g.run_frame(m, cfg, f)[0] for f in frs]
+        g.say("pi0_ddim full size: pipeline, both frames in one prefill and one action loop")
+        b2 = _pipeline_frames(g, m, cfg, frs, vlm_batch=2, act_batch=2, act_streams=1)
+    g.say("pi0_ddim full size: oracle")
+    P = synth.make_params(cfg, 0)
+    for r in range(2):
+        want = O.forward(P, cfg, frs[r])
+        err, err_b = float(np.abs(one[r] - want).max()), float(np.abs(b2[r] - want).max())
+        print(f"[gpu] pi0_ddim frame {r}: chunk max abs err {err:.3e}, batched loop {err_b:.3e}, "
+              f"max|chunk| {float(np.abs(want).max()):.3e}", flush=True)
+        assert err <= chunk_bound(cfg, want)
+        assert err_b <= chunk_bound(cfg, want)
 
 
 def _pipeline_frames(g, m, cfg, frames, **kw):
@@ -333,10 +392,7 @@ def test_pi0_three_views_full_size_vs_oracle(V):
     P = synth.make_params(cfg, 0)
     cap = {}
     want = O.forward(P, cfg, frames[0], cap)
-    nkvd = cfg["lm_kv_heads"] * cfg["head_dim"]
-    for l in (0, cfg["lm_layers"] - 1):
-        rk = cap["kv"][l][0].reshape(-1, nkvd).ravel()
-        assert np.all(np.abs(kv[l][0] - rk) <= _kv_tol(cfg, rk)), l
+    _check_cache(cfg, "pi0_3view", kv, cap)
     err = float(np.abs(got - want).max())
     err_b = float(np.abs(batched[0] - want).max())
     print(f"[gpu] pi0 three views chunk max abs err {err:.3e} (batched loop {err_b:.3e})", flush=True)
@@ -367,13 +423,7 @@ def test_gr00t_full_size_vs_oracle(V):
     P = synth.make_params(cfg, 0)
     cap = {}
     want = O.forward(P, cfg, fr, cap)
-    nkvd = cfg["lm_kv_heads"] * cfg["head_dim"]
-    for l in (0, cfg["lm_layers"] - 1):
-        rk = cap["kv"][l][0].reshape(-1, nkvd).ravel()
-        assert np.all(np.abs(kv[l][0] - rk) <= _kv_tol(cfg, rk)), l
-    for l in (0, cfg["ex_layers"] - 2):
-        rv = cap["cross_kv"][l][1].ravel()
-        assert np.all(np.abs(cross[l][1] - rv) <= _kv_tol(cfg, rv)), ("cross", l)
+    _check_cache(cfg, "gr00t", kv, cap, cross)
     err = float(np.abs(got - want).max())
     print(f"[gpu] gr00t chunk max abs err {err:.3e}", flush=True)
     assert err <= CHUNK_TOL[synth.BF16]
@@ -404,21 +454,10 @@ def test_dit_phases_vs_oracle(V, name, cfg):
         got, kv = g.run_frame(m, cfg, fr, cross=cross)
         got2, _ = g.run_frame(m, cfg, fr)
     assert np.array_equal(got, got2), "not deterministic"
-    nkvd = cfg["lm_kv_heads"] * cfg["head_dim"]
-    for l, (k, v) in enumerate(kv):
-        rk = cap["kv"][l][0].reshape(-1, nkvd).ravel()
-        rv = cap["kv"][l][1].reshape(-1, nkvd).ravel()
-        assert np.all(np.abs(k - rk) <= _kv_tol(cfg, rk)), ("lm", l, float(np.abs(k - rk).max()))
-        assert np.all(np.abs(v - rv) <= _kv_tol(cfg, rv)), ("lm", l, float(np.abs(v - rv).max()))
-    assert sorted(cross) == sorted(cap["cross_kv"])
-    for l, (k, v) in cross.items():
-        rk = cap["cross_kv"][l][0].ravel()
-        rv = cap["cross_kv"][l][1].ravel()
-        assert np.all(np.abs(k - rk) <= _kv_tol(cfg, rk)), ("cross", l, float(np.abs(k - rk).max()))
-        assert np.all(np.abs(v - rv) <= _kv_tol(cfg, rv)), ("cross", l, float(np.abs(v - rv).max()))
+    _check_cache(cfg, name, kv, cap, cross)
     err = float(np.abs(got - want).max())
     print(f"[gpu] {name}: chunk max abs err {err:.3e}", flush=True)
-    assert err <= CHUNK_TOL[cfg["dtype"]] * sampler_gain(cfg)
+    assert err <= chunk_bound(cfg, want)
 
 
 @pytest.mark.parametrize("cfg", [synth.micro(synth.BF16), synth.TINY, synth.micro_dit(synth.BF16),
@@ -517,9 +556,9 @@ def test_pipeline_modes_bit_identical(V, cfg):
     P = synth.make_params(cfg, 11)
     for i in (0, R - 1):
         want = O.forward(P, cfg, frames[i])
-        assert np.abs(ref[i] - want).max() <= CHUNK_TOL[cfg["dtype"]]
+        assert np.abs(ref[i] - want).max() <= chunk_bound(cfg, want)
         if bref is not None:
-            assert np.abs(bref[i] - want).max() <= CHUNK_TOL[cfg["dtype"]]
+            assert np.abs(bref[i] - want).max() <= chunk_bound(cfg, want)
 
 
 def test_abi_errors_on_device(V):
@@ -588,6 +627,6 @@ def test_async_inference_chunks(V, cfg):
     P = synth.make_params(cfg, 5)
     for r, j in ((0, 1), (R - 1, k - 1)):
         ref = O.forward(P, cfg, dict(frames[r], noise=noise_np[r * k + j]))
-        assert np.abs(want[r * k + j] - ref).max() <= CHUNK_TOL[cfg["dtype"]]
+        assert np.abs(want[r * k + j] - ref).max() <= chunk_bound(cfg, ref)
         if bref is not None:
-            assert np.abs(bref[r * k + j] - ref).max() <= CHUNK_TOL[cfg["dtype"]]
+            assert np.abs(bref[r * k + j] - ref).max() <= chunk_bound(cfg, ref)
