@@ -101,11 +101,21 @@ struct TT<uint16_t> {
   static __device__ __forceinline__ void st(uint16_t* p, float v) { *p = f2bf(v); }
 };
 
-__device__ __forceinline__ float gelu_tanh(float x) {
-  const float c = 0.7978845608028654f;  // sqrt(2 / pi)
-  return 0.5f * x * (1.f + tanhf(c * (x + 0.044715f * x * x * x)));
+// x / (1 + e^-z) with the hardware exp2 and reciprocal (about 1 ulp each):
+// e^-z = 2^(-z log2 e). For z below about -88 the exponential overflows to
+// +inf and the result is -0 or +0, the limit.
+__device__ __forceinline__ float x_sigmoid(float x, float z) {
+  const float e = __builtin_amdgcn_exp2f(-1.4426950408889634f * z);
+  return x * __builtin_amdgcn_rcpf(1.f + e);
 }
-__device__ __forceinline__ float swishf(float x) { return x / (1.f + expf(-x)); }
+// GELU, tanh form: 0.5 x (1 + tanh(u)) with u = sqrt(2/pi) (x + 0.044715 x^3);
+// since 0.5 (1 + tanh(u)) = 1 / (1 + e^(-2u)) exactly, it is x sigmoid(2u).
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float c2 = 1.5957691216057308f;  // 2 sqrt(2 / pi)
+  const float x2 = x * x;
+  return x_sigmoid(x, c2 * __builtin_fmaf(0.044715f * x2, x, x));
+}
+__device__ __forceinline__ float swishf(float x) { return x_sigmoid(x, x); }
 
 // One MFMA step over a 16-byte slice of K per lane (8 bf16 or 4 fp32).
 __device__ __forceinline__ f32x4 mfma_step(uint4 a, uint4 b, f32x4 c, uint16_t) {
@@ -693,6 +703,27 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
       if (na < N) ba = e.bias[na];
       if (nb < N) bb = e.bias[nb];
     }
+    // Row-major operand-type outputs of GeGLU, store, GELU and swish take
+    // 8 consecutive output columns per thread and row: one 16-byte store
+    // (two for fp32) instead of eight element stores. Thread tid always owns
+    // the same 8-column chunk (NT is a multiple of the chunks per row), so
+    // its bias is loaded once per tile.
+    const bool geglu = ek == EPI_GEGLU;
+    const bool vec8 = fast && !e.afrag && e.blk_rows == 0 &&
+                      (geglu || ek == EPI_T || ek == EPI_GELU || ek == EPI_SWISH) &&
+                      (((uintptr_t)e.out & 15) == 0) && (e.ldo % 8 == 0);
+    constexpr int OC8_G = BN / 16, OC8_T = BN / 8;  // 8-column chunks per row (GeGLU, others)
+    static_assert(NT % OC8_T == 0, "fixed output chunk per thread");
+    const int oc8 = geglu ? OC8_G : OC8_T;
+    const int c8 = tid % oc8;
+    float bv[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) bv[k] = 0.f;
+    if (vec8 && !geglu && e.bias) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+        if (n0 + c8 * 8 + k < N) bv[k] = e.bias[n0 + c8 * 8 + k];
+    }
     auto slice = [&](auto ic) {
       const int i = ic;
       __syncthreads();
@@ -702,7 +733,72 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
         for (int r = 0; r < 4; ++r)
           sm.c[(wm * 16 + (lane >> 4) * 4 + r) * CLD + wn * WN + j * 16 + (lane & 15)] = acc[i][j][r];
       __syncthreads();
-      if (fast) {
+      if (vec8) {
+        const int chunks = WGM * 16 * oc8;
+        for (int q = tid; q < chunks; q += NT) {
+          const int row = q / oc8;
+          const int m = m0 + (row >> 4) * WM + i * 16 + (row & 15);
+          if (m >= M) continue;
+          const float* cr = sm.c + row * CLD;
+          float o[8];
+          int col0, total;
+          if (geglu) {
+            // output column 16 g + j is gate column 32 g + j and up column
+            // 32 g + 16 + j of the tile
+            const int j0 = c8 * 8, g0 = 32 * (j0 >> 4) + (j0 & 15);
+            const float4 ga = *(const float4*)(cr + g0), gb = *(const float4*)(cr + g0 + 4);
+            const float4 ua = *(const float4*)(cr + g0 + 16), ub = *(const float4*)(cr + g0 + 20);
+            o[0] = gelu_tanh(ga.x) * ua.x;
+            o[1] = gelu_tanh(ga.y) * ua.y;
+            o[2] = gelu_tanh(ga.z) * ua.z;
+            o[3] = gelu_tanh(ga.w) * ua.w;
+            o[4] = gelu_tanh(gb.x) * ub.x;
+            o[5] = gelu_tanh(gb.y) * ub.y;
+            o[6] = gelu_tanh(gb.z) * ub.z;
+            o[7] = gelu_tanh(gb.w) * ub.w;
+            col0 = n0 / 2 + j0;
+            total = N / 2;
+          } else {
+            const int c0 = c8 * 8;
+            const float4 va = *(const float4*)(cr + c0), vb = *(const float4*)(cr + c0 + 4);
+            o[0] = va.x + bv[0];
+            o[1] = va.y + bv[1];
+            o[2] = va.z + bv[2];
+            o[3] = va.w + bv[3];
+            o[4] = vb.x + bv[4];
+            o[5] = vb.y + bv[5];
+            o[6] = vb.z + bv[6];
+            o[7] = vb.w + bv[7];
+            if (ek == EPI_GELU) {
+#pragma unroll
+              for (int k = 0; k < 8; ++k) o[k] = gelu_tanh(o[k]);
+            } else if (ek == EPI_SWISH) {
+#pragma unroll
+              for (int k = 0; k < 8; ++k) o[k] = swishf(o[k]);
+            }
+            col0 = n0 + c0;
+            total = N;
+          }
+          T* dst = (T*)e.out + (size_t)m * e.ldo + col0;
+          if (col0 + 8 <= total) {
+            if constexpr (sizeof(T) == 2) {
+              uint4 w;
+              w.x = f2bf2(o[0], o[1]);
+              w.y = f2bf2(o[2], o[3]);
+              w.z = f2bf2(o[4], o[5]);
+              w.w = f2bf2(o[6], o[7]);
+              *(uint4*)dst = w;
+            } else {
+              *(float4*)dst = make_float4(o[0], o[1], o[2], o[3]);
+              *(float4*)(dst + 4) = make_float4(o[4], o[5], o[6], o[7]);
+            }
+          } else {
+#pragma unroll
+            for (int k = 0; k < 8; ++k)
+              if (col0 + k < total) TT<T>::st(dst + k, o[k]);
+          }
+        }
+      } else if (fast) {
         constexpr int PER = WGM * 16 * (BN / 2) / NT;
         // f(m, v0, v1) for this thread's rows of the slice (same arithmetic
         // as epi_pair)
