@@ -482,6 +482,10 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
   // tiles keeps the row tiles that share a weight block (consecutive tile
   // indices) on one XCD, so the block comes from HBM once. Any bijection of
   // the workgroup index gives the same results.
+  // GeGLU of the direct-load tile into row-major bf16: formed in registers
+  // (see below); uniform over the launch
+  const bool reg_geglu = DL && sizeof(T) == 2 && splits == 1 && e.kind == EPI_GEGLU && !e.afrag &&
+                         e.blk_rows == 0 && (((uintptr_t)e.out & 15) == 0) && e.ldo % 8 == 0;
   const int G = gridDim.x;
   const int first = G % 8 == 0 ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
   const int plane = tiles_m * tiles_n;
@@ -582,6 +586,47 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
           __syncthreads();
         }
       }
+      // GeGLU straight from the accumulators: gate column n (n % 32 < 16)
+      // and its up column n + 16 sit in tiles j = 2g and 2g + 1 of the same
+      // lane, so each lane forms its outputs in registers. The bf16 tile
+      // (BM x BN/2) is staged once in LDS, wave row 0 in stage 0 and wave
+      // row 1 in stage 1 (rows padded to OLD elements, so the four row
+      // groups of one store hit different banks), then every thread stores
+      // 16-byte runs of 8 output columns. After the K loop's last barrier
+      // no stage is read any more.
+      if (reg_geglu) {
+        constexpr int OLD = BN / 2 + 8;
+        static_assert(WGM == 2 && BM / 2 * OLD <= (BM + BN) * BK, "staging fits a stage");
+        static_assert(TN % 2 == 0, "gate / up tiles in one wave");
+        uint16_t* ob = (uint16_t*)(wm == 0 ? d0 : d1);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int g = 0; g < TN / 2; ++g)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              const int lrow = i * 16 + (lane >> 4) * 4 + r;
+              const int ocol = wn * (WN / 2) + 16 * g + (lane & 15);
+              ob[lrow * OLD + ocol] = f2bf(gelu_tanh(acc[i][2 * g][r]) * acc[i][2 * g + 1][r]);
+            }
+        __syncthreads();
+        constexpr int CPR = BN / 16;  // 16-byte chunks per output row
+        const int ncols = N / 2, c00 = n0 / 2;
+#pragma unroll
+        for (int k = 0; k < BM * CPR / NT; ++k) {
+          const int q = tid + k * NT, row = q / CPR, c = q % CPR;
+          const int m = m0 + row;
+          const int col0 = c00 + c * 8;
+          if (m >= M || col0 >= ncols) continue;
+          const uint16_t* src = (const uint16_t*)(row < BM / 2 ? d0 : d1) + (row % (BM / 2)) * OLD + c * 8;
+          uint16_t* dst = (uint16_t*)e.out + (size_t)m * e.ldo + col0;
+          if (col0 + 8 <= ncols) {
+            *(uint4*)dst = *(const uint4*)src;
+          } else {
+            for (int t = 0; t < ncols - col0; ++t) dst[t] = src[t];
+          }
+        }
+      }
     } else {
       auto compute = [&](int buf) {
         const T* sa = sm.ld.a[buf];
@@ -676,6 +721,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
 
     }
 
+    if (reg_geglu) continue;  // stored above
     // epilogue in 16-row slices: slice i of every wave row goes through LDS,
     // then all threads apply the epilogue with row-contiguous stores
     float* P = (e.kind == EPI_PART ? (float*)e.out : part) + (size_t)s * M * N;
