@@ -35,7 +35,12 @@ cache; ``head == 1`` is a GR00T-style DiT whose even layers cross-attend to
 the LM's final normalised hidden states (the features) and whose odd layers
 self-attend, conditioned on the flow time through adaLN. The DiT config also
 pixel-shuffles the ViT grid 2x2 before the projector and runs every LM layer
-(the features need the last layer's output).
+(the features need the last layer's output). ``head == 2`` is a
+CogACT-style diffusion head: a learned cognition token is appended to the
+prefix, every LM layer runs, and the token's final normalised output,
+projected to the head's width, conditions a DiT of self-attention layers in
+context (with a time token); the head's output is the noise estimate of DDIM
+steps.
 """
 from __future__ import annotations
 
@@ -291,13 +296,16 @@ def image_tokens(P, cfg, pixels):
 
 
 def prefix(P, cfg, frame, img=None):
-    """LM input rows: [image tokens; E[ids] * sqrt(d_lm); W_s state + b_s]."""
+    """LM input rows: [image tokens; E[ids] * sqrt(d_lm); W_s state + b_s];
+    the cognition-token head appends its learned token row (unscaled)."""
     if img is None:
         img = image_tokens(P, cfg, frame["pixels"])
     rows = [img, _w(P, "lm.embed")[np.asarray(frame["ids"], dtype=np.int64)] * math.sqrt(cfg["lm_dim"])]
     if cfg["state_dim"] > 0:
         s = _op(np.asarray(frame["state"], np.float64)[None, :], cfg)
         rows.append(linear(s, _w(P, "state.w"), _w(P, "state.b")))
+    if cfg.get("head", 0) == 2:
+        rows.append(_w(P, "lm.cog"))
     return np.concatenate(rows, axis=0)
 
 
@@ -388,6 +396,9 @@ def vlm_prefill(P, cfg, frame, capture: Optional[dict] = None):
     if cfg.get("head", 0) == 1:
         feats, cache = lm_features(P, cfg, x0)
         out = dit_cross_kv(P, cfg, feats)
+    elif cfg.get("head", 0) == 2:
+        feats, cache = lm_features(P, cfg, x0)
+        out = cognition(P, cfg, feats)
     else:
         cache = lm_prefill(P, cfg, x0)
         out = cache
@@ -397,8 +408,17 @@ def vlm_prefill(P, cfg, frame, capture: Optional[dict] = None):
         capture["kv"] = cache
         if feats is not None:
             capture["features"] = feats
-            capture["cross_kv"] = out
+            capture["cog" if cfg.get("head", 0) == 2 else "cross_kv"] = out
     return out
+
+
+def cognition(P, cfg, feats):
+    """Hand-off of the cognition-token head (Section 2.1: CogACT's phase 1
+    output is a cognition feature): the features' last row, the learned
+    cognition token's final normalised output, projected to the head's width:
+    c = W_c f + b_c, [ex_dim]."""
+    f = _op(feats[-1:], cfg)
+    return linear(f, _w(P, "cog.w"), _w(P, "cog.b"))[0]
 
 
 # ---------------------------------------------------------------------------
@@ -475,13 +495,51 @@ def dit_velocity(P, cfg, cross, x, t):
     return linear(h, _w(P, "ex.out.w"), _w(P, "ex.out.b"))
 
 
+def cog_time_token(P, cfg, t):
+    """The time token of the cognition-token head: W_t2 swish(W_t1 phi_256(t)
+    + b_t1) + b_t2 (the DiT's timestep embedder without the final swish)."""
+    phi = _op(sinusoid(t, P["ex.time1.w"].shape[1])[None, :], cfg)
+    hid = _op(swish(linear(phi, _w(P, "ex.time1.w"), _w(P, "ex.time1.b"))), cfg)
+    return linear(hid, _w(P, "ex.time2.w"), _w(P, "ex.time2.b"))[0]
+
+
+def cog_velocity(P, cfg, cog, x, t):
+    """Output of the cognition-token head (a DiT of self-attention layers,
+    conditioned in context): the sequence [action tokens (W_a x + b_a + fixed
+    sinusoid positions); the cognition vector; the time token] runs through
+    pre-LN layers X += W_o MHA(LN1 X) (no mask, no biases), X += W_2 GELU(W_1
+    LN2 X); the action rows' final LayerNorm, then W_out . + b_out. With the
+    DDIM sampler this is the noise estimate."""
+    hlen, de, nh = x.shape[0], cfg["ex_dim"], cfg["ex_heads"]
+    hd = de // nh
+    act = linear(_op(x, cfg), _w(P, "ex.in.w"), _w(P, "ex.in.b")) + positions_sinusoid(hlen, de)
+    X = np.concatenate([act, np.asarray(cog, np.float64)[None, :], cog_time_token(P, cfg, t)[None, :]], axis=0)
+    s = X.shape[0]
+    for l in range(cfg["ex_layers"]):
+        p = f"ex.{l}."
+        h = _op(layer_norm(X, _w(P, p + "ln1.g"), _w(P, p + "ln1.b")), cfg)
+        q = _op(linear(h, _w(P, p + "q.w")), cfg).reshape(s, nh, hd)
+        k = _op(linear(h, _w(P, p + "k.w")), cfg).reshape(s, nh, hd)
+        v = _op(linear(h, _w(P, p + "v.w")), cfg).reshape(s, nh, hd)
+        a = _op(attention(q, k, v).reshape(s, de), cfg)
+        X = X + linear(a, _w(P, p + "o.w"))
+        h2 = _op(layer_norm(X, _w(P, p + "ln2.g"), _w(P, p + "ln2.b")), cfg)
+        f = _op(gelu_tanh(linear(h2, _w(P, p + "fc1.w"))), cfg)
+        X = X + linear(f, _w(P, p + "fc2.w"))
+    h = _op(layer_norm(X[:hlen], _w(P, "ex.final.g"), _w(P, "ex.final.b")), cfg)
+    return linear(h, _w(P, "ex.out.w"), _w(P, "ex.out.b"))
+
+
 def action_denoise(P, cfg, cache, noise):
     """Euler integration of the head's velocity from x_0 = noise (t = 1) to
     t = 0, or DDIM steps with the head's output as the noise estimate
     (cfg["sampler"] == 1); returns the action chunk [chunk_len, action_dim].
-    ``cache`` is the phase-1 hand-off (KV cache, or the DiT's cross K/V)."""
+    ``cache`` is the phase-1 hand-off (KV cache, the DiT's cross K/V, or the
+    cognition vector)."""
     if cfg.get("head", 0) == 1:
         vel = lambda x, t: dit_velocity(P, cfg, cache, x, t)
+    elif cfg.get("head", 0) == 2:
+        vel = lambda x, t: cog_velocity(P, cfg, cache, x, t)
     else:
         vel = lambda x, t: expert_velocity(P, cfg, cache, x, t)
     if cfg.get("sampler", 0) == 1:

@@ -177,7 +177,7 @@ CONFIG_FIELDS = (
 
 #: Action-head families: the pi0-style expert that shares the LM's KV cache,
 #: and the GR00T-style DiT that cross-attends to the LM's final features.
-HEAD_PI0, HEAD_DIT = 0, 1
+HEAD_PI0, HEAD_DIT, HEAD_COG = 0, 1, 2
 #: Samplers: flow-matching Euler steps, or deterministic DDIM steps with the
 #: head's output read as the noise estimate.
 SAMPLER_EULER, SAMPLER_DDIM = 0, 1
@@ -254,8 +254,40 @@ TINY_DIT = _cfg(dtype=F32, n_views=1, img_h=128, img_w=128, patch=16,
 TINY_DDIM = dict(TINY, sampler=SAMPLER_DDIM)
 PI0_DDIM = dict(PI0, sampler=SAMPLER_DDIM)
 
+#: CogACT-shaped VLA: the PaliGemma-shaped VLM with a learned cognition token
+#: appended to the prefix (48 text tokens, no state; prefix 305), every LM
+#: layer run; its final normalised output row, projected to the head's
+#: width, conditions a 300M-parameter DiT-L-shaped diffusion head (24
+#: self-attention layers, d = 1024, 16 heads of 64, MLP 4096) that predicts
+#: the noise of a 16 x 7 chunk over 10 DDIM steps.
+COGACT = _cfg(dtype=BF16, n_views=1, img_h=224, img_w=224, patch=14,
+              vit_dim=1152, vit_heads=16, vit_mlp=4304, vit_layers=27,
+              lm_dim=2048, lm_heads=8, lm_kv_heads=1, head_dim=256, lm_mlp=16384, lm_layers=18,
+              vocab=1024, n_text=48, state_dim=0,
+              ex_dim=1024, ex_mlp=4096, ex_layers=24, chunk_len=16, action_dim=7, n_steps=10,
+              head=HEAD_COG, ex_heads=16, sampler=SAMPLER_DDIM)
+
+#: The cognition-token head at tiny sizes (fp32).
+TINY_COG = _cfg(dtype=F32, n_views=1, img_h=128, img_w=128, patch=16,
+                vit_dim=256, vit_heads=4, vit_mlp=1024, vit_layers=2,
+                lm_dim=256, lm_heads=4, lm_kv_heads=1, head_dim=64, lm_mlp=1024, lm_layers=2,
+                vocab=1024, n_text=16, state_dim=0,
+                ex_dim=128, ex_mlp=512, ex_layers=2, chunk_len=8, action_dim=7, n_steps=4,
+                head=HEAD_COG, ex_heads=2, sampler=SAMPLER_DDIM)
+
+
+def micro_cog(dtype: int = F32) -> Dict[str, int]:
+    """Smallest cognition-token model: one LM layer, two head layers of width 64."""
+    return _cfg(dtype=dtype, n_views=1, img_h=32, img_w=32, patch=8,
+                vit_dim=64, vit_heads=2, vit_mlp=136, vit_layers=1,
+                lm_dim=64, lm_heads=2, lm_kv_heads=1, head_dim=32, lm_mlp=128, lm_layers=1,
+                vocab=1024, n_text=5, state_dim=0,
+                ex_dim=64, ex_mlp=128, ex_layers=2, chunk_len=5, action_dim=3, n_steps=2,
+                head=HEAD_COG, ex_heads=2, sampler=SAMPLER_DDIM)
+
+
 PRESETS = {"tiny": TINY, "pi0": PI0, "pi0_3view": PI0_3VIEW, "gr00t": GR00T, "tiny_dit": TINY_DIT,
-           "tiny_ddim": TINY_DDIM, "pi0_ddim": PI0_DDIM}
+           "tiny_ddim": TINY_DDIM, "pi0_ddim": PI0_DDIM, "cogact": COGACT, "tiny_cog": TINY_COG}
 
 
 def derived(cfg: Dict[str, int]) -> Dict[str, int]:
@@ -264,7 +296,7 @@ def derived(cfg: Dict[str, int]) -> Dict[str, int]:
     ph, pw = cfg["img_h"] // cfg["patch"], cfg["img_w"] // cfg["patch"]
     t_view = ph * pw
     n_img = cfg["n_views"] * t_view // cfg["shuffle"] ** 2
-    prefix = n_img + cfg["n_text"] + (1 if cfg["state_dim"] > 0 else 0)
+    prefix = n_img + cfg["n_text"] + (1 if cfg["state_dim"] > 0 else 0) + (1 if cfg["head"] == HEAD_COG else 0)
     return {"grid_h": ph, "grid_w": pw, "tokens_per_view": t_view, "n_img": n_img,
             "prefix": prefix, "patch_dim": 3 * cfg["patch"] ** 2,
             "kv_len": prefix + cfg["chunk_len"]}
@@ -332,6 +364,23 @@ def param_specs(cfg: Dict[str, int]) -> List[Tuple[str, Tuple[int, ...], float, 
             w(p + "o.w", (de, de))
             w(p + "fc1.w", (cfg["ex_mlp"], de)); w(p + "fc2.w", (de, cfg["ex_mlp"]))
         w("ex.final.ada.w", (2 * de, de)); w("ex.final.ada.b", (2 * de,))
+        w("ex.out.w", (a, de)); w("ex.out.b", (a,))
+        return out
+    if cfg["head"] == HEAD_COG:
+        g("lm.final.g", dl)
+        w("lm.cog", (1, dl))  # the learned cognition token, appended to the prefix
+        w("cog.w", (de, dl)); w("cog.b", (de,))
+        w("ex.in.w", (de, a)); w("ex.in.b", (de,))
+        w("ex.time1.w", (de, DIT_TIME_DIM)); w("ex.time1.b", (de,))
+        w("ex.time2.w", (de, de)); w("ex.time2.b", (de,))
+        for l in range(cfg["ex_layers"]):
+            p = f"ex.{l}."
+            g(p + "ln1.g", de); w(p + "ln1.b", (de,))
+            w(p + "q.w", (de, de)); w(p + "k.w", (de, de)); w(p + "v.w", (de, de))
+            w(p + "o.w", (de, de))
+            g(p + "ln2.g", de); w(p + "ln2.b", (de,))
+            w(p + "fc1.w", (cfg["ex_mlp"], de)); w(p + "fc2.w", (de, cfg["ex_mlp"]))
+        g("ex.final.g", de); w("ex.final.b", (de,))
         w("ex.out.w", (a, de)); w("ex.out.b", (a,))
         return out
     w("ex.in.w", (de, a)); w("ex.in.b", (de,))

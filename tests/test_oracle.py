@@ -693,3 +693,96 @@ def test_image_tokens_with_pixel_shuffle_vs_torch_assembly():
     assert got.shape == ((gh // s) * (gw // s), cfg["lm_dim"])
     # transformers computes the ViT softmax in fp32, hence 1e-7
     assert np.allclose(got, ref, rtol=1e-7, atol=1e-7)
+
+
+# ------------------------------------------------ cognition-token (CogACT) head
+
+def _cog_torch(P, cfg, cog, x, t):
+    """The cognition-token head assembled from torch modules: pre-LN
+    nn.TransformerEncoderLayer (tanh-GELU, eps 1e-6, linear biases zero, the
+    LayerNorms' own biases loaded), the time token from F.silu and F.linear,
+    F.layer_norm and F.linear on the action rows."""
+    de, nh, mlp, H = cfg["ex_dim"], cfg["ex_heads"], cfg["ex_mlp"], x.shape[0]
+    lin = lambda z, w, b=None: F.linear(z, t64(P[w]), None if b is None else t64(P[b]))
+    half = de // 2
+    ang = torch.arange(H, dtype=torch.float64)[:, None] * 10000.0 ** (-torch.arange(half, dtype=torch.float64) / half)
+    act = lin(t64(x), "ex.in.w", "ex.in.b") + torch.cat([ang.sin(), ang.cos()], 1)
+    phi = t64(O.sinusoid(t, 256))[None]
+    tt = lin(F.silu(lin(phi, "ex.time1.w", "ex.time1.b")), "ex.time2.w", "ex.time2.b")
+    X = torch.cat([act, t64(cog)[None], tt], 0)[None]
+    for l in range(cfg["ex_layers"]):
+        p = f"ex.{l}."
+        layer = torch.nn.TransformerEncoderLayer(de, nh, dim_feedforward=mlp, dropout=0.0,
+                                                 activation=lambda z: F.gelu(z, approximate="tanh"),
+                                                 layer_norm_eps=1e-6, batch_first=True, norm_first=True)
+        layer = layer.double().eval()
+        sd = layer.state_dict()
+        sd["self_attn.in_proj_weight"] = torch.cat([t64(P[p + "q.w"]), t64(P[p + "k.w"]), t64(P[p + "v.w"])], 0)
+        sd["self_attn.in_proj_bias"] = torch.zeros(3 * de, dtype=torch.float64)
+        sd["self_attn.out_proj.weight"] = t64(P[p + "o.w"])
+        sd["self_attn.out_proj.bias"] = torch.zeros(de, dtype=torch.float64)
+        sd["linear1.weight"], sd["linear1.bias"] = t64(P[p + "fc1.w"]), torch.zeros(mlp, dtype=torch.float64)
+        sd["linear2.weight"], sd["linear2.bias"] = t64(P[p + "fc2.w"]), torch.zeros(de, dtype=torch.float64)
+        sd["norm1.weight"], sd["norm1.bias"] = t64(P[p + "ln1.g"]), t64(P[p + "ln1.b"])
+        sd["norm2.weight"], sd["norm2.bias"] = t64(P[p + "ln2.g"]), t64(P[p + "ln2.b"])
+        layer.load_state_dict(sd)
+        X = layer(X)
+    h = F.layer_norm(X[0, :H], (de,), t64(P["ex.final.g"]), t64(P["ex.final.b"]), eps=1e-6)
+    return lin(h, "ex.out.w", "ex.out.b").numpy()
+
+
+def test_cog_velocity_vs_torch_encoder_layers():
+    cfg = dict(synth.micro_cog(), ex_layers=3)
+    P = synth.make_params(cfg, 0)
+    cog, x, t = rnd(cfg["ex_dim"]), rnd(cfg["chunk_len"], cfg["action_dim"]), 0.37
+    got = O.cog_velocity(P, cfg, cog, x, t)
+    with torch.no_grad():
+        ref = _cog_torch(P, cfg, cog, x, t)
+    assert np.allclose(got, ref, rtol=1e-10, atol=1e-10)
+    # the conditioning rows matter: another cognition vector moves the output
+    # (a constant shift would not: every LayerNorm removes it)
+    assert not np.allclose(O.cog_velocity(P, cfg, cog + rnd(cfg["ex_dim"]), x, t), got, atol=1e-6)
+
+
+def test_cog_hand_off_is_the_cognition_rows_projection():
+    """Phase 1 of the cognition-token head: the prefix ends with the learned
+    token (unscaled); the hand-off is W_c (final RMSNorm of a Gemma decoder
+    stack's output at that last row) + b_c."""
+    from transformers.cache_utils import DynamicCache
+    cfg = dict(synth.micro_cog(), lm_layers=2)
+    P = synth.make_params(cfg, 0)
+    fr = synth.make_frame(cfg, 0, 0)
+    cap = {}
+    got = O.vlm_prefill(P, cfg, fr, cap)
+    x0 = cap["prefix"]
+    d = synth.derived(cfg)
+    assert x0.shape[0] == d["prefix"] and np.array_equal(x0[-1], P["lm.cog"][0].astype(np.float64))
+    n, dl = x0.shape[0], cfg["lm_dim"]
+    with torch.no_grad():
+        h = t64(x0)[None]
+        cache = DynamicCache()
+        for l in range(cfg["lm_layers"]):
+            m = _gemma_layer(cfg, P, "lm", l, dl, cfg["lm_mlp"])
+            h = m(h, attention_mask=None, position_ids=torch.arange(n)[None], past_key_values=cache,
+                  use_cache=True, position_embeddings=_rope_tables(cfg["head_dim"], np.arange(n)))
+            h = h[0] if isinstance(h, tuple) else h
+        f = F.rms_norm(h[0, -1:], (dl,), t64(P["lm.final.g"]), eps=1e-6)
+        ref = F.linear(f, t64(P["cog.w"]), t64(P["cog.b"]))[0].numpy()
+    assert got.shape == (cfg["ex_dim"],)
+    assert np.allclose(got, ref, rtol=5e-5, atol=5e-5)
+
+
+def test_cog_zero_out_projection_recovers_x0_with_ddim():
+    """With W_out = 0 the head's noise estimate is the constant b_out; DDIM
+    started from x_T = sqrt(abar_0) x0 + sqrt(1 - abar_0) b_out lands exactly
+    on x0 (deterministic DDIM recovers x0 when the estimate is the true
+    noise), whatever the rest of the model computes."""
+    cfg = synth.micro_cog()
+    P = synth.make_params(cfg, 0)
+    P["ex.out.w"] = np.zeros_like(P["ex.out.w"])
+    fr = synth.make_frame(cfg, 0, 0)
+    x0 = rnd(cfg["chunk_len"], cfg["action_dim"])
+    _, _, abar = O.ddim_schedule(cfg["n_steps"])
+    noise = np.sqrt(abar[0]) * x0 + np.sqrt(1 - abar[0]) * P["ex.out.b"].astype(np.float64)
+    chunk = O.forward(P, cfg, dict(fr, noise=noise))
+    assert np.allclose(chunk, x0, rtol=0, atol=1e-8)
