@@ -62,9 +62,9 @@ typedef struct vla_config {
   int32_t vocab, n_text, state_dim;              /* state_dim 0 = no state token */
   int32_t ex_dim, ex_mlp, ex_layers;             /* ex_layers must equal lm_layers */
   int32_t chunk_len, action_dim, n_steps;        /* action chunk H x A, Euler steps */
-  int32_t head;     /* VLA_HEAD_PI0 or VLA_HEAD_DIT                                  */
+  int32_t head;     /* VLA_HEAD_PI0, VLA_HEAD_DIT or VLA_HEAD_COG                    */
   int32_t shuffle;  /* pixel-shuffle factor of the ViT grid before the projector (1: none) */
-  int32_t ex_heads; /* VLA_HEAD_DIT: attention heads of the DiT (head dim ex_dim / ex_heads) */
+  int32_t ex_heads; /* DiT and cognition heads: attention heads (head dim ex_dim / ex_heads) */
   int32_t sampler;  /* VLA_SAMPLER_EULER or VLA_SAMPLER_DDIM (see below)              */
 } vla_config;
 
@@ -75,6 +75,16 @@ typedef struct vla_config {
  * layers self-attending) reads per-frame cross K/V made from those features. */
 #define VLA_HEAD_PI0 0
 #define VLA_HEAD_DIT 1
+/* VLA_HEAD_COG: the CogACT-style diffusion head (Section 2.1 names CogACT's
+ * head as a 300M DiT fed by cognition features). A learned cognition token
+ * is appended to the prefix (prefix + 1 rows), every LM layer runs, and the
+ * token's final RMS-normalised output, projected to ex_dim (c = W_c f + b_c),
+ * is the hand-off (one fp32 vector per context). The head runs ex_layers
+ * pre-LN self-attention layers (ex_heads heads, no biases, GELU MLP of ex_mlp)
+ * over [chunk_len action tokens; c; a time token], chunk_len <= 62; the final
+ * LayerNorm and the out-projection of the action rows give the head output
+ * (the noise estimate under VLA_SAMPLER_DDIM). */
+#define VLA_HEAD_COG 2
 
 /* Samplers of the action head (Section 2.1 names flow-matching and diffusion
  * heads). EULER: flow matching from noise at t = 1 to data at t = 0, the head
@@ -150,8 +160,12 @@ typedef struct vla_timing {
 } vla_timing;
 
 /* Fill *out with a named preset: "tiny" (fp32, 2+2+2 layers, chunk 8x7,
- * 4 steps), "pi0" (PaliGemma-3B-shaped VLM + pi0-shaped expert, bf16) or
- * "pi0_3view" (pi0 with three camera views and 64 text tokens).
+ * 4 steps), "pi0" (PaliGemma-3B-shaped VLM + pi0-shaped expert, bf16),
+ * "pi0_3view" (pi0 with three camera views and 64 text tokens), "pi0_ddim"
+ * (pi0 sampled with DDIM), "tiny_ddim", "gr00t" (GR00T-shaped VLA with its
+ * DiT head, bf16), "tiny_dit", "cogact" (the PaliGemma-shaped VLM with the
+ * cognition-token head: 24 layers of width 1024, 16 heads, MLP 4096, chunk
+ * 16x7, 10 DDIM steps, bf16) or "tiny_cog" (fp32).
  * VLA_EINVAL for an unknown name or NULL pointers. */
 int vla_preset(const char* name, vla_config* out);
 
@@ -234,6 +248,10 @@ int vla_ctx_export_kv(vla_model* m, const vla_ctx* c, int32_t layer, float* host
  * from the LM features in the prefill) to host fp32 buffers of [prefix,
  * ex_dim] each (head-major columns). Blocking. */
 int vla_ctx_export_cross(vla_model* m, const vla_ctx* c, int32_t layer, float* host_k, float* host_v);
+
+/* VLA_HEAD_COG only: copy a context's cognition vector (fp32 [ex_dim]) to
+ * host_dst. Blocking. */
+int vla_ctx_export_cog(vla_model* m, const vla_ctx* c, float* host_dst);
 
 /* Test entry points for single kernels (same kernels and launch planner as
  * the phases). dtype VLA_F32 or VLA_BF16 selects the operand type of A and W

@@ -33,7 +33,7 @@ CONFIG_FIELDS = (
     "ex_dim", "ex_mlp", "ex_layers", "chunk_len", "action_dim", "n_steps",
     "head", "shuffle", "ex_heads", "sampler",
 )
-HEAD_PI0, HEAD_DIT = 0, 1
+HEAD_PI0, HEAD_DIT, HEAD_COG = 0, 1, 2
 SAMPLER_EULER, SAMPLER_DDIM = 0, 1
 
 
@@ -112,6 +112,7 @@ def _load():
         "vla_export_param": [P, ctypes.c_char_p, P, I64],
         "vla_ctx_export_kv": [P, P, I32, P, P],
         "vla_ctx_export_cross": [P, P, I32, P, P],
+        "vla_ctx_export_cog": [P, P, P],
         "vla_wavelog_enable": [P, I64],
         "vla_wavelog_read": [P, P, I64, ctypes.POINTER(I64)],
         "vla_debug_gemm": [I32, I32, I32, I32, P, I32, P, I32, P, P, P],
@@ -307,6 +308,12 @@ def vla_ctx_export_cross(model: int, ctx: int, layer: int, n: int) -> Tuple[np.n
     return k, v
 
 
+def vla_ctx_export_cog(model: int, ctx: int, n: int) -> np.ndarray:
+    c = np.empty(n, dtype=np.float32)
+    _check(_lib.vla_ctx_export_cog(model, ctx, c.ctypes.data))
+    return c
+
+
 WAVE_REC = np.dtype([("t", "<u8"), ("hwid", "<u4"), ("xcc", "<u4"), ("kind", "<u4"), ("end", "<u4")])
 
 
@@ -381,7 +388,7 @@ def exported_symbols() -> Iterable[str]:
     """Names of the C entry points this binding wraps."""
     return ["vla_preset", "vla_validate", "vla_model_config", "vla_create", "vla_destroy", "vla_ctx_create",
             "vla_ctx_destroy", "vla_vlm_prefill", "vla_action_denoise", "vla_pipeline_run",
-            "vla_param_count", "vla_param_info", "vla_export_param", "vla_ctx_export_kv", "vla_ctx_export_cross", "vla_wavelog_enable", "vla_wavelog_read",
+            "vla_param_count", "vla_param_info", "vla_export_param", "vla_ctx_export_kv", "vla_ctx_export_cross", "vla_ctx_export_cog", "vla_wavelog_enable", "vla_wavelog_read",
             "vla_debug_gemm", "vla_debug_gemm_epi", "vla_gemm_noalloc", "vla_debug_attention", "vla_debug_attention_cache", "vla_debug_generate",
             "vla_kernel_timer",
             "vla_kernel_timer_read", "vla_last_error"]

@@ -62,6 +62,7 @@ struct Dims {
   int kproj;  // projector input width (ViT width times the pixel-shuffle factor squared)
   int ehd;    // DiT head dim
   int prefix_pad, chunk_pad;  // key lengths rounded up to 32 (KV-cache blocks)
+  int arows;  // rows of the action head's token sequence (chunk, plus the cognition and time tokens)
 };
 
 static Dims derive(const vla_config& c) {
@@ -70,20 +71,21 @@ static Dims derive(const vla_config& c) {
   d.gw = c.img_w / c.patch;
   d.tview = d.gh * d.gw;
   d.nimg = c.n_views * d.tview / (c.shuffle * c.shuffle);
-  d.prefix = d.nimg + c.n_text + (c.state_dim > 0 ? 1 : 0);
+  d.prefix = d.nimg + c.n_text + (c.state_dim > 0 ? 1 : 0) + (c.head == VLA_HEAD_COG ? 1 : 0);
   d.kp = 3 * c.patch * c.patch;
   d.kp_pad = rnd_up(d.kp, 8);
   d.a_pad = rnd_up(c.action_dim, 8);
   d.s_pad = rnd_up(std::max(c.state_dim, 1), 8);
   d.rows_v = c.n_views * d.tview;
   d.kproj = c.vit_dim * c.shuffle * c.shuffle;
-  d.ehd = c.head == VLA_HEAD_DIT ? c.ex_dim / c.ex_heads : c.head_dim;
+  d.ehd = c.head != VLA_HEAD_PI0 ? c.ex_dim / c.ex_heads : c.head_dim;
   d.kvd = c.lm_kv_heads * c.head_dim;
   d.qd = c.lm_heads * c.head_dim;
   d.qkv_n = d.qd + 2 * d.kvd;
   d.vhd = c.vit_dim / c.vit_heads;
   d.prefix_pad = rnd_up(d.prefix, 32);
-  d.chunk_pad = rnd_up(c.chunk_len, 32);
+  d.arows = c.chunk_len + (c.head == VLA_HEAD_COG ? 2 : 0);
+  d.chunk_pad = rnd_up(d.arows, 32);
   return d;
 }
 
@@ -106,12 +108,14 @@ static int validate(const vla_config* c) {
   if (c->head_dim % 32 || c->head_dim > 256) return bad("head_dim must be a multiple of 32, <= 256");
   if (c->dtype == VLA_F32 && (c->head_dim > 128 || vhd > 128))
     return bad("fp32 configurations need head dims <= 128");
-  if (c->head != VLA_HEAD_PI0 && c->head != VLA_HEAD_DIT) return bad("head");
+  if (c->head != VLA_HEAD_PI0 && c->head != VLA_HEAD_DIT && c->head != VLA_HEAD_COG) return bad("head");
   if (c->shuffle < 1 || (c->img_h / c->patch) % c->shuffle || (c->img_w / c->patch) % c->shuffle)
     return bad("shuffle must be >= 1 and divide the patch grid");
   if (c->head == VLA_HEAD_PI0) {
     if (c->ex_layers != c->lm_layers) return bad("ex_layers must equal lm_layers (layer-wise KV sharing)");
   } else {
+    if (c->head == VLA_HEAD_COG && c->chunk_len > 62)
+      return bad("cognition-token head: chunk_len + 2 tokens must be <= 64");
     if (c->ex_heads <= 0 || c->ex_dim % c->ex_heads) return bad("ex_heads must divide ex_dim");
     const int ehd = c->ex_dim / c->ex_heads;
     if (ehd % 8 || ehd > 256 || (c->dtype == VLA_F32 && ehd > 128))
@@ -145,6 +149,15 @@ static bool preset(const char* name, vla_config* o) {
   if (n == "gr00t") {
     *o = vla_config{VLA_BF16, 1, 448, 448, 28, 1152, 16, 4304, 27, 2048, 16, 16, 128, 8192, 12,
                     1024, 32, 0, 1536, 6144, 16, 16, 32, 4, VLA_HEAD_DIT, 2, 32};
+    return true;
+  }
+  if (n == "cogact" || n == "tiny_cog") {
+    if (n == "cogact")
+      *o = vla_config{VLA_BF16, 1, 224, 224, 14, 1152, 16, 4304, 27, 2048, 8, 1, 256, 16384, 18,
+                      1024, 48, 0, 1024, 4096, 24, 16, 7, 10, VLA_HEAD_COG, 1, 16, VLA_SAMPLER_DDIM};
+    else
+      *o = vla_config{VLA_F32, 1, 128, 128, 16, 256, 4, 1024, 2, 256, 4, 1, 64, 1024, 2,
+                      1024, 16, 0, 128, 512, 2, 8, 7, 4, VLA_HEAD_COG, 1, 2, VLA_SAMPLER_DDIM};
     return true;
   }
   if (n == "pi0" || n == "pi0_3view" || n == "pi0_ddim") {
@@ -216,6 +229,12 @@ struct DitLayer {
   int ada_w = -1, ada_b = -1, q = -1, kv = -1, qkv = -1, o = -1, fc1 = -1, fc2 = -1;
 };
 
+// Cognition-token head layer: pre-LN self-attention (fused q|k|v, no
+// biases) and GELU MLP.
+struct CogLayer {
+  int ln1_g = -1, ln1_b = -1, qkv = -1, o = -1, ln2_g = -1, ln2_b = -1, fc1 = -1, fc2 = -1;
+};
+
 constexpr int MAX_ACT_STREAMS = 4;
 
 constexpr int MAX_VLM_STREAMS = 2;
@@ -272,6 +291,8 @@ struct vla_ctx {
   // DiT head: cross K/V of every even DiT layer (same layout, ex_heads heads)
   void* XK = nullptr;
   void* XV = nullptr;
+  // cognition-token head: the conditioning vector c = W_c f + b_c, fp32 [ex_dim]
+  float* cog = nullptr;
 };
 
 struct vla_model {
@@ -296,6 +317,11 @@ struct vla_model {
   // DiT head
   int lm_fin_g = -1, fada_w = -1, fada_b = -1;
   std::vector<DitLayer> dit;
+  // cognition-token head: the token row, its projection, the head's layers,
+  // the final LayerNorm bias and the time token of every step [n_steps][ex_dim]
+  int cog_tok = -1, cog_w = -1, cog_b = -1, fin_b = -1;
+  std::vector<CogLayer> cogl;
+  float* ttok = nullptr;
 
   // constant tables
   float* rope_cos = nullptr;
@@ -358,7 +384,7 @@ static size_t ctx_layer_v(const vla_model* m) {
   return kv_velems(m->dt, m->d.prefix_pad / 32, m->c.head_dim, m->c.lm_kv_heads);
 }
 static int own_heads(const vla_model* m) {
-  return m->c.head == VLA_HEAD_DIT ? m->c.ex_heads : m->c.lm_kv_heads;
+  return m->c.head != VLA_HEAD_PI0 ? m->c.ex_heads : m->c.lm_kv_heads;
 }
 static size_t own_k(const vla_model* m) {
   return kv_kelems(m->dt, m->d.chunk_pad / 32, m->d.ehd, own_heads(m));
@@ -516,6 +542,41 @@ static void build_inventory(vla_model* m) {
     }
     m->fada_w = add_mat(m, "ex.final.ada.w", 2 * de, de, true);
     m->fada_b = add_vec(m, "ex.final.ada.b", 2 * de);
+    m->out_w = add_mat(m, "ex.out.w", c.action_dim, de, true);
+    m->out_b = add_vec(m, "ex.out.b", c.action_dim);
+    return;
+  }
+  if (c.head == VLA_HEAD_COG) {
+    const int de = c.ex_dim;
+    m->lm_fin_g = add_vec(m, "lm.final.g", c.lm_dim, 1.0);
+    m->cog_tok = add_tensor(m, 1, c.lm_dim, DT_F32, true);
+    add_param(m, "lm.cog", 1, c.lm_dim, 0.0, m->cog_tok);
+    m->cog_w = add_mat(m, "cog.w", de, c.lm_dim);
+    m->cog_b = add_vec(m, "cog.b", de);
+    m->in_w = add_mat(m, "ex.in.w", de, c.action_dim, true);
+    m->in_b = add_vec(m, "ex.in.b", de);
+    m->t1_w = add_mat(m, "ex.time1.w", de, DIT_TIME_DIM, true);
+    m->t1_b = add_vec(m, "ex.time1.b", de);
+    m->t2_w = add_mat(m, "ex.time2.w", de, de, true);
+    m->t2_b = add_vec(m, "ex.time2.b", de);
+    for (int l = 0; l < c.ex_layers; ++l) {
+      const std::string p = "ex." + std::to_string(l) + ".";
+      CogLayer L;
+      L.ln1_g = add_vec(m, p + "ln1.g", de, 1.0);
+      L.ln1_b = add_vec(m, p + "ln1.b", de);
+      L.qkv = add_tensor(m, 3 * de, de, m->dt, false, true);
+      add_param(m, p + "q.w", de, de, 0.0, L.qkv, MAP_IDENT, 0);
+      add_param(m, p + "k.w", de, de, 0.0, L.qkv, MAP_IDENT, de);
+      add_param(m, p + "v.w", de, de, 0.0, L.qkv, MAP_IDENT, 2 * de);
+      L.o = add_mat(m, p + "o.w", de, de, true);
+      L.ln2_g = add_vec(m, p + "ln2.g", de, 1.0);
+      L.ln2_b = add_vec(m, p + "ln2.b", de);
+      L.fc1 = add_mat(m, p + "fc1.w", c.ex_mlp, de, true);
+      L.fc2 = add_mat(m, p + "fc2.w", de, c.ex_mlp, true);
+      m->cogl.push_back(L);
+    }
+    m->fin_g = add_vec(m, "ex.final.g", de, 1.0);
+    m->fin_b = add_vec(m, "ex.final.b", de);
     m->out_w = add_mat(m, "ex.out.w", c.action_dim, de, true);
     m->out_b = add_vec(m, "ex.out.b", c.action_dim);
     return;
@@ -969,6 +1030,8 @@ static int run_prefill_n(const Run& r, const vla_frame* f, int n, vla_ctx* const
                  dl, d.kproj, epi_kind(EPI_F32, xl, dl, m->f32(m->proj_b))));
     HIP_TRY(launch_embed(m->dt, m->tptr(m->embed), dl, c.vocab, f[i].text_ids, c.n_text, std::sqrt((float)dl),
                          xl + (size_t)d.nimg * dl, dl, r.st));
+    if (c.head == VLA_HEAD_COG)  // the learned cognition token, the prefix's last row
+      HIP_TRY(launch_copy(xl + (size_t)(P - 1) * dl, m->f32(m->cog_tok), (size_t)dl * 4, r.st));
     if (c.state_dim > 0) {
       void* sb = (char*)w.sbuf + (size_t)i * d.s_pad * m->esz;
       HIP_TRY(launch_cvt_pad(m->dt, f[i].state, 1, c.state_dim, sb, d.s_pad, false, nullptr, r.st));
@@ -987,7 +1050,16 @@ static int run_prefill_n(const Run& r, const vla_frame* f, int n, vla_ctx* const
     void* K = (char*)ctx->K + l * layer_k;
     void* V = (char*)ctx->V + l * layer_v;
     VLA_TRY(decoder_layer(r, true, m->lm[l], w.xl, P, dl, c.lm_mlp, w.h, w.qkv, K, V, 0, nullptr, nullptr, 0,
-                          w.att, w.mlp, !dit && l == c.lm_layers - 1, &pend, n, kstride, vstride));
+                          w.att, w.mlp, c.head == VLA_HEAD_PI0 && l == c.lm_layers - 1, &pend, n, kstride,
+                          vstride));
+  }
+  if (c.head == VLA_HEAD_COG) {
+    // features = final RMSNorm of the last layer; the hand-off is the
+    // cognition row's projection c = W_c f + b_c, one per frame
+    VLA_TRY(norm(r, w.xl, n * P, dl, pend, nullptr, m->lm_fin_g, -1, true, w.h));
+    for (int i = 0; i < n; ++i)
+      VLA_TRY(gemm(r, "cog", (char*)w.h + ((size_t)i * P + P - 1) * dl * m->esz, dl, m->cog_w, 1, c.ex_dim, dl,
+                   epi_kind(EPI_F32, ctxs[i]->cog, c.ex_dim, m->f32(m->cog_b))));
   }
   if (dit) {
     // features = final RMSNorm of the last layer; then the cross K/V of every
@@ -1117,6 +1189,97 @@ static int run_denoise_dit(const Run& r, const vla_ctx* ctx, const float* noise,
   return VLA_OK;
 }
 
+// Cognition-token head (DDIM or Euler steps as in run_denoise): the token
+// sequence [action tokens (W_a x + b_a + positions); the frame's cognition
+// vector; the step's time token] runs through pre-LN self-attention layers
+// (LayerNorm -> fused q|k|v -> attention over all tokens -> out-projection
+// whose partial sums the next norm adds -> LayerNorm -> GELU MLP ->
+// down-projection added by the next norm); the final LayerNorm's action rows
+// feed the out-projection fused with the sampler update.
+static int run_denoise_cog(const Run& r, const vla_ctx* ctx, const float* noise, float* x) {
+  vla_model* m = r.m;
+  const vla_config& c = m->c;
+  const Dims& d = m->d;
+  ActWs& w = *r.aw;
+  const int H = c.chunk_len, de = c.ex_dim, A = c.action_dim, S = d.arows;
+  if (!ctx->cog) return fail(VLA_ESTATE, "context has no cognition vector");
+  HIP_TRY(launch_cvt_pad(m->dt, noise, H, A, w.xop, d.a_pad, true, x, r.st));
+  auto ln = [&](int pend, int g, int b) {
+    NormDesc n;
+    n.x = w.u;
+    n.ldx = de;
+    n.rows = S;
+    n.d = de;
+    n.splits = pend;
+    n.g = m->f32(g);
+    n.b = m->f32(b);
+    n.out = w.h;
+    n.ldo = de;
+    n.afrag = 1;
+    return run_norm(r, n);
+  };
+  for (int k = 0; k < c.n_steps; ++k) {
+    {
+      Epi e = epi_kind(EPI_F32, w.u, de, m->f32(m->in_b));
+      e.rowadd = m->dpos;
+      e.rowadd_period = H;
+      e.ldra = de;
+      VLA_TRY(gemm(r, "ex.in", w.xop, d.a_pad, m->in_w, H, de, d.a_pad, e));
+    }
+    HIP_TRY(launch_copy(w.u + (size_t)H * de, ctx->cog, (size_t)de * 4, r.st));
+    HIP_TRY(launch_copy(w.u + (size_t)(H + 1) * de, m->ttok + (size_t)k * de, (size_t)de * 4, r.st));
+    int pend = 0;
+    for (int l = 0; l < c.ex_layers; ++l) {
+      const CogLayer& L = m->cogl[l];
+      VLA_TRY(ln(pend, L.ln1_g, L.ln1_b));
+      Epi e;
+      e.kind = EPI_QKV_PLAIN;
+      e.q = w.q;
+      e.ldq = de;
+      e.nq = c.ex_heads;
+      e.nkv = c.ex_heads;
+      e.hd = d.ehd;
+      e.k = w.kown;
+      e.v = w.vown;
+      e.kv_nb = d.chunk_pad / 32;
+      VLA_TRY(gemm(r, "ex.qkv", w.h, de, L.qkv, S, 3 * de, de, e));
+      AttnKvDesc a{};
+      a.dtype = m->dt;
+      a.q = w.q;
+      a.ldq = de;
+      a.k0 = w.kown;
+      a.v0 = w.vown;
+      a.S0 = S;
+      a.nq = a.nkv = c.ex_heads;
+      a.hd = d.ehd;
+      a.Sq = S;
+      a.out = w.att;
+      a.out_afrag = 1;
+      VLA_TRY(attn_kv(r, "ex.attn", a));
+      int so = 0;
+      VLA_TRY(gemm_part(r, "ex.o", w.att, de, L.o, S, de, de, &so));
+      VLA_TRY(ln(so, L.ln2_g, L.ln2_b));
+      Epi e1 = epi_kind(EPI_GELU, w.mlp, c.ex_mlp);
+      e1.afrag = 1;
+      VLA_TRY(gemm(r, "ex.fc1", w.h, de, L.fc1, S, c.ex_mlp, de, e1));
+      VLA_TRY(gemm_part(r, "ex.fc2", w.mlp, c.ex_mlp, L.fc2, S, de, c.ex_mlp, &pend));
+    }
+    VLA_TRY(ln(pend, m->fin_g, m->fin_b));
+    Epi e;
+    e.kind = EPI_EULER;
+    e.afrag = 1;
+    e.bias = m->f32(m->out_b);
+    e.x = x;
+    e.ldx = A;
+    e.xop = w.xop;
+    e.ldxop = d.a_pad;
+    e.dt = m->step_b[k];
+    e.xs = m->step_a[k];
+    VLA_TRY(gemm(r, "ex.out", w.h, de, m->out_w, H, A, de, e));
+  }
+  return VLA_OK;
+}
+
 // Row-major copies of the expert layers' matrices for batched action loops
 // (converted on the device from the fragment-ordered weights, once). Not
 // while a graph is being captured.
@@ -1164,9 +1327,9 @@ static int ensure_wide(vla_model* m) {
 // every weight load, and each frame's result equals its own run bit for bit.
 static int run_denoise_n(const Run& r, const vla_ctx* const* ctxs, int frames, const float* noise, float* x) {
   vla_model* m = r.m;
-  if (m->c.head == VLA_HEAD_DIT) {
+  if (m->c.head == VLA_HEAD_DIT || m->c.head == VLA_HEAD_COG) {
     if (frames != 1) return fail(VLA_EINVAL, "batched action phases: pi0-style head only");
-    return run_denoise_dit(r, ctxs[0], noise, x);
+    return m->c.head == VLA_HEAD_DIT ? run_denoise_dit(r, ctxs[0], noise, x) : run_denoise_cog(r, ctxs[0], noise, x);
   }
   if (frames < 1 || frames > MAX_ACT_BATCH) return fail(VLA_EINVAL, "frames per action phase: 1 to " + std::to_string(MAX_ACT_BATCH));
   if (frames > 1 && m->exw.size() != m->ex.size()) return fail(VLA_ESTATE, "row-major expert weights missing");
@@ -1325,7 +1488,7 @@ static int setup_tables(vla_model* m) {
   }
   // sinusoid phi(t_k): periods log-spaced on [4e-3, 4]; the DiT's timestep
   // embedder takes a 256-wide phi
-  const bool dit = c.head == VLA_HEAD_DIT;
+  const bool dit = c.head != VLA_HEAD_PI0;  // DiT and cognition-token heads: 256-wide phi, positions
   const int de = dit ? DIT_TIME_DIM : c.ex_dim, dh = de / 2;
   std::vector<float> phi((size_t)c.n_steps * de);
   for (int k = 0; k < c.n_steps; ++k) {
@@ -1359,8 +1522,12 @@ static int setup_tables(vla_model* m) {
   // DiT: adaLN tables (filled at create) and the fixed token positions,
   // [sin(p w_i)]_i ++ [cos(p w_i)]_i with w_i = 10000^(-i / (d/2))
   const int dx = c.ex_dim, hx = dx / 2;
-  VLA_TRY(dmalloc(m, (void**)&m->ada, (size_t)c.n_steps * c.ex_layers * 6 * dx * 4));
-  VLA_TRY(dmalloc(m, (void**)&m->fada, (size_t)c.n_steps * 2 * dx * 4));
+  if (c.head == VLA_HEAD_DIT) {
+    VLA_TRY(dmalloc(m, (void**)&m->ada, (size_t)c.n_steps * c.ex_layers * 6 * dx * 4));
+    VLA_TRY(dmalloc(m, (void**)&m->fada, (size_t)c.n_steps * 2 * dx * 4));
+  } else {
+    VLA_TRY(dmalloc(m, (void**)&m->ttok, (size_t)c.n_steps * dx * 4));
+  }
   std::vector<float> pos((size_t)c.chunk_len * dx);
   for (int p = 0; p < c.chunk_len; ++p)
     for (int i = 0; i < hx; ++i) {
@@ -1395,6 +1562,21 @@ static int setup_dit_tables(vla_model* m) {
   return VLA_OK;
 }
 
+// Cognition-token head: the time token of every step, W_t2 swish(W_t1
+// phi(t_k) + b_t1) + b_t2 (it depends on the step only), computed once with
+// the library's GEMMs.
+static int setup_cog_tables(vla_model* m) {
+  const vla_config& c = m->c;
+  const int de = c.ex_dim, N = c.n_steps;
+  ActWs& w = *m->aws[0];
+  Run r{m, nullptr, LaunchCaps{}, &w.scr, &w};
+  Epi e1 = epi_kind(EPI_SWISH, w.a, de, m->f32(m->t1_b));
+  e1.afrag = 1;
+  VLA_TRY(gemm(r, "cog.time1", m->phi, DIT_TIME_DIM, m->t1_w, N, de, DIT_TIME_DIM, e1));
+  VLA_TRY(gemm(r, "cog.time2", w.a, de, m->t2_w, N, de, de, epi_kind(EPI_F32, m->ttok, de, m->f32(m->t2_b))));
+  return VLA_OK;
+}
+
 // One action lane's scratch (activations of the chunk rows, own K / V^T,
 // partial sums, staging for graph replays).
 static int add_act_lane(vla_model* m) {
@@ -1402,7 +1584,7 @@ static int add_act_lane(vla_model* m) {
   const Dims& d = m->d;
   const int dt = m->dt;
   const size_t e = m->esz;
-  const int P = d.prefix, H = c.chunk_len, de = c.ex_dim;
+  const int P = d.prefix, H = c.chunk_len, de = c.ex_dim, S = d.arows;
   auto upd = [](ScratchNeed& s, ScratchNeed x) { s.floats = std::max(s.floats, x.floats); };
   std::unique_ptr<ActWs> lane(new ActWs());
   ActWs& a = *lane;
@@ -1414,7 +1596,7 @@ static int add_act_lane(vla_model* m) {
   a.blk_mlp = afrag_elems(dt, c.ex_mlp);
   a.blk_k = own_k(m);
   a.blk_v = own_v(m);
-  VLA_TRY(dmalloc(m, (void**)&a.u, (size_t)F * H * de * 4));
+  VLA_TRY(dmalloc(m, (void**)&a.u, (size_t)F * S * de * 4));
   // skinny-GEMM operands: row-block operand layout (64 rows per frame),
   // zeroed so the padding columns of xop stay zero
   VLA_TRY(dmalloc(m, &a.xop, F * a.blk_xop * e));
@@ -1422,7 +1604,7 @@ static int add_act_lane(vla_model* m) {
   VLA_TRY(dmalloc(m, &a.a, F * a.blk_de * e));
   VLA_TRY(dmalloc(m, &a.hid, F * a.blk_de * e));
   VLA_TRY(dmalloc(m, &a.h, F * a.blk_de * e));
-  VLA_TRY(dmalloc(m, &a.q, (size_t)F * H * qw * e));
+  VLA_TRY(dmalloc(m, &a.q, (size_t)F * S * qw * e));
   VLA_TRY(dmalloc(m, &a.kown, F * a.blk_k * e));
   VLA_TRY(dmalloc(m, &a.vown, F * a.blk_v * e));
   HIP_TRY(hipMemset(a.kown, 0, F * a.blk_k * e));  // padding stays zero
@@ -1442,6 +1624,17 @@ static int add_act_lane(vla_model* m) {
     upd(sa, gemm_scratch(dt, H, de, de, true, true));
     upd(sa, gemm_scratch(dt, H, c.ex_mlp, de, false, true));
     upd(sa, gemm_scratch(dt, H, de, c.ex_mlp, true, true));
+    upd(sa, gemm_scratch(dt, H, c.action_dim, de, false, true));
+  }
+  if (c.head == VLA_HEAD_COG) {
+    const int N = c.n_steps;
+    upd(sa, gemm_scratch(dt, H, de, d.a_pad, false, true));
+    upd(sa, gemm_scratch(dt, N, de, DIT_TIME_DIM, false, true));
+    upd(sa, gemm_scratch(dt, N, de, de, false, true));
+    upd(sa, gemm_scratch(dt, S, 3 * de, de, false, true));
+    upd(sa, gemm_scratch(dt, S, de, de, true, true));
+    upd(sa, gemm_scratch(dt, S, c.ex_mlp, de, false, true));
+    upd(sa, gemm_scratch(dt, S, de, c.ex_mlp, true, true));
     upd(sa, gemm_scratch(dt, H, c.action_dim, de, false, true));
   }
   // (split partials of all frames of a batched action phase)
@@ -1503,6 +1696,7 @@ static int make_vlm_lane(vla_model* m, int cap, int slot) {
   upd(sv, gemm_scratch(dt, r1, dv, c.vit_mlp, true, false, cap));
   upd(sv, gemm_scratch(dt, d.nimg, dl, d.kproj));
   if (c.head == VLA_HEAD_DIT) upd(sv, gemm_scratch(dt, p1, 2 * c.ex_dim, dl, false, false, cap));
+  if (c.head == VLA_HEAD_COG) upd(sv, gemm_scratch(dt, 1, c.ex_dim, dl));
   upd(sv, gemm_scratch(dt, 1, dl, d.s_pad));
   upd(sv, gemm_scratch(dt, p1, d.qkv_n, dl, false, false, cap));
   upd(sv, gemm_scratch(dt, p1, dl, d.qd, true, false, cap));
@@ -1576,6 +1770,8 @@ static int create_impl(const vla_config* cfg, uint64_t seed, vla_model** out) {
   if (rc == VLA_OK) rc = setup_workspaces(m.get());
   if (rc == VLA_OK && m->c.head == VLA_HEAD_DIT) {
     rc = setup_dit_tables(m.get());
+  } else if (rc == VLA_OK && m->c.head == VLA_HEAD_COG) {
+    rc = setup_cog_tables(m.get());
   } else if (rc == VLA_OK) {
     // c_k = W_2[:, d_e:] phi(t_k) + b_2 for every step (depends on the step only)
     Run r{m.get(), nullptr, LaunchCaps{}, &m->aws[0]->scr, m->aws[0].get()};
@@ -1608,6 +1804,7 @@ static void ctx_free(vla_ctx* c) {
     hipFree(c->V);
     hipFree(c->XK);
     hipFree(c->XV);
+    hipFree(c->cog);
   }
   delete c;
 }
@@ -1617,7 +1814,8 @@ static void ctx_free(vla_ctx* c) {
 // frame i's cache at a fixed stride. out[0] owns the allocations.
 static int ctx_create_n(vla_model* m, int n, vla_ctx** out) {
   const size_t kb = ctx_kbytes(m), vb = ctx_vbytes(m), xb = ctx_xbytes(m);
-  void *K = nullptr, *V = nullptr, *XK = nullptr, *XV = nullptr;
+  const size_t cb = m->c.head == VLA_HEAD_COG ? (size_t)m->c.ex_dim * 4 : 0;
+  void *K = nullptr, *V = nullptr, *XK = nullptr, *XV = nullptr, *CG = nullptr;
   auto zalloc = [](void** p, size_t bytes) {
     hipError_t e = hipMalloc(p, bytes);
     if (e == hipSuccess) e = hipMemset(*p, 0, bytes);  // padding stays zero
@@ -1627,11 +1825,13 @@ static int ctx_create_n(vla_model* m, int n, vla_ctx** out) {
   if (e == hipSuccess) e = zalloc(&V, n * vb);
   if (e == hipSuccess && xb) e = zalloc(&XK, n * xb);
   if (e == hipSuccess && xb) e = zalloc(&XV, n * xb);
+  if (e == hipSuccess && cb) e = zalloc(&CG, n * cb);
   if (e != hipSuccess) {
     hipFree(K);
     hipFree(V);
     hipFree(XK);
     hipFree(XV);
+    hipFree(CG);
     return fail(VLA_ENOMEM, std::string("context buffers: ") + hipGetErrorString(e));
   }
   for (int i = 0; i < n; ++i) {
@@ -1642,6 +1842,7 @@ static int ctx_create_n(vla_model* m, int n, vla_ctx** out) {
     c->V = (char*)V + i * vb;
     c->XK = xb ? (char*)XK + i * xb : nullptr;
     c->XV = xb ? (char*)XV + i * xb : nullptr;
+    c->cog = cb ? (float*)((char*)CG + i * cb) : nullptr;
     out[i] = c;
   }
   return VLA_OK;
@@ -2148,6 +2349,16 @@ int vla_ctx_export_cross(vla_model* m, const vla_ctx* c, int32_t layer, float* h
           host_k[(size_t)p * nh * hd + j * hd + dd] = val(kimg, kv_kidx(m->dt, nb, hd, j, p, dd));
           host_v[(size_t)p * nh * hd + j * hd + dd] = val(vimg, kv_vidx(m->dt, nb, hd, j, p, dd));
         }
+    return VLA_OK;
+  })
+}
+
+int vla_ctx_export_cog(vla_model* m, const vla_ctx* c, float* host_dst) {
+  ABI_GUARD({
+    if (!m || !c || !host_dst) return fail(VLA_EINVAL, "NULL argument");
+    if (c->m != m) return fail(VLA_ESTATE, "context belongs to another model");
+    if (m->c.head != VLA_HEAD_COG || !c->cog) return fail(VLA_EINVAL, "the model has no cognition-token head");
+    HIP_TRY(hipMemcpy(host_dst, c->cog, (size_t)m->c.ex_dim * 4, hipMemcpyDeviceToHost));
     return VLA_OK;
   })
 }

@@ -75,7 +75,8 @@ def context(m):
 def run_frame(m, cfg, fr, stream=0, cross=None):
     """Prefill + denoise of one frame on one stream; returns (chunk, ctx-kv
     list). For a DiT head, ``cross`` (a dict) receives the cross K/V of every
-    even DiT layer."""
+    even DiT layer; for the cognition-token head, its cognition vector under
+    the key "cog"."""
     d = synth.derived(cfg)
     df = DevFrame(fr)
     out = torch.empty_like(df.noise)
@@ -88,4 +89,6 @@ def run_frame(m, cfg, fr, stream=0, cross=None):
         if cross is not None and cfg.get("head", 0) == synth.HEAD_DIT:
             for l in range(0, cfg["ex_layers"], 2):
                 cross[l] = V.vla_ctx_export_cross(m, c, l, d["prefix"] * cfg["ex_dim"])
+        if cross is not None and cfg.get("head", 0) == synth.HEAD_COG:
+            cross["cog"] = V.vla_ctx_export_cog(m, c, cfg["ex_dim"]).astype(np.float64)
     return out.cpu().numpy().astype(np.float64), kv

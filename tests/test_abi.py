@@ -36,6 +36,10 @@ def test_presets_match_shapes():
     assert V.vla_preset("pi0_3view") == synth.PI0_3VIEW
     assert V.vla_preset("gr00t") == synth.GR00T
     assert V.vla_preset("tiny_dit") == synth.TINY_DIT
+    assert V.vla_preset("cogact") == synth.COGACT
+    assert V.vla_preset("tiny_cog") == synth.TINY_COG
+    assert V.vla_preset("pi0_ddim") == synth.PI0_DDIM
+    assert V.vla_preset("tiny_ddim") == synth.TINY_DDIM
     with pytest.raises(V.VlaError) as e:
         V.vla_preset("nope")
     assert e.value.code == -1
@@ -59,6 +63,10 @@ def test_validate_rejects(field, value, msg):
     V.vla_validate(synth.TINY)
     V.vla_validate(synth.PI0)
     V.vla_validate(synth.micro())
+    V.vla_validate(synth.micro_cog())
+    V.vla_validate(synth.COGACT)
+    with pytest.raises(V.VlaError):
+        V.vla_validate(dict(synth.micro_cog(), chunk_len=63))
 
 
 @pytest.mark.parametrize("seed,name,mean", [(0, "lm.3.q.w", 0.0), (7, "vit.0.ln1.g", 1.0),

@@ -169,8 +169,9 @@ def test_attention_cache_vs_oracle(V, case):
     assert np.all(err <= bound), float((err / bound).max())
 
 
-@pytest.mark.parametrize("cfg", [synth.micro(synth.F32), synth.micro(synth.BF16), synth.TINY],
-                         ids=["micro-f32", "micro-bf16", "tiny"])
+@pytest.mark.parametrize("cfg", [synth.micro(synth.F32), synth.micro(synth.BF16), synth.TINY,
+                                 synth.micro_cog(synth.BF16), synth.micro_dit(synth.BF16)],
+                         ids=["micro-f32", "micro-bf16", "tiny", "micro-cog-bf16", "micro-dit-bf16"])
 def test_weights_on_device_equal_seeded_generator(V, cfg):
     g = G()
     g.say(f"export params {cfg['dtype']}")
@@ -429,6 +430,66 @@ def test_gr00t_full_size_vs_oracle(V):
     assert err <= CHUNK_TOL[synth.BF16]
 
 
+COG_CFGS = [
+    ("micro-cog-f32", synth.micro_cog(synth.F32)),
+    ("micro-cog-bf16", synth.micro_cog(synth.BF16)),
+    ("micro-cog-euler-f32", dict(synth.micro_cog(synth.F32), sampler=synth.SAMPLER_EULER)),
+    ("tiny-cog", synth.TINY_COG),
+    ("tiny-cog-bf16", dict(synth.TINY_COG, dtype=synth.BF16)),
+]
+
+
+@pytest.mark.parametrize("name,cfg", COG_CFGS, ids=[p[0] for p in COG_CFGS])
+def test_cog_phases_vs_oracle(V, name, cfg):
+    """Cognition-token head: the LM cache and the cognition vector (phase 1)
+    and the chunk (phase 2) against the oracle."""
+    g = G()
+    g.say(f"cog phases {name}")
+    P = synth.make_params(cfg, 0)
+    fr = synth.make_frame(cfg, 0, 0)
+    cap = {}
+    want = O.forward(P, cfg, fr, cap)
+    with g.model(cfg, 0) as m:
+        hand = {}
+        got, kv = g.run_frame(m, cfg, fr, cross=hand)
+        got2, _ = g.run_frame(m, cfg, fr)
+    assert np.array_equal(got, got2), "not deterministic"
+    _check_cache(cfg, name, kv, cap)
+    _kv_check(cfg, f"{name} cog", hand["cog"], cap["cog"])
+    err = float(np.abs(got - want).max())
+    print(f"[gpu] {name}: chunk max abs err {err:.3e} (max|chunk| {float(np.abs(want).max()):.3e})", flush=True)
+    assert err <= chunk_bound(cfg, want)
+
+
+@pytest.mark.timeout(900)
+def test_cogact_full_size_vs_oracle(V):
+    """The CogACT-shaped VLA at its real sizes (PaliGemma-shaped VLM with the
+    cognition token, 24-layer DiT-L-shaped head, 10 DDIM steps): frame 0 of
+    seed 0 against the oracle, and the pipeline's two-action-lane graph
+    schedule against the standalone calls bit for bit."""
+    g = G()
+    cfg = synth.COGACT
+    g.say("cogact full size: GPU")
+    frs = [synth.make_frame(cfg, 0, r) for r in range(2)]
+    with g.model(cfg, 0) as m:
+        hand = {}
+        got, kv = g.run_frame(m, cfg, frs[0], cross=hand)
+        got1, _ = g.run_frame(m, cfg, frs[1])
+        g.say("cogact full size: pipeline, both frames in one prefill, two action lanes, graphs")
+        piped = _pipeline_frames(g, m, cfg, frs, vlm_batch=2)
+    assert np.array_equal(piped[0].astype(np.float64), got)
+    assert np.array_equal(piped[1].astype(np.float64), got1)
+    g.say("cogact full size: oracle")
+    P = synth.make_params(cfg, 0)
+    cap = {}
+    want = O.forward(P, cfg, frs[0], cap)
+    _check_cache(cfg, "cogact", kv, cap)
+    _kv_check(cfg, "cogact cog", hand["cog"], cap["cog"])
+    err = float(np.abs(got - want).max())
+    print(f"[gpu] cogact chunk max abs err {err:.3e} (max|chunk| {float(np.abs(want).max()):.3e})", flush=True)
+    assert err <= chunk_bound(cfg, want)
+
+
 DIT_CFGS = [
     ("micro-dit-f32", synth.micro_dit(synth.F32)),
     ("micro-dit-ddim-f32", dict(synth.micro_dit(synth.F32), sampler=synth.SAMPLER_DDIM)),
@@ -461,8 +522,9 @@ def test_dit_phases_vs_oracle(V, name, cfg):
 
 
 @pytest.mark.parametrize("cfg", [synth.micro(synth.BF16), synth.TINY, synth.micro_dit(synth.BF16),
-                                 dict(synth.micro(synth.BF16), sampler=synth.SAMPLER_DDIM)],
-                         ids=["micro-bf16", "tiny", "micro-dit-bf16", "micro-ddim-bf16"])
+                                 dict(synth.micro(synth.BF16), sampler=synth.SAMPLER_DDIM),
+                                 synth.micro_cog(synth.BF16)],
+                         ids=["micro-bf16", "tiny", "micro-dit-bf16", "micro-ddim-bf16", "micro-cog-bf16"])
 def test_pipeline_modes_bit_identical(V, cfg):
     """Every schedule (one stream, two streams, CU masks, workgroup caps,
     several action streams, graph replay) gives the same bits as standalone
