@@ -183,7 +183,7 @@ def main():
                                        "vb2_ab2_graph,vb2_ab2_lanes2_graph,vb2_ab4_graph,vb4_ab4_graph,"
                                        "vb4_ab2_lanes2_graph,vb4_ab4_lanes2_graph,vb8_ab8_graph,"
                                        "vb8_ab4_lanes2_graph,vb4_ab4_v2_lanes2_graph,"
-                                       "serial_vb8_ab4_graph,serial_vb4_ab4_graph")
+                                       "serial_vb8_ab4_graph,serial_vb4_ab4_graph,cu_160_96,cu_auto")
     ap.add_argument("--detail", default=os.path.join(ROOT, "gpurun_out", "bench_detail.json"),
                     help="JSON file for every schedule's numbers, residency logs and further workloads")
     ap.add_argument("--split", default="192,64", help="CU split VLM,action for cu_masked")
@@ -202,7 +202,9 @@ def main():
                                        "vb8_ab8_lanes2_graph;"
                                        "pi0:8:async2_serial,async2_lanes2_graph,async2_vb8_ab4_lanes2_graph,"
                                        "async2_vb8_ab8_lanes2_graph,async4_serial,async4_vb8_ab8_lanes2_graph;"
-                                       "pi0_ddim:8:serial,vb8_ab8_graph,vb8_ab4_lanes2_graph",
+                                       "pi0_ddim:8:serial,vb8_ab8_graph,vb8_ab4_lanes2_graph;"
+                                       "cogact:8:serial,concurrent,lanes2_graph,vb8_ab1_lanes2_graph,"
+                                       "vb8_ab1_lanes4_graph",
                     help="further workloads, ';'-separated preset:R:schedule,schedule,...")
     ap.add_argument("--extra-steps", type=int, default=5)
     ap.add_argument("--residency", type=int, default=8_000_000,
@@ -292,6 +294,16 @@ def main():
         kw[f"cu_{a_}_{b_}_lanes3"] = dict(mode="cu_masked", vlm_cus=a_, act_cus=b_, act_streams=3, graphs=True)
     for c_ in (1, 2, 4):
         kw[f"wg_cap{c_}"] = dict(mode="wg_capped", vlm_wg_cap=c_)
+    # cu_auto: the CU split the calibrated planner picks from the preset's
+    # intensity descriptors (profiles/intensity_<preset>.json)
+    auto_plan = None
+    ipath = os.path.join(ROOT, "profiles", f"intensity_{args.preset}.json")
+    if os.path.exists(ipath):
+        from paper_2609_22335_amd import intensity as IN
+        auto_plan = IN.plan_cu_split(IN.load(ipath), cal=IN.load_calibration(ipath))
+        kw["cu_auto"] = dict(mode="cu_masked", vlm_cus=auto_plan["vlm_cus"], act_cus=auto_plan["act_cus"])
+    elif "cu_auto" in modes:
+        modes.remove("cu_auto")
     # serialized with batching: one stream, groups as in the batched schedules
     # (the same outputs bit for bit), the baseline of their concurrency gain
     for v_ in (1, 2, 4, 8):
@@ -428,7 +440,10 @@ def main():
     # phase overlap, so a tag's summed launch time counts once per stream
     def lanes_of(tag):
         return max(1, sargs.get("vlm_streams" if tag.startswith(("lm.", "vit.")) else "act_streams", 1))
-    kernel = max(timed, key=lambda k: timed[k][0] / lanes_of(k))
+    ran = [k for k in timed if timed[k][1] > 0]
+    if not ran:
+        raise SystemExit(f"none of the timed kernels ({', '.join(tags)}) runs in {args.preset}")
+    kernel = max(ran, key=lambda k: timed[k][0] / lanes_of(k))
     tot_ms, launches = timed[kernel]
     avg_s = tot_ms * 1e-3 / max(launches, 1)
     vfr, afr = max(1, sargs.get("vlm_batch", 1)), max(1, sargs.get("act_batch", 1))
@@ -523,6 +538,10 @@ def main():
             "speedup_vs_serialized": rnd(results["concurrent"]["speedup_vs_serialized"]),
             "residency": short_res("concurrent")},
         "serialized_residency": short_res("serial"),
+        "cu_auto": None if (auto_plan is None or "cu_auto" not in results) else {
+            "split": f"{auto_plan['vlm_cus']}/{auto_plan['act_cus']}",
+            "predicted_frames_per_s": rnd(1.0 / auto_plan["per_frame_s"], 2),
+            "frames_per_s": rnd(results["cu_auto"]["frames_per_s"], 3)},
         "outputs_identical_across_modes": identical,
         "roofline": {k: (rnd(v, 5) if isinstance(v, float) else v) for k, v in roofline.items()},
         "mfma_util_dominant_kernel": rnd(roofline["frac"]) if roofline["bound"] == "mfma" else None,

@@ -26,7 +26,8 @@ Model (what the paper's Algorithm 1 needs, and no more):
       seen winning ties (strict comparison). GRID scales s by
       G_k / (c_k(j) + 1), REG by 1 / (c_k(j) R_k + 1), with c_k(j) the
       kernel's workgroups resident on CU j and R_k its registers per
-      workgroup.
+      workgroup, as a share of the CU's register file (from the traced VGPR
+      and AGPR counts).
 * Contention: a workgroup's progress rate on CU j is 1 / max(1, U_r[j] / 15)
   over the pipelines r it uses (tau_r > 0): a pipeline asked for more than
   one kernel's full level slows everyone on it in proportion. With one
@@ -34,7 +35,8 @@ Model (what the paper's Algorithm 1 needs, and no more):
   CU of one kernel is about its level).
 
 Readings (the paper leaves them open): U_max = 255 (the registers' 8-bit
-range); the dispatcher order is the kernels' launch order; the per-CU sum of
+range); R_k in units of a CU's register file (a raw register count would
+make any resident kernel's REG score vanish); the dispatcher order is the kernels' launch order; the per-CU sum of
 levels that saturates a pipeline is 15 (one kernel at full level), and a
 kernel's tau is split evenly over its resident workgroups on a CU
 (tau_r / o_k per workgroup).
@@ -45,6 +47,11 @@ import heapq
 import math
 from dataclasses import dataclass
 from typing import Dict, List, Optional, Sequence, Tuple
+
+try:  # as a module of the package, or as a script next to intensity.py
+    from .intensity import reg_share
+except ImportError:
+    from intensity import reg_share
 
 U_MAX = 255
 LEVEL = 15
@@ -57,7 +64,7 @@ class Kernel:
     occupancy: int          # workgroups that fit on one CU
     wg_seconds: float       # run time of one workgroup alone
     tau: Tuple[int, int, int] = (0, 0, 0)
-    regs: int = 0           # registers per workgroup (REG variant)
+    regs: float = 0.0       # R_k of the REG variant: the workgroup's share of a CU's registers
 
 
 @dataclass
@@ -275,8 +282,9 @@ def from_descriptors(desc: Sequence[dict], num_cus: int, frames: int, limit: Opt
                 continue
             n = int(round(d["launches_per_frame"]))
             o = max(1, int(d.get("wgs_per_cu", 1)))
+            regs = reg_share(int(d.get("wg_threads", 256)), int(d.get("vgpr", 0)), int(d.get("agpr", 0)))
             k = Kernel(d["kernel"], int(d["workgroups"]), o,
-                       wg_seconds(d["us"] * 1e-6, int(d["workgroups"]), o, num_cus), tuple(d["tau"]))
+                       wg_seconds(d["us"] * 1e-6, int(d["workgroups"]), o, num_cus), tuple(d["tau"]), regs)
             for i in range(n):
                 items.append(((i + 0.5) / n, k))
         items.sort(key=lambda x: x[0])

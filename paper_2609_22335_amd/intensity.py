@@ -71,20 +71,37 @@ def read_trace(path: str) -> Dict[Key, List[float]]:
     return dict(out)
 
 
+# rocprofv3's VGPR_Count on gfx950 is half the registers per lane the
+# kernel allocates (VGPRs and AGPRs together), and its Accum_VGPR_Count is 0:
+# compared with the compiler's resource report of the same code objects
+# (141 -> 72, 249 -> 128, 359 -> 180, 142 -> 72), so the count is doubled.
+TRACE_VGPR_SCALE = 2
+
+
 def read_resources(path: str) -> Dict[Key, Tuple[int, int, int]]:
     """Kernel trace CSV -> (LDS bytes, VGPRs, AGPRs) per workgroup / wave of
-    each launch configuration."""
+    each launch configuration (registers per lane as allocated)."""
     out = {}
     with open(path, newline="") as f:
         for r in csv.DictReader(f):
-            out.setdefault(_key(r), (int(r.get("LDS_Block_Size") or 0), int(r.get("VGPR_Count") or 0),
-                                     int(r.get("Accum_VGPR_Count") or 0)))
+            out.setdefault(_key(r), (int(r.get("LDS_Block_Size") or 0),
+                                     TRACE_VGPR_SCALE * int(r.get("VGPR_Count") or 0),
+                                     TRACE_VGPR_SCALE * int(r.get("Accum_VGPR_Count") or 0)))
     return out
 
 
 # CDNA4 compute unit: 4 SIMDs, 512 VGPRs (arch + accumulation) per lane per
 # SIMD, at most 8 waves per SIMD, 160 KB of LDS
 CU_SIMDS, SIMD_REGS, SIMD_WAVES, CU_LDS = 4, 512, 8, 160 * 1024
+
+
+def reg_share(wg_threads: int, vgpr: int, agpr: int) -> float:
+    """Share of a CU's register file one workgroup holds: its waves times the
+    registers per lane (VGPRs + AGPRs, allocated in granules of 8), over the
+    4 SIMDs x 512 registers per lane."""
+    waves = max(1, -(-wg_threads // 64))
+    regs = -(-(vgpr + agpr) // 8) * 8
+    return waves * regs / float(CU_SIMDS * SIMD_REGS)
 
 
 def wgs_per_cu(wg_threads: int, lds: int, vgpr: int, agpr: int) -> int:
@@ -157,6 +174,7 @@ def descriptors(trace: Dict[Key, List[float]], alu: Dict[Key, Dict[str, float]],
         lds, vgpr, agpr = (res or {}).get(k, (0, 0, 0))
         out.append({
             "kernel": k[0], "workgroups": k[1], "wg_threads": k[2], "phase": phase,
+            "vgpr": vgpr, "agpr": agpr, "lds": lds,
             "wgs_per_cu": wgs_per_cu(k[2], lds, vgpr, agpr) if vgpr else 1,
             "launches_per_frame": lpf, "us": t * 1e6,
             "frac": [tc_frac, alu_frac, mem_frac],
@@ -180,20 +198,26 @@ def load(path: str) -> List[dict]:
 # CU-split planner
 # ---------------------------------------------------------------------------
 
-def phase_time(desc: Iterable[dict], phase: str, cus: int, num_cus: int = NUM_CUS) -> float:
-    """Predicted time (s) of one frame's kernels of `phase` on `cus` CUs.
-    A launch keeps its isolated time while its workgroups all fit on the CUs
-    at once (wgs_per_cu each); beyond that its time grows with the workgroup
-    slots it had alone over the slots it gets:
-        t * max(1, min(G, num_cus * o) / (cus * o))."""
-    t = 0.0
-    for d in desc:
-        if d["phase"] != phase:
-            continue
-        o = d.get("wgs_per_cu", 1)
-        had = min(d["workgroups"], num_cus * o)
-        t += d["launches_per_frame"] * d["us"] * 1e-6 * max(1.0, had / (cus * o))
-    return t
+def kernel_time(d: dict, cus: int, rho: float = 0.0, num_cus: int = NUM_CUS) -> float:
+    """Predicted time (s) of one launch configuration's launches per frame on
+    `cus` CUs, alone. Two limits stretch its isolated time t:
+      * workgroup slots: t * min(G, num_cus o) / (cus o) when its G
+        workgroups (o per CU) no longer fit at once;
+      * bandwidth per CU: a kernel that reached a fraction f of HBM peak on
+        all CUs gets at most rho * cus / num_cus of the peak on `cus` CUs
+        (rho: how far a CU can pull above its even share), so
+        t * f num_cus / (rho cus) when that is larger (rho = 0: no limit)."""
+    o = max(1, d.get("wgs_per_cu", 1))
+    had = min(d["workgroups"], num_cus * o)
+    slot = max(1.0, had / (cus * o))
+    bw = max(1.0, d["frac"][2] * num_cus / (rho * cus)) if rho > 0 else 1.0
+    return d["launches_per_frame"] * d["us"] * 1e-6 * max(slot, bw)
+
+
+def phase_time(desc: Iterable[dict], phase: str, cus: int, num_cus: int = NUM_CUS, rho: float = 0.0) -> float:
+    """Predicted time (s) of one frame's kernels of `phase` alone on `cus`
+    CUs (the sum of kernel_time)."""
+    return sum(kernel_time(d, cus, rho, num_cus) for d in desc if d["phase"] == phase)
 
 
 def mem_level(desc: Iterable[dict], phase: str) -> float:
@@ -207,28 +231,59 @@ def mem_level(desc: Iterable[dict], phase: str) -> float:
     return s / w if w else 0.0
 
 
-def predict_split(desc: List[dict], vlm_cus: int, num_cus: int = NUM_CUS) -> dict:
+def predict_split(desc: List[dict], vlm_cus: int, num_cus: int = NUM_CUS, cal: Optional[dict] = None) -> dict:
     """Per-frame time of the pipelined two-phase schedule (prefill of frame
     r + 1 beside the actions of frame r) with the VLM stream on vlm_cus CUs
-    and the action stream on the rest. The CU sets are disjoint; HBM is not:
-    when the phases' mean DRAM fractions add up to more than 1, both stretch
-    by that sum."""
+    and the action stream on the rest.
+
+    Each phase's time alone on its CUs is phase_time (with the calibrated
+    rho); running beside each other, the longer phase sets the period and a
+    share kappa of the shorter one does not overlap (it contends for the
+    shared HBM, L2 and MALL the CU sets do not partition):
+        period = max(t_v, t_a) + kappa min(t_v, t_a).
+    Without a calibration rho = 0 and kappa = max(0, hbm_v + hbm_a - 1)
+    (the phases' summed mean HBM fractions beyond 1)."""
     act_cus = num_cus - vlm_cus
-    tv = phase_time(desc, "vlm", vlm_cus, num_cus)
-    ta = phase_time(desc, "action", act_cus, num_cus)
     share = mem_level(desc, "vlm") + mem_level(desc, "action")
-    stretch = max(1.0, share)
-    per_frame = max(tv, ta) * stretch
+    rho = cal["rho"] if cal else 0.0
+    kappa = cal["kappa"] if cal else max(0.0, share - 1.0)
+    tv = phase_time(desc, "vlm", vlm_cus, num_cus, rho)
+    ta = phase_time(desc, "action", act_cus, num_cus, rho)
+    per_frame = max(tv, ta) + kappa * min(tv, ta)
     return {"vlm_cus": vlm_cus, "act_cus": act_cus, "vlm_s": tv, "action_s": ta,
             "hbm_share": share, "per_frame_s": per_frame}
 
 
-def plan_cu_split(desc: List[dict], num_cus: int = NUM_CUS, step: int = 8) -> dict:
+def fit_calibration(desc: List[dict], measured: Dict[int, float], num_cus: int = NUM_CUS) -> dict:
+    """(rho, kappa) minimising the largest relative error of predicted
+    against measured frames/s over the measured splits ({vlm_cus: frames/s}
+    of the pipelined schedule); grid search, rho in (0, 3], kappa in [0, 1]."""
+    best = None
+    for i in range(1, 61):
+        rho = 0.05 * i
+        tv = {v: phase_time(desc, "vlm", v, num_cus, rho) for v in measured}
+        ta = {v: phase_time(desc, "action", num_cus - v, num_cus, rho) for v in measured}
+        for j in range(0, 101):
+            kappa = 0.01 * j
+            err = max(abs(1.0 / (max(tv[v], ta[v]) + kappa * min(tv[v], ta[v])) / fps - 1.0)
+                      for v, fps in measured.items())
+            if best is None or err < best["max_rel_err"] - 1e-12:
+                best = {"rho": rho, "kappa": kappa, "max_rel_err": err}
+    best["measured_fps"] = {str(v): f for v, f in measured.items()}
+    return best
+
+
+def plan_cu_split(desc: List[dict], num_cus: int = NUM_CUS, step: int = 8, cal: Optional[dict] = None) -> dict:
     """The split (multiples of `step`, both phases at least `step` CUs) with
     the smallest predicted per-frame time; ties go to more VLM CUs."""
     best = None
     for v in range(num_cus - step, step - 1, -step):
-        p = predict_split(desc, v, num_cus)
+        p = predict_split(desc, v, num_cus, cal)
         if best is None or p["per_frame_s"] < best["per_frame_s"] * (1 - 1e-12):
             best = p
     return best
+
+
+def load_calibration(path: str) -> Optional[dict]:
+    with open(path) as f:
+        return json.load(f)["meta"].get("calibration")

@@ -13,7 +13,8 @@ then FETCH_SIZE, then WRITE_SIZE; a plain device copy of known size scales
 the two byte counters. Launches per frame come from the difference of two
 traces that differ by two frames. The descriptors (intensity.py) go to
 `--out`, followed by the CU split that intensity.plan_cu_split picks for the
-one-frame pipeline.
+one-frame pipeline; with `--fit` the planner is first calibrated on the
+measured CU splits of a bench.py run (intensity.fit_calibration).
 
 With `--run vlm|action|copy` the script is the profiled workload itself.
 """
@@ -92,9 +93,25 @@ def rocprof(work: str, name: str, args, pmc=None, timeout=240) -> str:
     return d
 
 
-def profile(preset: str, out: str, work: str, collect: bool = True) -> None:
+def measured_splits(path: str) -> dict:
+    """{VLM CUs: frames/s} of the CU-split schedules (cu_V_A) in a bench.py
+    detail file."""
+    import json
+    modes = json.load(open(path))["modes"]
+    out = {}
+    for name, r in modes.items():
+        parts = name.split("_")
+        if len(parts) == 3 and parts[0] == "cu" and parts[1].isdigit() and parts[2].isdigit():
+            out[int(parts[1])] = r["frames_per_s"]
+    return out
+
+
+def profile(preset: str, out: str, work: str, collect: bool = True, fit: str = "") -> None:
     """Run the passes (collect) and build the descriptor file from their
-    outputs under `work`; with collect=False only the second part."""
+    outputs under `work`; with collect=False only the second part. With
+    `fit` (a bench.py detail file holding cu_V_A schedules of the same
+    preset), the planner's calibration is fitted to those measured splits
+    and stored with the descriptors."""
     out, work = os.path.abspath(out), os.path.abspath(work)  # the passes run in /tmp
     os.makedirs(work, exist_ok=True)
     me = os.path.abspath(__file__)
@@ -120,8 +137,9 @@ def profile(preset: str, out: str, work: str, collect: bool = True) -> None:
                              for p in ("alu", "fetch", "write"))
         desc += intensity.descriptors(large, alu, fetch, write, calib["FETCH_SIZE"], calib["WRITE_SIZE"], counts, phase,
                                       res)
-    plan = intensity.plan_cu_split(desc)
-    meta = {"preset": preset, "peaks": {"mfma_bf16": intensity.PEAK_MFMA_BF16, "mfma_f32": intensity.PEAK_MFMA_F32,
+    cal = intensity.fit_calibration(desc, measured_splits(fit)) if fit else None
+    plan = intensity.plan_cu_split(desc, cal=cal)
+    meta = {"preset": preset, "calibration": cal, "peaks": {"mfma_bf16": intensity.PEAK_MFMA_BF16, "mfma_f32": intensity.PEAK_MFMA_F32,
                                         "valu_f32": intensity.PEAK_VALU_F32, "hbm": intensity.PEAK_HBM},
             "counters": ALU_COUNTERS + ["FETCH_SIZE", "WRITE_SIZE"], "byte_scale": calib,
             "frames": [SMALL, LARGE], "cu_split_plan": plan}
@@ -138,11 +156,12 @@ def main() -> None:
     ap.add_argument("--run", choices=["vlm", "action", "copy"], help="be the profiled workload")
     ap.add_argument("--frames", type=int, default=LARGE)
     ap.add_argument("--build-only", action="store_true", help="only build the file from the passes under --work")
+    ap.add_argument("--fit", default="", help="bench.py detail file with cu_V_A schedules: fit the planner to them")
     a = ap.parse_args()
     if a.run:
         run_workload(a.run, a.preset, a.frames)
     else:
-        profile(a.preset, a.out, a.work, collect=not a.build_only)
+        profile(a.preset, a.out, a.work, collect=not a.build_only, fit=a.fit)
 
 
 if __name__ == "__main__":

@@ -100,13 +100,42 @@ def test_planner_worked_case():
     assert p["hbm_share"] == pytest.approx(0.2)
 
 
-def test_planner_hbm_stretch_and_weights():
+def test_planner_hbm_share_and_weights():
     # two launches per frame of the action kernel count twice; DRAM
-    # fractions 0.7 (VLM) and 0.6 (action, time-weighted) exceed 1 together,
-    # so both phases stretch by 1.3
+    # fractions 0.7 (VLM) and 0.6 (action, time-weighted) exceed 1 together
+    # by 0.3: without a calibration that share of the shorter phase does not
+    # overlap
     desc = [_d("vlm", 64, 100.0, mem=0.7), _d("action", 8, 50.0, lpf=2.0, mem=0.9), _d("action", 8, 100.0, mem=0.3)]
     assert I.mem_level(desc, "action") == pytest.approx((100 * 0.9 + 100 * 0.3) / 200)
     p = I.predict_split(desc, 128)
     assert p["vlm_s"] == pytest.approx(100e-6) and p["action_s"] == pytest.approx(200e-6)
-    assert p["per_frame_s"] == pytest.approx(200e-6 * 1.3)
+    assert p["per_frame_s"] == pytest.approx(200e-6 + 0.3 * 100e-6)
     assert math.isclose(p["hbm_share"], 1.3)
+
+
+def test_kernel_time_bandwidth_limit():
+    # a kernel at 40% of HBM peak on 256 CUs: with rho = 0.8 its CUs deliver
+    # at most 0.8 * C / 256 of the peak, so on 64 CUs it stretches by
+    # 0.4 * 256 / (0.8 * 64) = 2 (its 8 workgroups still fit)
+    d = _d("action", 8, 10.0, mem=0.4)
+    assert I.kernel_time(d, 256, 0.8) == pytest.approx(10e-6)
+    assert I.kernel_time(d, 64, 0.8) == pytest.approx(20e-6)
+    assert I.kernel_time(d, 64, 0.0) == pytest.approx(10e-6)
+    # the slot limit wins where it is larger: 64 workgroups at 1 per CU on 16 CUs
+    assert I.kernel_time(_d("vlm", 64, 10.0, mem=0.1), 16, 0.8) == pytest.approx(40e-6)
+
+
+def test_fit_calibration_recovers_the_model():
+    # frames/s generated by the model itself with rho = 0.5, kappa = 0.4 are
+    # fitted back exactly, and the planner then picks the generated optimum
+    # (the action kernels' bandwidth term binds on every split, so rho is
+    # identifiable)
+    desc = [_d("vlm", 512, 100.0, mem=0.3), _d("action", 64, 60.0, lpf=3.0, mem=0.6),
+            _d("action", 25, 20.0, lpf=2.0, mem=0.05)]
+    cal = {"rho": 0.5, "kappa": 0.4}
+    meas = {v: 1.0 / I.predict_split(desc, v, cal=cal)["per_frame_s"] for v in (224, 192, 160, 128, 96)}
+    fit = I.fit_calibration(desc, meas)
+    assert fit["rho"] == pytest.approx(0.5) and fit["kappa"] == pytest.approx(0.4)
+    assert fit["max_rel_err"] < 1e-9
+    best = I.plan_cu_split(desc, cal=fit)
+    assert best["vlm_cus"] == I.plan_cu_split(desc, cal=cal)["vlm_cus"]
