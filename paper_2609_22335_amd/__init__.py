@@ -18,7 +18,9 @@ from typing import Dict, Iterable, Optional, Sequence, Tuple
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libvla.so")
+# the in-tree build; VLA_LIBRARY names another build of the same library
+# (a tuning variant, say) to load instead
+LIB_PATH = os.environ.get("VLA_LIBRARY") or os.path.join(_HERE, "libvla.so")
 
 VLA_F32, VLA_BF16 = 0, 1
 MODE_SERIAL, MODE_CONCURRENT, MODE_CU_MASKED, MODE_WG_CAPPED = 0, 1, 2, 3

@@ -240,8 +240,23 @@ struct AttnKvDesc {
   const void* k0f[MAX_FRAMES] = {};
   const void* v0f[MAX_FRAMES] = {};
   size_t k1_blk = 0, v1_blk = 0, out_blk = 0;
+  // Room for key splits (optional): with part (part_floats floats) and cnt
+  // (cnt_n counters, zero before the first launch; every launch leaves them
+  // zero) a query tile's key blocks are split over several workgroups (at
+  // most one block per wave each) whose partials the last one to finish
+  // merges in split order. Without it each tile is one workgroup. The
+  // result does not depend on the arrival order, only on the split count,
+  // which depends on the shapes alone. Launches sharing part / cnt must not
+  // overlap.
+  float* part = nullptr;
+  size_t part_floats = 0;
+  unsigned* cnt = nullptr;
+  int cnt_n = 0;
 };
 hipError_t launch_attention_kv(const AttnKvDesc& d, const LaunchCaps& caps, hipStream_t st);
+// Floats of partials (and, in *counters, the counters) a launch of these
+// shapes needs for its key splits; 0 when it runs unsplit.
+size_t attn_kv_split_floats(int dtype, int frames, int Sq, int nq, int nkv, int hd, int S0, int S1, int* counters);
 hipError_t launch_attention(const AttnDesc& a, const Scratch& s, const LaunchCaps& caps, hipStream_t st);
 
 // Residual add + row norm: x[m] += bias + colscale * sum_s part[s][m] (split

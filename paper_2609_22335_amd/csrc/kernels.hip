@@ -165,6 +165,24 @@ constexpr int VMCNT0 = 0x0F70;
 __device__ __forceinline__ float bld1(Rsrc r, uint32_t off) {
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0));
 }
+// Loads and stores with the sc1 cache policy (the one agent-scope atomic
+// loads and stores get): stores write through to the memory side and loads
+// are served from it, so data one workgroup writes is seen by a workgroup on
+// another XCD, whose L2 is a different cache.
+constexpr int CP_SC1 = 16;
+__device__ __forceinline__ f32x4 bld16_sc1(Rsrc r, uint32_t off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, CP_SC1));
+}
+__device__ __forceinline__ float bld1_sc1(Rsrc r, uint32_t off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, CP_SC1));
+}
+__device__ __forceinline__ void bst16_sc1(Rsrc r, uint32_t off, f32x4 v) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, off, 0, CP_SC1);
+}
+__device__ __forceinline__ void bst1_sc1(Rsrc r, uint32_t off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, off, 0, CP_SC1);
+}
 
 // ---------------------------------------------------------------------------
 // GEMM epilogues
@@ -1288,11 +1306,26 @@ GemmPlan plan_gemm(const GemmDesc& g) {
     return p;
   }
   const TileCfg* cfgs = g.dtype == DT_BF16 ? kBf16Cfg : kF32Cfg;
+  // The 256 x 256 tile does about twice the work per CU-cycle of the
+  // 128 x 128 tile (one workgroup per CU at ~3,600 cycles per K-step against
+  // two at ~3,900), so where it leaves CUs idle it can still win: with the
+  // epilogues that take its short paths (GeGLU, store, GELU, swish) it is
+  // also chosen when its rounds of tiles take fewer cycles than the 128
+  // tile's, counting ~18K cycles of epilogue per 256 tile. The tile does not
+  // change any sum (same BK, same splits), only which workgroup computes it.
+  const int kb64 = (g.K + 63) / 64;
+  const bool cheap_epi = g.epi.kind == EPI_GEGLU || g.epi.kind == EPI_T || g.epi.kind == EPI_GELU ||
+                         g.epi.kind == EPI_SWISH;
   auto choose = [&](int M) {
     if (g.dtype == DT_BF16) {
       const int t128 = ((M + 127) / 128) * ((g.N + 127) / 128);
       const int t256 = ((M + 255) / 256) * ((g.N + 255) / 256);
       if (M >= 1024 && t256 >= NUM_CU_PLAN) return 3;
+      if (M >= 1024 && cheap_epi) {
+        const long long c256 = (long long)((t256 + NUM_CU_PLAN - 1) / NUM_CU_PLAN) * (kb64 * 3600LL + 18000);
+        const long long c128 = (long long)((t128 + 2 * NUM_CU_PLAN - 1) / (2 * NUM_CU_PLAN)) * (kb64 * 3900LL);
+        if (c256 < c128) return 3;
+      }
       if (M >= 256 && t128 >= NUM_CU_PLAN) return 0;
       return M > 32 ? 1 : 2;
     }
@@ -1795,9 +1828,23 @@ struct Attn2Args {
   int nb0, nb1;  // 32-key blocks per KV head in each segment's buffers
   int rtiles;    // 16-row tiles of packed rows per KV head
   float scale_log2;
+  // key splits: split s of a query tile takes blocks [s bps, (s + 1) bps);
+  // with nsplit > 1 its partial (row max, sum, unnormalised O) goes to
+  // part and the last split to arrive merges them (see the kernel)
+  int nsplit, bps;
+  float* part;
+  unsigned* cnt;
 };
 
 constexpr float ATT_TAU = 8.f;  // lazy-rescaling slack, log2 units
+// key splits (attn2_plan): 32-key blocks per wave and split, most splits,
+// workgroups beyond which a launch takes no more splits
+#ifndef VLA_ATT_BPW
+#define VLA_ATT_BPW 4
+#endif
+constexpr int ATT_BPW = VLA_ATT_BPW;
+constexpr int ATT_MAX_SPLITS = 8;
+constexpr int ATT_SPLIT_WGS = 512;
 
 // waves per workgroup: eight, or four where a wave needs more than the 256
 // registers eight waves leave it
@@ -1832,9 +1879,13 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
   const T dummy = T();
   const Rsrc rq = rsrc(a.q, span(a.Sq * a.frames, a.ldq, a.nq * a.hd, sizeof(T)));
 
-  for (int w = blockIdx.x; w < total * a.frames; w += gridDim.x) {
-    // frame f: its queries, its two key segments and its output block
-    const int f = __builtin_amdgcn_readfirstlane(w / total), wl = w % total;
+  __shared__ int sLast;
+  for (int w = blockIdx.x; w < total * a.frames * a.nsplit; w += gridDim.x) {
+    // item w: split sp of query tile wt; frame f: its queries, its two key
+    // segments and its output block
+    const int sp = w % a.nsplit, wt = w / a.nsplit;
+    const int f = __builtin_amdgcn_readfirstlane(wt / total), wl = wt % total;
+    const int b_lo = sp * a.bps, b_hi = min(nblk, b_lo + a.bps);
     const int rt = wl % a.rtiles, j = wl / a.rtiles;
     const Rsrc rk0 = rsrc(a.k0[f], (size_t)a.nkv * a.nb0 * 2 * ns * FRAG * sizeof(T));
     const Rsrc rv0 = rsrc(a.v0[f], (size_t)a.nkv * a.nb0 * ndt * PVS * FRAG * sizeof(T));
@@ -1857,7 +1908,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
       qld[u] = bld16(rq, ok ? (uint32_t)(((size_t)sq * a.ldq + h * a.hd + d) * sizeof(T)) : OOB);
     }
 
-    // fragment loads of one 32-key block (b past the end reads zeros)
+    // fragment loads of one 32-key block (b past the split's end reads zeros)
     auto load_k = [&](int b, uint4 (&kf)[2][NQF]) {
       const bool seg1 = b >= a.nb0;
       const int bl = seg1 ? b - a.nb0 : b, nb = seg1 ? a.nb1 : a.nb0;
@@ -1866,7 +1917,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
       for (int nt = 0; nt < 2; ++nt)
 #pragma unroll
         for (int ks = 0; ks < NQF; ++ks) {
-          const bool ok = b < nblk && ks * SW + g4 * VEC < a.hd;
+          const bool ok = b < b_hi && ks * SW + g4 * VEC < a.hd;
           const size_t off = ((((size_t)j * nb + bl) * 2 + nt) * ns + ks) * FRAG + lane * VEC;
           kf[nt][ks] = bld16(rk, ok ? (uint32_t)(off * sizeof(T)) : OOB);
         }
@@ -1879,7 +1930,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
       for (int dt = 0; dt < NOT; ++dt)
 #pragma unroll
         for (int kk = 0; kk < PVS; ++kk) {
-          const bool ok = b < nblk && dt * 16 + (lane & 15) < a.hd;
+          const bool ok = b < b_hi && dt * 16 + (lane & 15) < a.hd;
           const size_t off = ((((size_t)j * nb + bl) * ndt + dt) * PVS + kk) * FRAG + lane * VEC;
           vf[dt][kk] = bld16(rv, ok ? (uint32_t)(off * sizeof(T)) : OOB);
         }
@@ -1888,8 +1939,8 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
     // Loads are issued unconditionally: with the same loads in flight on
     // every path each wait covers only the oldest group.
     uint4 kf[2][NQF], vf[NOT][PVS];
-    load_k(wave, kf);
-    load_v(wave, vf);
+    load_k(b_lo + wave, kf);
+    load_v(b_lo + wave, vf);
 
     float mrun = -INFINITY, lpart = 0.f;  // running max of this lane's query; partial sum
     f32x4 o[NOT];
@@ -1984,7 +2035,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
       load_v(b + NW, vf);
     };
 
-    for (int b = wave; b < nblk; b += NW) process(b);
+    for (int b = b_lo + wave; b < b_hi; b += NW) process(b);
 
     // the four lane groups' partial sums of one query
     lpart = wave_sum_x16_x32(lpart);
@@ -1998,6 +2049,29 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
     }
     __syncthreads();
     // merge the waves in order; eight consecutive outputs per thread
+    constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
+    auto store_out = [&](int prow, int d0, const float (&num)[8], float den) {
+      const float inv = 1.f / den;
+      const int sq = prow / group, col = (j * group + prow % group) * a.hd + d0;
+      // 16-byte pieces: one VEC group each in the row-block operand layout
+      auto at = [&](int c) {
+        return (T*)a.out + f * a.out_blk + (a.out_afrag ? afrag_index(DT, sq, c) : (size_t)sq * a.ldo + c);
+      };
+      if constexpr (sizeof(T) == 2) {
+        uint32_t pk[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) pk[e] = f2bf2(num[2 * e] * inv, num[2 * e + 1] * inv);
+        *(uint4*)at(col) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+      } else {
+        *(float4*)at(col) = make_float4(num[0] * inv, num[1] * inv, num[2] * inv, num[3] * inv);
+        *(float4*)at(col + 4) = make_float4(num[4] * inv, num[5] * inv, num[6] * inv, num[7] * inv);
+      }
+    };
+    // a split's partial: [16 rows][HDP] unnormalised O, then 16 row maxima
+    // and 16 sums
+    constexpr int PSZ = 16 * HDP + 32;
+    const Rsrc rp = rsrc(a.part, a.nsplit > 1 ? (size_t)total * a.frames * a.nsplit * PSZ * sizeof(float) : 0);
+    const uint32_t mybase = (uint32_t)(((size_t)wt * a.nsplit + sp) * PSZ);
     for (int idx = tid * 8; idx < 16 * HDP; idx += NT * 8) {
       const int rr = idx / HDP, d0 = idx % HDP;
       const int prow = rt * 16 + rr;
@@ -2020,21 +2094,72 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
         }
         den += wgt * sL[u][rr];
       }
-      const float inv = 1.f / den;
-      const int sq = prow / group, col = (j * group + prow % group) * a.hd + d0;
-      // 16-byte pieces: one VEC group each in the row-block operand layout
-      auto at = [&](int c) {
-        constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
-        return (T*)a.out + f * a.out_blk + (a.out_afrag ? afrag_index(DT, sq, c) : (size_t)sq * a.ldo + c);
-      };
-      if constexpr (sizeof(T) == 2) {
-        uint32_t pk[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) pk[e] = f2bf2(num[2 * e] * inv, num[2 * e + 1] * inv);
-        *(uint4*)at(col) = make_uint4(pk[0], pk[1], pk[2], pk[3]);
+      if (a.nsplit == 1) {
+        store_out(prow, d0, num, den);
       } else {
-        *(float4*)at(col) = make_float4(num[0] * inv, num[1] * inv, num[2] * inv, num[3] * inv);
-        *(float4*)at(col + 4) = make_float4(num[4] * inv, num[5] * inv, num[6] * inv, num[7] * inv);
+        const uint32_t o = (mybase + rr * HDP + d0) * 4;
+        bst16_sc1(rp, o, f32x4{num[0], num[1], num[2], num[3]});
+        bst16_sc1(rp, o + 16, f32x4{num[4], num[5], num[6], num[7]});
+        if (d0 == 0) {
+          bst1_sc1(rp, (mybase + 16 * HDP + rr) * 4, mx);
+          bst1_sc1(rp, (mybase + 16 * HDP + 16 + rr) * 4, den);
+        }
+      }
+    }
+    if (a.nsplit > 1) {
+      // Every thread's partial stores have completed (vmcnt counts stores
+      // on this architecture) before thread 0 counts this split in; the
+      // split that counts last sees every other split's stores done and
+      // merges. No split waits for another: the last arrival does the work.
+      __builtin_amdgcn_s_waitcnt(VMCNT0);
+      __syncthreads();
+      if (tid == 0) {
+        const unsigned old = __hip_atomic_fetch_add(a.cnt + wt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        sLast = old == (unsigned)(a.nsplit - 1);
+        // the counter goes back to zero for the next launch (and graph replay)
+        if (sLast) __hip_atomic_store(a.cnt + wt, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      __syncthreads();
+      if (sLast) {
+        const uint32_t tile = (uint32_t)((size_t)wt * a.nsplit * PSZ);
+        for (int idx = tid * 8; idx < 16 * HDP; idx += NT * 8) {
+          const int rr = idx / HDP, d0 = idx % HDP;
+          const int prow = rt * 16 + rr;
+          if (prow >= R || d0 >= a.hd) continue;
+          // every split's values in flight at once; splits past nsplit read
+          // zeros and are skipped below
+          float mq[ATT_MAX_SPLITS], lq[ATT_MAX_SPLITS];
+          f32x4 oq[ATT_MAX_SPLITS][2];
+#pragma unroll
+          for (int q = 0; q < ATT_MAX_SPLITS; ++q) {
+            const bool ok = q < a.nsplit;
+            const uint32_t b = tile + q * PSZ;
+            oq[q][0] = bld16_sc1(rp, ok ? (b + rr * HDP + d0) * 4 : OOB);
+            oq[q][1] = bld16_sc1(rp, ok ? (b + rr * HDP + d0 + 4) * 4 : OOB);
+            mq[q] = bld1_sc1(rp, ok ? (b + 16 * HDP + rr) * 4 : OOB);
+            lq[q] = bld1_sc1(rp, ok ? (b + 16 * HDP + 16 + rr) * 4 : OOB);
+          }
+          // splits in order: the result does not depend on the arrival order
+          float mx = -INFINITY;
+#pragma unroll
+          for (int q = 0; q < ATT_MAX_SPLITS; ++q)
+            if (q < a.nsplit) mx = fmaxf(mx, mq[q]);
+          float num[8], den = 0.f;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) num[e] = 0.f;
+#pragma unroll
+          for (int q = 0; q < ATT_MAX_SPLITS; ++q) {
+            if (q >= a.nsplit) continue;
+            const float wgt = mq[q] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mq[q] - mx);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              num[e] += wgt * oq[q][0][e];
+              num[4 + e] += wgt * oq[q][1][e];
+            }
+            den += wgt * lq[q];
+          }
+          store_out(prow, d0, num, den);
+        }
       }
     }
     __syncthreads();
@@ -2042,10 +2167,51 @@ __global__ __launch_bounds__(64 * NW) void k_attn2(Attn2Args a) {
   VLA_WAVE_END(KK_ATTN2);
 }
 
+// Key splits of the cache attention. A split gives each wave ATT_BPW 32-key
+// blocks; there are at most ATT_MAX_SPLITS of them, and splits stop where the
+// launch would exceed ATT_SPLIT_WGS workgroups (enough query tiles fill the
+// chip without them). Returns the split count and the blocks per split.
+static int attn2_plan(int nblk, int nw, int tiles, int* bps) {
+  int ns = std::min((nblk + nw * ATT_BPW - 1) / (nw * ATT_BPW), ATT_MAX_SPLITS);
+  while (ns > 1 && tiles * ns > ATT_SPLIT_WGS) --ns;
+  if (ns <= 1) {
+    *bps = nblk;
+    return 1;
+  }
+  // balanced splits of whole wave rounds
+  const int per = (nblk + ns - 1) / ns;
+  *bps = (per + nw - 1) / nw * nw;
+  return (nblk + *bps - 1) / *bps;
+}
+
+// a launch uses splits only when the caller gave room for their partials and
+// counters (otherwise one split, the whole key range)
+template <typename T, int H>
+static void attn2_split(Attn2Args& a, float* part, size_t part_floats, unsigned* cnt, int cnt_n) {
+  const int nblk = a.nb0 + a.nb1;
+  const int tiles = a.rtiles * a.nkv * a.frames;
+  int bps;
+  int ns = attn2_plan(nblk, att2_waves<T, H>(), tiles, &bps);
+  if (ns > 1 && (!part || !cnt || cnt_n < tiles || (size_t)tiles * ns * (16 * H + 32) > part_floats)) ns = 1;
+  a.nsplit = ns;
+  a.bps = ns > 1 ? bps : nblk;
+  a.part = part;
+  a.cnt = cnt;
+}
+
 template <typename T>
-static hipError_t run_attn2_t(const Attn2Args& a, int hdp, const LaunchCaps& caps, hipStream_t st) {
+static hipError_t run_attn2_t(Attn2Args& a, int hdp, const LaunchCaps& caps, hipStream_t st, float* part,
+                              size_t part_floats, unsigned* cnt, int cnt_n) {
   if (sizeof(T) == 4 && hdp > 128) return hipErrorInvalidValue;  // fp32: head dim <= 128
-  int grid = a.rtiles * a.nkv * a.frames;
+  switch (hdp) {
+    case 32: attn2_split<T, 32>(a, part, part_floats, cnt, cnt_n); break;
+    case 64: attn2_split<T, 64>(a, part, part_floats, cnt, cnt_n); break;
+    case 96: attn2_split<T, 96>(a, part, part_floats, cnt, cnt_n); break;
+    case 128: attn2_split<T, 128>(a, part, part_floats, cnt, cnt_n); break;
+    case 256: attn2_split<T, 256>(a, part, part_floats, cnt, cnt_n); break;
+    default: return hipErrorInvalidValue;
+  }
+  int grid = a.rtiles * a.nkv * a.frames * a.nsplit;
   if (caps.max_wgs > 0) grid = std::min(grid, caps.max_wgs);
 #define VLA_ATTN2(H)                                                                           \
   hipExtLaunchKernelGGL((k_attn2<T, H, att2_waves<T, H>()>), dim3(grid),                        \
@@ -2102,8 +2268,21 @@ hipError_t launch_attention_kv(const AttnKvDesc& d, const LaunchCaps& caps, hipS
   a.nb1 = (d.S1 + 31) / 32;
   a.rtiles = (d.Sq * (d.nq / d.nkv) + 15) / 16;
   a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)d.hd));
-  if (d.dtype == DT_BF16) return run_attn2_t<uint16_t>(a, hdp, caps, st);
-  return run_attn2_t<float>(a, hdp, caps, st);
+  if (d.dtype == DT_BF16) return run_attn2_t<uint16_t>(a, hdp, caps, st, d.part, d.part_floats, d.cnt, d.cnt_n);
+  return run_attn2_t<float>(a, hdp, caps, st, d.part, d.part_floats, d.cnt, d.cnt_n);
+}
+
+size_t attn_kv_split_floats(int dtype, int frames, int Sq, int nq, int nkv, int hd, int S0, int S1, int* counters) {
+  const int hdp = attn_hdp(hd, dtype);
+  *counters = 0;
+  if (hdp < 0 || nkv <= 0 || nq % nkv) return 0;
+  const int nw = dtype == DT_BF16 ? (hdp * 2 >= 512 ? 4 : 8) : (hdp * 4 >= 512 ? 4 : 8);
+  const int nblk = (S0 + 31) / 32 + (S1 + 31) / 32;
+  const int tiles = (Sq * (nq / nkv) + 15) / 16 * nkv * frames;
+  int bps;
+  const int ns = attn2_plan(nblk, nw, tiles, &bps);
+  *counters = ns > 1 ? tiles : 0;
+  return ns > 1 ? (size_t)tiles * ns * (16 * hdp + 32) : 0;
 }
 
 // ---------------------------------------------------------------------------

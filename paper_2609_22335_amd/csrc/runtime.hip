@@ -275,6 +275,12 @@ struct ActWs {
   void *kown = nullptr, *vown = nullptr, *att = nullptr, *mlp = nullptr;
   float* xg = nullptr;      // chunks written by graph replays, copied out afterwards
   float* nstage = nullptr;  // noise staged for graph replays
+  // key-split partials and counters of the cache attention (counters zero
+  // between launches)
+  float* apart = nullptr;
+  size_t apart_floats = 0;
+  unsigned* acnt = nullptr;
+  int acnt_n = 0;
   size_t blk_xop = 0, blk_de = 0, blk_att = 0, blk_mlp = 0, blk_k = 0, blk_v = 0;
   Scratch scr;
 };
@@ -712,9 +718,16 @@ static int gemm_rm(const Run& r, const char* tag, const void* A, int lda, const 
   return VLA_OK;
 }
 
-static int attn_kv(const Run& r, const char* tag, const AttnKvDesc& a) {
+static int attn_kv(const Run& r, const char* tag, const AttnKvDesc& a0) {
   LaunchCaps caps = r.caps;
   VLA_TRY(timer_events(r, tag, &caps));
+  AttnKvDesc a = a0;
+  if (r.aw) {  // action phases: the lane's room for key splits
+    a.part = r.aw->apart;
+    a.part_floats = r.aw->apart_floats;
+    a.cnt = r.aw->acnt;
+    a.cnt_n = r.aw->acnt_n;
+  }
   hipError_t err = launch_attention_kv(a, caps, r.st);
   if (err != hipSuccess) return fail(VLA_EHIP, std::string("attention: ") + hipGetErrorString(err));
   return VLA_OK;
@@ -1653,6 +1666,31 @@ static int add_act_lane(vla_model* m) {
   upd(sa, gemm_scratch(dt, F * H, c.action_dim, de, false, true));
   upd(sa, attn_scratch(dt, H, c.lm_heads, c.lm_kv_heads, c.head_dim, P, H, 1));
   VLA_TRY(alloc_scratch(m, sa, &a.scr));
+  {
+    // the largest cache-attention launch of this head (all frames of a batched loop)
+    int nc = 0;
+    size_t nf = 0;
+    if (c.head == VLA_HEAD_PI0)
+      nf = attn_kv_split_floats(dt, F, H, c.lm_heads, c.lm_kv_heads, c.head_dim, P, H, &nc);
+    else if (c.head == VLA_HEAD_DIT)
+      nf = std::max(attn_kv_split_floats(dt, 1, H, c.ex_heads, c.ex_heads, d.ehd, P, 0, &nc),
+                    attn_kv_split_floats(dt, 1, H, c.ex_heads, c.ex_heads, d.ehd, H, 0, &nc));
+    else
+      nf = attn_kv_split_floats(dt, 1, S, c.ex_heads, c.ex_heads, d.ehd, S, 0, &nc);
+    if (c.head == VLA_HEAD_DIT) {  // counters for the larger of the two launches
+      int n1 = 0, n2 = 0;
+      attn_kv_split_floats(dt, 1, H, c.ex_heads, c.ex_heads, d.ehd, P, 0, &n1);
+      attn_kv_split_floats(dt, 1, H, c.ex_heads, c.ex_heads, d.ehd, H, 0, &n2);
+      nc = std::max(n1, n2);
+    }
+    if (nf) {
+      VLA_TRY(dmalloc(m, (void**)&a.apart, nf * 4));
+      a.apart_floats = nf;
+      VLA_TRY(dmalloc(m, (void**)&a.acnt, (size_t)std::max(nc, 1) * 4));
+      HIP_TRY(hipMemset(a.acnt, 0, (size_t)std::max(nc, 1) * 4));
+      a.acnt_n = nc;
+    }
+  }
   VLA_TRY(dmalloc(m, (void**)&a.xg, (size_t)F * H * c.action_dim * 4));
   VLA_TRY(dmalloc(m, (void**)&a.nstage, (size_t)F * H * c.action_dim * 4));
   m->aws.push_back(std::move(lane));
@@ -2781,7 +2819,30 @@ int vla_debug_attention_cache(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv
     a.nq = nq;
     a.nkv = nkv;
     a.hd = hd;
+    // room for key splits, as the action phases give it (zeroed counters)
+    int nc = 0;
+    const size_t nf = attn_kv_split_floats(a.dtype, 1, Sq, nq, nkv, hd, S0, S1, &nc);
+    void *part = nullptr, *cnt = nullptr;
+    if (nf) {
+      HIP_TRY(hipMalloc(&part, nf * 4));
+      hipError_t ce = hipMalloc(&cnt, (size_t)nc * 4);
+      if (ce == hipSuccess) ce = hipMemset(cnt, 0, (size_t)nc * 4);
+      if (ce != hipSuccess) {
+        hipFree(part);
+        hipFree(cnt);
+        return fail(VLA_ENOMEM, std::string("attention split room: ") + hipGetErrorString(ce));
+      }
+      a.part = (float*)part;
+      a.part_floats = nf;
+      a.cnt = (unsigned*)cnt;
+      a.cnt_n = nc;
+    }
     hipError_t e = launch_attention_kv(a, LaunchCaps{}, (hipStream_t)stream);
+    if (part) {
+      hipStreamSynchronize((hipStream_t)stream);
+      hipFree(part);
+      hipFree(cnt);
+    }
     if (e != hipSuccess) return fail(VLA_EHIP, std::string("attention: ") + hipGetErrorString(e));
     return VLA_OK;
   })

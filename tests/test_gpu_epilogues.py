@@ -84,10 +84,12 @@ CASES = [
     # and its cross K/V from the 96 feature rows
     ("qkv_plain", 1, 16, 4608, 1536, "skinny", dict(nq=32, nkv=32, hd=48, pos0=0)),
     ("qkv_plain", 1, 96, 3072, 2048, "64", dict(nq=0, nkv=32, hd=48, pos0=0)),
-    # GELU + bias: the ViT MLP (N = 4304, K = 1152) for 1, 8 and 16 views;
+    # GELU + bias: the ViT MLP (N = 4304, K = 1152) for 1, 4, 8 and 16 views
+    # (8 views: a half-empty round of 256 tiles beats two of 128);
     # the DiT MLP (N = 6144, K = 1536) on the skinny kernel
     ("gelu", 1, 256, 4304, 1152, "64", {}),
-    ("gelu", 1, 2048, 4304, 1152, "128", {}),
+    ("gelu", 1, 1024, 4304, 1152, "128", {}),
+    ("gelu", 1, 2048, 4304, 1152, "256", {}),
     ("gelu", 1, 4096, 4304, 1152, "256", {}),
     ("gelu", 1, 16, 6144, 1536, "skinny", {}),
     # swish + bias: the expert's time MLP
