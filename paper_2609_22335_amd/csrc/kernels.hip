@@ -26,10 +26,12 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int NUM_CU_PLAN = 256;  // planner constant; never the live CU count
 
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
-// Residency log (see WaveLog): one load of the log pointer at the start and
-// at the end of a workgroup; one vector atomic per record while logging. No
-// register is held between the two points.
-__device__ WaveLog* g_wavelog = nullptr;
+// Residency log (see WaveLog): the log pointer lives in constant memory, so
+// the check at the start and at the end of a workgroup is a scalar load that
+// issues beside the kernel-argument loads (a vector load there would delay
+// every workgroup's first memory round trip); one vector atomic per record
+// while logging. No register is held between the two points.
+__constant__ WaveLog* g_wavelog = nullptr;
 
 __device__ __forceinline__ void wave_event(uint32_t kind, uint32_t end) {
   WaveLog* L = g_wavelog;

@@ -139,3 +139,22 @@ def test_fit_calibration_recovers_the_model():
     assert fit["max_rel_err"] < 1e-9
     best = I.plan_cu_split(desc, cal=fit)
     assert best["vlm_cus"] == I.plan_cu_split(desc, cal=cal)["vlm_cus"]
+
+
+def test_trace_stats_table_row(tmp_path):
+    # the paper's micro-kernel table: median cycles and the shares below 5K,
+    # 10K, 25K and 50K cycles; at 2 GHz, 1 us = 2000 cycles
+    from paper_2609_22335_amd import trace_stats as T
+    rows = [["k_a", 256, 256, 0, 1_000], ["k_b", 256, 256, 0, 3_000], ["k_c", 256, 256, 0, 6_000],
+            ["k_d", 256, 256, 0, 20_000], ["k_unfrag", 256, 256, 0, 1]]
+    _write(tmp_path / "t.csv", TRACE_H, rows)
+    d = T.durations_ns(str(tmp_path / "t.csv"))
+    assert d == [1000, 3000, 6000, 20000]  # the weight re-layout is skipped
+    r = T.table_row(d, 2.0)
+    # cycles 2000, 6000, 12000, 40000: median (6000 + 12000) / 2
+    assert r["kernels"] == 4 and r["median_cyc"] == 9000
+    assert (r["lt5k_pct"], r["lt10k_pct"], r["lt25k_pct"], r["lt50k_pct"]) == (25.0, 50.0, 75.0, 100.0)
+    assert T.table_row([4999 / 2.0], 2.0)["lt5k_pct"] == 100.0  # strictly below the bound
+    assert T.table_row([5000 / 2.0], 2.0)["lt5k_pct"] == 0.0
+    with pytest.raises(ValueError):
+        T.table_row([], 2.0)
