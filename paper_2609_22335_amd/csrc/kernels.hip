@@ -202,9 +202,11 @@ __device__ __forceinline__ size_t epi_kblk(const Epi& e, int m, size_t blk) {
   return e.blk_rows > 0 ? (size_t)(m / e.blk_rows) * blk : 0;
 }
 
-template <typename T>
+// KIND >= 0 fixes the epilogue kind at compile time (only that kind's code is
+// emitted); KIND = -1 dispatches on e.kind at run time.
+template <typename T, int KIND = -1>
 __device__ __forceinline__ void epi_one(const Epi& e, int m, int n, float v) {
-  switch (e.kind) {
+  switch (KIND >= 0 ? KIND : e.kind) {
     case EPI_F32: {
       if (e.bias) v += e.bias[n];
       if (e.rowadd) v += e.rowadd[(size_t)(m % e.rowadd_period) * e.ldra + n];
@@ -259,17 +261,18 @@ __device__ __forceinline__ void epi_one(const Epi& e, int m, int n, float v) {
 }
 
 // n: a physical column with n % 32 < 16; v1 is the value of column n + 16.
-template <typename T>
+template <typename T, int KIND = -1>
 __device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int n, float v0,
                                          float v1) {
+  const int kind = KIND >= 0 ? KIND : e.kind;
   if (m >= M) return;
-  if (e.kind == EPI_GEGLU) {
+  if (kind == EPI_GEGLU) {
     if (n + 16 >= N) return;
     const int g = n >> 5, j = n & 15;
     TT<T>::st((T*)e.out + out_at<T>(e, m, 16 * g + j, e.ldo, e.blk_out), gelu_tanh(v0) * v1);
     return;
   }
-  if (e.kind == EPI_QKV_ROPE) {
+  if (kind == EPI_QKV_ROPE) {
     if (n + 16 >= N) return;
     const int hd = e.hd, qcols = e.nq * hd, kcols = e.nkv * hd;
     if (n < qcols + kcols) {
@@ -299,8 +302,8 @@ __device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int 
     }
     return;
   }
-  if (n < N) epi_one<T>(e, m, n, v0);
-  if (n + 16 < N) epi_one<T>(e, m, n + 16, v1);
+  if (n < N) epi_one<T, KIND>(e, m, n, v0);
+  if (n + 16 < N) epi_one<T, KIND>(e, m, n + 16, v1);
 }
 
 // The epilogue of PER column pairs of one thread (pair k: row m[k], columns
@@ -310,10 +313,10 @@ __device__ __forceinline__ void epi_pair(const Epi& e, int M, int N, int m, int 
 // memory counter keeps loads and stores in one issue order, so a load placed
 // after a store waits for that store's write to complete, and one epi_pair
 // after another would serialise on them. Rows m[k] >= M are skipped.
-template <typename T, int PER>
+template <typename T, int PER, int KIND = -1>
 __device__ __forceinline__ void epi_pairs(const Epi& e, int M, int N, const int (&m)[PER],
                                           const int (&n)[PER], float (&v0)[PER], float (&v1)[PER]) {
-  const int kind = e.kind;
+  const int kind = KIND >= 0 ? KIND : e.kind;
   const bool biased = kind == EPI_F32 || kind == EPI_T || kind == EPI_RESID || kind == EPI_GELU ||
                       kind == EPI_SWISH || kind == EPI_EULER;
   if (biased && e.bias) {
@@ -402,7 +405,7 @@ __device__ __forceinline__ void epi_pairs(const Epi& e, int M, int N, const int 
           TT<T>::st(dst + kv_kidx(DT, e.kv_nb, hd, head, key, i + hd / 2), b);
         }
       } else {
-        epi_pair<T>(e, M, N, m[k], n[k], v0[k], v1[k]);  // V columns: stores only
+        epi_pair<T, KIND>(e, M, N, m[k], n[k], v0[k], v1[k]);  // V columns: stores only
       }
     }
     return;
@@ -412,7 +415,7 @@ __device__ __forceinline__ void epi_pairs(const Epi& e, int M, int N, const int 
   f.bias = nullptr;
   f.rowadd = nullptr;
 #pragma unroll
-  for (int k = 0; k < PER; ++k) epi_pair<T>(f, M, N, m[k], n[k], v0[k], v1[k]);
+  for (int k = 0; k < PER; ++k) epi_pair<T, KIND>(f, M, N, m[k], n[k], v0[k], v1[k]);
 }
 
 // ---------------------------------------------------------------------------
@@ -1087,7 +1090,10 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__
 // frames of a tile are consecutive tile indices, and with the XCD-aware
 // order below they run on one XCD at the same time, so the weights come
 // from HBM once and from that XCD's L2 for the other frame.
-template <typename T, int SPW>
+// One instantiation per epilogue kind (KIND): the action loop launches these
+// kernels back to back, and each carries only its own epilogue's code, which
+// keeps the code the loop runs small enough to stay in the instruction cache.
+template <typename T, int SPW, int KIND>
 __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, size_t a_blk, int frames,
                                                 const T* __restrict__ Wf, int KS, int ks0, int M,
                                                 int N, int K, int splits, Epi e,
@@ -1164,13 +1170,13 @@ __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, size_t 
       mg[r] = m < M ? f * M + m : Mt;  // row over all frames (Mt: skipped)
       nn[r] = n;
     }
-    if (splits == 1 && e.kind != EPI_PART) {
-      epi_pairs<T, 4>(e, Mt, N, mg, nn, v0, v1);
+    if (KIND != EPI_PART && splits == 1) {
+      epi_pairs<T, 4, KIND>(e, Mt, N, mg, nn, v0, v1);
     } else {
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         if (mg[r] >= Mt) continue;
-        float* P = (e.kind == EPI_PART ? (float*)e.out : part) + (size_t)s * Mt * N + (size_t)mg[r] * N;
+        float* P = (KIND == EPI_PART ? (float*)e.out : part) + (size_t)s * Mt * N + (size_t)mg[r] * N;
         if (n < N) P[n] = v0[r];
         if (n + 16 < N) P[n + 16] = v1[r];
       }
@@ -1251,12 +1257,12 @@ int skinny_splits(const GemmDesc& g) {
   return std::max(1, (g.K + per_wg - 1) / per_wg);
 }
 
-template <typename T, int SPW>
+template <typename T, int SPW, int KIND>
 static hipError_t run_skinny_t(const GemmDesc& g, int splits, const Scratch& s,
                                const LaunchCaps& caps, hipStream_t st) {
   int grid = ((g.N + 31) / 32) * splits * g.frames;
   if (caps.max_wgs > 0) grid = std::min(grid, caps.max_wgs);
-  hipExtLaunchKernelGGL((k_skinny<T, SPW>), dim3(grid), dim3(256), 0, st, caps.ev_start,
+  hipExtLaunchKernelGGL((k_skinny<T, SPW, KIND>), dim3(grid), dim3(256), 0, st, caps.ev_start,
                         caps.ev_stop, 0, (const T*)g.A, g.a_blk, g.frames, (const T*)g.W, g.frag_ks,
                         g.frag_ks0, g.M, g.N, g.K, splits, g.epi, s.ptr);
   if (splits > 1 && g.epi.kind != EPI_PART) {
@@ -1267,6 +1273,24 @@ static hipError_t run_skinny_t(const GemmDesc& g, int splits, const Scratch& s,
     k_splitk_reduce<T><<<rgrid, 256, 0, st>>>(s.ptr, splits, Mt, g.N, g.epi);
   }
   return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t run_skinny_kind(const GemmDesc& g, int splits, const Scratch& s, const LaunchCaps& caps,
+                                  hipStream_t st) {
+  switch (g.epi.kind) {
+    case EPI_F32: return run_skinny_t<T, 8, EPI_F32>(g, splits, s, caps, st);
+    case EPI_T: return run_skinny_t<T, 8, EPI_T>(g, splits, s, caps, st);
+    case EPI_RESID: return run_skinny_t<T, 8, EPI_RESID>(g, splits, s, caps, st);
+    case EPI_GELU: return run_skinny_t<T, 8, EPI_GELU>(g, splits, s, caps, st);
+    case EPI_SWISH: return run_skinny_t<T, 8, EPI_SWISH>(g, splits, s, caps, st);
+    case EPI_GEGLU: return run_skinny_t<T, 8, EPI_GEGLU>(g, splits, s, caps, st);
+    case EPI_QKV_ROPE: return run_skinny_t<T, 8, EPI_QKV_ROPE>(g, splits, s, caps, st);
+    case EPI_QKV_PLAIN: return run_skinny_t<T, 8, EPI_QKV_PLAIN>(g, splits, s, caps, st);
+    case EPI_EULER: return run_skinny_t<T, 8, EPI_EULER>(g, splits, s, caps, st);
+    case EPI_PART: return run_skinny_t<T, 4, EPI_PART>(g, splits, s, caps, st);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 static hipError_t launch_skinny(const GemmDesc& g, const Scratch& s, const LaunchCaps& caps,
@@ -1281,12 +1305,8 @@ static hipError_t launch_skinny(const GemmDesc& g, const Scratch& s, const Launc
   } else if (splits > 1 && need > s.floats) {
     return hipErrorInvalidValue;
   }
-  const bool part = g.epi.kind == EPI_PART;
-  if (g.dtype == DT_BF16)
-    return part ? run_skinny_t<uint16_t, 4>(g, splits, s, caps, st)
-                : run_skinny_t<uint16_t, 8>(g, splits, s, caps, st);
-  return part ? run_skinny_t<float, 4>(g, splits, s, caps, st)
-              : run_skinny_t<float, 8>(g, splits, s, caps, st);
+  if (g.dtype == DT_BF16) return run_skinny_kind<uint16_t>(g, splits, s, caps, st);
+  return run_skinny_kind<float>(g, splits, s, caps, st);
 }
 
 struct TileCfg {
