@@ -472,8 +472,11 @@ struct GemmSmemDL {
   };
 };
 
+// KIND >= 0: the epilogue kind fixed at compile time (the tiles of the
+// batched action loops, short launches whose code should stay in the
+// instruction cache); KIND = -1: chosen at run time from e.kind.
 template <typename T, int BM, int BN, int BK, int WGM = 2, int WGN = 2, int PD = 1, int PAD = VLA_GEMM_LDS_PAD,
-          bool DL = false>
+          bool DL = false, int KIND = -1>
 __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A, int lda,
                                               const T* __restrict__ W, int ldw, int M, int N,
                                               int K, int kchunk, int splits, int tiles_m,
@@ -507,7 +510,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
   // the workgroup index gives the same results.
   // GeGLU of the direct-load tile into row-major bf16: formed in registers
   // (see below); uniform over the launch
-  const bool reg_geglu = DL && sizeof(T) == 2 && splits == 1 && e.kind == EPI_GEGLU && !e.afrag &&
+  const int ekind = KIND >= 0 ? KIND : e.kind;
+  const bool reg_geglu = DL && sizeof(T) == 2 && splits == 1 && ekind == EPI_GEGLU && !e.afrag &&
                          e.blk_rows == 0 && (((uintptr_t)e.out & 15) == 0) && e.ldo % 8 == 0;
   const int G = gridDim.x;
   const int first = G % 8 == 0 ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8) : (int)blockIdx.x;
@@ -747,8 +751,8 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
     if (reg_geglu) continue;  // stored above
     // epilogue in 16-row slices: slice i of every wave row goes through LDS,
     // then all threads apply the epilogue with row-contiguous stores
-    float* P = (e.kind == EPI_PART ? (float*)e.out : part) + (size_t)s * M * N;
-    const bool direct = splits == 1 && e.kind != EPI_PART;
+    float* P = (ekind == EPI_PART ? (float*)e.out : part) + (size_t)s * M * N;
+    const bool direct = splits == 1 && ekind != EPI_PART;
     // In the direct epilogue thread tid always owns the same two columns,
     // na and na + 16 (pair index tid % (BN / 2), since NT is a multiple of
     // BN / 2). Epilogues that only store, or that read nothing but the bias,
@@ -759,7 +763,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
     static_assert(NT % (BN / 2) == 0, "fixed columns per thread");
     const int qc = tid % (BN / 2), colc = (qc >> 4) * 32 + (qc & 15);
     const int na = n0 + colc, nb = na + 16;
-    const int ek = e.kind;
+    const int ek = ekind;
     // (the row-operand paths are left out of the largest tile, whose 128
     // accumulators per thread leave few registers; it runs the FFN GEMMs)
     constexpr bool ROWK = TM * TN < 32;
@@ -1028,7 +1032,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A
           const int row = p / (BN / 2), q = p % (BN / 2);
           const int col = (q >> 4) * 32 + (q & 15);
           const int m = m0 + (row >> 4) * WM + i * 16 + (row & 15);
-          epi_pair<T>(e, M, N, m, n0 + col, sm.c[row * CLD + col], sm.c[row * CLD + col + 16]);
+          epi_pair<T, KIND>(e, M, N, m, n0 + col, sm.c[row * CLD + col], sm.c[row * CLD + col + 16]);
         }
       } else {
         // raw fp32 partial of split s: [splits][M][N]
@@ -1392,7 +1396,7 @@ void plan_tile(const GemmDesc& g, const GemmPlan& p, int* bm, int* bn) {
 }
 
 template <typename T, int BM, int BN, int BK, int WGM = 2, int WGN = 2, int PD = 1, int PAD = VLA_GEMM_LDS_PAD,
-          bool DL = false>
+          bool DL = false, int KIND = -1>
 static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch& s,
                              const LaunchCaps& caps, hipStream_t st) {
   const int tiles_m = (g.M + BM - 1) / BM, tiles_n = (g.N + BN - 1) / BN;
@@ -1404,7 +1408,7 @@ static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch
   // 4 MB L2
   const size_t band_bytes = (size_t)BM * kchunk * sizeof(T);
   const int group_m = std::max(1, std::min(tiles_m, (int)((2u << 20) / std::max<size_t>(band_bytes, 1))));
-  hipExtLaunchKernelGGL((k_gemm<T, BM, BN, BK, WGM, WGN, PD, PAD, DL>), dim3(grid), dim3(64 * WGM * WGN), 0, st,
+  hipExtLaunchKernelGGL((k_gemm<T, BM, BN, BK, WGM, WGN, PD, PAD, DL, KIND>), dim3(grid), dim3(64 * WGM * WGN), 0, st,
                         caps.ev_start,
                         caps.ev_stop, 0, (const T*)g.A, g.lda, (const T*)g.W, g.ldw, g.M, g.N,
                         g.K, kchunk, p.splits, tiles_m, tiles_n, group_m, g.epi, s.ptr);
@@ -1415,6 +1419,18 @@ static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch
     k_splitk_reduce<T><<<rgrid, 256, 0, st>>>(s.ptr, p.splits, g.M, g.N, g.epi);
   }
   return hipGetLastError();
+}
+
+// the small tiles: the expert layers' epilogues get their own instantiations
+template <typename T, int BM, int BN, int BK>
+static hipError_t run_gemm_kind(const GemmDesc& g, const GemmPlan& p, const Scratch& s, const LaunchCaps& caps,
+                                hipStream_t st) {
+  switch (g.epi.kind) {
+    case EPI_QKV_ROPE: return run_gemm_t<T, BM, BN, BK, 2, 2, 2, VLA_GEMM_LDS_PAD, false, EPI_QKV_ROPE>(g, p, s, caps, st);
+    case EPI_GEGLU: return run_gemm_t<T, BM, BN, BK, 2, 2, 2, VLA_GEMM_LDS_PAD, false, EPI_GEGLU>(g, p, s, caps, st);
+    case EPI_PART: return run_gemm_t<T, BM, BN, BK, 2, 2, 2, VLA_GEMM_LDS_PAD, false, EPI_PART>(g, p, s, caps, st);
+    default: return run_gemm_t<T, BM, BN, BK, 2, 2, 2>(g, p, s, caps, st);
+  }
 }
 
 hipError_t launch_gemm(const GemmDesc& g, const Scratch& s, const LaunchCaps& caps,
@@ -1429,9 +1445,9 @@ hipError_t launch_gemm(const GemmDesc& g, const Scratch& s, const LaunchCaps& ca
   if (g.dtype == DT_BF16) {
     switch (p.cfg) {
       case 0: return run_gemm_t<uint16_t, 128, 128, 64, 2, 2, 3>(g, p, s, caps, st);
-      case 1: return run_gemm_t<uint16_t, 64, 64, 64, 2, 2, 2>(g, p, s, caps, st);
+      case 1: return run_gemm_kind<uint16_t, 64, 64, 64>(g, p, s, caps, st);
       case 3: return run_gemm_t<uint16_t, 256, 256, 64, 2, 4, 1, 0, true>(g, p, s, caps, st);
-      default: return run_gemm_t<uint16_t, 32, 64, 64, 2, 2, 2>(g, p, s, caps, st);
+      default: return run_gemm_kind<uint16_t, 32, 64, 64>(g, p, s, caps, st);
     }
   }
   switch (p.cfg) {
