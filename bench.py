@@ -15,7 +15,11 @@ prefills / action loops (several robots' frames through one pass). In a
 schedule whose prefills come in two or more groups (one-frame prefills, or
 groups smaller than R) a later group's prefill runs while an earlier
 group's action loop runs on another stream; with one prefill group of all R
-frames the action loops start after it.
+frames the action loops start after it. A cross-step schedule (``xs_``
+prefix) runs the timed steps as one pipeline over steps x R frames (robot
+r's frame of step j at index j R + r), so step j + 1's prefills overlap step
+j's action loops, as R robots streaming frames would; every step's chunks
+are checked to equal the first step's.
 
 `value` is the frames/s of the schedule named by ``--mode`` (fixed in
 advance, not the fastest measured one); the line also gives its speedup over
@@ -175,7 +179,7 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--R", type=int, default=8, help="robot request streams (frames per step)")
-    ap.add_argument("--mode", default="vb8_ab4_lanes2_graph",
+    ap.add_argument("--mode", default="xs_vb8_ab8_lanes2_graph",
                     help="schedule reported as `value` (auto: the fastest measured one)")
     ap.add_argument("--modes", default="serial,concurrent,cu_masked,wg_capped,serial_graph,"
                                        "concurrent_graph,lanes2_graph,lanes3_graph,batch2_graph,"
@@ -183,7 +187,10 @@ def main():
                                        "vb2_ab2_graph,vb2_ab2_lanes2_graph,vb2_ab4_graph,vb4_ab4_graph,"
                                        "vb4_ab2_lanes2_graph,vb4_ab4_lanes2_graph,vb8_ab8_graph,"
                                        "vb8_ab4_lanes2_graph,vb4_ab4_v2_lanes2_graph,"
-                                       "serial_vb8_ab4_graph,serial_vb4_ab4_graph,cu_160_96,cu_auto")
+                                       "vb8_ab8_lanes2_graph,serial_vb8_ab4_graph,serial_vb4_ab4_graph,"
+                                       "serial_vb8_ab8_graph,cu_160_96,cu_auto,xs_lanes2_graph,"
+                                       "xs_vb4_ab4_lanes2_graph,xs_vb8_ab4_graph,xs_vb8_ab4_lanes2_graph,"
+                                       "xs_vb8_ab8_lanes2_graph")
     ap.add_argument("--detail", default=os.path.join(ROOT, "gpurun_out", "bench_detail.json"),
                     help="JSON file for every schedule's numbers, residency logs and further workloads")
     ap.add_argument("--split", default="192,64", help="CU split VLM,action for cu_masked")
@@ -195,16 +202,18 @@ def main():
     ap.add_argument("--preset", default="pi0")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--extra", default="gr00t:8:serial,concurrent,cu_masked,lanes2_graph,v2_lanes2_graph,"
-                                       "vb4_ab1_lanes2_graph,vb8_ab1_lanes4_graph,vb4_ab1_v2_lanes2_graph;"
+                                       "vb4_ab1_lanes2_graph,vb8_ab1_lanes4_graph,vb4_ab1_v2_lanes2_graph,"
+                                       "xs_vb8_ab1_lanes4_graph;"
                                        "pi0_3view:32:serial,concurrent,cu_224_32,cu_192_64,cu_160_96,"
                                        "wg_cap1,wg_cap2,lanes2_graph,cu_160_96_lanes2,batch4_lanes2_graph,"
                                        "batch8_lanes2_graph,vb4_ab4_lanes2_graph,vb8_ab4_lanes2_graph,"
-                                       "vb8_ab8_lanes2_graph;"
+                                       "vb8_ab8_lanes2_graph,xs_vb8_ab8_lanes2_graph;"
                                        "pi0:8:async2_serial,async2_lanes2_graph,async2_vb8_ab4_lanes2_graph,"
-                                       "async2_vb8_ab8_lanes2_graph,async4_serial,async4_vb8_ab8_lanes2_graph;"
-                                       "pi0_ddim:8:serial,vb8_ab8_graph,vb8_ab4_lanes2_graph;"
+                                       "async2_vb8_ab8_lanes2_graph,async4_serial,async4_vb8_ab8_lanes2_graph,"
+                                       "xs_async2_vb8_ab8_lanes2_graph;"
+                                       "pi0_ddim:8:serial,vb8_ab8_graph,vb8_ab4_lanes2_graph,xs_vb8_ab8_lanes2_graph;"
                                        "cogact:8:serial,concurrent,lanes2_graph,vb8_ab1_lanes2_graph,"
-                                       "vb8_ab1_lanes4_graph",
+                                       "vb8_ab1_lanes4_graph,xs_vb8_ab1_lanes2_graph,xs_vb8_ab1_lanes4_graph",
                     help="further workloads, ';'-separated preset:R:schedule,schedule,...")
     ap.add_argument("--extra-steps", type=int, default=5)
     ap.add_argument("--residency", type=int, default=8_000_000,
@@ -309,6 +318,15 @@ def main():
     for v_ in (1, 2, 4, 8):
         for a_ in (1, 2, 4, 8):
             kw[f"serial_vb{v_}_ab{a_}_graph"] = dict(mode="serial", vlm_batch=v_, act_batch=a_, graphs=True)
+    # cross-step schedules (xs_<schedule>): the timed steps run as one pipeline
+    # over steps x R frames (robot r's frame of step j at index j R + r), so
+    # the prefills of step j + 1 run beside the action loops of step j: the
+    # steady state of R robots streaming frames under asynchronous inference
+    for name_ in list(kw):
+        kw["xs_" + name_] = dict(kw[name_], xsteps=True)
+
+    def lib_args(a):
+        return {k: v for k, v in a.items() if k != "xsteps"}
 
     def measure(preset, R, modes, steps, warmup):
         """vla_pipeline_run over R seeded frames of `preset` in each schedule."""
@@ -333,29 +351,64 @@ def main():
                 nt = torch.from_numpy(nk).cuda().contiguous()
                 chunk_bufs[k] = (nt, torch.empty_like(nt))
             return chunk_bufs[k]
+        xs_bufs = {}
+
+        def xbufs(k, n):
+            # noise and outputs of n steps: the same R frames' noise per step
+            if (k, n) not in xs_bufs:
+                nz = bufs(k)[0]
+                nx = nz.repeat(n, 1, 1).contiguous()
+                xs_bufs[(k, n)] = (nx, torch.empty_like(nx))
+            return xs_bufs[(k, n)]
         results, outputs = {}, {}
         for mode in modes:
-            kc = kw[mode].get("act_chunks", 1)
+            a = kw[mode]
+            kc = a.get("act_chunks", 1)
             noise, actions = bufs(kc)
-            print(f"[bench] {preset} mode {mode}: {warmup} warmup + {steps} timed steps of R={R}",
-                  file=sys.stderr, flush=True)
-            for _ in range(warmup):
-                V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **kw[mode])
-            torch.cuda.synchronize()
-            lib_ms = []
-            t0 = time.perf_counter()
-            for _ in range(steps):
-                t = V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **kw[mode])
-                lib_ms.append(t["wall_ms"])
-            torch.cuda.synchronize()
-            el = time.perf_counter() - t0
+            if a.get("xsteps"):
+                # one call over all steps' frames; the warm-up call has as
+                # many frames, so every graph the timed call replays is
+                # captured before it
+                print(f"[bench] {preset} mode {mode}: {steps} steps of R={R} as one pipeline (warm-up: the "
+                      f"same)", file=sys.stderr, flush=True)
+                nx, ax = xbufs(kc, steps)
+                fx = cframes * steps
+                V.vla_pipeline_run(m, fx, nx, R * steps, actions=ax, **lib_args(a))
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                t = V.vla_pipeline_run(m, fx, nx, R * steps, actions=ax, **lib_args(a))
+                torch.cuda.synchronize()
+                el = time.perf_counter() - t0
+                lib_ms = [t["wall_ms"] / steps]
+                per_frame = R * steps
+                out_all = ax.cpu().numpy().reshape(steps, R * kc, *ax.shape[1:])
+                outputs[mode] = out_all[0].copy()
+                steps_same = all(np.array_equal(out_all[j], out_all[0]) for j in range(1, steps))
+            else:
+                print(f"[bench] {preset} mode {mode}: {warmup} warmup + {steps} timed steps of R={R}",
+                      file=sys.stderr, flush=True)
+                for _ in range(warmup):
+                    V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **a)
+                torch.cuda.synchronize()
+                lib_ms = []
+                t0 = time.perf_counter()
+                for _ in range(steps):
+                    t = V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **a)
+                    lib_ms.append(t["wall_ms"])
+                torch.cuda.synchronize()
+                el = time.perf_counter() - t0
+                per_frame = R
+                outputs[mode] = actions.cpu().numpy().copy()
+                steps_same = None
             fps = steps * R / el
             results[mode] = {"frames_per_s": fps, "actions_per_s": fps * kc * cfg["chunk_len"],
                              "chunks_per_frame": kc,
                              "ms_per_step": 1e3 * el / steps,
                              "median_step_ms": float(np.median(lib_ms)), "min_step_ms": float(np.min(lib_ms)),
-                             "vlm_ms_per_frame": t["vlm_ms"] / R, "action_ms_per_frame": t["act_ms"] / R}
-            outputs[mode] = actions.cpu().numpy().copy()
+                             "vlm_ms_per_frame": t["vlm_ms"] / per_frame,
+                             "action_ms_per_frame": t["act_ms"] / per_frame}
+            if steps_same is not None:
+                results[mode]["steps_identical"] = steps_same
         # speedup over the serialized schedule with as many chunks per frame
         for mode in results:
             kc = kw[mode].get("act_chunks", 1)
@@ -376,6 +429,9 @@ def main():
         a_, b_ = [[outputs[m0] for m0 in outputs if grp(m0) == g_] for g_ in ("one_frame", "batched")]
         if a_ and b_:
             identical["max_abs_diff_batched_vs_one_frame"] = float(np.abs(a_[0] - b_[0]).max())
+        xs_ = [m0 for m0 in results if "steps_identical" in results[m0]]
+        if xs_:  # cross-step schedules: every step's chunks equal the first step's
+            identical["cross_step_every_step"] = all(results[m0]["steps_identical"] for m0 in xs_)
         noise, actions = chunk_bufs[1]
         return cfg, m, results, outputs, identical, (cframes, noise, actions)
 
@@ -389,8 +445,21 @@ def main():
 
     def overlaps(name):
         """Both phases can run at once: two streams, and a later prefill group
-        exists to run beside an earlier group's action loop."""
-        return kw[name].get("mode") != "serial" and n_prefill_groups(name) >= 2
+        exists to run beside an earlier group's action loop (in a cross-step
+        schedule the next step's prefills)."""
+        return kw[name].get("mode") != "serial" and (n_prefill_groups(name) >= 2 or kw[name].get("xsteps", False))
+
+    def run_once(name, nxs=4):
+        """One pipeline run of a schedule outside the timed steps (a
+        cross-step schedule over nxs steps' frames)."""
+        a = kw[name]
+        if a.get("xsteps"):
+            kc = a.get("act_chunks", 1)
+            nz = noise.repeat(nxs, 1, 1).contiguous() if kc == 1 else None
+            if nz is None:
+                raise SystemExit("cross-step schedules with several chunks per frame are not logged")
+            return V.vla_pipeline_run(m, cframes * nxs, nz, R * nxs, actions=torch.empty_like(nz), **lib_args(a))
+        return V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **a)
 
     def same_batching_serial(name):
         a = kw[name]
@@ -413,7 +482,7 @@ def main():
         logged = ["serial", "concurrent", "cu_masked", "wg_capped", "lanes2_graph", best_ovl, args.mode]
         for name in dict.fromkeys(x for x in logged if x and x in kw):
             V.vla_wavelog_read(m, 0)
-            V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **kw[name])
+            run_once(name)
             rec, n = V.vla_wavelog_read(m, args.residency)
             full = cu_residency(rec, window=(int(rec["t"].min()), int(rec["t"].max())))
             ovl = cu_residency(rec)
@@ -432,8 +501,11 @@ def main():
     for tag in tags:
         print(f"[bench] kernel timer on {tag} in {args.mode}", file=sys.stderr, flush=True)
         V.vla_kernel_timer(m, tag)
-        for _ in range(args.steps):
-            V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **sargs)
+        if sargs.get("xsteps"):
+            run_once(args.mode, args.steps)
+        else:
+            for _ in range(args.steps):
+                V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **sargs)
         timed[tag] = V.vla_kernel_timer_read(m)
         V.vla_kernel_timer(m, None)
     # dominant: the most stream time; launches of concurrent lanes of one
@@ -458,6 +530,20 @@ def main():
                 "frac": ach / peak, "traffic": measured_traffic(args.preset, R, kernel, args.mode),
                 "kernel": kernel, "schedule": args.mode, "avg_us": avg_s * 1e6, "launches": launches,
                 "algorithmic_bytes": byts, "flops": flops}
+    if sargs.get("xsteps") and args.mode[3:] in kw:
+        # the same kernel in the per-step schedule, where the prefill of a
+        # step has the chip to itself (in the cross-step schedule it shares
+        # the CUs with the previous step's action loops)
+        base = args.mode[3:]
+        V.vla_kernel_timer(m, kernel)
+        for _ in range(args.steps):
+            V.vla_pipeline_run(m, cframes, noise, R, actions=actions, **kw[base])
+        b_ms, b_n = V.vla_kernel_timer_read(m)
+        V.vla_kernel_timer(m, None)
+        b_s = b_ms * 1e-3 / max(b_n, 1)
+        b_ach = (byts / b_s / 1e9) if hbm_bound else (flops / b_s / 1e12)
+        roofline["per_step_schedule"] = {"schedule": base, "avg_us": b_s * 1e6, "achieved": b_ach,
+                                         "frac": b_ach / peak, "launches": b_n}
     roofline_detail = dict(roofline, gpu_ms_per_step_by_tag={k: v[0] / args.steps for k, v in timed.items()},
                            stream_ms_per_step_by_tag={k: v[0] / args.steps / lanes_of(k) for k, v in timed.items()})
     outs = outputs[args.mode]
@@ -543,7 +629,9 @@ def main():
             "predicted_frames_per_s": rnd(1.0 / auto_plan["per_frame_s"], 2),
             "frames_per_s": rnd(results["cu_auto"]["frames_per_s"], 3)},
         "outputs_identical_across_modes": identical,
-        "roofline": {k: (rnd(v, 5) if isinstance(v, float) else v) for k, v in roofline.items()},
+        "roofline": {k: (rnd(v, 5) if isinstance(v, float) else
+                         {k2: (rnd(v2, 5) if isinstance(v2, float) else v2) for k2, v2 in v.items()}
+                         if isinstance(v, dict) else v) for k, v in roofline.items()},
         "mfma_util_dominant_kernel": rnd(roofline["frac"]) if roofline["bound"] == "mfma" else None,
         "cpu_baseline": None if cpu is None else {
             "value": rnd(cpu["value"], 6), "unit": cpu["unit"], "cores": cpu["cores"], "kind": "oracle",

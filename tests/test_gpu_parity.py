@@ -623,6 +623,41 @@ def test_pipeline_modes_bit_identical(V, cfg):
             assert np.abs(bref[i] - want).max() <= chunk_bound(cfg, want)
 
 
+@pytest.mark.parametrize("cfg", [synth.micro(synth.BF16), synth.TINY], ids=["micro-bf16", "tiny"])
+def test_pipeline_cross_step(V, cfg):
+    """Several steps of R robots as one pipeline (robot r's frame of step j
+    at index j R + r), so step j + 1's prefills run beside step j's action
+    loops: every step's chunks equal those of one step run alone, for batched
+    and one-frame action loops, eager and replayed graphs (graphs three
+    times, with eager work in between)."""
+    g = G()
+    R, K = 8, 3
+    g.say(f"cross-step pipeline dtype={cfg['dtype']} R={R} steps={K}")
+    frames = [synth.make_frame(cfg, 5, r) for r in range(R)]
+    dfs = [g.DevFrame(f) for f in frames]
+    noise = torch.stack([d.noise for d in dfs]).contiguous()
+    noise_k = noise.repeat(K, 1, 1).contiguous()
+    scheds = [dict(vlm_batch=8, act_batch=8, act_streams=2, graphs=True),
+              dict(vlm_batch=8, act_batch=4, act_streams=2, graphs=True),
+              dict(vlm_batch=4, act_batch=4, act_streams=3),
+              dict(act_streams=2, graphs=True)]
+    with g.model(cfg, 5) as m:
+        for kw in scheds:
+            name = "".join(f"/{k}={v}" for k, v in kw.items())
+            one = torch.full_like(noise, float("nan"))
+            V.vla_pipeline_run(m, [d.c for d in dfs], noise, R, mode="concurrent", actions=one, **kw)
+            one = one.cpu().numpy()
+            assert np.isfinite(one).all(), name
+            for rep in range(3 if kw.get("graphs") else 1):
+                g.say(f"cross-step {name} replay {rep}")
+                out = torch.full_like(noise_k, float("nan"))
+                V.vla_pipeline_run(m, [d.c for d in dfs] * K, noise_k, R * K, mode="concurrent", actions=out, **kw)
+                out = out.cpu().numpy().reshape(K, R, *noise.shape[1:])
+                for j in range(K):
+                    assert np.array_equal(out[j], one), (name, rep, j)
+                g.run_frame(m, cfg, frames[rep])  # eager work between replays
+
+
 def test_abi_errors_on_device(V):
     g = G()
     cfg = synth.micro()
