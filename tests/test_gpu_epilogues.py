@@ -105,9 +105,11 @@ CASES = [
     ("step", 1, 400, 32, 1024, "64", dict(xs=1.0, dt=-0.1)),
     ("step", 0, 8, 8, 128, "skinny", dict(xs=1.0, dt=-0.25)),
     # split-K partials + residual + RMSNorm: the LM's down projection
-    # (K = 16384) and O projection, the expert's down and O projections
+    # (K = 16384) and O projection, the expert's down and O projections; the
+    # 256 tile's partials (two splits of a 32 x 8 grid of tiles)
     ("resid_norm", 1, 305, 2048, 16384, "64", {}),
     ("resid_norm", 1, 2440, 2048, 16384, "128", {}),
+    ("resid_norm", 1, 8192, 2048, 1024, "256", {}),
     ("resid_norm", 1, 305, 2048, 2048, "64", {}),
     ("resid_norm", 1, 50, 1024, 4096, "skinny", {}),
     ("resid_norm", 1, 50, 1024, 2048, "skinny", {}),
