@@ -285,6 +285,13 @@ def main():
                                                            act_streams=l_, graphs=True)
             kw[f"vb{v_}_ab{a_}_v2_lanes2_graph"] = dict(mode="concurrent", vlm_batch=v_, act_batch=a_,
                                                         vlm_streams=2, act_streams=2, graphs=True)
+            for c_ in (1, 2, 3):  # VLM workgroups capped at c_ per CU
+                kw[f"vb{v_}_ab{a_}_lanes2_cap{c_}_graph"] = dict(mode="wg_capped", vlm_wg_cap=c_, vlm_batch=v_,
+                                                                act_batch=a_, act_streams=2, graphs=True)
+            for cv_, ca_ in ((224, 32), (192, 64)):  # disjoint CU sets
+                kw[f"vb{v_}_ab{a_}_lanes2_cu_{cv_}_{ca_}_graph"] = dict(
+                    mode="cu_masked", vlm_cus=cv_, act_cus=ca_, vlm_batch=v_, act_batch=a_, act_streams=2,
+                    graphs=True)
     # asynchronous inference: k action chunks per VLM output
     for k_ in (2, 4):
         kw[f"async{k_}_serial"] = dict(mode="serial", act_chunks=k_)
