@@ -1421,15 +1421,16 @@ static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch
   return hipGetLastError();
 }
 
-// the small tiles: the expert layers' epilogues get their own instantiations
-template <typename T, int BM, int BN, int BK>
+// the 4-wave tiles: the decoder layers' epilogues (QKV-RoPE, GeGLU, split-K
+// partials) get their own instantiations, the rest share the run-time one
+template <typename T, int BM, int BN, int BK, int PD>
 static hipError_t run_gemm_kind(const GemmDesc& g, const GemmPlan& p, const Scratch& s, const LaunchCaps& caps,
                                 hipStream_t st) {
   switch (g.epi.kind) {
-    case EPI_QKV_ROPE: return run_gemm_t<T, BM, BN, BK, 2, 2, 2, VLA_GEMM_LDS_PAD, false, EPI_QKV_ROPE>(g, p, s, caps, st);
-    case EPI_GEGLU: return run_gemm_t<T, BM, BN, BK, 2, 2, 2, VLA_GEMM_LDS_PAD, false, EPI_GEGLU>(g, p, s, caps, st);
-    case EPI_PART: return run_gemm_t<T, BM, BN, BK, 2, 2, 2, VLA_GEMM_LDS_PAD, false, EPI_PART>(g, p, s, caps, st);
-    default: return run_gemm_t<T, BM, BN, BK, 2, 2, 2>(g, p, s, caps, st);
+    case EPI_QKV_ROPE: return run_gemm_t<T, BM, BN, BK, 2, 2, PD, VLA_GEMM_LDS_PAD, false, EPI_QKV_ROPE>(g, p, s, caps, st);
+    case EPI_GEGLU: return run_gemm_t<T, BM, BN, BK, 2, 2, PD, VLA_GEMM_LDS_PAD, false, EPI_GEGLU>(g, p, s, caps, st);
+    case EPI_PART: return run_gemm_t<T, BM, BN, BK, 2, 2, PD, VLA_GEMM_LDS_PAD, false, EPI_PART>(g, p, s, caps, st);
+    default: return run_gemm_t<T, BM, BN, BK, 2, 2, PD>(g, p, s, caps, st);
   }
 }
 
@@ -1444,10 +1445,10 @@ hipError_t launch_gemm(const GemmDesc& g, const Scratch& s, const LaunchCaps& ca
   }
   if (g.dtype == DT_BF16) {
     switch (p.cfg) {
-      case 0: return run_gemm_t<uint16_t, 128, 128, 64, 2, 2, 3>(g, p, s, caps, st);
-      case 1: return run_gemm_kind<uint16_t, 64, 64, 64>(g, p, s, caps, st);
+      case 0: return run_gemm_kind<uint16_t, 128, 128, 64, 3>(g, p, s, caps, st);
+      case 1: return run_gemm_kind<uint16_t, 64, 64, 64, 2>(g, p, s, caps, st);
       case 3: return run_gemm_t<uint16_t, 256, 256, 64, 2, 4, 1, 0, true>(g, p, s, caps, st);
-      default: return run_gemm_kind<uint16_t, 32, 64, 64>(g, p, s, caps, st);
+      default: return run_gemm_kind<uint16_t, 32, 64, 64, 2>(g, p, s, caps, st);
     }
   }
   switch (p.cfg) {
