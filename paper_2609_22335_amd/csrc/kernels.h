@@ -129,6 +129,25 @@ struct Epi {
   // and RoPE positions pos0 + m % blk_rows. Row-major outputs use row m.
   int blk_rows = 0;
   size_t blk_out = 0, blk_xop = 0, blk_k = 0, blk_v = 0;
+  // RMSNorm folded across a split-K skinny GEMM and the next skinny GEMM
+  // (one frame, M <= 64, N <= 64 x 32):
+  // * producer (EPI_PART with norm_g set): the last split to arrive for a
+  //   32-column pair sums the pair's partials in split order into the fp32
+  //   residual x (ldx), writes norm_out = T(x * norm_g) (per column; in the
+  //   row-block operand layout when afrag) and the pair's per-row sum of
+  //   squares rowss[pair][m]. cnt: one counter per pair, zero before the
+  //   first launch and left at zero;
+  // * consumer (any other kind, rowss set): the product of each row m is
+  //   scaled by 1 / sqrt(sum over the rowss_n pairs of rowss[pair][m] /
+  //   rowss_d + 1e-6) before the epilogue; the pairs are summed in a fixed
+  //   order. Since the scale is per row it commutes with the product, so
+  //   the two launches compute the RMSNorm of x with gain norm_g followed
+  //   by the GEMM, with T rounding before the scale instead of after.
+  const float* norm_g = nullptr;
+  void* norm_out = nullptr;
+  float* rowss = nullptr;
+  int rowss_n = 0, rowss_d = 0;
+  unsigned* cnt = nullptr;
 };
 
 struct GemmDesc {

@@ -185,6 +185,9 @@ __device__ __forceinline__ void bst16_sc1(Rsrc r, uint32_t off, f32x4 v) {
 __device__ __forceinline__ void bst1_sc1(Rsrc r, uint32_t off, float v) {
   __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, off, 0, CP_SC1);
 }
+__device__ __forceinline__ f32x4 bld4f(Rsrc r, uint32_t off) {
+  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
 
 // ---------------------------------------------------------------------------
 // GEMM epilogues
@@ -1088,6 +1091,66 @@ __global__ __launch_bounds__(256) void k_splitk_reduce(const float* __restrict__
 // epilogues go through the split-K reduce kernel.
 // ---------------------------------------------------------------------------
 
+// The last split of a 32-column pair of a folded-norm producer (one frame):
+// thread t takes row t / 4 and columns 8 (t % 4) .. + 7 of the pair; the
+// pair's split partials are summed in split order (all loads in flight at
+// once) and added to the residual x, as the norm kernel adds them; then the
+// operand x * g and the row's sum of squares over the pair's columns (eight
+// in order per thread, then the row's four threads in order) are written.
+template <typename T>
+__device__ __forceinline__ void fold_pair(const Epi& e, int np, int M, int N, int splits, int tid,
+                                          float (&sPart)[64][4]) {
+  constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
+  constexpr int MAXS = 8;  // splits (checked on the host)
+  const int row = tid >> 2, c0 = np * 32 + (tid & 3) * 8;
+  const bool ok = row < M && c0 < N;
+  const Rsrc rp = rsrc(e.out, (size_t)splits * M * N * 4);
+  f32x4 pa[MAXS], pb[MAXS];
+#pragma unroll
+  for (int q = 0; q < MAXS; ++q) {
+    const uint32_t off = (uint32_t)((((size_t)q * M + row) * N + c0) * 4);
+    const bool okq = ok && q < splits;
+    pa[q] = bld16_sc1(rp, okq ? off : OOB);
+    pb[q] = bld16_sc1(rp, okq ? off + 16 : OOB);
+  }
+  const Rsrc rx = rsrc(e.x, span(M, e.ldx, N, 4));
+  const Rsrc rg = rsrc(e.norm_g, (size_t)N * 4);
+  const uint32_t xo = (uint32_t)(((size_t)row * e.ldx + c0) * 4);
+  f32x4 xa = bld4f(rx, ok ? xo : OOB), xb = bld4f(rx, ok ? xo + 16 : OOB);
+  const f32x4 ga = bld4f(rg, ok ? (uint32_t)(c0 * 4) : OOB), gb = bld4f(rg, ok ? (uint32_t)(c0 * 4 + 16) : OOB);
+  f32x4 sa = {0.f, 0.f, 0.f, 0.f}, sb = sa;
+#pragma unroll
+  for (int q = 0; q < MAXS; ++q)
+    if (q < splits) {
+      sa += pa[q];
+      sb += pb[q];
+    }
+  xa += sa;
+  xb += sb;
+  float ss = 0.f;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) ss += xa[k] * xa[k];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) ss += xb[k] * xb[k];
+  if (ok) {
+    *(f32x4*)(e.x + (size_t)row * e.ldx + c0) = xa;
+    *(f32x4*)(e.x + (size_t)row * e.ldx + c0 + 4) = xb;
+    const f32x4 ya = xa * ga, yb = xb * gb;
+    if constexpr (sizeof(T) == 2) {
+      *(uint4*)((T*)e.norm_out + afrag_index(DT, row, c0)) =
+          make_uint4(f2bf2(ya[0], ya[1]), f2bf2(ya[2], ya[3]), f2bf2(yb[0], yb[1]), f2bf2(yb[2], yb[3]));
+    } else {
+      *(f32x4*)((T*)e.norm_out + afrag_index(DT, row, c0)) = ya;
+      *(f32x4*)((T*)e.norm_out + afrag_index(DT, row, c0 + 4)) = yb;
+    }
+  }
+  sPart[row][tid & 3] = ss;
+  __syncthreads();
+  if ((tid & 3) == 0 && row < M)
+    e.rowss[(size_t)np * M + row] = ((sPart[row][0] + sPart[row][1]) + sPart[row][2]) + sPart[row][3];
+  __syncthreads();  // sPart is free again
+}
+
 // Frames (a batched action phase): `frames` row blocks of M rows, block f of
 // A at A + f a_blk elements. Every (column pair, K-range) tile is computed
 // once per frame by its own workgroup, exactly as in a one-frame call; the
@@ -1118,6 +1181,26 @@ __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, size_t 
   const int G = gridDim.x;
   const int first = frames > 1 && G % 8 == 0 ? (int)(blockIdx.x % 8) * (G / 8) + (int)(blockIdx.x / 8)
                                              : (int)blockIdx.x;
+  // Folded RMSNorm (see Epi::rowss). Consumer: thread t holds the partial
+  // sums of squares of row t / 4 for the pairs congruent to t % 4 (mod 4),
+  // requested before the first tile's loads (waiting for those covers them)
+  // and turned into the rows' scales at the first epilogue.
+  __shared__ float sPart[64][4];
+  __shared__ float sInv[64];
+  __shared__ int sLast;
+  constexpr int SSQ = 16;  // pairs per thread: at most 64 pairs
+  const bool rowscale = KIND != EPI_PART && e.rowss != nullptr;
+  const int srow = tid >> 2, squ = tid & 3;
+  float ssq[SSQ];
+  if (rowscale) {
+    const Rsrc rs = rsrc(e.rowss, (size_t)e.rowss_n * M * 4);
+#pragma unroll
+    for (int k = 0; k < SSQ; ++k) {
+      const int p = squ + 4 * k;
+      ssq[k] = bld1(rs, p < e.rowss_n && srow < M ? (uint32_t)(((size_t)p * M + srow) * 4) : OOB);
+    }
+  }
+  bool inv_ready = false;
   for (int w = first; w < total; w += G) {
     const int f = w % frames, wt = w / frames;
     const int s = wt % splits, np = wt / splits;
@@ -1174,15 +1257,62 @@ __global__ __launch_bounds__(256) void k_skinny(const T* __restrict__ A, size_t 
       mg[r] = m < M ? f * M + m : Mt;  // row over all frames (Mt: skipped)
       nn[r] = n;
     }
+    if (rowscale) {
+      if (!inv_ready) {
+        float t = 0.f;
+#pragma unroll
+        for (int k = 0; k < SSQ; ++k) t += ssq[k];  // pairs in increasing order (absent ones read 0)
+        sPart[srow][squ] = t;
+        __syncthreads();
+        if (squ == 0)
+          sInv[srow] = 1.f / sqrtf((((sPart[srow][0] + sPart[srow][1]) + sPart[srow][2]) + sPart[srow][3]) /
+                                       e.rowss_d + 1e-6f);
+        __syncthreads();
+        inv_ready = true;
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = mt * 16 + (lane >> 4) * 4 + r;
+        const float sc = sInv[m];
+        v0[r] *= sc;
+        v1[r] *= sc;
+      }
+    }
     if (KIND != EPI_PART && splits == 1) {
       epi_pairs<T, 4, KIND>(e, Mt, N, mg, nn, v0, v1);
     } else {
+      const bool fold = KIND == EPI_PART && e.norm_g != nullptr;
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         if (mg[r] >= Mt) continue;
         float* P = (KIND == EPI_PART ? (float*)e.out : part) + (size_t)s * Mt * N + (size_t)mg[r] * N;
-        if (n < N) P[n] = v0[r];
-        if (n + 16 < N) P[n + 16] = v1[r];
+        if (fold) {
+          // write-through: the pair's last split, on any XCD, reads them
+          if (n < N) __hip_atomic_store((uint32_t*)P + n, __float_as_uint(v0[r]), __ATOMIC_RELAXED,
+                                        __HIP_MEMORY_SCOPE_AGENT);
+          if (n + 16 < N) __hip_atomic_store((uint32_t*)P + n + 16, __float_as_uint(v1[r]), __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+          if (n < N) P[n] = v0[r];
+          if (n + 16 < N) P[n + 16] = v1[r];
+        }
+      }
+      if constexpr (KIND == EPI_PART) {
+        if (fold) {
+          // Every thread's partial stores have completed (vmcnt counts
+          // stores here) before thread 0 counts this split in; the split
+          // that counts last finishes the pair. No split waits for another.
+          __builtin_amdgcn_s_waitcnt(VMCNT0);
+          __syncthreads();
+          if (tid == 0) {
+            const unsigned old = __hip_atomic_fetch_add(e.cnt + np, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            sLast = old == (unsigned)(splits - 1);
+            // back to zero for the next launch (and graph replay)
+            if (sLast) __hip_atomic_store(e.cnt + np, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
+          __syncthreads();
+          if (sLast) fold_pair<T>(e, np, M, N, splits, tid, sPart);
+        }
       }
     }
   }
@@ -1304,6 +1434,17 @@ static hipError_t launch_skinny(const GemmDesc& g, const Scratch& s, const Launc
     return hipErrorInvalidValue;
   const int splits = skinny_splits(g);
   const size_t need = (size_t)splits * g.M * g.frames * g.N;
+  const Epi& e = g.epi;
+  // folded RMSNorm (Epi::rowss): one frame; a producer's partials in at most
+  // 8 splits, whole 8-column groups, its operand output in the row-block
+  // layout; a consumer's product unsplit (the scale precedes the epilogue)
+  if (e.kind == EPI_PART && e.norm_g &&
+      (g.frames != 1 || splits > 8 || g.N % 8 || (g.N + 31) / 32 > 64 || !e.x || e.ldx < g.N || !e.norm_out ||
+       !e.rowss || !e.cnt || !e.afrag))
+    return hipErrorInvalidValue;
+  if (e.kind != EPI_PART && e.rowss &&
+      (g.frames != 1 || splits != 1 || e.rowss_n < 1 || e.rowss_n > 64 || e.rowss_d < 1))
+    return hipErrorInvalidValue;
   if (g.epi.kind == EPI_PART) {
     if (!g.epi.out || need > (size_t)g.epi.ldo) return hipErrorInvalidValue;
   } else if (splits > 1 && need > s.floats) {
@@ -1423,14 +1564,14 @@ static hipError_t run_gemm_t(const GemmDesc& g, const GemmPlan& p, const Scratch
 
 // the 4-wave tiles: the decoder layers' epilogues (QKV-RoPE, GeGLU, split-K
 // partials) get their own instantiations, the rest share the run-time one
-template <typename T, int BM, int BN, int BK, int PD>
+template <typename T, int BM, int BN, int BK, int PD, int PAD = VLA_GEMM_LDS_PAD, bool DL = false>
 static hipError_t run_gemm_kind(const GemmDesc& g, const GemmPlan& p, const Scratch& s, const LaunchCaps& caps,
                                 hipStream_t st) {
   switch (g.epi.kind) {
-    case EPI_QKV_ROPE: return run_gemm_t<T, BM, BN, BK, 2, 2, PD, VLA_GEMM_LDS_PAD, false, EPI_QKV_ROPE>(g, p, s, caps, st);
-    case EPI_GEGLU: return run_gemm_t<T, BM, BN, BK, 2, 2, PD, VLA_GEMM_LDS_PAD, false, EPI_GEGLU>(g, p, s, caps, st);
-    case EPI_PART: return run_gemm_t<T, BM, BN, BK, 2, 2, PD, VLA_GEMM_LDS_PAD, false, EPI_PART>(g, p, s, caps, st);
-    default: return run_gemm_t<T, BM, BN, BK, 2, 2, PD>(g, p, s, caps, st);
+    case EPI_QKV_ROPE: return run_gemm_t<T, BM, BN, BK, 2, 2, PD, PAD, DL, EPI_QKV_ROPE>(g, p, s, caps, st);
+    case EPI_GEGLU: return run_gemm_t<T, BM, BN, BK, 2, 2, PD, PAD, DL, EPI_GEGLU>(g, p, s, caps, st);
+    case EPI_PART: return run_gemm_t<T, BM, BN, BK, 2, 2, PD, PAD, DL, EPI_PART>(g, p, s, caps, st);
+    default: return run_gemm_t<T, BM, BN, BK, 2, 2, PD, PAD, DL>(g, p, s, caps, st);
   }
 }
 
@@ -2345,9 +2486,6 @@ __device__ __forceinline__ float block_sum(float v, float* red) {
 // the first use, so a row costs one memory round trip.
 constexpr int NORM_VPT = 2;  // four-column groups per thread: d <= 2048
 
-__device__ __forceinline__ f32x4 bld4f(Rsrc r, uint32_t off) {
-  return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
-}
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_norm(NormDesc n) {

@@ -281,9 +281,15 @@ struct ActWs {
   size_t apart_floats = 0;
   unsigned* acnt = nullptr;
   int acnt_n = 0;
+  // one-frame expert layers fold each RMSNorm into the GEMMs around it
+  // (Epi::rowss): the per-pair row sums of squares [pair][row] and the pair
+  // counters of the split-K producers (zero between launches)
+  float* rowss = nullptr;
+  unsigned* pcnt = nullptr;
   size_t blk_xop = 0, blk_de = 0, blk_att = 0, blk_mlp = 0, blk_k = 0, blk_v = 0;
   Scratch scr;
 };
+constexpr int FOLD_MAX_PAIRS = 64;  // expert width <= 64 x 32
 
 struct vla_ctx {
   vla_model* m = nullptr;
@@ -800,6 +806,33 @@ static int gemm_part(const Run& r, const char* tag, const void* A, int lda, int 
   return gemm(r, tag, A, lda, W, M, N, K, e, 0, fr);
 }
 
+// Split-K skinny GEMM whose partials the kernel itself adds to the residual
+// x, leaving h = x * gain (row-block operand layout) and the rows' sums of
+// squares for the next GEMM: an RMSNorm folded across two launches (see
+// Epi::rowss). One frame.
+static int gemm_part_fold(const Run& r, const char* tag, const void* A, int lda, int W, int M, int N, int K,
+                          float* x, int g, void* h) {
+  Epi e;
+  e.kind = EPI_PART;
+  e.out = r.scr->ptr;
+  e.ldo = (int)std::min<size_t>(r.scr->floats, (size_t)INT32_MAX);
+  e.x = x;
+  e.ldx = N;
+  e.norm_g = r.m->f32(g);
+  e.norm_out = h;
+  e.afrag = 1;
+  e.rowss = r.aw->rowss;
+  e.cnt = r.aw->pcnt;
+  return gemm(r, tag, A, lda, W, M, N, K, e, 0, Frames());
+}
+
+// the consumer side: scale each row of the product by the folded norm's 1/rms
+static void fold_consumer(const Run& r, Epi& e, int d) {
+  e.rowss = r.aw->rowss;
+  e.rowss_n = (d + 31) / 32;
+  e.rowss_d = d;
+}
+
 static Epi epi_kind(int kind, void* out = nullptr, int ldo = 0, const float* bias = nullptr) {
   Epi e;
   e.kind = kind;
@@ -812,7 +845,11 @@ static Epi epi_kind(int kind, void* out = nullptr, int ldo = 0, const float* bia
 // One Gemma-style decoder layer: RMSNorm (after adding the pending residual
 // partials) -> QKV (+RoPE, K/V stored) -> attention over [past; own] -> O ->
 // RMSNorm (after adding O) -> GeGLU -> down. The down projection is left
-// pending in the scratch (*pend = its split count) for the next norm.
+// pending in the scratch (*pend = its split count) for the next norm. In a
+// one-frame expert layer both norms are folded into the GEMMs around them
+// (gemm_part_fold, fold_consumer): the O projection leaves h = x * rms2 for
+// the gate/up GEMM, and the down projection x * next_g (the next norm's
+// gain) with *pend = -1, so the layer is five launches.
 // Several frames may run together, `rows` rows each:
 //  * LM layers (a batched prefill): x holds the frames' rows one after
 //    another, frame f's own K/V (its cache) sit kstride / vstride elements
@@ -831,7 +868,7 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
                          void* h, void* q, void* kout, void* vout, int pos0, const void* const* kpast,
                          const void* const* vpast, int npast, void* att, void* mlpbuf, bool kv_only,
                          int* pend, int frames = 1, size_t kstride = 0, size_t vstride = 0,
-                         const vla_model::WideLayer* wl = nullptr) {
+                         const vla_model::WideLayer* wl = nullptr, int next_g = -1) {
   vla_model* m = r.m;
   const vla_config& c = m->c;
   const Dims& d = m->d;
@@ -858,7 +895,10 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   const bool skin_fb = fb && !stacked;  // skinny frame blocks
   const int nblk = skin_fb ? rows : 0;   // norm output frame blocks (operand layout)
   const size_t nblk_out = skin_fb ? aw->blk_de : 0;
-  VLA_TRY(norm(r, x, frames * rows, dim, *pend, nullptr, L.rms1, -1, true, h, af, nblk, nblk_out));
+  const bool fold = !lm && af && !fb && aw && aw->rowss;
+  const bool folded_in = *pend < 0;  // h holds x * rms1 already
+  if (folded_in && !fold) return fail(VLA_ESTATE, "a folded norm is pending outside a one-frame expert layer");
+  if (!folded_in) VLA_TRY(norm(r, x, frames * rows, dim, *pend, nullptr, L.rms1, -1, true, h, af, nblk, nblk_out));
   *pend = 0;
   Epi e;
   e.kind = EPI_QKV_ROPE;
@@ -878,6 +918,7 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
     e.blk_k = lm ? kstride : aw->blk_k;
     e.blk_v = lm ? vstride : aw->blk_v;
   }
+  if (folded_in) fold_consumer(r, e, dim);
   const char* tq = lm ? "lm.qkv" : "ex.qkv";
   if (wide)
     VLA_TRY(gemm_rm(r, tq, h, dim, wl->qkv, dim, gm, d.qkv_n, dim, e, frm(0)));
@@ -929,13 +970,18 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   VLA_TRY(attn_kv(r, lm ? "lm.attn" : "ex.attn", a));
   int so = 0;
   const char* to = lm ? "lm.o" : "ex.o";
-  if (wide)
-    VLA_TRY(gemm_part_rm(r, to, att, d.qd, wl->o, d.qd, gm, dim, d.qd, &so, frm(0)));
-  else
-    VLA_TRY(gemm_part(r, to, att, d.qd, L.o, gm, dim, d.qd, &so, frm(skin_fb ? aw->blk_att : 0)));
-  VLA_TRY(norm(r, x, frames * rows, dim, so, nullptr, L.rms2, -1, true, h, af, nblk, nblk_out));
+  if (fold) {
+    VLA_TRY(gemm_part_fold(r, to, att, d.qd, L.o, gm, dim, d.qd, x, L.rms2, h));
+  } else {
+    if (wide)
+      VLA_TRY(gemm_part_rm(r, to, att, d.qd, wl->o, d.qd, gm, dim, d.qd, &so, frm(0)));
+    else
+      VLA_TRY(gemm_part(r, to, att, d.qd, L.o, gm, dim, d.qd, &so, frm(skin_fb ? aw->blk_att : 0)));
+    VLA_TRY(norm(r, x, frames * rows, dim, so, nullptr, L.rms2, -1, true, h, af, nblk, nblk_out));
+  }
   Epi eg = epi_kind(EPI_GEGLU, mlpbuf, mlp);
   eg.afrag = af;
+  if (fold) fold_consumer(r, eg, dim);
   if (skin_fb) {
     eg.blk_rows = rows;
     eg.blk_out = aw->blk_mlp;
@@ -946,10 +992,14 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   else
     VLA_TRY(gemm(r, tg, h, dim, L.gu, gm, 2 * mlp, dim, eg, 0, frm(skin_fb ? aw->blk_de : 0)));
   const char* td = lm ? "lm.down" : "ex.down";
-  if (wide)
+  if (fold && next_g >= 0) {
+    VLA_TRY(gemm_part_fold(r, td, mlpbuf, mlp, L.down, gm, dim, mlp, x, next_g, h));
+    *pend = -1;
+  } else if (wide) {
     VLA_TRY(gemm_part_rm(r, td, mlpbuf, mlp, wl->down, mlp, gm, dim, mlp, pend, frm(0)));
-  else
+  } else {
     VLA_TRY(gemm_part(r, td, mlpbuf, mlp, L.down, gm, dim, mlp, pend, frm(skin_fb ? aw->blk_mlp : 0)));
+  }
   return VLA_OK;
 }
 
@@ -1382,10 +1432,12 @@ static int run_denoise_n(const Run& r, const vla_ctx* const* ctxs, int frames, c
       }
       VLA_TRY(decoder_layer(r, false, m->ex[l], w.u, H, de, c.ex_mlp, w.h, w.q, w.kown, w.vown, d.prefix,
                             K, V, d.prefix, w.att, w.mlp, false, &pend, frames, 0, 0,
-                            fb ? &m->exw[l] : nullptr));
+                            fb ? &m->exw[l] : nullptr, l + 1 < c.ex_layers ? m->ex[l + 1].rms1 : m->fin_g));
     }
-    VLA_TRY(norm(r, w.u, frames * H, de, pend, nullptr, m->fin_g, -1, true, w.h, true, blk, w.blk_de));
+    // (pend < 0: the last down projection left h = x * fin_g and its row sums)
+    if (pend >= 0) VLA_TRY(norm(r, w.u, frames * H, de, pend, nullptr, m->fin_g, -1, true, w.h, true, blk, w.blk_de));
     Epi e;
+    if (pend < 0) fold_consumer(r, e, de);
     e.kind = EPI_EULER;
     e.afrag = 1;
     e.bias = m->f32(m->out_b);
@@ -1690,6 +1742,11 @@ static int add_act_lane(vla_model* m) {
       HIP_TRY(hipMemset(a.acnt, 0, (size_t)std::max(nc, 1) * 4));
       a.acnt_n = nc;
     }
+  }
+  if (c.head == VLA_HEAD_PI0 && (c.ex_dim + 31) / 32 <= FOLD_MAX_PAIRS && c.ex_dim % 8 == 0 && H <= 64) {
+    VLA_TRY(dmalloc(m, (void**)&a.rowss, (size_t)FOLD_MAX_PAIRS * 64 * 4));
+    VLA_TRY(dmalloc(m, (void**)&a.pcnt, (size_t)FOLD_MAX_PAIRS * 4));
+    HIP_TRY(hipMemset(a.pcnt, 0, (size_t)FOLD_MAX_PAIRS * 4));
   }
   VLA_TRY(dmalloc(m, (void**)&a.xg, (size_t)F * H * c.action_dim * 4));
   VLA_TRY(dmalloc(m, (void**)&a.nstage, (size_t)F * H * c.action_dim * 4));
