@@ -175,6 +175,10 @@ struct GemmDesc {
   // one-frame call; batched action loops pass a fixed reference (the largest
   // group), so the reduction does not depend on the group size.
   int plan_m = 0;
+  // The most plan_m-row blocks a launch of this plan stacks (a prefill
+  // batch). The split count may then be planned for that launch as well
+  // (fixed for every batch, so the reduction stays the same).
+  int plan_batch = 1;
 };
 
 // Offset of element (n, k) of a weight stored in MFMA fragment order with KS

@@ -1483,11 +1483,22 @@ GemmPlan plan_gemm(const GemmDesc& g) {
   const int kb64 = (g.K + 63) / 64;
   const bool cheap_epi = g.epi.kind == EPI_GEGLU || g.epi.kind == EPI_T || g.epi.kind == EPI_GELU ||
                          g.epi.kind == EPI_SWISH;
-  auto choose = [&](int M) {
+  // Split-K partials of `splits` K-ranges of kc 64-wide blocks each also go
+  // to the 256 tile when its workgroups make exactly one round on the chip
+  // (at least 7/8 of it) and each split is long enough (kc >= 32) to carry
+  // the partial epilogue; a second, partly empty round of 256 tiles loses to
+  // the 128 tile (measured), a single full one wins.
+  auto part256 = [&](int t256, int splits) {
+    const int kc = (kb64 + splits - 1) / splits;
+    return g.epi.kind == EPI_PART && splits > 0 && kc >= 32 && t256 * splits <= NUM_CU_PLAN &&
+           t256 * splits >= NUM_CU_PLAN * 7 / 8;
+  };
+  auto choose = [&](int M, int splits) {
     if (g.dtype == DT_BF16) {
       const int t128 = ((M + 127) / 128) * ((g.N + 127) / 128);
       const int t256 = ((M + 255) / 256) * ((g.N + 255) / 256);
       if (M >= 1024 && t256 >= NUM_CU_PLAN) return 3;
+      if (M >= 1024 && part256(t256, splits)) return 3;
       if (M >= 1024 && cheap_epi) {
         const long long c256 = (long long)((t256 + NUM_CU_PLAN - 1) / NUM_CU_PLAN) * (kb64 * 3600LL + 18000);
         const long long c128 = (long long)((t128 + 2 * NUM_CU_PLAN - 1) / (2 * NUM_CU_PLAN)) * (kb64 * 3900LL);
@@ -1502,10 +1513,11 @@ GemmPlan plan_gemm(const GemmDesc& g) {
   // from all M rows; every configuration of a dtype has the same BK, so the
   // K range of each split (and every sum) is the same as in a one-frame call.
   const int Mp = g.plan_m > 0 ? g.plan_m : g.M;  // may exceed M (a fixed reference row count)
-  const int c = choose(g.M);
-  const TileCfg t = cfgs[c], tp = cfgs[choose(Mp)];
+  // (the split count is planned first, from the tile of Mp rows chosen as
+  // if unsplit; every tile of a dtype has the same BK)
+  const TileCfg tp = cfgs[choose(Mp, 0)];
   const int tiles = ((Mp + tp.bm - 1) / tp.bm) * ((g.N + tp.bn - 1) / tp.bn);
-  const int kblocks = (g.K + t.bk - 1) / t.bk;
+  const int kblocks = (g.K + tp.bk - 1) / tp.bk;
   // Split K where it is free: partial sums (EPI_PART) are added by their
   // consumer, so aim for two workgroups per CU with at least four K-blocks
   // each. Other epilogues need a separate reduction pass, so only very
@@ -1516,8 +1528,18 @@ GemmPlan plan_gemm(const GemmDesc& g) {
   else if (tiles < 32 && kblocks >= 16)
     splits = std::min(NUM_CU_PLAN / tiles, kblocks / 4);
   splits = std::max(splits, 1);
+  // One split fewer where that lets the largest batched launch of the plan
+  // (plan_batch x Mp rows, a prefill batch) run on the 256 tile in one round
+  // (part256); the count stays the same for every batch size.
+  if (g.dtype == DT_BF16 && g.plan_batch > 1 && splits > 1) {
+    const int Mb = g.plan_batch * Mp;
+    const int t256b = ((Mb + 255) / 256) * ((g.N + 255) / 256);
+    if (Mb >= 1024 && !part256(t256b, splits) && part256(t256b, splits - 1)) splits -= 1;
+  }
   const int kchunk_blocks = (kblocks + splits - 1) / splits;
   splits = (kblocks + kchunk_blocks - 1) / kchunk_blocks;
+  const int c = choose(g.M, splits);
+  const TileCfg t = cfgs[c];
   p.cfg = c;
   p.splits = splits;
   p.tiles = ((g.M + t.bm - 1) / t.bm) * ((g.N + t.bn - 1) / t.bn) * splits;

@@ -676,6 +676,7 @@ struct Frames {
   int n = 1;
   size_t a_blk = 0;
   int plan_m = 0;  // rows of one frame when M stacks several frames (0: M)
+  int plan_batch = 1;  // the most frames a launch of this plan stacks
 };
 
 // C = A W[:, koff : koff + K]^T with the epilogue e; W is a weight tensor id.
@@ -692,6 +693,7 @@ static GemmDesc gemm_desc(vla_model* m, const void* A, int lda, int W, int M, in
   g.frames = fr.n;
   g.a_blk = fr.a_blk;
   g.plan_m = fr.plan_m;
+  g.plan_batch = fr.plan_batch;
   return g;
 }
 
@@ -715,6 +717,7 @@ static int gemm_rm(const Run& r, const char* tag, const void* A, int lda, const 
   vla_model* m = r.m;
   GemmDesc g{m->dt, A, lda, W, ldw, M, N, K, e};
   g.plan_m = fr.plan_m;
+  g.plan_batch = fr.plan_batch;
   LaunchCaps caps = r.caps;
   VLA_TRY(timer_events(r, tag, &caps));
   hipError_t err = launch_gemm(g, *r.scr, caps, r.st);
@@ -790,6 +793,7 @@ static int gemm_part_rm(const Run& r, const char* tag, const void* A, int lda, c
   e.ldo = (int)std::min<size_t>(r.scr->floats, (size_t)INT32_MAX);
   GemmDesc g{m->dt, A, lda, W, ldw, M, N, K, e};
   g.plan_m = fr.plan_m;
+  g.plan_batch = fr.plan_batch;
   *splits = plan_gemm(g).splits;
   return gemm_rm(r, tag, A, lda, W, ldw, M, N, K, e, fr);
 }
@@ -883,9 +887,11 @@ static int decoder_layer(const Run& r, bool lm, const DecLayer& L, float* x, int
   auto frm = [&](size_t a_blk) {
     Frames f;
     if (stacked) {
-      // splits: those of one frame's prefix rows (LM), or of the largest
-      // batched action loop (expert): fixed for every group size
+      // splits: those of one frame's prefix rows (LM; planned for prefill
+      // batches of up to MAX_VLM_BATCH frames), or of the largest batched
+      // action loop (expert): fixed for every group size
       f.plan_m = lm ? rows : MAX_ACT_BATCH * rows;
+      if (lm) f.plan_batch = MAX_VLM_BATCH;
     } else {
       f.n = frames;
       f.a_blk = fb ? a_blk : 0;
@@ -1018,9 +1024,10 @@ static int run_prefill_n(const Run& r, const vla_frame* f, int n, vla_ctx* const
   if (n > 1 && !ctx_consecutive(m, ctxs, n)) return fail(VLA_EINVAL, "batched prefill: contexts not consecutive");
   const int dv = c.vit_dim, dl = c.lm_dim, rows = d.rows_v, P = d.prefix;
   const int nv = n * c.n_views;  // views of all frames
-  auto fr1 = [&](int rows1) {  // splits of one frame's rows
+  auto fr1 = [&](int rows1) {  // splits of one frame's rows, for prefill batches
     Frames x;
     x.plan_m = rows1;
+    x.plan_batch = MAX_VLM_BATCH;
     return x;
   };
   // ViT: patch embedding + bias + position
