@@ -1485,12 +1485,15 @@ GemmPlan plan_gemm(const GemmDesc& g) {
                          g.epi.kind == EPI_SWISH;
   // Split-K partials of `splits` K-ranges of kc 64-wide blocks each also go
   // to the 256 tile when its workgroups make exactly one round on the chip
-  // (at least 7/8 of it) and each split is long enough (kc >= 32) to carry
+  // (at least 7/8 of it) and each split is long enough (kc >= 10) to carry
   // the partial epilogue; a second, partly empty round of 256 tiles loses to
-  // the 128 tile (measured), a single full one wins.
+  // the 128 tile, a single full one wins (measured alone, weights from HBM:
+  // 2440 x 2048 x 2048 in 3 splits of kc 11, 35 us against 51 us on the
+  // 128 tile; 2048 x 1152 x 4304 in 6 splits of kc 12, 40 us against 51 us
+  // on the 64 tile; with kc 3 the 256 tile loses).
   auto part256 = [&](int t256, int splits) {
     const int kc = (kb64 + splits - 1) / splits;
-    return g.epi.kind == EPI_PART && splits > 0 && kc >= 32 && t256 * splits <= NUM_CU_PLAN &&
+    return g.epi.kind == EPI_PART && splits > 0 && kc >= 10 && t256 * splits <= NUM_CU_PLAN &&
            t256 * splits >= NUM_CU_PLAN * 7 / 8;
   };
   auto choose = [&](int M, int splits) {
@@ -1528,13 +1531,19 @@ GemmPlan plan_gemm(const GemmDesc& g) {
   else if (tiles < 32 && kblocks >= 16)
     splits = std::min(NUM_CU_PLAN / tiles, kblocks / 4);
   splits = std::max(splits, 1);
-  // One split fewer where that lets the largest batched launch of the plan
+  // Fewer splits where that lets the largest batched launch of the plan
   // (plan_batch x Mp rows, a prefill batch) run on the 256 tile in one round
-  // (part256); the count stays the same for every batch size.
+  // (part256): the most splits below the planned count that do; the count
+  // stays the same for every batch size.
   if (g.dtype == DT_BF16 && g.plan_batch > 1 && splits > 1) {
     const int Mb = g.plan_batch * Mp;
     const int t256b = ((Mb + 255) / 256) * ((g.N + 255) / 256);
-    if (Mb >= 1024 && !part256(t256b, splits) && part256(t256b, splits - 1)) splits -= 1;
+    if (Mb >= 1024 && !part256(t256b, splits))
+      for (int s2 = splits - 1; s2 >= 1; --s2)
+        if (part256(t256b, s2)) {
+          splits = s2;
+          break;
+        }
   }
   const int kchunk_blocks = (kblocks + splits - 1) / splits;
   splits = (kblocks + kchunk_blocks - 1) / kchunk_blocks;

@@ -1473,15 +1473,21 @@ struct ScratchNeed {
   size_t floats = 0;
 };
 
-// (frames: that many frames' rows stacked, split-K planned for one frame)
+// (frames: up to that many frames' rows stacked, split-K planned for the
+// rows plan_m (default: one frame's), for launches of up to plan_batch
+// frames, as the launches plan them; the largest need over the frame counts)
 static ScratchNeed gemm_scratch(int dt, int M, int N, int K, bool part = false, bool frag = false,
-                                int frames = 1) {
-  GemmDesc g{dt, nullptr, K, nullptr, K, M * frames, N, K, Epi()};
-  g.plan_m = M;
-  if (part) g.epi.kind = EPI_PART;
-  if (frag) g.frag_ks = (K + frag_slab(dt) - 1) / frag_slab(dt);
-  const GemmPlan p = plan_gemm(g);
-  return ScratchNeed{p.scratch_floats};
+                                int frames = 1, int plan_batch = 1, int plan_m = 0) {
+  ScratchNeed n{0};
+  for (int f = 1; f <= frames; ++f) {
+    GemmDesc g{dt, nullptr, K, nullptr, K, M * f, N, K, Epi()};
+    g.plan_m = plan_m > 0 ? plan_m : M;
+    g.plan_batch = plan_batch;
+    if (part) g.epi.kind = EPI_PART;
+    if (frag) g.frag_ks = (K + frag_slab(dt) - 1) / frag_slab(dt);
+    n.floats = std::max(n.floats, plan_gemm(g).scratch_floats);
+  }
+  return n;
 }
 
 static ScratchNeed attn_scratch(int dt, int Sq, int nq, int nkv, int hd, int S0, int S1, int segs,
@@ -1718,10 +1724,11 @@ static int add_act_lane(vla_model* m) {
   upd(sa, gemm_scratch(dt, F * H, 2 * c.ex_mlp, de, false, true));
   upd(sa, gemm_scratch(dt, F * H, de, c.ex_mlp, true, true));
   // batched loops: tiled GEMMs over all frames' rows, splits of one frame
-  upd(sa, gemm_scratch(dt, H, d.qkv_n, de, false, false, F));
-  upd(sa, gemm_scratch(dt, H, de, d.qd, true, false, F));
-  upd(sa, gemm_scratch(dt, H, 2 * c.ex_mlp, de, false, false, F));
-  upd(sa, gemm_scratch(dt, H, de, c.ex_mlp, true, false, F));
+  // (groups of 1 .. F frames, each planned for the largest group's rows)
+  upd(sa, gemm_scratch(dt, H, d.qkv_n, de, false, false, F, 1, F * H));
+  upd(sa, gemm_scratch(dt, H, de, d.qd, true, false, F, 1, F * H));
+  upd(sa, gemm_scratch(dt, H, 2 * c.ex_mlp, de, false, false, F, 1, F * H));
+  upd(sa, gemm_scratch(dt, H, de, c.ex_mlp, true, false, F, 1, F * H));
   upd(sa, gemm_scratch(dt, F * H, c.action_dim, de, false, true));
   upd(sa, attn_scratch(dt, H, c.lm_heads, c.lm_kv_heads, c.head_dim, P, H, 1));
   VLA_TRY(alloc_scratch(m, sa, &a.scr));
@@ -1791,19 +1798,19 @@ static int make_vlm_lane(vla_model* m, int cap, int slot) {
   ScratchNeed sv;
   auto upd = [](ScratchNeed& s, ScratchNeed x) { s.floats = std::max(s.floats, x.floats); };
   const int r1 = d.rows_v, p1 = d.prefix;
-  upd(sv, gemm_scratch(dt, r1, dv, d.kp_pad, false, false, cap));
-  upd(sv, gemm_scratch(dt, r1, 3 * dv, dv, false, false, cap));
-  upd(sv, gemm_scratch(dt, r1, dv, dv, true, false, cap));
-  upd(sv, gemm_scratch(dt, r1, c.vit_mlp, dv, false, false, cap));
-  upd(sv, gemm_scratch(dt, r1, dv, c.vit_mlp, true, false, cap));
+  upd(sv, gemm_scratch(dt, r1, dv, d.kp_pad, false, false, cap, MAX_VLM_BATCH));
+  upd(sv, gemm_scratch(dt, r1, 3 * dv, dv, false, false, cap, MAX_VLM_BATCH));
+  upd(sv, gemm_scratch(dt, r1, dv, dv, true, false, cap, MAX_VLM_BATCH));
+  upd(sv, gemm_scratch(dt, r1, c.vit_mlp, dv, false, false, cap, MAX_VLM_BATCH));
+  upd(sv, gemm_scratch(dt, r1, dv, c.vit_mlp, true, false, cap, MAX_VLM_BATCH));
   upd(sv, gemm_scratch(dt, d.nimg, dl, d.kproj));
-  if (c.head == VLA_HEAD_DIT) upd(sv, gemm_scratch(dt, p1, 2 * c.ex_dim, dl, false, false, cap));
+  if (c.head == VLA_HEAD_DIT) upd(sv, gemm_scratch(dt, p1, 2 * c.ex_dim, dl, false, false, cap, MAX_VLM_BATCH));
   if (c.head == VLA_HEAD_COG) upd(sv, gemm_scratch(dt, 1, c.ex_dim, dl));
   upd(sv, gemm_scratch(dt, 1, dl, d.s_pad));
-  upd(sv, gemm_scratch(dt, p1, d.qkv_n, dl, false, false, cap));
-  upd(sv, gemm_scratch(dt, p1, dl, d.qd, true, false, cap));
-  upd(sv, gemm_scratch(dt, p1, 2 * c.lm_mlp, dl, false, false, cap));
-  upd(sv, gemm_scratch(dt, p1, dl, c.lm_mlp, true, false, cap));
+  upd(sv, gemm_scratch(dt, p1, d.qkv_n, dl, false, false, cap, MAX_VLM_BATCH));
+  upd(sv, gemm_scratch(dt, p1, dl, d.qd, true, false, cap, MAX_VLM_BATCH));
+  upd(sv, gemm_scratch(dt, p1, 2 * c.lm_mlp, dl, false, false, cap, MAX_VLM_BATCH));
+  upd(sv, gemm_scratch(dt, p1, dl, c.lm_mlp, true, false, cap, MAX_VLM_BATCH));
   upd(sv, attn_scratch(dt, d.tview, c.vit_heads, c.vit_heads, d.vhd, d.tview, 0, cap * c.n_views, c.n_views));
   upd(sv, attn_scratch(dt, p1, c.lm_heads, c.lm_kv_heads, c.head_dim, p1, 0, 1));
   if (sv.floats) {
