@@ -392,6 +392,20 @@ int vla_wavelog_read(vla_model* m, void* host_dst, int64_t max_records, int64_t*
 int vla_debug_generate(uint64_t seed, const char* name, int64_t n, double mean, double stdv,
                        float* host_dst);
 
+/* Host-only test entry point: the launch plan that the phases' GEMMs and
+ * vla_debug_gemm_epi get for an M x N x K product. kind is a VLA_DEBUG_EPI_* epilogue
+ * (RESID_NORM: split-K partials for a norm); skinny = 1 plans the action
+ * head's kernel (M <= 64 rows per frame), 0 the tiled one. plan_m (0: M) is
+ * the row count the split factor is planned for and plan_batch the most
+ * frames of plan_m rows one launch may stack (the phases plan a batched
+ * prefill for one frame's rows with plan_batch 8, and the batched action
+ * loops for 8 frames' rows with plan_batch 1). out (host int32[4])
+ * receives the tile's rows and columns (0 and 32 for the skinny kernel), the
+ * split-K factor and the workgroup count; scratch_floats (host, may be NULL)
+ * the fp32 partials the launch needs. Needs no GPU. */
+int vla_debug_gemm_plan(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t kind, int32_t skinny,
+                        int32_t plan_m, int32_t plan_batch, int32_t* out, int64_t* scratch_floats);
+
 /* Message for the last non-zero status on this thread ("" if none). */
 const char* vla_last_error(void);
 

@@ -122,6 +122,7 @@ def _load():
         "vla_debug_gemm_epi": [I32, I32, I32, I32, P, P, ctypes.POINTER(vla_debug_epi), P],
         "vla_debug_attention": [I32, I32, I32, I32, I32, P, P, P, I32, P, P, I32, P, P],
         "vla_debug_generate": [U64, ctypes.c_char_p, I64, D, D, P],
+        "vla_debug_gemm_plan": [I32, I32, I32, I32, I32, I32, I32, I32, P, ctypes.POINTER(I64)],
         "vla_debug_attention_cache": [I32, I32, I32, I32, I32, P, P, P, I32, P, P, I32, P, P],
         "vla_kernel_timer": [P, ctypes.c_char_p],
         "vla_kernel_timer_read": [P, ctypes.POINTER(D), ctypes.POINTER(I64)],
@@ -386,11 +387,24 @@ def vla_debug_generate(seed: int, name: str, n: int, mean: float, std: float) ->
     return out
 
 
+def vla_debug_gemm_plan(dtype: int, M: int, N: int, K: int, kind: int, skinny: bool = False, plan_m: int = 0,
+                        plan_batch: int = 1) -> dict:
+    """The launch plan of an M x N x K GEMM (host only): tile rows and
+    columns, split-K factor, workgroups and fp32 scratch floats."""
+    out = np.zeros(4, dtype=np.int32)
+    scratch = ctypes.c_int64(0)
+    _check(_lib.vla_debug_gemm_plan(dtype, M, N, K, kind, int(skinny), plan_m, plan_batch, out.ctypes.data,
+                                    ctypes.byref(scratch)))
+    return {"tile": (int(out[0]), int(out[1])), "splits": int(out[2]), "workgroups": int(out[3]),
+            "scratch_floats": int(scratch.value)}
+
+
 def exported_symbols() -> Iterable[str]:
     """Names of the C entry points this binding wraps."""
     return ["vla_preset", "vla_validate", "vla_model_config", "vla_create", "vla_destroy", "vla_ctx_create",
             "vla_ctx_destroy", "vla_vlm_prefill", "vla_action_denoise", "vla_pipeline_run",
             "vla_param_count", "vla_param_info", "vla_export_param", "vla_ctx_export_kv", "vla_ctx_export_cross", "vla_ctx_export_cog", "vla_wavelog_enable", "vla_wavelog_read",
             "vla_debug_gemm", "vla_debug_gemm_epi", "vla_gemm_noalloc", "vla_debug_attention", "vla_debug_attention_cache", "vla_debug_generate",
+            "vla_debug_gemm_plan",
             "vla_kernel_timer",
             "vla_kernel_timer_read", "vla_last_error"]

@@ -2947,6 +2947,37 @@ int vla_kernel_timer_read(vla_model* m, double* total_ms, int64_t* launches) {
   })
 }
 
+int vla_debug_gemm_plan(int32_t dtype, int32_t M, int32_t N, int32_t K, int32_t kind, int32_t skinny,
+                        int32_t plan_m, int32_t plan_batch, int32_t* out, int64_t* scratch_floats) {
+  ABI_GUARD({
+    if (dtype != VLA_F32 && dtype != VLA_BF16) return fail(VLA_EINVAL, "dtype");
+    if (!out) return fail(VLA_EINVAL, "out is NULL");
+    if (M <= 0 || N <= 0 || K <= 0 || K % 8 || plan_m < 0 || plan_batch < 1)
+      return fail(VLA_EINVAL, "shape: M, N, K > 0, K a multiple of 8, plan_m >= 0, plan_batch >= 1");
+    if (skinny && M > 64) return fail(VLA_EINVAL, "the skinny kernel takes M <= 64");
+    static const int kinds[] = {EPI_F32, EPI_T, EPI_GELU, EPI_SWISH, EPI_GEGLU, EPI_QKV_ROPE, EPI_QKV_PLAIN,
+                                EPI_EULER, EPI_PART};
+    if (kind < VLA_DEBUG_EPI_BIAS || kind > VLA_DEBUG_EPI_RESID_NORM) return fail(VLA_EINVAL, "unknown epilogue");
+    static_assert(VLA_DEBUG_EPI_RESID_NORM - VLA_DEBUG_EPI_BIAS + 1 == sizeof(kinds) / sizeof(kinds[0]),
+                  "one internal kind per epilogue");
+    const int dt = dtype == VLA_BF16 ? DT_BF16 : DT_F32;
+    GemmDesc g{dt, nullptr, K, nullptr, K, M, N, K, Epi()};
+    g.epi.kind = kinds[kind - VLA_DEBUG_EPI_BIAS];
+    g.plan_m = plan_m;
+    g.plan_batch = plan_batch;
+    if (skinny) {
+      g.frag_ks = (K + frag_slab(dt) - 1) / frag_slab(dt);
+      g.epi.afrag = 1;
+    }
+    const GemmPlan p = plan_gemm(g);
+    plan_tile(g, p, &out[0], &out[1]);
+    out[2] = p.splits;
+    out[3] = p.tiles;
+    if (scratch_floats) *scratch_floats = (int64_t)p.scratch_floats;
+    return VLA_OK;
+  })
+}
+
 int vla_debug_generate(uint64_t seed, const char* name, int64_t n, double mean, double stdv,
                        float* host_dst) {
   ABI_GUARD({
