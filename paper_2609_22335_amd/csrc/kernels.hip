@@ -475,12 +475,24 @@ struct GemmSmemDL {
   };
 };
 
+// Waves per SIMD each tile is built for, so that its registers leave room
+// for the workgroups its LDS allows on a CU (160 KB): the 4-wave 128 x 128
+// bf16 tile (80 KB) two per CU, the smaller 4-wave bf16 tiles (40 and 30 KB)
+// four (the fp32 tiles, which only the small test models run, three); the
+// 8-wave 256 x 256 tile runs alone. Without it the compiler may take a few
+// registers more than that leaves (the 128 x 128 GeGLU tile took 260 of
+// 256) and a CU then holds one workgroup fewer.
+constexpr int gemm_waves_per_eu(int bm, int waves, bool dl, int esize) {
+  return dl || waves != 4 ? 2 : esize == 4 ? 3 : bm >= 128 ? 2 : 4;
+}
+
 // KIND >= 0: the epilogue kind fixed at compile time (the tiles of the
 // batched action loops, short launches whose code should stay in the
 // instruction cache); KIND = -1: chosen at run time from e.kind.
 template <typename T, int BM, int BN, int BK, int WGM = 2, int WGN = 2, int PD = 1, int PAD = VLA_GEMM_LDS_PAD,
           bool DL = false, int KIND = -1>
-__global__ __launch_bounds__(64 * WGM * WGN) void k_gemm(const T* __restrict__ A, int lda,
+__global__ __launch_bounds__(64 * WGM * WGN)
+__attribute__((amdgpu_waves_per_eu(gemm_waves_per_eu(BM, WGM * WGN, DL, (int)sizeof(T))))) void k_gemm(const T* __restrict__ A, int lda,
                                               const T* __restrict__ W, int ldw, int M, int N,
                                               int K, int kchunk, int splits, int tiles_m,
                                               int tiles_n, int group_m, Epi e, float* __restrict__ part) {
