@@ -2672,6 +2672,117 @@ __global__ __launch_bounds__(256) void k_norm(NormDesc n) {
   VLA_WAVE_END(KK_NORM);
 }
 
+// Rows of at most 1024 columns (the action expert's): one wave per row, four
+// rows per workgroup. Lane l owns the four-column groups starting at columns
+// 4 l, 4 l + 256, 4 l + 512 and 4 l + 768; every load of the row is issued
+// before the first use, the split partials are added in split order as in
+// k_norm, and the row statistics are reduced inside the wave (no LDS round
+// trip, no barrier), which shortens the launch for the many small norms of
+// the action loop. (The column sums are grouped differently from k_norm's,
+// so a row's statistics may differ from it in the last bits.)
+constexpr int NORMW_VPL = 4;  // four-column groups per lane: d <= 1024
+template <typename T>
+__global__ __launch_bounds__(256) void k_norm_w(NormDesc n) {
+  VLA_WAVE_BEGIN(KK_NORM);
+  constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
+  constexpr int SPL = 4;  // split partials requested together
+  const int rows = n.rows, d = n.d, ldx = n.ldx, splits = n.splits;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  float* __restrict__ x = n.x;
+  const size_t pstride = (size_t)rows * d;
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f}, one4 = {1.f, 1.f, 1.f, 1.f};
+  const Rsrc rx = rsrc(x, span(rows, ldx, d, 4));
+  const Rsrc rp = rsrc(n.part ? n.part : x, n.part ? (size_t)splits * pstride * 4 : 0);
+  const Rsrc rb = rsrc(n.bias ? n.bias : x, n.bias ? (size_t)d * 4 : 0);
+  const Rsrc rc = rsrc(n.colscale ? n.colscale : x, n.colscale ? (size_t)d * 4 : 0);
+  const Rsrc rg = rsrc(n.g, (size_t)d * 4);
+  const Rsrc rs = rsrc(n.b ? n.b : x, n.b ? (size_t)d * 4 : 0);
+  for (int row = blockIdx.x * 4 + wave; row < rows; row += gridDim.x * 4) {
+    f32x4 v[NORMW_VPL], add[NORMW_VPL], cs[NORMW_VPL], gn[NORMW_VPL], sh[NORMW_VPL];
+#pragma unroll
+    for (int q = 0; q < NORMW_VPL; ++q) {
+      const int c = (lane + q * 64) * 4;
+      const bool ok = c < d;
+      v[q] = bld4f(rx, ok ? (uint32_t)(((size_t)row * ldx + c) * 4) : OOB);
+      add[q] = bld4f(rb, ok ? (uint32_t)(c * 4) : OOB);
+      cs[q] = bld4f(rc, ok ? (uint32_t)(c * 4) : OOB);
+      gn[q] = bld4f(rg, ok ? (uint32_t)(c * 4) : OOB);
+      sh[q] = bld4f(rs, ok ? (uint32_t)(c * 4) : OOB);
+    }
+    if (splits > 0) {
+      f32x4 sum[NORMW_VPL];
+#pragma unroll
+      for (int q = 0; q < NORMW_VPL; ++q) sum[q] = zero4;
+      for (int sp = 0; sp < splits; sp += SPL) {
+        f32x4 t[SPL][NORMW_VPL];
+#pragma unroll
+        for (int u = 0; u < SPL; ++u)
+#pragma unroll
+          for (int q = 0; q < NORMW_VPL; ++q) {
+            const int c = (lane + q * 64) * 4;
+            const bool ok = c < d && sp + u < splits;
+            t[u][q] = bld4f(rp, ok ? (uint32_t)(((size_t)row * d + (sp + u) * pstride + c) * 4) : OOB);
+          }
+#pragma unroll
+        for (int u = 0; u < SPL; ++u)
+#pragma unroll
+          for (int q = 0; q < NORMW_VPL; ++q)
+            if (sp + u < splits) sum[q] += t[u][q];
+      }
+#pragma unroll
+      for (int q = 0; q < NORMW_VPL; ++q) add[q] += n.colscale ? cs[q] * sum[q] : sum[q];
+    }
+    float s1 = 0.f;
+#pragma unroll
+    for (int q = 0; q < NORMW_VPL; ++q) {
+      const int c = (lane + q * 64) * 4;
+      if (c < d) {
+        if (splits > 0) {
+          v[q] += add[q];
+          *(f32x4*)(x + (size_t)row * ldx + c) = v[q];
+        }
+        s1 += (v[q][0] + v[q][1]) + (v[q][2] + v[q][3]);
+      }
+    }
+    float mean = 0.f;
+    if (!n.rms) {
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) s1 += __shfl_xor(s1, off);
+      mean = s1 / d;
+    }
+    float s2 = 0.f;
+#pragma unroll
+    for (int q = 0; q < NORMW_VPL; ++q) {
+      const int c = (lane + q * 64) * 4;
+      if (c < d) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float cd = v[q][e] - mean;
+          s2 += cd * cd;
+        }
+      }
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) s2 += __shfl_xor(s2, off);
+    const float inv = 1.f / sqrtf(s2 / d + 1e-6f);
+#pragma unroll
+    for (int q = 0; q < NORMW_VPL; ++q) {
+      const int c = (lane + q * 64) * 4;
+      if (c < d) {
+        const f32x4 gi = n.g_plus_one ? one4 + gn[q] : gn[q];
+        f32x4 y = (v[q] - mean) * inv * gi;
+        if (n.b) y += sh[q];
+        T* dst = (T*)n.out + (n.afrag ? afrag_index_blk(DT, row, c, n.blk_rows, n.blk_out) : (size_t)row * n.ldo + c);
+        if constexpr (sizeof(T) == 2)
+          *(uint2*)dst = make_uint2(f2bf2(y[0], y[1]), f2bf2(y[2], y[3]));
+        else
+          *(f32x4*)dst = y;
+      }
+    }
+  }
+  VLA_WAVE_END(KK_NORM);
+}
+
 hipError_t launch_norm(const NormDesc& n, hipStream_t st) {
   // four-column accesses: 16-byte fp32 loads and stores, 8-byte bf16 stores
   auto mis = [](const void* p, uintptr_t a) { return ((uintptr_t)p & (a - 1)) != 0; };
@@ -2682,6 +2793,14 @@ hipError_t launch_norm(const NormDesc& n, hipStream_t st) {
       (n.afrag && (n.blk_rows > 0 ? n.blk_rows > 64 : n.rows > 64)) || !n.x || !n.g || !n.out ||
       (n.shuffle > 1 && (n.grid_w % n.shuffle || n.tview % (n.shuffle * n.grid_w) || n.afrag)))
     return hipErrorInvalidValue;
+  if (n.d <= 256 * NORMW_VPL && n.shuffle <= 1) {  // a wave per row
+    const int grid = std::min((n.rows + 3) / 4, 4096);
+    if (n.dtype == DT_BF16)
+      k_norm_w<uint16_t><<<grid, 256, 0, st>>>(n);
+    else
+      k_norm_w<float><<<grid, 256, 0, st>>>(n);
+    return hipGetLastError();
+  }
   const int grid = std::min(n.rows, 4096);
   if (n.dtype == DT_BF16)
     k_norm<uint16_t><<<grid, 256, 0, st>>>(n);
