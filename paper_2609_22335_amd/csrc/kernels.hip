@@ -937,7 +937,70 @@ __attribute__((amdgpu_waves_per_eu(gemm_waves_per_eu(BM, WGM * WGN, DL, (int)siz
         };
         constexpr int DT = sizeof(T) == 2 ? DT_BF16 : DT_F32;
         T* out = (T*)e.out;
-        if (ROWK && (ek == EPI_QKV_ROPE || ek == EPI_QKV_PLAIN)) {
+        // QKV-RoPE with four rotated columns per thread: the four output
+        // columns ri .. ri + 3 (and their partners + hd / 2) are contiguous in
+        // both Q and the K cache layout, so each goes out as one 8-byte (fp32:
+        // 16-byte) store; the V columns keep element stores (the cache layout
+        // runs along the keys there). Same arithmetic as the pair path below.
+        constexpr int VB = 4 * (int)sizeof(T);  // bytes of four elements
+        const bool ropev = ROWK && ek == EPI_QKV_ROPE && ((uintptr_t)e.q % VB) == 0 && e.ldq % 4 == 0 &&
+                           ((uintptr_t)e.k % VB) == 0 && e.blk_k % 4 == 0 && (e.hd / 2) % 4 == 0 &&
+                           ((uintptr_t)e.rope_cos % 16) == 0 && ((uintptr_t)e.rope_sin % 16) == 0;
+        if (ropev) {
+          constexpr int QPR = BN / 8;        // column quads per row: four in each 32-column group
+          constexpr int RPP = NT / QPR;      // rows per pass
+          static_assert(NT % QPR == 0 && (WGM * 16) % RPP == 0, "quads per pass");
+          const int hd = e.hd, qcols = e.nq * hd, kcols = e.nkv * hd;
+          auto st4 = [&](T* dst, const float (&v)[4]) {
+            if constexpr (sizeof(T) == 2)
+              *(uint2*)dst = make_uint2(f2bf2(v[0], v[1]), f2bf2(v[2], v[3]));
+            else
+              *(float4*)dst = make_float4(v[0], v[1], v[2], v[3]);
+          };
+          for (int r0 = 0; r0 < WGM * 16; r0 += RPP) {
+            const int row = r0 + tid / QPR, qd = tid % QPR;
+            const int m = m0 + (row >> 4) * WM + i * 16 + (row & 15);
+            const int c0 = (qd >> 2) * 32 + (qd & 3) * 4;  // first-half column of the tile
+            const int n = n0 + c0;
+            if (m >= M || n >= N) continue;
+            const float4 va = *(const float4*)(sm.c + row * CLD + c0);
+            const float4 vb = *(const float4*)(sm.c + row * CLD + c0 + 16);
+            const float v0[4] = {va.x, va.y, va.z, va.w}, v1[4] = {vb.x, vb.y, vb.z, vb.w};
+            const int key = epi_key(e, m);
+            if (n < qcols + kcols) {
+              const bool isq = n < qcols;
+              const int rn = isq ? n : n - qcols;
+              const int head = rn / hd, pp = rn - head * hd;
+              const int ri = 16 * (pp >> 5) + (pp & 15);
+              const size_t t = (size_t)(e.pos0 + key) * (hd / 2) + ri;
+              const float4 cs = *(const float4*)(e.rope_cos + t), sn = *(const float4*)(e.rope_sin + t);
+              const float c[4] = {cs.x, cs.y, cs.z, cs.w}, sv[4] = {sn.x, sn.y, sn.z, sn.w};
+              float a[4], b[4];
+#pragma unroll
+              for (int k = 0; k < 4; ++k) {
+                a[k] = v0[k] * c[k] - v1[k] * sv[k];
+                b[k] = v1[k] * c[k] + v0[k] * sv[k];
+              }
+              if (isq) {
+                T* dst = (T*)e.q + (size_t)m * e.ldq + head * hd;
+                st4(dst + ri, a);
+                st4(dst + ri + hd / 2, b);
+              } else {
+                T* dst = (T*)e.k + epi_kblk(e, m, e.blk_k);
+                st4(dst + kv_kidx(DT, e.kv_nb, hd, head, key, ri), a);
+                st4(dst + kv_kidx(DT, e.kv_nb, hd, head, key, ri + hd / 2), b);
+              }
+            } else {
+              const int c = n - qcols - kcols;
+              T* dst = (T*)e.v + epi_kblk(e, m, e.blk_v);
+#pragma unroll
+              for (int k = 0; k < 4; ++k) {
+                TT<T>::st(dst + kv_vidx(DT, e.kv_nb, hd, (c + k) / hd, key, (c + k) % hd), v0[k]);
+                TT<T>::st(dst + kv_vidx(DT, e.kv_nb, hd, (c + 16 + k) / hd, key, (c + 16 + k) % hd), v1[k]);
+              }
+            }
+          }
+        } else if (ROWK && (ek == EPI_QKV_ROPE || ek == EPI_QKV_PLAIN)) {
           const int hd = e.hd, qcols = e.nq * hd, kcols = e.nkv * hd;
           if (ek == EPI_QKV_ROPE && na < qcols + kcols) {
             // column pair (na, nb) holds a rotate-half pair (ri, ri + hd / 2)
