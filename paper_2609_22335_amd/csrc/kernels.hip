@@ -1112,6 +1112,14 @@ __attribute__((amdgpu_waves_per_eu(gemm_waves_per_eu(BM, WGM * WGN, DL, (int)siz
           const int m = m0 + (row >> 4) * WM + i * 16 + (row & 15);
           epi_pair<T, KIND>(e, M, N, m, n0 + col, sm.c[row * CLD + col], sm.c[row * CLD + col + 16]);
         }
+      } else if (N % 4 == 0 && ((uintptr_t)P & 15) == 0) {
+        // raw fp32 partial of split s: [splits][M][N], four columns per
+        // 16-byte store
+        for (int p = tid; p < WGM * 16 * (BN / 4); p += NT) {
+          const int row = p / (BN / 4), col = (p % (BN / 4)) * 4;
+          const int m = m0 + (row >> 4) * WM + i * 16 + (row & 15), n = n0 + col;
+          if (m < M && n < N) *(float4*)(P + (size_t)m * N + n) = *(const float4*)(sm.c + row * CLD + col);
+        }
       } else {
         // raw fp32 partial of split s: [splits][M][N]
         for (int p = tid; p < WGM * 16 * BN; p += NT) {
