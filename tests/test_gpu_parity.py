@@ -117,6 +117,11 @@ ATTN_CACHE_CASES = [  # dtype, Sq, nq, nkv, hd, S0, S1
     (0, 80, 4, 1, 64, 80, 0),
     (0, 3, 2, 2, 32, 1, 0),        # single key
     (0, 17, 3, 1, 96, 40, 33),
+    # 200 query tiles of 16 packed rows
+    (1, 400, 8, 1, 256, 305, 50),  # eight frames' action queries in one launch
+    (1, 397, 8, 1, 256, 305, 50),  # odd tile count, last tile ragged
+    (1, 200, 16, 1, 64, 96, 7),
+    (1, 200, 16, 4, 128, 96, 0),   # four KV heads
 ]
 
 
@@ -167,6 +172,30 @@ def test_attention_cache_vs_oracle(V, case):
     bound = (2.0 ** -8 * np.abs(ref) + 1e-4) if dtype else (2e-5 + 1e-5 * np.abs(ref))
     err = np.abs(got - ref)
     assert np.all(err <= bound), float((err / bound).max())
+
+
+def test_attention_cache_row_tiles_bit_identical(V):
+    """Rows are independent: 400 queries in one launch (200 query tiles)
+    equal the same rows in two launches of 200 queries bit for bit, whatever
+    workgroup a tile lands on."""
+    g = G()
+    Sq, nq, nkv, hd, S0, S1 = 400, 8, 1, 256, 305, 50
+    g.say("attention (KV-cache layout) one launch against two")
+    q = RNG.standard_normal((Sq, nq, hd))
+    k0, v0 = RNG.standard_normal((S0, nkv, hd)), RNG.standard_normal((S0, nkv, hd))
+    k1, v1 = RNG.standard_normal((S1, nkv, hd)), RNG.standard_normal((S1, nkv, hd))
+    lay = lambda x, kind: g.operand_dev(cache_layout(x, 1, kind), 1)
+    kd0, vd0, kd1, vd1 = lay(k0, "k"), lay(v0, "v"), lay(k1, "k"), lay(v1, "v")
+    qd = g.operand_dev(q.reshape(Sq, -1), 1)
+    whole = torch.empty((Sq, nq * hd), dtype=torch.bfloat16, device="cuda")
+    V.vla_debug_attention_cache(1, Sq, nq, nkv, hd, qd, kd0, vd0, S0, kd1, vd1, S1, whole)
+    halves = torch.empty_like(whole)
+    h = Sq // 2
+    for r0 in (0, h):
+        V.vla_debug_attention_cache(1, h, nq, nkv, hd, qd[r0:r0 + h].contiguous(), kd0, vd0, S0, kd1, vd1, S1,
+                                    halves[r0:r0 + h])
+    torch.cuda.synchronize()
+    assert torch.equal(whole, halves)
 
 
 @pytest.mark.parametrize("cfg", [synth.micro(synth.F32), synth.micro(synth.BF16), synth.TINY,
