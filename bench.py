@@ -176,7 +176,7 @@ def kernel_source_digest():
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--R", type=int, default=8, help="robot request streams (frames per step)")
     ap.add_argument("--mode", default="xs_vb8_ab8_lanes2_graph",
