@@ -361,6 +361,44 @@ def test_pi0_full_size_vs_oracle(V):
 
 
 @pytest.mark.timeout(900)
+def test_pi0_reported_schedule_full_size_vs_oracle(V):
+    """The benchmark's reported launch configuration at full size: R = 8
+    frames per step, two steps as one cross-step pipeline (step 1's prefill
+    beside step 0's action loop), prefills of 8, action loops of 8, two
+    action lanes, graph replay. Both steps' chunks equal those of one step
+    run alone bit for bit; frames 0 and 7 (the first and last rows of the
+    stacked batch) are within the chunk tolerance of the oracle."""
+    g = G()
+    cfg = synth.PI0
+    R, K = 8, 2
+    frames = [synth.make_frame(cfg, 0, r) for r in range(R)]
+    kw = dict(vlm_batch=8, act_batch=8, act_streams=2, graphs=True)
+    with g.model(cfg, 0) as m:
+        dfs = [g.DevFrame(f) for f in frames]
+        noise = torch.stack([d.noise for d in dfs]).contiguous()
+        g.say("pi0 full size: reported schedule, one step")
+        one = torch.full_like(noise, float("nan"))
+        V.vla_pipeline_run(m, [d.c for d in dfs], noise, R, mode="concurrent", actions=one, **kw)
+        g.say("pi0 full size: reported schedule, two steps as one pipeline")
+        noise_k = noise.repeat(K, 1, 1).contiguous()
+        out = torch.full_like(noise_k, float("nan"))
+        V.vla_pipeline_run(m, [d.c for d in dfs] * K, noise_k, R * K, mode="concurrent", actions=out, **kw)
+        torch.cuda.synchronize()
+        one = one.cpu().numpy()
+        out = out.cpu().numpy().reshape(K, R, *noise.shape[1:])
+    assert np.isfinite(one).all()
+    for j in range(K):
+        assert np.array_equal(out[j], one), j
+    g.say("pi0 full size: reported schedule, oracle of frames 0 and 7")
+    P = synth.make_params(cfg, 0)
+    for r in (0, R - 1):
+        want = O.forward(P, cfg, frames[r])
+        err = float(np.abs(one[r].astype(np.float64) - want).max())
+        print(f"[gpu] pi0 reported schedule frame {r} chunk max abs err {err:.3e}", flush=True)
+        assert err <= CHUNK_TOL[synth.BF16], r
+
+
+@pytest.mark.timeout(900)
 def test_pi0_ddim_full_size_vs_oracle(V):
     """The pi0-shaped model sampled with 10 DDIM steps at its real sizes:
     frames 0 and 1 of seed 0 from the standalone calls and from one batched
