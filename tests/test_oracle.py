@@ -289,47 +289,54 @@ def test_lm_decoder_layer_vs_gemma():
     assert np.allclose(v, cache.layers[0].values[0].transpose(0, 1).numpy(), rtol=2e-5, atol=2e-5)
 
 
-def test_expert_velocity_vs_library_assembly():
-    """The whole expert (in-proj, time MLP, decoder layers with the prefix KV in
-    the cache at positions P.., final RMSNorm, out-proj) assembled from torch and
-    transformers modules."""
+def _expert_torch(cfg, P, kv, x, t):
+    """The expert's velocity assembled from torch and transformers modules:
+    in-proj, time MLP, Gemma decoder layers with the prefix K/V of `kv`
+    ([(K, V)] per layer, [n, n_kv, hd]) in a DynamicCache at positions n..,
+    final RMSNorm, out-proj."""
     from transformers.cache_utils import DynamicCache
-    cfg = dict(synth.micro(), lm_layers=2, ex_layers=2)
-    P = synth.make_params(cfg, 0)
-    npre, H, A, de = 21, cfg["chunk_len"], cfg["action_dim"], cfg["ex_dim"]
-    nkv, hd = cfg["lm_kv_heads"], cfg["head_dim"]
-    kv = [(rnd(npre, nkv, hd), rnd(npre, nkv, hd)) for _ in range(2)]
-    x, t = rnd(H, A), 0.75
-    got = O.expert_velocity(P, cfg, kv, x, t)
-
+    H, de, hd, L = cfg["chunk_len"], cfg["ex_dim"], cfg["head_dim"], cfg["ex_layers"]
+    npre = kv[0][0].shape[0]
     lin = lambda w, b=None: (lambda z: F.linear(z, t64(P[w]), None if b is None else t64(P[b])))
     with torch.no_grad():
         a = lin("ex.in.w", "ex.in.b")(t64(x))
         phi = t64(O.sinusoid(t, de))[None].expand(H, de)
         u = lin("ex.time2.w", "ex.time2.b")(F.silu(lin("ex.time1.w", "ex.time1.b")(torch.cat([a, phi], 1))))
         cache = DynamicCache()
-        for l in range(2):
+        for l in range(L):
             cache.update(t64(kv[l][0]).transpose(0, 1)[None], t64(kv[l][1]).transpose(0, 1)[None], l)
         pos = np.arange(npre, npre + H)
         h = u[None]
-        for l in range(2):
+        for l in range(L):
             m = _gemma_layer(cfg, P, "ex", l, de, cfg["ex_mlp"])
             h = m(h, attention_mask=None, position_ids=torch.from_numpy(pos)[None], past_key_values=cache,
                   use_cache=True, position_embeddings=_rope_tables(hd, pos))
             h = h[0] if isinstance(h, tuple) else h
-        ref = lin("ex.out.w", "ex.out.b")(F.rms_norm(h[0], (de,), t64(P["ex.final.g"]), eps=1e-6)).numpy()
-    assert np.allclose(got, ref, rtol=2e-5, atol=2e-5)
+        return lin("ex.out.w", "ex.out.b")(F.rms_norm(h[0], (de,), t64(P["ex.final.g"]), eps=1e-6)).numpy()
 
 
-def test_vlm_prefill_vs_library_assembly():
-    """Phase 1 end to end (ViT from SigLIP layers, post-LN, projector, text
-    embedding x sqrt(d), state row, Gemma layers writing the cache)."""
-    from transformers.cache_utils import DynamicCache
-    cfg = dict(synth.micro(), vit_layers=2, lm_layers=2)
+def test_expert_velocity_vs_library_assembly():
+    """The whole expert (in-proj, time MLP, decoder layers with the prefix KV in
+    the cache at positions P.., final RMSNorm, out-proj) assembled from torch and
+    transformers modules."""
+    cfg = dict(synth.micro(), lm_layers=2, ex_layers=2)
     P = synth.make_params(cfg, 0)
-    fr = synth.make_frame(cfg, 0, 0)
-    got = O.vlm_prefill(P, cfg, fr)
-    p, dl = cfg["patch"], cfg["lm_dim"]
+    npre, H, A = 21, cfg["chunk_len"], cfg["action_dim"]
+    nkv, hd = cfg["lm_kv_heads"], cfg["head_dim"]
+    kv = [(rnd(npre, nkv, hd), rnd(npre, nkv, hd)) for _ in range(2)]
+    x, t = rnd(H, A), 0.75
+    got = O.expert_velocity(P, cfg, kv, x, t)
+    assert np.allclose(got, _expert_torch(cfg, P, kv, x, t), rtol=2e-5, atol=2e-5)
+
+
+def _prefill_torch(cfg, P, fr):
+    """Phase 1 of one view from library modules (patches by unfold, SigLIP
+    layers, post-LN, projector, text embedding x sqrt(d), state row, Gemma
+    layers writing a DynamicCache; the last layer only projects K and V);
+    returns [(K, V)] per LM layer as [n, n_kv, hd] arrays."""
+    from transformers.cache_utils import DynamicCache
+    from transformers.models.gemma.modeling_gemma import apply_rotary_pos_emb
+    p, dl, L = cfg["patch"], cfg["lm_dim"], cfg["lm_layers"]
     with torch.no_grad():
         img = t64(fr["pixels"][0])
         gh, gw = cfg["img_h"] // p, cfg["img_w"] // p
@@ -337,7 +344,7 @@ def test_vlm_prefill_vs_library_assembly():
         patches = img.permute(2, 0, 1).unfold(1, p, p).unfold(2, p, p)  # [3, gh, gw, p, p]
         patches = patches.permute(1, 2, 3, 4, 0).reshape(gh * gw, p * p * 3)
         x = F.linear(patches, t64(P["vit.patch.w"]), t64(P["vit.patch.b"])) + t64(P["vit.pos"])
-        for l in range(2):
+        for l in range(cfg["vit_layers"]):
             y = _siglip_layer(cfg, P, l)(x[None], None)
             x = (y[0] if isinstance(y, tuple) else y)[0]
         x = F.layer_norm(x, (cfg["vit_dim"],), t64(P["vit.post.g"]), t64(P["vit.post.b"]), eps=1e-6)
@@ -348,25 +355,62 @@ def test_vlm_prefill_vs_library_assembly():
         st = F.linear(t64(fr["state"])[None], t64(P["state.w"]), t64(P["state.b"]))
         h = torch.cat([img_tok, txt, st], 0)[None]
         n = h.shape[1]
+        cos, sin = _rope_tables(cfg["head_dim"], np.arange(n))
         cache = DynamicCache()
-        for l in range(2):
-            m = _gemma_layer(cfg, P, "lm", l, dl, cfg["lm_mlp"]) if l == 0 else None
-            if m is None:  # the last layer has no MLP / o-proj weights: only its K, V matter
+        for l in range(L):
+            if l == L - 1:  # the last layer has no MLP / o-proj weights: only its K, V matter
                 q = F.rms_norm(h[0], (dl,), t64(P[f"lm.{l}.rms1.g"]), eps=1e-6)
                 k = F.linear(q, t64(P[f"lm.{l}.k.w"])).reshape(n, cfg["lm_kv_heads"], -1)
                 v = F.linear(q, t64(P[f"lm.{l}.v.w"])).reshape(n, cfg["lm_kv_heads"], -1)
-                cos, sin = _rope_tables(cfg["head_dim"], np.arange(n))
-                from transformers.models.gemma.modeling_gemma import apply_rotary_pos_emb
                 kt = k.transpose(0, 1)[None]
                 kt, _ = apply_rotary_pos_emb(kt, kt, cos, sin)
                 cache.update(kt, v.transpose(0, 1)[None], l)
                 break
+            m = _gemma_layer(cfg, P, "lm", l, dl, cfg["lm_mlp"])
             h = m(h, attention_mask=None, position_ids=torch.arange(n)[None], past_key_values=cache,
-                  use_cache=True, position_embeddings=_rope_tables(cfg["head_dim"], np.arange(n)))
+                  use_cache=True, position_embeddings=(cos, sin))
             h = h[0] if isinstance(h, tuple) else h
+    return [(cache.layers[l].keys[0].transpose(0, 1).numpy(), cache.layers[l].values[0].transpose(0, 1).numpy())
+            for l in range(L)]
+
+
+def test_vlm_prefill_vs_library_assembly():
+    """Phase 1 end to end (ViT from SigLIP layers, post-LN, projector, text
+    embedding x sqrt(d), state row, Gemma layers writing the cache)."""
+    cfg = dict(synth.micro(), vit_layers=2, lm_layers=2)
+    P = synth.make_params(cfg, 0)
+    fr = synth.make_frame(cfg, 0, 0)
+    got = O.vlm_prefill(P, cfg, fr)
+    ref = _prefill_torch(cfg, P, fr)
     for l in range(2):
-        assert np.allclose(got[l][0], cache.layers[l].keys[0].transpose(0, 1).numpy(), rtol=5e-5, atol=5e-5)
-        assert np.allclose(got[l][1], cache.layers[l].values[0].transpose(0, 1).numpy(), rtol=5e-5, atol=5e-5)
+        assert np.allclose(got[l][0], ref[l][0], rtol=5e-5, atol=5e-5)
+        assert np.allclose(got[l][1], ref[l][1], rtol=5e-5, atol=5e-5)
+
+
+def test_full_forward_vs_library_assembly():
+    """Both phases end to end: the library prefill writes the cache, then the
+    library expert is integrated from the noise at t = 1 to t = 0 in N Euler
+    steps (flow-matching section of the paper's background: the action head
+    integrates a learned velocity field), with t_k = (N - k) / N and
+    dt = -1 / N each a single fp32 division (a reading of the schedule). The
+    oracle's chunk must match, so a mistake in how the forward joins the two
+    phases (the cache layers, the time schedule, the update's sign or step
+    count) fails here."""
+    cfg = dict(synth.micro(), vit_layers=2, lm_layers=3, ex_layers=3)
+    P = synth.make_params(cfg, 0)
+    fr = synth.make_frame(cfg, 0, 0)
+    got = O.forward(P, cfg, fr)
+    kv = _prefill_torch(cfg, P, fr)
+    N = cfg["n_steps"]
+    dt = float(np.float32(-1.0) / np.float32(N))
+    x = fr["noise"].astype(np.float64)
+    for k in range(N):
+        t = float(np.float32(N - k) / np.float32(N))
+        x = x + dt * _expert_torch(cfg, P, kv, x, t)
+    assert N >= 2 and not np.allclose(x, fr["noise"], atol=1e-3)  # the loop moved the state
+    # the two sides agree to ~3e-9; a step-count, time-shift, dt-sign or
+    # cache-layer mistake moves the chunk by 1.8e-2 or more
+    assert np.allclose(got, x, rtol=1e-6, atol=1e-6)
 
 
 # ------------------------------------------------------------ model wiring
