@@ -739,6 +739,103 @@ def test_image_tokens_with_pixel_shuffle_vs_torch_assembly():
     assert np.allclose(got, ref, rtol=1e-7, atol=1e-7)
 
 
+def _image_tokens_torch(cfg, P, fr):
+    """Image tokens of one view from library modules: patches by unfold,
+    SigLIP layers, the final LayerNorm, space-to-depth by pixel_unshuffle
+    (channels reordered to (dy, dx, c)) when the config shuffles, projector."""
+    p, dv, s = cfg["patch"], cfg["vit_dim"], cfg.get("shuffle", 1)
+    gh, gw = cfg["img_h"] // p, cfg["img_w"] // p
+    with torch.no_grad():
+        img = t64(fr["pixels"][0])
+        patches = img.permute(2, 0, 1).unfold(1, p, p).unfold(2, p, p)
+        patches = patches.permute(1, 2, 3, 4, 0).reshape(gh * gw, p * p * 3)
+        x = F.linear(patches, t64(P["vit.patch.w"]), t64(P["vit.patch.b"])) + t64(P["vit.pos"])
+        for l in range(cfg["vit_layers"]):
+            y = _siglip_layer(cfg, P, l)(x[None], None)
+            x = (y[0] if isinstance(y, tuple) else y)[0]
+        x = F.layer_norm(x, (dv,), t64(P["vit.post.g"]), t64(P["vit.post.b"]), eps=1e-6)
+        if s > 1:
+            g = F.pixel_unshuffle(x.T.reshape(1, dv, gh, gw), s)[0]
+            x = g.reshape(dv, s * s, gh // s, gw // s).permute(2, 3, 1, 0).reshape(-1, s * s * dv)
+        return F.linear(x, t64(P["proj.w"]), t64(P["proj.b"]))
+
+
+def _features_torch(cfg, P, fr):
+    """Phase 1 of the feature heads from library modules: [image tokens; text
+    embedding x sqrt(d); the state row if any; the learned cognition token for
+    that head] through every LM layer as a transformers Gemma decoder layer,
+    then torch's RMSNorm with the final gain."""
+    from transformers.cache_utils import DynamicCache
+    dl = cfg["lm_dim"]
+    with torch.no_grad():
+        rows = [_image_tokens_torch(cfg, P, fr)]
+        emb = torch.nn.Embedding(cfg["vocab"], dl).double()
+        emb.weight.data = t64(P["lm.embed"])
+        rows.append(emb(torch.from_numpy(fr["ids"].astype(np.int64))) * math.sqrt(dl))
+        if cfg["state_dim"] > 0:
+            rows.append(F.linear(t64(fr["state"])[None], t64(P["state.w"]), t64(P["state.b"])))
+        if cfg.get("head", 0) == 2:
+            rows.append(t64(P["lm.cog"]))
+        h = torch.cat(rows, 0)[None]
+        n = h.shape[1]
+        cache = DynamicCache()
+        for l in range(cfg["lm_layers"]):
+            m = _gemma_layer(cfg, P, "lm", l, dl, cfg["lm_mlp"])
+            h = m(h, attention_mask=None, position_ids=torch.arange(n)[None], past_key_values=cache,
+                  use_cache=True, position_embeddings=_rope_tables(cfg["head_dim"], np.arange(n)))
+            h = h[0] if isinstance(h, tuple) else h
+        return F.rms_norm(h[0], (dl,), t64(P["lm.final.g"]), eps=1e-6).numpy()
+
+
+def _euler_reading(x0, velocity, N):
+    """N Euler steps from t = 1: t_k = (N - k) / N and dt = -1 / N, each a
+    single fp32 division (the flow-matching time reading)."""
+    dt = float(np.float32(-1.0) / np.float32(N))
+    x = np.asarray(x0, np.float64)
+    for k in range(N):
+        x = x + dt * velocity(x, float(np.float32(N - k) / np.float32(N)))
+    return x
+
+
+def test_dit_full_forward_vs_library_assembly():
+    """The GR00T-shaped model end to end: library image tokens (2x2 shuffle),
+    the Gemma feature stack, the cross K / V of the even DiT layers by
+    F.linear, and the torch DiT integrated over N Euler steps; the oracle's
+    chunk must match."""
+    cfg = dict(synth.micro_dit(), vit_layers=2, lm_layers=2, ex_layers=4, n_steps=3)  # cross, self, cross, self
+    P = synth.make_params(cfg, 0)
+    fr = synth.make_frame(cfg, 0, 0)
+    got = O.forward(P, cfg, fr)
+    cross = _dit_cross_torch(P, cfg, _features_torch(cfg, P, fr))
+    with torch.no_grad():
+        want = _euler_reading(fr["noise"], lambda x, t: _dit_torch(P, cfg, cross, x, t), cfg["n_steps"])
+    assert not np.allclose(want, fr["noise"], atol=1e-3)
+    assert np.allclose(got, want, rtol=DIT_COG_FWD_TOL, atol=DIT_COG_FWD_TOL)
+
+
+def test_cog_full_forward_vs_library_assembly():
+    """The cognition-token head end to end (Euler sampler): the Gemma feature
+    stack over the prefix ending in the learned token, the projection of its
+    last row, and the torch head integrated over N Euler steps."""
+    cfg = dict(synth.micro_cog(), vit_layers=2, lm_layers=2, sampler=0, n_steps=3)
+    P = synth.make_params(cfg, 0)
+    fr = synth.make_frame(cfg, 0, 0)
+    got = O.forward(P, cfg, fr)
+    feats = _features_torch(cfg, P, fr)
+    with torch.no_grad():
+        cog = F.linear(t64(feats[-1:]), t64(P["cog.w"]), t64(P["cog.b"]))[0].numpy()
+        want = _euler_reading(fr["noise"], lambda x, t: _cog_torch(P, cfg, cog, x, t), cfg["n_steps"])
+    assert not np.allclose(want, fr["noise"], atol=1e-3)
+    assert np.allclose(got, want, rtol=DIT_COG_FWD_TOL, atol=DIT_COG_FWD_TOL)
+
+
+# the oracle and the assemblies agree to 2e-12 (DiT) and 2e-10 (cognition
+# head); shifted times, features without the final norm, another layer's
+# cross K / V, the cognition hand-off from the first row or without its bias
+# move the chunk by 3.7e-6 or more
+DIT_COG_FWD_TOL = 1e-8
+
+
 # ------------------------------------------------ cognition-token (CogACT) head
 
 def _cog_torch(P, cfg, cog, x, t):
