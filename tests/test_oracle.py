@@ -720,21 +720,10 @@ def test_image_tokens_with_pixel_shuffle_vs_torch_assembly():
     P = synth.make_params(cfg, 0)
     fr = synth.make_frame(cfg, 0, 0)
     got = O.image_tokens(P, cfg, fr["pixels"])
-    p, dv, s = cfg["patch"], cfg["vit_dim"], cfg["shuffle"]
+    p, s = cfg["patch"], cfg["shuffle"]
     gh, gw = cfg["img_h"] // p, cfg["img_w"] // p
-    with torch.no_grad():
-        img = t64(fr["pixels"][0])
-        patches = img.permute(2, 0, 1).unfold(1, p, p).unfold(2, p, p)
-        patches = patches.permute(1, 2, 3, 4, 0).reshape(gh * gw, p * p * 3)
-        x = F.linear(patches, t64(P["vit.patch.w"]), t64(P["vit.patch.b"])) + t64(P["vit.pos"])
-        for l in range(cfg["vit_layers"]):
-            y = _siglip_layer(cfg, P, l)(x[None], None)
-            x = (y[0] if isinstance(y, tuple) else y)[0]
-        x = F.layer_norm(x, (dv,), t64(P["vit.post.g"]), t64(P["vit.post.b"]), eps=1e-6)
-        g = F.pixel_unshuffle(x.T.reshape(1, dv, gh, gw), s)[0]  # [dv s s, gh/s, gw/s], channels (c, dy, dx)
-        g = g.reshape(dv, s * s, gh // s, gw // s).permute(2, 3, 1, 0).reshape(-1, s * s * dv)
-        ref = F.linear(g, t64(P["proj.w"]), t64(P["proj.b"])).numpy()
-    assert got.shape == ((gh // s) * (gw // s), cfg["lm_dim"])
+    ref = _image_tokens_torch(cfg, P, fr).numpy()
+    assert s == 2 and got.shape == ((gh // s) * (gw // s), cfg["lm_dim"])
     # transformers computes the ViT softmax in fp32, hence 1e-7
     assert np.allclose(got, ref, rtol=1e-7, atol=1e-7)
 
