@@ -786,6 +786,41 @@ def _euler_reading(x0, velocity, N):
     return x
 
 
+def _ddim_reading(x0, eps, N, T=1000):
+    """Deterministic DDIM from its reading: the DDPM linear beta schedule
+    (1e-4 .. 0.02 over T steps), timesteps s_k = floor((N - k) T / N) - 1 with
+    the head's time input s_k / T as one fp32 division, and the update written
+    as x <- a_k x + b_k eps with a_k = sqrt(abar_{k+1} / abar_k) and
+    b_k = sqrt(1 - abar_{k+1}) - a_k sqrt(1 - abar_k), abar = 1 after the last
+    step."""
+    abar = np.cumprod(1.0 - np.linspace(1e-4, 0.02, T))
+    s = [(N - k) * T // N - 1 for k in range(N)]
+    ab = [abar[sk] for sk in s] + [1.0]
+    x = np.asarray(x0, np.float64)
+    for k in range(N):
+        a = math.sqrt(ab[k + 1] / ab[k])
+        b = math.sqrt(1.0 - ab[k + 1]) - a * math.sqrt(1.0 - ab[k])
+        x = a * x + b * eps(x, float(np.float32(s[k]) / np.float32(T)))
+    return x
+
+
+def test_ddim_full_forward_vs_library_assembly():
+    """The pi0-shaped model sampled with DDIM end to end: the library prefill
+    and the library expert read as the noise estimate, the steps written in
+    the a_k x + b_k eps form (the oracle takes the clean-estimate form; the two
+    are equal algebraically). The chunk is ~1/sqrt(abar_0) times the noise, so
+    the bound is relative to its magnitude."""
+    cfg = dict(synth.micro(), vit_layers=2, lm_layers=2, ex_layers=2, sampler=1, n_steps=3)
+    P = synth.make_params(cfg, 0)
+    fr = synth.make_frame(cfg, 0, 0)
+    got = O.forward(P, cfg, fr)
+    kv = _prefill_torch(cfg, P, fr)
+    want = _ddim_reading(fr["noise"], lambda x, t: _expert_torch(cfg, P, kv, x, t), cfg["n_steps"])
+    scale = float(np.abs(want).max())
+    assert scale > 10 * float(np.abs(fr["noise"]).max())  # the sampler scaled the state up
+    assert float(np.abs(got - want).max()) <= DDIM_FWD_REL_TOL * scale
+
+
 def test_dit_full_forward_vs_library_assembly():
     """The GR00T-shaped model end to end: library image tokens (2x2 shuffle),
     the Gemma feature stack, the cross K / V of the even DiT layers by
@@ -823,6 +858,7 @@ def test_cog_full_forward_vs_library_assembly():
 # cross K / V, the cognition hand-off from the first row or without its bias
 # move the chunk by 3.7e-6 or more
 DIT_COG_FWD_TOL = 1e-8
+DDIM_FWD_REL_TOL = 1e-6
 
 
 # ------------------------------------------------ cognition-token (CogACT) head
