@@ -191,7 +191,7 @@ def main():
                                        "serial_vb8_ab8_graph,cu_160_96,cu_auto,xs_lanes2_graph,"
                                        "xs_vb4_ab4_lanes2_graph,xs_vb8_ab4_graph,xs_vb8_ab4_lanes2_graph,"
                                        "xs_vb8_ab8_lanes2_graph")
-    ap.add_argument("--detail", default=os.path.join(ROOT, "gpurun_out", "bench_detail.json"),
+    ap.add_argument("--detail", default=os.path.join(ROOT, "bench_detail.json"),
                     help="JSON file for every schedule's numbers, residency logs and further workloads")
     ap.add_argument("--split", default="192,64", help="CU split VLM,action for cu_masked")
     ap.add_argument("--wg-cap", type=int, default=2, help="VLM workgroups per CU for wg_capped")
