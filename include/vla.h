@@ -21,9 +21,14 @@
  *  - Objects made by *_create are owned by the library until *_destroy.
  *    All other buffers are owned by the caller and must stay alive until the
  *    asynchronous work that reads or writes them has completed.
- *  - One model may run one prefill and one denoise at a time (they use
- *    model-owned scratch memory per phase); calls of the same phase on two
- *    streams at once race.
+ *  - One model runs one prefill and one denoise at a time (they use
+ *    model-owned scratch memory per phase). A prefill (or denoise) called on
+ *    another stream than the previous one first waits, on the device, for
+ *    that call's work, so calls of one phase never overlap; a prefill and a
+ *    denoise do overlap. Calls made while their stream is being captured into
+ *    a graph are not ordered this way: captured calls of one phase on two
+ *    streams race. vla_pipeline_run first waits on the host for the last
+ *    standalone call of each phase.
  */
 #ifndef VLA_H
 #define VLA_H
@@ -354,6 +359,31 @@ int vla_gemm_noalloc(int32_t dtype, int32_t M, int32_t N, int32_t K, const void*
 int vla_debug_attention_cache(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int32_t hd,
                               const void* q, const void* k0, const void* v0, int32_t S0, const void* k1,
                               const void* v1, int32_t S1, void* out, void* stream);
+
+/* Test entry point for the row norm of every layer (the pre-norms of the
+ * ViT, LM and expert layers: LayerNorm with biased variance, or RMSNorm;
+ * epsilon 1e-6). For each of `rows` rows of d fp32 values x (device,
+ * row-major, leading dimension ldx elements):
+ *  - with splits > 0, x <- x + bias + colscale * (part[0] + ... +
+ *    part[splits-1]) first, the partials summed in split order and the
+ *    result written back to x (the residual update of a split-K GEMM);
+ *    part is [splits][rows][d] fp32, contiguous; bias and colscale [d] may
+ *    be NULL. With splits = 0, x is only read and bias and colscale are not
+ *    used;
+ *  - y = (x - mean) / sqrt(var + 1e-6) * g + shift (rms = 0, LayerNorm), or
+ *    y = x / sqrt(mean(x^2) + 1e-6) * g (rms = 1; shift may still be given),
+ *    with g = gain, or 1 + gain when gain_plus_one != 0; gain [d] required,
+ *    shift [d] may be NULL;
+ *  - out [rows][ldo] in the operand type of dtype (bf16 as uint16 bits).
+ * d is a multiple of 4 in 4 .. 2048; ldx and ldo are multiples of 4 and at
+ * least d; x, part, bias, colscale, gain and shift are 16-byte aligned, out
+ * 16-byte (fp32) or 8-byte (bf16) aligned, else VLA_EINVAL. rows = 0 does
+ * nothing and reads no pointer (they may be NULL). All pointers device;
+ * asynchronous on `stream`. */
+int vla_debug_norm(int32_t dtype, int32_t rows, int32_t d, float* x, int32_t ldx, const float* part,
+                   int32_t splits, const float* bias, const float* colscale, const float* gain,
+                   int32_t gain_plus_one, const float* shift, int32_t rms, void* out, int32_t ldo,
+                   void* stream);
 
 /* Kernel timer for measurement: while `tag` is set, every launch of the
  * kernels behind that call site (tags: "vit.patch", "vit.qkv", "vit.attn",

@@ -124,6 +124,7 @@ def _load():
         "vla_debug_generate": [U64, ctypes.c_char_p, I64, D, D, P],
         "vla_debug_gemm_plan": [I32, I32, I32, I32, I32, I32, I32, I32, P, ctypes.POINTER(I64)],
         "vla_debug_attention_cache": [I32, I32, I32, I32, I32, P, P, P, I32, P, P, I32, P, P],
+        "vla_debug_norm": [I32, I32, I32, P, I32, P, I32, P, P, P, I32, P, I32, P, I32, P],
         "vla_kernel_timer": [P, ctypes.c_char_p],
         "vla_kernel_timer_read": [P, ctypes.POINTER(D), ctypes.POINTER(I64)],
     }
@@ -370,6 +371,12 @@ def vla_debug_attention_cache(dtype: int, Sq: int, nq: int, nkv: int, hd: int, q
                                           _ptr(k1), _ptr(v1), S1, _ptr(out), stream or None))
 
 
+def vla_debug_norm(dtype: int, rows: int, d: int, x, ldx: int, part, splits: int, bias, colscale, gain,
+                   gain_plus_one: int, shift, rms: int, out, ldo: int, stream: int = 0) -> None:
+    _check(_lib.vla_debug_norm(dtype, rows, d, _ptr(x), ldx, _ptr(part), splits, _ptr(bias), _ptr(colscale),
+                               _ptr(gain), gain_plus_one, _ptr(shift), rms, _ptr(out), ldo, stream or None))
+
+
 def vla_kernel_timer(model: int, tag: Optional[str]) -> None:
     _check(_lib.vla_kernel_timer(model, tag.encode() if tag else None))
 
@@ -404,7 +411,7 @@ def exported_symbols() -> Iterable[str]:
     return ["vla_preset", "vla_validate", "vla_model_config", "vla_create", "vla_destroy", "vla_ctx_create",
             "vla_ctx_destroy", "vla_vlm_prefill", "vla_action_denoise", "vla_pipeline_run",
             "vla_param_count", "vla_param_info", "vla_export_param", "vla_ctx_export_kv", "vla_ctx_export_cross", "vla_ctx_export_cog", "vla_wavelog_enable", "vla_wavelog_read",
-            "vla_debug_gemm", "vla_debug_gemm_epi", "vla_gemm_noalloc", "vla_debug_attention", "vla_debug_attention_cache", "vla_debug_generate",
+            "vla_debug_gemm", "vla_debug_gemm_epi", "vla_gemm_noalloc", "vla_debug_attention", "vla_debug_attention_cache", "vla_debug_norm", "vla_debug_generate",
             "vla_debug_gemm_plan",
             "vla_kernel_timer",
             "vla_kernel_timer_read", "vla_last_error"]

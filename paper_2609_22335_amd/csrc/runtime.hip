@@ -364,6 +364,14 @@ struct vla_model {
   WaveLog* wlog = nullptr;                  // residency log (measurement), device memory
   size_t wlog_cap = 0;
   std::vector<std::unique_ptr<ActWs>> aws;  // action lanes; lane 0 serves standalone calls
+  // Standalone calls share lane 0 of their phase (0: prefill, 1: denoise):
+  // the stream and completion event of the last one, so that a call on
+  // another stream first waits for it.
+  struct Solo {
+    hipEvent_t done = nullptr;
+    hipStream_t stream = nullptr;
+    bool pending = false;
+  } solo[2];
   std::vector<void*> allocs;
 
   // pipeline
@@ -2316,6 +2324,8 @@ int vla_destroy(vla_model* m) {
     for (auto e : m->ev) hipEventDestroy(e);
     for (auto e : m->eva) hipEventDestroy(e);
     for (auto e : m->timer_ev) hipEventDestroy(e);
+    for (auto& so : m->solo)
+      if (so.done) hipEventDestroy(so.done);
     if (m->wlog) {
       wavelog_set(nullptr);
       hipFree(m->wlog);
@@ -2344,14 +2354,61 @@ int vla_ctx_destroy(vla_ctx* c) {
   })
 }
 
+// Orders standalone calls of one phase: a call on another stream than the
+// previous one waits (on the device) for that call's work, so the two never
+// share the lane-0 scratch at once. Under stream capture the call is neither
+// ordered nor recorded (an event recorded outside the capture cannot be
+// waited on inside it); captured calls on several streams still race.
+static hipError_t solo_begin(vla_model* m, int phase, hipStream_t st, bool* capturing) {
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(st, &cs);
+  if (e != hipSuccess) return e;
+  *capturing = cs != hipStreamCaptureStatusNone;
+  auto& s = m->solo[phase];
+  if (*capturing) {
+    s.pending = false;
+    return hipSuccess;
+  }
+  if (!s.done && (e = hipEventCreateWithFlags(&s.done, hipEventDisableTiming)) != hipSuccess) return e;
+  if (s.pending && s.stream != st && (e = hipStreamWaitEvent(st, s.done, 0)) != hipSuccess) return e;
+  return hipSuccess;
+}
+
+static hipError_t solo_end(vla_model* m, int phase, hipStream_t st, bool capturing) {
+  auto& s = m->solo[phase];
+  if (capturing) return hipSuccess;
+  const hipError_t e = hipEventRecord(s.done, st);
+  s.stream = st;
+  s.pending = e == hipSuccess;
+  return e;
+}
+
+// host wait for the last standalone call of each phase (the pipeline reuses
+// the lane-0 scratch)
+static hipError_t solo_drain(vla_model* m) {
+  for (auto& s : m->solo)
+    if (s.pending) {
+      const hipError_t e = hipEventSynchronize(s.done);
+      if (e != hipSuccess) return e;
+      s.pending = false;
+    }
+  return hipSuccess;
+}
+
 int vla_vlm_prefill(vla_model* m, const vla_frame* in, vla_ctx* ctx, void* stream) {
   ABI_GUARD({
     if (!m || !in || !ctx || !in->pixels || (!in->text_ids && m->c.n_text > 0))
       return fail(VLA_EINVAL, "NULL argument");
     if (m->c.state_dim > 0 && !in->state) return fail(VLA_EINVAL, "state is NULL but state_dim > 0");
     if (ctx->m != m) return fail(VLA_ESTATE, "context belongs to another model");
+    bool cap = false;
+    hipError_t e = solo_begin(m, 0, (hipStream_t)stream, &cap);
+    if (e != hipSuccess) return fail(VLA_EHIP, std::string("ordering standalone prefills: ") + hipGetErrorString(e));
     Run r{m, (hipStream_t)stream, LaunchCaps{}, &m->vws[0]->scr, nullptr, m->vws[0].get()};
-    return run_prefill(r, in, ctx);
+    const int rc = run_prefill(r, in, ctx);
+    e = solo_end(m, 0, (hipStream_t)stream, cap);
+    if (rc == VLA_OK && e != hipSuccess) return fail(VLA_EHIP, std::string("ordering standalone prefills: ") + hipGetErrorString(e));
+    return rc;
   })
 }
 
@@ -2359,8 +2416,14 @@ int vla_action_denoise(vla_model* m, const vla_ctx* ctx, const float* noise, flo
   ABI_GUARD({
     if (!m || !ctx || !noise || !actions) return fail(VLA_EINVAL, "NULL argument");
     if (ctx->m != m) return fail(VLA_ESTATE, "context belongs to another model");
+    bool cap = false;
+    hipError_t e = solo_begin(m, 1, (hipStream_t)stream, &cap);
+    if (e != hipSuccess) return fail(VLA_EHIP, std::string("ordering standalone denoises: ") + hipGetErrorString(e));
     Run r{m, (hipStream_t)stream, LaunchCaps{}, &m->aws[0]->scr, m->aws[0].get()};
-    return run_denoise(r, ctx, noise, actions);
+    const int rc = run_denoise(r, ctx, noise, actions);
+    e = solo_end(m, 1, (hipStream_t)stream, cap);
+    if (rc == VLA_OK && e != hipSuccess) return fail(VLA_EHIP, std::string("ordering standalone denoises: ") + hipGetErrorString(e));
+    return rc;
   })
 }
 
@@ -2368,6 +2431,8 @@ int vla_pipeline_run(vla_model* m, const vla_frame* frames, const float* noise, 
                      const vla_sched* sched, float* actions, vla_timing* t) {
   ABI_GUARD({
     if (!m) return fail(VLA_EINVAL, "model is NULL");
+    const hipError_t e = solo_drain(m);
+    if (e != hipSuccess) return fail(VLA_EHIP, std::string("waiting for standalone calls: ") + hipGetErrorString(e));
     return pipeline_impl(m, frames, noise, R, sched, actions, t);
   })
 }
@@ -2860,6 +2925,39 @@ int vla_debug_attention(int32_t dtype, int32_t Sq, int32_t nq, int32_t nkv, int3
       hipFree(s.ptr);
     }
     if (e != hipSuccess) return fail(VLA_EHIP, std::string("attention: ") + hipGetErrorString(e));
+    return VLA_OK;
+  })
+}
+
+int vla_debug_norm(int32_t dtype, int32_t rows, int32_t d, float* x, int32_t ldx, const float* part,
+                   int32_t splits, const float* bias, const float* colscale, const float* gain,
+                   int32_t gain_plus_one, const float* shift, int32_t rms, void* out, int32_t ldo,
+                   void* stream) {
+  ABI_GUARD({
+    if (dtype != VLA_F32 && dtype != VLA_BF16) return fail(VLA_EINVAL, "dtype");
+    if (rows < 0 || d < 4 || d > 2048 || d % 4 || ldx < d || ldx % 4 || ldo < d || ldo % 4 || splits < 0)
+      return fail(VLA_EINVAL, "shape");
+    if (rows == 0) return VLA_OK;  // nothing is read or written
+    if (!x || !gain || !out || (splits > 0 && !part)) return fail(VLA_EINVAL, "NULL argument");
+    NormDesc n{};
+    n.dtype = dtype == VLA_BF16 ? DT_BF16 : DT_F32;
+    n.x = x;
+    n.ldx = ldx;
+    n.rows = rows;
+    n.d = d;
+    n.part = splits > 0 ? part : nullptr;
+    n.splits = splits;
+    n.bias = bias;
+    n.colscale = colscale;
+    n.g = gain;
+    n.g_plus_one = gain_plus_one ? 1 : 0;
+    n.b = shift;
+    n.rms = rms ? 1 : 0;
+    n.out = out;
+    n.ldo = ldo;
+    const hipError_t e = launch_norm(n, (hipStream_t)stream);
+    if (e == hipErrorInvalidValue) return fail(VLA_EINVAL, "a pointer is not aligned (16 bytes; bf16 out 8)");
+    if (e != hipSuccess) return fail(VLA_EHIP, std::string("norm launch: ") + hipGetErrorString(e));
     return VLA_OK;
   })
 }

@@ -725,6 +725,113 @@ def test_pipeline_cross_step(V, cfg):
                 g.run_frame(m, cfg, frames[rep])  # eager work between replays
 
 
+def test_standalone_calls_on_two_streams(V):
+    """Standalone prefills (and denoises) share their phase's scratch: a call
+    on another stream than the previous one waits for it, so two frames
+    prefilled and denoised on two streams give the chunks of the same calls
+    on one stream, bit for bit, every time (with eager work in between)."""
+    g = G()
+    cfg = synth.TINY
+    frames = [synth.make_frame(cfg, 3, r) for r in range(2)]
+    with g.model(cfg, 3) as m:
+        g.say("standalone calls: one stream")
+        ref = [g.run_frame(m, cfg, f)[0] for f in frames]
+        dfs = [g.DevFrame(f) for f in frames]
+        streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+        with g.context(m) as c0, g.context(m) as c1:
+            ctxs = [c0, c1]
+            for rep in range(3):
+                g.say(f"standalone calls: two streams, repetition {rep}")
+                outs = [torch.full_like(d.noise, float("nan")) for d in dfs]
+                for i in range(2):
+                    V.vla_vlm_prefill(m, dfs[i].c, ctxs[i], streams[i].cuda_stream)
+                for i in range(2):
+                    V.vla_action_denoise(m, ctxs[i], dfs[i].noise, outs[i], streams[i].cuda_stream)
+                torch.cuda.synchronize()
+                for i in range(2):
+                    assert np.array_equal(outs[i].cpu().numpy().astype(np.float64), ref[i]), (rep, i)
+                g.run_frame(m, cfg, frames[rep % 2])  # eager work on the null stream between repetitions
+
+
+NORM_CASES = [  # dtype, rows, d, splits, rms, gain_plus_one, bias, colscale, shift, pad, x scale
+    (1, 37, 1024, 4, 1, 0, False, False, False, 0, 2.0),  # expert RMSNorm after split-K partials, ragged rows
+    (1, 305, 2048, 3, 1, 0, False, False, False, 0, 2.0),  # LM RMSNorm after the down projection's splits
+    (1, 256, 1152, 6, 0, 0, True, False, True, 0, 2.0),    # ViT LayerNorm after fc2's splits and bias
+    (1, 50, 1024, 2, 1, 0, True, True, False, 0, 2.0),     # column-scaled partials (the folded form)
+    (0, 50, 1024, 0, 1, 1, False, False, False, 8, 2.0),   # fp32 out, 1 + gain, padded rows, no partials
+    (0, 9, 1536, 5, 0, 0, True, True, True, 4, 2.0),       # fp32, one workgroup per row, everything on
+    (0, 16, 256, 0, 0, 0, False, False, False, 0, 1e-3),   # variance near epsilon: epsilon 1e-6 pinned
+    (0, 16, 2048, 0, 1, 0, False, False, False, 0, 1e-3),  # the same for RMSNorm, one workgroup per row
+    (1, 3, 4, 1, 0, 0, True, False, True, 0, 2.0),         # narrowest rows
+    (0, 0, 64, 0, 0, 0, False, False, True, 0, 2.0),       # no rows
+]
+
+
+@pytest.mark.parametrize("case", NORM_CASES, ids=lambda c: "-".join(map(str, c)))
+def test_norm_vs_oracle(V, case):
+    """vla_debug_norm against the oracle's LayerNorm / RMSNorm in fp64 on the
+    same fp32 inputs. Bound: the fp32 sums and statistics, 64 ulp of fp32 on
+    |ref| + |g|, plus one rounding to bf16 (2^-8 |ref|, round to nearest is
+    2^-9) for bf16 output; the residual written back within (splits + 2) ulp
+    of its terms' magnitudes. Padding columns stay untouched."""
+    g = G()
+    dtype, rows, d, splits, rms, gp1, has_b, has_cs, has_sh, pad, xs = case
+    g.say(f"norm {case}")
+    rng = np.random.default_rng(11 + rows + d)
+    ldx = ldo = d + pad
+    x = (rng.standard_normal((rows, ldx)) + 0.15) * xs
+    part = rng.standard_normal((max(splits, 1), rows, d)) * 0.25 * xs
+    bias = rng.standard_normal(d) * 0.05 * xs if has_b else None
+    cs = 1.0 + rng.standard_normal(d) * 0.2 if has_cs else None
+    gain = rng.standard_normal(d) * 0.1 + (0.0 if gp1 else 1.0)
+    shift = rng.standard_normal(d) * 0.1 if has_sh else None
+    f32 = lambda a: None if a is None else a.astype(np.float32)
+    dev = lambda a: None if a is None else torch.from_numpy(np.ascontiguousarray(f32(a))).cuda()
+    xd, pd = dev(x), dev(part) if splits > 0 else None
+    od = torch.full((rows, ldo), 7.0, dtype=torch.bfloat16 if dtype else torch.float32, device="cuda")
+    V.vla_debug_norm(dtype, rows, d, xd, ldx, pd, splits, dev(bias), dev(cs), dev(gain), gp1, dev(shift), rms,
+                     od, ldo)
+    torch.cuda.synchronize()
+    if rows == 0:
+        return
+    xv = f32(x).astype(np.float64)
+    xn = xv[:, :d].copy()
+    if splits > 0:
+        ps = f32(part).astype(np.float64).sum(0)
+        b64 = 0.0 if bias is None else f32(bias).astype(np.float64)
+        c64 = 1.0 if cs is None else f32(cs).astype(np.float64)
+        xn = xn + b64 + c64 * ps
+        xb = (splits + 2) * 2.0 ** -23 * (np.abs(xv[:, :d]) + np.abs(b64) + np.abs(c64) * np.abs(f32(part)).sum(0))
+        xg = xd.cpu().numpy().astype(np.float64)
+        assert np.all(np.abs(xg[:, :d] - xn) <= xb), float((np.abs(xg[:, :d] - xn) / xb).max())
+        assert np.array_equal(xg[:, d:], xv[:, d:])  # padding untouched
+    gv = f32(gain).astype(np.float64) + (1.0 if gp1 else 0.0)
+    sv = 0.0 if shift is None else f32(shift).astype(np.float64)
+    ref = (O.rms_norm(xn, gv) if rms else O.layer_norm(xn, gv, 0.0)) + sv
+    got = od.float().cpu().numpy().astype(np.float64)
+    bound = 64 * 2.0 ** -23 * (np.abs(ref) + np.abs(gv)) + (2.0 ** -8 * np.abs(ref) if dtype else 0.0)
+    err = np.abs(got[:, :d] - ref)
+    assert np.all(err <= bound), float((err / bound).max())
+    assert np.all(got[:, d:] == 7.0)  # padding untouched
+
+
+def test_norm_rejects_bad_arguments(V):
+    x = torch.zeros((4, 64), dtype=torch.float32, device="cuda")
+    gn = torch.ones(64, dtype=torch.float32, device="cuda")
+    out = torch.zeros((4, 64), dtype=torch.float32, device="cuda")
+    for args in [dict(d=6, ldx=64, ldo=64), dict(d=64, ldx=60, ldo=64), dict(d=4096, ldx=4096, ldo=4096)]:
+        with pytest.raises(V.VlaError) as e:
+            V.vla_debug_norm(0, 4, args["d"], x, args["ldx"], None, 0, None, None, gn, 0, None, 1, out, args["ldo"])
+        assert e.value.code == -1
+    with pytest.raises(V.VlaError) as e:  # partials announced but not given
+        V.vla_debug_norm(0, 4, 64, x, 64, None, 2, None, None, gn, 0, None, 1, out, 64)
+    assert e.value.code == -1
+    with pytest.raises(V.VlaError) as e:  # x not 16-byte aligned
+        V.vla_debug_norm(0, 3, 60, x.view(-1)[1:].view(3, -1)[:, :60], 84, None, 0, None, None, gn, 0, None, 1, out,
+                         64)
+    assert e.value.code == -1
+
+
 def test_abi_errors_on_device(V):
     g = G()
     cfg = synth.micro()
