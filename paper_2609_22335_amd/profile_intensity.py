@@ -93,11 +93,18 @@ def rocprof(work: str, name: str, args, pmc=None, timeout=240) -> str:
     return d
 
 
-def measured_splits(path: str) -> dict:
+def measured_splits(path: str, preset: str = "") -> dict:
     """{VLM CUs: frames/s} of the CU-split schedules (cu_V_A) in a bench.py
-    detail file."""
+    detail file: those of the further workload named <preset>_R<R> when the
+    file holds one, else those of its main workload."""
     import json
-    modes = json.load(open(path))["modes"]
+    import re
+    d = json.load(open(path))
+    modes = d["modes"]
+    for name, w in (d.get("other_workloads") or {}).items():
+        if preset and re.fullmatch(re.escape(preset) + r"_R\d+", name):
+            modes = w["modes"]
+            break
     out = {}
     for name, r in modes.items():
         parts = name.split("_")
@@ -137,7 +144,7 @@ def profile(preset: str, out: str, work: str, collect: bool = True, fit: str = "
                              for p in ("alu", "fetch", "write"))
         desc += intensity.descriptors(large, alu, fetch, write, calib["FETCH_SIZE"], calib["WRITE_SIZE"], counts, phase,
                                       res)
-    cal = intensity.fit_calibration(desc, measured_splits(fit)) if fit else None
+    cal = intensity.fit_calibration(desc, measured_splits(fit, preset)) if fit else None
     plan = intensity.plan_cu_split(desc, cal=cal)
     meta = {"preset": preset, "calibration": cal, "peaks": {"mfma_bf16": intensity.PEAK_MFMA_BF16, "mfma_f32": intensity.PEAK_MFMA_F32,
                                         "valu_f32": intensity.PEAK_VALU_F32, "hbm": intensity.PEAK_HBM},
@@ -145,6 +152,22 @@ def profile(preset: str, out: str, work: str, collect: bool = True, fit: str = "
             "frames": [SMALL, LARGE], "cu_split_plan": plan}
     intensity.save(out, desc, meta)
     print(f"[intensity] {len(desc)} launch configurations -> {out}; planned CU split VLM/action "
+          f"{plan['vlm_cus']}/{plan['act_cus']}, predicted {1.0 / plan['per_frame_s']:.1f} frames/s", flush=True)
+
+
+def refit(preset: str, path: str, fit: str) -> None:
+    """Fit the planner's calibration of an existing descriptor file to the
+    measured CU splits of a bench.py detail file and store it, with the split
+    the calibrated planner then picks, in the file (CPU only)."""
+    import json
+    d = json.load(open(path))
+    desc, meta = d["descriptors"], d["meta"]
+    cal = intensity.fit_calibration(desc, measured_splits(fit, preset))
+    plan = intensity.plan_cu_split(desc, cal=cal)
+    meta["calibration"], meta["cu_split_plan"] = cal, plan
+    intensity.save(path, desc, meta)
+    print(f"[intensity] {path}: rho {cal['rho']:.2f}, kappa {cal['kappa']:.2f}, largest error "
+          f"{100 * cal['max_rel_err']:.1f}% over {len(cal['measured_fps'])} splits; planned CU split VLM/action "
           f"{plan['vlm_cus']}/{plan['act_cus']}, predicted {1.0 / plan['per_frame_s']:.1f} frames/s", flush=True)
 
 
@@ -157,9 +180,14 @@ def main() -> None:
     ap.add_argument("--frames", type=int, default=LARGE)
     ap.add_argument("--build-only", action="store_true", help="only build the file from the passes under --work")
     ap.add_argument("--fit", default="", help="bench.py detail file with cu_V_A schedules: fit the planner to them")
+    ap.add_argument("--fit-only", action="store_true", help="only fit the descriptor file --out to --fit (CPU)")
     a = ap.parse_args()
     if a.run:
         run_workload(a.run, a.preset, a.frames)
+    elif a.fit_only:
+        if not a.fit:
+            ap.error("--fit-only needs --fit")
+        refit(a.preset, a.out, a.fit)
     else:
         profile(a.preset, a.out, a.work, collect=not a.build_only, fit=a.fit)
 

@@ -158,3 +158,21 @@ def test_trace_stats_table_row(tmp_path):
     assert T.table_row([5000 / 2.0], 2.0)["lt5k_pct"] == 0.0
     with pytest.raises(ValueError):
         T.table_row([], 2.0)
+
+
+def test_measured_splits_of_the_main_and_further_workloads(tmp_path):
+    # the main workload's cu_V_A schedules, or those of the further workload
+    # named <preset>_R<R> (exactly: "pi0_R8_async" is not the pi0 workload)
+    import json
+    from paper_2609_22335_amd import profile_intensity as PI
+    det = {"modes": {"serial": {"frames_per_s": 1.0}, "cu_192_64": {"frames_per_s": 2.0},
+                     "cu_160_96": {"frames_per_s": 3.0}, "cu_160_96_lanes2": {"frames_per_s": 9.0}},
+           "other_workloads": {"pi0_R8_async": {"modes": {"cu_224_32": {"frames_per_s": 7.0}}},
+                               "pi0_3view_R32": {"modes": {"cu_224_32": {"frames_per_s": 4.0},
+                                                           "cu_192_64": {"frames_per_s": 5.0}}}}}
+    p = tmp_path / "detail.json"
+    p.write_text(json.dumps(det))
+    assert PI.measured_splits(str(p)) == {192: 2.0, 160: 3.0}
+    assert PI.measured_splits(str(p), "pi0") == {192: 2.0, 160: 3.0}
+    assert PI.measured_splits(str(p), "pi0_3view") == {224: 4.0, 192: 5.0}
+
