@@ -176,3 +176,26 @@ def test_measured_splits_of_the_main_and_further_workloads(tmp_path):
     assert PI.measured_splits(str(p), "pi0") == {192: 2.0, 160: 3.0}
     assert PI.measured_splits(str(p), "pi0_3view") == {224: 4.0, 192: 5.0}
 
+
+def test_refit_stores_the_calibration_and_plan(tmp_path):
+    # splits generated by the model itself (rho 0.5, kappa 0.4) are fitted
+    # back and stored in the descriptor file with the split the calibrated
+    # planner picks, as the bench's cu_auto schedule reads them
+    import json
+    from paper_2609_22335_amd import profile_intensity as PI
+    desc = [_d("vlm", 512, 100.0, mem=0.3), _d("action", 64, 60.0, lpf=3.0, mem=0.6),
+            _d("action", 25, 20.0, lpf=2.0, mem=0.05)]
+    cal = {"rho": 0.5, "kappa": 0.4}
+    fps = {v: 1.0 / I.predict_split(desc, v, cal=cal)["per_frame_s"] for v in (224, 192, 160)}
+    path = tmp_path / "intensity.json"
+    I.save(str(path), desc, {"preset": "x"})
+    det = tmp_path / "detail.json"
+    det.write_text(json.dumps({"modes": {}, "other_workloads": {
+        "x_R32": {"modes": {f"cu_{v}_{256 - v}": {"frames_per_s": f} for v, f in fps.items()}}}}))
+    PI.refit("x", str(path), str(det))
+    got = I.load_calibration(str(path))
+    assert got["rho"] == pytest.approx(0.5) and got["kappa"] == pytest.approx(0.4)
+    meta = json.load(open(path))["meta"]
+    assert meta["preset"] == "x"
+    assert meta["cu_split_plan"]["vlm_cus"] == I.plan_cu_split(desc, cal=cal)["vlm_cus"]
+
